@@ -1,0 +1,280 @@
+"""CPU oracle of the RGCN block (forward, backward, integer plan) -- TEST INFRASTRUCTURE.
+
+Only the tests, ``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may
+import this package.  It shares no code with the HIP library: the arithmetic lives in
+``rgcn_oracle.c`` (plain loops, IEEE double), and this wrapper only marshals numpy
+arrays into it.  Block objects are duck-typed: anything with ``n_src``, ``n_dst`` and
+``rels`` (each with ``src_type``, ``dst_type``, ``indptr``, ``indices``) is accepted.
+
+Which passage each function follows is stated in ``rgcn_oracle.c``.  The degree-sorted
+schedules are the library's documented ordering rule (a stable counting sort of
+segments by a degree key), restated here from that rule.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "rgcn_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+# Degree keys of the schedules: key = SCHED_BUCKETS - 1 - min(deg, SCHED_BUCKETS - 1), so a
+# stable ascending sort lists the heaviest segments first.
+SCHED_BUCKETS = 64
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with the host C compiler (plain IEEE double, no fast-math)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        subprocess.run(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fno-fast-math",
+                        "-ffp-contract=off", _SRC, "-o", tmp], check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+class _Rel(ctypes.Structure):
+    _fields_ = [("src_type", ctypes.c_int32), ("dst_type", ctypes.c_int32),
+                ("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p)]
+
+
+class _Block(ctypes.Structure):
+    _fields_ = [("num_types", ctypes.c_int32), ("num_rels", ctypes.c_int32),
+                ("n_src", ctypes.c_void_p), ("n_dst", ctypes.c_void_p),
+                ("rels", ctypes.POINTER(_Rel))]
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=False)
+        lib = ctypes.CDLL(_LIB_PATH)
+        vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        lib.orc_check_block.argtypes = [vp]
+        lib.orc_check_block.restype = ctypes.c_int
+        lib.orc_degrees.argtypes = [vp, i64, vp]
+        lib.orc_mean_aggregate.argtypes = [vp, vp, i64, vp, i64, vp]
+        lib.orc_block_forward.argtypes = [vp, i64, i64, vp, vp, vp, vp, ctypes.c_int, vp]
+        lib.orc_block_forward.restype = ctypes.c_int
+        lib.orc_block_backward.argtypes = [vp, i64, i64, vp, vp, vp, vp, ctypes.c_int,
+                                           vp, vp, vp, vp]
+        lib.orc_block_backward.restype = ctypes.c_int
+        lib.orc_scatter_add.argtypes = [i64, i64, vp, vp, vp]
+        lib.orc_csc.argtypes = [i64, i64, vp, vp, vp, vp, vp]
+        lib.orc_csc.restype = ctypes.c_int
+        lib.orc_stable_bucket_order.argtypes = [i64, vp, i32, vp]
+        lib.orc_stable_bucket_order.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: Optional[np.ndarray]) -> Optional[int]:
+    return None if a is None else a.ctypes.data
+
+
+class _Marshal:
+    """Holds the ctypes mirror of a block (and keeps its arrays alive)."""
+
+    def __init__(self, block):
+        self.keep = []
+        T = len(block.n_src)
+        self.n_src = np.asarray(block.n_src, dtype=np.int64)
+        self.n_dst = np.asarray(block.n_dst, dtype=np.int64)
+        rels = (_Rel * max(len(block.rels), 1))()
+        for r, rel in enumerate(block.rels):
+            ip = np.ascontiguousarray(rel.indptr, dtype=np.int32)
+            ix = np.ascontiguousarray(rel.indices, dtype=np.int32)
+            if ix.size == 0:
+                ix = np.zeros(1, dtype=np.int32)
+            self.keep += [ip, ix]
+            rels[r] = _Rel(rel.src_type, rel.dst_type, ip.ctypes.data, ix.ctypes.data)
+        self.rels = rels
+        self.c = _Block(T, len(block.rels), self.n_src.ctypes.data, self.n_dst.ctypes.data,
+                        ctypes.cast(rels, ctypes.POINTER(_Rel)))
+
+    def ptrs(self, arrays: Sequence[Optional[np.ndarray]]):
+        arr = (ctypes.c_void_p * max(len(arrays), 1))()
+        for i, a in enumerate(arrays):
+            if a is not None:
+                a = np.ascontiguousarray(a, dtype=np.float64)
+                self.keep.append(a)
+                arr[i] = a.ctypes.data
+        self.keep.append(arr)
+        return ctypes.cast(arr, ctypes.c_void_p)
+
+    def out_ptrs(self, arrays: Sequence[Optional[np.ndarray]]):
+        arr = (ctypes.c_void_p * max(len(arrays), 1))()
+        for i, a in enumerate(arrays):
+            if a is not None:
+                assert a.dtype == np.float64 and a.flags.c_contiguous
+                arr[i] = a.ctypes.data
+        self.keep.append(arr)
+        return ctypes.cast(arr, ctypes.c_void_p)
+
+
+def check_block(block) -> bool:
+    m = _Marshal(block)
+    return _load().orc_check_block(ctypes.byref(m.c)) == 0
+
+
+def degrees(indptr: np.ndarray) -> np.ndarray:
+    ip = np.ascontiguousarray(indptr, dtype=np.int32)
+    n = ip.shape[0] - 1
+    out = np.zeros(max(n, 1), dtype=np.int32)
+    _load().orc_degrees(ip.ctypes.data, n, out.ctypes.data)
+    return out[:n]
+
+
+def mean_aggregate(indptr, indices, h_src: np.ndarray) -> np.ndarray:
+    ip = np.ascontiguousarray(indptr, dtype=np.int32)
+    ix = np.ascontiguousarray(indices, dtype=np.int32)
+    if ix.size == 0:
+        ix = np.zeros(1, dtype=np.int32)
+    h = np.ascontiguousarray(h_src, dtype=np.float64)
+    n = ip.shape[0] - 1
+    d = h.shape[1]
+    out = np.zeros((n, d), dtype=np.float64)
+    _load().orc_mean_aggregate(ip.ctypes.data, ix.ctypes.data, n, _ptr(h) or 0, d,
+                               out.ctypes.data)
+    return out
+
+
+def block_forward(block, h_src: Sequence[Optional[np.ndarray]], w_rel, w_self, bias=None,
+                  relu: bool = False) -> List[Optional[np.ndarray]]:
+    """Y_t for every type with n_dst[t] > 0 (None otherwise), in float64."""
+    m = _Marshal(block)
+    T = len(block.n_src)
+    d_in = int(np.asarray(w_rel[0] if len(w_rel) else w_self[0]).shape[0])
+    d_out = int(np.asarray(w_rel[0] if len(w_rel) else w_self[0]).shape[1])
+    ys = [np.zeros((block.n_dst[t], d_out), dtype=np.float64) if block.n_dst[t] > 0 else None
+          for t in range(T)]
+    bias = bias if bias is not None else [None] * T
+    rc = _load().orc_block_forward(ctypes.byref(m.c), d_in, d_out, m.ptrs(h_src),
+                                   m.ptrs(w_rel), m.ptrs(w_self),
+                                   m.ptrs(bias) if any(b is not None for b in bias) else None,
+                                   int(relu), m.out_ptrs(ys))
+    if rc != 0:
+        raise ValueError("oracle: invalid block")
+    return ys
+
+
+def block_backward(block, h_src, w_rel, w_self, dy, input_relu: bool = False,
+                   want_dh: Optional[Sequence[bool]] = None, want_dw: bool = True):
+    """Gradients of one block in float64: dict with dw_rel, dw_self, dbias, dh_src."""
+    m = _Marshal(block)
+    T, R = len(block.n_src), len(block.rels)
+    d_in = int(np.asarray(w_self[0]).shape[0])
+    d_out = int(np.asarray(w_self[0]).shape[1])
+    want_dh = [True] * T if want_dh is None else list(want_dh)
+    dw_rel = [np.zeros((d_in, d_out)) for _ in range(R)] if want_dw else []
+    dw_self = [np.zeros((d_in, d_out)) for _ in range(T)] if want_dw else []
+    dbias = [np.zeros(d_out) for _ in range(T)] if want_dw else []
+    dh = [np.zeros((block.n_src[t], d_in)) if want_dh[t] else None for t in range(T)]
+    rc = _load().orc_block_backward(
+        ctypes.byref(m.c), d_in, d_out, m.ptrs(h_src), m.ptrs(w_rel), m.ptrs(w_self),
+        m.ptrs(dy), int(input_relu),
+        m.out_ptrs(dw_rel) if want_dw else None, m.out_ptrs(dw_self) if want_dw else None,
+        m.out_ptrs(dbias) if want_dw else None, m.out_ptrs(dh))
+    if rc != 0:
+        raise ValueError("oracle: invalid block")
+    return {"dw_rel": dw_rel, "dw_self": dw_self, "dbias": dbias, "dh_src": dh}
+
+
+def scatter_add(ids: np.ndarray, dh: np.ndarray, demb: np.ndarray) -> None:
+    """demb[ids[j]] += dh[j] in ascending j (in place; demb float64, C-contiguous)."""
+    ids = np.ascontiguousarray(ids, dtype=np.int64)
+    dh = np.ascontiguousarray(dh, dtype=np.float64)
+    assert demb.dtype == np.float64 and demb.flags.c_contiguous
+    if ids.size == 0:
+        return
+    if ids.min() < 0 or ids.max() >= demb.shape[0]:
+        raise IndexError("oracle: scatter id out of range")
+    _load().orc_scatter_add(ids.shape[0], dh.shape[1], ids.ctypes.data, dh.ctypes.data,
+                            demb.ctypes.data)
+
+
+def csc(n_src: int, indptr, indices):
+    """(csc_indptr [n_src+1], csc_dst [nnz], csc_eid [nnz]) as int32."""
+    ip = np.ascontiguousarray(indptr, dtype=np.int32)
+    ix = np.ascontiguousarray(indices, dtype=np.int32)
+    nnz = int(ip[-1])
+    ix1 = ix if ix.size else np.zeros(1, dtype=np.int32)
+    cip = np.zeros(n_src + 1, dtype=np.int32)
+    cd = np.zeros(max(nnz, 1), dtype=np.int32)
+    ce = np.zeros(max(nnz, 1), dtype=np.int32)
+    rc = _load().orc_csc(n_src, ip.shape[0] - 1, ip.ctypes.data, ix1.ctypes.data,
+                         cip.ctypes.data, cd.ctypes.data, ce.ctypes.data)
+    if rc != 0:
+        raise MemoryError
+    return cip, cd[:nnz], ce[:nnz]
+
+
+def stable_bucket_order(key: np.ndarray, nbuckets: int) -> np.ndarray:
+    k = np.ascontiguousarray(key, dtype=np.int32)
+    n = k.shape[0]
+    out = np.zeros(max(n, 1), dtype=np.int32)
+    k1 = k if n else np.zeros(1, dtype=np.int32)
+    if _load().orc_stable_bucket_order(n, k1.ctypes.data, nbuckets, out.ctypes.data) != 0:
+        raise ValueError("oracle: bucket key out of range")
+    return out[:n]
+
+
+def degree_key(deg: np.ndarray) -> np.ndarray:
+    """Schedule key of a segment of degree deg: heaviest first, degrees >= 63 share key 0."""
+    return (SCHED_BUCKETS - 1 - np.minimum(deg.astype(np.int64), SCHED_BUCKETS - 1)).astype(
+        np.int32)
+
+
+def forward_segments(block):
+    """Forward segments of a block in enumeration order.
+
+    Slots are listed destination type by destination type (ascending); each type with
+    n_dst[t] > 0 contributes its self-loop slot first (degree 1), then one slot per relation
+    into t in ascending relation order.  A segment is (slot, destination row); segment ids
+    run slot by slot, rows ascending.  Returns (slot_type, slot_rel (-1 for self),
+    slot_base, degrees) where degrees is the per-segment degree array.
+    """
+    slot_type, slot_rel, slot_base, degs = [], [], [], []
+    base = 0
+    for t in range(len(block.n_src)):
+        nd = int(block.n_dst[t])
+        if nd == 0:
+            continue
+        slot_type.append(t); slot_rel.append(-1); slot_base.append(base)
+        degs.append(np.ones(nd, dtype=np.int32)); base += nd
+        for r, rel in enumerate(block.rels):
+            if rel.dst_type != t:
+                continue
+            slot_type.append(t); slot_rel.append(r); slot_base.append(base)
+            degs.append(degrees(rel.indptr)); base += nd
+    deg = np.concatenate(degs) if degs else np.zeros(0, dtype=np.int32)
+    return slot_type, slot_rel, slot_base, deg
+
+
+def forward_schedule(block) -> np.ndarray:
+    """Segment ids in the library's forward processing order (heaviest degree first)."""
+    _, _, _, deg = forward_segments(block)
+    return stable_bucket_order(degree_key(deg), SCHED_BUCKETS)
+
+
+def backward_schedule(block, grad_types: Sequence[int]) -> np.ndarray:
+    """Source rows (as ids over the requested types, type-major, rows ascending) in the
+    library's backward processing order: key from the row's total in-degree in the
+    transpose, summed over the relations leaving its type, heaviest first."""
+    parts = []
+    for s in sorted(grad_types):
+        cnt = np.zeros(int(block.n_src[s]), dtype=np.int64)
+        for rel in block.rels:
+            if rel.src_type == s:
+                cnt += np.bincount(np.asarray(rel.indices, dtype=np.int64),
+                                   minlength=int(block.n_src[s]))[: int(block.n_src[s])]
+        parts.append(cnt)
+    deg = np.concatenate(parts) if parts else np.zeros(0, dtype=np.int64)
+    return stable_bucket_order(degree_key(deg), SCHED_BUCKETS)
