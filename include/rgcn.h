@@ -1,0 +1,211 @@
+/*
+ * rgcn.h -- C ABI of the MI355X (gfx950) relational graph-convolution block library.
+ *
+ * One call computes one GNN layer on one sampled mini-batch block, the unit the paper's
+ * models iterate over (programming-interface appendix, customised-model figure: one
+ * layer applied per block, node representations kept per node type).  The layer is the
+ * relational GCN the paper lists for heterogeneous graphs (Sec. 3.1.4, model zoo):
+ *
+ *   M_r[i]  = mean of H_{src(r)}[indices_r[k]] over the sampled in-edges k of row i
+ *             (0 when row i has no in-edge in relation r; repeated edges count)
+ *   Y_t[i]  = H_t[i] W_self_t + sum_{r : dst(r) = t} M_r[i] W_r (+ b_t)
+ *
+ * where the destination rows of type t are the first n_dst[t] source rows of type t.
+ * At the first layer H_t[j] is row row_ids_t[j] of a feature table or of a learnable
+ * embedding table (featureless node types, Sec. 3.3.2); backward then scatter-adds the
+ * input gradient into a table-shaped gradient buffer.
+ *
+ * Conventions (all entry points):
+ *  - Pointers marked [host] are host memory; every other pointer is device memory.
+ *  - The library allocates no device memory.  The caller owns every buffer, including
+ *    the workspace, whose size comes from rgcn_block_workspace_size().  Forward leaves
+ *    the per-relation aggregates there for backward, so plan, forward and backward of a
+ *    block use the same workspace, in that order, on the same stream.
+ *  - Calls enqueue work on `stream` and return without synchronising, except with
+ *    RGCN_VALIDATE_DEVICE, which synchronises to report index/CSR errors.
+ *  - Device arrays must be 16-byte aligned; d_in and d_out must be multiples of 8
+ *    (bf16) or 4 (fp32); ld a multiple of the same; row counts and nnz below 2^31.
+ *  - Functions are stateless and thread-safe.  On any non-OK status nothing has been
+ *    enqueued (host-detected errors) or the stream has been synchronised (device
+ *    validation); rgcn_last_error() returns a message for the calling thread.
+ */
+#ifndef RGCN_H
+#define RGCN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    RGCN_OK = 0,
+    RGCN_ERR_INVALID_ARG = 1,          /* NULL required pointer, bad count, misalignment */
+    RGCN_ERR_SHAPE = 2,                /* inconsistent sizes (n_dst > n_src, ld < d_in, ...) */
+    RGCN_ERR_DTYPE = 3,                /* unknown dtype */
+    RGCN_ERR_INDEX_OOB = 4,            /* device validation: index or row id out of range */
+    RGCN_ERR_BAD_CSR = 5,              /* device validation: indptr not a valid CSR offset array */
+    RGCN_ERR_WORKSPACE_TOO_SMALL = 6,
+    RGCN_ERR_UNSUPPORTED = 7,          /* valid request outside the implemented limits */
+    RGCN_ERR_HIP = 8                   /* a HIP runtime call failed */
+} rgcn_status;
+
+typedef enum { RGCN_F32 = 0, RGCN_BF16 = 1 } rgcn_dtype;
+
+#define RGCN_MAX_TYPES 16
+#define RGCN_MAX_RELS 64
+
+/* flags */
+#define RGCN_VALIDATE_DEVICE 0x1u /* check CSR and indices on the device first (synchronises) */
+#define RGCN_FUSE_RELU       0x2u /* forward: y = max(0, .) (block followed by ReLU) */
+#define RGCN_INPUT_RELU      0x4u /* backward: the input H is a ReLU output, so the input
+                                     gradient is multiplied elementwise by [H > 0] */
+#define RGCN_IDS_UNIQUE      0x8u /* backward: the caller asserts row_ids are distinct per
+                                     type, so demb rows are updated without atomics */
+
+/* One relation (canonical edge type src_type -> dst_type) of a block, as a CSR over the
+ * destination rows.  indptr[0] = 0, non-decreasing, indptr[n_dst] = nnz; indices are
+ * block-local source rows in [0, n_src[src_type]); repeats allowed. */
+typedef struct {
+    int32_t src_type;
+    int32_t dst_type;
+    int64_t nnz;
+    const int32_t *indptr;    /* [n_dst[dst_type] + 1] */
+    const int32_t *indices;   /* [nnz] */
+} rgcn_relation;
+
+/* A block: node-type counts and relations.  grad_src_types has bit t set when backward
+ * may be asked for dh_src[t] or demb[t]; plan builds the transpose only for those. */
+typedef struct {
+    int32_t num_types;
+    int32_t num_rels;
+    const int64_t *n_src;           /* [host][num_types] */
+    const int64_t *n_dst;           /* [host][num_types], n_dst[t] <= n_src[t] */
+    const rgcn_relation *rels;      /* [host][num_rels] */
+    uint32_t grad_src_types;
+} rgcn_block;
+
+/* Input rows of one node type: H[j] = base[row_ids[j] * ld + 0 .. d_in) (row_ids NULL:
+ * H[j] = base[j * ld ...]).  base has num_rows rows of the block's dtype. */
+typedef struct {
+    const void *base;
+    const int64_t *row_ids;   /* [n_src[t]] or NULL */
+    int64_t num_rows;
+    int64_t ld;
+} rgcn_input;
+
+/* Weights of one block in the block's dtype, row-major [d_in x d_out]. */
+typedef struct {
+    rgcn_dtype dtype;
+    int32_t d_in;
+    int32_t d_out;
+    const void *const *w_rel;     /* [host][num_rels] */
+    const void *const *w_self;    /* [host][num_types]; needed for types with n_dst > 0 */
+    const void *const *bias;      /* [host][num_types] entries may be NULL; or NULL = none */
+} rgcn_params;
+
+/* Byte offsets inside the workspace of the integer plan (for inspection and tests).
+ * An offset of SIZE_MAX means "not built". */
+typedef struct {
+    int64_t n_fwd_segments;                 /* forward segments (self-loop + relation rows) */
+    size_t fwd_order;                       /* int32 [n_fwd_segments]: segment ids, heaviest first */
+    int64_t n_bwd_rows;                     /* source rows of the types in grad_src_types */
+    size_t bwd_order;                       /* int32 [n_bwd_rows] */
+    size_t csc_indptr[RGCN_MAX_RELS];       /* int32 [n_src[src_type] + 1] */
+    size_t csc_dst[RGCN_MAX_RELS];          /* int32 [nnz]: destination row of each edge */
+    size_t total_bytes;                     /* = rgcn_block_workspace_size */
+} rgcn_plan_layout;
+
+/* Workspace bytes needed by plan/forward/backward of this block and parameter shape.
+ * Host only; enqueues nothing. */
+rgcn_status rgcn_block_workspace_size(const rgcn_block *block, const rgcn_params *params,
+                                      size_t *bytes /* [host] */);
+
+/* Where the plan arrays sit inside the workspace.  Host only. */
+rgcn_status rgcn_block_plan_layout(const rgcn_block *block, const rgcn_params *params,
+                                   rgcn_plan_layout *layout /* [host] */);
+
+/* Integer plan of a block (exact, deterministic):
+ *  - the forward schedule: segments (self-loop rows, then each relation's rows, type by
+ *    type) as a stable counting sort by degree key 63 - min(deg, 63), heaviest first;
+ *  - for every relation whose source type is in grad_src_types, the CSC transpose:
+ *    csc_indptr and csc_dst, a stable sort of edges by source row (ascending edge
+ *    position inside a source row);
+ *  - the backward schedule: for each type in grad_src_types (ascending), a section
+ *    holding that type's rows (local ids) stably sorted by 63 - min(d, 63), d the row's
+ *    in-degree in the transpose summed over the relations leaving the type.
+ * Only structural arrays are read.  flags: RGCN_VALIDATE_DEVICE. */
+rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
+                            void *workspace, size_t workspace_bytes, unsigned flags,
+                            hipStream_t stream);
+
+/* Forward: y[t] (device [n_dst[t] x d_out], block dtype, row-major) for every type with
+ * n_dst[t] > 0; entries for other types are ignored.  in: [host][num_types].
+ * flags: RGCN_VALIDATE_DEVICE, RGCN_FUSE_RELU.  Requires rgcn_block_plan first. */
+rgcn_status rgcn_block_forward(const rgcn_block *block, const rgcn_input *in,
+                               const rgcn_params *params, void *const *y /* [host] */,
+                               void *workspace, size_t workspace_bytes, unsigned flags,
+                               hipStream_t stream);
+
+/* Backward, after forward on the same workspace.  dy[t]: fp32 [n_dst[t] x d_out].
+ * Outputs are fp32 and overwritten unless stated; any array argument may be NULL and any
+ * entry NULL to skip that output:
+ *   dw_rel[r], dw_self[t]: [d_in x d_out];  dbias[t]: [d_out];
+ *   dh_src[t]: [n_src[t] x d_in] gradient w.r.t. the block input H_t;
+ *   demb[t]:   [num_rows x d_in] table-shaped; row row_ids[j] += dH_t[j] (scatter-ADD into
+ *              caller-initialised memory; rows never named are untouched).
+ * dh_src[t] / demb[t] require bit t of grad_src_types.  dw_self entries must not alias.
+ * flags: RGCN_VALIDATE_DEVICE, RGCN_INPUT_RELU, RGCN_IDS_UNIQUE. */
+rgcn_status rgcn_block_backward(const rgcn_block *block, const rgcn_input *in,
+                                const rgcn_params *params, const float *const *dy,
+                                float *const *dw_rel, float *const *dw_self,
+                                float *const *dbias, float *const *dh_src,
+                                float *const *demb, void *workspace, size_t workspace_bytes,
+                                unsigned flags, hipStream_t stream);
+
+/* The two stages of rgcn_block_forward, for callers that schedule or time them apart.
+ * rgcn_block_aggregate: the input gather and per-relation segmented means (self-loop
+ *   rows copied, relation rows averaged over their sampled in-edges) into the workspace.
+ *   flags: RGCN_VALIDATE_DEVICE.  Requires rgcn_block_plan first.
+ * rgcn_block_transform: the per-destination-type transform
+ *   Y_t = [H_t | M_r ...] [W_self_t; W_r ...] (+ b_t) on the matrix cores, reading the
+ *   aggregates left by rgcn_block_aggregate.  flags: RGCN_FUSE_RELU. */
+rgcn_status rgcn_block_aggregate(const rgcn_block *block, const rgcn_input *in,
+                                 const rgcn_params *params, void *workspace,
+                                 size_t workspace_bytes, unsigned flags, hipStream_t stream);
+rgcn_status rgcn_block_transform(const rgcn_block *block, const rgcn_params *params,
+                                 void *const *y /* [host] */, void *workspace,
+                                 size_t workspace_bytes, unsigned flags, hipStream_t stream);
+
+/* The two stages of rgcn_block_backward.
+ * rgcn_block_backward_dense: weight and bias gradients (dw_rel, dw_self, dbias as in
+ *   rgcn_block_backward) and, for the types in grad_src_types, the per-edge input-side
+ *   products dY_t W^T / deg kept in the workspace.
+ * rgcn_block_backward_sparse: the transposed sums over the CSC transpose that turn those
+ *   products into dh_src[t] and the scatter-add into demb[t] (as in rgcn_block_backward);
+ *   must follow rgcn_block_backward_dense on the same workspace.
+ *   flags: RGCN_VALIDATE_DEVICE, RGCN_INPUT_RELU, RGCN_IDS_UNIQUE. */
+rgcn_status rgcn_block_backward_dense(const rgcn_block *block, const rgcn_params *params,
+                                      const float *const *dy, float *const *dw_rel,
+                                      float *const *dw_self, float *const *dbias,
+                                      void *workspace, size_t workspace_bytes, unsigned flags,
+                                      hipStream_t stream);
+rgcn_status rgcn_block_backward_sparse(const rgcn_block *block, const rgcn_input *in,
+                                       const rgcn_params *params, float *const *dh_src,
+                                       float *const *demb, void *workspace,
+                                       size_t workspace_bytes, unsigned flags,
+                                       hipStream_t stream);
+
+/* Message for the last non-OK status returned on the calling thread ("" if none). */
+const char *rgcn_last_error(void);
+
+/* Library version string. */
+const char *rgcn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RGCN_H */

@@ -265,16 +265,65 @@ def forward_schedule(block) -> np.ndarray:
 
 
 def backward_schedule(block, grad_types: Sequence[int]) -> np.ndarray:
-    """Source rows (as ids over the requested types, type-major, rows ascending) in the
-    library's backward processing order: key from the row's total in-degree in the
-    transpose, summed over the relations leaving its type, heaviest first."""
+    """Backward processing order: for each requested source type (ascending), that type's
+    rows (local ids) stably sorted by the degree key of the row's in-degree in the
+    transpose, summed over the relations leaving the type; sections concatenated."""
     parts = []
-    for s in sorted(grad_types):
-        cnt = np.zeros(int(block.n_src[s]), dtype=np.int64)
+    for s in sorted(set(grad_types)):
+        ns = int(block.n_src[s])
+        cnt = np.zeros(ns, dtype=np.int64)
         for rel in block.rels:
-            if rel.src_type == s:
-                cnt += np.bincount(np.asarray(rel.indices, dtype=np.int64),
-                                   minlength=int(block.n_src[s]))[: int(block.n_src[s])]
-        parts.append(cnt)
-    deg = np.concatenate(parts) if parts else np.zeros(0, dtype=np.int64)
-    return stable_bucket_order(degree_key(deg), SCHED_BUCKETS)
+            if rel.src_type == s and len(rel.indices):
+                cnt += np.bincount(np.asarray(rel.indices, dtype=np.int64), minlength=ns)[:ns]
+        parts.append(stable_bucket_order(degree_key(cnt), SCHED_BUCKETS))
+    return np.concatenate(parts) if parts else np.zeros(0, dtype=np.int32)
+
+
+class _SubRel:
+    def __init__(self, s, t, indptr, indices):
+        self.src_type, self.dst_type, self.indptr, self.indices = s, t, indptr, indices
+
+
+class _SubBlock:
+    def __init__(self, n_src, n_dst, rels):
+        self.n_src, self.n_dst, self.rels = n_src, n_dst, rels
+
+
+def sub_block(block, dst_rows):
+    """The part of ``block`` that determines the outputs of the listed destination rows.
+
+    dst_rows[t]: sorted int array of destination rows of type t to keep.  Each kept row
+    keeps its whole segment in every relation, so its aggregates and outputs, and the
+    input gradient of every source row that only kept rows reference, are unchanged.
+    Returns (sub, src_map): sub is a block whose destination rows of type t are the kept
+    rows in the given order (the prefix of the type's sources), and src_map[t] lists, for
+    each source row of the sub-block, its row in ``block``."""
+    T = len(block.n_src)
+    keep = [np.asarray(dst_rows[t], dtype=np.int64) for t in range(T)]
+    used = [[keep[t]] for t in range(T)]
+    segs = []
+    for rel in block.rels:
+        rows = keep[rel.dst_type]
+        ip = np.asarray(rel.indptr, dtype=np.int64)
+        lo, hi = ip[rows], ip[rows + 1]
+        deg = hi - lo
+        idx = np.concatenate([np.arange(a, b) for a, b in zip(lo, hi)]) if rows.size else np.zeros(0, np.int64)
+        src = np.asarray(rel.indices, dtype=np.int64)[idx] if idx.size else np.zeros(0, np.int64)
+        segs.append((deg, src))
+        used[rel.src_type].append(src)
+    src_map = []
+    for t in range(T):
+        others = np.unique(np.concatenate(used[t][1:])) if len(used[t]) > 1 else np.zeros(0, np.int64)
+        others = others[~np.isin(others, keep[t])]
+        src_map.append(np.concatenate([keep[t], others]))
+    rels = []
+    for rel, (deg, src) in zip(block.rels, segs):
+        m = src_map[rel.src_type]
+        order = np.argsort(m, kind="stable")
+        local = order[np.searchsorted(m[order], src)] if src.size else np.zeros(0, np.int64)
+        indptr = np.zeros(deg.size + 1, dtype=np.int64)
+        np.cumsum(deg, out=indptr[1:])
+        rels.append(_SubRel(rel.src_type, rel.dst_type, indptr.astype(np.int32),
+                            local.astype(np.int32)))
+    sub = _SubBlock([int(m.size) for m in src_map], [int(k.size) for k in keep], rels)
+    return sub, src_map

@@ -1,0 +1,135 @@
+"""Multi-block mini-batch driver: one RGCN layer per sampled block, input side first.
+
+Follows the model loop of the paper's programming interface (customised-model figure in
+the appendix): representations are kept per node type and layer i is applied to
+blocks[i].  Between layers the output goes through a ReLU (fused into the producing
+transform); the last layer has no activation.  Backward runs from the last block to the
+first: block l+1's input gradient is block l's output gradient, masked by the ReLU.  At
+the first block the featureless node types read learnable embedding tables (Sec. 3.3.2)
+and their gradient is scatter-added into table-shaped buffers.
+
+This module only allocates buffers and sequences calls of the C ABI.
+"""
+from __future__ import annotations
+
+from typing import List, Optional, Sequence
+
+import torch
+
+from . import rgcn
+
+
+class MiniBatchStack:
+    def __init__(self, blocks, input_tables: Sequence[Optional[torch.Tensor]],
+                 input_ids: Sequence[Optional[torch.Tensor]], weights, dtype: str,
+                 dims: Sequence[int], emb_types: Sequence[int] = (), device="cuda",
+                 want_weight_grads: bool = True, ids_unique: bool = True):
+        """blocks: host blocks (blocks[0] nearest the input); input_tables[t] / input_ids[t]:
+        layer-0 table and int64 global row ids of each type; weights[l] = (w_rel, w_self,
+        bias) device tensors of layer l; emb_types: types whose table is learnable."""
+        self.L = len(blocks)
+        self.dtype = dtype
+        self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
+        self.dims = list(dims)
+        self.device = device
+        self.emb_types = list(emb_types)
+        self.ids_unique = ids_unique
+        self.blocks: List[rgcn.DeviceBlock] = []
+        for l, blk in enumerate(blocks):
+            if l == 0:
+                mask = 0
+                for t in self.emb_types:
+                    mask |= 1 << t
+            else:
+                mask = 0
+                for t in range(len(blk.n_src)):
+                    if blk.n_src[t] > 0:
+                        mask |= 1 << t
+            self.blocks.append(rgcn.DeviceBlock(blk, mask, device))
+        self.params = [rgcn.Params(dtype, dims[l], dims[l + 1], *weights[l]) for l in range(self.L)]
+        self.workspaces = [rgcn.new_workspace(b, p, device) for b, p in zip(self.blocks, self.params)]
+        # activations: y[l][t] = output of block l, [n_dst x d_{l+1}]
+        self.y = [[torch.empty((n, dims[l + 1]), dtype=self.tdtype, device=device) if n > 0 else None
+                   for n in b.n_dst] for l, b in enumerate(self.blocks)]
+        self.inputs = [rgcn.Inputs(list(input_tables), list(input_ids))]
+        for l in range(1, self.L):
+            self.inputs.append(rgcn.Inputs(self.y[l - 1], None))
+        # gradients
+        f32 = torch.float32
+        self.want_weight_grads = want_weight_grads
+        self.dw_rel = [[torch.empty((dims[l], dims[l + 1]), dtype=f32, device=device)
+                        for _ in b.types] if want_weight_grads else None
+                       for l, b in enumerate(self.blocks)]
+        self.dw_self = [[torch.empty((dims[l], dims[l + 1]), dtype=f32, device=device)
+                         for _ in range(b.num_types)] if want_weight_grads else None
+                        for l, b in enumerate(self.blocks)]
+        self.dbias = [[torch.empty((dims[l + 1],), dtype=f32, device=device)
+                       if weights[l][2] is not None and weights[l][2][t] is not None else None
+                       for t in range(b.num_types)] if want_weight_grads else None
+                      for l, b in enumerate(self.blocks)]
+        # dh[l][t]: gradient w.r.t. block l's input (l >= 1) = output gradient of block l-1
+        self.dh = [None] + [[torch.empty((n, dims[l]), dtype=f32, device=device) if n > 0 else None
+                             for n in b.n_src] for l, b in enumerate(self.blocks) if l >= 1]
+        self.demb = [None] * len(self.blocks[0].n_src)
+        for t in self.emb_types:
+            tab = input_tables[t]
+            self.demb[t] = torch.zeros((tab.shape[0], dims[0]), dtype=f32, device=device)
+
+    @property
+    def nnz(self) -> int:
+        return sum(b.nnz for b in self.blocks)
+
+    def plan(self, flags: int = 0, timer=None) -> None:
+        for l, (b, p, ws) in enumerate(zip(self.blocks, self.params, self.workspaces)):
+            _mark(timer, ("plan", l), 0)
+            rgcn.rgcn_block_plan(b, p, ws, flags)
+            _mark(timer, ("plan", l), 1)
+
+    def forward(self, flags: int = 0, timer=None) -> List[Optional[torch.Tensor]]:
+        """Forward through all blocks (each as its aggregate and transform stages)."""
+        for l in range(self.L):
+            f = flags | (rgcn.RGCN_FUSE_RELU if l < self.L - 1 else 0)
+            _mark(timer, ("aggregate", l), 0)
+            rgcn.rgcn_block_aggregate(self.blocks[l], self.inputs[l], self.params[l],
+                                      self.workspaces[l], f)
+            _mark(timer, ("aggregate", l), 1)
+            _mark(timer, ("transform", l), 0)
+            rgcn.rgcn_block_transform(self.blocks[l], self.params[l], self.y[l],
+                                      self.workspaces[l], f & ~rgcn.RGCN_VALIDATE_DEVICE)
+            _mark(timer, ("transform", l), 1)
+        return self.y[-1]
+
+    def backward(self, dy_top: Sequence[Optional[torch.Tensor]], flags: int = 0,
+                 timer=None) -> None:
+        """Backward from the last block to the first (dense then sparse stage per block)."""
+        for l in reversed(range(self.L)):
+            dy = dy_top if l == self.L - 1 else self.dh[l + 1]
+            f = flags
+            if l > 0:
+                f |= rgcn.RGCN_INPUT_RELU
+                dh, demb = self.dh[l], None
+            else:
+                dh = None
+                demb = self.demb if any(x is not None for x in self.demb) else None
+                if self.ids_unique:
+                    f |= rgcn.RGCN_IDS_UNIQUE
+            _mark(timer, ("dense", l), 0)
+            rgcn.rgcn_block_backward_dense(self.blocks[l], self.params[l], dy, self.dw_rel[l],
+                                           self.dw_self[l], self.dbias[l],
+                                           self.workspaces[l], f)
+            _mark(timer, ("dense", l), 1)
+            _mark(timer, ("sparse", l), 0)
+            rgcn.rgcn_block_backward_sparse(self.blocks[l], self.inputs[l], self.params[l], dh,
+                                            demb, self.workspaces[l], f)
+            _mark(timer, ("sparse", l), 1)
+
+    def step(self, dy_top, timer=None) -> None:
+        """One pass of the whole path: plan, forward, backward."""
+        self.plan(timer=timer)
+        self.forward(timer=timer)
+        self.backward(dy_top, timer=timer)
+
+
+def _mark(timer, tag, edge: int) -> None:
+    if timer is not None:
+        timer(tag, edge)

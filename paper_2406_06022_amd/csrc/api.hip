@@ -1,0 +1,638 @@
+// C ABI of librgcn: argument validation, workspace layout and the order of kernel
+// launches for plan / forward / backward of one block.  No device memory is allocated
+// here; everything lives in the caller's workspace.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "common.h"
+
+using namespace rgcn;
+
+namespace {
+
+thread_local std::string g_err;
+
+rgcn_status fail(rgcn_status st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return st;
+}
+
+rgcn_status hip_fail(hipError_t e, const char *what) {
+    return fail(RGCN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define TRY_HIP(expr, what)                           \
+    do {                                              \
+        hipError_t _e = (expr);                       \
+        if (_e != hipSuccess) return hip_fail(_e, what); \
+    } while (0)
+
+inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+inline bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+inline bool aligned4(const void *p) { return ((uintptr_t)p & 3u) == 0; }
+constexpr int64_t kI32Max = 2147483647;
+
+// Everything the launches need to know about a block, derived on the host.
+struct Layout {
+    int T = 0, R = 0, d_in = 0, d_out = 0, es = 0;
+    rgcn_dtype dt = RGCN_F32;
+    uint32_t grad_mask = 0;
+    // forward slots: per destination type with n_dst > 0, self then relations into it
+    int nslots = 0;
+    FwdSlot slots[kMaxSlots];
+    int64_t n_seg = 0;
+    int type_slot0[kMaxTypes];          // first slot of type t (-1: no destination rows)
+    int type_nslots[kMaxTypes];
+    int rel_pos[kMaxRels];              // position of relation r among its type's slots
+    int64_t K[kMaxTypes];               // Mcat row length = nslots_t * d_in
+    // backward input-side slots (dMs): self if t is a grad type, relations leaving one
+    int dms_nslots[kMaxTypes];
+    int dms_self[kMaxTypes];            // slot index or -1
+    int dms_rel[kMaxRels];              // slot index in dMs_{dst(r)} or -1
+    int64_t bwd_base[kMaxTypes];
+    int64_t n_bwd_rows = 0;
+    // workspace offsets
+    size_t off_slots = 0, off_fwd_order = 0, off_bwd_order = 0, off_err = 0;
+    size_t off_csc_indptr[kMaxRels], off_csc_dst[kMaxRels];
+    size_t off_mcat[kMaxTypes], off_wcat[kMaxTypes];
+    size_t off_scratch = 0;
+    // scratch (a union: plan temporaries, or backward temporaries)
+    size_t plan_temp = 0;
+    size_t off_dms[kMaxTypes];          // relative to scratch
+    size_t off_partial = 0, off_colsum = 0;
+    size_t total = 0;
+};
+
+rgcn_status check_block(const rgcn_block *b) {
+    if (!b) return fail(RGCN_ERR_INVALID_ARG, "block is NULL");
+    if (b->num_types < 1 || b->num_types > kMaxTypes)
+        return fail(RGCN_ERR_INVALID_ARG, "num_types %d outside [1, %d]", b->num_types, kMaxTypes);
+    if (b->num_rels < 0 || b->num_rels > kMaxRels)
+        return fail(RGCN_ERR_INVALID_ARG, "num_rels %d outside [0, %d]", b->num_rels, kMaxRels);
+    if (!b->n_src || !b->n_dst) return fail(RGCN_ERR_INVALID_ARG, "n_src / n_dst is NULL");
+    if (b->num_rels > 0 && !b->rels) return fail(RGCN_ERR_INVALID_ARG, "rels is NULL");
+    if (b->grad_src_types >> b->num_types)
+        return fail(RGCN_ERR_INVALID_ARG, "grad_src_types names a type >= num_types");
+    for (int t = 0; t < b->num_types; ++t) {
+        if (b->n_dst[t] < 0 || b->n_src[t] < b->n_dst[t])
+            return fail(RGCN_ERR_SHAPE, "type %d: need 0 <= n_dst (%lld) <= n_src (%lld)", t,
+                        (long long)b->n_dst[t], (long long)b->n_src[t]);
+        if (b->n_src[t] >= kI32Max)
+            return fail(RGCN_ERR_UNSUPPORTED, "type %d: n_src must be below 2^31", t);
+    }
+    for (int r = 0; r < b->num_rels; ++r) {
+        const rgcn_relation &rel = b->rels[r];
+        if (rel.src_type < 0 || rel.src_type >= b->num_types || rel.dst_type < 0 ||
+            rel.dst_type >= b->num_types)
+            return fail(RGCN_ERR_INVALID_ARG, "relation %d: node type out of range", r);
+        if (rel.nnz < 0 || rel.nnz >= kI32Max)
+            return fail(RGCN_ERR_UNSUPPORTED, "relation %d: nnz must be in [0, 2^31)", r);
+        if (!rel.indptr || !aligned4(rel.indptr))
+            return fail(RGCN_ERR_INVALID_ARG, "relation %d: indptr NULL or misaligned", r);
+        if (rel.nnz > 0 && (!rel.indices || !aligned4(rel.indices)))
+            return fail(RGCN_ERR_INVALID_ARG, "relation %d: indices NULL or misaligned", r);
+        if (rel.nnz > 0 && b->n_src[rel.src_type] == 0)
+            return fail(RGCN_ERR_SHAPE, "relation %d: edges into an empty source type", r);
+    }
+    return RGCN_OK;
+}
+
+rgcn_status check_params(const rgcn_block *b, const rgcn_params *p) {
+    if (!p) return fail(RGCN_ERR_INVALID_ARG, "params is NULL");
+    if (p->dtype != RGCN_F32 && p->dtype != RGCN_BF16)
+        return fail(RGCN_ERR_DTYPE, "unknown dtype %d", (int)p->dtype);
+    const int vec = p->dtype == RGCN_BF16 ? 8 : 4;
+    if (p->d_in <= 0 || p->d_out <= 0)
+        return fail(RGCN_ERR_INVALID_ARG, "d_in / d_out must be positive");
+    if (p->d_in % vec || p->d_out % vec)
+        return fail(RGCN_ERR_UNSUPPORTED, "d_in and d_out must be multiples of %d", vec);
+    if (p->d_in > 256 * vec)
+        return fail(RGCN_ERR_UNSUPPORTED, "d_in above %d", 256 * vec);
+    if (b->num_rels > 0 && !p->w_rel) return fail(RGCN_ERR_INVALID_ARG, "w_rel is NULL");
+    for (int r = 0; r < b->num_rels; ++r)
+        if (!p->w_rel[r] || !aligned16(p->w_rel[r]))
+            return fail(RGCN_ERR_INVALID_ARG, "w_rel[%d] NULL or not 16-byte aligned", r);
+    if (!p->w_self) return fail(RGCN_ERR_INVALID_ARG, "w_self is NULL");
+    for (int t = 0; t < b->num_types; ++t) {
+        if (b->n_dst[t] > 0 && (!p->w_self[t] || !aligned16(p->w_self[t])))
+            return fail(RGCN_ERR_INVALID_ARG, "w_self[%d] NULL or not 16-byte aligned", t);
+        if (p->bias && p->bias[t] && !aligned16(p->bias[t]))
+            return fail(RGCN_ERR_INVALID_ARG, "bias[%d] not 16-byte aligned", t);
+    }
+    return RGCN_OK;
+}
+
+rgcn_status make_layout(const rgcn_block *b, const rgcn_params *p, Layout &L) {
+    rgcn_status st = check_block(b);
+    if (st != RGCN_OK) return st;
+    if ((st = check_params(b, p)) != RGCN_OK) return st;
+    L.T = b->num_types;
+    L.R = b->num_rels;
+    L.d_in = p->d_in;
+    L.d_out = p->d_out;
+    L.dt = p->dtype;
+    L.es = p->dtype == RGCN_BF16 ? 2 : 4;
+    L.grad_mask = b->grad_src_types;
+    // forward slots
+    L.nslots = 0;
+    L.n_seg = 0;
+    for (int r = 0; r < kMaxRels; ++r) { L.rel_pos[r] = -1; L.dms_rel[r] = -1; }
+    for (int t = 0; t < kMaxTypes; ++t) {
+        L.type_slot0[t] = -1;
+        L.type_nslots[t] = 0;
+        L.K[t] = 0;
+        L.dms_nslots[t] = 0;
+        L.dms_self[t] = -1;
+        L.bwd_base[t] = -1;
+    }
+    for (int t = 0; t < L.T; ++t) {
+        const int64_t nd = b->n_dst[t];
+        if (nd == 0) continue;
+        L.type_slot0[t] = L.nslots;
+        FwdSlot self{};
+        self.seg_base = L.n_seg;
+        self.src_type = t;
+        self.dst_type = t;
+        self.col_off = 0;
+        L.slots[L.nslots++] = self;
+        L.n_seg += nd;
+        int pos = 1;
+        for (int r = 0; r < L.R; ++r) {
+            if (b->rels[r].dst_type != t) continue;
+            FwdSlot s{};
+            s.seg_base = L.n_seg;
+            s.indptr = b->rels[r].indptr;
+            s.indices = b->rels[r].indices;
+            s.src_type = b->rels[r].src_type;
+            s.dst_type = t;
+            s.col_off = pos * L.d_in;
+            L.rel_pos[r] = pos;
+            L.slots[L.nslots++] = s;
+            L.n_seg += nd;
+            ++pos;
+        }
+        L.type_nslots[t] = pos;
+        L.K[t] = (int64_t)pos * L.d_in;
+    }
+    if (L.n_seg >= kI32Max) return fail(RGCN_ERR_UNSUPPORTED, "too many forward segments");
+    // backward slots
+    for (int t = 0; t < L.T; ++t) {
+        if (b->n_dst[t] == 0) continue;
+        int n = 0;
+        if (L.grad_mask >> t & 1u) L.dms_self[t] = n++;
+        for (int r = 0; r < L.R; ++r)
+            if (b->rels[r].dst_type == t && (L.grad_mask >> b->rels[r].src_type & 1u))
+                L.dms_rel[r] = n++;
+        L.dms_nslots[t] = n;
+    }
+    L.n_bwd_rows = 0;
+    for (int t = 0; t < L.T; ++t)
+        if (L.grad_mask >> t & 1u) {
+            L.bwd_base[t] = L.n_bwd_rows;
+            L.n_bwd_rows += b->n_src[t];
+        }
+    if (L.n_bwd_rows >= kI32Max) return fail(RGCN_ERR_UNSUPPORTED, "too many backward rows");
+
+    // persistent region
+    size_t off = 0;
+    L.off_err = off;                      off += 256;
+    L.off_slots = off;                    off += align256(sizeof(FwdSlot) * kMaxSlots);
+    L.off_fwd_order = off;                off += align256((size_t)L.n_seg * 4 + 4);
+    L.off_bwd_order = off;                off += align256((size_t)L.n_bwd_rows * 4 + 4);
+    for (int r = 0; r < kMaxRels; ++r) L.off_csc_indptr[r] = L.off_csc_dst[r] = SIZE_MAX;
+    for (int r = 0; r < L.R; ++r) {
+        const rgcn_relation &rel = b->rels[r];
+        if (!(L.grad_mask >> rel.src_type & 1u)) continue;
+        L.off_csc_indptr[r] = off;  off += align256((size_t)(b->n_src[rel.src_type] + 1) * 4);
+        L.off_csc_dst[r] = off;     off += align256((size_t)rel.nnz * 4 + 4);
+    }
+    for (int t = 0; t < kMaxTypes; ++t) L.off_mcat[t] = L.off_wcat[t] = SIZE_MAX;
+    for (int t = 0; t < L.T; ++t) {
+        if (b->n_dst[t] == 0) continue;
+        L.off_mcat[t] = off;  off += align256((size_t)b->n_dst[t] * L.K[t] * L.es);
+        L.off_wcat[t] = off;  off += align256((size_t)L.d_out * L.K[t] * L.es);
+    }
+    L.off_scratch = off;
+    // plan temporaries
+    size_t pt = bucket_sort_temp_bytes(L.n_seg, kSchedBuckets);
+    for (int r = 0; r < L.R; ++r) {
+        const rgcn_relation &rel = b->rels[r];
+        if (!(L.grad_mask >> rel.src_type & 1u)) continue;
+        size_t c = csc_temp_bytes(rel.nnz, b->n_src[rel.src_type]);
+        if (c > pt) pt = c;
+    }
+    for (int t = 0; t < L.T; ++t)
+        if (L.grad_mask >> t & 1u) {
+            size_t c = bucket_sort_temp_bytes(b->n_src[t], kSchedBuckets);
+            if (c > pt) pt = c;
+        }
+    L.plan_temp = align256(pt);
+    // backward temporaries
+    size_t bt = 0;
+    for (int t = 0; t < kMaxTypes; ++t) L.off_dms[t] = SIZE_MAX;
+    size_t part = 256, cols = 256;
+    for (int t = 0; t < L.T; ++t) {
+        if (b->n_dst[t] == 0) continue;
+        if (L.dms_nslots[t] > 0) {
+            L.off_dms[t] = bt;
+            bt += align256((size_t)b->n_dst[t] * L.dms_nslots[t] * L.d_in * 4);
+        }
+        size_t pb = gemm_dw_partial_bytes(b->n_dst[t], (int)L.K[t], L.d_out);
+        if (pb > part) part = pb;
+        size_t cb = column_sums_temp_bytes(b->n_dst[t], L.d_out);
+        if (cb > cols) cols = cb;
+    }
+    L.off_partial = bt;   bt += align256(part);
+    L.off_colsum = bt;    bt += align256(cols);
+    L.total = L.off_scratch + (L.plan_temp > bt ? L.plan_temp : bt);
+    return RGCN_OK;
+}
+
+rgcn_status check_workspace(const Layout &L, void *ws, size_t bytes) {
+    if (!ws) return fail(RGCN_ERR_INVALID_ARG, "workspace is NULL");
+    if ((uintptr_t)ws & 255u) return fail(RGCN_ERR_INVALID_ARG, "workspace not 256-byte aligned");
+    if (bytes < L.total)
+        return fail(RGCN_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", bytes, L.total);
+    return RGCN_OK;
+}
+
+rgcn_status check_inputs(const rgcn_block *b, const rgcn_input *in, const Layout &L,
+                         bool need_all_types) {
+    if (!in) return fail(RGCN_ERR_INVALID_ARG, "inputs are NULL");
+    const int vec = L.dt == RGCN_BF16 ? 8 : 4;
+    for (int t = 0; t < L.T; ++t) {
+        bool read = b->n_dst[t] > 0 || need_all_types;
+        for (int r = 0; r < L.R && !read; ++r)
+            read = b->rels[r].src_type == t && b->rels[r].nnz > 0;
+        if (!read || b->n_src[t] == 0) continue;
+        const rgcn_input &x = in[t];
+        if (!x.base || !aligned16(x.base))
+            return fail(RGCN_ERR_INVALID_ARG, "input %d: base NULL or not 16-byte aligned", t);
+        if (x.ld < L.d_in || x.ld % vec)
+            return fail(RGCN_ERR_SHAPE, "input %d: ld %lld must be >= d_in and a multiple of %d", t,
+                        (long long)x.ld, vec);
+        if (x.row_ids && !((uintptr_t)x.row_ids % 8 == 0))
+            return fail(RGCN_ERR_INVALID_ARG, "input %d: row_ids misaligned", t);
+        if (!x.row_ids && x.num_rows < b->n_src[t])
+            return fail(RGCN_ERR_SHAPE, "input %d: %lld rows < n_src %lld", t,
+                        (long long)x.num_rows, (long long)b->n_src[t]);
+        if (x.num_rows < 0) return fail(RGCN_ERR_SHAPE, "input %d: negative num_rows", t);
+    }
+    return RGCN_OK;
+}
+
+__global__ void k_zero_word(uint32_t *p) { *p = 0u; }
+
+// Device-side structural check (synchronises the stream).
+rgcn_status device_validate(const rgcn_block *b, const rgcn_input *in, const Layout &L,
+                            char *ws, hipStream_t s) {
+    uint32_t *err = (uint32_t *)(ws + L.off_err);
+    hipLaunchKernelGGL(k_zero_word, dim3(1), dim3(1), 0, s, err);
+    TRY_HIP(hipGetLastError(), "validate");
+    for (int r = 0; r < L.R; ++r) {
+        const rgcn_relation &rel = b->rels[r];
+        TRY_HIP(validate_csr(rel.indptr, rel.indices, b->n_dst[rel.dst_type], rel.nnz,
+                             b->n_src[rel.src_type], err, s), "validate_csr");
+    }
+    if (in)
+        for (int t = 0; t < L.T; ++t)
+            if (in[t].row_ids)
+                TRY_HIP(validate_ids(in[t].row_ids, b->n_src[t], in[t].num_rows, err, s),
+                        "validate_ids");
+    uint32_t host = 0;
+    TRY_HIP(hipMemcpyAsync(&host, err, 4, hipMemcpyDeviceToHost, s), "validate copy");
+    TRY_HIP(hipStreamSynchronize(s), "validate sync");
+    if (host & 1u) return fail(RGCN_ERR_BAD_CSR, "indptr is not a valid CSR offset array");
+    if (host & 2u) return fail(RGCN_ERR_INDEX_OOB, "an index or row id is out of range");
+    return RGCN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *rgcn_last_error(void) { return g_err.c_str(); }
+
+const char *rgcn_version(void) { return "rgcn-mi355x 0.1 (gfx950)"; }
+
+rgcn_status rgcn_block_workspace_size(const rgcn_block *block, const rgcn_params *params,
+                                      size_t *bytes) {
+    if (!bytes) return fail(RGCN_ERR_INVALID_ARG, "bytes is NULL");
+    Layout L;
+    rgcn_status st = make_layout(block, params, L);
+    if (st != RGCN_OK) return st;
+    *bytes = L.total;
+    return RGCN_OK;
+}
+
+rgcn_status rgcn_block_plan_layout(const rgcn_block *block, const rgcn_params *params,
+                                   rgcn_plan_layout *out) {
+    if (!out) return fail(RGCN_ERR_INVALID_ARG, "layout is NULL");
+    Layout L;
+    rgcn_status st = make_layout(block, params, L);
+    if (st != RGCN_OK) return st;
+    memset(out, 0, sizeof(*out));
+    out->n_fwd_segments = L.n_seg;
+    out->fwd_order = L.off_fwd_order;
+    out->n_bwd_rows = L.n_bwd_rows;
+    out->bwd_order = L.off_bwd_order;
+    for (int r = 0; r < RGCN_MAX_RELS; ++r) {
+        out->csc_indptr[r] = L.off_csc_indptr[r];
+        out->csc_dst[r] = L.off_csc_dst[r];
+    }
+    out->total_bytes = L.total;
+    return RGCN_OK;
+}
+
+rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
+                            void *workspace, size_t workspace_bytes, unsigned flags,
+                            hipStream_t stream) {
+    Layout L;
+    rgcn_status st = make_layout(block, params, L);
+    if (st != RGCN_OK) return st;
+    if ((st = check_workspace(L, workspace, workspace_bytes)) != RGCN_OK) return st;
+    char *ws = (char *)workspace;
+    if (flags & RGCN_VALIDATE_DEVICE) {
+        if ((st = device_validate(block, nullptr, L, ws, stream)) != RGCN_OK) return st;
+    }
+    char *scratch = ws + L.off_scratch;
+    if (L.nslots > 0)
+        TRY_HIP(fill_words(ws + L.off_slots, L.slots, sizeof(FwdSlot) * L.nslots, stream),
+                "slot table");
+    TRY_HIP(fwd_schedule(L.slots, L.nslots, L.n_seg, (int32_t *)(ws + L.off_fwd_order), scratch,
+                         stream), "forward schedule");
+    for (int r = 0; r < L.R; ++r) {
+        if (L.off_csc_indptr[r] == SIZE_MAX) continue;
+        const rgcn_relation &rel = block->rels[r];
+        TRY_HIP(csc_build(rel.indptr, rel.indices, block->n_dst[rel.dst_type],
+                          block->n_src[rel.src_type], rel.nnz,
+                          (int32_t *)(ws + L.off_csc_indptr[r]), (int32_t *)(ws + L.off_csc_dst[r]),
+                          scratch, stream), "csc build");
+    }
+    for (int t = 0; t < L.T; ++t) {
+        if (!(L.grad_mask >> t & 1u)) continue;
+        BwdKeyRels kr{};
+        for (int r = 0; r < L.R; ++r)
+            if (block->rels[r].src_type == t)
+                kr.csc_indptr[kr.count++] = (const int32_t *)(ws + L.off_csc_indptr[r]);
+        TRY_HIP(bwd_schedule(kr, block->n_src[t], (int32_t *)(ws + L.off_bwd_order) + L.bwd_base[t],
+                             scratch, stream), "backward schedule");
+    }
+    return RGCN_OK;
+}
+
+rgcn_status rgcn_block_aggregate(const rgcn_block *block, const rgcn_input *in,
+                                 const rgcn_params *params, void *workspace,
+                                 size_t workspace_bytes, unsigned flags, hipStream_t stream) {
+    Layout L;
+    rgcn_status st = make_layout(block, params, L);
+    if (st != RGCN_OK) return st;
+    if ((st = check_workspace(L, workspace, workspace_bytes)) != RGCN_OK) return st;
+    if ((st = check_inputs(block, in, L, false)) != RGCN_OK) return st;
+    char *ws = (char *)workspace;
+    if (flags & RGCN_VALIDATE_DEVICE) {
+        if ((st = device_validate(block, in, L, ws, stream)) != RGCN_OK) return st;
+    }
+    TypeInput tin[kMaxTypes];
+    void *mcat[kMaxTypes];
+    int64_t mld[kMaxTypes];
+    for (int t = 0; t < kMaxTypes; ++t) {
+        tin[t] = TypeInput{nullptr, nullptr, 0};
+        mcat[t] = nullptr;
+        mld[t] = 0;
+        if (t < L.T) {
+            tin[t] = TypeInput{in[t].base, in[t].row_ids, in[t].ld};
+            if (block->n_dst[t] > 0) {
+                mcat[t] = ws + L.off_mcat[t];
+                mld[t] = L.K[t];
+            }
+        }
+    }
+    TRY_HIP(gather_mean(L.dt, L.d_in, (const int32_t *)(ws + L.off_fwd_order), L.n_seg,
+                        (const FwdSlot *)(ws + L.off_slots), L.nslots, tin, mcat, mld, stream),
+            "gather mean");
+    return RGCN_OK;
+}
+
+rgcn_status rgcn_block_transform(const rgcn_block *block, const rgcn_params *params,
+                                 void *const *y, void *workspace, size_t workspace_bytes,
+                                 unsigned flags, hipStream_t stream) {
+    Layout L;
+    rgcn_status st = make_layout(block, params, L);
+    if (st != RGCN_OK) return st;
+    if ((st = check_workspace(L, workspace, workspace_bytes)) != RGCN_OK) return st;
+    if (!y) return fail(RGCN_ERR_INVALID_ARG, "y is NULL");
+    for (int t = 0; t < L.T; ++t)
+        if (block->n_dst[t] > 0 && (!y[t] || !aligned16(y[t])))
+            return fail(RGCN_ERR_INVALID_ARG, "y[%d] NULL or not 16-byte aligned", t);
+    char *ws = (char *)workspace;
+    for (int t = 0; t < L.T; ++t) {
+        if (block->n_dst[t] == 0) continue;
+        // weights of type t, K-contiguous: [W_self_t; W_r for r into t] transposed
+        const void *wslots[kMaxSlots];
+        wslots[0] = params->w_self[t];
+        for (int r = 0; r < L.R; ++r)
+            if (L.rel_pos[r] > 0 && block->rels[r].dst_type == t) wslots[L.rel_pos[r]] = params->w_rel[r];
+        TRY_HIP(pack_weights(L.dt, L.d_in, L.d_out, wslots, L.type_nslots[t], ws + L.off_wcat[t],
+                             stream), "pack weights");
+        const void *bias = params->bias ? params->bias[t] : nullptr;
+        TRY_HIP(gemm_forward(L.dt, ws + L.off_mcat[t], block->n_dst[t], L.d_out, (int)L.K[t],
+                             ws + L.off_wcat[t], bias, (flags & RGCN_FUSE_RELU) ? 1 : 0, y[t],
+                             stream), "forward transform");
+    }
+    return RGCN_OK;
+}
+
+rgcn_status rgcn_block_forward(const rgcn_block *block, const rgcn_input *in,
+                               const rgcn_params *params, void *const *y, void *workspace,
+                               size_t workspace_bytes, unsigned flags, hipStream_t stream) {
+    // check everything the second stage needs before enqueueing the first
+    if (!y) return fail(RGCN_ERR_INVALID_ARG, "y is NULL");
+    if (block && block->n_dst && block->num_types > 0 && block->num_types <= kMaxTypes)
+        for (int t = 0; t < block->num_types; ++t)
+            if (block->n_dst[t] > 0 && (!y[t] || !aligned16(y[t])))
+                return fail(RGCN_ERR_INVALID_ARG, "y[%d] NULL or not 16-byte aligned", t);
+    rgcn_status st = rgcn_block_aggregate(block, in, params, workspace, workspace_bytes, flags,
+                                          stream);
+    if (st != RGCN_OK) return st;
+    return rgcn_block_transform(block, params, y, workspace, workspace_bytes,
+                                flags & ~RGCN_VALIDATE_DEVICE, stream);
+}
+
+static rgcn_status check_dy(const rgcn_block *block, const Layout &L, const float *const *dy) {
+    if (!dy) return fail(RGCN_ERR_INVALID_ARG, "dy is NULL");
+    for (int t = 0; t < L.T; ++t)
+        if (block->n_dst[t] > 0 && (!dy[t] || !aligned16(dy[t])))
+            return fail(RGCN_ERR_INVALID_ARG, "dy[%d] NULL or not 16-byte aligned", t);
+    return RGCN_OK;
+}
+
+static rgcn_status check_sparse_outputs(const rgcn_block *block, const rgcn_input *in,
+                                        const Layout &L, float *const *dh_src,
+                                        float *const *demb, unsigned flags) {
+    for (int t = 0; t < L.T; ++t) {
+        const bool want = (dh_src && dh_src[t]) || (demb && demb[t]);
+        if (want && !(L.grad_mask >> t & 1u))
+            return fail(RGCN_ERR_INVALID_ARG,
+                        "dh_src/demb of type %d requested but bit %d of grad_src_types is clear", t, t);
+        if (dh_src && dh_src[t] && !aligned16(dh_src[t]))
+            return fail(RGCN_ERR_INVALID_ARG, "dh_src[%d] not 16-byte aligned", t);
+        if (demb && demb[t] && !aligned16(demb[t]))
+            return fail(RGCN_ERR_INVALID_ARG, "demb[%d] not 16-byte aligned", t);
+        if (want && block->n_src[t] > 0 && (!in || !in[t].base ||
+                                            ((flags & RGCN_INPUT_RELU) && !aligned16(in[t].base))))
+            return fail(RGCN_ERR_INVALID_ARG, "input %d needed for its gradient", t);
+    }
+    return RGCN_OK;
+}
+
+rgcn_status rgcn_block_backward_dense(const rgcn_block *block, const rgcn_params *params,
+                                      const float *const *dy, float *const *dw_rel,
+                                      float *const *dw_self, float *const *dbias,
+                                      void *workspace, size_t workspace_bytes, unsigned flags,
+                                      hipStream_t stream) {
+    (void)flags;
+    Layout L;
+    rgcn_status st = make_layout(block, params, L);
+    if (st != RGCN_OK) return st;
+    if ((st = check_workspace(L, workspace, workspace_bytes)) != RGCN_OK) return st;
+    if ((st = check_dy(block, L, dy)) != RGCN_OK) return st;
+    for (int t = 0; t < L.T; ++t)
+        if (dw_self && dw_self[t])
+            for (int u = 0; u < t; ++u)
+                if (dw_self[u] == dw_self[t])
+                    return fail(RGCN_ERR_INVALID_ARG, "dw_self[%d] aliases dw_self[%d]", t, u);
+    char *ws = (char *)workspace;
+    char *scratch = ws + L.off_scratch;
+    for (int t = 0; t < L.T; ++t) {
+        const int64_t nd = block->n_dst[t];
+        // weight side: [dW_self_t; dW_r ...] = Mcat_t^T dY_t
+        DwOut out{};
+        out.count = nd > 0 ? L.type_nslots[t] : 1;
+        out.w[0] = dw_self ? dw_self[t] : nullptr;
+        bool any = out.w[0] != nullptr;
+        if (nd > 0) {
+            for (int r = 0; r < L.R; ++r)
+                if (L.rel_pos[r] > 0 && block->rels[r].dst_type == t) {
+                    out.w[L.rel_pos[r]] = dw_rel ? dw_rel[r] : nullptr;
+                    any |= out.w[L.rel_pos[r]] != nullptr;
+                }
+        } else {  // no rows: gradients of the weights into t are zero
+            for (int r = 0; r < L.R; ++r)
+                if (block->rels[r].dst_type == t && dw_rel && dw_rel[r] && out.count < kMaxSlots) {
+                    out.w[out.count++] = dw_rel[r];
+                    any = true;
+                }
+        }
+        if (any)
+            TRY_HIP(gemm_dw(L.dt, nd > 0 ? ws + L.off_mcat[t] : nullptr, nd,
+                            nd > 0 ? (int)L.K[t] : out.count * L.d_in, L.d_in,
+                            nd > 0 ? dy[t] : nullptr, L.d_out, out,
+                            (float *)(scratch + L.off_partial), stream), "weight gradient");
+        if (dbias && dbias[t])
+            TRY_HIP(column_sums(nd > 0 ? dy[t] : nullptr, nd, L.d_out, dbias[t],
+                                (float *)(scratch + L.off_colsum), 0, stream), "bias gradient");
+        // input side: dMs_t = dY_t [W_self_t | W_r ...]^T, relation slots divided by deg
+        if (nd > 0 && L.dms_nslots[t] > 0) {
+            DmsSlots ds{};
+            ds.count = L.dms_nslots[t];
+            if (L.dms_self[t] >= 0) {
+                ds.w[L.dms_self[t]] = params->w_self[t];
+                ds.indptr[L.dms_self[t]] = nullptr;
+            }
+            for (int r = 0; r < L.R; ++r)
+                if (L.dms_rel[r] >= 0 && block->rels[r].dst_type == t) {
+                    ds.w[L.dms_rel[r]] = params->w_rel[r];
+                    ds.indptr[L.dms_rel[r]] = block->rels[r].indptr;
+                }
+            TRY_HIP(gemm_dms(L.dt, dy[t], nd, L.d_out, L.d_in, ds,
+                             (float *)(scratch + L.off_dms[t]), stream), "input-side transform");
+        }
+    }
+    return RGCN_OK;
+}
+
+rgcn_status rgcn_block_backward_sparse(const rgcn_block *block, const rgcn_input *in,
+                                       const rgcn_params *params, float *const *dh_src,
+                                       float *const *demb, void *workspace,
+                                       size_t workspace_bytes, unsigned flags,
+                                       hipStream_t stream) {
+    Layout L;
+    rgcn_status st = make_layout(block, params, L);
+    if (st != RGCN_OK) return st;
+    if ((st = check_workspace(L, workspace, workspace_bytes)) != RGCN_OK) return st;
+    if ((st = check_sparse_outputs(block, in, L, dh_src, demb, flags)) != RGCN_OK) return st;
+    char *ws = (char *)workspace;
+    if ((flags & RGCN_VALIDATE_DEVICE) && in) {
+        if ((st = device_validate(block, in, L, ws, stream)) != RGCN_OK) return st;
+    }
+    char *scratch = ws + L.off_scratch;
+    for (int s = 0; s < L.T; ++s) {
+        float *dh = dh_src ? dh_src[s] : nullptr;
+        float *de = demb ? demb[s] : nullptr;
+        if (!dh && !de) continue;
+        TsumArgs a;
+        memset(&a, 0, sizeof(a));
+        a.order = (const int32_t *)(ws + L.off_bwd_order) + L.bwd_base[s];
+        a.n_rows = block->n_src[s];
+        a.n_dst = block->n_dst[s];
+        if (block->n_dst[s] > 0 && L.dms_self[s] >= 0) {
+            a.self_dms = (const float *)(scratch + L.off_dms[s]) + (int64_t)L.dms_self[s] * L.d_in;
+            a.self_ld = (int64_t)L.dms_nslots[s] * L.d_in;
+        }
+        a.in = TypeInput{in[s].base, in[s].row_ids, in[s].ld};
+        a.input_relu = (flags & RGCN_INPUT_RELU) ? 1 : 0;
+        a.ids_unique = (flags & RGCN_IDS_UNIQUE) ? 1 : 0;
+        a.dh = dh;
+        a.demb = de;
+        a.d_in = L.d_in;
+        for (int r = 0; r < L.R; ++r) {
+            const rgcn_relation &rel = block->rels[r];
+            if (rel.src_type != s || block->n_dst[rel.dst_type] == 0) continue;
+            const int t = rel.dst_type;
+            TsumRel tr;
+            tr.csc_indptr = (const int32_t *)(ws + L.off_csc_indptr[r]);
+            tr.csc_dst = (const int32_t *)(ws + L.off_csc_dst[r]);
+            tr.dms = (const float *)(scratch + L.off_dms[t]) + (int64_t)L.dms_rel[r] * L.d_in;
+            tr.dms_ld = (int64_t)L.dms_nslots[t] * L.d_in;
+            a.rel[a.nrel++] = tr;
+        }
+        TRY_HIP(transpose_sum(L.dt, a, stream), "transposed sum");
+    }
+    return RGCN_OK;
+}
+
+rgcn_status rgcn_block_backward(const rgcn_block *block, const rgcn_input *in,
+                                const rgcn_params *params, const float *const *dy,
+                                float *const *dw_rel, float *const *dw_self,
+                                float *const *dbias, float *const *dh_src, float *const *demb,
+                                void *workspace, size_t workspace_bytes, unsigned flags,
+                                hipStream_t stream) {
+    // validate what both stages need before enqueueing anything
+    Layout L;
+    rgcn_status st = make_layout(block, params, L);
+    if (st != RGCN_OK) return st;
+    if ((st = check_workspace(L, workspace, workspace_bytes)) != RGCN_OK) return st;
+    if ((st = check_inputs(block, in, L, false)) != RGCN_OK) return st;
+    if ((st = check_dy(block, L, dy)) != RGCN_OK) return st;
+    if ((st = check_sparse_outputs(block, in, L, dh_src, demb, flags)) != RGCN_OK) return st;
+    if (flags & RGCN_VALIDATE_DEVICE) {
+        if ((st = device_validate(block, in, L, (char *)workspace, stream)) != RGCN_OK) return st;
+    }
+    const unsigned f = flags & ~RGCN_VALIDATE_DEVICE;
+    st = rgcn_block_backward_dense(block, params, dy, dw_rel, dw_self, dbias, workspace,
+                                   workspace_bytes, f, stream);
+    if (st != RGCN_OK) return st;
+    return rgcn_block_backward_sparse(block, in, params, dh_src, demb, workspace,
+                                      workspace_bytes, f, stream);
+}
+
+}  // extern "C"

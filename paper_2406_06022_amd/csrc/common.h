@@ -1,0 +1,162 @@
+// Internal declarations shared by the HIP translation units of librgcn (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "rgcn.h"
+
+namespace rgcn {
+
+// ------------------------------------------------------------------------------------
+// Element helpers
+// ------------------------------------------------------------------------------------
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+// Number of set bits of `mask` below the calling lane (wave64).
+__device__ __forceinline__ int lanes_below(uint64_t mask) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                          __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+// Workgroup index remapped so that consecutive logical ids run on the same XCD.  The
+// dispatcher hands workgroup w to XCD (w mod 8); logical id = XCD-major order.
+__device__ __forceinline__ int64_t xcd_major_id(int64_t wg, int64_t total) {
+    const int64_t nx = 8;
+    int64_t per = total / nx, rem = total % nx;
+    int64_t x = wg % nx, idx = wg / nx;
+    return x < rem ? x * (per + 1) + idx : rem * (per + 1) + (x - rem) * per + idx;
+}
+
+// ------------------------------------------------------------------------------------
+// Limits and launch-side tables
+// ------------------------------------------------------------------------------------
+constexpr int kMaxTypes = RGCN_MAX_TYPES;
+constexpr int kMaxRels = RGCN_MAX_RELS;
+constexpr int kMaxSlots = RGCN_MAX_TYPES + RGCN_MAX_RELS;  // forward slots: self + relations
+constexpr int kSchedBuckets = 64;                          // degree keys 0..63
+
+// A forward slot: the self-loop rows of a destination type, or the rows of one relation.
+struct FwdSlot {
+    int64_t seg_base;        // first segment id of this slot
+    const int32_t *indptr;   // NULL: self-loop slot (every row has degree 1)
+    const int32_t *indices;
+    int32_t src_type;
+    int32_t dst_type;
+    int32_t col_off;         // element offset of this slot inside a row of Mcat_t
+    int32_t pad;
+};
+
+struct TypeInput {           // rgcn_input restated for the device
+    const void *base;
+    const int64_t *row_ids;
+    int64_t ld;
+};
+
+// ------------------------------------------------------------------------------------
+// Host launchers (each enqueues on `stream`; return hipSuccess or the launch error)
+// ------------------------------------------------------------------------------------
+// sort.hip
+size_t scan_temp_bytes(int64_t n);
+hipError_t exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, void *temp,
+                              hipStream_t s);
+size_t bucket_sort_temp_bytes(int64_t n, int nbuckets);
+hipError_t fwd_schedule(const FwdSlot *slots_dev, int nslots, int64_t n_seg, int32_t *order,
+                        void *temp, hipStream_t s);
+hipError_t csc_build(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
+                     int64_t n_src, int64_t nnz, int32_t *csc_indptr, int32_t *csc_dst,
+                     void *temp, hipStream_t s);
+size_t csc_temp_bytes(int64_t nnz, int64_t n_src);
+struct BwdKeyRels {          // relations leaving one source type
+    int32_t count;
+    const int32_t *csc_indptr[kMaxRels];
+};
+hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, void *temp,
+                        hipStream_t s);
+hipError_t fill_words(void *dst, const void *src_host, size_t bytes, hipStream_t s);
+
+// aggregate.hip
+hipError_t gather_mean(rgcn_dtype dt, int d_in, const int32_t *order, int64_t n_seg,
+                       const FwdSlot *slots_dev, int nslots, const TypeInput *in,
+                       void *const *mcat, const int64_t *mcat_ld, hipStream_t s);
+
+struct TsumRel {
+    const int32_t *csc_indptr;
+    const int32_t *csc_dst;
+    const float *dms;        // dMs of the destination type, already offset to this slot
+    int64_t dms_ld;
+};
+struct TsumArgs {
+    const int32_t *order;    // backward schedule of this source type
+    int64_t n_rows;          // n_src[s]
+    int64_t n_dst;           // n_dst[s]
+    const float *self_dms;   // dY_s W_self_s^T rows (NULL if n_dst == 0)
+    int64_t self_ld;
+    TypeInput in;            // block input of type s (for the ReLU mask and row ids)
+    int32_t input_relu;
+    int32_t ids_unique;
+    float *dh;               // [n_src x d_in] or NULL
+    float *demb;             // table-shaped or NULL
+    int32_t d_in;
+    int32_t nrel;
+    TsumRel rel[kMaxRels];
+};
+hipError_t transpose_sum(rgcn_dtype dt, const TsumArgs &a, hipStream_t s);
+
+hipError_t pack_weights(rgcn_dtype dt, int d_in, int d_out, const void *const *w_slots,
+                        int nslots, void *wcat_t, hipStream_t s);
+hipError_t column_sums(const float *dy, int64_t rows, int cols, float *out, float *partial,
+                       int64_t max_splits, hipStream_t s);
+size_t column_sums_temp_bytes(int64_t rows, int cols);
+hipError_t validate_csr(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
+                        int64_t nnz, int64_t n_src, uint32_t *err, hipStream_t s);
+hipError_t validate_ids(const int64_t *ids, int64_t n, int64_t num_rows, uint32_t *err,
+                        hipStream_t s);
+
+// gemm.hip
+// Forward: Y = A W + bias (opt. ReLU); A [M x K] row-major (ld K), wcat_t [N x K].
+hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
+                        const void *wcat_t, const void *bias, int relu, void *y,
+                        hipStream_t s);
+// Backward input side: C[m][n] = (sum_k dy[m][k] W_slot(n)[c(n)][k]) / deg_slot(n)(m);
+// slot(n) = n / d_in, c(n) = n % d_in; indptr[slot] NULL: no scaling (self-loop slot).
+struct DmsSlots {
+    int32_t count;
+    const void *w[kMaxSlots];
+    const int32_t *indptr[kMaxSlots];
+};
+hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_in,
+                    const DmsSlots &slots, float *dms, hipStream_t s);
+// Weight side: dWcat[kc][o] = sum_i Mcat[i][kc] dy[i][o], K = rows of Mcat.
+size_t gemm_dw_partial_bytes(int64_t M, int Kcat, int d_out);
+struct DwOut {
+    int32_t count;            // slots
+    float *w[kMaxSlots];      // destination of slot s ([d_in x d_out]) or NULL
+};
+hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_in,
+                   const float *dy, int d_out, const DwOut &out, float *partial,
+                   hipStream_t s);
+
+}  // namespace rgcn
+
+#define RGCN_HIP_TRY(expr)                         \
+    do {                                           \
+        hipError_t _e = (expr);                    \
+        if (_e != hipSuccess) return _e;           \
+    } while (0)

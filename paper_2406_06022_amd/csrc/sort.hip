@@ -1,0 +1,349 @@
+// Integer plan of a block: exclusive scans, stable counting sorts by small keys (the
+// degree-sorted schedules) and LSD radix sorts of edges by source row (the CSC
+// transpose).  Everything here is integer arithmetic and deterministic: the result does
+// not depend on scheduling, so it is bit-exact against a sequential stable sort.
+#include "common.h"
+
+namespace rgcn {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kScanItems = 8;
+constexpr int kScanTile = kThreads * kScanItems;     // 2048
+constexpr int kSortItems = 16;
+constexpr int kSortTile = kThreads * kSortItems;     // 4096
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+__host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Exclusive scan of one value per thread over a 256-thread workgroup.
+__device__ int wg_exclusive_scan(int v, int *total) {
+    __shared__ int buf[kThreads];
+    const int t = threadIdx.x;
+    buf[t] = v;
+    __syncthreads();
+    for (int off = 1; off < kThreads; off <<= 1) {
+        int x = t >= off ? buf[t - off] : 0;
+        __syncthreads();
+        buf[t] += x;
+        __syncthreads();
+    }
+    int incl = buf[t];
+    *total = buf[kThreads - 1];
+    __syncthreads();
+    return incl - v;
+}
+
+// ---------------------------------------------------------------- scan (3 kernels)
+__global__ __launch_bounds__(kThreads) void k_scan_reduce(const int32_t *in, int64_t n,
+                                                          int32_t *partial) {
+    const int64_t base = (int64_t)blockIdx.x * kScanTile;
+    int sum = 0;
+    for (int u = 0; u < kScanItems; ++u) {
+        int64_t i = base + (int64_t)u * kThreads + threadIdx.x;
+        if (i < n) sum += in[i];
+    }
+    int total;
+    wg_exclusive_scan(sum, &total);
+    if (threadIdx.x == 0) partial[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(kThreads) void k_scan_partials(int32_t *partial, int64_t nb) {
+    int carry = 0;
+    for (int64_t c0 = 0; c0 < nb; c0 += kScanTile) {
+        int v[kScanItems];
+        int sum = 0;
+        for (int u = 0; u < kScanItems; ++u) {
+            int64_t i = c0 + (int64_t)threadIdx.x * kScanItems + u;
+            v[u] = i < nb ? partial[i] : 0;
+            sum += v[u];
+        }
+        int total;
+        int pre = wg_exclusive_scan(sum, &total) + carry;
+        for (int u = 0; u < kScanItems; ++u) {
+            int64_t i = c0 + (int64_t)threadIdx.x * kScanItems + u;
+            if (i < nb) partial[i] = pre;
+            pre += v[u];
+        }
+        carry += total;
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void k_scan_apply(const int32_t *in, int32_t *out,
+                                                         int64_t n, const int32_t *partial) {
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    int v[kScanItems];
+    int sum = 0;
+    for (int u = 0; u < kScanItems; ++u) {
+        int64_t i = base + u;
+        v[u] = i < n ? in[i] : 0;
+        sum += v[u];
+    }
+    int total;
+    int pre = wg_exclusive_scan(sum, &total) + partial[blockIdx.x];
+    for (int u = 0; u < kScanItems; ++u) {
+        int64_t i = base + u;
+        if (i < n) out[i] = pre;
+        pre += v[u];
+    }
+}
+
+// ---------------------------------------------------------------- stable bucket sort
+// Items of a tile are visited in "striped" order: round u, thread t -> item
+// tile*4096 + u*256 + t.  That order is ascending item index, so ranking items of equal
+// key in that order keeps the sort stable.
+template <int NB, class KeyFn>
+__global__ __launch_bounds__(kThreads) void k_bucket_hist(KeyFn kf, int64_t n, int32_t *hist,
+                                                          int32_t ntiles) {
+    __shared__ int32_t h[NB];
+    for (int b = threadIdx.x; b < NB; b += kThreads) h[b] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kSortTile;
+    for (int u = 0; u < kSortItems; ++u) {
+        int64_t idx = base + (int64_t)u * kThreads + threadIdx.x;
+        if (idx < n) atomicAdd(&h[kf(idx)], 1);
+    }
+    __syncthreads();
+    for (int b = threadIdx.x; b < NB; b += kThreads)
+        hist[(int64_t)b * ntiles + blockIdx.x] = h[b];
+}
+
+template <int NB, int BITS, class KeyFn, class PutFn>
+__global__ __launch_bounds__(kThreads) void k_bucket_scatter(KeyFn kf, PutFn put, int64_t n,
+                                                             const int32_t *offs,
+                                                             int32_t ntiles) {
+    __shared__ int32_t run[NB];
+    __shared__ int32_t wcnt[kThreads / 64][NB];
+    for (int b = threadIdx.x; b < NB; b += kThreads) {
+        run[b] = offs[(int64_t)b * ntiles + blockIdx.x];
+        for (int w = 0; w < kThreads / 64; ++w) wcnt[w][b] = 0;
+    }
+    __syncthreads();
+    const int wave = threadIdx.x >> 6;
+    const int64_t base = (int64_t)blockIdx.x * kSortTile;
+    for (int u = 0; u < kSortItems; ++u) {
+        const int64_t idx = base + (int64_t)u * kThreads + threadIdx.x;
+        const bool valid = idx < n;
+        const int key = valid ? kf(idx) : 0;
+        // lanes of this wave holding the same key (all lanes take part in every ballot)
+        uint64_t peers = __ballot(valid);
+        for (int b = 0; b < BITS; ++b) {
+            const bool bit = (key >> b) & 1;
+            const uint64_t m = __ballot(bit);
+            peers &= bit ? m : ~m;
+        }
+        const int rank = lanes_below(peers);
+        if (valid && rank == 0) wcnt[wave][key] = __popcll(peers);
+        __syncthreads();
+        if (valid) {
+            int pos = run[key] + rank;
+            for (int w = 0; w < wave; ++w) pos += wcnt[w][key];
+            put(pos, idx);
+        }
+        __syncthreads();
+        for (int b = threadIdx.x; b < NB; b += kThreads) {
+            int add = 0;
+            for (int w = 0; w < kThreads / 64; ++w) {
+                add += wcnt[w][b];
+                wcnt[w][b] = 0;
+            }
+            run[b] += add;
+        }
+        __syncthreads();
+    }
+}
+
+template <int NB, int BITS, class KeyFn, class PutFn>
+hipError_t bucket_sort(const KeyFn &kf, const PutFn &put, int64_t n, void *temp,
+                       hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    const int64_t ntiles = cdiv(n, kSortTile);
+    int32_t *hist = (int32_t *)temp;
+    void *scan_tmp = (char *)temp + align_up((size_t)NB * ntiles * 4, 256);
+    hipLaunchKernelGGL((k_bucket_hist<NB, KeyFn>), dim3((unsigned)ntiles), dim3(kThreads), 0,
+                       s, kf, n, hist, (int32_t)ntiles);
+    RGCN_HIP_TRY(hipGetLastError());
+    RGCN_HIP_TRY(exclusive_scan_i32(hist, hist, (int64_t)NB * ntiles, scan_tmp, s));
+    hipLaunchKernelGGL((k_bucket_scatter<NB, BITS, KeyFn, PutFn>), dim3((unsigned)ntiles),
+                       dim3(kThreads), 0, s, kf, put, n, hist, (int32_t)ntiles);
+    return hipGetLastError();
+}
+
+__device__ __forceinline__ int degree_key(int64_t deg) {
+    return kSchedBuckets - 1 - (int)(deg < kSchedBuckets - 1 ? deg : kSchedBuckets - 1);
+}
+
+// Forward segments: key of segment id = degree key of its (slot, row).
+struct FwdKey {
+    int32_t nslots;
+    int64_t base[kMaxSlots];
+    const int32_t *indptr[kMaxSlots];
+    __device__ int operator()(int64_t seg) const {
+        int lo = 0, hi = nslots - 1;           // last slot with base <= seg
+        while (lo < hi) {
+            int mid = (lo + hi + 1) >> 1;
+            if (base[mid] <= seg) lo = mid; else hi = mid - 1;
+        }
+        const int32_t *ip = indptr[lo];
+        if (!ip) return degree_key(1);
+        int64_t row = seg - base[lo];
+        return degree_key((int64_t)ip[row + 1] - ip[row]);
+    }
+};
+
+struct PutIndex {
+    int32_t *order;
+    __device__ void operator()(int pos, int64_t idx) const { order[pos] = (int32_t)idx; }
+};
+
+// Backward rows of one source type: key = degree key of the in-degree summed over the
+// relations leaving the type.
+struct BwdKey {
+    BwdKeyRels rels;
+    __device__ int operator()(int64_t j) const {
+        int64_t deg = 0;
+        for (int r = 0; r < rels.count; ++r)
+            deg += (int64_t)rels.csc_indptr[r][j + 1] - rels.csc_indptr[r][j];
+        return degree_key(deg);
+    }
+};
+
+// Radix pass: 8-bit digit of the key at `shift`.
+struct RadixKey {
+    const uint32_t *keys;
+    int shift;
+    __device__ int operator()(int64_t i) const { return (int)((keys[i] >> shift) & 255u); }
+};
+struct RadixPut {
+    const uint32_t *kin;
+    const int32_t *vin;
+    uint32_t *kout;
+    int32_t *vout;
+    __device__ void operator()(int pos, int64_t i) const {
+        kout[pos] = kin[i];
+        vout[pos] = vin[i];
+    }
+};
+
+// Destination row of every edge: vals[k] = i for k in [indptr[i], indptr[i+1]).
+__global__ __launch_bounds__(kThreads) void k_expand_rows(const int32_t *indptr, int64_t n_dst,
+                                                          int32_t *vals) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= n_dst) return;
+    for (int32_t k = indptr[i]; k < indptr[i + 1]; ++k) vals[k] = (int32_t)i;
+}
+
+// csc_indptr[j] = number of sorted keys < j (lower bound), j in [0, n_src].
+__global__ __launch_bounds__(kThreads) void k_lower_bounds(const uint32_t *sorted, int64_t nnz,
+                                                           int64_t n_src, int32_t *out) {
+    const int64_t j = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (j > n_src) return;
+    int64_t lo = 0, hi = nnz;
+    while (lo < hi) {
+        int64_t mid = (lo + hi) >> 1;
+        if ((int64_t)sorted[mid] < j) lo = mid + 1; else hi = mid;
+    }
+    out[j] = (int32_t)lo;
+}
+
+struct Words {
+    uint32_t n;
+    uint32_t w[512];
+};
+__global__ void k_fill_words(uint32_t *dst, Words a) {
+    for (uint32_t i = threadIdx.x; i < a.n; i += blockDim.x) dst[i] = a.w[i];
+}
+
+}  // namespace
+
+size_t scan_temp_bytes(int64_t n) { return align_up((size_t)cdiv(n, kScanTile) * 4 + 4, 256); }
+
+hipError_t exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, void *temp,
+                              hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    const int64_t nb = cdiv(n, kScanTile);
+    int32_t *partial = (int32_t *)temp;
+    hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)nb), dim3(kThreads), 0, s, in, n, partial);
+    RGCN_HIP_TRY(hipGetLastError());
+    hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kThreads), 0, s, partial, nb);
+    RGCN_HIP_TRY(hipGetLastError());
+    hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)nb), dim3(kThreads), 0, s, in, out, n,
+                       partial);
+    return hipGetLastError();
+}
+
+size_t bucket_sort_temp_bytes(int64_t n, int nbuckets) {
+    const int64_t ntiles = cdiv(n, kSortTile);
+    return align_up((size_t)nbuckets * ntiles * 4, 256) +
+           scan_temp_bytes((int64_t)nbuckets * ntiles);
+}
+
+hipError_t fwd_schedule(const FwdSlot *slots_host, int nslots, int64_t n_seg, int32_t *order,
+                        void *temp, hipStream_t s) {
+    FwdKey kf;
+    kf.nslots = nslots;
+    for (int i = 0; i < kMaxSlots; ++i) {
+        kf.base[i] = i < nslots ? slots_host[i].seg_base : 0;
+        kf.indptr[i] = i < nslots ? slots_host[i].indptr : nullptr;
+    }
+    return bucket_sort<kSchedBuckets, 6>(kf, PutIndex{order}, n_seg, temp, s);
+}
+
+hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, void *temp,
+                        hipStream_t s) {
+    return bucket_sort<kSchedBuckets, 6>(BwdKey{rels}, PutIndex{order}, n_rows, temp, s);
+}
+
+static int radix_passes(int64_t n_src) {
+    int bits = 0;
+    while (bits < 31 && (((int64_t)1 << bits) < n_src)) ++bits;  // keys < n_src <= 2^bits
+    return (bits + 7) / 8;
+}
+
+size_t csc_temp_bytes(int64_t nnz, int64_t n_src) {
+    (void)n_src;
+    return 3 * align_up((size_t)nnz * 4 + 4, 256) + bucket_sort_temp_bytes(nnz, 256);
+}
+
+hipError_t csc_build(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
+                     int64_t n_src, int64_t nnz, int32_t *csc_indptr, int32_t *csc_dst,
+                     void *temp, hipStream_t s) {
+    const size_t arr = align_up((size_t)nnz * 4 + 4, 256);
+    int32_t *tmp_vals = (int32_t *)temp;
+    uint32_t *kb[2] = {(uint32_t *)((char *)temp + arr), (uint32_t *)((char *)temp + 2 * arr)};
+    void *sort_tmp = (char *)temp + 3 * arr;
+    const int np = nnz > 0 ? radix_passes(n_src) : 0;
+    int32_t *vb[2];
+    vb[np % 2] = csc_dst;
+    vb[(np + 1) % 2] = tmp_vals;
+    if (n_dst > 0 && nnz > 0) {
+        hipLaunchKernelGGL(k_expand_rows, dim3((unsigned)cdiv(n_dst, kThreads)), dim3(kThreads),
+                           0, s, indptr, n_dst, vb[0]);
+        RGCN_HIP_TRY(hipGetLastError());
+    }
+    const uint32_t *keys = (const uint32_t *)indices;
+    for (int p = 0; p < np; ++p) {
+        RadixKey kf{keys, 8 * p};
+        RadixPut put{keys, vb[p % 2], kb[p % 2], vb[(p + 1) % 2]};
+        RGCN_HIP_TRY((bucket_sort<256, 8>(kf, put, nnz, sort_tmp, s)));
+        keys = kb[p % 2];
+    }
+    hipLaunchKernelGGL(k_lower_bounds, dim3((unsigned)cdiv(n_src + 1, kThreads)), dim3(kThreads),
+                       0, s, keys, nnz, n_src, csc_indptr);
+    return hipGetLastError();
+}
+
+hipError_t fill_words(void *dst, const void *src_host, size_t bytes, hipStream_t s) {
+    const uint32_t *src = (const uint32_t *)src_host;
+    size_t nw = bytes / 4;
+    for (size_t off = 0; off < nw; off += 512) {
+        Words a;
+        a.n = (uint32_t)((nw - off) < 512 ? (nw - off) : 512);
+        for (uint32_t i = 0; i < a.n; ++i) a.w[i] = src[off + i];
+        hipLaunchKernelGGL(k_fill_words, dim3(1), dim3(256), 0, s, (uint32_t *)dst + off, a);
+        RGCN_HIP_TRY(hipGetLastError());
+    }
+    return hipSuccess;
+}
+
+}  // namespace rgcn

@@ -1,0 +1,306 @@
+"""Python binding of librgcn (include/rgcn.h): argument marshalling only.
+
+Every function here passes device pointers and sizes across the C ABI and raises
+``RgcnError`` on a non-OK status.  No arithmetic of the layer happens in Python; there is
+no CPU fallback.  Tensors are torch tensors used as device memory; the stream is torch's
+current stream unless one is given.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librgcn.so")
+
+RGCN_F32, RGCN_BF16 = 0, 1
+RGCN_MAX_TYPES, RGCN_MAX_RELS = 16, 64
+RGCN_VALIDATE_DEVICE = 0x1
+RGCN_FUSE_RELU = 0x2
+RGCN_INPUT_RELU = 0x4
+RGCN_IDS_UNIQUE = 0x8
+STATUS_NAMES = {0: "RGCN_OK", 1: "RGCN_ERR_INVALID_ARG", 2: "RGCN_ERR_SHAPE",
+                3: "RGCN_ERR_DTYPE", 4: "RGCN_ERR_INDEX_OOB", 5: "RGCN_ERR_BAD_CSR",
+                6: "RGCN_ERR_WORKSPACE_TOO_SMALL", 7: "RGCN_ERR_UNSUPPORTED", 8: "RGCN_ERR_HIP"}
+EXPORTED = ("rgcn_block_workspace_size", "rgcn_block_plan_layout", "rgcn_block_plan",
+            "rgcn_block_forward", "rgcn_block_backward", "rgcn_block_aggregate",
+            "rgcn_block_transform", "rgcn_block_backward_dense", "rgcn_block_backward_sparse",
+            "rgcn_last_error", "rgcn_version")
+
+
+class RgcnError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class _Relation(ctypes.Structure):
+    _fields_ = [("src_type", ctypes.c_int32), ("dst_type", ctypes.c_int32),
+                ("nnz", ctypes.c_int64), ("indptr", ctypes.c_void_p),
+                ("indices", ctypes.c_void_p)]
+
+
+class _Block(ctypes.Structure):
+    _fields_ = [("num_types", ctypes.c_int32), ("num_rels", ctypes.c_int32),
+                ("n_src", ctypes.POINTER(ctypes.c_int64)), ("n_dst", ctypes.POINTER(ctypes.c_int64)),
+                ("rels", ctypes.POINTER(_Relation)), ("grad_src_types", ctypes.c_uint32)]
+
+
+class _Input(ctypes.Structure):
+    _fields_ = [("base", ctypes.c_void_p), ("row_ids", ctypes.c_void_p),
+                ("num_rows", ctypes.c_int64), ("ld", ctypes.c_int64)]
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int), ("d_in", ctypes.c_int32), ("d_out", ctypes.c_int32),
+                ("w_rel", ctypes.POINTER(ctypes.c_void_p)),
+                ("w_self", ctypes.POINTER(ctypes.c_void_p)),
+                ("bias", ctypes.POINTER(ctypes.c_void_p))]
+
+
+class _PlanLayout(ctypes.Structure):
+    _fields_ = [("n_fwd_segments", ctypes.c_int64), ("fwd_order", ctypes.c_size_t),
+                ("n_bwd_rows", ctypes.c_int64), ("bwd_order", ctypes.c_size_t),
+                ("csc_indptr", ctypes.c_size_t * RGCN_MAX_RELS),
+                ("csc_dst", ctypes.c_size_t * RGCN_MAX_RELS),
+                ("total_bytes", ctypes.c_size_t)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load librgcn.so; raises if it has not been built (there is no fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with "
+                               "`python -m paper_2406_06022_amd.build`")
+        lib = ctypes.CDLL(path)
+        vp, st = ctypes.c_void_p, ctypes.c_int
+        lib.rgcn_block_workspace_size.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_size_t)]
+        lib.rgcn_block_workspace_size.restype = st
+        lib.rgcn_block_plan_layout.argtypes = [vp, vp, vp]
+        lib.rgcn_block_plan_layout.restype = st
+        lib.rgcn_block_plan.argtypes = [vp, vp, vp, ctypes.c_size_t, ctypes.c_uint, vp]
+        lib.rgcn_block_plan.restype = st
+        lib.rgcn_block_forward.argtypes = [vp, vp, vp, vp, vp, ctypes.c_size_t, ctypes.c_uint, vp]
+        lib.rgcn_block_forward.restype = st
+        lib.rgcn_block_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                            ctypes.c_size_t, ctypes.c_uint, vp]
+        lib.rgcn_block_backward.restype = st
+        lib.rgcn_block_aggregate.argtypes = [vp, vp, vp, vp, ctypes.c_size_t, ctypes.c_uint, vp]
+        lib.rgcn_block_aggregate.restype = st
+        lib.rgcn_block_transform.argtypes = [vp, vp, vp, vp, ctypes.c_size_t, ctypes.c_uint, vp]
+        lib.rgcn_block_transform.restype = st
+        lib.rgcn_block_backward_dense.argtypes = [vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t,
+                                                  ctypes.c_uint, vp]
+        lib.rgcn_block_backward_dense.restype = st
+        lib.rgcn_block_backward_sparse.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_size_t,
+                                                   ctypes.c_uint, vp]
+        lib.rgcn_block_backward_sparse.restype = st
+        lib.rgcn_last_error.restype = ctypes.c_char_p
+        lib.rgcn_version.restype = ctypes.c_char_p
+        _lib = lib
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        raise RgcnError(status, load_library().rgcn_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _ptr_array(ptrs: Sequence[Optional[int]]):
+    arr = (ctypes.c_void_p * max(len(ptrs), 1))()
+    for i, p in enumerate(ptrs):
+        arr[i] = p
+    return arr
+
+
+# ------------------------------------------------------------------------------------
+class DeviceBlock:
+    """A block's structure in device memory plus its C mirror.
+
+    ``blk`` is anything with ``n_src``, ``n_dst`` and ``rels`` (each relation with
+    ``src_type``, ``dst_type``, ``indptr`` and ``indices``); arrays are copied to
+    ``device`` as int32."""
+
+    def __init__(self, blk, grad_src_types: int = 0, device="cuda"):
+        self.n_src = [int(x) for x in blk.n_src]
+        self.n_dst = [int(x) for x in blk.n_dst]
+        self.num_types = len(self.n_src)
+        self.grad_src_types = int(grad_src_types)
+        self.indptr: List[torch.Tensor] = []
+        self.indices: List[torch.Tensor] = []
+        self.types = []
+        for rel in blk.rels:
+            ip = torch.as_tensor(np.ascontiguousarray(rel.indptr, dtype=np.int32)).to(device)
+            ix = torch.as_tensor(np.ascontiguousarray(rel.indices, dtype=np.int32))
+            ix = (ix if ix.numel() else torch.zeros(1, dtype=torch.int32)).to(device)
+            self.indptr.append(ip)
+            self.indices.append(ix)
+            self.types.append((int(rel.src_type), int(rel.dst_type), int(len(rel.indices))))
+        self.num_rels = len(self.types)
+        self._n_src = (ctypes.c_int64 * self.num_types)(*self.n_src)
+        self._n_dst = (ctypes.c_int64 * self.num_types)(*self.n_dst)
+        self._rels = (_Relation * max(self.num_rels, 1))()
+        for r, (s, t, nnz) in enumerate(self.types):
+            self._rels[r] = _Relation(s, t, nnz, self.indptr[r].data_ptr(),
+                                      self.indices[r].data_ptr())
+        self.c = _Block(self.num_types, self.num_rels, self._n_src, self._n_dst, self._rels,
+                        self.grad_src_types)
+
+    @property
+    def nnz(self) -> int:
+        return sum(x[2] for x in self.types)
+
+
+class Params:
+    """Weights of one block (device tensors in the block dtype)."""
+
+    def __init__(self, dtype: str, d_in: int, d_out: int, w_rel, w_self, bias=None):
+        self.dtype = dtype
+        self.d_in, self.d_out = int(d_in), int(d_out)
+        self.w_rel, self.w_self = list(w_rel), list(w_self)
+        self.bias = list(bias) if bias is not None else None
+        self._w_rel = _ptr_array([_ptr(w) for w in self.w_rel])
+        self._w_self = _ptr_array([_ptr(w) for w in self.w_self])
+        self._bias = _ptr_array([_ptr(b) for b in self.bias]) if self.bias is not None else None
+        self.c = _Params(RGCN_BF16 if dtype == "bf16" else RGCN_F32, self.d_in, self.d_out,
+                         self._w_rel, self._w_self, self._bias)
+
+
+class Inputs:
+    """Per-type input rows: (base table, optional int64 row ids) with base [rows x ld]."""
+
+    def __init__(self, bases: Sequence[Optional[torch.Tensor]],
+                 row_ids: Optional[Sequence[Optional[torch.Tensor]]] = None):
+        self.bases = list(bases)
+        self.row_ids = list(row_ids) if row_ids is not None else [None] * len(self.bases)
+        self.c = (_Input * max(len(self.bases), 1))()
+        for t, (b, ids) in enumerate(zip(self.bases, self.row_ids)):
+            if b is None:
+                self.c[t] = _Input(None, None, 0, 0)
+            else:
+                self.c[t] = _Input(b.data_ptr(), _ptr(ids), int(b.shape[0]), int(b.stride(0)))
+
+
+# ------------------------------------------------------------------------------------
+def rgcn_version() -> str:
+    return load_library().rgcn_version().decode()
+
+
+def rgcn_last_error() -> str:
+    return load_library().rgcn_last_error().decode()
+
+
+def rgcn_block_workspace_size(block: DeviceBlock, params: Params) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load_library().rgcn_block_workspace_size(ctypes.byref(block.c), ctypes.byref(params.c),
+                                                    ctypes.byref(out)))
+    return int(out.value)
+
+
+def rgcn_block_plan_layout(block: DeviceBlock, params: Params) -> dict:
+    lay = _PlanLayout()
+    _check(load_library().rgcn_block_plan_layout(ctypes.byref(block.c), ctypes.byref(params.c),
+                                                 ctypes.byref(lay)))
+    none = (1 << (8 * ctypes.sizeof(ctypes.c_size_t))) - 1
+    return {"n_fwd_segments": lay.n_fwd_segments, "fwd_order": lay.fwd_order,
+            "n_bwd_rows": lay.n_bwd_rows, "bwd_order": lay.bwd_order,
+            "csc_indptr": [None if x == none else x for x in lay.csc_indptr],
+            "csc_dst": [None if x == none else x for x in lay.csc_dst],
+            "total_bytes": lay.total_bytes}
+
+
+def new_workspace(block: DeviceBlock, params: Params, device="cuda") -> torch.Tensor:
+    return torch.empty(rgcn_block_workspace_size(block, params), dtype=torch.uint8, device=device)
+
+
+def rgcn_block_plan(block: DeviceBlock, params: Params, workspace: torch.Tensor, flags: int = 0,
+                    stream=None) -> None:
+    _check(load_library().rgcn_block_plan(ctypes.byref(block.c), ctypes.byref(params.c),
+                                          workspace.data_ptr(), workspace.numel(), flags,
+                                          _stream(stream)))
+
+
+def rgcn_block_forward(block: DeviceBlock, inputs: Inputs, params: Params,
+                       y: Sequence[Optional[torch.Tensor]], workspace: torch.Tensor,
+                       flags: int = 0, stream=None) -> None:
+    ys = _ptr_array([_ptr(t) for t in y])
+    _check(load_library().rgcn_block_forward(ctypes.byref(block.c), inputs.c,
+                                             ctypes.byref(params.c), ys, workspace.data_ptr(),
+                                             workspace.numel(), flags, _stream(stream)))
+
+
+def rgcn_block_backward(block: DeviceBlock, inputs: Inputs, params: Params,
+                        dy: Sequence[Optional[torch.Tensor]],
+                        dw_rel: Optional[Sequence[Optional[torch.Tensor]]] = None,
+                        dw_self: Optional[Sequence[Optional[torch.Tensor]]] = None,
+                        dbias: Optional[Sequence[Optional[torch.Tensor]]] = None,
+                        dh_src: Optional[Sequence[Optional[torch.Tensor]]] = None,
+                        demb: Optional[Sequence[Optional[torch.Tensor]]] = None,
+                        workspace: torch.Tensor = None, flags: int = 0, stream=None) -> None:
+    def arr(xs):
+        return None if xs is None else _ptr_array([_ptr(t) for t in xs])
+
+    keep = [arr(dy), arr(dw_rel), arr(dw_self), arr(dbias), arr(dh_src), arr(demb)]
+    _check(load_library().rgcn_block_backward(
+        ctypes.byref(block.c), inputs.c, ctypes.byref(params.c), *keep,
+        workspace.data_ptr(), workspace.numel(), flags, _stream(stream)))
+
+
+def rgcn_block_aggregate(block: DeviceBlock, inputs: Inputs, params: Params,
+                         workspace: torch.Tensor, flags: int = 0, stream=None) -> None:
+    _check(load_library().rgcn_block_aggregate(ctypes.byref(block.c), inputs.c,
+                                               ctypes.byref(params.c), workspace.data_ptr(),
+                                               workspace.numel(), flags, _stream(stream)))
+
+
+def rgcn_block_transform(block: DeviceBlock, params: Params, y: Sequence[Optional[torch.Tensor]],
+                         workspace: torch.Tensor, flags: int = 0, stream=None) -> None:
+    ys = _ptr_array([_ptr(t) for t in y])
+    _check(load_library().rgcn_block_transform(ctypes.byref(block.c), ctypes.byref(params.c), ys,
+                                               workspace.data_ptr(), workspace.numel(), flags,
+                                               _stream(stream)))
+
+
+def rgcn_block_backward_dense(block: DeviceBlock, params: Params,
+                              dy: Sequence[Optional[torch.Tensor]], dw_rel=None, dw_self=None,
+                              dbias=None, workspace: torch.Tensor = None, flags: int = 0,
+                              stream=None) -> None:
+    def arr(xs):
+        return None if xs is None else _ptr_array([_ptr(t) for t in xs])
+
+    keep = [arr(dy), arr(dw_rel), arr(dw_self), arr(dbias)]
+    _check(load_library().rgcn_block_backward_dense(
+        ctypes.byref(block.c), ctypes.byref(params.c), *keep, workspace.data_ptr(),
+        workspace.numel(), flags, _stream(stream)))
+
+
+def rgcn_block_backward_sparse(block: DeviceBlock, inputs: Inputs, params: Params, dh_src=None,
+                               demb=None, workspace: torch.Tensor = None, flags: int = 0,
+                               stream=None) -> None:
+    def arr(xs):
+        return None if xs is None else _ptr_array([_ptr(t) for t in xs])
+
+    keep = [arr(dh_src), arr(demb)]
+    _check(load_library().rgcn_block_backward_sparse(
+        ctypes.byref(block.c), inputs.c, ctypes.byref(params.c), *keep, workspace.data_ptr(),
+        workspace.numel(), flags, _stream(stream)))

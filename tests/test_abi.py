@@ -1,0 +1,113 @@
+"""The C ABI library loads, exports every function include/rgcn.h declares, and rejects
+invalid arguments on the host before touching the GPU (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2406_06022_amd import rgcn
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(rgcn.LIB_PATH):
+        from paper_2406_06022_amd import build
+        build.build()
+    return rgcn.load_library()
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "rgcn.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rgcn_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert set(names) == set(rgcn.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert "gfx950" in rgcn.rgcn_version()
+
+
+class _FakeBlock:
+    """A structurally valid block whose device pointers are fake: only host validation may
+    run on it."""
+
+    def __init__(self, n_src, n_dst, rels, grad=0):
+        self.n_src_a = (ctypes.c_int64 * len(n_src))(*n_src)
+        self.n_dst_a = (ctypes.c_int64 * len(n_dst))(*n_dst)
+        self.rels_a = (rgcn._Relation * max(len(rels), 1))()
+        for i, (s, t, nnz) in enumerate(rels):
+            self.rels_a[i] = rgcn._Relation(s, t, nnz, 0x10000, 0x20000)
+        self.c = rgcn._Block(len(n_src), len(rels), self.n_src_a, self.n_dst_a, self.rels_a, grad)
+
+
+def _params(d_in=8, d_out=8, dtype=rgcn.RGCN_F32, nrel=1, ntypes=1):
+    w_rel = (ctypes.c_void_p * max(nrel, 1))(*([0x40000] * nrel))
+    w_self = (ctypes.c_void_p * ntypes)(*([0x40000] * ntypes))
+    p = rgcn._Params(dtype, d_in, d_out, w_rel, w_self, None)
+    p._keep = (w_rel, w_self)
+    return p
+
+
+def _ws_size(lib, blk, p):
+    out = ctypes.c_size_t(0)
+    st = lib.rgcn_block_workspace_size(ctypes.byref(blk.c), ctypes.byref(p), ctypes.byref(out))
+    return st, out.value
+
+
+def test_workspace_size_and_host_validation(lib):
+    good = _FakeBlock([20], [10], [(0, 0, 30)])
+    st, n = _ws_size(lib, good, _params())
+    assert st == 0 and n > 0
+    cases = [
+        (_FakeBlock([20], [10], [(0, 0, 30)], grad=0b10), _params(), 1),   # grad bit past types
+        (_FakeBlock([5], [10], [(0, 0, 30)]), _params(), 2),               # n_dst > n_src
+        (_FakeBlock([20], [10], [(0, 3, 30)]), _params(), 1),              # bad dst type
+        (_FakeBlock([20], [10], [(0, 0, -1)]), _params(), 7),              # negative nnz
+        (good, _params(dtype=5), 3),                                       # dtype
+        (good, _params(d_in=6), 7),                                        # d_in not multiple of 4
+        (good, _params(d_in=8, d_out=12, dtype=rgcn.RGCN_BF16), 7),        # bf16 needs 8
+        (good, _params(d_in=0), 1),
+    ]
+    for blk, p, want in cases:
+        st, _ = _ws_size(lib, blk, p)
+        assert st == want, (st, want, lib.rgcn_last_error())
+        assert lib.rgcn_last_error()
+
+
+def test_null_and_small_workspace_rejected(lib):
+    blk = _FakeBlock([20], [10], [(0, 0, 30)])
+    p = _params()
+    st = lib.rgcn_block_plan(ctypes.byref(blk.c), ctypes.byref(p), None, 0, 0, None)
+    assert st == 1
+    st = lib.rgcn_block_plan(ctypes.byref(blk.c), ctypes.byref(p), 0x100000, 16, 0, None)
+    assert st == 6
+    st = lib.rgcn_block_plan(ctypes.byref(blk.c), ctypes.byref(p), 0x100008, 1 << 40, 0, None)
+    assert st == 1  # misaligned
+    _, n = _ws_size(lib, blk, p)
+    # forward: NULL inputs, then NULL outputs
+    st = lib.rgcn_block_forward(ctypes.byref(blk.c), None, ctypes.byref(p), None, 0x100000, n,
+                                0, None)
+    assert st == 1
+    inp = (rgcn._Input * 1)(rgcn._Input(0x40000, None, 20, 8))
+    st = lib.rgcn_block_forward(ctypes.byref(blk.c), inp, ctypes.byref(p), None, 0x100000, n, 0,
+                                None)
+    assert st == 1
+    bad_ld = (rgcn._Input * 1)(rgcn._Input(0x40000, None, 20, 6))
+    y = (ctypes.c_void_p * 1)(0x80000)
+    st = lib.rgcn_block_forward(ctypes.byref(blk.c), bad_ld, ctypes.byref(p), y, 0x100000, n, 0,
+                                None)
+    assert st == 2
+    # backward: a gradient of a type that is not in grad_src_types
+    dy = (ctypes.c_void_p * 1)(0x80000)
+    dh = (ctypes.c_void_p * 1)(0x90000)
+    st = lib.rgcn_block_backward(ctypes.byref(blk.c), inp, ctypes.byref(p), dy, None, None, None,
+                                 dh, None, 0x100000, n, 0, None)
+    assert st == 1
+    assert "grad_src_types" in lib.rgcn_last_error().decode()

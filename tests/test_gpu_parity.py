@@ -1,0 +1,231 @@
+"""HIP path vs the CPU oracle, through the C ABI, on seeded inputs.
+
+Random small blocks (ragged degrees, zero-degree rows, empty relations, repeated edges,
+types without destination rows, several dims), the five workload configurations at a
+size the oracle evaluates in seconds (every block of every mini-batch), the integer plan
+bit for bit, an integer index probe, determinism, and the device-side validation errors.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from harness import BlockRun, TOL, rel_err, to64
+from paper_2406_06022_amd import rgcn, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _random_blocks():
+    rng = np.random.default_rng(1234)
+    yield "one-type-dup", synth.random_block(rng, [300], [170], [(0, 0), (0, 0)], 9)
+    yield "three-types", synth.random_block(rng, [400, 260, 333], [130, 257, 0],
+                                            [(0, 1), (1, 0), (2, 0), (2, 1), (0, 0), (1, 1)], 12)
+    yield "zero-heavy", synth.random_block(rng, [500, 90], [200, 77], [(0, 0), (1, 0), (0, 1)], 40,
+                                           zero_frac=0.7)
+    yield "empty-rel", synth.random_block(rng, [64, 50], [40, 33], [(0, 1), (1, 0)], 0)
+    yield "wide-deg", synth.random_block(rng, [2000], [129], [(0, 0)], 300)
+
+
+@pytest.mark.parametrize("dtype,d_in,d_out", [("f32", 32, 64), ("f32", 12, 20), ("bf16", 128, 256),
+                                              ("bf16", 24, 40), ("bf16", 512, 128),
+                                              ("f32", 256, 64)])
+@pytest.mark.parametrize("name,blk", list(_random_blocks()))
+def test_random_block_parity(name, blk, dtype, d_in, d_out):
+    run = BlockRun(blk, dtype, d_in, d_out, seed=hash((name, d_in)) % 1000, bias=True,
+                   use_ids=True)
+    print(f"case {name} {dtype} {d_in}->{d_out}", flush=True)
+    run.run_gpu()
+    run.run_oracle()
+    run.assert_parity()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_relu_flags_and_embedding_scatter(dtype):
+    rng = np.random.default_rng(77)
+    blk = synth.random_block(rng, [700, 300], [250, 100], [(0, 1), (1, 0), (0, 0)], 14)
+    d = 32 if dtype == "f32" else 64
+    for unique in (True, False):
+        run = BlockRun(blk, dtype, d, d, seed=5, use_ids=True, input_relu=True, fwd_relu=True,
+                       emb_types=(0,), grad_types=(0, 1), ids_unique=unique, dup_ids=not unique)
+        run.run_gpu()
+        run.run_oracle()
+        run.assert_parity()
+
+
+@pytest.mark.parametrize("index", range(5))
+def test_small_config_blocks_parity(index):
+    spec = synth.small_config(index)
+    mb = synth.sample_minibatch(spec)
+    for l, blk in enumerate(mb.blocks):
+        d_in, d_out = spec.dims[l], spec.dims[l + 1]
+        emb = [t for t in range(len(spec.ntype_names)) if spec.featureless[t]] if l == 0 else []
+        grad = list(range(len(spec.ntype_names))) if l > 0 else []
+        print(f"config {spec.name} block {l} nnz {blk.nnz} {d_in}->{d_out}", flush=True)
+        run = BlockRun(blk, spec.dtype, d_in, d_out, seed=100 + 10 * index + l,
+                       use_ids=(l == 0), input_relu=(l > 0), emb_types=emb, grad_types=grad)
+        run.run_gpu()
+        run.run_oracle()
+        errs = run.assert_parity()
+        print({k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+
+
+def _plan_arrays(run):
+    lay = rgcn.rgcn_block_plan_layout(run.dblk, run.params)
+    ws = run.ws.cpu().numpy()
+
+    def arr(off, n):
+        return np.frombuffer(ws[off:off + 4 * n].tobytes(), dtype=np.int32)
+
+    fwd = arr(lay["fwd_order"], lay["n_fwd_segments"])
+    bwd = arr(lay["bwd_order"], lay["n_bwd_rows"])
+    csc = {}
+    for r, rel in enumerate(run.blk.rels):
+        if lay["csc_indptr"][r] is not None:
+            ns = run.blk.n_src[rel.src_type]
+            csc[r] = (arr(lay["csc_indptr"][r], ns + 1), arr(lay["csc_dst"][r], len(rel.indices)))
+    return fwd, bwd, csc
+
+
+@pytest.mark.parametrize("index", [1, 2, 3, 4])
+def test_plan_is_bit_exact(index):
+    spec = synth.small_config(index)
+    mb = synth.sample_minibatch(spec)
+    for blk in mb.blocks:
+        T = len(blk.n_src)
+        run = BlockRun(blk, spec.dtype, 8 if spec.dtype == "bf16" else 4, 8, seed=1,
+                       grad_types=[t for t in range(T) if blk.n_src[t] > 0])
+        run.run_gpu()
+        fwd, bwd, csc = _plan_arrays(run)
+        assert np.array_equal(fwd, oracle.forward_schedule(blk))
+        assert np.array_equal(bwd, oracle.backward_schedule(blk, run.grad_types))
+        for r, (cip, cdst) in csc.items():
+            rel = blk.rels[r]
+            want_ip, want_dst, _ = oracle.csc(blk.n_src[rel.src_type], rel.indptr, rel.indices)
+            assert np.array_equal(cip, want_ip), r
+            assert np.array_equal(cdst, want_dst), r
+
+
+def test_plan_skewed_sources_bit_exact():
+    """Power-law source popularity: long transpose segments (hub sources)."""
+    spec = synth.WorkloadSpec("skewed", "bf16", ("A", "B"), (300000, 5000), (False, False),
+                              ((0, 1), (1, 0), (0, 0)), (1,), 3000, (25,), "zipf", (8, 8),
+                              synth.BASE_SEED + 50, skew=0.9)
+    mb = synth.sample_minibatch(spec)
+    blk = mb.blocks[0]
+    run = BlockRun(blk, "bf16", 8, 8, seed=3, grad_types=[0, 1])
+    run.run_gpu()
+    fwd, bwd, csc = _plan_arrays(run)
+    assert np.array_equal(fwd, oracle.forward_schedule(blk))
+    assert np.array_equal(bwd, oracle.backward_schedule(blk, [0, 1]))
+    longest = 0
+    for r, (cip, cdst) in csc.items():
+        rel = blk.rels[r]
+        want_ip, want_dst, _ = oracle.csc(blk.n_src[rel.src_type], rel.indptr, rel.indices)
+        longest = max(longest, int(np.diff(want_ip).max(initial=0)))
+        assert np.array_equal(cip, want_ip) and np.array_equal(cdst, want_dst)
+    assert longest > 20  # hub sources exist
+
+
+def test_index_probe_is_exact():
+    """fp32 integer features encoding the global id bytes; W_self = 0 and W_r = I, so every
+    output is a gathered-row sum divided by the degree; times the degree it must equal the
+    oracle's integer sums exactly (any wrong row would show)."""
+    rng = np.random.default_rng(99)
+    blk = synth.random_block(rng, [5000], [1500], [(0, 0)], 25)
+    rows = 1 << 16
+    ids = torch.randperm(rows)[:5000].to(torch.int64)
+    allid = torch.arange(rows, dtype=torch.int64)
+    cols = [((allid >> (8 * c)) & 0xFF) + 1 for c in range(2)] + [torch.ones(rows, dtype=torch.int64)] * 2
+    table = torch.stack(cols, dim=1).to(torch.float32)
+    d = 4
+    dev = "cuda"
+    dblk = rgcn.DeviceBlock(blk, 0, dev)
+    eye = torch.eye(d, dtype=torch.float32, device=dev)
+    zero = torch.zeros((d, d), dtype=torch.float32, device=dev)
+    params = rgcn.Params("f32", d, d, [eye], [zero])
+    inputs = rgcn.Inputs([table.to(dev)], [ids.to(dev)])
+    ws = rgcn.new_workspace(dblk, params)
+    y = torch.empty((1500, d), dtype=torch.float32, device=dev)
+    rgcn.rgcn_block_plan(dblk, params, ws)
+    rgcn.rgcn_block_forward(dblk, inputs, params, [y], ws)
+    torch.cuda.synchronize()
+    deg = oracle.degrees(blk.rels[0].indptr)
+    got = np.rint(to64(y.cpu()) * np.maximum(deg, 1)[:, None])
+    h = table[ids].to(torch.float64).numpy()
+    m = oracle.mean_aggregate(blk.rels[0].indptr, blk.rels[0].indices, h)
+    want = np.rint(m * np.maximum(deg, 1)[:, None])
+    assert np.array_equal(got, want)
+
+
+def test_deterministic_bitwise():
+    spec = synth.small_config(2)
+    blk = synth.sample_minibatch(spec).blocks[0]
+    run = BlockRun(blk, "bf16", 128, 256, seed=8, use_ids=True, emb_types=(0,), grad_types=())
+    a, b = run.run_gpu(repeat=2)
+    for key in ("y", "dw_rel", "dw_self", "demb"):
+        for x, z in zip(a[key], b[key]):
+            if x is not None:
+                assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x,
+                                   z.view(torch.int16) if z.dtype == torch.bfloat16 else z), key
+
+
+def test_degenerate_blocks():
+    # no destination rows at all; no edges at all; one row one edge
+    cases = [
+        synth.Block([10, 5], [0, 0], [synth.Relation(0, 1, np.zeros(1, np.int32),
+                                                     np.zeros(0, np.int32))]),
+        synth.Block([10, 5], [4, 5], [synth.Relation(0, 1, np.zeros(6, np.int32),
+                                                     np.zeros(0, np.int32)),
+                                      synth.Relation(1, 0, np.zeros(5, np.int32),
+                                                     np.zeros(0, np.int32))]),
+        synth.Block([1], [1], [synth.Relation(0, 0, np.array([0, 1], np.int32),
+                                              np.array([0], np.int32))]),
+    ]
+    for blk in cases:
+        for dtype, d in (("f32", 8), ("bf16", 16)):
+            run = BlockRun(blk, dtype, d, d, seed=2, bias=True)
+            run.run_gpu()
+            run.run_oracle()
+            run.assert_parity()
+
+
+def test_device_validation_reports_errors():
+    blk = synth.Block([20], [10], [synth.Relation(0, 0, np.arange(11, dtype=np.int32),
+                                                  np.arange(10, dtype=np.int32))])
+    run = BlockRun(blk, "f32", 8, 8, seed=4)
+    run.run_gpu(validate=True)  # valid block passes validation
+    bad_idx = synth.Block([20], [10], [synth.Relation(0, 0, np.arange(11, dtype=np.int32),
+                                                      np.array([0] * 9 + [20], np.int32))])
+    run = BlockRun(bad_idx, "f32", 8, 8, seed=4)
+    with pytest.raises(rgcn.RgcnError) as e:
+        run.run_gpu(validate=True)
+    assert e.value.status == 4
+    ip = np.arange(11, dtype=np.int32)
+    ip[5] = 2  # not monotone
+    bad_csr = synth.Block([20], [10], [synth.Relation(0, 0, ip, np.arange(10, dtype=np.int32))])
+    run = BlockRun(bad_csr, "f32", 8, 8, seed=4)
+    with pytest.raises(rgcn.RgcnError) as e:
+        run.run_gpu(validate=True)
+    assert e.value.status == 5
+    # out-of-range row id of the input table
+    run = BlockRun(blk, "f32", 8, 8, seed=4, use_ids=True)
+    run.ids[0][3] = run.tables[0].shape[0]
+    with pytest.raises(rgcn.RgcnError) as e:
+        run.run_gpu(validate=True)
+    assert e.value.status == 4
+
+
+def test_workspace_too_small_and_bad_dims():
+    blk = synth.Block([20], [10], [synth.Relation(0, 0, np.arange(11, dtype=np.int32),
+                                                  np.arange(10, dtype=np.int32))])
+    dblk = rgcn.DeviceBlock(blk, 0)
+    w = torch.zeros((8, 8), device="cuda")
+    params = rgcn.Params("f32", 8, 8, [w], [w])
+    ws = torch.empty(64, dtype=torch.uint8, device="cuda")
+    with pytest.raises(rgcn.RgcnError) as e:
+        rgcn.rgcn_block_plan(dblk, params, ws)
+    assert e.value.status == 6
+    with pytest.raises(rgcn.RgcnError) as e:
+        rgcn.rgcn_block_workspace_size(dblk, rgcn.Params("f32", 6, 8, [w], [w]))
+    assert e.value.status == 7

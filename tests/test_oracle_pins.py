@@ -394,3 +394,29 @@ def test_relu_epilogue_exact_small_values(orc):
     w_self = [vals.reshape(1, d)]
     y = orc.block_forward(blk, h, [], w_self, None, relu=True)[0]
     assert y.ravel().tolist() == [0.0, 0.0, 2.0 ** -12, 1.0, 0.0, 0.0]
+
+
+def test_sub_block_preserves_kept_rows(orc):
+    """Outputs of kept rows, and input gradients of sources referenced only by kept rows,
+    equal those of the whole block."""
+    rng = np.random.default_rng(51)
+    blk = synth.random_block(rng, [60, 45], [30, 20], [(0, 1), (1, 0), (0, 0)], 5)
+    h, w_rel, w_self, b, dy = _rand_inputs(rng, blk, 3, 4)
+    keep = [np.array([2, 5, 11, 29]), np.array([0, 7])]
+    sub, src_map = orc.sub_block(blk, keep)
+    y = orc.block_forward(blk, h, w_rel, w_self, b)
+    ys = orc.block_forward(sub, [h[t][src_map[t]] for t in range(2)], w_rel, w_self, b)
+    for t in range(2):
+        np.testing.assert_allclose(ys[t], y[t][keep[t]], rtol=1e-13, atol=1e-13)
+    # gradient: zero dY outside the kept rows on the full block
+    dy_full = [np.zeros_like(x) for x in dy]
+    for t in range(2):
+        dy_full[t][keep[t]] = dy[t][keep[t]]
+    g = orc.block_backward(blk, h, w_rel, w_self, dy_full)
+    gs = orc.block_backward(sub, [h[t][src_map[t]] for t in range(2)], w_rel, w_self,
+                            [dy[t][keep[t]] for t in range(2)])
+    for t in range(2):
+        np.testing.assert_allclose(gs["dh_src"][t], g["dh_src"][t][src_map[t]], rtol=1e-12,
+                                   atol=1e-12)
+    for r in range(3):
+        np.testing.assert_allclose(gs["dw_rel"][r], g["dw_rel"][r], rtol=1e-12, atol=1e-12)
