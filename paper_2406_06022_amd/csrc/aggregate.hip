@@ -41,107 +41,138 @@ __device__ __forceinline__ void acc_chunk(float *acc, const uint4 &v) {
     }
 }
 
-struct GatherIO {
+// Broadcast a 64-bit value from absolute lane `src` of the wave.
+__device__ __forceinline__ int64_t shfl64(int64_t v, int src) {
+    const int lo = __shfl((int)(uint32_t)v, src, 64);
+    const int hi = __shfl((int)(uint32_t)((uint64_t)v >> 32), src, 64);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// Forward segments in schedule order (heaviest first), one group of G lanes per segment,
+// persistent: group q handles segments q, q + ngroups, ...  A segment is the self-loop
+// row of a destination (copied) or the sampled in-edges of a destination row in one
+// relation (mean of the gathered source rows; 0 if none).  Lane lg of the group fetches
+// edge lg's source index and global row id, the group walks the edges broadcasting row
+// addresses, U row loads in flight.  Software pipeline, two round trips per segment:
+//   {row ids of this segment, descriptor of the next}  then
+//   {rows of this segment, source indices of the next}.
+// The sum runs in ascending edge position; one division by the degree.
+struct GatherTabs {
     TypeInput in[kMaxTypes];
-    void *mcat[kMaxTypes];
-    int64_t mcat_ld[kMaxTypes];   // elements per Mcat row
 };
 
-// One group per forward segment, in schedule order (heaviest segments first).  A
-// segment is the self-loop row of a destination (copied) or the sampled in-edges of a
-// destination row in one relation (mean of the gathered source rows; 0 if none).  The
-// sum runs in ascending edge position; the result is divided once by the degree.
 template <bool BF16, int CPL>
-__global__ __launch_bounds__(kThreads) void k_gather_mean(const int32_t *__restrict__ order,
+__global__ __launch_bounds__(kThreads) void k_gather_mean(const SegDesc *__restrict__ desc,
                                                           int64_t n_seg,
                                                           const FwdSlot *__restrict__ slots,
-                                                          int nslots, GatherIO io, int G,
-                                                          int gpw, int chunks) {
+                                                          int nslots, GatherTabs tabs,
+                                                          char *__restrict__ ws, int G, int gpw,
+                                                          int chunks) {
     constexpr int VEC = BF16 ? 8 : 4;
     constexpr int ES = BF16 ? 2 : 4;
-    constexpr int U = 4;  // independent row loads in flight per lane
-    __shared__ int64_t s_base[kMaxSlots];
-    for (int i = threadIdx.x; i < nslots; i += kThreads) s_base[i] = slots[i].seg_base;
+    constexpr int U = CPL == 1 ? 8 : 4;  // row loads in flight per lane
+    __shared__ const int32_t *s_idx[kMaxSlots];
+    __shared__ int32_t s_src[kMaxSlots];
+    for (int i = threadIdx.x; i < nslots; i += kThreads) {
+        s_idx[i] = slots[i].indices;
+        s_src[i] = slots[i].src_type;
+    }
     __syncthreads();
 
     const int lane = threadIdx.x & 63;
     const int gi = lane / G;
     const int lg = lane - gi * G;
+    const int g0 = gi * G;
     if (gi >= gpw) return;
-    const int64_t wave = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
-    const int64_t g = wave * gpw + gi;
-    if (g >= n_seg) return;
+    const int64_t stride = (int64_t)gridDim.x * (kThreads / 64) * gpw;
+    int64_t sg = ((int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)) * gpw + gi;
+    if (sg >= n_seg) return;
 
-    const int64_t seg = order[g];
-    int lo = 0, hi = nslots - 1;
-    while (lo < hi) {
-        int mid = (lo + hi + 1) >> 1;
-        if (s_base[mid] <= seg) lo = mid; else hi = mid - 1;
-    }
-    const FwdSlot sl = slots[lo];
-    const int64_t row = seg - sl.seg_base;
-    const TypeInput in = io.in[sl.src_type];
-    const char *src = (const char *)in.base;
-    const int64_t ld_bytes = in.ld * ES;
+    // source index of edge e of segment d (self-loop slot: the row itself), -1 past the end
+    auto edge_src = [&](const SegDesc &d, int e) -> int64_t {
+        if (e >= d.deg) return -1;
+        const int32_t *ix = s_idx[(d.info >> 8) & 0xff];
+        return ix ? (int64_t)ix[d.k0 + e] : (int64_t)d.k0 + e;
+    };
+    // byte offset of that source row in its table
+    auto row_off = [&](const SegDesc &d, int64_t j) -> int64_t {
+        if (j < 0) return 0;
+        const TypeInput &in = tabs.in[s_src[(d.info >> 8) & 0xff]];
+        const int64_t grow = in.row_ids ? in.row_ids[j] : j;
+        return grow * in.ld * ES;
+    };
 
-    int64_t k0 = row, k1 = row + 1;  // self-loop slot: the row itself
-    if (sl.indptr) {
-        k0 = sl.indptr[row];
-        k1 = sl.indptr[row + 1];
-    }
-    float acc[CPL][VEC];
-#pragma unroll
-    for (int p = 0; p < CPL; ++p)
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[p][e] = 0.f;
+    SegDesc d = desc[sg];
+    int64_t j = edge_src(d, lg);
+    while (true) {
+        const int64_t off0 = row_off(d, j);
+        const int64_t sn = sg + stride;
+        SegDesc dn = d;
+        if (sn < n_seg) dn = desc[sn];
+        const char *src = (const char *)tabs.in[s_src[(d.info >> 8) & 0xff]].base;
+        const int deg = d.deg;
 
-    for (int64_t k = k0; k < k1; k += U) {
-        const char *rp[U];
+        float acc[CPL][VEC];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t kk = k + u;
-            rp[u] = nullptr;
-            if (kk < k1) {
-                const int64_t j = sl.indices ? (int64_t)sl.indices[kk] : kk;
-                const int64_t grow = in.row_ids ? in.row_ids[j] : j;
-                rp[u] = src + grow * ld_bytes;
+        for (int p = 0; p < CPL; ++p)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc[p][e] = 0.f;
+
+        int64_t jn = -1;
+        bool next_issued = false;
+        for (int kc = 0; kc < deg; kc += G) {
+            const int64_t off = kc == 0 ? off0 : row_off(d, edge_src(d, kc + lg));
+            const int n = (deg - kc) < G ? (deg - kc) : G;
+            for (int q = 0; q < n; q += U) {
+                int64_t o[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) o[u] = shfl64(off, g0 + ((q + u) < n ? q + u : 0));
+                uint4 v[U][CPL];
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int p = 0; p < CPL; ++p) {
+                        const int c = lg + p * G;
+                        v[u][p] = (q + u < n && c < chunks)
+                                      ? *(const uint4 *)(src + o[u] + (int64_t)c * 16)
+                                      : make_uint4(0, 0, 0, 0);
+                    }
+                if (!next_issued) {  // next segment's source indices, alongside these rows
+                    next_issued = true;
+                    if (sn < n_seg) jn = edge_src(dn, lg);
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int p = 0; p < CPL; ++p) acc_chunk<BF16>(acc[p], v[u][p]);
             }
         }
-        uint4 v[U][CPL];
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int p = 0; p < CPL; ++p) {
-                const int c = lg + p * G;
-                if (rp[u] && c < chunks) v[u][p] = *(const uint4 *)(rp[u] + (int64_t)c * 16);
-                else v[u][p] = make_uint4(0, 0, 0, 0);
-            }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int p = 0; p < CPL; ++p) acc_chunk<BF16>(acc[p], v[u][p]);
-    }
+        if (!next_issued && sn < n_seg) jn = edge_src(dn, lg);
 
-    const int64_t deg = k1 - k0;
-    const float fdeg = (float)deg;
-    char *out = (char *)io.mcat[sl.dst_type] +
-                (row * io.mcat_ld[sl.dst_type] + sl.col_off) * ES;
+        const float fdeg = (float)deg;
+        const uint64_t out16 = ((uint64_t)(d.info & 0xffu) << 32) | d.out_lo;
+        char *out = ws + (out16 << 4);
 #pragma unroll
-    for (int p = 0; p < CPL; ++p) {
-        const int c = lg + p * G;
-        if (c >= chunks) continue;
-        float r[VEC];
+        for (int p = 0; p < CPL; ++p) {
+            const int c = lg + p * G;
+            if (c >= chunks) continue;
+            float r[VEC];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) r[e] = deg > 0 ? acc[p][e] / fdeg : 0.f;
-        uint4 w;
-        if constexpr (BF16) {
-            w.x = pack_bf16x2(r[0], r[1]); w.y = pack_bf16x2(r[2], r[3]);
-            w.z = pack_bf16x2(r[4], r[5]); w.w = pack_bf16x2(r[6], r[7]);
-        } else {
-            w.x = __float_as_uint(r[0]); w.y = __float_as_uint(r[1]);
-            w.z = __float_as_uint(r[2]); w.w = __float_as_uint(r[3]);
+            for (int e = 0; e < VEC; ++e) r[e] = deg > 0 ? acc[p][e] / fdeg : 0.f;
+            uint4 w;
+            if constexpr (BF16) {
+                w.x = pack_bf16x2(r[0], r[1]); w.y = pack_bf16x2(r[2], r[3]);
+                w.z = pack_bf16x2(r[4], r[5]); w.w = pack_bf16x2(r[6], r[7]);
+            } else {
+                w.x = __float_as_uint(r[0]); w.y = __float_as_uint(r[1]);
+                w.z = __float_as_uint(r[2]); w.w = __float_as_uint(r[3]);
+            }
+            *(uint4 *)(out + (int64_t)c * 16) = w;
         }
-        *(uint4 *)(out + (int64_t)c * 16) = w;
+        if (sn >= n_seg) break;
+        sg = sn;
+        d = dn;
+        j = jn;
     }
 }
 
@@ -150,81 +181,124 @@ __global__ __launch_bounds__(kThreads) void k_gather_mean(const int32_t *__restr
 //         transpose segment of j (ascending destination row), of dMs_r[i]
 // where dMs rows already carry the 1/deg factor.  Then the optional ReLU-input mask,
 // the dh_src store and the embedding scatter-add demb[row_ids[j]] += acc.
+// Lanes first fetch the transpose offsets of up to G relations at once, then the
+// destination rows of up to G edges at once (flattened relation by relation), then walk
+// the edges broadcasting row addresses, U row loads in flight; the embedding-gradient
+// row and the ReLU mask input are requested before the walk.
 template <bool BF16IN, int CPL>
 __global__ __launch_bounds__(kThreads) void k_transpose_sum(TsumArgs a, int G, int gpw,
                                                             int chunks) {
     constexpr int HES = BF16IN ? 2 : 4;  // element size of the block input (ReLU mask)
-    constexpr int U = 4;
+    constexpr int U = CPL == 1 ? 8 : 4;
     const int lane = threadIdx.x & 63;
     const int gi = lane / G;
     const int lg = lane - gi * G;
+    const int g0 = gi * G;
     if (gi >= gpw) return;
     const int64_t wave = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
     const int64_t g = wave * gpw + gi;
     if (g >= a.n_rows) return;
     const int64_t j = a.order[g];
+    const int64_t grow = a.in.row_ids ? a.in.row_ids[j] : j;
 
+    // early requests: embedding-gradient row (read-add-write), ReLU mask input, self term
+    float4 old[CPL];
+    float hm[CPL][4];
     float acc[CPL][4];
 #pragma unroll
     for (int p = 0; p < CPL; ++p) {
         const int c = lg + p * G;
-        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (a.self_dms && j < a.n_dst && c < chunks)
-            s = *(const float4 *)(a.self_dms + j * a.self_ld + (int64_t)c * 4);
-        acc[p][0] = s.x; acc[p][1] = s.y; acc[p][2] = s.z; acc[p][3] = s.w;
+        const bool okc = c < chunks;
+        old[p] = (a.demb && a.ids_unique && okc)
+                     ? *(const float4 *)(a.demb + grow * a.d_in + (int64_t)c * 4)
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+        if (a.input_relu && okc) {
+            const char *hp = (const char *)a.in.base + (grow * a.in.ld + (int64_t)c * 4) * HES;
+            if constexpr (BF16IN) {
+                const uint2 hv = *(const uint2 *)hp;
+                hm[p][0] = bf16_lo(hv.x); hm[p][1] = bf16_hi(hv.x);
+                hm[p][2] = bf16_lo(hv.y); hm[p][3] = bf16_hi(hv.y);
+            } else {
+                const float4 hv = *(const float4 *)hp;
+                hm[p][0] = hv.x; hm[p][1] = hv.y; hm[p][2] = hv.z; hm[p][3] = hv.w;
+            }
+        } else {
+            hm[p][0] = hm[p][1] = hm[p][2] = hm[p][3] = 1.f;
+        }
+        float4 sv = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (a.self_dms && j < a.n_dst && okc)
+            sv = *(const float4 *)(a.self_dms + j * a.self_ld + (int64_t)c * 4);
+        acc[p][0] = sv.x; acc[p][1] = sv.y; acc[p][2] = sv.z; acc[p][3] = sv.w;
     }
-    for (int r = 0; r < a.nrel; ++r) {
-        const TsumRel rel = a.rel[r];
-        const int64_t p0 = rel.csc_indptr[j], p1 = rel.csc_indptr[j + 1];
-        for (int64_t q = p0; q < p1; q += U) {
-            const float *rp[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-                rp[u] = (q + u < p1) ? rel.dms + (int64_t)rel.csc_dst[q + u] * rel.dms_ld : nullptr;
-            float4 v[U][CPL];
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-#pragma unroll
-                for (int p = 0; p < CPL; ++p) {
-                    const int c = lg + p * G;
-                    v[u][p] = (rp[u] && c < chunks) ? *(const float4 *)(rp[u] + (int64_t)c * 4)
-                                                    : make_float4(0.f, 0.f, 0.f, 0.f);
+
+    for (int r0 = 0; r0 < a.nrel; r0 += G) {
+        // lane lg: transpose segment of relation r0 + lg
+        const int nr = (a.nrel - r0) < G ? (a.nrel - r0) : G;
+        int p0 = 0, cnt = 0;
+        if (lg < nr) {
+            const int32_t *ip = a.rel[r0 + lg].csc_indptr;
+            p0 = ip[j];
+            cnt = ip[j + 1] - p0;
+        }
+        int total = 0;
+        for (int r = 0; r < nr; ++r) total += __shfl(cnt, g0 + r, 64);
+        for (int ec = 0; ec < total; ec += G) {
+            // lane lg: flattened edge ec + lg -> (relation, position) -> dMs row address.
+            // Every lane of the group runs the shuffles; only the owner loads.
+            const int e = ec + lg;
+            uint64_t addr = 0;
+            int base = 0;
+            for (int r = 0; r < nr; ++r) {
+                const int cr = __shfl(cnt, g0 + r, 64);
+                const int pr = __shfl(p0, g0 + r, 64);
+                if (e < total && e >= base && e < base + cr) {
+                    const TsumRel &rel = a.rel[r0 + r];
+                    const int64_t i = rel.csc_dst[pr + (e - base)];
+                    addr = (uint64_t)(uintptr_t)(rel.dms + i * rel.dms_ld);
                 }
+                base += cr;
+            }
+            const int n = (total - ec) < G ? (total - ec) : G;
+            for (int q = 0; q < n; q += U) {
+                int64_t o[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u)
+                for (int u = 0; u < U; ++u)
+                    o[u] = shfl64((int64_t)addr, g0 + ((q + u) < n ? q + u : 0));
+                float4 v[U][CPL];
 #pragma unroll
-                for (int p = 0; p < CPL; ++p) {
-                    acc[p][0] += v[u][p].x; acc[p][1] += v[u][p].y;
-                    acc[p][2] += v[u][p].z; acc[p][3] += v[u][p].w;
-                }
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int p = 0; p < CPL; ++p) {
+                        const int c = lg + p * G;
+                        const float *rp = (const float *)(uintptr_t)(uint64_t)o[u];
+                        v[u][p] = (q + u < n && c < chunks) ? *(const float4 *)(rp + (int64_t)c * 4)
+                                                            : make_float4(0.f, 0.f, 0.f, 0.f);
+                    }
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int p = 0; p < CPL; ++p) {
+                        acc[p][0] += v[u][p].x; acc[p][1] += v[u][p].y;
+                        acc[p][2] += v[u][p].z; acc[p][3] += v[u][p].w;
+                    }
+            }
         }
     }
-    const int64_t grow = a.in.row_ids ? a.in.row_ids[j] : j;
 #pragma unroll
     for (int p = 0; p < CPL; ++p) {
         const int c = lg + p * G;
         if (c >= chunks) continue;
         if (a.input_relu) {
-            const char *hp = (const char *)a.in.base + (grow * a.in.ld + (int64_t)c * 4) * HES;
-            float h[4];
-            if constexpr (BF16IN) {
-                const uint2 hv = *(const uint2 *)hp;
-                h[0] = bf16_lo(hv.x); h[1] = bf16_hi(hv.x); h[2] = bf16_lo(hv.y); h[3] = bf16_hi(hv.y);
-            } else {
-                const float4 hv = *(const float4 *)hp;
-                h[0] = hv.x; h[1] = hv.y; h[2] = hv.z; h[3] = hv.w;
-            }
 #pragma unroll
-            for (int e = 0; e < 4; ++e) acc[p][e] = h[e] > 0.f ? acc[p][e] : 0.f;
+            for (int e = 0; e < 4; ++e) acc[p][e] = hm[p][e] > 0.f ? acc[p][e] : 0.f;
         }
         const float4 res = make_float4(acc[p][0], acc[p][1], acc[p][2], acc[p][3]);
         if (a.dh) *(float4 *)(a.dh + j * a.d_in + (int64_t)c * 4) = res;
         if (a.demb) {
             float *dp = a.demb + grow * a.d_in + (int64_t)c * 4;
             if (a.ids_unique) {
-                float4 old = *(float4 *)dp;
-                old.x += res.x; old.y += res.y; old.z += res.z; old.w += res.w;
-                *(float4 *)dp = old;
+                *(float4 *)dp = make_float4(old[p].x + res.x, old[p].y + res.y, old[p].z + res.z,
+                                            old[p].w + res.w);
             } else {
                 unsafeAtomicAdd(dp + 0, res.x);
                 unsafeAtomicAdd(dp + 1, res.y);
@@ -313,30 +387,56 @@ __global__ __launch_bounds__(kThreads) void k_validate_ids(const int64_t *ids, i
 
 }  // namespace
 
-hipError_t gather_mean(rgcn_dtype dt, int d_in, const int32_t *order, int64_t n_seg,
+// Workgroups of `kernel` that fit on the device at once (persistent grids).
+template <class K>
+int64_t resident_wgs(K kernel) {
+    static int cus = 0;
+    if (cus == 0) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            cus = 256;
+    }
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0) != hipSuccess ||
+        per_cu <= 0)
+        per_cu = 1;
+    return (int64_t)per_cu * cus;
+}
+
+template <bool B, int C>
+hipError_t launch_gather(const SegDesc *desc, int64_t n_seg, const FwdSlot *slots_dev,
+                         int nslots, const GatherTabs &tabs, char *ws_base, const GroupShape &gs,
+                         int chunks, hipStream_t s) {
+    const int64_t groups_per_wg = (int64_t)(kThreads / 64) * gs.gpw;
+    int64_t wgs = cdiv(n_seg, groups_per_wg);
+    const int64_t cap = resident_wgs(k_gather_mean<B, C>);
+    if (wgs > cap) wgs = cap;
+    hipLaunchKernelGGL((k_gather_mean<B, C>), dim3((unsigned)wgs), dim3(kThreads), 0, s, desc,
+                       n_seg, slots_dev, nslots, tabs, ws_base, gs.G, gs.gpw, chunks);
+    return hipGetLastError();
+}
+
+hipError_t gather_mean(rgcn_dtype dt, int d_in, const SegDesc *desc, int64_t n_seg,
                        const FwdSlot *slots_dev, int nslots, const TypeInput *in,
-                       void *const *mcat, const int64_t *mcat_ld, hipStream_t s) {
+                       char *ws_base, hipStream_t s) {
     if (n_seg == 0) return hipSuccess;
     const bool bf = dt == RGCN_BF16;
     const int chunks = bf ? d_in / 8 : d_in / 4;
     const GroupShape gs = group_shape(chunks);
-    GatherIO io;
-    for (int t = 0; t < kMaxTypes; ++t) {
-        io.in[t] = in[t];
-        io.mcat[t] = mcat[t];
-        io.mcat_ld[t] = mcat_ld[t];
-    }
-    const int64_t waves = cdiv(n_seg, gs.gpw);
-    const dim3 grid((unsigned)cdiv(waves, kThreads / 64));
-#define RGCN_GM(B, C)                                                                        \
-    hipLaunchKernelGGL((k_gather_mean<B, C>), grid, dim3(kThreads), 0, s, order, n_seg,      \
-                       slots_dev, nslots, io, gs.G, gs.gpw, chunks)
-    if (gs.cpl == 1) { if (bf) RGCN_GM(true, 1); else RGCN_GM(false, 1); }
-    else if (gs.cpl == 2) { if (bf) RGCN_GM(true, 2); else RGCN_GM(false, 2); }
-    else if (gs.cpl <= 4) { if (bf) RGCN_GM(true, 4); else RGCN_GM(false, 4); }
-    else return hipErrorInvalidValue;
-#undef RGCN_GM
-    return hipGetLastError();
+    GatherTabs tabs;
+    for (int t = 0; t < kMaxTypes; ++t) tabs.in[t] = in[t];
+    if (gs.cpl == 1)
+        return bf ? launch_gather<true, 1>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s)
+                  : launch_gather<false, 1>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
+    if (gs.cpl == 2)
+        return bf ? launch_gather<true, 2>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s)
+                  : launch_gather<false, 2>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
+    if (gs.cpl <= 4)
+        return bf ? launch_gather<true, 4>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s)
+                  : launch_gather<false, 4>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
+    return hipErrorInvalidValue;
 }
 
 hipError_t transpose_sum(rgcn_dtype dt, const TsumArgs &a, hipStream_t s) {

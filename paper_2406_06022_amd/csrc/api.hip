@@ -60,7 +60,7 @@ struct Layout {
     int64_t bwd_base[kMaxTypes];
     int64_t n_bwd_rows = 0;
     // workspace offsets
-    size_t off_slots = 0, off_fwd_order = 0, off_bwd_order = 0, off_err = 0;
+    size_t off_slots = 0, off_fwd_order = 0, off_fwd_desc = 0, off_bwd_order = 0, off_err = 0;
     size_t off_csc_indptr[kMaxRels], off_csc_dst[kMaxRels];
     size_t off_mcat[kMaxTypes], off_wcat[kMaxTypes];
     size_t off_scratch = 0;
@@ -206,6 +206,7 @@ rgcn_status make_layout(const rgcn_block *b, const rgcn_params *p, Layout &L) {
     L.off_err = off;                      off += 256;
     L.off_slots = off;                    off += align256(sizeof(FwdSlot) * kMaxSlots);
     L.off_fwd_order = off;                off += align256((size_t)L.n_seg * 4 + 4);
+    L.off_fwd_desc = off;                 off += align256((size_t)L.n_seg * sizeof(SegDesc) + 16);
     L.off_bwd_order = off;                off += align256((size_t)L.n_bwd_rows * 4 + 4);
     for (int r = 0; r < kMaxRels; ++r) L.off_csc_indptr[r] = L.off_csc_dst[r] = SIZE_MAX;
     for (int r = 0; r < L.R; ++r) {
@@ -369,6 +370,16 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
                 "slot table");
     TRY_HIP(fwd_schedule(L.slots, L.nslots, L.n_seg, (int32_t *)(ws + L.off_fwd_order), scratch,
                          stream), "forward schedule");
+    {
+        int64_t moff[kMaxTypes], mld[kMaxTypes];
+        for (int t = 0; t < kMaxTypes; ++t) {
+            moff[t] = (t < L.T && L.off_mcat[t] != SIZE_MAX) ? (int64_t)L.off_mcat[t] : 0;
+            mld[t] = t < L.T ? L.K[t] : 0;
+        }
+        TRY_HIP(fwd_descriptors(L.slots, L.nslots, (const int32_t *)(ws + L.off_fwd_order), L.n_seg,
+                                moff, mld, L.es, (SegDesc *)(ws + L.off_fwd_desc), stream),
+                "forward descriptors");
+    }
     for (int r = 0; r < L.R; ++r) {
         if (L.off_csc_indptr[r] == SIZE_MAX) continue;
         const rgcn_relation &rel = block->rels[r];
@@ -402,22 +413,10 @@ rgcn_status rgcn_block_aggregate(const rgcn_block *block, const rgcn_input *in,
         if ((st = device_validate(block, in, L, ws, stream)) != RGCN_OK) return st;
     }
     TypeInput tin[kMaxTypes];
-    void *mcat[kMaxTypes];
-    int64_t mld[kMaxTypes];
-    for (int t = 0; t < kMaxTypes; ++t) {
-        tin[t] = TypeInput{nullptr, nullptr, 0};
-        mcat[t] = nullptr;
-        mld[t] = 0;
-        if (t < L.T) {
-            tin[t] = TypeInput{in[t].base, in[t].row_ids, in[t].ld};
-            if (block->n_dst[t] > 0) {
-                mcat[t] = ws + L.off_mcat[t];
-                mld[t] = L.K[t];
-            }
-        }
-    }
-    TRY_HIP(gather_mean(L.dt, L.d_in, (const int32_t *)(ws + L.off_fwd_order), L.n_seg,
-                        (const FwdSlot *)(ws + L.off_slots), L.nslots, tin, mcat, mld, stream),
+    for (int t = 0; t < kMaxTypes; ++t)
+        tin[t] = t < L.T ? TypeInput{in[t].base, in[t].row_ids, in[t].ld} : TypeInput{nullptr, nullptr, 0};
+    TRY_HIP(gather_mean(L.dt, L.d_in, (const SegDesc *)(ws + L.off_fwd_desc), L.n_seg,
+                        (const FwdSlot *)(ws + L.off_slots), L.nslots, tin, ws, stream),
             "gather mean");
     return RGCN_OK;
 }

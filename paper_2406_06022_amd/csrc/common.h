@@ -18,15 +18,18 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// fp32 -> bf16, round to nearest even (NaN stays NaN).
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
-}
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 values -> packed bf16 pair (low half = lo), round to nearest even; one
+// v_cvt_pk_bf16_f32 on gfx950.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+    f32x2_t f = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
+}
+// fp32 value rounded to bf16 and widened back to fp32.
+__device__ __forceinline__ float round_bf16(float x) {
+    return __uint_as_float(pack_bf16x2(x, 0.f) << 16);
 }
 
 // Number of set bits of `mask` below the calling lane (wave64).
@@ -63,6 +66,17 @@ struct FwdSlot {
     int32_t pad;
 };
 
+// A forward segment in schedule order, as the gather kernel reads it (16 bytes):
+//   k0, deg: first edge position and degree in the slot's CSR (self-loop: k0 = row, deg 1)
+//   out:     byte offset / 16 of the segment's output in the workspace (40 bits: out_lo
+//            and info bits 0-7); slot: info bits 8-15
+struct SegDesc {
+    int32_t k0;
+    int32_t deg;
+    uint32_t out_lo;
+    uint32_t info;
+};
+
 struct TypeInput {           // rgcn_input restated for the device
     const void *base;
     const int64_t *row_ids;
@@ -79,6 +93,11 @@ hipError_t exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, void *
 size_t bucket_sort_temp_bytes(int64_t n, int nbuckets);
 hipError_t fwd_schedule(const FwdSlot *slots_dev, int nslots, int64_t n_seg, int32_t *order,
                         void *temp, hipStream_t s);
+// Segment descriptors in schedule order; mcat_off[t]: byte offset of Mcat_t in the
+// workspace, mcat_ld[t]: its row length in elements, es: element size.
+hipError_t fwd_descriptors(const FwdSlot *slots_host, int nslots, const int32_t *order,
+                           int64_t n_seg, const int64_t *mcat_off, const int64_t *mcat_ld,
+                           int es, SegDesc *desc, hipStream_t s);
 hipError_t csc_build(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
                      int64_t n_src, int64_t nnz, int32_t *csc_indptr, int32_t *csc_dst,
                      void *temp, hipStream_t s);
@@ -92,9 +111,9 @@ hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, 
 hipError_t fill_words(void *dst, const void *src_host, size_t bytes, hipStream_t s);
 
 // aggregate.hip
-hipError_t gather_mean(rgcn_dtype dt, int d_in, const int32_t *order, int64_t n_seg,
+hipError_t gather_mean(rgcn_dtype dt, int d_in, const SegDesc *desc, int64_t n_seg,
                        const FwdSlot *slots_dev, int nslots, const TypeInput *in,
-                       void *const *mcat, const int64_t *mcat_ld, hipStream_t s);
+                       char *ws_base, hipStream_t s);
 
 struct TsumRel {
     const int32_t *csc_indptr;

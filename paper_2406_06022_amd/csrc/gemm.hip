@@ -10,43 +10,69 @@
 //
 // Workgroup tile 128 x 128, four waves in a 2 x 2 arrangement of 64 x 64, each wave a 4 x 4
 // grid of 16 x 16 MFMA tiles.  LDS holds both operands K-contiguous ("row r, k..."), one
-// row = 64 bytes of K (32 bf16 or 16 fp32) + 16 bytes of padding, so the 16 rows read by a
-// 16-lane group for an MFMA operand fall in distinct bank groups.  Double-buffered:
-// global loads of step k+1 are in flight while step k is multiplied.
+// row = BK elements of K + 16 bytes of padding; the row pitch is an odd number of
+// 16-byte units, so the 16 rows a 16-lane group reads for one MFMA operand fall in
+// distinct bank groups.  Double-buffered: global loads of step k+1 are in flight while
+// step k is multiplied.
+//
+// The weight-side product reduces over the rows of both operands, so its tiles are
+// transposed on the way to LDS: each thread loads an 8 x 8 block (8 rows x 16 bytes,
+// row-contiguous global reads), transposes it in registers and writes eight 16-byte LDS
+// rows; with BK = 64 and a 144-byte pitch these writes are bank-conflict free.
 //
 // bf16 mode: v_mfma_f32_16x16x32_bf16, fp32 accumulation.  The fp32 output gradient dY
-// enters the weight-side product rounded to bf16 (nearest-even) and the input-side
+// enters the weight-side product rounded to bf16 (nearest even) and the input-side
 // product as a hi + lo pair of bf16 values.  fp32 mode: v_mfma_f32_16x16x4_f32 (full fp32).
 #include "common.h"
+
+#ifndef RGCN_GEMM_BK_BF16
+#define RGCN_GEMM_BK_BF16 64
+#endif
 
 namespace rgcn {
 namespace {
 
 constexpr int kThreads = 256;
 constexpr int kTile = 128;
-constexpr int kPitch = 80;                        // LDS bytes per operand row
-constexpr int kTileBytes = kTile * kPitch;        // 10240
 constexpr int kStagePitch = 68;                   // epilogue staging row (floats)
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+template <int BK_, int ES_>
+struct Tile {
+    static constexpr int BK = BK_;                // K elements per step
+    static constexpr int ES = ES_;                // LDS element size
+    static constexpr int PAYLOAD = BK_ * ES_;     // bytes of K per LDS row
+    static constexpr int PITCH = PAYLOAD + 16;
+    static constexpr int CPR = PAYLOAD / 16;      // 16-byte chunks per LDS row
+    static constexpr int BYTES = kTile * PITCH;   // one operand tile
+    static_assert((PITCH / 16) % 2 == 1, "pitch must be an odd number of 16-byte units");
+};
+using TileBf16 = Tile<RGCN_GEMM_BK_BF16, 2>;
+using TileBf16T = Tile<64, 2>;                    // weight side (transposing loaders)
+using TileF32 = Tile<16, 4>;
+
 // ------------------------------------------------------------------ MFMA cores
+template <class TL>
 struct MmaBf16 {
-    static constexpr int BK = 32;
+    using T = TL;
     __device__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
                                int wn, int lane) {
-        bf16x8 a[4], b[4];
         const int r = lane & 15, q = lane >> 4;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            a[i] = *(const bf16x8 *)(As + (wm * 64 + i * 16 + r) * kPitch + q * 16);
-            b[i] = *(const bf16x8 *)(Bs + (wn * 64 + i * 16 + r) * kPitch + q * 16);
+        for (int s = 0; s < TL::BK / 32; ++s) {
+            bf16x8 a[4], b[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                a[i] = *(const bf16x8 *)(As + (wm * 64 + i * 16 + r) * TL::PITCH + s * 64 + q * 16);
+                b[i] = *(const bf16x8 *)(Bs + (wn * 64 + i * 16 + r) * TL::PITCH + s * 64 + q * 16);
+            }
+#pragma unroll
+            for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < 4; ++ni)
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], b[ni],
+                                                                          acc[mi][ni], 0, 0, 0);
         }
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-            for (int ni = 0; ni < 4; ++ni)
-                acc[mi][ni] =
-                    __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], b[ni], acc[mi][ni], 0, 0, 0);
     }
 };
 
@@ -54,15 +80,15 @@ struct MmaBf16 {
 // four steps together cover k = 0..15 (the sum over k is taken in a different order, not
 // a different set).
 struct MmaF32 {
-    static constexpr int BK = 16;
+    using T = TileF32;
     __device__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
                                int wn, int lane) {
         f32x4 a[4], b[4];
         const int r = lane & 15, q = lane >> 4;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            a[i] = *(const f32x4 *)(As + (wm * 64 + i * 16 + r) * kPitch + q * 16);
-            b[i] = *(const f32x4 *)(Bs + (wn * 64 + i * 16 + r) * kPitch + q * 16);
+            a[i] = *(const f32x4 *)(As + (wm * 64 + i * 16 + r) * T::PITCH + q * 16);
+            b[i] = *(const f32x4 *)(Bs + (wn * 64 + i * 16 + r) * T::PITCH + q * 16);
         }
 #pragma unroll
         for (int s = 0; s < 4; ++s)
@@ -76,8 +102,6 @@ struct MmaF32 {
 };
 
 // ------------------------------------------------------------------ tile loaders
-// K-contiguous rows, element type equal to the LDS type.  Each thread moves 2 of the 512
-// 16-byte chunks of a 128-row x 64-byte tile.  Row addresses come from a policy.
 struct PlainRows {
     const char *base;
     int64_t ld_bytes;
@@ -96,194 +120,211 @@ struct SlotRows {  // row n = (slot n / d_in, column c = n % d_in) of W_slot [d_
     }
 };
 
-template <class RowPolicy, bool WRAP = false>
+// K-contiguous rows whose element type is the LDS type.  WRAP: the product's K is twice
+// the row length and k >= row length re-reads the row (used with LoadRowsF32Split).
+template <class TL, class RowPolicy, bool WRAP = false>
 struct LoadRows {
+    static constexpr int NCH = kTile * TL::CPR / kThreads;
     RowPolicy pol;
-    int64_t kbytes;     // bytes of K per row
-    int es;             // element size
-    int64_t wrap_bytes; // WRAP: the product's K is twice the row; k >= row length re-reads it
-    const char *rp[2];
-    int lr[2], lq[2];
-    uint4 reg[2];
-    __device__ void init(int64_t row0) {
+    int64_t kbytes;       // bytes of K per source row
+    int64_t wrap_bytes;
+    struct State {
+        const char *rp[NCH];
+        int lr[NCH], lq[NCH];
+        uint4 reg[NCH];
+    };
+    __device__ void init(State &st, int64_t row0) const {
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
+        for (int c = 0; c < NCH; ++c) {
             const int chunk = threadIdx.x + c * kThreads;
-            lr[c] = chunk >> 2;
-            lq[c] = chunk & 3;
-            rp[c] = pol.row(row0 + lr[c]);
+            st.lr[c] = chunk / TL::CPR;
+            st.lq[c] = chunk % TL::CPR;
+            st.rp[c] = pol.row(row0 + st.lr[c]);
         }
     }
-    __device__ void load(int64_t k0) {
+    __device__ void load(State &st, int64_t k0) const {
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            int64_t kb = k0 * es + lq[c] * 16;
+        for (int c = 0; c < NCH; ++c) {
+            int64_t kb = k0 * TL::ES + st.lq[c] * 16;
             if constexpr (WRAP) {
                 if (kb >= wrap_bytes) kb -= wrap_bytes;
             }
-            reg[c] = (rp[c] && kb < kbytes) ? *(const uint4 *)(rp[c] + kb) : make_uint4(0, 0, 0, 0);
+            st.reg[c] = (st.rp[c] && kb < kbytes) ? *(const uint4 *)(st.rp[c] + kb)
+                                                  : make_uint4(0, 0, 0, 0);
         }
     }
-    __device__ void store(char *lds) const {
+    __device__ void store(const State &st, char *lds) const {
 #pragma unroll
-        for (int c = 0; c < 2; ++c) *(uint4 *)(lds + lr[c] * kPitch + lq[c] * 16) = reg[c];
+        for (int c = 0; c < NCH; ++c)
+            *(uint4 *)(lds + st.lr[c] * TL::PITCH + st.lq[c] * 16) = st.reg[c];
     }
 };
 
-// K-contiguous fp32 rows rounded to bf16 (bf16 mode): a 16-byte LDS chunk = 8 values =
-// 32 source bytes.
-struct LoadRowsF32ToBf16 {
-    PlainRows pol;
-    int64_t K;
-    const char *rp[2];
-    int lr[2], lq[2];
-    float4 reg[2][2];
-    __device__ void init(int64_t row0) {
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            const int chunk = threadIdx.x + c * kThreads;
-            lr[c] = chunk >> 2;
-            lq[c] = chunk & 3;
-            rp[c] = pol.row(row0 + lr[c]);
-        }
-    }
-    __device__ void load(int64_t k0) {
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            const int64_t k = k0 + lq[c] * 8;
-            if (rp[c] && k < K) {
-                reg[c][0] = *(const float4 *)(rp[c] + k * 4);
-                reg[c][1] = *(const float4 *)(rp[c] + k * 4 + 16);
-            } else {
-                reg[c][0] = reg[c][1] = make_float4(0.f, 0.f, 0.f, 0.f);
-            }
-        }
-    }
-    __device__ void store(char *lds) const {
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            uint4 w;
-            w.x = pack_bf16x2(reg[c][0].x, reg[c][0].y);
-            w.y = pack_bf16x2(reg[c][0].z, reg[c][0].w);
-            w.z = pack_bf16x2(reg[c][1].x, reg[c][1].y);
-            w.w = pack_bf16x2(reg[c][1].z, reg[c][1].w);
-            *(uint4 *)(lds + lr[c] * kPitch + lq[c] * 16) = w;
-        }
-    }
-};
-
-// fp32 rows entering a bf16 product as two bf16 terms: for k < K the high part
-// hi = bf16(x), for K <= k < 2K the low part lo = bf16(x - hi) of element k - K.  With
-// the other operand repeated along K (LoadRows<..., true>), the product accumulates
-// hi.W + lo.W, which carries x to ~16 significant bits instead of 8.
+// fp32 rows entering a bf16 product as two bf16 terms: chunk k < K holds the high part
+// hi = bf16(x) of element k, chunk K <= k < 2K the low part lo = bf16(x - hi) of element
+// k - K.  With the other operand read twice along K (LoadRows<..., true>) the product
+// accumulates hi.W + lo.W, which carries x to ~16 significant bits instead of 8.  K is a
+// multiple of 8, so a 16-byte chunk (8 values) never straddles the two halves.
+template <class TL>
 struct LoadRowsF32Split {
+    static constexpr int CPR = TL::BK / 8;        // 8 bf16 per 16-byte LDS chunk
+    static constexpr int NCH = kTile * CPR / kThreads;
     PlainRows pol;
     int64_t K;
-    const char *rp[2];
-    int lr[2], lq[2];
-    float4 reg[2][2];
-    bool low;
-    __device__ void init(int64_t row0) {
+    struct State {
+        const char *rp[NCH];
+        int lr[NCH], lq[NCH];
+        bool low[NCH];
+        float4 reg[NCH][2];
+    };
+    __device__ void init(State &st, int64_t row0) const {
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
+        for (int c = 0; c < NCH; ++c) {
             const int chunk = threadIdx.x + c * kThreads;
-            lr[c] = chunk >> 2;
-            lq[c] = chunk & 3;
-            rp[c] = pol.row(row0 + lr[c]);
+            st.lr[c] = chunk / CPR;
+            st.lq[c] = chunk % CPR;
+            st.rp[c] = pol.row(row0 + st.lr[c]);
         }
     }
-    __device__ void load(int64_t k0) {
-        low = k0 >= K;
-        const int64_t kbase = low ? k0 - K : k0;
+    __device__ void load(State &st, int64_t k0) const {
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            const int64_t k = kbase + lq[c] * 8;
-            if (rp[c] && k < K) {
-                reg[c][0] = *(const float4 *)(rp[c] + k * 4);
-                reg[c][1] = *(const float4 *)(rp[c] + k * 4 + 16);
+        for (int c = 0; c < NCH; ++c) {
+            int64_t k = k0 + st.lq[c] * 8;
+            st.low[c] = k >= K;
+            if (st.low[c]) k -= K;
+            if (st.rp[c] && k < K) {
+                st.reg[c][0] = *(const float4 *)(st.rp[c] + k * 4);
+                st.reg[c][1] = *(const float4 *)(st.rp[c] + k * 4 + 16);
             } else {
-                reg[c][0] = reg[c][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+                st.reg[c][0] = st.reg[c][1] = make_float4(0.f, 0.f, 0.f, 0.f);
             }
         }
     }
-    __device__ static float part(float x, bool low) {
-        const float hi = __uint_as_float(f32_to_bf16_bits(x) << 16);
-        return low ? x - hi : x;
-    }
-    __device__ void store(char *lds) const {
+    __device__ static float part(float x, bool lo) { return lo ? x - round_bf16(x) : x; }
+    __device__ void store(const State &st, char *lds) const {
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
+        for (int c = 0; c < NCH; ++c) {
+            const bool lo = st.low[c];
+            const float4 a = st.reg[c][0], b = st.reg[c][1];
             uint4 w;
-            w.x = pack_bf16x2(part(reg[c][0].x, low), part(reg[c][0].y, low));
-            w.y = pack_bf16x2(part(reg[c][0].z, low), part(reg[c][0].w, low));
-            w.z = pack_bf16x2(part(reg[c][1].x, low), part(reg[c][1].y, low));
-            w.w = pack_bf16x2(part(reg[c][1].z, low), part(reg[c][1].w, low));
-            *(uint4 *)(lds + lr[c] * kPitch + lq[c] * 16) = w;
+            w.x = pack_bf16x2(part(a.x, lo), part(a.y, lo));
+            w.y = pack_bf16x2(part(a.z, lo), part(a.w, lo));
+            w.z = pack_bf16x2(part(b.x, lo), part(b.y, lo));
+            w.w = pack_bf16x2(part(b.z, lo), part(b.w, lo));
+            *(uint4 *)(lds + st.lr[c] * TL::PITCH + st.lq[c] * 16) = w;
         }
     }
 };
 
-// Transposed operand for the weight-side product: source [Ksrc rows x C cols] row-major;
-// LDS row = source column (128 of them from col0), LDS k = source row.  Global reads are
-// row-contiguous; the transpose happens in the LDS writes.
-//   SRC_BF16 && LDS bf16:  32 k x 16 chunks of 8 columns, 2 chunks per thread
-//   SRC_F32  && LDS f32:   16 k x 32 chunks of 4 columns, 2 chunks per thread
-//   SRC_F32  && LDS bf16:  32 k x 32 chunks of 4 columns, 4 chunks per thread
-template <bool SRC_BF16, bool LDS_BF16>
-struct LoadTrans {
-    static constexpr int NCH = (!SRC_BF16 && LDS_BF16) ? 4 : 2;
-    static constexpr int CPR = SRC_BF16 ? 16 : 32;       // chunks per source row
-    static constexpr int VEC = SRC_BF16 ? 8 : 4;         // columns per chunk
-    static constexpr int SES = SRC_BF16 ? 2 : 4;         // source element size
-    static constexpr int LES = LDS_BF16 ? 2 : 4;         // LDS element size
+// Weight-side operands (bf16 mode, BK = 64): source [ksrc rows x cols] row-major; LDS row
+// = source column (128 from col0), LDS k = source row.  Half of the workgroup serves each
+// operand: waves 0-1 (HALF 0) or waves 2-3 (HALF 1).  Thread b of the half owns the 8 x 8
+// block (source rows k0 + 8*(b%8) .. +7, columns col0 + 8*(b/8) .. +7): eight row reads of
+// 16 bytes (bf16 source) or 32 bytes (fp32 source, rounded to bf16), a transpose in
+// registers, eight 16-byte LDS writes.  Lanes with consecutive b hit consecutive 16-byte
+// units of one LDS row or, across rows, units shifted by the odd pitch: no conflicts.
+template <int HALF, bool SRC_F32>
+struct LoadTransBlock {
+    using TL = TileBf16T;
+    static constexpr int SES = SRC_F32 ? 4 : 2;
+    static constexpr int NH = SRC_F32 ? 2 : 1;
     const char *base;
     int64_t ld_bytes;
-    int64_t ksrc;       // source rows (the reduction length)
-    int64_t cols;       // source columns
-    int64_t col0;
-    int ik[NCH], cq[NCH];
-    uint4 reg[NCH];
-    __device__ void init(int64_t c0) {
-        col0 = c0;
+    int64_t ksrc;
+    int64_t cols;
+    struct State {
+        int64_t col0;
+        int ib, cb;
+        bool active;
+        uint4 reg[8][NH];
+    };
+    __device__ void init(State &st, int64_t c0) const {
+        st.col0 = c0;
+        const int b = (int)threadIdx.x - HALF * 128;
+        st.active = b >= 0 && b < 128;
+        st.ib = b & 7;
+        st.cb = (b >> 3) & 15;
+    }
+    __device__ void load(State &st, int64_t k0) const {
+        if (!st.active) return;
+        const int64_t col = st.col0 + (int64_t)st.cb * 8;
+        const bool colok = col < cols;
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-            const int chunk = threadIdx.x + c * kThreads;
-            ik[c] = chunk / CPR;
-            cq[c] = chunk % CPR;
+        for (int r = 0; r < 8; ++r) {
+            const int64_t i = k0 + st.ib * 8 + r;
+            const bool ok = colok && i < ksrc;
+            const char *p = base + i * ld_bytes + col * SES;
+#pragma unroll
+            for (int h = 0; h < NH; ++h)
+                st.reg[r][h] = ok ? *(const uint4 *)(p + h * 16) : make_uint4(0, 0, 0, 0);
         }
     }
-    __device__ void load(int64_t k0) {
-#pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-            const int64_t i = k0 + ik[c];
-            const int64_t col = col0 + (int64_t)cq[c] * VEC;
-            reg[c] = (i < ksrc && col < cols)
-                         ? *(const uint4 *)(base + i * ld_bytes + col * SES)
-                         : make_uint4(0, 0, 0, 0);
-        }
+    __device__ static uint32_t word(const uint4 &u, int i) {
+        return i == 0 ? u.x : i == 1 ? u.y : i == 2 ? u.z : u.w;
     }
-    __device__ void store(char *lds) const {
+    __device__ void store(const State &st, char *lds) const {
+        if (!st.active) return;
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-            const uint32_t w[4] = {reg[c].x, reg[c].y, reg[c].z, reg[c].w};
-            if constexpr (SRC_BF16) {
+        for (int c = 0; c < 8; ++c) {
+            uint32_t w[4];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const uint16_t h = (uint16_t)(w[e >> 1] >> ((e & 1) * 16));
-                    *(uint16_t *)(lds + (cq[c] * 8 + e) * kPitch + ik[c] * 2) = h;
+            for (int p = 0; p < 4; ++p) {
+                if constexpr (SRC_F32) {
+                    const uint32_t a0 = word(st.reg[2 * p][c >> 2], c & 3);
+                    const uint32_t a1 = word(st.reg[2 * p + 1][c >> 2], c & 3);
+                    w[p] = pack_bf16x2(__uint_as_float(a0), __uint_as_float(a1));
+                } else {
+                    const uint32_t a0 = word(st.reg[2 * p][0], c >> 1);
+                    const uint32_t a1 = word(st.reg[2 * p + 1][0], c >> 1);
+                    w[p] = (c & 1) ? ((a0 >> 16) | (a1 & 0xffff0000u))
+                                   : ((a0 & 0xffffu) | (a1 << 16));
                 }
-            } else if constexpr (LDS_BF16) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    *(uint16_t *)(lds + (cq[c] * 4 + e) * kPitch + ik[c] * 2) =
-                        (uint16_t)f32_to_bf16_bits(__uint_as_float(w[e]));
-            } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    *(uint32_t *)(lds + (cq[c] * 4 + e) * kPitch + ik[c] * 4) = w[e];
             }
+            *(uint4 *)(lds + (st.cb * 8 + c) * TL::PITCH + st.ib * 16) =
+                make_uint4(w[0], w[1], w[2], w[3]);
         }
-        (void)LES;
+    }
+};
+
+// fp32 weight side: 16 k x 32 chunks of 4 columns, 2 chunks per thread, transposed by
+// scalar LDS writes (used only in fp32 mode).
+struct LoadTransF32 {
+    using TL = TileF32;
+    const char *base;
+    int64_t ld_bytes;
+    int64_t ksrc;
+    int64_t cols;
+    struct State {
+        int64_t col0;
+        int ik[2], cq[2];
+        uint4 reg[2];
+    };
+    __device__ void init(State &st, int64_t c0) const {
+        st.col0 = c0;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            const int chunk = threadIdx.x + c * kThreads;
+            st.ik[c] = chunk >> 5;
+            st.cq[c] = chunk & 31;
+        }
+    }
+    __device__ void load(State &st, int64_t k0) const {
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            const int64_t i = k0 + st.ik[c];
+            const int64_t col = st.col0 + (int64_t)st.cq[c] * 4;
+            st.reg[c] = (i < ksrc && col < cols) ? *(const uint4 *)(base + i * ld_bytes + col * 4)
+                                                 : make_uint4(0, 0, 0, 0);
+        }
+    }
+    __device__ void store(const State &st, char *lds) const {
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            const uint32_t w[4] = {st.reg[c].x, st.reg[c].y, st.reg[c].z, st.reg[c].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                *(uint32_t *)(lds + (st.cq[c] * 4 + e) * TL::PITCH + st.ik[c] * 4) = w[e];
+        }
     }
 };
 
@@ -296,7 +337,7 @@ struct EpiForward {
     int64_t M;
     int32_t N;
     int32_t relu;
-    __device__ void operator()(int64_t m, int64_t n0, const float *v) const {
+    __device__ void operator()(int64_t m, int64_t n0, const float *v, int64_t) const {
         if (m >= M) return;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -333,7 +374,7 @@ struct EpiDms {
     int32_t N;
     int32_t d_in;
     const int32_t *indptr[kMaxSlots];
-    __device__ void operator()(int64_t m, int64_t n0, const float *v) const {
+    __device__ void operator()(int64_t m, int64_t n0, const float *v, int64_t) const {
         if (m >= M) return;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -361,9 +402,9 @@ struct EpiPartial {
     float *out;          // [splits][M][N]
     int64_t M;
     int32_t N;
-    __device__ void operator()(int64_t m, int64_t n0, const float *v) const {
+    __device__ void operator()(int64_t m, int64_t n0, const float *v, int64_t split) const {
         if (m >= M) return;
-        float *o = out + (int64_t)blockIdx.y * M * N + m * N;
+        float *o = out + split * M * N + m * N;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int64_t n = n0 + 4 * q;
@@ -374,43 +415,51 @@ struct EpiPartial {
 };
 
 // ------------------------------------------------------------------ the kernel
-// Grid: x = output tiles (XCD-major so tiles sharing an A row-block share an L2),
-// y = splits of the reduction (weight side only).
+// One-dimensional grid over (split, output tile), numbered XCD-major: the dispatcher
+// sends workgroup w to XCD w mod 8, and consecutive logical ids -- the tiles of one
+// split, and within a split the tiles sharing a row block of A -- land on the same XCD
+// and share its L2.
 template <class Mma, class LA, class LB, class Epi>
-__global__ __launch_bounds__(kThreads, 2) void k_gemm(LA la, LB lb, Epi epi, int64_t K,
+__global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, const Epi epi,
+                                                      int64_t K, int64_t tiles_m,
                                                       int64_t tiles_n, int64_t k_per_split) {
-    __shared__ __attribute__((aligned(16))) char lds[4 * kTileBytes];
-    const int64_t total = (int64_t)gridDim.x;
-    const int64_t t = xcd_major_id(blockIdx.x, total);
+    using TL = typename Mma::T;
+    __shared__ __attribute__((aligned(16))) char lds[4 * TL::BYTES];
+    const int64_t logical = xcd_major_id(blockIdx.x, (int64_t)gridDim.x);
+    const int64_t tiles = tiles_m * tiles_n;
+    const int64_t split = logical / tiles;
+    const int64_t t = logical - split * tiles;
     const int64_t tm = t / tiles_n, tn = t - tm * tiles_n;
     const int64_t m0 = tm * kTile, n0 = tn * kTile;
-    const int64_t kb = (int64_t)blockIdx.y * k_per_split;
+    const int64_t kb = split * k_per_split;
     const int64_t ke = kb + k_per_split < K ? kb + k_per_split : K;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    la.init(m0);
-    lb.init(n0);
+    typename LA::State sa;
+    typename LB::State sb;
+    la.init(sa, m0);
+    lb.init(sb, n0);
     f32x4 acc[4][4];
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int64_t nk = ke > kb ? cdiv(ke - kb, Mma::BK) : 0;
+    const int64_t nk = ke > kb ? cdiv(ke - kb, TL::BK) : 0;
     if (nk > 0) {
-        la.load(kb);
-        lb.load(kb);
+        la.load(sa, kb);
+        lb.load(sb, kb);
     }
     for (int64_t it = 0; it < nk; ++it) {
-        char *As = lds + (it & 1) * 2 * kTileBytes;
-        char *Bs = As + kTileBytes;
-        la.store(As);
-        lb.store(Bs);
+        char *As = lds + (it & 1) * 2 * TL::BYTES;
+        char *Bs = As + TL::BYTES;
+        la.store(sa, As);
+        lb.store(sb, Bs);
         __syncthreads();
         if (it + 1 < nk) {
-            la.load(kb + (it + 1) * Mma::BK);
-            lb.load(kb + (it + 1) * Mma::BK);
+            la.load(sa, kb + (it + 1) * TL::BK);
+            lb.load(sb, kb + (it + 1) * TL::BK);
         }
         Mma::run(As, Bs, acc, wm, wn, lane);
     }
@@ -434,7 +483,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm(LA la, LB lb, Epi epi, int
             const float4 x = *(const float4 *)(stage + r * kStagePitch + c0 + e);
             vals[e] = x.x; vals[e + 1] = x.y; vals[e + 2] = x.z; vals[e + 3] = x.w;
         }
-        epi(m0 + wm * 64 + mi * 16 + r, n0 + wn * 64 + c0, vals);
+        epi(m0 + wm * 64 + mi * 16 + r, n0 + wn * 64 + c0, vals, split);
         __syncthreads();
     }
 }
@@ -444,9 +493,8 @@ hipError_t launch_gemm(const LA &la, const LB &lb, const Epi &epi, int64_t M, in
                        int64_t K, int64_t splits, int64_t k_per_split, hipStream_t s) {
     const int64_t tiles_m = cdiv(M, kTile), tiles_n = cdiv(N, kTile);
     if (tiles_m == 0 || tiles_n == 0 || splits == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_gemm<Mma, LA, LB, Epi>), dim3((unsigned)(tiles_m * tiles_n),
-                       (unsigned)splits), dim3(kThreads), 0, s, la, lb, epi, K, tiles_n,
-                       k_per_split);
+    hipLaunchKernelGGL((k_gemm<Mma, LA, LB, Epi>), dim3((unsigned)(tiles_m * tiles_n * splits)),
+                       dim3(kThreads), 0, s, la, lb, epi, K, tiles_m, tiles_n, k_per_split);
     return hipGetLastError();
 }
 
@@ -491,12 +539,17 @@ __global__ __launch_bounds__(kThreads) void k_zero_outputs(DwOut out, int d_in, 
 hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
                         const void *wcat_t, const void *bias, int relu, void *y,
                         hipStream_t s) {
-    const int es = dt == RGCN_BF16 ? 2 : 4;
-    LoadRows<PlainRows> la{PlainRows{(const char *)a, (int64_t)K * es, M}, (int64_t)K * es, es, 0};
-    LoadRows<PlainRows> lb{PlainRows{(const char *)wcat_t, (int64_t)K * es, N}, (int64_t)K * es,
-                           es, 0};
-    if (dt == RGCN_BF16)
-        return launch_gemm<MmaBf16>(la, lb, EpiForward<true>{y, bias, M, N, relu}, M, N, K, 1, K, s);
+    if (dt == RGCN_BF16) {
+        using TL = TileBf16;
+        LoadRows<TL, PlainRows> la{PlainRows{(const char *)a, (int64_t)K * 2, M}, (int64_t)K * 2, 0};
+        LoadRows<TL, PlainRows> lb{PlainRows{(const char *)wcat_t, (int64_t)K * 2, N},
+                                   (int64_t)K * 2, 0};
+        return launch_gemm<MmaBf16<TL>>(la, lb, EpiForward<true>{y, bias, M, N, relu}, M, N, K, 1,
+                                        K, s);
+    }
+    using TL = TileF32;
+    LoadRows<TL, PlainRows> la{PlainRows{(const char *)a, (int64_t)K * 4, M}, (int64_t)K * 4, 0};
+    LoadRows<TL, PlainRows> lb{PlainRows{(const char *)wcat_t, (int64_t)K * 4, N}, (int64_t)K * 4, 0};
     return launch_gemm<MmaF32>(la, lb, EpiForward<false>{y, bias, M, N, relu}, M, N, K, 1, K, s);
 }
 
@@ -509,7 +562,6 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_
     sr.d_in = d_in;
     sr.es_dout = d_out * es;
     sr.rows = N;
-    LoadRows<SlotRows> lb{sr, (int64_t)d_out * es, es, 0};
     EpiDms epi;
     epi.out = dms;
     epi.M = M;
@@ -519,19 +571,23 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_
     PlainRows pa{(const char *)dy, (int64_t)d_out * 4, M};
     if (dt == RGCN_BF16) {
         // dY enters as hi + lo bf16 parts: K = 2 d_out, the weight rows read twice
-        LoadRowsF32Split la{pa, d_out};
-        LoadRows<SlotRows, true> lbw{sr, (int64_t)d_out * es, es, (int64_t)d_out * es};
-        return launch_gemm<MmaBf16>(la, lbw, epi, M, N, 2 * (int64_t)d_out, 1, 2 * (int64_t)d_out, s);
+        using TL = TileBf16;
+        LoadRowsF32Split<TL> la{pa, d_out};
+        LoadRows<TL, SlotRows, true> lb{sr, (int64_t)d_out * 2, (int64_t)d_out * 2};
+        return launch_gemm<MmaBf16<TL>>(la, lb, epi, M, N, 2 * (int64_t)d_out, 1,
+                                        2 * (int64_t)d_out, s);
     }
-    LoadRows<PlainRows> la{pa, (int64_t)d_out * 4, 4, 0};
+    using TL = TileF32;
+    LoadRows<TL, PlainRows> la{pa, (int64_t)d_out * 4, 0};
+    LoadRows<TL, SlotRows> lb{sr, (int64_t)d_out * 4, 0};
     return launch_gemm<MmaF32>(la, lb, epi, M, N, d_out, 1, d_out, s);
 }
 
 size_t gemm_dw_partial_bytes(int64_t M, int Kcat, int d_out) {
-    int64_t sp16, p16, sp32, p32;
-    dw_split(M, Kcat, d_out, 16, &sp16, &p16);
-    dw_split(M, Kcat, d_out, 32, &sp32, &p32);
-    const int64_t sp = sp16 > sp32 ? sp16 : sp32;
+    int64_t sp16, p16, sp64, p64;
+    dw_split(M, Kcat, d_out, TileF32::BK, &sp16, &p16);
+    dw_split(M, Kcat, d_out, TileBf16T::BK, &sp64, &p64);
+    const int64_t sp = sp16 > sp64 ? sp16 : sp64;
     return (size_t)(sp > 0 ? sp : 1) * Kcat * d_out * 4 + 256;
 }
 
@@ -539,7 +595,7 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
                    const float *dy, int d_out, const DwOut &out, float *partial,
                    hipStream_t s) {
     const bool bf = dt == RGCN_BF16;
-    const int bk = bf ? MmaBf16::BK : MmaF32::BK;
+    const int bk = bf ? TileBf16T::BK : TileF32::BK;
     int64_t splits, per;
     dw_split(M, Kcat, d_out, bk, &splits, &per);
     if (splits == 0) {  // no rows: every requested gradient is zero
@@ -549,12 +605,12 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
     }
     EpiPartial epi{partial, Kcat, d_out};
     if (bf) {
-        LoadTrans<true, true> la{(const char *)mcat, (int64_t)Kcat * 2, M, Kcat};
-        LoadTrans<false, true> lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
-        RGCN_HIP_TRY(launch_gemm<MmaBf16>(la, lb, epi, Kcat, d_out, M, splits, per, s));
+        LoadTransBlock<0, false> la{(const char *)mcat, (int64_t)Kcat * 2, M, Kcat};
+        LoadTransBlock<1, true> lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
+        RGCN_HIP_TRY(launch_gemm<MmaBf16<TileBf16T>>(la, lb, epi, Kcat, d_out, M, splits, per, s));
     } else {
-        LoadTrans<false, false> la{(const char *)mcat, (int64_t)Kcat * 4, M, Kcat};
-        LoadTrans<false, false> lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
+        LoadTransF32 la{(const char *)mcat, (int64_t)Kcat * 4, M, Kcat};
+        LoadTransF32 lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
         RGCN_HIP_TRY(launch_gemm<MmaF32>(la, lb, epi, Kcat, d_out, M, splits, per, s));
     }
     const int64_t total = (int64_t)Kcat * d_out;

@@ -246,6 +246,43 @@ __global__ __launch_bounds__(kThreads) void k_lower_bounds(const uint32_t *sorte
     out[j] = (int32_t)lo;
 }
 
+// Descriptor of the segment at schedule position p (see SegDesc).
+struct DescArgs {
+    int32_t nslots;
+    int64_t base[kMaxSlots];
+    const int32_t *indptr[kMaxSlots];
+    int16_t dst[kMaxSlots];
+    int32_t col_off[kMaxSlots];
+    int64_t mcat_off[kMaxTypes];
+    int64_t mcat_ld[kMaxTypes];
+    int32_t es;
+};
+__global__ __launch_bounds__(kThreads) void k_fwd_desc(DescArgs a, const int32_t *order,
+                                                       int64_t n_seg, SegDesc *desc) {
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= n_seg) return;
+    const int64_t seg = order[p];
+    int lo = 0, hi = a.nslots - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (a.base[mid] <= seg) lo = mid; else hi = mid - 1;
+    }
+    const int64_t row = seg - a.base[lo];
+    SegDesc d;
+    if (a.indptr[lo]) {
+        d.k0 = a.indptr[lo][row];
+        d.deg = a.indptr[lo][row + 1] - d.k0;
+    } else {
+        d.k0 = (int32_t)row;
+        d.deg = 1;
+    }
+    const int t = a.dst[lo];
+    const uint64_t out = (uint64_t)(a.mcat_off[t] + (row * a.mcat_ld[t] + a.col_off[lo]) * a.es) >> 4;
+    d.out_lo = (uint32_t)out;
+    d.info = (uint32_t)((out >> 32) & 0xffu) | ((uint32_t)lo << 8);
+    desc[p] = d;
+}
+
 struct Words {
     uint32_t n;
     uint32_t w[512];
@@ -287,6 +324,28 @@ hipError_t fwd_schedule(const FwdSlot *slots_host, int nslots, int64_t n_seg, in
         kf.indptr[i] = i < nslots ? slots_host[i].indptr : nullptr;
     }
     return bucket_sort<kSchedBuckets, 6>(kf, PutIndex{order}, n_seg, temp, s);
+}
+
+hipError_t fwd_descriptors(const FwdSlot *slots_host, int nslots, const int32_t *order,
+                           int64_t n_seg, const int64_t *mcat_off, const int64_t *mcat_ld,
+                           int es, SegDesc *desc, hipStream_t s) {
+    if (n_seg == 0) return hipSuccess;
+    DescArgs a;
+    a.nslots = nslots;
+    for (int i = 0; i < kMaxSlots; ++i) {
+        a.base[i] = i < nslots ? slots_host[i].seg_base : 0;
+        a.indptr[i] = i < nslots ? slots_host[i].indptr : nullptr;
+        a.dst[i] = (int16_t)(i < nslots ? slots_host[i].dst_type : 0);
+        a.col_off[i] = i < nslots ? slots_host[i].col_off : 0;
+    }
+    for (int t = 0; t < kMaxTypes; ++t) {
+        a.mcat_off[t] = mcat_off[t];
+        a.mcat_ld[t] = mcat_ld[t];
+    }
+    a.es = es;
+    hipLaunchKernelGGL(k_fwd_desc, dim3((unsigned)cdiv(n_seg, kThreads)), dim3(kThreads), 0, s, a,
+                       order, n_seg, desc);
+    return hipGetLastError();
 }
 
 hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, void *temp,
