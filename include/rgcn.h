@@ -113,8 +113,11 @@ typedef struct {
     size_t fwd_order;                       /* int32 [n_fwd_segments]: segment ids, heaviest first */
     int64_t n_bwd_rows;                     /* source rows of the types in grad_src_types */
     size_t bwd_order;                       /* int32 [n_bwd_rows] */
-    size_t csc_indptr[RGCN_MAX_RELS];       /* int32 [n_src[src_type] + 1] */
-    size_t csc_dst[RGCN_MAX_RELS];          /* int32 [nnz]: destination row of each edge */
+    size_t csc_indptr[RGCN_MAX_RELS];       /* int32 [n_src[src_type] + 1]: csc_indptr[j+1] -
+                                               csc_indptr[j] = in-degree of source row j;
+                                               values are offset by csc_indptr[0] */
+    size_t csc_dst[RGCN_MAX_RELS];          /* int32 [nnz]: destination row of each edge, edges
+                                               of source row j at csc_indptr[j] - csc_indptr[0] */
     size_t total_bytes;                     /* = rgcn_block_workspace_size */
 } rgcn_plan_layout;
 

@@ -62,6 +62,10 @@ struct Layout {
     // workspace offsets
     size_t off_slots = 0, off_fwd_order = 0, off_fwd_desc = 0, off_bwd_order = 0, off_err = 0;
     size_t off_csc_indptr[kMaxRels], off_csc_dst[kMaxRels];
+    // combined transpose of the relations leaving grad types
+    int64_t koff[kMaxRels], e0[kMaxRels];
+    int64_t key_range = 0, csc_nnz = 0, csc_rows = 0;
+    size_t off_ip = 0, off_csd = 0;
     size_t off_mcat[kMaxTypes], off_wcat[kMaxTypes];
     size_t off_scratch = 0;
     // scratch (a union: plan temporaries, or backward temporaries)
@@ -208,13 +212,29 @@ rgcn_status make_layout(const rgcn_block *b, const rgcn_params *p, Layout &L) {
     L.off_fwd_order = off;                off += align256((size_t)L.n_seg * 4 + 4);
     L.off_fwd_desc = off;                 off += align256((size_t)L.n_seg * sizeof(SegDesc) + 16);
     L.off_bwd_order = off;                off += align256((size_t)L.n_bwd_rows * 4 + 4);
-    for (int r = 0; r < kMaxRels; ++r) L.off_csc_indptr[r] = L.off_csc_dst[r] = SIZE_MAX;
+    for (int r = 0; r < kMaxRels; ++r) {
+        L.off_csc_indptr[r] = L.off_csc_dst[r] = SIZE_MAX;
+        L.koff[r] = L.e0[r] = -1;
+    }
+    L.key_range = L.csc_nnz = L.csc_rows = 0;
     for (int r = 0; r < L.R; ++r) {
         const rgcn_relation &rel = b->rels[r];
         if (!(L.grad_mask >> rel.src_type & 1u)) continue;
-        L.off_csc_indptr[r] = off;  off += align256((size_t)(b->n_src[rel.src_type] + 1) * 4);
-        L.off_csc_dst[r] = off;     off += align256((size_t)rel.nnz * 4 + 4);
+        L.koff[r] = L.key_range;
+        L.e0[r] = L.csc_nnz;
+        L.key_range += b->n_src[rel.src_type];
+        L.csc_nnz += rel.nnz;
+        L.csc_rows += b->n_dst[rel.dst_type];
     }
+    if (L.key_range >= kI32Max || L.csc_nnz >= kI32Max)
+        return fail(RGCN_ERR_UNSUPPORTED, "transpose of the grad relations exceeds 2^31 entries");
+    L.off_ip = off;   off += align256((size_t)(L.key_range + 1) * 4);
+    L.off_csd = off;  off += align256((size_t)L.csc_nnz * 4 + 4);
+    for (int r = 0; r < L.R; ++r)
+        if (L.koff[r] >= 0) {
+            L.off_csc_indptr[r] = L.off_ip + 4 * (size_t)L.koff[r];
+            L.off_csc_dst[r] = L.off_csd + 4 * (size_t)L.e0[r];
+        }
     for (int t = 0; t < kMaxTypes; ++t) L.off_mcat[t] = L.off_wcat[t] = SIZE_MAX;
     for (int t = 0; t < L.T; ++t) {
         if (b->n_dst[t] == 0) continue;
@@ -224,10 +244,8 @@ rgcn_status make_layout(const rgcn_block *b, const rgcn_params *p, Layout &L) {
     L.off_scratch = off;
     // plan temporaries
     size_t pt = bucket_sort_temp_bytes(L.n_seg, kSchedBuckets);
-    for (int r = 0; r < L.R; ++r) {
-        const rgcn_relation &rel = b->rels[r];
-        if (!(L.grad_mask >> rel.src_type & 1u)) continue;
-        size_t c = csc_temp_bytes(rel.nnz, b->n_src[rel.src_type]);
+    {
+        size_t c = csc_temp_bytes(L.csc_nnz, L.key_range);
         if (c > pt) pt = c;
     }
     for (int t = 0; t < L.T; ++t)
@@ -380,13 +398,22 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
                                 moff, mld, L.es, (SegDesc *)(ws + L.off_fwd_desc), stream),
                 "forward descriptors");
     }
-    for (int r = 0; r < L.R; ++r) {
-        if (L.off_csc_indptr[r] == SIZE_MAX) continue;
-        const rgcn_relation &rel = block->rels[r];
-        TRY_HIP(csc_build(rel.indptr, rel.indices, block->n_dst[rel.dst_type],
-                          block->n_src[rel.src_type], rel.nnz,
-                          (int32_t *)(ws + L.off_csc_indptr[r]), (int32_t *)(ws + L.off_csc_dst[r]),
-                          scratch, stream), "csc build");
+    if (L.key_range > 0) {
+        CscRels cr{};
+        int64_t rows = 0;
+        for (int r = 0; r < L.R; ++r) {
+            if (L.koff[r] < 0) continue;
+            const rgcn_relation &rel = block->rels[r];
+            cr.row_base[cr.count] = rows;
+            cr.indptr[cr.count] = rel.indptr;
+            cr.indices[cr.count] = rel.indices;
+            cr.koff[cr.count] = L.koff[r];
+            cr.e0[cr.count] = L.e0[r];
+            ++cr.count;
+            rows += block->n_dst[rel.dst_type];
+        }
+        TRY_HIP(csc_build_all(cr, rows, L.csc_nnz, L.key_range, (int32_t *)(ws + L.off_ip),
+                              (int32_t *)(ws + L.off_csd), scratch, stream), "transpose");
     }
     for (int t = 0; t < L.T; ++t) {
         if (!(L.grad_mask >> t & 1u)) continue;
@@ -599,7 +626,7 @@ rgcn_status rgcn_block_backward_sparse(const rgcn_block *block, const rgcn_input
             const int t = rel.dst_type;
             TsumRel tr;
             tr.csc_indptr = (const int32_t *)(ws + L.off_csc_indptr[r]);
-            tr.csc_dst = (const int32_t *)(ws + L.off_csc_dst[r]);
+            tr.csc_dst = (const int32_t *)(ws + L.off_csd);
             tr.dms = (const float *)(scratch + L.off_dms[t]) + (int64_t)L.dms_rel[r] * L.d_in;
             tr.dms_ld = (int64_t)L.dms_nslots[t] * L.d_in;
             a.rel[a.nrel++] = tr;

@@ -98,10 +98,22 @@ hipError_t fwd_schedule(const FwdSlot *slots_dev, int nslots, int64_t n_seg, int
 hipError_t fwd_descriptors(const FwdSlot *slots_host, int nslots, const int32_t *order,
                            int64_t n_seg, const int64_t *mcat_off, const int64_t *mcat_ld,
                            int es, SegDesc *desc, hipStream_t s);
-hipError_t csc_build(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
-                     int64_t n_src, int64_t nnz, int32_t *csc_indptr, int32_t *csc_dst,
-                     void *temp, hipStream_t s);
-size_t csc_temp_bytes(int64_t nnz, int64_t n_src);
+// Combined transpose of several relations: one stable sort of all their edges by
+// key = koff_r + source row.  ip[key] (key in [0, key_range]) = position of the first edge
+// with that key; csd = destination rows in sorted order.  Relation r's transpose is
+// ip + koff_r (values are positions in csd).
+struct CscRels {
+    int32_t count;
+    int64_t row_base[kMaxRels];   // prefix over the relations' destination-row counts
+    const int32_t *indptr[kMaxRels];
+    const int32_t *indices[kMaxRels];
+    int64_t koff[kMaxRels];
+    int64_t e0[kMaxRels];         // position of the relation's first edge
+};
+hipError_t csc_build_all(const CscRels &rels, int64_t total_rows, int64_t nnz,
+                         int64_t key_range, int32_t *ip, int32_t *csd, void *temp,
+                         hipStream_t s);
+size_t csc_temp_bytes(int64_t nnz, int64_t key_range);
 struct BwdKeyRels {          // relations leaving one source type
     int32_t count;
     const int32_t *csc_indptr[kMaxRels];

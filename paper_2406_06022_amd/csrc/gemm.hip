@@ -16,13 +16,13 @@
 // step k is multiplied.
 //
 // The weight-side product reduces over the rows of both operands, so its tiles are
-// transposed on the way to LDS: each thread loads an 8 x 8 block (8 rows x 16 bytes,
-// row-contiguous global reads), transposes it in registers and writes eight 16-byte LDS
-// rows; with BK = 64 and a 144-byte pitch these writes are bank-conflict free.
+// transposed on the way to LDS: each thread loads half of an 8 x 8 block (4 rows x 16
+// bytes, row-contiguous global reads), transposes it in registers and writes eight 8-byte
+// LDS pieces; BK = 64 with a 144-byte pitch.
 //
 // bf16 mode: v_mfma_f32_16x16x32_bf16, fp32 accumulation.  The fp32 output gradient dY
-// enters the weight-side product rounded to bf16 (nearest even) and the input-side
-// product as a hi + lo pair of bf16 values.  fp32 mode: v_mfma_f32_16x16x4_f32 (full fp32).
+// enters both backward products as a hi + lo pair of bf16 values (hi = bf16(x), lo =
+// bf16(x - hi)), which carries ~16 significant bits.  fp32 mode: v_mfma_f32_16x16x4_f32.
 #include "common.h"
 
 #ifndef RGCN_GEMM_BK_BF16
@@ -55,6 +55,7 @@ using TileF32 = Tile<16, 4>;
 template <class TL>
 struct MmaBf16 {
     using T = TL;
+    static constexpr int TILES = 2;   // A, B
     __device__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
                                int wn, int lane) {
         const int r = lane & 15, q = lane >> 4;
@@ -79,8 +80,43 @@ struct MmaBf16 {
 // fp32: lane group q holds k = 4q..4q+3 of its row; MFMA step s uses element s, so the
 // four steps together cover k = 0..15 (the sum over k is taken in a different order, not
 // a different set).
+// B held as two bf16 tiles (hi, lo) of one fp32 operand, next to each other in LDS:
+// acc += A.B_hi + A.B_lo, fp32 accumulation.
+template <class TL>
+struct MmaBf16Split {
+    using T = TL;
+    static constexpr int TILES = 3;   // A, B_hi, B_lo
+    __device__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
+                               int wn, int lane) {
+        const int r = lane & 15, q = lane >> 4;
+        const char *Bl = Bs + TL::BYTES;
+#pragma unroll
+        for (int s = 0; s < TL::BK / 32; ++s) {
+            bf16x8 a[4], bh[4], bl[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int ao = (wm * 64 + i * 16 + r) * TL::PITCH + s * 64 + q * 16;
+                const int bo = (wn * 64 + i * 16 + r) * TL::PITCH + s * 64 + q * 16;
+                a[i] = *(const bf16x8 *)(As + ao);
+                bh[i] = *(const bf16x8 *)(Bs + bo);
+                bl[i] = *(const bf16x8 *)(Bl + bo);
+            }
+#pragma unroll
+            for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < 4; ++ni) {
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], bh[ni],
+                                                                          acc[mi][ni], 0, 0, 0);
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], bl[ni],
+                                                                          acc[mi][ni], 0, 0, 0);
+                }
+        }
+    }
+};
+
 struct MmaF32 {
     using T = TileF32;
+    static constexpr int TILES = 2;
     __device__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
                                int wn, int lane) {
         f32x4 a[4], b[4];
@@ -217,14 +253,14 @@ struct LoadRowsF32Split {
 };
 
 // Weight-side operands (bf16 mode, BK = 64): source [ksrc rows x cols] row-major; LDS row
-// = source column (128 from col0), LDS k = source row.  Half of the workgroup serves each
-// operand: waves 0-1 (HALF 0) or waves 2-3 (HALF 1).  Thread b of the half owns the 8 x 8
-// block (source rows k0 + 8*(b%8) .. +7, columns col0 + 8*(b/8) .. +7): eight row reads of
-// 16 bytes (bf16 source) or 32 bytes (fp32 source, rounded to bf16), a transpose in
-// registers, eight 16-byte LDS writes.  Lanes with consecutive b hit consecutive 16-byte
-// units of one LDS row or, across rows, units shifted by the odd pitch: no conflicts.
-template <int HALF, bool SRC_F32>
-struct LoadTransBlock {
+// = source column (128 from col0), LDS k = source row.  The tile is 8 x 16 blocks of 8 x 8;
+// thread t owns half a block: block b = t / 2 (source rows k0 + 8*(b%8) + 4*(t%2) .. +3,
+// columns col0 + 8*(b/8) .. +7).  Four row reads of 16 bytes (bf16 source) or 32 bytes
+// (fp32 source), a transpose in registers, eight 8-byte LDS writes.  SPLIT (fp32 source):
+// the values go to two bf16 tiles, hi = bf16(x) at lds and lo = bf16(x - hi) at
+// lds + tile bytes, for MmaBf16Split.
+template <bool SRC_F32, bool SPLIT>
+struct LoadTransHalf {
     using TL = TileBf16T;
     static constexpr int SES = SRC_F32 ? 4 : 2;
     static constexpr int NH = SRC_F32 ? 2 : 1;
@@ -234,24 +270,22 @@ struct LoadTransBlock {
     int64_t cols;
     struct State {
         int64_t col0;
-        int ib, cb;
-        bool active;
-        uint4 reg[8][NH];
+        int ib, cb, hb;
+        uint4 reg[4][NH];
     };
     __device__ void init(State &st, int64_t c0) const {
         st.col0 = c0;
-        const int b = (int)threadIdx.x - HALF * 128;
-        st.active = b >= 0 && b < 128;
+        const int b = (int)threadIdx.x >> 1;
+        st.hb = threadIdx.x & 1;
         st.ib = b & 7;
-        st.cb = (b >> 3) & 15;
+        st.cb = b >> 3;
     }
     __device__ void load(State &st, int64_t k0) const {
-        if (!st.active) return;
         const int64_t col = st.col0 + (int64_t)st.cb * 8;
         const bool colok = col < cols;
 #pragma unroll
-        for (int r = 0; r < 8; ++r) {
-            const int64_t i = k0 + st.ib * 8 + r;
+        for (int r = 0; r < 4; ++r) {
+            const int64_t i = k0 + st.ib * 8 + st.hb * 4 + r;
             const bool ok = colok && i < ksrc;
             const char *p = base + i * ld_bytes + col * SES;
 #pragma unroll
@@ -263,16 +297,19 @@ struct LoadTransBlock {
         return i == 0 ? u.x : i == 1 ? u.y : i == 2 ? u.z : u.w;
     }
     __device__ void store(const State &st, char *lds) const {
-        if (!st.active) return;
+        const int off = st.ib * 16 + st.hb * 8;
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
-            uint32_t w[4];
+            uint32_t w[2], wl[2];
 #pragma unroll
-            for (int p = 0; p < 4; ++p) {
+            for (int p = 0; p < 2; ++p) {
                 if constexpr (SRC_F32) {
-                    const uint32_t a0 = word(st.reg[2 * p][c >> 2], c & 3);
-                    const uint32_t a1 = word(st.reg[2 * p + 1][c >> 2], c & 3);
-                    w[p] = pack_bf16x2(__uint_as_float(a0), __uint_as_float(a1));
+                    const float x0 = __uint_as_float(word(st.reg[2 * p][c >> 2], c & 3));
+                    const float x1 = __uint_as_float(word(st.reg[2 * p + 1][c >> 2], c & 3));
+                    w[p] = pack_bf16x2(x0, x1);
+                    if constexpr (SPLIT)
+                        wl[p] = pack_bf16x2(x0 - __uint_as_float(w[p] << 16),
+                                            x1 - __uint_as_float(w[p] & 0xffff0000u));
                 } else {
                     const uint32_t a0 = word(st.reg[2 * p][0], c >> 1);
                     const uint32_t a1 = word(st.reg[2 * p + 1][0], c >> 1);
@@ -280,8 +317,9 @@ struct LoadTransBlock {
                                    : ((a0 & 0xffffu) | (a1 << 16));
                 }
             }
-            *(uint4 *)(lds + (st.cb * 8 + c) * TL::PITCH + st.ib * 16) =
-                make_uint4(w[0], w[1], w[2], w[3]);
+            char *dst = lds + (st.cb * 8 + c) * TL::PITCH + off;
+            *(uint2 *)dst = make_uint2(w[0], w[1]);
+            if constexpr (SPLIT) *(uint2 *)(dst + TL::BYTES) = make_uint2(wl[0], wl[1]);
         }
     }
 };
@@ -419,12 +457,16 @@ struct EpiPartial {
 // sends workgroup w to XCD w mod 8, and consecutive logical ids -- the tiles of one
 // split, and within a split the tiles sharing a row block of A -- land on the same XCD
 // and share its L2.
-template <class Mma, class LA, class LB, class Epi>
+// STAGES = 2: double-buffered LDS (one barrier per step); STAGES = 1: one buffer, the
+// next step's global loads still in flight in registers during the multiply.
+template <class Mma, class LA, class LB, class Epi, int STAGES>
 __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, const Epi epi,
                                                       int64_t K, int64_t tiles_m,
                                                       int64_t tiles_n, int64_t k_per_split) {
     using TL = typename Mma::T;
-    __shared__ __attribute__((aligned(16))) char lds[4 * TL::BYTES];
+    constexpr int STAGE_BYTES = Mma::TILES * TL::BYTES;
+    __shared__ __attribute__((aligned(16))) char lds[STAGES * STAGE_BYTES];
+    static_assert(STAGES * STAGE_BYTES >= 4 * 16 * kStagePitch * 4, "epilogue staging space");
     const int64_t logical = xcd_major_id(blockIdx.x, (int64_t)gridDim.x);
     const int64_t tiles = tiles_m * tiles_n;
     const int64_t split = logical / tiles;
@@ -452,8 +494,9 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, 
         lb.load(sb, kb);
     }
     for (int64_t it = 0; it < nk; ++it) {
-        char *As = lds + (it & 1) * 2 * TL::BYTES;
+        char *As = lds + (STAGES == 2 ? (it & 1) * STAGE_BYTES : 0);
         char *Bs = As + TL::BYTES;
+        if constexpr (STAGES == 1) __syncthreads();
         la.store(sa, As);
         lb.store(sb, Bs);
         __syncthreads();
@@ -488,12 +531,12 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, 
     }
 }
 
-template <class Mma, class LA, class LB, class Epi>
+template <class Mma, class LA, class LB, class Epi, int STAGES = 2>
 hipError_t launch_gemm(const LA &la, const LB &lb, const Epi &epi, int64_t M, int64_t N,
                        int64_t K, int64_t splits, int64_t k_per_split, hipStream_t s) {
     const int64_t tiles_m = cdiv(M, kTile), tiles_n = cdiv(N, kTile);
     if (tiles_m == 0 || tiles_n == 0 || splits == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_gemm<Mma, LA, LB, Epi>), dim3((unsigned)(tiles_m * tiles_n * splits)),
+    hipLaunchKernelGGL((k_gemm<Mma, LA, LB, Epi, STAGES>), dim3((unsigned)(tiles_m * tiles_n * splits)),
                        dim3(kThreads), 0, s, la, lb, epi, K, tiles_m, tiles_n, k_per_split);
     return hipGetLastError();
 }
@@ -605,9 +648,11 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
     }
     EpiPartial epi{partial, Kcat, d_out};
     if (bf) {
-        LoadTransBlock<0, false> la{(const char *)mcat, (int64_t)Kcat * 2, M, Kcat};
-        LoadTransBlock<1, true> lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
-        RGCN_HIP_TRY(launch_gemm<MmaBf16<TileBf16T>>(la, lb, epi, Kcat, d_out, M, splits, per, s));
+        // dY enters as hi + lo bf16 tiles (two MFMAs per operand pair, one load)
+        LoadTransHalf<false, false> la{(const char *)mcat, (int64_t)Kcat * 2, M, Kcat};
+        LoadTransHalf<true, true> lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
+        RGCN_HIP_TRY((launch_gemm<MmaBf16Split<TileBf16T>, decltype(la), decltype(lb), EpiPartial, 1>(
+            la, lb, epi, Kcat, d_out, M, splits, per, s)));
     } else {
         LoadTransF32 la{(const char *)mcat, (int64_t)Kcat * 4, M, Kcat};
         LoadTransF32 lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};

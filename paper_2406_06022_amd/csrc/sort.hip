@@ -208,11 +208,12 @@ struct BwdKey {
     }
 };
 
-// Radix pass: 8-bit digit of the key at `shift`.
+// Radix pass: the digit (key >> shift) & mask.
 struct RadixKey {
     const uint32_t *keys;
     int shift;
-    __device__ int operator()(int64_t i) const { return (int)((keys[i] >> shift) & 255u); }
+    uint32_t mask;
+    __device__ int operator()(int64_t i) const { return (int)((keys[i] >> shift) & mask); }
 };
 struct RadixPut {
     const uint32_t *kin;
@@ -225,25 +226,35 @@ struct RadixPut {
     }
 };
 
-// Destination row of every edge: vals[k] = i for k in [indptr[i], indptr[i+1]).
-__global__ __launch_bounds__(kThreads) void k_expand_rows(const int32_t *indptr, int64_t n_dst,
-                                                          int32_t *vals) {
-    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (i >= n_dst) return;
-    for (int32_t k = indptr[i]; k < indptr[i + 1]; ++k) vals[k] = (int32_t)i;
+// Edges of every relation taking part in the combined transpose, as (key, value) pairs:
+// key = koff_r + source row (disjoint key ranges per relation), value = destination row;
+// relation r's edges occupy positions [E_r, E_r + nnz_r) in input order.  Also counts the
+// edges per key.  One thread per destination row of the concatenated relations.
+__global__ __launch_bounds__(kThreads) void k_expand_edges(CscRels a, int64_t total_rows,
+                                                           uint32_t *keys, int32_t *vals,
+                                                           int32_t *cnt) {
+    const int64_t x = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (x >= total_rows) return;
+    int lo = 0, hi = a.count - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (a.row_base[mid] <= x) lo = mid; else hi = mid - 1;
+    }
+    const int64_t i = x - a.row_base[lo];
+    const int32_t *ip = a.indptr[lo];
+    const int32_t *ix = a.indices[lo];
+    const int64_t koff = a.koff[lo], e0 = a.e0[lo];
+    for (int64_t k = ip[i]; k < ip[i + 1]; ++k) {
+        const uint32_t key = (uint32_t)(koff + ix[k]);
+        keys[e0 + k] = key;
+        vals[e0 + k] = (int32_t)i;
+        atomicAdd(&cnt[key], 1);
+    }
 }
 
-// csc_indptr[j] = number of sorted keys < j (lower bound), j in [0, n_src].
-__global__ __launch_bounds__(kThreads) void k_lower_bounds(const uint32_t *sorted, int64_t nnz,
-                                                           int64_t n_src, int32_t *out) {
-    const int64_t j = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (j > n_src) return;
-    int64_t lo = 0, hi = nnz;
-    while (lo < hi) {
-        int64_t mid = (lo + hi) >> 1;
-        if ((int64_t)sorted[mid] < j) lo = mid + 1; else hi = mid;
-    }
-    out[j] = (int32_t)lo;
+__global__ __launch_bounds__(kThreads) void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < n) p[i] = v;
 }
 
 // Descriptor of the segment at schedule position p (see SegDesc).
@@ -353,43 +364,64 @@ hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, 
     return bucket_sort<kSchedBuckets, 6>(BwdKey{rels}, PutIndex{order}, n_rows, temp, s);
 }
 
-static int radix_passes(int64_t n_src) {
-    int bits = 0;
-    while (bits < 31 && (((int64_t)1 << bits) < n_src)) ++bits;  // keys < n_src <= 2^bits
-    return (bits + 7) / 8;
+// Digit plan of an LSD radix sort of keys < key_range: the fewest passes of at most 10
+// bits, digits as even as possible.
+static void radix_plan(int64_t key_range, int *passes, int *bits) {
+    int nb = 0;
+    while (nb < 32 && ((int64_t)1 << nb) < key_range) ++nb;  // keys < 2^nb
+    *passes = (nb + 9) / 10;
+    *bits = *passes ? (nb + *passes - 1) / *passes : 0;
 }
 
-size_t csc_temp_bytes(int64_t nnz, int64_t n_src) {
-    (void)n_src;
-    return 3 * align_up((size_t)nnz * 4 + 4, 256) + bucket_sort_temp_bytes(nnz, 256);
+size_t csc_temp_bytes(int64_t nnz, int64_t key_range) {
+    int passes, bits;
+    radix_plan(key_range, &passes, &bits);
+    const int nbk = bits <= 8 ? 256 : (1 << bits);
+    const size_t sort = bucket_sort_temp_bytes(nnz, nbk);
+    const size_t scan = scan_temp_bytes(key_range + 1);
+    return 3 * align_up((size_t)nnz * 4 + 4, 256) + (sort > scan ? sort : scan);
 }
 
-hipError_t csc_build(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
-                     int64_t n_src, int64_t nnz, int32_t *csc_indptr, int32_t *csc_dst,
-                     void *temp, hipStream_t s) {
+hipError_t csc_build_all(const CscRels &rels, int64_t total_rows, int64_t nnz,
+                         int64_t key_range, int32_t *ip, int32_t *csd, void *temp,
+                         hipStream_t s) {
+    // counts per key -> exclusive scan = offsets (ip[key_range] = nnz)
+    hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)cdiv(key_range + 1, kThreads)), dim3(kThreads), 0,
+                       s, ip, key_range + 1, 0);
+    RGCN_HIP_TRY(hipGetLastError());
+    int passes, bits;
+    radix_plan(key_range, &passes, &bits);
+    if (nnz == 0) passes = 0;
     const size_t arr = align_up((size_t)nnz * 4 + 4, 256);
     int32_t *tmp_vals = (int32_t *)temp;
     uint32_t *kb[2] = {(uint32_t *)((char *)temp + arr), (uint32_t *)((char *)temp + 2 * arr)};
     void *sort_tmp = (char *)temp + 3 * arr;
-    const int np = nnz > 0 ? radix_passes(n_src) : 0;
     int32_t *vb[2];
-    vb[np % 2] = csc_dst;
-    vb[(np + 1) % 2] = tmp_vals;
-    if (n_dst > 0 && nnz > 0) {
-        hipLaunchKernelGGL(k_expand_rows, dim3((unsigned)cdiv(n_dst, kThreads)), dim3(kThreads),
-                           0, s, indptr, n_dst, vb[0]);
+    vb[passes % 2] = csd;
+    vb[(passes + 1) % 2] = tmp_vals;
+    if (total_rows > 0 && nnz > 0) {
+        hipLaunchKernelGGL(k_expand_edges, dim3((unsigned)cdiv(total_rows, kThreads)),
+                           dim3(kThreads), 0, s, rels, total_rows, kb[1], vb[0], ip);
         RGCN_HIP_TRY(hipGetLastError());
     }
-    const uint32_t *keys = (const uint32_t *)indices;
-    for (int p = 0; p < np; ++p) {
-        RadixKey kf{keys, 8 * p};
-        RadixPut put{keys, vb[p % 2], kb[p % 2], vb[(p + 1) % 2]};
-        RGCN_HIP_TRY((bucket_sort<256, 8>(kf, put, nnz, sort_tmp, s)));
-        keys = kb[p % 2];
+    void *scan_tmp = (char *)temp + 3 * arr;  // free until the radix passes start
+    RGCN_HIP_TRY(exclusive_scan_i32(ip, ip, key_range + 1, scan_tmp, s));
+    const uint32_t *keys = kb[1];
+    const uint32_t mask = bits ? (uint32_t)((1u << bits) - 1u) : 0u;
+    for (int p = 0; p < passes; ++p) {
+        RadixKey kf{keys, bits * p, mask};
+        uint32_t *kout = kb[p % 2] == keys ? kb[(p + 1) % 2] : kb[p % 2];
+        RadixPut put{keys, vb[p % 2], kout, vb[(p + 1) % 2]};
+        if (bits <= 8) {
+            RGCN_HIP_TRY((bucket_sort<256, 8>(kf, put, nnz, sort_tmp, s)));
+        } else if (bits == 9) {
+            RGCN_HIP_TRY((bucket_sort<512, 9>(kf, put, nnz, sort_tmp, s)));
+        } else {
+            RGCN_HIP_TRY((bucket_sort<1024, 10>(kf, put, nnz, sort_tmp, s)));
+        }
+        keys = kout;
     }
-    hipLaunchKernelGGL(k_lower_bounds, dim3((unsigned)cdiv(n_src + 1, kThreads)), dim3(kThreads),
-                       0, s, keys, nnz, n_src, csc_indptr);
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 hipError_t fill_words(void *dst, const void *src_host, size_t bytes, hipStream_t s) {
