@@ -138,11 +138,16 @@ struct MmaF32 {
 };
 
 // ------------------------------------------------------------------ tile loaders
+// Row addressing policies.  row(r) always returns a readable row (out-of-range rows are
+// clamped to the last one) so tile loads need no branches; callers zero the values of
+// rows r >= rows with a select.
 struct PlainRows {
     const char *base;
     int64_t ld_bytes;
     int64_t rows;
-    __device__ const char *row(int64_t r) const { return r < rows ? base + r * ld_bytes : nullptr; }
+    __device__ const char *row(int64_t r) const {
+        return base + (r < rows ? r : rows - 1) * ld_bytes;
+    }
 };
 struct SlotRows {  // row n = (slot n / d_in, column c = n % d_in) of W_slot [d_in x d_out]
     const void *w[kMaxSlots];
@@ -150,11 +155,17 @@ struct SlotRows {  // row n = (slot n / d_in, column c = n % d_in) of W_slot [d_
     int32_t es_dout;   // bytes per W row (d_out * element size)
     int64_t rows;
     __device__ const char *row(int64_t r) const {
-        if (r >= rows) return nullptr;
-        const int64_t sl = r / d_in, c = r - sl * d_in;
+        const int64_t rr = r < rows ? r : rows - 1;
+        const int64_t sl = rr / d_in, c = rr - sl * d_in;
         return (const char *)w[sl] + c * es_dout;
     }
 };
+__device__ __forceinline__ uint4 select4(bool ok, const uint4 &v) {
+    return make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
+}
+__device__ __forceinline__ float4 select4f(bool ok, const float4 &v) {
+    return make_float4(ok ? v.x : 0.f, ok ? v.y : 0.f, ok ? v.z : 0.f, ok ? v.w : 0.f);
+}
 
 // K-contiguous rows whose element type is the LDS type.  WRAP: the product's K is twice
 // the row length and k >= row length re-reads the row (used with LoadRowsF32Split).
@@ -166,6 +177,8 @@ struct LoadRows {
     int64_t wrap_bytes;
     struct State {
         const char *rp[NCH];
+        bool rok[NCH];
+        bool ok[NCH];
         int lr[NCH], lq[NCH];
         uint4 reg[NCH];
     };
@@ -175,6 +188,7 @@ struct LoadRows {
             const int chunk = threadIdx.x + c * kThreads;
             st.lr[c] = chunk / TL::CPR;
             st.lq[c] = chunk % TL::CPR;
+            st.rok[c] = row0 + st.lr[c] < pol.rows;
             st.rp[c] = pol.row(row0 + st.lr[c]);
         }
     }
@@ -182,17 +196,15 @@ struct LoadRows {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             int64_t kb = k0 * TL::ES + st.lq[c] * 16;
-            if constexpr (WRAP) {
-                if (kb >= wrap_bytes) kb -= wrap_bytes;
-            }
-            st.reg[c] = (st.rp[c] && kb < kbytes) ? *(const uint4 *)(st.rp[c] + kb)
-                                                  : make_uint4(0, 0, 0, 0);
+            if constexpr (WRAP) kb = kb >= wrap_bytes ? kb - wrap_bytes : kb;
+            st.ok[c] = st.rok[c] && kb < kbytes;
+            st.reg[c] = *(const uint4 *)(st.rp[c] + (st.ok[c] ? kb : 0));
         }
     }
     __device__ void store(const State &st, char *lds) const {
 #pragma unroll
         for (int c = 0; c < NCH; ++c)
-            *(uint4 *)(lds + st.lr[c] * TL::PITCH + st.lq[c] * 16) = st.reg[c];
+            *(uint4 *)(lds + st.lr[c] * TL::PITCH + st.lq[c] * 16) = select4(st.ok[c], st.reg[c]);
     }
 };
 
@@ -209,6 +221,8 @@ struct LoadRowsF32Split {
     int64_t K;
     struct State {
         const char *rp[NCH];
+        bool rok[NCH];
+        bool ok[NCH];
         int lr[NCH], lq[NCH];
         bool low[NCH];
         float4 reg[NCH][2];
@@ -219,6 +233,7 @@ struct LoadRowsF32Split {
             const int chunk = threadIdx.x + c * kThreads;
             st.lr[c] = chunk / CPR;
             st.lq[c] = chunk % CPR;
+            st.rok[c] = row0 + st.lr[c] < pol.rows;
             st.rp[c] = pol.row(row0 + st.lr[c]);
         }
     }
@@ -227,13 +242,11 @@ struct LoadRowsF32Split {
         for (int c = 0; c < NCH; ++c) {
             int64_t k = k0 + st.lq[c] * 8;
             st.low[c] = k >= K;
-            if (st.low[c]) k -= K;
-            if (st.rp[c] && k < K) {
-                st.reg[c][0] = *(const float4 *)(st.rp[c] + k * 4);
-                st.reg[c][1] = *(const float4 *)(st.rp[c] + k * 4 + 16);
-            } else {
-                st.reg[c][0] = st.reg[c][1] = make_float4(0.f, 0.f, 0.f, 0.f);
-            }
+            k = st.low[c] ? k - K : k;
+            st.ok[c] = st.rok[c] && k < K;
+            const char *p = st.rp[c] + (st.ok[c] ? k * 4 : 0);
+            st.reg[c][0] = *(const float4 *)p;
+            st.reg[c][1] = *(const float4 *)(p + 16);
         }
     }
     __device__ static float part(float x, bool lo) { return lo ? x - round_bf16(x) : x; }
@@ -241,7 +254,7 @@ struct LoadRowsF32Split {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             const bool lo = st.low[c];
-            const float4 a = st.reg[c][0], b = st.reg[c][1];
+            const float4 a = select4f(st.ok[c], st.reg[c][0]), b = select4f(st.ok[c], st.reg[c][1]);
             uint4 w;
             w.x = pack_bf16x2(part(a.x, lo), part(a.y, lo));
             w.y = pack_bf16x2(part(a.z, lo), part(a.w, lo));
@@ -271,6 +284,7 @@ struct LoadTransHalf {
     struct State {
         int64_t col0;
         int ib, cb, hb;
+        bool ok[4];
         uint4 reg[4][NH];
     };
     __device__ void init(State &st, int64_t c0) const {
@@ -286,11 +300,10 @@ struct LoadTransHalf {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int64_t i = k0 + st.ib * 8 + st.hb * 4 + r;
-            const bool ok = colok && i < ksrc;
-            const char *p = base + i * ld_bytes + col * SES;
+            st.ok[r] = colok && i < ksrc;
+            const char *p = base + (st.ok[r] ? i * ld_bytes + col * SES : 0);
 #pragma unroll
-            for (int h = 0; h < NH; ++h)
-                st.reg[r][h] = ok ? *(const uint4 *)(p + h * 16) : make_uint4(0, 0, 0, 0);
+            for (int h = 0; h < NH; ++h) st.reg[r][h] = *(const uint4 *)(p + h * 16);
         }
     }
     __device__ static uint32_t word(const uint4 &u, int i) {
@@ -298,21 +311,26 @@ struct LoadTransHalf {
     }
     __device__ void store(const State &st, char *lds) const {
         const int off = st.ib * 16 + st.hb * 8;
+        uint4 rg[4][NH];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int h = 0; h < NH; ++h) rg[r][h] = select4(st.ok[r], st.reg[r][h]);
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
             uint32_t w[2], wl[2];
 #pragma unroll
             for (int p = 0; p < 2; ++p) {
                 if constexpr (SRC_F32) {
-                    const float x0 = __uint_as_float(word(st.reg[2 * p][c >> 2], c & 3));
-                    const float x1 = __uint_as_float(word(st.reg[2 * p + 1][c >> 2], c & 3));
+                    const float x0 = __uint_as_float(word(rg[2 * p][c >> 2], c & 3));
+                    const float x1 = __uint_as_float(word(rg[2 * p + 1][c >> 2], c & 3));
                     w[p] = pack_bf16x2(x0, x1);
                     if constexpr (SPLIT)
                         wl[p] = pack_bf16x2(x0 - __uint_as_float(w[p] << 16),
                                             x1 - __uint_as_float(w[p] & 0xffff0000u));
                 } else {
-                    const uint32_t a0 = word(st.reg[2 * p][0], c >> 1);
-                    const uint32_t a1 = word(st.reg[2 * p + 1][0], c >> 1);
+                    const uint32_t a0 = word(rg[2 * p][0], c >> 1);
+                    const uint32_t a1 = word(rg[2 * p + 1][0], c >> 1);
                     w[p] = (c & 1) ? ((a0 >> 16) | (a1 & 0xffff0000u))
                                    : ((a0 & 0xffffu) | (a1 << 16));
                 }
@@ -335,6 +353,7 @@ struct LoadTransF32 {
     struct State {
         int64_t col0;
         int ik[2], cq[2];
+        bool ok[2];
         uint4 reg[2];
     };
     __device__ void init(State &st, int64_t c0) const {
@@ -351,14 +370,15 @@ struct LoadTransF32 {
         for (int c = 0; c < 2; ++c) {
             const int64_t i = k0 + st.ik[c];
             const int64_t col = st.col0 + (int64_t)st.cq[c] * 4;
-            st.reg[c] = (i < ksrc && col < cols) ? *(const uint4 *)(base + i * ld_bytes + col * 4)
-                                                 : make_uint4(0, 0, 0, 0);
+            st.ok[c] = i < ksrc && col < cols;
+            st.reg[c] = *(const uint4 *)(base + (st.ok[c] ? i * ld_bytes + col * 4 : 0));
         }
     }
     __device__ void store(const State &st, char *lds) const {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-            const uint32_t w[4] = {st.reg[c].x, st.reg[c].y, st.reg[c].z, st.reg[c].w};
+            const uint4 v = select4(st.ok[c], st.reg[c]);
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
             for (int e = 0; e < 4; ++e)
                 *(uint32_t *)(lds + (st.cq[c] * 4 + e) * TL::PITCH + st.ik[c] * 4) = w[e];
@@ -377,6 +397,29 @@ struct EpiForward {
     int32_t relu;
     __device__ void operator()(int64_t m, int64_t n0, const float *v, int64_t) const {
         if (m >= M) return;
+        // N is a multiple of 4: each group of 4 columns is either whole or absent.  The
+        // bias loads are issued together (clamped, then zeroed) before any is used.
+        float bq[4][4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t n = n0 + 4 * q;
+            const bool ok = bias != nullptr && n < N;
+            if constexpr (OUT_BF16) {
+                const uint2 w = *(const uint2 *)((const uint16_t *)(ok ? bias : (const void *)y) +
+                                                 (ok ? n : 0));
+                bq[q][0] = ok ? bf16_lo(w.x) : 0.f;
+                bq[q][1] = ok ? bf16_hi(w.x) : 0.f;
+                bq[q][2] = ok ? bf16_lo(w.y) : 0.f;
+                bq[q][3] = ok ? bf16_hi(w.y) : 0.f;
+            } else {
+                const float4 w = *(const float4 *)((const float *)(ok ? bias : (const void *)y) +
+                                                   (ok ? n : 0));
+                bq[q][0] = ok ? w.x : 0.f;
+                bq[q][1] = ok ? w.y : 0.f;
+                bq[q][2] = ok ? w.z : 0.f;
+                bq[q][3] = ok ? w.w : 0.f;
+            }
+        }
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int64_t n = n0 + 4 * q;
@@ -384,14 +427,7 @@ struct EpiForward {
             float r[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                float b = 0.f;
-                if (bias) {
-                    if constexpr (OUT_BF16)
-                        b = __uint_as_float((uint32_t)((const uint16_t *)bias)[n + e] << 16);
-                    else
-                        b = ((const float *)bias)[n + e];
-                }
-                r[e] = v[4 * q + e] + b;
+                r[e] = v[4 * q + e] + bq[q][e];
                 if (relu) r[e] = r[e] > 0.f ? r[e] : 0.f;
             }
             if constexpr (OUT_BF16) {
@@ -457,9 +493,10 @@ struct EpiPartial {
 // sends workgroup w to XCD w mod 8, and consecutive logical ids -- the tiles of one
 // split, and within a split the tiles sharing a row block of A -- land on the same XCD
 // and share its L2.
-// STAGES = 2: double-buffered LDS (one barrier per step); STAGES = 1: one buffer, the
-// next step's global loads still in flight in registers during the multiply.
-template <class Mma, class LA, class LB, class Epi, int STAGES>
+// STAGES = 2: double-buffered LDS (one barrier per step); STAGES = 1: one buffer.
+// R register stages: the global loads of step k + R are issued right after step k's tiles
+// reach LDS, so R multiplies overlap each load's latency.
+template <class Mma, class LA, class LB, class Epi, int STAGES, int R>
 __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, const Epi epi,
                                                       int64_t K, int64_t tiles_m,
                                                       int64_t tiles_n, int64_t k_per_split) {
@@ -478,10 +515,13 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    typename LA::State sa;
-    typename LB::State sb;
-    la.init(sa, m0);
-    lb.init(sb, n0);
+    typename LA::State sa[R];
+    typename LB::State sb[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        la.init(sa[r], m0);
+        lb.init(sb[r], n0);
+    }
     f32x4 acc[4][4];
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
@@ -489,22 +529,30 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, 
         for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const int64_t nk = ke > kb ? cdiv(ke - kb, TL::BK) : 0;
-    if (nk > 0) {
-        la.load(sa, kb);
-        lb.load(sb, kb);
-    }
-    for (int64_t it = 0; it < nk; ++it) {
-        char *As = lds + (STAGES == 2 ? (it & 1) * STAGE_BYTES : 0);
-        char *Bs = As + TL::BYTES;
-        if constexpr (STAGES == 1) __syncthreads();
-        la.store(sa, As);
-        lb.store(sb, Bs);
-        __syncthreads();
-        if (it + 1 < nk) {
-            la.load(sa, kb + (it + 1) * TL::BK);
-            lb.load(sb, kb + (it + 1) * TL::BK);
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        if (r < nk) {
+            la.load(sa[r], kb + r * TL::BK);
+            lb.load(sb[r], kb + r * TL::BK);
         }
-        Mma::run(As, Bs, acc, wm, wn, lane);
+    for (int64_t it0 = 0; it0 < nk; it0 += R) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int64_t it = it0 + r;
+            if (it < nk) {
+                char *As = lds + (STAGES == 2 ? (it & 1) * STAGE_BYTES : 0);
+                char *Bs = As + TL::BYTES;
+                if constexpr (STAGES == 1) __syncthreads();
+                la.store(sa[r], As);
+                lb.store(sb[r], Bs);
+                __syncthreads();
+                if (it + R < nk) {
+                    la.load(sa[r], kb + (it + R) * TL::BK);
+                    lb.load(sb[r], kb + (it + R) * TL::BK);
+                }
+                Mma::run(As, Bs, acc, wm, wn, lane);
+            }
+        }
     }
     __syncthreads();
 
@@ -531,12 +579,19 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, 
     }
 }
 
-template <class Mma, class LA, class LB, class Epi, int STAGES = 2>
+#ifndef RGCN_GEMM_RSTAGES
+#define RGCN_GEMM_RSTAGES 2
+#endif
+#ifndef RGCN_GEMM_RSTAGES_DW
+#define RGCN_GEMM_RSTAGES_DW 1
+#endif
+
+template <class Mma, class LA, class LB, class Epi, int STAGES = 2, int R = RGCN_GEMM_RSTAGES>
 hipError_t launch_gemm(const LA &la, const LB &lb, const Epi &epi, int64_t M, int64_t N,
                        int64_t K, int64_t splits, int64_t k_per_split, hipStream_t s) {
     const int64_t tiles_m = cdiv(M, kTile), tiles_n = cdiv(N, kTile);
     if (tiles_m == 0 || tiles_n == 0 || splits == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_gemm<Mma, LA, LB, Epi, STAGES>), dim3((unsigned)(tiles_m * tiles_n * splits)),
+    hipLaunchKernelGGL((k_gemm<Mma, LA, LB, Epi, STAGES, R>), dim3((unsigned)(tiles_m * tiles_n * splits)),
                        dim3(kThreads), 0, s, la, lb, epi, K, tiles_m, tiles_n, k_per_split);
     return hipGetLastError();
 }
@@ -651,8 +706,8 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
         // dY enters as hi + lo bf16 tiles (two MFMAs per operand pair, one load)
         LoadTransHalf<false, false> la{(const char *)mcat, (int64_t)Kcat * 2, M, Kcat};
         LoadTransHalf<true, true> lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
-        RGCN_HIP_TRY((launch_gemm<MmaBf16Split<TileBf16T>, decltype(la), decltype(lb), EpiPartial, 1>(
-            la, lb, epi, Kcat, d_out, M, splits, per, s)));
+        RGCN_HIP_TRY((launch_gemm<MmaBf16Split<TileBf16T>, decltype(la), decltype(lb), EpiPartial, 1,
+                                  RGCN_GEMM_RSTAGES_DW>(la, lb, epi, Kcat, d_out, M, splits, per, s)));
     } else {
         LoadTransF32 la{(const char *)mcat, (int64_t)Kcat * 4, M, Kcat};
         LoadTransF32 lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
