@@ -19,8 +19,11 @@ launches inside the timed steps), and the CPU oracle timed on a bounded sample.
 from __future__ import annotations
 
 import argparse
+import csv
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -33,8 +36,55 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
 METRIC = "aggregated edges/sec and ms per RGCN block fwd+bwd; % of HBM roofline"
 
 
+# Files each timed kernel and its workload come from: the HBM-traffic figures recorded
+# under profiles/ hold a digest of these files and count only while it still matches.
+_COMMON_INPUTS = ["paper_2406_06022_amd/csrc/common.h", "include/rgcn.h",
+                  "paper_2406_06022_amd/build.py", "paper_2406_06022_amd/synth.py"]
+KERNEL_SOURCES = {
+    "k_gather_mean": ["paper_2406_06022_amd/csrc/aggregate.hip"] + _COMMON_INPUTS,
+    "k_transpose_sum": ["paper_2406_06022_amd/csrc/aggregate.hip"] + _COMMON_INPUTS,
+}
+# Plain copy of known size run after the timed steps (an fp32 negation of a 1 GiB buffer:
+# one read and one write of every byte per dispatch).  Its time gives the box's attainable
+# streaming bandwidth; under rocprofv3 --pmc its HBM counters calibrate those of the timed
+# kernels.
+COPY_KERNEL = "neg_kernel"
+COPY_BYTES = 1 << 30
+
+
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def source_digest(kernel: str) -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(rel.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def profile_path(kernel: str, workload: str, what: str) -> str:
+    return os.path.join(ROOT, "profiles", f"{kernel}.{workload}.{what}.md")
+
+
+def read_traffic(kernel: str, workload: str, position: int):
+    """HBM bytes of one launch from the committed counter summary, or None when there is
+    none for this kernel, workload and launch position, or the kernel's sources changed
+    since the counters were taken."""
+    path = profile_path(kernel, workload, "hbm")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            m = re.match(r"^- (\w+): (\S+)", line)
+            if m:
+                kv[m.group(1)] = m.group(2)
+    if kv.get("source_digest") != source_digest(kernel):
+        return None
+    key = f"traffic_bytes_pos{position}"
+    return float(kv[key]) if key in kv else None
 
 
 def build_stack(index: int, device: str):
@@ -157,6 +207,104 @@ def cpu_baseline(spec, mb, tables, ids, weights, budget_s: float):
     return result
 
 
+def _short_name(name: str) -> str:
+    name = re.sub(r"^void ", "", name)
+    name = name.replace("(anonymous namespace)::", "")
+    name = re.sub(r"\(.*$", "", name)
+    name = name.replace("rgcn::", "")
+    return name[:90]
+
+
+def _dispatches(path: str, kernel_re: str, value_col=None, counter=None):
+    """[(dispatch id, short name, value)] of the matching kernels, in dispatch order."""
+    out = []
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            if not re.search(kernel_re, r["Kernel_Name"]):
+                continue
+            if counter is not None and r["Counter_Name"] != counter:
+                continue
+            if value_col is None:
+                v = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+            else:
+                v = float(r[value_col])
+            out.append((int(r["Dispatch_Id"]), _short_name(r["Kernel_Name"]), v))
+    out.sort()
+    return out
+
+
+def _by_position(rows, per_step: int, skip_steps: int):
+    rows = rows[skip_steps * per_step:]
+    if per_step <= 0 or len(rows) % per_step:
+        raise SystemExit(f"{len(rows)} dispatches are not a whole number of steps of {per_step}")
+    pos = []
+    for p in range(per_step):
+        vals = [v for i, (_, _, v) in enumerate(rows) if i % per_step == p]
+        pos.append((sum(vals) / len(vals), len(vals), rows[p][1]))
+    return pos
+
+
+def summarize_trace(args) -> str:
+    """Per-kernel time of a kernel-trace run, and the launches of --kernel by position."""
+    per, other = {}, [0, 0.0]
+    with open(args.summarize_trace, newline="") as f:
+        for r in csv.DictReader(f):
+            d = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+            a = per.setdefault(_short_name(r["Kernel_Name"]), [0, 0.0]) \
+                if "rgcn::" in r["Kernel_Name"] else other
+            a[0] += 1
+            a[1] += d
+    steps = args.steps + args.warmup
+    lines = [f"# {args.kernel}: kernel trace", "", "Command:", "", "```", args.command, "```", "",
+             f"Launches of {args.kernel} by position within a step ({args.launches_per_step} "
+             f"per step, first {args.warmup} steps skipped):", ""]
+    for p, (avg, n, name) in enumerate(_by_position(
+            _dispatches(args.summarize_trace, args.kernel), args.launches_per_step, args.warmup)):
+        lines.append(f"- avg_us_pos{p}: {avg / 1e3:.1f} ({n} launches, {name})")
+    ours = sum(v[1] for v in per.values())
+    lines += ["", f"Kernels of the library over the run's {steps} steps (warmup and timed): "
+              f"{ours / 1e6:.3f} ms, {ours / steps / 1e6:.3f} ms per step.  Other kernels "
+              f"(workload set-up: sampling, tables, weights): {other[0]} launches, "
+              f"{other[1] / 1e6:.3f} ms.", "",
+              "| kernel | calls | total ms | avg us | ms per step |", "|---|---:|---:|---:|---:|"]
+    for name, (n, tot) in sorted(per.items(), key=lambda x: -x[1][1]):
+        lines.append(f"| `{name}` | {n} | {tot / 1e6:.3f} | {tot / n / 1e3:.1f} | "
+                     f"{tot / steps / 1e6:.3f} |")
+    return "\n".join(lines) + "\n"
+
+
+def summarize_pmc(args) -> str:
+    """Per-launch HBM traffic of --kernel from FETCH_SIZE and WRITE_SIZE runs, each scaled
+    by what the same counter reads for the plain copy of --copy-probe-mib MiB."""
+    fetch_csv, write_csv = args.summarize_pmc
+    copy_bytes = float(COPY_BYTES)
+    cf = [v for _, _, v in _dispatches(fetch_csv, COPY_KERNEL, "Counter_Value", "FETCH_SIZE")]
+    cw = [v for _, _, v in _dispatches(write_csv, COPY_KERNEL, "Counter_Value", "WRITE_SIZE")]
+    if not cf or not cw:
+        raise SystemExit("no calibration copy dispatches in the counter files")
+    f_scale = copy_bytes / (sum(cf) / len(cf) * 1024.0)
+    w_scale = copy_bytes / (sum(cw) / len(cw) * 1024.0)
+    fpos = _by_position(_dispatches(fetch_csv, args.kernel, "Counter_Value", "FETCH_SIZE"),
+                        args.launches_per_step, args.warmup)
+    wpos = _by_position(_dispatches(write_csv, args.kernel, "Counter_Value", "WRITE_SIZE"),
+                        args.launches_per_step, args.warmup)
+    lines = [f"# {args.kernel}: HBM traffic per launch", "", "Commands:", "", "```",
+             args.command, "```", "",
+             f"Calibration: a plain copy of {COPY_BYTES >> 20} MiB (fp32 negation, kernel "
+             f"matching '{COPY_KERNEL}', {len(cf)} dispatches) reads "
+             f"FETCH_SIZE {sum(cf) / len(cf):.0f} KiB and WRITE_SIZE {sum(cw) / len(cw):.0f} KiB; "
+             f"scale factors {f_scale:.3f} (fetch) and {w_scale:.3f} (write).", "",
+             f"- source_digest: {source_digest(args.kernel)}",
+             f"- fetch_scale: {f_scale:.4f}",
+             f"- write_scale: {w_scale:.4f}"]
+    for p, ((fk, n, name), (wk, _, _)) in enumerate(zip(fpos, wpos)):
+        tb = fk * 1024.0 * f_scale + wk * 1024.0 * w_scale
+        lines.append(f"- traffic_bytes_pos{p}: {tb:.0f}")
+        lines.append(f"  - FETCH_SIZE {fk:.0f} KiB, WRITE_SIZE {wk:.0f} KiB per launch "
+                     f"({n} launches, {name})")
+    return "\n".join(lines) + "\n"
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -165,7 +313,22 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=4, help="workload index 0..4 (default 4)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="reduce two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, "
+                         "WRITE_SIZE) into the per-launch HBM traffic summary and exit")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
+                    help="reduce a rocprofv3 kernel_trace.csv into a per-kernel summary and exit")
+    ap.add_argument("--kernel", default="k_gather_mean")
+    ap.add_argument("--launches-per-step", type=int, default=3,
+                    help="launches of --kernel per step (summaries split them by position)")
+    ap.add_argument("--command", default="", help="command line recorded in a summary")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        print(summarize_pmc(args), end="")
+        return 0
+    if args.summarize_trace:
+        print(summarize_trace(args), end="")
+        return 0
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for --gpus {args.gpus}); the multi-GPU "
               "sharding of this path is a design note, not an implementation.", file=sys.stderr)
@@ -229,12 +392,40 @@ def main() -> int:
         rooflines[f"{s}[{l}]"] = {"ms": round(t_ms, 4), "bytes": byts, "GB/s": round(gbs, 1),
                                   "frac": round(gbs / HBM_PEAK_GBS, 4)}
     dom = rooflines[f"{dom_stage}[{dom_layer}]"]
+    # launch position of the dominant stage within a step's launches of its kernel: the
+    # gather runs once per block, input side first; the transposed sum once per requested
+    # source type, output side first
+    if dom_stage == "aggregate":
+        position = dom_layer
+    else:
+        position = 0
+        for l in reversed(range(stack.L)):
+            db = stack.blocks[l]
+            n = sum(1 for t in range(db.num_types)
+                    if db.grad_src_types >> t & 1 and db.n_src[t] > 0)
+            if l == dom_layer:
+                break
+            position += n
+    traffic = read_traffic(kernel_name, spec.name, position)
     mfma = {}
     for l in range(stack.L):
         fl = transform_flops(spec, mb.blocks[l], l)
         tf = fl / (avg[("transform", l)] * 1e-3) / 1e12
         mfma[f"transform[{l}]"] = {"ms": round(avg[("transform", l)], 4), "TFLOP/s": round(tf, 1),
                                    "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)}
+
+    # attainable streaming bandwidth of this machine: a plain 1 GiB fp32 copy (read + write)
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.neg(src, out=dst)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for _ in range(5):
+        torch.neg(src, out=dst)
+    c1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 2.0 * src.numel() * 4 * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del src, dst
 
     cpu = None
     if args.cpu_budget > 0:
@@ -268,8 +459,9 @@ def main() -> int:
         "stage_ms": {f"{s}[{l}]": round(v, 4) for (s, l), v in sorted(avg.items(), key=lambda x: (x[0][1], x[0][0]))},
         "roofline": {"bound": "hbm", "kernel": kernel_name, "stage": f"{dom_stage}[{dom_layer}]",
                      "achieved": dom["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": dom["frac"], "traffic": None},
+                     "frac": dom["frac"], "traffic": traffic, "launch_position": position},
         "hbm_kernels": rooflines,
+        "copy_probe_GBs": round(copy_gbs, 1),
         "mfma_transforms": mfma,
         "cpu_baseline": cpu,
     }

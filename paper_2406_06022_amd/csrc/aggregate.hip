@@ -41,6 +41,20 @@ __device__ __forceinline__ void acc_chunk(float *acc, const uint4 &v) {
     }
 }
 
+// A pointer known to address global memory, as a global-address-space pointer (loads
+// through it are global loads rather than flat loads).
+template <class T>
+__device__ __forceinline__ const __attribute__((address_space(1))) T *gbl(const T *p) {
+    return (const __attribute__((address_space(1))) T *)p;
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// 16-byte global load
+__device__ __forceinline__ uint4 ld16(const char *p) {
+    const u32x4 v = *gbl((const u32x4 *)p);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // Broadcast a 64-bit value from absolute lane `src` of the wave.
 __device__ __forceinline__ int64_t shfl64(int64_t v, int src) {
     const int lo = __shfl((int)(uint32_t)v, src, 64);
@@ -51,18 +65,40 @@ __device__ __forceinline__ int64_t shfl64(int64_t v, int src) {
 // Forward segments in schedule order (heaviest first), one group of G lanes per segment,
 // persistent: group q handles segments q, q + ngroups, ...  A segment is the self-loop
 // row of a destination (copied) or the sampled in-edges of a destination row in one
-// relation (mean of the gathered source rows; 0 if none).  Lane lg of the group fetches
-// edge lg's source index and global row id, the group walks the edges broadcasting row
-// addresses, U row loads in flight.  Software pipeline, two round trips per segment:
-//   {row ids of this segment, descriptor of the next}  then
-//   {rows of this segment, source indices of the next}.
+// relation (mean of the gathered source rows; 0 if none).
+//
+// The address of a gathered row takes three dependent loads: the segment descriptor, the
+// source index of the edge, the global row id of that source.  They are software-
+// pipelined over the group's successive segments, so that while the rows of segment i
+// are in flight the row ids of segment i+1, the source indices of segment i+2 and the
+// descriptor of segment i+3 are too.  Lane lg holds edges lg, lg+G, ... (EPL of them) of
+// each segment in the pipeline; edges past EPL*G (degrees above the pipelined width)
+// are resolved in place.  Row byte offsets are published to the group's LDS slots and
+// read back as broadcasts while U rows per lane are in flight.
 // The sum runs in ascending edge position; one division by the degree.
 struct GatherTabs {
     TypeInput in[kMaxTypes];
 };
 
-template <bool BF16, int CPL>
-__global__ __launch_bounds__(kThreads) void k_gather_mean(const SegDesc *__restrict__ desc,
+// Read (never written) by loads whose value is not needed; zero-initialised.
+__device__ int64_t g_zero[2];
+
+#ifndef RGCN_GATHER_U1
+#define RGCN_GATHER_U1 4
+#endif
+
+template <int CPL>
+struct GatherU {
+    static constexpr int U = CPL == 1 ? RGCN_GATHER_U1 : (CPL == 2 ? 8 : 4);
+};
+
+#ifndef RGCN_GATHER_MIN_WAVES
+#define RGCN_GATHER_MIN_WAVES 1
+#endif
+
+template <bool BF16, int CPL, int EPL>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(RGCN_GATHER_MIN_WAVES)))
+void k_gather_mean(const SegDesc *__restrict__ desc,
                                                           int64_t n_seg,
                                                           const FwdSlot *__restrict__ slots,
                                                           int nslots, GatherTabs tabs,
@@ -70,47 +106,86 @@ __global__ __launch_bounds__(kThreads) void k_gather_mean(const SegDesc *__restr
                                                           int chunks) {
     constexpr int VEC = BF16 ? 8 : 4;
     constexpr int ES = BF16 ? 2 : 4;
-    constexpr int U = CPL == 1 ? 8 : 4;  // row loads in flight per lane
+    constexpr int U = GatherU<CPL>::U;
+    constexpr int W = kThreads / 64;
     __shared__ const int32_t *s_idx[kMaxSlots];
     __shared__ int32_t s_src[kMaxSlots];
+    __shared__ TypeInput s_tab[kMaxTypes];
+    __shared__ int64_t s_off[W][64 * EPL];
     for (int i = threadIdx.x; i < nslots; i += kThreads) {
         s_idx[i] = slots[i].indices;
         s_src[i] = slots[i].src_type;
     }
+    for (int i = threadIdx.x; i < kMaxTypes; i += kThreads) s_tab[i] = tabs.in[i];
     __syncthreads();
 
-    const int lane = threadIdx.x & 63;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int gi = lane / G;
     const int lg = lane - gi * G;
-    const int g0 = gi * G;
     if (gi >= gpw) return;
-    const int64_t stride = (int64_t)gridDim.x * (kThreads / 64) * gpw;
-    int64_t sg = ((int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)) * gpw + gi;
+    int64_t *goff = &s_off[wave][gi * G * EPL];
+    const int64_t stride = (int64_t)gridDim.x * W * gpw;
+    int64_t sg = ((int64_t)blockIdx.x * W + wave) * gpw + gi;
     if (sg >= n_seg) return;
+    // Loads that a lane does not need read a zero word instead, so that every load is
+    // unconditional (no branch, no wait at a join) and its value enters by an addition.
+    // Pointers read back from LDS are re-qualified as global so the loads are global (not
+    // flat) loads.
+    const char *zero = (const char *)g_zero;
 
+    // descriptor of segment s (degree 0 past the end)
+    auto load_desc = [&](int64_t s) -> SegDesc {
+        SegDesc d = desc[s < n_seg ? s : n_seg - 1];
+        d.deg = s < n_seg ? d.deg : 0;
+        return d;
+    };
     // source index of edge e of segment d (self-loop slot: the row itself), -1 past the end
-    auto edge_src = [&](const SegDesc &d, int e) -> int64_t {
-        if (e >= d.deg) return -1;
+    auto edge_src = [&](const SegDesc &d, int e) -> int32_t {
         const int32_t *ix = s_idx[(d.info >> 8) & 0xff];
-        return ix ? (int64_t)ix[d.k0 + e] : (int64_t)d.k0 + e;
+        const bool ok = e < d.deg;
+        const bool has = ix != nullptr;
+        const int32_t *p = (ok && has) ? ix + d.k0 + e : (const int32_t *)zero;
+        const int32_t v = *gbl(p);
+        return v + (!ok ? -1 : (has ? 0 : d.k0 + e));
     };
-    // byte offset of that source row in its table
-    auto row_off = [&](const SegDesc &d, int64_t j) -> int64_t {
-        if (j < 0) return 0;
-        const TypeInput &in = tabs.in[s_src[(d.info >> 8) & 0xff]];
-        const int64_t grow = in.row_ids ? in.row_ids[j] : j;
-        return grow * in.ld * ES;
+    // byte offset of that source row in its table (0 for -1)
+    auto row_off = [&](const SegDesc &d, int32_t j) -> int64_t {
+        const int t = s_src[(d.info >> 8) & 0xff];
+        const int64_t *rid = s_tab[t].row_ids;
+        const int64_t ldb = s_tab[t].ld * ES;
+        const bool look = j >= 0 && rid != nullptr;
+        const int64_t *p = look ? rid + j : (const int64_t *)zero;
+        const int64_t v = *gbl(p);
+        return (v + ((j < 0 || rid != nullptr) ? 0 : j)) * ldb;
     };
 
-    SegDesc d = desc[sg];
-    int64_t j = edge_src(d, lg);
+    // pipeline prologue
+    SegDesc d = load_desc(sg);
+    SegDesc dn = load_desc(sg + stride);
+    SegDesc dnn = load_desc(sg + 2 * stride);
+    int64_t off[EPL];
+    int32_t jn[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) off[e] = row_off(d, edge_src(d, lg + e * G));
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) jn[e] = edge_src(dn, lg + e * G);
+
     while (true) {
-        const int64_t off0 = row_off(d, j);
-        const int64_t sn = sg + stride;
-        SegDesc dn = d;
-        if (sn < n_seg) dn = desc[sn];
-        const char *src = (const char *)tabs.in[s_src[(d.info >> 8) & 0xff]].base;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) goff[e * G + lg] = off[e];
+        __builtin_amdgcn_wave_barrier();
         const int deg = d.deg;
+        const int n1 = deg < EPL * G ? deg : EPL * G;
+        const char *src = (const char *)s_tab[s_src[(d.info >> 8) & 0xff]].base;
+
+        // later stages of the pipeline, issued before this segment's rows are consumed
+        int64_t offn[EPL];
+        int32_t jnn[EPL];
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) offn[e] = row_off(dn, jn[e]);
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) jnn[e] = edge_src(dnn, lg + e * G);
+        const SegDesc dnnn = load_desc(sg + 3 * stride);
 
         float acc[CPL][VEC];
 #pragma unroll
@@ -118,36 +193,39 @@ __global__ __launch_bounds__(kThreads) void k_gather_mean(const SegDesc *__restr
 #pragma unroll
             for (int e = 0; e < VEC; ++e) acc[p][e] = 0.f;
 
-        int64_t jn = -1;
-        bool next_issued = false;
-        for (int kc = 0; kc < deg; kc += G) {
-            const int64_t off = kc == 0 ? off0 : row_off(d, edge_src(d, kc + lg));
-            const int n = (deg - kc) < G ? (deg - kc) : G;
+        // edges [0, n) of the offsets in goff: U rows per lane in flight; a batch's unused
+        // slots re-read the last row (a cache hit) and are dropped
+        auto rows = [&](int n) {
             for (int q = 0; q < n; q += U) {
                 int64_t o[U];
 #pragma unroll
-                for (int u = 0; u < U; ++u) o[u] = shfl64(off, g0 + ((q + u) < n ? q + u : 0));
+                for (int u = 0; u < U; ++u) o[u] = goff[q + u < n ? q + u : n - 1];
                 uint4 v[U][CPL];
 #pragma unroll
                 for (int u = 0; u < U; ++u)
 #pragma unroll
                     for (int p = 0; p < CPL; ++p) {
-                        const int c = lg + p * G;
-                        v[u][p] = (q + u < n && c < chunks)
-                                      ? *(const uint4 *)(src + o[u] + (int64_t)c * 16)
-                                      : make_uint4(0, 0, 0, 0);
+                        const int c = lg + p * G < chunks ? lg + p * G : chunks - 1;
+                        v[u][p] = ld16(src + o[u] + (int64_t)c * 16);
                     }
-                if (!next_issued) {  // next segment's source indices, alongside these rows
-                    next_issued = true;
-                    if (sn < n_seg) jn = edge_src(dn, lg);
-                }
 #pragma unroll
                 for (int u = 0; u < U; ++u)
 #pragma unroll
-                    for (int p = 0; p < CPL; ++p) acc_chunk<BF16>(acc[p], v[u][p]);
+                    for (int p = 0; p < CPL; ++p) {
+                        const bool ok = q + u < n && lg + p * G < chunks;
+                        const uint4 x = v[u][p];
+                        acc_chunk<BF16>(acc[p], ok ? x : make_uint4(0, 0, 0, 0));
+                    }
             }
+        };
+        rows(n1);
+        // degrees above the pipelined width: G more edges at a time, resolved in place
+        for (int kc = EPL * G; kc < deg; kc += G) {
+            __builtin_amdgcn_wave_barrier();
+            goff[lg] = row_off(d, edge_src(d, kc + lg));
+            __builtin_amdgcn_wave_barrier();
+            rows(deg - kc < G ? deg - kc : G);
         }
-        if (!next_issued && sn < n_seg) jn = edge_src(dn, lg);
 
         const float fdeg = (float)deg;
         const uint64_t out16 = ((uint64_t)(d.info & 0xffu) << 32) | d.out_lo;
@@ -169,10 +247,17 @@ __global__ __launch_bounds__(kThreads) void k_gather_mean(const SegDesc *__restr
             }
             *(uint4 *)(out + (int64_t)c * 16) = w;
         }
-        if (sn >= n_seg) break;
-        sg = sn;
+        sg += stride;
+        if (sg >= n_seg) break;
+        __builtin_amdgcn_wave_barrier();
         d = dn;
-        j = jn;
+        dn = dnn;
+        dnn = dnnn;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+            off[e] = offn[e];
+            jn[e] = jnn[e];
+        }
     }
 }
 
@@ -405,17 +490,36 @@ int64_t resident_wgs(K kernel) {
     return (int64_t)per_cu * cus;
 }
 
-template <bool B, int C>
+template <bool B, int C, int E>
 hipError_t launch_gather(const SegDesc *desc, int64_t n_seg, const FwdSlot *slots_dev,
                          int nslots, const GatherTabs &tabs, char *ws_base, const GroupShape &gs,
                          int chunks, hipStream_t s) {
     const int64_t groups_per_wg = (int64_t)(kThreads / 64) * gs.gpw;
     int64_t wgs = cdiv(n_seg, groups_per_wg);
-    const int64_t cap = resident_wgs(k_gather_mean<B, C>);
+    const int64_t cap = resident_wgs(k_gather_mean<B, C, E>);
     if (wgs > cap) wgs = cap;
-    hipLaunchKernelGGL((k_gather_mean<B, C>), dim3((unsigned)wgs), dim3(kThreads), 0, s, desc,
+    hipLaunchKernelGGL((k_gather_mean<B, C, E>), dim3((unsigned)wgs), dim3(kThreads), 0, s, desc,
                        n_seg, slots_dev, nslots, tabs, ws_base, gs.G, gs.gpw, chunks);
     return hipGetLastError();
+}
+
+// Edges per lane in the gather pipeline: enough for degree 32 at any row width.
+template <bool B>
+hipError_t gather_dispatch(const SegDesc *desc, int64_t n_seg, const FwdSlot *slots_dev,
+                           int nslots, const GatherTabs &tabs, char *ws_base, const GroupShape &gs,
+                           int chunks, hipStream_t s) {
+    if (gs.cpl == 1) {
+        if (gs.G >= 32)
+            return launch_gather<B, 1, 1>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
+        if (gs.G >= 16)
+            return launch_gather<B, 1, 2>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
+        return launch_gather<B, 1, 4>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
+    }
+    if (gs.cpl == 2)
+        return launch_gather<B, 2, 1>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
+    if (gs.cpl <= 4)
+        return launch_gather<B, 4, 1>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
+    return hipErrorInvalidValue;
 }
 
 hipError_t gather_mean(rgcn_dtype dt, int d_in, const SegDesc *desc, int64_t n_seg,
@@ -427,16 +531,8 @@ hipError_t gather_mean(rgcn_dtype dt, int d_in, const SegDesc *desc, int64_t n_s
     const GroupShape gs = group_shape(chunks);
     GatherTabs tabs;
     for (int t = 0; t < kMaxTypes; ++t) tabs.in[t] = in[t];
-    if (gs.cpl == 1)
-        return bf ? launch_gather<true, 1>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s)
-                  : launch_gather<false, 1>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
-    if (gs.cpl == 2)
-        return bf ? launch_gather<true, 2>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s)
-                  : launch_gather<false, 2>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
-    if (gs.cpl <= 4)
-        return bf ? launch_gather<true, 4>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s)
-                  : launch_gather<false, 4>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
-    return hipErrorInvalidValue;
+    return bf ? gather_dispatch<true>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s)
+              : gather_dispatch<false>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
 }
 
 hipError_t transpose_sum(rgcn_dtype dt, const TsumArgs &a, hipStream_t s) {

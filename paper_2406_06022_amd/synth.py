@@ -16,7 +16,10 @@ Block convention: the destination nodes of type t are the first ``n_dst[t]`` sou
 of type t, so the self-loop term reads rows ``[0, n_dst[t])`` of the source input.
 ``fanouts[l]`` applies to block ``l``; block 0 is nearest the input and the seed-adjacent
 block uses the last fanout.  Sources are drawn uniformly without replacement per
-(destination, relation) segment.
+(destination, relation) segment.  Source rows after the destination prefix are numbered
+in order of first appearance over the relations' edge lists (relations in order, edges in
+CSR order), the compaction order of the block construction in DGL, on which the paper's
+system builds its mini-batches.
 """
 from __future__ import annotations
 
@@ -249,6 +252,18 @@ def _draw_sources(rng: np.random.Generator, deg: np.ndarray, rows: int,
         src[dup] = draw(dup.shape[0])
 
 
+def _unique_first_appearance(x):
+    """Distinct values of the 1-D tensor ``x`` in order of their first occurrence."""
+    import torch
+    if x.numel() == 0:
+        return x
+    uniq, inv = torch.unique(x, return_inverse=True)
+    pos = torch.arange(x.numel(), dtype=torch.int64, device=x.device)
+    first = torch.full((uniq.numel(),), x.numel(), dtype=torch.int64, device=x.device)
+    first.scatter_reduce_(0, inv, pos, reduce="amin")
+    return uniq[torch.argsort(first)]
+
+
 def _relabel(global_ids, table):
     """Position of each global id inside ``table`` (torch tensors; every id is present)."""
     import torch
@@ -288,8 +303,8 @@ def sample_minibatch(spec: WorkloadSpec, seed_ids: Optional[List[np.ndarray]] = 
         for s in range(T):
             dst_t = torch.as_tensor(dst_ids[s], device=device)
             if per_type_new[s]:
-                pool = torch.unique(torch.as_tensor(np.concatenate(per_type_new[s]),
-                                                    device=device))
+                pool = _unique_first_appearance(
+                    torch.as_tensor(np.concatenate(per_type_new[s]), device=device))
                 fresh = pool[~torch.isin(pool, dst_t)]
             else:
                 fresh = torch.zeros(0, dtype=torch.int64, device=device)

@@ -61,3 +61,24 @@ def test_skewed_sources_are_distinct_and_in_range():
     for i in range(500):
         seg = src[off[i]:off[i + 1]]
         assert np.unique(seg).size == seg.size
+
+
+@pytest.mark.parametrize("index", [1, 3])
+def test_sources_numbered_by_first_appearance(index):
+    """Past the destination prefix, source rows are numbered in order of first use over the
+    relations' edge lists (relations in order, edges in CSR order)."""
+    mb = synth.sample_minibatch(synth.small_config(index))
+    for blk in mb.blocks:
+        for s in range(len(blk.n_src)):
+            seen = []
+            for rel in blk.rels:
+                if rel.src_type == s:
+                    seen.append(rel.indices.astype(np.int64))
+            if not seen:
+                assert blk.n_src[s] == blk.n_dst[s]
+                continue
+            edges = np.concatenate(seen)
+            fresh = edges[edges >= blk.n_dst[s]]
+            _, first = np.unique(fresh, return_index=True)
+            order = fresh[np.sort(first)]
+            assert np.array_equal(order, np.arange(blk.n_dst[s], blk.n_src[s]))
