@@ -1,0 +1,124 @@
+"""Multi-layer mini-batch through the chain driver the benchmark uses, against the oracle
+applied layer by layer (ReLU between layers, last layer linear, backward from the top).
+
+ReLU's derivative is a decision taken on a floating-point value, so both sides must see
+the same sign at every pre-activation.  Each layer gets a bias of +c or -c per output
+column (seeded signs) with c = 1.5 * 2^k and 2^k above twice the largest |pre-activation|
+z the oracle computes without bias: every pre-activation is then at least 2^k away from
+zero and its sign is the bias's, on both sides; the positive ones stay inside the binade
+[2^k, 2^(k+1)), so their rounding to the block dtype has one spacing.  c is exact in bf16.  The oracle computes c, so no expected value comes
+from the GPU.  Between layers the oracle stores each block's output in the block dtype
+(round to nearest even), as the block's output is defined; inside a block it keeps fp64.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2406_06022_amd import chain, rgcn, synth
+from tests.harness import TOL, rel_err, to64
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _margin_biases(blocks, h0, w64, T, seed, quant):
+    """Per-layer biases (fp64 lists per type, exact in the block dtype via ``quant``) and the
+    oracle's forward outputs."""
+    rng = np.random.default_rng(seed)
+    h = h0
+    biases, ys = [], []
+    L = len(blocks)
+    for l, blk in enumerate(blocks):
+        w_rel, w_self = w64[l]
+        z = oracle.block_forward(blk, h, w_rel, w_self)
+        d_out = w_self[0].shape[1]
+        if l < L - 1:
+            zmax = max((np.abs(x).max() for x in z if x is not None and x.size), default=1.0)
+            c = 1.5 * 2.0 ** math.ceil(math.log2(2.0 * zmax + 1.0))
+            sign = np.where(rng.random(d_out) < 0.5, -1.0, 1.0)
+            b = [c * sign for _ in range(T)]
+        else:
+            b = [quant(rng.uniform(-0.5, 0.5, d_out)) for _ in range(T)]
+        y = oracle.block_forward(blk, h, w_rel, w_self, b, relu=l < L - 1)
+        if l < L - 1:
+            # a block's output is stored in the block dtype and is the next block's input
+            y = [quant(x) if x is not None else None for x in y]
+        biases.append(b)
+        ys.append(y)
+        h = [y[t] if y[t] is not None else np.zeros((0, d_out)) for t in range(T)]
+    return biases, ys
+
+
+@pytest.mark.parametrize("index", [2, 4])
+def test_chain_matches_layerwise_oracle(index):
+    spec = synth.small_config(index)
+    mb = synth.sample_minibatch(spec)
+    T, R, L = len(spec.ntype_names), len(spec.rels), spec.num_layers
+    tdt = synth.torch_dtype(spec.dtype)
+    emb = [t for t in range(T) if spec.featureless[t]]
+    tables = [synth.normal_table(spec.type_rows[t], spec.dims[0], tdt, 300 + t) for t in range(T)]
+    ids = [torch.as_tensor(mb.input_ids[t]) for t in range(T)]
+    w = [synth.block_weights(T, R, spec.dims[l], spec.dims[l + 1], tdt, 40 + l)[:2]
+         for l in range(L)]
+    w64 = [([to64(x) for x in wr], [to64(x) for x in wsf]) for wr, wsf in w]
+    h0 = [to64(tables[t])[mb.input_ids[t]] for t in range(T)]
+    def quant(x):
+        return to64(torch.as_tensor(x).to(tdt))
+
+    biases, ys = _margin_biases(mb.blocks, h0, w64, T, 77 + index, quant)
+    b_dev = [[torch.as_tensor(b[t]).to(tdt) for t in range(T)] for b in biases]
+    for l in range(L):  # every bias is exact in the block dtype
+        for t in range(T):
+            assert np.array_equal(to64(b_dev[l][t]), biases[l][t])
+
+    gen = torch.Generator().manual_seed(90 + index)
+    top = mb.blocks[-1]
+    dy_top = [torch.randn((n, spec.dims[-1]), generator=gen) for n in top.n_dst]
+
+    # ---- GPU through the chain driver
+    weights = [([x.to(DEV) for x in w[l][0]], [x.to(DEV) for x in w[l][1]],
+                [x.to(DEV) for x in b_dev[l]]) for l in range(L)]
+    stack = chain.MiniBatchStack(mb.blocks, [x.to(DEV) for x in tables],
+                                 [x.to(DEV) for x in ids], weights, spec.dtype, spec.dims,
+                                 emb_types=emb, device=DEV)
+    stack.step([x.to(DEV) if x.numel() else None for x in dy_top])
+    torch.cuda.synchronize()
+
+    # ---- oracle, layer by layer from the top
+    hs = [h0] + [[ys[l][t] if ys[l][t] is not None else np.zeros((0, spec.dims[l + 1]))
+                  for t in range(T)] for l in range(L - 1)]
+    dy = [to64(x) for x in dy_top]
+    grads = [None] * L
+    for l in reversed(range(L)):
+        blk = mb.blocks[l]
+        want = [(t in emb) if l == 0 else blk.n_src[t] > 0 for t in range(T)]
+        g = oracle.block_backward(blk, hs[l], w64[l][0], w64[l][1], dy, input_relu=l > 0,
+                                  want_dh=want)
+        grads[l] = g
+        dy = [g["dh_src"][t] if g["dh_src"][t] is not None else np.zeros((0, spec.dims[l]))
+              for t in range(T)]
+    demb_ref = {}
+    for t in emb:
+        d = np.zeros((spec.type_rows[t], spec.dims[0]))
+        oracle.scatter_add(mb.input_ids[t], grads[0]["dh_src"][t], d)
+        demb_ref[t] = d
+
+    tol = TOL[spec.dtype]
+    errs = {}
+    for t in range(T):
+        if top.n_dst[t] > 0:
+            errs[f"y_top[{t}]"] = rel_err(to64(stack.y[-1][t]), ys[-1][t])
+    for l in range(L):
+        for r in range(R):
+            errs[f"dw_rel[{l}][{r}]"] = rel_err(to64(stack.dw_rel[l][r]), grads[l]["dw_rel"][r])
+        for t in range(T):
+            errs[f"dw_self[{l}][{t}]"] = rel_err(to64(stack.dw_self[l][t]), grads[l]["dw_self"][t])
+            errs[f"dbias[{l}][{t}]"] = rel_err(to64(stack.dbias[l][t]), grads[l]["dbias"][t])
+    for t in emb:
+        errs[f"demb[{t}]"] = rel_err(to64(stack.demb[t]), demb_ref[t])
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    print(f"[chain] {spec.name}: worst {max(errs.values()):.3g} ({max(errs, key=errs.get)})")
+    assert not bad, f"chain parity failures (tol {tol}): {bad}"
