@@ -42,7 +42,7 @@ _COMMON_INPUTS = ["paper_2406_06022_amd/csrc/common.h", "include/rgcn.h",
                   "paper_2406_06022_amd/build.py", "paper_2406_06022_amd/synth.py"]
 KERNEL_SOURCES = {
     "k_gather_mean": ["paper_2406_06022_amd/csrc/aggregate.hip"] + _COMMON_INPUTS,
-    "k_transpose_sum": ["paper_2406_06022_amd/csrc/aggregate.hip"] + _COMMON_INPUTS,
+    "k_transpose_pipe": ["paper_2406_06022_amd/csrc/aggregate.hip"] + _COMMON_INPUTS,
 }
 # Plain copy of known size run after the timed steps (an fp32 negation of a 1 GiB buffer:
 # one read and one write of every byte per dispatch).  Its time gives the box's attainable
@@ -384,7 +384,7 @@ def main() -> int:
                 cands.append((avg[(s, l)], s, l))
     cands.sort(reverse=True)
     _, dom_stage, dom_layer = cands[0]
-    kernel_name = {"aggregate": "k_gather_mean", "sparse": "k_transpose_sum"}[dom_stage]
+    kernel_name = {"aggregate": "k_gather_mean", "sparse": "k_transpose_pipe"}[dom_stage]
     rooflines = {}
     for t_ms, s, l in cands:
         byts = algorithmic_bytes(spec, mb.blocks[l], stack.blocks[l], s, l)

@@ -49,6 +49,7 @@ __device__ __forceinline__ const __attribute__((address_space(1))) T *gbl(const 
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 // 16-byte global load
 __device__ __forceinline__ uint4 ld16(const char *p) {
     const u32x4 v = *gbl((const u32x4 *)p);
@@ -76,12 +77,101 @@ __device__ __forceinline__ int64_t shfl64(int64_t v, int src) {
 // are resolved in place.  Row byte offsets are published to the group's LDS slots and
 // read back as broadcasts while U rows per lane are in flight.
 // The sum runs in ascending edge position; one division by the degree.
+// Read (never written) by loads whose value is not needed; zero-initialised.  g_zero_row
+// covers the widest row a group reads (256 chunks of 16 bytes), so a lane's chunk offset
+// into it stays in bounds.
+__device__ int64_t g_zero[2];
+__device__ u32x4 g_zero_row[256];
+
+// Row batches: rows [q, q + r) of a group, B loads per lane in flight; slots past r read
+// the zero row.  The batch size is chosen per wave from ballots (uniform branches): the
+// largest of UMAX, 4, 2, 1 that some group of the wave can fill past half.
+template <int B, class LoadAcc>
+__device__ __forceinline__ void row_batch(const int64_t *goff, int q, int r, LoadAcc &&la) {
+    int64_t o[B];
+    bool ok[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+        ok[u] = u < r;
+        o[u] = goff[ok[u] ? q + u : 0];
+    }
+    la.template run<B>(o, ok);
+}
+template <int UMAX, class LoadAcc>
+__device__ __forceinline__ void row_walk(const int64_t *goff, int n, LoadAcc &&la) {
+    int q = 0;
+    while (true) {
+        const int r = n - q;
+        if (__ballot(r > 0) == 0) break;
+        if (UMAX > 4 && __ballot(r > 4) != 0) {
+            row_batch<UMAX>(goff, q, r, la);
+            q += UMAX;
+        } else if (__ballot(r > 2) != 0) {
+            row_batch<4>(goff, q, r, la);
+            q += 4;
+        } else if (__ballot(r > 1) != 0) {
+            row_batch<2>(goff, q, r, la);
+            q += 2;
+        } else {
+            row_batch<1>(goff, q, r, la);
+            q += 1;
+        }
+    }
+}
+
+// Batch bodies: load B rows' chunks (16 bytes per lane per chunk) and add them into acc.
+// GatherLoad: block-dtype rows at src + offset; SumLoad: fp32 rows at absolute addresses.
+template <bool BF16, int CPL>
+struct GatherLoad {
+    const char *src;
+    int lg, G, chunks;
+    float (*acc)[BF16 ? 8 : 4];
+    template <int B>
+    __device__ __forceinline__ void run(const int64_t (&o)[B], const bool (&ok)[B]) const {
+        u32x4 v[B][CPL];
+#pragma unroll
+        for (int u = 0; u < B; ++u)
+#pragma unroll
+            for (int p = 0; p < CPL; ++p) {
+                const int c = lg + p * G;
+                const char *pa = (ok[u] && c < chunks) ? src + o[u] + (int64_t)c * 16
+                                                       : (const char *)g_zero_row + c * 16;
+                v[u][p] = *gbl((const u32x4 *)pa);
+            }
+#pragma unroll
+        for (int u = 0; u < B; ++u)
+#pragma unroll
+            for (int p = 0; p < CPL; ++p)
+                acc_chunk<BF16>(acc[p], make_uint4(v[u][p].x, v[u][p].y, v[u][p].z, v[u][p].w));
+    }
+};
+template <int CPL>
+struct SumLoad {
+    int lg, G, chunks;
+    f32x4 *acc;
+    template <int B>
+    __device__ __forceinline__ void run(const int64_t (&o)[B], const bool (&ok)[B]) const {
+        f32x4 v[B][CPL];
+#pragma unroll
+        for (int u = 0; u < B; ++u)
+#pragma unroll
+            for (int p = 0; p < CPL; ++p) {
+                const int c = lg + p * G;
+                const char *pa = (ok[u] && c < chunks) ? (const char *)(uintptr_t)o[u] + (int64_t)c * 16
+                                                       : (const char *)g_zero_row + c * 16;
+                v[u][p] = *gbl((const f32x4 *)pa);
+            }
+#pragma unroll
+        for (int u = 0; u < B; ++u)
+#pragma unroll
+            for (int p = 0; p < CPL; ++p) acc[p] += v[u][p];
+    }
+};
+
 struct GatherTabs {
     TypeInput in[kMaxTypes];
 };
 
-// Read (never written) by loads whose value is not needed; zero-initialised.
-__device__ int64_t g_zero[2];
 
 #ifndef RGCN_GATHER_U1
 #define RGCN_GATHER_U1 4
@@ -195,29 +285,8 @@ void k_gather_mean(const SegDesc *__restrict__ desc,
 
         // edges [0, n) of the offsets in goff: U rows per lane in flight; a batch's unused
         // slots re-read the last row (a cache hit) and are dropped
-        auto rows = [&](int n) {
-            for (int q = 0; q < n; q += U) {
-                int64_t o[U];
-#pragma unroll
-                for (int u = 0; u < U; ++u) o[u] = goff[q + u < n ? q + u : n - 1];
-                uint4 v[U][CPL];
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-#pragma unroll
-                    for (int p = 0; p < CPL; ++p) {
-                        const int c = lg + p * G < chunks ? lg + p * G : chunks - 1;
-                        v[u][p] = ld16(src + o[u] + (int64_t)c * 16);
-                    }
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-#pragma unroll
-                    for (int p = 0; p < CPL; ++p) {
-                        const bool ok = q + u < n && lg + p * G < chunks;
-                        const uint4 x = v[u][p];
-                        acc_chunk<BF16>(acc[p], ok ? x : make_uint4(0, 0, 0, 0));
-                    }
-            }
-        };
+        // U-row batches of the group's published offsets; an empty slot reads the zero row
+        auto rows = [&](int n) { row_walk<U>(goff, n, GatherLoad<BF16, CPL>{src, lg, G, chunks, acc}); };
         rows(n1);
         // degrees above the pipelined width: G more edges at a time, resolved in place
         for (int kc = EPL * G; kc < deg; kc += G) {
@@ -394,6 +463,185 @@ __global__ __launch_bounds__(kThreads) void k_transpose_sum(TsumArgs a, int G, i
     }
 }
 
+// The same sum, persistent and software-pipelined over a group's successive source rows
+// (used when the relations leaving the type fit in one group, nrel <= G).  A row takes
+// four dependent steps: its schedule entry j; the global row id and, on lane r, the
+// transpose offsets of relation r; on lane e, the destination row of flattened edge e
+// (with the embedding-gradient row, the ReLU-mask input and the self term); the dMs rows.
+// While the rows of one source row are in flight, the earlier steps of the next three
+// rows are too.  Edges past the group width are resolved in place.  Every load is
+// unconditional (unused lanes read a zero word).
+#ifndef RGCN_TSUM_U1
+#define RGCN_TSUM_U1 4
+#endif
+
+template <bool BF16IN, int CPL>
+__global__ __launch_bounds__(kThreads) void k_transpose_pipe(TsumArgs a, int G, int gpw,
+                                                             int chunks) {
+    constexpr int HES = BF16IN ? 2 : 4;
+    constexpr int U = CPL == 1 ? RGCN_TSUM_U1 : 4;
+    constexpr int W = kThreads / 64;
+    __shared__ TsumRel s_rel[kMaxRels];
+    __shared__ int64_t s_off[W][64];
+    for (int i = threadIdx.x; i < a.nrel; i += kThreads) s_rel[i] = a.rel[i];
+    __syncthreads();
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int gi = lane / G;
+    const int lg = lane - gi * G;
+    const int g0 = gi * G;
+    if (gi >= gpw) return;
+    int64_t *goff = &s_off[wave][g0];
+    const int64_t stride = (int64_t)gridDim.x * W * gpw;
+    int64_t g = ((int64_t)blockIdx.x * W + wave) * gpw + gi;
+    if (g >= a.n_rows) return;
+    const char *zero = (const char *)g_zero;
+    const int nrel = a.nrel;
+    const int rl = lg < nrel ? lg : 0;   // this lane's relation (stage 2)
+
+    struct Meta {
+        int32_t j, p0, cnt;
+        int64_t grow;
+    };
+    struct Row {
+        Meta m;
+        int32_t total, ei, er;
+        f32x4 old[CPL], self[CPL], hm[CPL];
+    };
+    // stage 1: source row at schedule position q (-1 past the end)
+    auto s1 = [&](int64_t q) -> int32_t {
+        const int32_t v = *gbl(a.order + (q < a.n_rows ? q : a.n_rows - 1));
+        return q < a.n_rows ? v : -1;
+    };
+    // stage 2: global row id; lane r < nrel: transpose segment of relation r
+    auto s2 = [&](int32_t j) -> Meta {
+        Meta m;
+        m.j = j;
+        const bool okj = j >= 0;
+        const int64_t *rid = a.in.row_ids;
+        const int64_t gv = *gbl((okj && rid != nullptr) ? rid + j : (const int64_t *)zero);
+        m.grow = gv + (rid != nullptr ? 0 : (int64_t)j);
+        const bool okr = okj && lg < nrel;
+        const int32_t *ip = okr ? s_rel[rl].csc_indptr + j : (const int32_t *)zero;
+        const int32_t v0 = *gbl(ip), v1 = *gbl(ip + (okr ? 1 : 0));
+        m.p0 = v0;
+        m.cnt = v1 - v0;
+        return m;
+    };
+    // flattened edge e of a row -> (relation, position in the shared transpose arrays)
+    auto locate = [&](const Meta &m, int e, int &r_out, int &pos_out) -> int {
+        int total = 0, ridx = 0, pos = 0;
+        for (int r = 0; r < nrel; ++r) {
+            const int cr = __shfl(m.cnt, g0 + r, 64);
+            const int pr = __shfl(m.p0, g0 + r, 64);
+            const bool in = e >= total && e < total + cr;
+            ridx = in ? r : ridx;
+            pos = in ? pr + (e - total) : pos;
+            total += cr;
+        }
+        r_out = ridx;
+        pos_out = pos;
+        return total;
+    };
+    // stage 3: destination row of this lane's edge, and the row's per-chunk side data
+    auto s3 = [&](const Meta &m, Row &rw) {
+        rw.m = m;
+        int ridx, pos;
+        rw.total = locate(m, lg, ridx, pos);
+        const bool oke = lg < rw.total;
+        rw.ei = *gbl(oke ? s_rel[ridx].csc_dst + pos : (const int32_t *)zero);
+        rw.er = ridx;
+#pragma unroll
+        for (int p = 0; p < CPL; ++p) {
+            const int c = lg + p * G;
+            const bool okc = c < chunks && m.j >= 0;
+            const bool ok_old = okc && a.demb != nullptr && a.ids_unique;
+            rw.old[p] = *gbl(ok_old ? (const f32x4 *)(a.demb + m.grow * a.d_in + (int64_t)c * 4)
+                                    : (const f32x4 *)zero);
+            const bool ok_self = okc && a.self_dms != nullptr && m.j < a.n_dst;
+            rw.self[p] = *gbl(ok_self ? (const f32x4 *)(a.self_dms + m.j * a.self_ld + (int64_t)c * 4)
+                                      : (const f32x4 *)zero);
+            const bool ok_h = okc && a.input_relu;
+            const char *hp = ok_h ? (const char *)a.in.base + (m.grow * a.in.ld + (int64_t)c * 4) * HES
+                                  : zero;
+            if constexpr (BF16IN) {
+                const u32x2 hv = *gbl((const u32x2 *)hp);
+                rw.hm[p] = f32x4{bf16_lo(hv.x), bf16_hi(hv.x), bf16_lo(hv.y), bf16_hi(hv.y)};
+            } else {
+                rw.hm[p] = *gbl((const f32x4 *)hp);
+            }
+        }
+    };
+    // rows [0, n) whose addresses are in goff, added into acc; a batch's unused slots re-read
+    // the last row and are dropped
+    auto rows = [&](int n, f32x4 (&acc)[CPL]) { row_walk<U>(goff, n, SumLoad<CPL>{lg, G, chunks, acc}); };
+    auto edge_addr = [&](int r, int32_t i) -> int64_t {
+        return (int64_t)(uintptr_t)(s_rel[r].dms + (int64_t)i * s_rel[r].dms_ld);
+    };
+    // last step of a row: its dMs rows, the mask, the stores
+    auto finish = [&](const Row &rw) {
+        f32x4 acc[CPL];
+#pragma unroll
+        for (int p = 0; p < CPL; ++p) acc[p] = rw.self[p];
+        const int n1 = rw.total < G ? rw.total : G;
+        goff[lg] = edge_addr(rw.er, rw.ei);
+        __builtin_amdgcn_wave_barrier();
+        rows(n1, acc);
+        for (int ec = G; ec < rw.total; ec += G) {
+            int ridx, pos;
+            locate(rw.m, ec + lg, ridx, pos);
+            const bool oke = ec + lg < rw.total;
+            const int32_t i = *gbl(oke ? s_rel[ridx].csc_dst + pos : (const int32_t *)zero);
+            __builtin_amdgcn_wave_barrier();
+            goff[lg] = edge_addr(ridx, i);
+            __builtin_amdgcn_wave_barrier();
+            rows(rw.total - ec < G ? rw.total - ec : G, acc);
+        }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int p = 0; p < CPL; ++p) {
+            const int c = lg + p * G;
+            if (c >= chunks) continue;
+            f32x4 res = acc[p];
+            if (a.input_relu) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) res[e] = rw.hm[p][e] > 0.f ? res[e] : 0.f;
+            }
+            if (a.dh) *(f32x4 *)(a.dh + (int64_t)rw.m.j * a.d_in + (int64_t)c * 4) = res;
+            if (a.demb) {
+                float *dp = a.demb + rw.m.grow * a.d_in + (int64_t)c * 4;
+                if (a.ids_unique) {
+                    *(f32x4 *)dp = rw.old[p] + res;
+                } else {
+                    unsafeAtomicAdd(dp + 0, res[0]);
+                    unsafeAtomicAdd(dp + 1, res[1]);
+                    unsafeAtomicAdd(dp + 2, res[2]);
+                    unsafeAtomicAdd(dp + 3, res[3]);
+                }
+            }
+        }
+    };
+
+    // pipeline prologue: row g through stage 3, row g+stride through stage 2, row
+    // g+2*stride through stage 1
+    Row cur;
+    s3(s2(s1(g)), cur);
+    Meta mn = s2(s1(g + stride));
+    int32_t jnn = s1(g + 2 * stride);
+    while (true) {
+        Row nxt;
+        s3(mn, nxt);
+        const Meta mnn = s2(jnn);
+        const int32_t jn3 = s1(g + 3 * stride);
+        finish(cur);
+        g += stride;
+        if (g >= a.n_rows) break;
+        cur = nxt;
+        mn = mnn;
+        jnn = jn3;
+    }
+}
+
 // WcatT[n][s*d_in + c] = W_s[c][n]: the forward transform's weights, K-contiguous.
 struct WSlots {
     const void *w[kMaxSlots];
@@ -535,10 +783,31 @@ hipError_t gather_mean(rgcn_dtype dt, int d_in, const SegDesc *desc, int64_t n_s
               : gather_dispatch<false>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
 }
 
+template <bool B, int C>
+hipError_t launch_transpose_pipe(const TsumArgs &a, const GroupShape &gs, int chunks,
+                                 hipStream_t s) {
+    const int64_t groups_per_wg = (int64_t)(kThreads / 64) * gs.gpw;
+    int64_t wgs = cdiv(a.n_rows, groups_per_wg);
+    const int64_t cap = resident_wgs(k_transpose_pipe<B, C>);
+    if (wgs > cap) wgs = cap;
+    hipLaunchKernelGGL((k_transpose_pipe<B, C>), dim3((unsigned)wgs), dim3(kThreads), 0, s, a, gs.G,
+                       gs.gpw, chunks);
+    return hipGetLastError();
+}
+
 hipError_t transpose_sum(rgcn_dtype dt, const TsumArgs &a, hipStream_t s) {
     if (a.n_rows == 0) return hipSuccess;
     const int chunks = a.d_in / 4;
     const GroupShape gs = group_shape(chunks);
+    const bool bfp = dt == RGCN_BF16;
+    if (a.nrel <= gs.G) {
+        if (gs.cpl == 1) return bfp ? launch_transpose_pipe<true, 1>(a, gs, chunks, s)
+                                    : launch_transpose_pipe<false, 1>(a, gs, chunks, s);
+        if (gs.cpl == 2) return bfp ? launch_transpose_pipe<true, 2>(a, gs, chunks, s)
+                                    : launch_transpose_pipe<false, 2>(a, gs, chunks, s);
+        if (gs.cpl <= 4) return bfp ? launch_transpose_pipe<true, 4>(a, gs, chunks, s)
+                                    : launch_transpose_pipe<false, 4>(a, gs, chunks, s);
+    }
     const int64_t waves = cdiv(a.n_rows, gs.gpw);
     const dim3 grid((unsigned)cdiv(waves, kThreads / 64));
     const bool bf = dt == RGCN_BF16;

@@ -56,7 +56,7 @@ template <class TL>
 struct MmaBf16 {
     using T = TL;
     static constexpr int TILES = 2;   // A, B
-    __device__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
+    __device__ __forceinline__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
                                int wn, int lane) {
         const int r = lane & 15, q = lane >> 4;
 #pragma unroll
@@ -86,7 +86,7 @@ template <class TL>
 struct MmaBf16Split {
     using T = TL;
     static constexpr int TILES = 3;   // A, B_hi, B_lo
-    __device__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
+    __device__ __forceinline__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
                                int wn, int lane) {
         const int r = lane & 15, q = lane >> 4;
         const char *Bl = Bs + TL::BYTES;
@@ -117,7 +117,7 @@ struct MmaBf16Split {
 struct MmaF32 {
     using T = TileF32;
     static constexpr int TILES = 2;
-    __device__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
+    __device__ __forceinline__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
                                int wn, int lane) {
         f32x4 a[4], b[4];
         const int r = lane & 15, q = lane >> 4;
@@ -145,7 +145,7 @@ struct PlainRows {
     const char *base;
     int64_t ld_bytes;
     int64_t rows;
-    __device__ const char *row(int64_t r) const {
+    __device__ __forceinline__ const char *row(int64_t r) const {
         return base + (r < rows ? r : rows - 1) * ld_bytes;
     }
 };
@@ -154,18 +154,18 @@ struct SlotRows {  // row n = (slot n / d_in, column c = n % d_in) of W_slot [d_
     int32_t d_in;
     int32_t es_dout;   // bytes per W row (d_out * element size)
     int64_t rows;
-    __device__ const char *row(int64_t r) const {
+    __device__ __forceinline__ const char *row(int64_t r) const {
         const int64_t rr = r < rows ? r : rows - 1;
         const int64_t sl = rr / d_in, c = rr - sl * d_in;
         return (const char *)w[sl] + c * es_dout;
     }
 };
-__device__ __forceinline__ uint4 select4(bool ok, const uint4 &v) {
-    return make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
-}
-__device__ __forceinline__ float4 select4f(bool ok, const float4 &v) {
-    return make_float4(ok ? v.x : 0.f, ok ? v.y : 0.f, ok ? v.z : 0.f, ok ? v.w : 0.f);
-}
+// Loads a thread does not need (rows past the end, K past the range) read these zero bytes
+// instead, so the registers hold zeros without a select; never written.
+// Register staging uses the compiler's native vector types (one 16-byte load or LDS store,
+// no struct copies).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ u32x4 g_zero16[2];
 
 // K-contiguous rows whose element type is the LDS type.  WRAP: the product's K is twice
 // the row length and k >= row length re-reads the row (used with LoadRowsF32Split).
@@ -178,11 +178,10 @@ struct LoadRows {
     struct State {
         const char *rp[NCH];
         bool rok[NCH];
-        bool ok[NCH];
         int lr[NCH], lq[NCH];
-        uint4 reg[NCH];
+        u32x4 reg[NCH];
     };
-    __device__ void init(State &st, int64_t row0) const {
+    __device__ __forceinline__ void init(State &st, int64_t row0) const {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             const int chunk = threadIdx.x + c * kThreads;
@@ -192,19 +191,20 @@ struct LoadRows {
             st.rp[c] = pol.row(row0 + st.lr[c]);
         }
     }
-    __device__ void load(State &st, int64_t k0) const {
+    __device__ __forceinline__ void load(State &st, int64_t k0, int64_t kend) const {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-            int64_t kb = k0 * TL::ES + st.lq[c] * 16;
+            const int64_t k = k0 + st.lq[c] * (16 / TL::ES);
+            int64_t kb = k * TL::ES;
             if constexpr (WRAP) kb = kb >= wrap_bytes ? kb - wrap_bytes : kb;
-            st.ok[c] = st.rok[c] && kb < kbytes;
-            st.reg[c] = *(const uint4 *)(st.rp[c] + (st.ok[c] ? kb : 0));
+            const bool ok = st.rok[c] && kb < kbytes && k < kend;
+            st.reg[c] = *(const u32x4 *)(ok ? st.rp[c] + kb : (const char *)g_zero16);
         }
     }
-    __device__ void store(const State &st, char *lds) const {
+    __device__ __forceinline__ void store(const State &st, char *lds) const {
 #pragma unroll
         for (int c = 0; c < NCH; ++c)
-            *(uint4 *)(lds + st.lr[c] * TL::PITCH + st.lq[c] * 16) = select4(st.ok[c], st.reg[c]);
+            *(u32x4 *)(lds + st.lr[c] * TL::PITCH + st.lq[c] * 16) = st.reg[c];
     }
 };
 
@@ -222,12 +222,11 @@ struct LoadRowsF32Split {
     struct State {
         const char *rp[NCH];
         bool rok[NCH];
-        bool ok[NCH];
         int lr[NCH], lq[NCH];
         bool low[NCH];
-        float4 reg[NCH][2];
+        f32x4 reg[NCH][2];
     };
-    __device__ void init(State &st, int64_t row0) const {
+    __device__ __forceinline__ void init(State &st, int64_t row0) const {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             const int chunk = threadIdx.x + c * kThreads;
@@ -237,30 +236,31 @@ struct LoadRowsF32Split {
             st.rp[c] = pol.row(row0 + st.lr[c]);
         }
     }
-    __device__ void load(State &st, int64_t k0) const {
+    __device__ __forceinline__ void load(State &st, int64_t k0, int64_t kend) const {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             int64_t k = k0 + st.lq[c] * 8;
+            const bool in = k < kend;
             st.low[c] = k >= K;
             k = st.low[c] ? k - K : k;
-            st.ok[c] = st.rok[c] && k < K;
-            const char *p = st.rp[c] + (st.ok[c] ? k * 4 : 0);
-            st.reg[c][0] = *(const float4 *)p;
-            st.reg[c][1] = *(const float4 *)(p + 16);
+            const bool ok = st.rok[c] && k < K && in;
+            const char *p = ok ? st.rp[c] + k * 4 : (const char *)g_zero16;
+            st.reg[c][0] = *(const f32x4 *)p;
+            st.reg[c][1] = *(const f32x4 *)(p + 16);
         }
     }
-    __device__ static float part(float x, bool lo) { return lo ? x - round_bf16(x) : x; }
-    __device__ void store(const State &st, char *lds) const {
+    __device__ __forceinline__ static float part(float x, bool lo) { return lo ? x - round_bf16(x) : x; }
+    __device__ __forceinline__ void store(const State &st, char *lds) const {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             const bool lo = st.low[c];
-            const float4 a = select4f(st.ok[c], st.reg[c][0]), b = select4f(st.ok[c], st.reg[c][1]);
-            uint4 w;
+            const f32x4 a = st.reg[c][0], b = st.reg[c][1];
+            u32x4 w;
             w.x = pack_bf16x2(part(a.x, lo), part(a.y, lo));
             w.y = pack_bf16x2(part(a.z, lo), part(a.w, lo));
             w.z = pack_bf16x2(part(b.x, lo), part(b.y, lo));
             w.w = pack_bf16x2(part(b.z, lo), part(b.w, lo));
-            *(uint4 *)(lds + st.lr[c] * TL::PITCH + st.lq[c] * 16) = w;
+            *(u32x4 *)(lds + st.lr[c] * TL::PITCH + st.lq[c] * 16) = w;
         }
     }
 };
@@ -284,38 +284,32 @@ struct LoadTransHalf {
     struct State {
         int64_t col0;
         int ib, cb, hb;
-        bool ok[4];
-        uint4 reg[4][NH];
+        u32x4 reg[4][NH];
     };
-    __device__ void init(State &st, int64_t c0) const {
+    __device__ __forceinline__ void init(State &st, int64_t c0) const {
         st.col0 = c0;
         const int b = (int)threadIdx.x >> 1;
         st.hb = threadIdx.x & 1;
         st.ib = b & 7;
         st.cb = b >> 3;
     }
-    __device__ void load(State &st, int64_t k0) const {
+    __device__ __forceinline__ void load(State &st, int64_t k0, int64_t kend) const {
         const int64_t col = st.col0 + (int64_t)st.cb * 8;
         const bool colok = col < cols;
+        const int64_t lim = kend < ksrc ? kend : ksrc;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int64_t i = k0 + st.ib * 8 + st.hb * 4 + r;
-            st.ok[r] = colok && i < ksrc;
-            const char *p = base + (st.ok[r] ? i * ld_bytes + col * SES : 0);
+            const bool ok = colok && i < lim;
+            const char *p = ok ? base + i * ld_bytes + col * SES : (const char *)g_zero16;
 #pragma unroll
-            for (int h = 0; h < NH; ++h) st.reg[r][h] = *(const uint4 *)(p + h * 16);
+            for (int h = 0; h < NH; ++h) st.reg[r][h] = *(const u32x4 *)(p + h * 16);
         }
     }
-    __device__ static uint32_t word(const uint4 &u, int i) {
-        return i == 0 ? u.x : i == 1 ? u.y : i == 2 ? u.z : u.w;
-    }
-    __device__ void store(const State &st, char *lds) const {
+    __device__ __forceinline__ static uint32_t word(const u32x4 &u, int i) { return u[i]; }
+    __device__ __forceinline__ void store(const State &st, char *lds) const {
         const int off = st.ib * 16 + st.hb * 8;
-        uint4 rg[4][NH];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-#pragma unroll
-            for (int h = 0; h < NH; ++h) rg[r][h] = select4(st.ok[r], st.reg[r][h]);
+        const auto &rg = st.reg;
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
             uint32_t w[2], wl[2];
@@ -353,10 +347,9 @@ struct LoadTransF32 {
     struct State {
         int64_t col0;
         int ik[2], cq[2];
-        bool ok[2];
-        uint4 reg[2];
+        u32x4 reg[2];
     };
-    __device__ void init(State &st, int64_t c0) const {
+    __device__ __forceinline__ void init(State &st, int64_t c0) const {
         st.col0 = c0;
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
@@ -365,19 +358,20 @@ struct LoadTransF32 {
             st.cq[c] = chunk & 31;
         }
     }
-    __device__ void load(State &st, int64_t k0) const {
+    __device__ __forceinline__ void load(State &st, int64_t k0, int64_t kend) const {
+        const int64_t lim = kend < ksrc ? kend : ksrc;
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
             const int64_t i = k0 + st.ik[c];
             const int64_t col = st.col0 + (int64_t)st.cq[c] * 4;
-            st.ok[c] = i < ksrc && col < cols;
-            st.reg[c] = *(const uint4 *)(base + (st.ok[c] ? i * ld_bytes + col * 4 : 0));
+            const bool ok = i < lim && col < cols;
+            st.reg[c] = *(const u32x4 *)(ok ? base + i * ld_bytes + col * 4 : (const char *)g_zero16);
         }
     }
-    __device__ void store(const State &st, char *lds) const {
+    __device__ __forceinline__ void store(const State &st, char *lds) const {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-            const uint4 v = select4(st.ok[c], st.reg[c]);
+            const u32x4 v = st.reg[c];
             const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
             for (int e = 0; e < 4; ++e)
@@ -395,7 +389,7 @@ struct EpiForward {
     int64_t M;
     int32_t N;
     int32_t relu;
-    __device__ void operator()(int64_t m, int64_t n0, const float *v, int64_t) const {
+    __device__ __forceinline__ void operator()(int64_t m, int64_t n0, const float *v, int64_t) const {
         if (m >= M) return;
         // N is a multiple of 4: each group of 4 columns is either whole or absent.  The
         // bias loads are issued together (clamped, then zeroed) before any is used.
@@ -448,7 +442,7 @@ struct EpiDms {
     int32_t N;
     int32_t d_in;
     const int32_t *indptr[kMaxSlots];
-    __device__ void operator()(int64_t m, int64_t n0, const float *v, int64_t) const {
+    __device__ __forceinline__ void operator()(int64_t m, int64_t n0, const float *v, int64_t) const {
         if (m >= M) return;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -476,7 +470,7 @@ struct EpiPartial {
     float *out;          // [splits][M][N]
     int64_t M;
     int32_t N;
-    __device__ void operator()(int64_t m, int64_t n0, const float *v, int64_t split) const {
+    __device__ __forceinline__ void operator()(int64_t m, int64_t n0, const float *v, int64_t split) const {
         if (m >= M) return;
         float *o = out + split * M * N + m * N;
 #pragma unroll
@@ -528,30 +522,33 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, 
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // Steps are padded to a multiple of R and every load is issued unconditionally
+    // (steps past the range load zero tiles), so all paths through the loop have the same
+    // loads in flight and the waits before each LDS store cover only its own register set.
     const int64_t nk = ke > kb ? cdiv(ke - kb, TL::BK) : 0;
+    const int64_t nkp = cdiv(nk, R) * R;
 #pragma unroll
-    for (int r = 0; r < R; ++r)
-        if (r < nk) {
-            la.load(sa[r], kb + r * TL::BK);
-            lb.load(sb[r], kb + r * TL::BK);
-        }
-    for (int64_t it0 = 0; it0 < nk; it0 += R) {
+    for (int r = 0; r < R; ++r) {
+        la.load(sa[r], kb + r * TL::BK, ke);
+        lb.load(sb[r], kb + r * TL::BK, ke);
+        __builtin_amdgcn_sched_barrier(0);   // register set r's loads all precede set r+1's
+    }
+    for (int64_t it0 = 0; it0 < nkp; it0 += R) {
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int64_t it = it0 + r;
-            if (it < nk) {
-                char *As = lds + (STAGES == 2 ? (it & 1) * STAGE_BYTES : 0);
-                char *Bs = As + TL::BYTES;
-                if constexpr (STAGES == 1) __syncthreads();
-                la.store(sa[r], As);
-                lb.store(sb[r], Bs);
-                __syncthreads();
-                if (it + R < nk) {
-                    la.load(sa[r], kb + (it + R) * TL::BK);
-                    lb.load(sb[r], kb + (it + R) * TL::BK);
-                }
-                Mma::run(As, Bs, acc, wm, wn, lane);
-            }
+            char *As = lds + (STAGES == 2 ? ((it0 + r) & 1) * STAGE_BYTES : 0);
+            char *Bs = As + TL::BYTES;
+            if constexpr (STAGES == 1) __syncthreads();
+            la.store(sa[r], As);
+            lb.store(sb[r], Bs);
+            __syncthreads();
+            la.load(sa[r], kb + (it + R) * TL::BK, ke);
+            lb.load(sb[r], kb + (it + R) * TL::BK, ke);
+            // keep the loads ahead of the multiplies and their consumers after them
+            __builtin_amdgcn_sched_barrier(0);
+            Mma::run(As, Bs, acc, wm, wn, lane);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
     __syncthreads();
@@ -584,6 +581,9 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, 
 #endif
 #ifndef RGCN_GEMM_RSTAGES_DW
 #define RGCN_GEMM_RSTAGES_DW 1
+#endif
+#ifndef RGCN_GEMM_RSTAGES_DMS
+#define RGCN_GEMM_RSTAGES_DMS 1
 #endif
 
 template <class Mma, class LA, class LB, class Epi, int STAGES = 2, int R = RGCN_GEMM_RSTAGES>
@@ -672,8 +672,8 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_
         using TL = TileBf16;
         LoadRowsF32Split<TL> la{pa, d_out};
         LoadRows<TL, SlotRows, true> lb{sr, (int64_t)d_out * 2, (int64_t)d_out * 2};
-        return launch_gemm<MmaBf16<TL>>(la, lb, epi, M, N, 2 * (int64_t)d_out, 1,
-                                        2 * (int64_t)d_out, s);
+        return launch_gemm<MmaBf16<TL>, decltype(la), decltype(lb), EpiDms, 2, RGCN_GEMM_RSTAGES_DMS>(
+            la, lb, epi, M, N, 2 * (int64_t)d_out, 1, 2 * (int64_t)d_out, s);
     }
     using TL = TileF32;
     LoadRows<TL, PlainRows> la{pa, (int64_t)d_out * 4, 0};
