@@ -24,9 +24,10 @@ _SRC = os.path.join(_HERE, "rgcn_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
-# Degree keys of the schedules: key = SCHED_BUCKETS - 1 - min(deg, SCHED_BUCKETS - 1), so a
-# stable ascending sort lists the heaviest segments first.
-SCHED_BUCKETS = 64
+# Schedule keys: segments of at most 32 edges share the last key; heavier segments get one
+# key per power of two of their degree, heaviest first; a stable ascending sort by key
+# lists the heavy segments first and leaves the rest in enumeration order.
+SCHED_BUCKETS = 32
 
 
 def build(force: bool = True) -> str:
@@ -227,9 +228,14 @@ def stable_bucket_order(key: np.ndarray, nbuckets: int) -> np.ndarray:
 
 
 def degree_key(deg: np.ndarray) -> np.ndarray:
-    """Schedule key of a segment of degree deg: heaviest first, degrees >= 63 share key 0."""
-    return (SCHED_BUCKETS - 1 - np.minimum(deg.astype(np.int64), SCHED_BUCKETS - 1)).astype(
-        np.int32)
+    """Schedule key of a segment of degree deg: SCHED_BUCKETS - 1 for deg <= 32, else
+    SCHED_BUCKETS - 2 - (floor(log2 deg) - 5), at least 0."""
+    d = np.asarray(deg, dtype=np.int64)
+    out = np.full(d.shape, SCHED_BUCKETS - 1, dtype=np.int64)
+    heavy = d > 32
+    lg = np.floor(np.log2(np.where(heavy, d, 1).astype(np.float64))).astype(np.int64)
+    out[heavy] = np.maximum(SCHED_BUCKETS - 2 - (lg[heavy] - 5), 0)
+    return out.astype(np.int32)
 
 
 def forward_segments(block):
@@ -259,7 +265,8 @@ def forward_segments(block):
 
 
 def forward_schedule(block) -> np.ndarray:
-    """Segment ids in the library's forward processing order (heaviest degree first)."""
+    """Segment ids in the library's forward processing order: segments of more than 32
+    edges first, heaviest power of two first; everything else in enumeration order."""
     _, _, _, deg = forward_segments(block)
     return stable_bucket_order(degree_key(deg), SCHED_BUCKETS)
 

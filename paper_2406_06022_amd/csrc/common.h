@@ -53,7 +53,7 @@ __device__ __forceinline__ int64_t xcd_major_id(int64_t wg, int64_t total) {
 constexpr int kMaxTypes = RGCN_MAX_TYPES;
 constexpr int kMaxRels = RGCN_MAX_RELS;
 constexpr int kMaxSlots = RGCN_MAX_TYPES + RGCN_MAX_RELS;  // forward slots: self + relations
-constexpr int kSchedBuckets = 64;                          // degree keys 0..63
+constexpr int kSchedBuckets = 32;                          // schedule keys 0..31
 
 // A forward slot: the self-loop rows of a destination type, or the rows of one relation.
 struct FwdSlot {

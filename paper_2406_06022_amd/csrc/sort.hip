@@ -169,8 +169,14 @@ hipError_t bucket_sort(const KeyFn &kf, const PutFn &put, int64_t n, void *temp,
     return hipGetLastError();
 }
 
+// Schedule key of a segment of degree deg: segments of at most 32 edges share the last key
+// (they keep their enumeration order, so neighbours stay together); heavier ones come
+// first, one key per power of two, heaviest first.
 __device__ __forceinline__ int degree_key(int64_t deg) {
-    return kSchedBuckets - 1 - (int)(deg < kSchedBuckets - 1 ? deg : kSchedBuckets - 1);
+    if (deg <= 32) return kSchedBuckets - 1;
+    const int lg = 63 - __clzll((unsigned long long)deg);   // floor(log2 deg) >= 5
+    const int k = (kSchedBuckets - 2) - (lg - 5);
+    return k > 0 ? k : 0;
 }
 
 // Forward segments: key of segment id = degree key of its (slot, row).
@@ -334,7 +340,7 @@ hipError_t fwd_schedule(const FwdSlot *slots_host, int nslots, int64_t n_seg, in
         kf.base[i] = i < nslots ? slots_host[i].seg_base : 0;
         kf.indptr[i] = i < nslots ? slots_host[i].indptr : nullptr;
     }
-    return bucket_sort<kSchedBuckets, 6>(kf, PutIndex{order}, n_seg, temp, s);
+    return bucket_sort<kSchedBuckets, 5>(kf, PutIndex{order}, n_seg, temp, s);
 }
 
 hipError_t fwd_descriptors(const FwdSlot *slots_host, int nslots, const int32_t *order,
@@ -361,7 +367,7 @@ hipError_t fwd_descriptors(const FwdSlot *slots_host, int nslots, const int32_t 
 
 hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, void *temp,
                         hipStream_t s) {
-    return bucket_sort<kSchedBuckets, 6>(BwdKey{rels}, PutIndex{order}, n_rows, temp, s);
+    return bucket_sort<kSchedBuckets, 5>(BwdKey{rels}, PutIndex{order}, n_rows, temp, s);
 }
 
 // Digit plan of an LSD radix sort of keys < key_range: the fewest passes of at most 10

@@ -372,8 +372,8 @@ def test_bucket_order_is_a_stable_sort(orc):
         got = orc.stable_bucket_order(key, 64)
         want = sorted(range(n), key=lambda x: int(key[x]))
         assert got.tolist() == want
-    deg = np.array([0, 1, 62, 63, 64, 1000, 5])
-    assert orc.degree_key(deg).tolist() == [63, 62, 1, 0, 0, 0, 58]
+    deg = np.array([0, 1, 5, 32, 33, 63, 64, 127, 128, 1000, 2 ** 31 - 1])
+    assert orc.degree_key(deg).tolist() == [31, 31, 31, 31, 30, 30, 29, 29, 28, 26, 5]
 
 
 def test_invalid_blocks_are_rejected(orc):
@@ -420,3 +420,16 @@ def test_sub_block_preserves_kept_rows(orc):
                                    atol=1e-12)
     for r in range(3):
         np.testing.assert_allclose(gs["dw_rel"][r], g["dw_rel"][r], rtol=1e-12, atol=1e-12)
+
+
+def test_forward_schedule_heavy_first_by_hand(orc):
+    """One type, six destination rows, one relation with degrees 1, 40, 3, 100, 33, 64.
+    Segments 0-5 are the self-loop rows (degree 1), 6-11 the relation's rows.  Keys: 31 up
+    to degree 32, 30 for 33-63, 29 for 64-127.  Worked by hand: the relation rows of degree
+    100 and 64 (segments 9, 11), then 40 and 33 (7, 10), then the rest in order."""
+    degs = [1, 40, 3, 100, 33, 64]
+    indptr = np.concatenate([[0], np.cumsum(degs)]).astype(np.int32)
+    indices = np.concatenate([np.arange(d) for d in degs]).astype(np.int32)
+    blk = _B([120], [6], [_R(0, 0, indptr, indices)])
+    assert orc.forward_schedule(blk).tolist() == [9, 11, 7, 10, 0, 1, 2, 3, 4, 5, 6, 8]
+    assert orc.backward_schedule(blk, [0])[:3].tolist() == [0, 1, 2]  # every source: degree <= 6
