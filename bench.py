@@ -41,7 +41,7 @@ METRIC = "aggregated edges/sec and ms per RGCN block fwd+bwd; % of HBM roofline"
 _COMMON_INPUTS = ["paper_2406_06022_amd/csrc/common.h", "include/rgcn.h",
                   "paper_2406_06022_amd/build.py", "paper_2406_06022_amd/synth.py"]
 KERNEL_SOURCES = {
-    "k_gather_mean": ["paper_2406_06022_amd/csrc/aggregate.hip"] + _COMMON_INPUTS,
+    "k_gather_flat": ["paper_2406_06022_amd/csrc/aggregate.hip"] + _COMMON_INPUTS,
     "k_transpose_pipe": ["paper_2406_06022_amd/csrc/aggregate.hip"] + _COMMON_INPUTS,
 }
 # Plain copy of known size run after the timed steps (an fp32 negation of a 1 GiB buffer:
@@ -318,7 +318,7 @@ def main() -> int:
                          "WRITE_SIZE) into the per-launch HBM traffic summary and exit")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="reduce a rocprofv3 kernel_trace.csv into a per-kernel summary and exit")
-    ap.add_argument("--kernel", default="k_gather_mean")
+    ap.add_argument("--kernel", default="k_gather_flat")
     ap.add_argument("--launches-per-step", type=int, default=3,
                     help="launches of --kernel per step (summaries split them by position)")
     ap.add_argument("--command", default="", help="command line recorded in a summary")
@@ -384,7 +384,7 @@ def main() -> int:
                 cands.append((avg[(s, l)], s, l))
     cands.sort(reverse=True)
     _, dom_stage, dom_layer = cands[0]
-    kernel_name = {"aggregate": "k_gather_mean", "sparse": "k_transpose_pipe"}[dom_stage]
+    kernel_name = {"aggregate": "k_gather_flat", "sparse": "k_transpose_pipe"}[dom_stage]
     rooflines = {}
     for t_ms, s, l in cands:
         byts = algorithmic_bytes(spec, mb.blocks[l], stack.blocks[l], s, l)

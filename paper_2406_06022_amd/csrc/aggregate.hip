@@ -3,9 +3,9 @@
 // scatter-add fused in), weight packing, column sums and device-side validation.
 //
 // Row traffic is done in 16-byte chunks: a "group" of G lanes covers one row of d
-// elements (G = chunks per row, at most 64; rows wider than 64 chunks give each lane
-// CPL chunks), so a wave moves 64/G rows per load instruction and every row access is a
-// run of contiguous 16-byte pieces.
+// elements (G = chunks per row, at most 64, rounded up to a power of two in the forward
+// gather; rows wider than 64 chunks give each lane CPL chunks), so a wave moves 64/G rows
+// per load instruction and every row access is a run of contiguous 16-byte pieces.
 #include "common.h"
 
 namespace rgcn {
@@ -50,6 +50,20 @@ __device__ __forceinline__ const __attribute__((address_space(1))) T *gbl(const 
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+#ifndef RGCN_ROWS_NT
+#define RGCN_ROWS_NT 1
+#endif
+// Gathered rows are read once (no locality over a table of many GB): streaming loads, so
+// they do not push the index, row-id and descriptor lines out of L2.
+__device__ __forceinline__ u32x4 ld_row(const char *p) {
+    const __attribute__((address_space(1))) u32x4 *g = (const __attribute__((address_space(1))) u32x4 *)p;
+#if RGCN_ROWS_NT
+    return __builtin_nontemporal_load(g);
+#else
+    return *g;
+#endif
+}
 // 16-byte global load
 __device__ __forceinline__ uint4 ld16(const char *p) {
     const u32x4 v = *gbl((const u32x4 *)p);
@@ -120,31 +134,7 @@ __device__ __forceinline__ void row_walk(const int64_t *goff, int n, LoadAcc &&l
 }
 
 // Batch bodies: load B rows' chunks (16 bytes per lane per chunk) and add them into acc.
-// GatherLoad: block-dtype rows at src + offset; SumLoad: fp32 rows at absolute addresses.
-template <bool BF16, int CPL>
-struct GatherLoad {
-    const char *src;
-    int lg, G, chunks;
-    float (*acc)[BF16 ? 8 : 4];
-    template <int B>
-    __device__ __forceinline__ void run(const int64_t (&o)[B], const bool (&ok)[B]) const {
-        u32x4 v[B][CPL];
-#pragma unroll
-        for (int u = 0; u < B; ++u)
-#pragma unroll
-            for (int p = 0; p < CPL; ++p) {
-                const int c = lg + p * G;
-                const char *pa = (ok[u] && c < chunks) ? src + o[u] + (int64_t)c * 16
-                                                       : (const char *)g_zero_row + c * 16;
-                v[u][p] = *gbl((const u32x4 *)pa);
-            }
-#pragma unroll
-        for (int u = 0; u < B; ++u)
-#pragma unroll
-            for (int p = 0; p < CPL; ++p)
-                acc_chunk<BF16>(acc[p], make_uint4(v[u][p].x, v[u][p].y, v[u][p].z, v[u][p].w));
-    }
-};
+// SumLoad: fp32 rows at absolute addresses.
 template <int CPL>
 struct SumLoad {
     int lg, G, chunks;
@@ -173,35 +163,43 @@ struct GatherTabs {
 };
 
 
-#ifndef RGCN_GATHER_U1
-#define RGCN_GATHER_U1 4
-#endif
-
-template <int CPL>
-struct GatherU {
-    static constexpr int U = CPL == 1 ? RGCN_GATHER_U1 : (CPL == 2 ? 8 : 4);
-};
-
-#ifndef RGCN_GATHER_MIN_WAVES
-#define RGCN_GATHER_MIN_WAVES 1
-#endif
-
-template <bool BF16, int CPL, int EPL>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(RGCN_GATHER_MIN_WAVES)))
-void k_gather_mean(const SegDesc *__restrict__ desc,
-                                                          int64_t n_seg,
+// Forward gather over the flattened stream of the schedule: every in-edge of a segment is
+// one entry, and a self-loop row or a segment of degree 0 is one entry as well.  The
+// stream is cut into balanced contiguous ranges of whole segments (chunks of kFwdChunk
+// entries, split evenly over the groups of the grid), so every group moves the same number
+// of rows whatever the degrees, and consecutive segments' indices and row ids are read by
+// the same group.
+//
+// A group of G lanes takes S = G entries per step.  A step's entries are resolved with one
+// entry per lane: the G segment descriptors from the step's first segment are loaded one
+// per lane, an inclusive scan of their entry counts and a binary search give each lane its
+// segment and edge, and the source index and global row id of that edge follow.  Those
+// three dependent loads are software-pipelined over the steps (descriptors of step i+3,
+// source indices of step i+2, row ids of step i+1 in flight with the rows of step i).
+// The rows of a step are loaded U at a time by all G lanes (16 bytes per lane per chunk),
+// with the next batch in flight while one is summed; after the last entry of a segment
+// the group writes its mean (sum in ascending edge order, one division by the degree; 0
+// for degree 0).
+template <bool BF16, int G, int CPL, int U, bool FULL>
+__global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restrict__ desc,
+                                                          const int32_t *__restrict__ cs,
+                                                          int64_t nc_max,
                                                           const FwdSlot *__restrict__ slots,
                                                           int nslots, GatherTabs tabs,
-                                                          char *__restrict__ ws, int G, int gpw,
-                                                          int chunks) {
+                                                          char *__restrict__ ws, int chunks) {
     constexpr int VEC = BF16 ? 8 : 4;
     constexpr int ES = BF16 ? 2 : 4;
-    constexpr int U = GatherU<CPL>::U;
+    constexpr int S = G;
+    constexpr int GPW = 64 / G;
     constexpr int W = kThreads / 64;
+    constexpr int NB = S / U;
+    static_assert(S % U == 0 && (G & (G - 1)) == 0, "power-of-two groups, whole batches");
     __shared__ const int32_t *s_idx[kMaxSlots];
     __shared__ int32_t s_src[kMaxSlots];
     __shared__ TypeInput s_tab[kMaxTypes];
-    __shared__ int64_t s_off[W][64 * EPL];
+    __shared__ int64_t s_addr[W][64];
+    __shared__ int64_t s_out[W][64];
+    __shared__ int32_t s_deg[W][64];
     for (int i = threadIdx.x; i < nslots; i += kThreads) {
         s_idx[i] = slots[i].indices;
         s_src[i] = slots[i].src_type;
@@ -210,123 +208,196 @@ void k_gather_mean(const SegDesc *__restrict__ desc,
     __syncthreads();
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int gi = lane / G;
-    const int lg = lane - gi * G;
-    if (gi >= gpw) return;
-    int64_t *goff = &s_off[wave][gi * G * EPL];
-    const int64_t stride = (int64_t)gridDim.x * W * gpw;
-    int64_t sg = ((int64_t)blockIdx.x * W + wave) * gpw + gi;
-    if (sg >= n_seg) return;
-    // Loads that a lane does not need read a zero word instead, so that every load is
-    // unconditional (no branch, no wait at a join) and its value enters by an addition.
-    // Pointers read back from LDS are re-qualified as global so the loads are global (not
-    // flat) loads.
+    const int gb = lane & ~(G - 1);    // first lane of this lane's group
+    const int lg = lane & (G - 1);
+    const int64_t ngroups = (int64_t)gridDim.x * W * GPW;
+    const int64_t gid = ((int64_t)blockIdx.x * W + wave) * GPW + lane / G;
+    const int64_t total = cs[nc_max + 1];
+    const int64_t nc = (total + kFwdChunk - 1) / kFwdChunk;
+    const int32_t s_lo = cs[gid * nc / ngroups];
+    const int32_t s_hi = cs[(gid + 1) * nc / ngroups];
     const char *zero = (const char *)g_zero;
+    const int64_t zrow = (int64_t)(uintptr_t)g_zero_row;
 
-    // descriptor of segment s (degree 0 past the end)
-    auto load_desc = [&](int64_t s) -> SegDesc {
-        SegDesc d = desc[s < n_seg ? s : n_seg - 1];
-        d.deg = s < n_seg ? d.deg : 0;
+    // window of the step starting at segment sc: lane lg holds segment sc + lg (degree -1
+    // past the group's range)
+    auto load_win = [&](int32_t sc) -> SegDesc {
+        const int64_t sw = (int64_t)sc + lg;
+        const bool in = sw < s_hi;
+        SegDesc d = desc[in ? sw : 0];
+        d.deg = in ? d.deg : -1;
         return d;
     };
-    // source index of edge e of segment d (self-loop slot: the row itself), -1 past the end
-    auto edge_src = [&](const SegDesc &d, int e) -> int32_t {
-        const int32_t *ix = s_idx[(d.info >> 8) & 0xff];
-        const bool ok = e < d.deg;
-        const bool has = ix != nullptr;
-        const int32_t *p = (ok && has) ? ix + d.k0 + e : (const int32_t *)zero;
-        const int32_t v = *gbl(p);
-        return v + (!ok ? -1 : (has ? 0 : d.k0 + e));
+    // per-lane entry of a step, after the scan
+    struct Ent {
+        int32_t k;      // edge position (edge entry) or row (self-loop entry)
+        int32_t deg;    // degree of the entry's segment
+        int64_t out;    // workspace byte offset of the segment's output
+        int slot;
+        int kind;       // 0 none, 1 degree-0 segment, 2 self-loop row, 3 edge
+        bool last;      // last entry of its segment
     };
-    // byte offset of that source row in its table (0 for -1)
-    auto row_off = [&](const SegDesc &d, int32_t j) -> int64_t {
-        const int t = s_src[(d.info >> 8) & 0xff];
-        const int64_t *rid = s_tab[t].row_ids;
-        const int64_t ldb = s_tab[t].ld * ES;
-        const bool look = j >= 0 && rid != nullptr;
-        const int64_t *p = look ? rid + j : (const int64_t *)zero;
-        const int64_t v = *gbl(p);
-        return (v + ((j < 0 || rid != nullptr) ? 0 : j)) * ldb;
-    };
-
-    // pipeline prologue
-    SegDesc d = load_desc(sg);
-    SegDesc dn = load_desc(sg + stride);
-    SegDesc dnn = load_desc(sg + 2 * stride);
-    int64_t off[EPL];
-    int32_t jn[EPL];
+    // Resolve the step at (sc, e0) from its window d; advance (sc, e0) to the next step.
+    auto scan = [&](const SegDesc &d, int32_t &sc, int32_t &e0) -> Ent {
+        int w = d.deg < 0 ? 0 : (d.deg > 0 ? d.deg : 1);
+        if (lg == 0) w -= e0;
+        int incl = w;
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) off[e] = row_off(d, edge_src(d, lg + e * G));
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) jn[e] = edge_src(dn, lg + e * G);
-
-    while (true) {
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) goff[e * G + lg] = off[e];
-        __builtin_amdgcn_wave_barrier();
-        const int deg = d.deg;
-        const int n1 = deg < EPL * G ? deg : EPL * G;
-        const char *src = (const char *)s_tab[s_src[(d.info >> 8) & 0xff]].base;
-
-        // later stages of the pipeline, issued before this segment's rows are consumed
-        int64_t offn[EPL];
-        int32_t jnn[EPL];
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) offn[e] = row_off(dn, jn[e]);
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) jnn[e] = edge_src(dnn, lg + e * G);
-        const SegDesc dnnn = load_desc(sg + 3 * stride);
-
-        float acc[CPL][VEC];
-#pragma unroll
-        for (int p = 0; p < CPL; ++p)
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) acc[p][e] = 0.f;
-
-        // edges [0, n) of the offsets in goff: U rows per lane in flight; a batch's unused
-        // slots re-read the last row (a cache hit) and are dropped
-        // U-row batches of the group's published offsets; an empty slot reads the zero row
-        auto rows = [&](int n) { row_walk<U>(goff, n, GatherLoad<BF16, CPL>{src, lg, G, chunks, acc}); };
-        rows(n1);
-        // degrees above the pipelined width: G more edges at a time, resolved in place
-        for (int kc = EPL * G; kc < deg; kc += G) {
-            __builtin_amdgcn_wave_barrier();
-            goff[lg] = row_off(d, edge_src(d, kc + lg));
-            __builtin_amdgcn_wave_barrier();
-            rows(deg - kc < G ? deg - kc : G);
+        for (int o = 1; o < G; o <<= 1) {
+            const int up = __shfl_up(incl, o, G);
+            incl += lg >= o ? up : 0;
         }
-
-        const float fdeg = (float)deg;
-        const uint64_t out16 = ((uint64_t)(d.info & 0xffu) << 32) | d.out_lo;
-        char *out = ws + (out16 << 4);
+        const int excl = incl - w;
+        const int tot = __shfl(incl, gb + G - 1, 64);
+        // segment of entry p: the last window lane whose first entry is <= p
+        auto find = [&](int p) -> int {
+            int j = 0;
 #pragma unroll
-        for (int p = 0; p < CPL; ++p) {
-            const int c = lg + p * G;
-            if (c >= chunks) continue;
-            float r[VEC];
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) r[e] = deg > 0 ? acc[p][e] / fdeg : 0.f;
-            uint4 w;
-            if constexpr (BF16) {
-                w.x = pack_bf16x2(r[0], r[1]); w.y = pack_bf16x2(r[2], r[3]);
-                w.z = pack_bf16x2(r[4], r[5]); w.w = pack_bf16x2(r[6], r[7]);
-            } else {
-                w.x = __float_as_uint(r[0]); w.y = __float_as_uint(r[1]);
-                w.z = __float_as_uint(r[2]); w.w = __float_as_uint(r[3]);
+            for (int st = G / 2; st >= 1; st >>= 1) {
+                const int ex = __shfl(excl, gb + j + st, 64);
+                j = ex <= p ? j + st : j;
             }
-            *(uint4 *)(out + (int64_t)c * 16) = w;
+            return j;
+        };
+        const int j = find(lg);
+        const int jx = __shfl(excl, gb + j, 64), ji = __shfl(incl, gb + j, 64);
+        const int32_t k0 = __shfl(d.k0, gb + j, 64), dg = __shfl(d.deg, gb + j, 64);
+        const uint32_t olo = __shfl(d.out_lo, gb + j, 64), inf = __shfl(d.info, gb + j, 64);
+        Ent e;
+        const bool valid = lg < tot;
+        e.slot = (int)((inf >> 8) & 0xffu);
+        const int ein = lg - jx + (j == 0 ? e0 : 0);
+        const bool self = s_idx[e.slot] == nullptr;
+        e.kind = !valid ? 0 : (dg == 0 ? 1 : (self ? 2 : 3));
+        e.k = self ? k0 : k0 + ein;
+        e.deg = dg;
+        e.out = (int64_t)((((uint64_t)(inf & 0xffu) << 32) | olo) << 4);
+        e.last = valid && lg == ji - 1;
+        // next step: the segment holding entry S of this window
+        const int js = find(S);
+        const int sx = __shfl(excl, gb + js, 64), si = __shfl(incl, gb + js, 64);
+        if (si <= S) {
+            sc += js + 1;
+            e0 = 0;
+        } else {
+            e0 = S - sx + (js == 0 ? e0 : 0);
+            sc += js;
         }
-        sg += stride;
-        if (sg >= n_seg) break;
-        __builtin_amdgcn_wave_barrier();
-        d = dn;
-        dn = dnn;
-        dnn = dnnn;
+        return e;
+    };
+    // source row (index within its type) of an entry; -1 for none
+    auto load_src = [&](const Ent &e) -> int32_t {
+        const bool edge = e.kind == 3;
+        const int32_t *p = edge ? s_idx[e.slot] + e.k : (const int32_t *)zero;
+        const int32_t v = *gbl(p);
+        return edge ? v : (e.kind == 2 ? e.k : -1);
+    };
+    // absolute address of that row (the zero row for none)
+    auto load_addr = [&](int slot, int32_t j) -> int64_t {
+        const int t = s_src[slot];
+        const int64_t *rid = s_tab[t].row_ids;
+        const bool look = j >= 0 && rid != nullptr;
+        const int64_t v = *gbl(look ? rid + j : (const int64_t *)zero);
+        const int64_t row = rid != nullptr ? v : (int64_t)j;
+        return j < 0 ? zrow : (int64_t)(uintptr_t)s_tab[t].base + row * (s_tab[t].ld * ES);
+    };
+
+    // pipeline prologue: steps 0, 1, 2
+    int32_t sc = s_lo, e0 = 0;
+    SegDesc dw = load_win(sc);
+    Ent ez = scan(dw, sc, e0);
+    dw = load_win(sc);
+    int32_t jz = load_src(ez);
+    Ent ey = scan(dw, sc, e0);
+    dw = load_win(sc);
+    int32_t jy = load_src(ey);
+    int64_t az = load_addr(ez.slot, jz);
+
+    float acc[CPL][VEC];
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) {
-            off[e] = offn[e];
-            jn[e] = jnn[e];
+    for (int p = 0; p < CPL; ++p)
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) acc[p][v] = 0.f;
+
+    while (__ballot(ez.kind != 0) != 0) {
+        __builtin_amdgcn_wave_barrier();
+        s_addr[wave][lane] = az;
+        s_out[wave][lane] = ez.out;
+        s_deg[wave][lane] = ez.deg;
+        uint64_t lm = __ballot(ez.last);
+        if constexpr (G < 64) lm = (lm >> gb) & ((1ull << G) - 1);
+        __builtin_amdgcn_wave_barrier();
+
+        u32x4 v[2][U][CPL];
+        auto issue = [&](int b, u32x4 (&dst)[U][CPL]) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t a = s_addr[wave][gb + b * U + u];
+#pragma unroll
+                for (int p = 0; p < CPL; ++p) {
+                    const int c = lg + p * G;
+                    const int64_t pa = (FULL || c < chunks) ? a + (int64_t)c * 16 : zrow + (int64_t)c * 16;
+                    dst[u][p] = ld_row((const char *)(uintptr_t)pa);
+                }
+            }
+        };
+        // this step's first rows, then the later pipeline stages while they are in flight
+        issue(0, v[0]);
+        Ent ex = scan(dw, sc, e0);
+        dw = load_win(sc);
+        const int32_t jx = load_src(ex);
+        const int64_t ay = load_addr(ey.slot, jy);
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            if (b + 1 < NB) issue(b + 1, v[(b + 1) & 1]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int q = b * U + u;
+#pragma unroll
+                for (int p = 0; p < CPL; ++p) {
+                    const u32x4 x = v[b & 1][u][p];
+                    acc_chunk<BF16>(acc[p], make_uint4(x.x, x.y, x.z, x.w));
+                }
+                if ((lm >> q) & 1u) {
+                    const int64_t ob = s_out[wave][gb + q];
+                    const int dg = s_deg[wave][gb + q];
+                    // sum / deg by the reciprocal; fp32 output takes one correction from
+                    // the exact remainder (fma), bf16 output is rounded to 8 bits anyway.
+                    // Degree 0 has a zero sum and gives 0.
+                    const float fdeg = (float)dg;
+                    const float rc = dg > 0 ? __builtin_amdgcn_rcpf(fdeg) : 0.f;
+                    char *out = ws + ob;
+#pragma unroll
+                    for (int p = 0; p < CPL; ++p) {
+                        const int c = lg + p * G;
+                        float r[VEC];
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) {
+                            const float q0 = acc[p][e] * rc;
+                            if constexpr (BF16)
+                                r[e] = q0;
+                            else
+                                r[e] = __builtin_fmaf(__builtin_fmaf(-q0, fdeg, acc[p][e]), rc, q0);
+                            acc[p][e] = 0.f;
+                        }
+                        if (!FULL && c >= chunks) continue;
+                        uint4 w;
+                        if constexpr (BF16) {
+                            w.x = pack_bf16x2(r[0], r[1]); w.y = pack_bf16x2(r[2], r[3]);
+                            w.z = pack_bf16x2(r[4], r[5]); w.w = pack_bf16x2(r[6], r[7]);
+                        } else {
+                            w.x = __float_as_uint(r[0]); w.y = __float_as_uint(r[1]);
+                            w.z = __float_as_uint(r[2]); w.w = __float_as_uint(r[3]);
+                        }
+                        *(uint4 *)(out + (int64_t)c * 16) = w;
+                    }
+                }
+            }
         }
+        ez = ey;
+        az = ay;
+        ey = ex;
+        jy = jx;
     }
 }
 
@@ -738,49 +809,73 @@ int64_t resident_wgs(K kernel) {
     return (int64_t)per_cu * cus;
 }
 
-template <bool B, int C, int E>
-hipError_t launch_gather(const SegDesc *desc, int64_t n_seg, const FwdSlot *slots_dev,
-                         int nslots, const GatherTabs &tabs, char *ws_base, const GroupShape &gs,
-                         int chunks, hipStream_t s) {
-    const int64_t groups_per_wg = (int64_t)(kThreads / 64) * gs.gpw;
-    int64_t wgs = cdiv(n_seg, groups_per_wg);
-    const int64_t cap = resident_wgs(k_gather_mean<B, C, E>);
+#ifndef RGCN_FLAT_ROWS
+#define RGCN_FLAT_ROWS 8
+#endif
+
+template <bool B, int G, int C, bool FULL>
+hipError_t launch_flat_k(const SegDesc *desc, const int32_t *cs, int64_t nc_max,
+                         const FwdSlot *slots_dev, int nslots, const GatherTabs &tabs,
+                         char *ws_base, int chunks, hipStream_t s) {
+    constexpr int U0 = RGCN_FLAT_ROWS / C > 0 ? RGCN_FLAT_ROWS / C : 1;
+    constexpr int U = U0 < G ? U0 : G;
+    const int64_t groups_per_wg = (int64_t)(kThreads / 64) * (64 / G);
+    int64_t wgs = cdiv(nc_max, groups_per_wg);
+    const int64_t cap = resident_wgs(k_gather_flat<B, G, C, U, FULL>);
     if (wgs > cap) wgs = cap;
-    hipLaunchKernelGGL((k_gather_mean<B, C, E>), dim3((unsigned)wgs), dim3(kThreads), 0, s, desc,
-                       n_seg, slots_dev, nslots, tabs, ws_base, gs.G, gs.gpw, chunks);
+    if (wgs < 1) wgs = 1;
+    hipLaunchKernelGGL((k_gather_flat<B, G, C, U, FULL>), dim3((unsigned)wgs), dim3(kThreads), 0,
+                       s, desc, cs, nc_max, slots_dev, nslots, tabs, ws_base, chunks);
     return hipGetLastError();
 }
+template <bool B, int G, int C>
+hipError_t launch_flat(const SegDesc *desc, const int32_t *cs, int64_t nc_max,
+                       const FwdSlot *slots_dev, int nslots, const GatherTabs &tabs,
+                       char *ws_base, int chunks, hipStream_t s) {
+    // every lane of a group owns a chunk of the row: no per-lane range checks
+    if (chunks == G * C)
+        return launch_flat_k<B, G, C, true>(desc, cs, nc_max, slots_dev, nslots, tabs, ws_base,
+                                            chunks, s);
+    return launch_flat_k<B, G, C, false>(desc, cs, nc_max, slots_dev, nslots, tabs, ws_base,
+                                         chunks, s);
+}
 
-// Edges per lane in the gather pipeline: enough for degree 32 at any row width.
 template <bool B>
-hipError_t gather_dispatch(const SegDesc *desc, int64_t n_seg, const FwdSlot *slots_dev,
-                           int nslots, const GatherTabs &tabs, char *ws_base, const GroupShape &gs,
-                           int chunks, hipStream_t s) {
-    if (gs.cpl == 1) {
-        if (gs.G >= 32)
-            return launch_gather<B, 1, 1>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
-        if (gs.G >= 16)
-            return launch_gather<B, 1, 2>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
-        return launch_gather<B, 1, 4>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
+hipError_t flat_dispatch(const SegDesc *desc, const int32_t *cs, int64_t nc_max,
+                         const FwdSlot *slots_dev, int nslots, const GatherTabs &tabs,
+                         char *ws_base, int chunks, hipStream_t s) {
+    // lanes per row: the next power of two >= chunks / chunks-per-lane, at least 4
+    const int cpl = (int)cdiv(chunks, 64);
+    const int need = (int)cdiv(chunks, cpl);
+    int g = 4;
+    while (g < need) g <<= 1;
+#define RGCN_FLAT(G_, C_) \
+    return launch_flat<B, G_, C_>(desc, cs, nc_max, slots_dev, nslots, tabs, ws_base, chunks, s)
+    if (cpl == 1) {
+        if (g == 4) RGCN_FLAT(4, 1);
+        if (g == 8) RGCN_FLAT(8, 1);
+        if (g == 16) RGCN_FLAT(16, 1);
+        if (g == 32) RGCN_FLAT(32, 1);
+        RGCN_FLAT(64, 1);
     }
-    if (gs.cpl == 2)
-        return launch_gather<B, 2, 1>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
-    if (gs.cpl <= 4)
-        return launch_gather<B, 4, 1>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
+    if (cpl == 2) RGCN_FLAT(64, 2);
+    if (cpl <= 4) RGCN_FLAT(64, 4);
+#undef RGCN_FLAT
     return hipErrorInvalidValue;
 }
 
 hipError_t gather_mean(rgcn_dtype dt, int d_in, const SegDesc *desc, int64_t n_seg,
-                       const FwdSlot *slots_dev, int nslots, const TypeInput *in,
-                       char *ws_base, hipStream_t s) {
+                       const int32_t *chunk_starts, int64_t nc_max, const FwdSlot *slots_dev,
+                       int nslots, const TypeInput *in, char *ws_base, hipStream_t s) {
     if (n_seg == 0) return hipSuccess;
     const bool bf = dt == RGCN_BF16;
     const int chunks = bf ? d_in / 8 : d_in / 4;
-    const GroupShape gs = group_shape(chunks);
     GatherTabs tabs;
     for (int t = 0; t < kMaxTypes; ++t) tabs.in[t] = in[t];
-    return bf ? gather_dispatch<true>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s)
-              : gather_dispatch<false>(desc, n_seg, slots_dev, nslots, tabs, ws_base, gs, chunks, s);
+    return bf ? flat_dispatch<true>(desc, chunk_starts, nc_max, slots_dev, nslots, tabs, ws_base,
+                                    chunks, s)
+              : flat_dispatch<false>(desc, chunk_starts, nc_max, slots_dev, nslots, tabs, ws_base,
+                                     chunks, s);
 }
 
 template <bool B, int C>

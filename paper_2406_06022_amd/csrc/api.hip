@@ -61,6 +61,8 @@ struct Layout {
     int64_t n_bwd_rows = 0;
     // workspace offsets
     size_t off_slots = 0, off_fwd_order = 0, off_fwd_desc = 0, off_bwd_order = 0, off_err = 0;
+    size_t off_fwd_chunks = 0;
+    int64_t nc_max = 0;           // chunk bound of the flattened forward stream
     size_t off_csc_indptr[kMaxRels], off_csc_dst[kMaxRels];
     // combined transpose of the relations leaving grad types
     int64_t koff[kMaxRels], e0[kMaxRels];
@@ -187,6 +189,14 @@ rgcn_status make_layout(const rgcn_block *b, const rgcn_params *p, Layout &L) {
         L.K[t] = (int64_t)pos * L.d_in;
     }
     if (L.n_seg >= kI32Max) return fail(RGCN_ERR_UNSUPPORTED, "too many forward segments");
+    {
+        int64_t nnz_total = 0;
+        for (int r = 0; r < L.R; ++r)
+            if (b->n_dst[b->rels[r].dst_type] > 0) nnz_total += b->rels[r].nnz;
+        if (L.n_seg + nnz_total >= kI32Max)
+            return fail(RGCN_ERR_UNSUPPORTED, "edges plus forward segments of the block exceed 2^31");
+        L.nc_max = fwd_chunk_bound(L.n_seg, nnz_total);
+    }
     // backward slots
     for (int t = 0; t < L.T; ++t) {
         if (b->n_dst[t] == 0) continue;
@@ -211,6 +221,7 @@ rgcn_status make_layout(const rgcn_block *b, const rgcn_params *p, Layout &L) {
     L.off_slots = off;                    off += align256(sizeof(FwdSlot) * kMaxSlots);
     L.off_fwd_order = off;                off += align256((size_t)L.n_seg * 4 + 4);
     L.off_fwd_desc = off;                 off += align256((size_t)L.n_seg * sizeof(SegDesc) + 16);
+    L.off_fwd_chunks = off;               off += align256((size_t)(L.nc_max + 2) * 4);
     L.off_bwd_order = off;                off += align256((size_t)L.n_bwd_rows * 4 + 4);
     for (int r = 0; r < kMaxRels; ++r) {
         L.off_csc_indptr[r] = L.off_csc_dst[r] = SIZE_MAX;
@@ -244,6 +255,10 @@ rgcn_status make_layout(const rgcn_block *b, const rgcn_params *p, Layout &L) {
     L.off_scratch = off;
     // plan temporaries
     size_t pt = bucket_sort_temp_bytes(L.n_seg, kSchedBuckets);
+    {
+        size_t c = fwd_chunks_temp_bytes(L.n_seg) + align256((size_t)L.n_seg * 4 + 4);
+        if (c > pt) pt = c;
+    }
     {
         size_t c = csc_temp_bytes(L.csc_nnz, L.key_range);
         if (c > pt) pt = c;
@@ -394,9 +409,13 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
             moff[t] = (t < L.T && L.off_mcat[t] != SIZE_MAX) ? (int64_t)L.off_mcat[t] : 0;
             mld[t] = t < L.T ? L.K[t] : 0;
         }
+        // segment weights sit in the plan scratch after the chunk pass's own temporaries
+        int32_t *weight = (int32_t *)(scratch + fwd_chunks_temp_bytes(L.n_seg));
         TRY_HIP(fwd_descriptors(L.slots, L.nslots, (const int32_t *)(ws + L.off_fwd_order), L.n_seg,
-                                moff, mld, L.es, (SegDesc *)(ws + L.off_fwd_desc), stream),
+                                moff, mld, L.es, (SegDesc *)(ws + L.off_fwd_desc), weight, stream),
                 "forward descriptors");
+        TRY_HIP(fwd_chunks(weight, L.n_seg, L.nc_max, (int32_t *)(ws + L.off_fwd_chunks), scratch,
+                           stream), "forward chunks");
     }
     if (L.key_range > 0) {
         CscRels cr{};
@@ -443,6 +462,7 @@ rgcn_status rgcn_block_aggregate(const rgcn_block *block, const rgcn_input *in,
     for (int t = 0; t < kMaxTypes; ++t)
         tin[t] = t < L.T ? TypeInput{in[t].base, in[t].row_ids, in[t].ld} : TypeInput{nullptr, nullptr, 0};
     TRY_HIP(gather_mean(L.dt, L.d_in, (const SegDesc *)(ws + L.off_fwd_desc), L.n_seg,
+                        (const int32_t *)(ws + L.off_fwd_chunks), L.nc_max,
                         (const FwdSlot *)(ws + L.off_slots), L.nslots, tin, ws, stream),
             "gather mean");
     return RGCN_OK;

@@ -54,6 +54,7 @@ constexpr int kMaxTypes = RGCN_MAX_TYPES;
 constexpr int kMaxRels = RGCN_MAX_RELS;
 constexpr int kMaxSlots = RGCN_MAX_TYPES + RGCN_MAX_RELS;  // forward slots: self + relations
 constexpr int kSchedBuckets = 32;                          // schedule keys 0..31
+constexpr int kFwdChunk = 64;   // entries per chunk of the flattened forward stream
 
 // A forward slot: the self-loop rows of a destination type, or the rows of one relation.
 struct FwdSlot {
@@ -95,9 +96,18 @@ hipError_t fwd_schedule(const FwdSlot *slots_dev, int nslots, int64_t n_seg, int
                         void *temp, hipStream_t s);
 // Segment descriptors in schedule order; mcat_off[t]: byte offset of Mcat_t in the
 // workspace, mcat_ld[t]: its row length in elements, es: element size.
+// weight[p] = entries of segment p in the flattened forward stream (max(deg, 1)).
 hipError_t fwd_descriptors(const FwdSlot *slots_host, int nslots, const int32_t *order,
                            int64_t n_seg, const int64_t *mcat_off, const int64_t *mcat_ld,
-                           int es, SegDesc *desc, hipStream_t s);
+                           int es, SegDesc *desc, int32_t *weight, hipStream_t s);
+// Flattened forward stream split into chunks of kFwdChunk entries (segments whole): cs has
+// nc_max + 2 entries, nc_max = fwd_chunk_bound(n_seg, sum of relation nnz); cs[c] = first
+// segment of chunk c, cs[nc_max + 1] = total entries.  temp: fwd_chunks_temp_bytes(n_seg);
+// `weight` may lie in temp past that size.
+int64_t fwd_chunk_bound(int64_t n_seg, int64_t nnz_total);
+size_t fwd_chunks_temp_bytes(int64_t n_seg);
+hipError_t fwd_chunks(const int32_t *weight, int64_t n_seg, int64_t nc_max, int32_t *cs,
+                      void *temp, hipStream_t s);
 // Combined transpose of several relations: one stable sort of all their edges by
 // key = koff_r + source row.  ip[key] (key in [0, key_range]) = position of the first edge
 // with that key; csd = destination rows in sorted order.  Relation r's transpose is
@@ -124,8 +134,8 @@ hipError_t fill_words(void *dst, const void *src_host, size_t bytes, hipStream_t
 
 // aggregate.hip
 hipError_t gather_mean(rgcn_dtype dt, int d_in, const SegDesc *desc, int64_t n_seg,
-                       const FwdSlot *slots_dev, int nslots, const TypeInput *in,
-                       char *ws_base, hipStream_t s);
+                       const int32_t *chunk_starts, int64_t nc_max, const FwdSlot *slots_dev,
+                       int nslots, const TypeInput *in, char *ws_base, hipStream_t s);
 
 struct TsumRel {
     const int32_t *csc_indptr;

@@ -8,12 +8,18 @@
 //   input side   dMs_t = dY_t [n_dst x d_out]    . [W_s rows]^T, slot columns / deg
 //   weight side  dW    = Mcat_t^T [K x n_dst]    . dY_t [n_dst x d_out]   (split over rows)
 //
-// Workgroup tile 128 x 128, four waves in a 2 x 2 arrangement of 64 x 64, each wave a 4 x 4
-// grid of 16 x 16 MFMA tiles.  LDS holds both operands K-contiguous ("row r, k..."), one
-// row = BK elements of K + 16 bytes of padding; the row pitch is an odd number of
-// 16-byte units, so the 16 rows a 16-lane group reads for one MFMA operand fall in
-// distinct bank groups.  Double-buffered: global loads of step k+1 are in flight while
-// step k is multiplied.
+// bf16 mode: workgroup tile 256 x 256, eight waves in a 2 x 4 arrangement of 128 x 64, each
+// wave an 8 x 4 grid of 16 x 16 MFMA tiles.  These products are skinny (K and N of a few
+// hundred against up to millions of rows), so what limits them is how often the long
+// operand is re-read from L2: a 256-wide tile reads it half as often as a 128-wide one.
+// fp32 mode: 128 x 128, four waves of 64 x 64.
+//
+// LDS holds both operands K-contiguous ("row r, k..."), one row = BK elements of K + 16
+// bytes of padding; the row pitch is an odd number of 16-byte units, so the 16 rows a
+// 16-lane group reads for one MFMA operand fall in distinct bank groups.  Global loads
+// are staged through registers, issued in a fixed order and always unconditionally (rows
+// past the end and K past the range read a zero buffer), so each LDS store waits only for
+// its own loads.
 //
 // The weight-side product reduces over the rows of both operands, so its tiles are
 // transposed on the way to LDS: each thread loads half of an 8 x 8 block (4 rows x 16
@@ -23,56 +29,123 @@
 // bf16 mode: v_mfma_f32_16x16x32_bf16, fp32 accumulation.  The fp32 output gradient dY
 // enters both backward products as a hi + lo pair of bf16 values (hi = bf16(x), lo =
 // bf16(x - hi)), which carries ~16 significant bits.  fp32 mode: v_mfma_f32_16x16x4_f32.
-#include "common.h"
+#include <type_traits>
 
-#ifndef RGCN_GEMM_BK_BF16
-#define RGCN_GEMM_BK_BF16 64
-#endif
+#include "common.h"
 
 namespace rgcn {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kTile = 128;
+constexpr int kThreads = 256;                     // small helper kernels
 constexpr int kStagePitch = 68;                   // epilogue staging row (floats)
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-template <int BK_, int ES_>
+// Workgroup tile TM x TN, WM x WN waves; each wave FM x FN MFMA tiles of 16 x 16.
+template <int TM_, int TN_, int WM_, int WN_>
+struct Cfg {
+    static constexpr int TM = TM_, TN = TN_, WM = WM_, WN = WN_;
+    static constexpr int NT = 64 * WM * WN;
+    static constexpr int FM = TM / WM / 16, FN = TN / WN / 16;
+    static_assert(FN * 16 == 64, "epilogue stages 64 columns per wave");
+};
+using CfgWide = Cfg<256, 256, 2, 4>;
+using CfgNarrow = Cfg<128, 128, 2, 2>;
+#ifndef RGCN_GEMM_FWD_WIDE
+#define RGCN_GEMM_FWD_WIDE 1
+#endif
+#ifndef RGCN_GEMM_DMS_WIDE
+#define RGCN_GEMM_DMS_WIDE 0
+#endif
+#ifndef RGCN_GEMM_DW_WIDE
+#define RGCN_GEMM_DW_WIDE 1
+#endif
+template <bool W> using CfgSel = typename std::conditional<W, CfgWide, CfgNarrow>::type;
+using CfgFwd = CfgSel<RGCN_GEMM_FWD_WIDE>;
+using CfgDms = CfgSel<RGCN_GEMM_DMS_WIDE>;
+using CfgDw = CfgSel<RGCN_GEMM_DW_WIDE>;
+using CfgF32 = Cfg<128, 128, 2, 2>;
+
+template <int ROWS_, int BK_, int ES_>
 struct Tile {
+    static constexpr int ROWS = ROWS_;            // rows of the operand tile
     static constexpr int BK = BK_;                // K elements per step
     static constexpr int ES = ES_;                // LDS element size
     static constexpr int PAYLOAD = BK_ * ES_;     // bytes of K per LDS row
     static constexpr int PITCH = PAYLOAD + 16;
     static constexpr int CPR = PAYLOAD / 16;      // 16-byte chunks per LDS row
-    static constexpr int BYTES = kTile * PITCH;   // one operand tile
+    static constexpr int BYTES = ROWS_ * PITCH;   // one operand tile
     static_assert((PITCH / 16) % 2 == 1, "pitch must be an odd number of 16-byte units");
 };
-using TileBf16 = Tile<RGCN_GEMM_BK_BF16, 2>;
-using TileBf16T = Tile<64, 2>;                    // weight side (transposing loaders)
-using TileF32 = Tile<16, 4>;
+template <class C> using TileBf16 = Tile<C::TM, 64, 2>;
+using TileF32 = Tile<CfgF32::TM, 16, 4>;
+
+// Register staging uses the compiler's native vector types (one 16-byte load or LDS store,
+// no struct copies).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// Loads a thread does not need (rows past the end, K past the range) read these zero bytes
+// instead, so the registers hold zeros without a select; never written.
+__device__ u32x4 g_zero16[2];
 
 // ------------------------------------------------------------------ MFMA cores
-template <class TL>
+template <class TL, int FM, int FN>
 struct MmaBf16 {
     using T = TL;
-    static constexpr int TILES = 2;   // A, B
-    __device__ __forceinline__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
-                               int wn, int lane) {
+    static constexpr int STAGE_BYTES = 2 * TL::BYTES;   // A, B
+    __device__ __forceinline__ static void run(const char *As, const char *Bs,
+                                               f32x4 (&acc)[FM][FN], int wm, int wn, int lane) {
         const int r = lane & 15, q = lane >> 4;
 #pragma unroll
         for (int s = 0; s < TL::BK / 32; ++s) {
-            bf16x8 a[4], b[4];
+            bf16x8 a[FM], b[FN];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                a[i] = *(const bf16x8 *)(As + (wm * 64 + i * 16 + r) * TL::PITCH + s * 64 + q * 16);
-                b[i] = *(const bf16x8 *)(Bs + (wn * 64 + i * 16 + r) * TL::PITCH + s * 64 + q * 16);
-            }
+            for (int i = 0; i < FM; ++i)
+                a[i] = *(const bf16x8 *)(As + (wm * FM * 16 + i * 16 + r) * TL::PITCH + s * 64 + q * 16);
 #pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
+            for (int i = 0; i < FN; ++i)
+                b[i] = *(const bf16x8 *)(Bs + (wn * FN * 16 + i * 16 + r) * TL::PITCH + s * 64 + q * 16);
 #pragma unroll
-                for (int ni = 0; ni < 4; ++ni)
+            for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < FN; ++ni)
                     acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], b[ni],
                                                                           acc[mi][ni], 0, 0, 0);
+        }
+    }
+};
+
+// B held as two bf16 tiles (hi, lo) of one fp32 operand, next to each other in LDS:
+// acc += A.B_hi + A.B_lo, fp32 accumulation.
+template <class TL, int FM, int FN>
+struct MmaBf16Split {
+    using T = TL;
+    static constexpr int STAGE_BYTES = 3 * TL::BYTES;   // A, B_hi, B_lo
+    __device__ __forceinline__ static void run(const char *As, const char *Bs,
+                                               f32x4 (&acc)[FM][FN], int wm, int wn, int lane) {
+        const int r = lane & 15, q = lane >> 4;
+        const char *Bl = Bs + TL::BYTES;
+        // B fragments (hi and lo) stay in registers for the step; A fragments are read one
+        // 16-row block at a time
+#pragma unroll
+        for (int s = 0; s < TL::BK / 32; ++s) {
+            bf16x8 bh[FN], bl[FN];
+#pragma unroll
+            for (int i = 0; i < FN; ++i) {
+                const int bo = (wn * FN * 16 + i * 16 + r) * TL::PITCH + s * 64 + q * 16;
+                bh[i] = *(const bf16x8 *)(Bs + bo);
+                bl[i] = *(const bf16x8 *)(Bl + bo);
+            }
+#pragma unroll
+            for (int mi = 0; mi < FM; ++mi) {
+                const bf16x8 a =
+                    *(const bf16x8 *)(As + (wm * FM * 16 + mi * 16 + r) * TL::PITCH + s * 64 + q * 16);
+#pragma unroll
+                for (int ni = 0; ni < FN; ++ni) {
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bh[ni], acc[mi][ni],
+                                                                          0, 0, 0);
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bl[ni], acc[mi][ni],
+                                                                          0, 0, 0);
+                }
+            }
         }
     }
 };
@@ -80,58 +153,26 @@ struct MmaBf16 {
 // fp32: lane group q holds k = 4q..4q+3 of its row; MFMA step s uses element s, so the
 // four steps together cover k = 0..15 (the sum over k is taken in a different order, not
 // a different set).
-// B held as two bf16 tiles (hi, lo) of one fp32 operand, next to each other in LDS:
-// acc += A.B_hi + A.B_lo, fp32 accumulation.
-template <class TL>
-struct MmaBf16Split {
-    using T = TL;
-    static constexpr int TILES = 3;   // A, B_hi, B_lo
-    __device__ __forceinline__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
-                               int wn, int lane) {
-        const int r = lane & 15, q = lane >> 4;
-        const char *Bl = Bs + TL::BYTES;
-#pragma unroll
-        for (int s = 0; s < TL::BK / 32; ++s) {
-            bf16x8 a[4], bh[4], bl[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int ao = (wm * 64 + i * 16 + r) * TL::PITCH + s * 64 + q * 16;
-                const int bo = (wn * 64 + i * 16 + r) * TL::PITCH + s * 64 + q * 16;
-                a[i] = *(const bf16x8 *)(As + ao);
-                bh[i] = *(const bf16x8 *)(Bs + bo);
-                bl[i] = *(const bf16x8 *)(Bl + bo);
-            }
-#pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-                for (int ni = 0; ni < 4; ++ni) {
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], bh[ni],
-                                                                          acc[mi][ni], 0, 0, 0);
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], bl[ni],
-                                                                          acc[mi][ni], 0, 0, 0);
-                }
-        }
-    }
-};
-
+template <int FM, int FN>
 struct MmaF32 {
     using T = TileF32;
-    static constexpr int TILES = 2;
-    __device__ __forceinline__ static void run(const char *As, const char *Bs, f32x4 (&acc)[4][4], int wm,
-                               int wn, int lane) {
-        f32x4 a[4], b[4];
+    static constexpr int STAGE_BYTES = 2 * T::BYTES;
+    __device__ __forceinline__ static void run(const char *As, const char *Bs,
+                                               f32x4 (&acc)[FM][FN], int wm, int wn, int lane) {
+        f32x4 a[FM], b[FN];
         const int r = lane & 15, q = lane >> 4;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            a[i] = *(const f32x4 *)(As + (wm * 64 + i * 16 + r) * T::PITCH + q * 16);
-            b[i] = *(const f32x4 *)(Bs + (wn * 64 + i * 16 + r) * T::PITCH + q * 16);
-        }
+        for (int i = 0; i < FM; ++i)
+            a[i] = *(const f32x4 *)(As + (wm * FM * 16 + i * 16 + r) * T::PITCH + q * 16);
+#pragma unroll
+        for (int i = 0; i < FN; ++i)
+            b[i] = *(const f32x4 *)(Bs + (wn * FN * 16 + i * 16 + r) * T::PITCH + q * 16);
 #pragma unroll
         for (int s = 0; s < 4; ++s)
 #pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
+            for (int mi = 0; mi < FM; ++mi)
 #pragma unroll
-                for (int ni = 0; ni < 4; ++ni)
+                for (int ni = 0; ni < FN; ++ni)
                     acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mi][s], b[ni][s],
                                                                        acc[mi][ni], 0, 0, 0);
     }
@@ -139,8 +180,7 @@ struct MmaF32 {
 
 // ------------------------------------------------------------------ tile loaders
 // Row addressing policies.  row(r) always returns a readable row (out-of-range rows are
-// clamped to the last one) so tile loads need no branches; callers zero the values of
-// rows r >= rows with a select.
+// clamped to the last one); loads of rows r >= rows read the zero buffer instead.
 struct PlainRows {
     const char *base;
     int64_t ld_bytes;
@@ -160,18 +200,13 @@ struct SlotRows {  // row n = (slot n / d_in, column c = n % d_in) of W_slot [d_
         return (const char *)w[sl] + c * es_dout;
     }
 };
-// Loads a thread does not need (rows past the end, K past the range) read these zero bytes
-// instead, so the registers hold zeros without a select; never written.
-// Register staging uses the compiler's native vector types (one 16-byte load or LDS store,
-// no struct copies).
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-__device__ u32x4 g_zero16[2];
 
 // K-contiguous rows whose element type is the LDS type.  WRAP: the product's K is twice
 // the row length and k >= row length re-reads the row (used with LoadRowsF32Split).
-template <class TL, class RowPolicy, bool WRAP = false>
+template <class TL, int NT, class RowPolicy, bool WRAP = false>
 struct LoadRows {
-    static constexpr int NCH = kTile * TL::CPR / kThreads;
+    static constexpr int NCH = TL::ROWS * TL::CPR / NT;
+    static_assert(NCH * NT == TL::ROWS * TL::CPR, "threads must divide the tile's chunks");
     RowPolicy pol;
     int64_t kbytes;       // bytes of K per source row
     int64_t wrap_bytes;
@@ -184,7 +219,7 @@ struct LoadRows {
     __device__ __forceinline__ void init(State &st, int64_t row0) const {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-            const int chunk = threadIdx.x + c * kThreads;
+            const int chunk = threadIdx.x + c * NT;
             st.lr[c] = chunk / TL::CPR;
             st.lq[c] = chunk % TL::CPR;
             st.rok[c] = row0 + st.lr[c] < pol.rows;
@@ -213,10 +248,11 @@ struct LoadRows {
 // k - K.  With the other operand read twice along K (LoadRows<..., true>) the product
 // accumulates hi.W + lo.W, which carries x to ~16 significant bits instead of 8.  K is a
 // multiple of 8, so a 16-byte chunk (8 values) never straddles the two halves.
-template <class TL>
+template <class TL, int NT>
 struct LoadRowsF32Split {
     static constexpr int CPR = TL::BK / 8;        // 8 bf16 per 16-byte LDS chunk
-    static constexpr int NCH = kTile * CPR / kThreads;
+    static constexpr int NCH = TL::ROWS * CPR / NT;
+    static_assert(NCH * NT == TL::ROWS * CPR, "threads must divide the tile's chunks");
     PlainRows pol;
     int64_t K;
     struct State {
@@ -229,7 +265,7 @@ struct LoadRowsF32Split {
     __device__ __forceinline__ void init(State &st, int64_t row0) const {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-            const int chunk = threadIdx.x + c * kThreads;
+            const int chunk = threadIdx.x + c * NT;
             st.lr[c] = chunk / CPR;
             st.lq[c] = chunk % CPR;
             st.rok[c] = row0 + st.lr[c] < pol.rows;
@@ -249,7 +285,9 @@ struct LoadRowsF32Split {
             st.reg[c][1] = *(const f32x4 *)(p + 16);
         }
     }
-    __device__ __forceinline__ static float part(float x, bool lo) { return lo ? x - round_bf16(x) : x; }
+    __device__ __forceinline__ static float part(float x, bool lo) {
+        return lo ? x - round_bf16(x) : x;
+    }
     __device__ __forceinline__ void store(const State &st, char *lds) const {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
@@ -266,15 +304,15 @@ struct LoadRowsF32Split {
 };
 
 // Weight-side operands (bf16 mode, BK = 64): source [ksrc rows x cols] row-major; LDS row
-// = source column (128 from col0), LDS k = source row.  The tile is 8 x 16 blocks of 8 x 8;
-// thread t owns half a block: block b = t / 2 (source rows k0 + 8*(b%8) + 4*(t%2) .. +3,
-// columns col0 + 8*(b/8) .. +7).  Four row reads of 16 bytes (bf16 source) or 32 bytes
-// (fp32 source), a transpose in registers, eight 8-byte LDS writes.  SPLIT (fp32 source):
-// the values go to two bf16 tiles, hi = bf16(x) at lds and lo = bf16(x - hi) at
-// lds + tile bytes, for MmaBf16Split.
-template <bool SRC_F32, bool SPLIT>
+// = source column (TL::ROWS from col0), LDS k = source row.  The tile is 8 x (ROWS / 8)
+// blocks of 8 x 8; thread t owns half a block: block b = t / 2 (source rows
+// k0 + 8*(b%8) + 4*(t%2) .. +3, columns col0 + 8*(b/8) .. +7).  Four row reads of 16 bytes
+// (bf16 source) or 32 bytes (fp32 source), a transpose in registers, eight 8-byte LDS
+// writes.  SPLIT (fp32 source): the values go to two bf16 tiles, hi = bf16(x) at lds and
+// lo = bf16(x - hi) at lds + tile bytes, for MmaBf16Split.
+template <class TL, int NT, bool SRC_F32, bool SPLIT>
 struct LoadTransHalf {
-    using TL = TileBf16T;
+    static_assert(TL::BK == 64 && NT == 2 * TL::ROWS, "one half block per thread");
     static constexpr int SES = SRC_F32 ? 4 : 2;
     static constexpr int NH = SRC_F32 ? 2 : 1;
     const char *base;
@@ -306,7 +344,6 @@ struct LoadTransHalf {
             for (int h = 0; h < NH; ++h) st.reg[r][h] = *(const u32x4 *)(p + h * 16);
         }
     }
-    __device__ __forceinline__ static uint32_t word(const u32x4 &u, int i) { return u[i]; }
     __device__ __forceinline__ void store(const State &st, char *lds) const {
         const int off = st.ib * 16 + st.hb * 8;
         const auto &rg = st.reg;
@@ -316,15 +353,15 @@ struct LoadTransHalf {
 #pragma unroll
             for (int p = 0; p < 2; ++p) {
                 if constexpr (SRC_F32) {
-                    const float x0 = __uint_as_float(word(rg[2 * p][c >> 2], c & 3));
-                    const float x1 = __uint_as_float(word(rg[2 * p + 1][c >> 2], c & 3));
+                    const float x0 = __uint_as_float(rg[2 * p][c >> 2][c & 3]);
+                    const float x1 = __uint_as_float(rg[2 * p + 1][c >> 2][c & 3]);
                     w[p] = pack_bf16x2(x0, x1);
                     if constexpr (SPLIT)
                         wl[p] = pack_bf16x2(x0 - __uint_as_float(w[p] << 16),
                                             x1 - __uint_as_float(w[p] & 0xffff0000u));
                 } else {
-                    const uint32_t a0 = word(rg[2 * p][0], c >> 1);
-                    const uint32_t a1 = word(rg[2 * p + 1][0], c >> 1);
+                    const uint32_t a0 = rg[2 * p][0][c >> 1];
+                    const uint32_t a1 = rg[2 * p + 1][0][c >> 1];
                     w[p] = (c & 1) ? ((a0 >> 16) | (a1 & 0xffff0000u))
                                    : ((a0 & 0xffffu) | (a1 << 16));
                 }
@@ -336,32 +373,35 @@ struct LoadTransHalf {
     }
 };
 
-// fp32 weight side: 16 k x 32 chunks of 4 columns, 2 chunks per thread, transposed by
-// scalar LDS writes (used only in fp32 mode).
+// fp32 weight side: 16 k x (ROWS / 4) chunks of 4 columns, transposed by scalar LDS writes
+// (used only in fp32 mode).
+template <int NT>
 struct LoadTransF32 {
     using TL = TileF32;
+    static constexpr int NCH = 16 * (TL::ROWS / 4) / NT;
+    static_assert(NCH * NT == 16 * (TL::ROWS / 4), "threads must divide the tile's chunks");
     const char *base;
     int64_t ld_bytes;
     int64_t ksrc;
     int64_t cols;
     struct State {
         int64_t col0;
-        int ik[2], cq[2];
-        u32x4 reg[2];
+        int ik[NCH], cq[NCH];
+        u32x4 reg[NCH];
     };
     __device__ __forceinline__ void init(State &st, int64_t c0) const {
         st.col0 = c0;
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            const int chunk = threadIdx.x + c * kThreads;
-            st.ik[c] = chunk >> 5;
-            st.cq[c] = chunk & 31;
+        for (int c = 0; c < NCH; ++c) {
+            const int chunk = threadIdx.x + c * NT;
+            st.ik[c] = chunk / (TL::ROWS / 4);
+            st.cq[c] = chunk % (TL::ROWS / 4);
         }
     }
     __device__ __forceinline__ void load(State &st, int64_t k0, int64_t kend) const {
         const int64_t lim = kend < ksrc ? kend : ksrc;
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
+        for (int c = 0; c < NCH; ++c) {
             const int64_t i = k0 + st.ik[c];
             const int64_t col = st.col0 + (int64_t)st.cq[c] * 4;
             const bool ok = i < lim && col < cols;
@@ -370,12 +410,11 @@ struct LoadTransF32 {
     }
     __device__ __forceinline__ void store(const State &st, char *lds) const {
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
+        for (int c = 0; c < NCH; ++c) {
             const u32x4 v = st.reg[c];
-            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                *(uint32_t *)(lds + (st.cq[c] * 4 + e) * TL::PITCH + st.ik[c] * 4) = w[e];
+                *(uint32_t *)(lds + (st.cq[c] * 4 + e) * TL::PITCH + st.ik[c] * 4) = v[e];
         }
     }
 };
@@ -470,7 +509,8 @@ struct EpiPartial {
     float *out;          // [splits][M][N]
     int64_t M;
     int32_t N;
-    __device__ __forceinline__ void operator()(int64_t m, int64_t n0, const float *v, int64_t split) const {
+    __device__ __forceinline__ void operator()(int64_t m, int64_t n0, const float *v,
+                                               int64_t split) const {
         if (m >= M) return;
         float *o = out + split * M * N + m * N;
 #pragma unroll
@@ -490,24 +530,26 @@ struct EpiPartial {
 // STAGES = 2: double-buffered LDS (one barrier per step); STAGES = 1: one buffer.
 // R register stages: the global loads of step k + R are issued right after step k's tiles
 // reach LDS, so R multiplies overlap each load's latency.
-template <class Mma, class LA, class LB, class Epi, int STAGES, int R>
-__global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, const Epi epi,
-                                                      int64_t K, int64_t tiles_m,
-                                                      int64_t tiles_n, int64_t k_per_split) {
+template <class C, class Mma, class LA, class LB, class Epi, int STAGES, int R>
+__global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const Epi epi,
+                                                int64_t K, int64_t tiles_m, int64_t tiles_n,
+                                                int64_t k_per_split) {
     using TL = typename Mma::T;
-    constexpr int STAGE_BYTES = Mma::TILES * TL::BYTES;
+    constexpr int FM = C::FM, FN = C::FN;
+    constexpr int STAGE_BYTES = Mma::STAGE_BYTES;
+    constexpr int NW = C::NT / 64;
     __shared__ __attribute__((aligned(16))) char lds[STAGES * STAGE_BYTES];
-    static_assert(STAGES * STAGE_BYTES >= 4 * 16 * kStagePitch * 4, "epilogue staging space");
+    static_assert(STAGES * STAGE_BYTES >= NW * 16 * kStagePitch * 4, "epilogue staging space");
     const int64_t logical = xcd_major_id(blockIdx.x, (int64_t)gridDim.x);
     const int64_t tiles = tiles_m * tiles_n;
     const int64_t split = logical / tiles;
     const int64_t t = logical - split * tiles;
     const int64_t tm = t / tiles_n, tn = t - tm * tiles_n;
-    const int64_t m0 = tm * kTile, n0 = tn * kTile;
+    const int64_t m0 = tm * C::TM, n0 = tn * C::TN;
     const int64_t kb = split * k_per_split;
     const int64_t ke = kb + k_per_split < K ? kb + k_per_split : K;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / C::WN, wn = wave % C::WN;
 
     typename LA::State sa[R];
     typename LB::State sb[R];
@@ -516,11 +558,11 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, 
         la.init(sa[r], m0);
         lb.init(sb[r], n0);
     }
-    f32x4 acc[4][4];
+    f32x4 acc[FM][FN];
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < FM; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // Steps are padded to a multiple of R and every load is issued unconditionally
     // (steps past the range load zero tiles), so all paths through the loop have the same
@@ -537,7 +579,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, 
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int64_t it = it0 + r;
-            char *As = lds + (STAGES == 2 ? ((it0 + r) & 1) * STAGE_BYTES : 0);
+            char *As = lds + (STAGES == 2 ? (it & 1) * STAGE_BYTES : 0);
             char *Bs = As + TL::BYTES;
             if constexpr (STAGES == 1) __syncthreads();
             la.store(sa[r], As);
@@ -557,9 +599,9 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, 
     float *stage = (float *)lds + wave * 16 * kStagePitch;
     const int rq = lane >> 4, cc = lane & 15;
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi) {
+    for (int mi = 0; mi < FM; ++mi) {
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
+        for (int ni = 0; ni < FN; ++ni)
 #pragma unroll
             for (int v = 0; v < 4; ++v)
                 stage[(4 * rq + v) * kStagePitch + ni * 16 + cc] = acc[mi][ni][v];
@@ -571,36 +613,28 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm(const LA la, const LB lb, 
             const float4 x = *(const float4 *)(stage + r * kStagePitch + c0 + e);
             vals[e] = x.x; vals[e + 1] = x.y; vals[e + 2] = x.z; vals[e + 3] = x.w;
         }
-        epi(m0 + wm * 64 + mi * 16 + r, n0 + wn * 64 + c0, vals, split);
+        epi(m0 + wm * FM * 16 + mi * 16 + r, n0 + wn * FN * 16 + c0, vals, split);
         __syncthreads();
     }
 }
 
-#ifndef RGCN_GEMM_RSTAGES
-#define RGCN_GEMM_RSTAGES 2
-#endif
-#ifndef RGCN_GEMM_RSTAGES_DW
-#define RGCN_GEMM_RSTAGES_DW 1
-#endif
-#ifndef RGCN_GEMM_RSTAGES_DMS
-#define RGCN_GEMM_RSTAGES_DMS 1
-#endif
-
-template <class Mma, class LA, class LB, class Epi, int STAGES = 2, int R = RGCN_GEMM_RSTAGES>
+template <class C, class Mma, class LA, class LB, class Epi, int STAGES, int R>
 hipError_t launch_gemm(const LA &la, const LB &lb, const Epi &epi, int64_t M, int64_t N,
                        int64_t K, int64_t splits, int64_t k_per_split, hipStream_t s) {
-    const int64_t tiles_m = cdiv(M, kTile), tiles_n = cdiv(N, kTile);
+    const int64_t tiles_m = cdiv(M, C::TM), tiles_n = cdiv(N, C::TN);
     if (tiles_m == 0 || tiles_n == 0 || splits == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_gemm<Mma, LA, LB, Epi, STAGES, R>), dim3((unsigned)(tiles_m * tiles_n * splits)),
-                       dim3(kThreads), 0, s, la, lb, epi, K, tiles_m, tiles_n, k_per_split);
+    hipLaunchKernelGGL((k_gemm<C, Mma, LA, LB, Epi, STAGES, R>),
+                       dim3((unsigned)(tiles_m * tiles_n * splits)), dim3(C::NT), 0, s, la, lb,
+                       epi, K, tiles_m, tiles_n, k_per_split);
     return hipGetLastError();
 }
 
-// Split of the weight-side reduction over rows: enough workgroups to fill the chip
-// (~4 per CU), each split a whole number of K steps and at least 8 of them.
+// Split of the weight-side reduction over rows: about two workgroups per CU in total, each
+// split a whole number of K steps and at least 8 of them.
+template <class C>
 void dw_split(int64_t M, int Kcat, int d_out, int bk, int64_t *splits, int64_t *per) {
-    const int64_t tiles = cdiv(Kcat, kTile) * cdiv(d_out, kTile);
-    int64_t want = cdiv(1024, tiles);
+    const int64_t tiles = cdiv(Kcat, C::TM) * cdiv(d_out, C::TN);
+    int64_t want = cdiv(512, tiles);
     const int64_t max_by_len = cdiv(M, (int64_t)bk * 8);
     if (want > max_by_len) want = max_by_len;
     if (want < 1) want = 1;
@@ -632,23 +666,33 @@ __global__ __launch_bounds__(kThreads) void k_zero_outputs(DwOut out, int d_in, 
     if (e < per && out.w[sl]) out.w[sl][e] = 0.f;
 }
 
+#ifndef RGCN_GEMM_RSTAGES
+#define RGCN_GEMM_RSTAGES 1
+#endif
+
 }  // namespace
 
 hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
                         const void *wcat_t, const void *bias, int relu, void *y,
                         hipStream_t s) {
     if (dt == RGCN_BF16) {
-        using TL = TileBf16;
-        LoadRows<TL, PlainRows> la{PlainRows{(const char *)a, (int64_t)K * 2, M}, (int64_t)K * 2, 0};
-        LoadRows<TL, PlainRows> lb{PlainRows{(const char *)wcat_t, (int64_t)K * 2, N},
-                                   (int64_t)K * 2, 0};
-        return launch_gemm<MmaBf16<TL>>(la, lb, EpiForward<true>{y, bias, M, N, relu}, M, N, K, 1,
-                                        K, s);
+        using C = CfgFwd;
+        using TL = TileBf16<C>;
+        LoadRows<TL, C::NT, PlainRows> la{PlainRows{(const char *)a, (int64_t)K * 2, M},
+                                          (int64_t)K * 2, 0};
+        LoadRows<TL, C::NT, PlainRows> lb{PlainRows{(const char *)wcat_t, (int64_t)K * 2, N},
+                                          (int64_t)K * 2, 0};
+        return launch_gemm<C, MmaBf16<TL, C::FM, C::FN>, decltype(la), decltype(lb),
+                           EpiForward<true>, 2, RGCN_GEMM_RSTAGES>(
+            la, lb, EpiForward<true>{y, bias, M, N, relu}, M, N, K, 1, K, s);
     }
+    using C = CfgF32;
     using TL = TileF32;
-    LoadRows<TL, PlainRows> la{PlainRows{(const char *)a, (int64_t)K * 4, M}, (int64_t)K * 4, 0};
-    LoadRows<TL, PlainRows> lb{PlainRows{(const char *)wcat_t, (int64_t)K * 4, N}, (int64_t)K * 4, 0};
-    return launch_gemm<MmaF32>(la, lb, EpiForward<false>{y, bias, M, N, relu}, M, N, K, 1, K, s);
+    LoadRows<TL, C::NT, PlainRows> la{PlainRows{(const char *)a, (int64_t)K * 4, M}, (int64_t)K * 4, 0};
+    LoadRows<TL, C::NT, PlainRows> lb{PlainRows{(const char *)wcat_t, (int64_t)K * 4, N},
+                                      (int64_t)K * 4, 0};
+    return launch_gemm<C, MmaF32<C::FM, C::FN>, decltype(la), decltype(lb), EpiForward<false>, 2, 2>(
+        la, lb, EpiForward<false>{y, bias, M, N, relu}, M, N, K, 1, K, s);
 }
 
 hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_in,
@@ -669,22 +713,25 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_
     PlainRows pa{(const char *)dy, (int64_t)d_out * 4, M};
     if (dt == RGCN_BF16) {
         // dY enters as hi + lo bf16 parts: K = 2 d_out, the weight rows read twice
-        using TL = TileBf16;
-        LoadRowsF32Split<TL> la{pa, d_out};
-        LoadRows<TL, SlotRows, true> lb{sr, (int64_t)d_out * 2, (int64_t)d_out * 2};
-        return launch_gemm<MmaBf16<TL>, decltype(la), decltype(lb), EpiDms, 2, RGCN_GEMM_RSTAGES_DMS>(
+        using C = CfgDms;
+        using TL = TileBf16<C>;
+        LoadRowsF32Split<TL, C::NT> la{pa, d_out};
+        LoadRows<TL, C::NT, SlotRows, true> lb{sr, (int64_t)d_out * 2, (int64_t)d_out * 2};
+        return launch_gemm<C, MmaBf16<TL, C::FM, C::FN>, decltype(la), decltype(lb), EpiDms, 2, 1>(
             la, lb, epi, M, N, 2 * (int64_t)d_out, 1, 2 * (int64_t)d_out, s);
     }
+    using C = CfgF32;
     using TL = TileF32;
-    LoadRows<TL, PlainRows> la{pa, (int64_t)d_out * 4, 0};
-    LoadRows<TL, SlotRows> lb{sr, (int64_t)d_out * 4, 0};
-    return launch_gemm<MmaF32>(la, lb, epi, M, N, d_out, 1, d_out, s);
+    LoadRows<TL, C::NT, PlainRows> la{pa, (int64_t)d_out * 4, 0};
+    LoadRows<TL, C::NT, SlotRows> lb{sr, (int64_t)d_out * 4, 0};
+    return launch_gemm<C, MmaF32<C::FM, C::FN>, decltype(la), decltype(lb), EpiDms, 2, 2>(
+        la, lb, epi, M, N, d_out, 1, d_out, s);
 }
 
 size_t gemm_dw_partial_bytes(int64_t M, int Kcat, int d_out) {
     int64_t sp16, p16, sp64, p64;
-    dw_split(M, Kcat, d_out, TileF32::BK, &sp16, &p16);
-    dw_split(M, Kcat, d_out, TileBf16T::BK, &sp64, &p64);
+    dw_split<CfgF32>(M, Kcat, d_out, TileF32::BK, &sp16, &p16);
+    dw_split<CfgDw>(M, Kcat, d_out, TileBf16<CfgDw>::BK, &sp64, &p64);
     const int64_t sp = sp16 > sp64 ? sp16 : sp64;
     return (size_t)(sp > 0 ? sp : 1) * Kcat * d_out * 4 + 256;
 }
@@ -693,9 +740,11 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
                    const float *dy, int d_out, const DwOut &out, float *partial,
                    hipStream_t s) {
     const bool bf = dt == RGCN_BF16;
-    const int bk = bf ? TileBf16T::BK : TileF32::BK;
     int64_t splits, per;
-    dw_split(M, Kcat, d_out, bk, &splits, &per);
+    if (bf)
+        dw_split<CfgDw>(M, Kcat, d_out, TileBf16<CfgDw>::BK, &splits, &per);
+    else
+        dw_split<CfgF32>(M, Kcat, d_out, TileF32::BK, &splits, &per);
     if (splits == 0) {  // no rows: every requested gradient is zero
         hipLaunchKernelGGL(k_zero_outputs, dim3((unsigned)cdiv((int64_t)d_in * d_out, kThreads),
                            (unsigned)out.count), dim3(kThreads), 0, s, out, d_in, d_out);
@@ -704,14 +753,18 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
     EpiPartial epi{partial, Kcat, d_out};
     if (bf) {
         // dY enters as hi + lo bf16 tiles (two MFMAs per operand pair, one load)
-        LoadTransHalf<false, false> la{(const char *)mcat, (int64_t)Kcat * 2, M, Kcat};
-        LoadTransHalf<true, true> lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
-        RGCN_HIP_TRY((launch_gemm<MmaBf16Split<TileBf16T>, decltype(la), decltype(lb), EpiPartial, 1,
-                                  RGCN_GEMM_RSTAGES_DW>(la, lb, epi, Kcat, d_out, M, splits, per, s)));
+        using C = CfgDw;
+        using TL = TileBf16<C>;
+        LoadTransHalf<TL, C::NT, false, false> la{(const char *)mcat, (int64_t)Kcat * 2, M, Kcat};
+        LoadTransHalf<TL, C::NT, true, true> lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
+        RGCN_HIP_TRY((launch_gemm<C, MmaBf16Split<TL, C::FM, C::FN>, decltype(la), decltype(lb),
+                                  EpiPartial, 1, 1>(la, lb, epi, Kcat, d_out, M, splits, per, s)));
     } else {
-        LoadTransF32 la{(const char *)mcat, (int64_t)Kcat * 4, M, Kcat};
-        LoadTransF32 lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
-        RGCN_HIP_TRY(launch_gemm<MmaF32>(la, lb, epi, Kcat, d_out, M, splits, per, s));
+        using C = CfgF32;
+        LoadTransF32<C::NT> la{(const char *)mcat, (int64_t)Kcat * 4, M, Kcat};
+        LoadTransF32<C::NT> lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
+        RGCN_HIP_TRY((launch_gemm<C, MmaF32<C::FM, C::FN>, decltype(la), decltype(lb), EpiPartial,
+                                  2, 2>(la, lb, epi, Kcat, d_out, M, splits, per, s)));
     }
     const int64_t total = (int64_t)Kcat * d_out;
     hipLaunchKernelGGL(k_dw_reduce, dim3((unsigned)cdiv(total, kThreads)), dim3(kThreads), 0, s,

@@ -275,7 +275,8 @@ struct DescArgs {
     int32_t es;
 };
 __global__ __launch_bounds__(kThreads) void k_fwd_desc(DescArgs a, const int32_t *order,
-                                                       int64_t n_seg, SegDesc *desc) {
+                                                       int64_t n_seg, SegDesc *desc,
+                                                       int32_t *weight) {
     const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (p >= n_seg) return;
     const int64_t seg = order[p];
@@ -298,6 +299,26 @@ __global__ __launch_bounds__(kThreads) void k_fwd_desc(DescArgs a, const int32_t
     d.out_lo = (uint32_t)out;
     d.info = (uint32_t)((out >> 32) & 0xffu) | ((uint32_t)lo << 8);
     desc[p] = d;
+    weight[p] = d.deg > 0 ? d.deg : 1;
+}
+
+// Chunk starts of the flattened forward stream.  pre = exclusive prefix of the segment
+// weights (entries per segment).  Segment p belongs to chunk pre[p] / kFwdChunk; cs[c] is
+// the first segment of chunk c or later (chunks no segment starts in are empty), for
+// c <= ceil(total / kFwdChunk); cs[nc_max + 1] = total entries.
+__global__ __launch_bounds__(kThreads) void k_chunk_starts(const int32_t *pre, const int32_t *weight,
+                                                           int64_t n_seg, int64_t nc_max, int32_t *cs) {
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= n_seg) return;
+    const int64_t cur = pre[p] / kFwdChunk;
+    const int64_t prev = p == 0 ? -1 : pre[p - 1] / kFwdChunk;
+    for (int64_t c = prev + 1; c <= cur; ++c) cs[c] = (int32_t)p;
+    if (p == n_seg - 1) {
+        const int64_t total = (int64_t)pre[p] + weight[p];
+        const int64_t nc = (total + kFwdChunk - 1) / kFwdChunk;
+        for (int64_t c = cur + 1; c <= nc; ++c) cs[c] = (int32_t)n_seg;
+        cs[nc_max + 1] = (int32_t)total;
+    }
 }
 
 struct Words {
@@ -345,7 +366,7 @@ hipError_t fwd_schedule(const FwdSlot *slots_host, int nslots, int64_t n_seg, in
 
 hipError_t fwd_descriptors(const FwdSlot *slots_host, int nslots, const int32_t *order,
                            int64_t n_seg, const int64_t *mcat_off, const int64_t *mcat_ld,
-                           int es, SegDesc *desc, hipStream_t s) {
+                           int es, SegDesc *desc, int32_t *weight, hipStream_t s) {
     if (n_seg == 0) return hipSuccess;
     DescArgs a;
     a.nslots = nslots;
@@ -361,7 +382,26 @@ hipError_t fwd_descriptors(const FwdSlot *slots_host, int nslots, const int32_t 
     }
     a.es = es;
     hipLaunchKernelGGL(k_fwd_desc, dim3((unsigned)cdiv(n_seg, kThreads)), dim3(kThreads), 0, s, a,
-                       order, n_seg, desc);
+                       order, n_seg, desc, weight);
+    return hipGetLastError();
+}
+
+int64_t fwd_chunk_bound(int64_t n_seg, int64_t nnz_total) {
+    return cdiv(n_seg + nnz_total, kFwdChunk);
+}
+
+size_t fwd_chunks_temp_bytes(int64_t n_seg) {
+    return 2 * align_up((size_t)n_seg * 4 + 4, 256) + scan_temp_bytes(n_seg);
+}
+
+hipError_t fwd_chunks(const int32_t *weight, int64_t n_seg, int64_t nc_max, int32_t *cs,
+                      void *temp, hipStream_t s) {
+    if (n_seg == 0) return hipSuccess;
+    int32_t *pre = (int32_t *)temp;
+    void *stemp = (char *)temp + align_up((size_t)n_seg * 4 + 4, 256);
+    RGCN_HIP_TRY(exclusive_scan_i32(weight, pre, n_seg, stemp, s));
+    hipLaunchKernelGGL(k_chunk_starts, dim3((unsigned)cdiv(n_seg, kThreads)), dim3(kThreads), 0, s,
+                       pre, weight, n_seg, nc_max, cs);
     return hipGetLastError();
 }
 
