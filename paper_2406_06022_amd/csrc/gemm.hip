@@ -8,11 +8,12 @@
 //   input side   dMs_t = dY_t [n_dst x d_out]    . [W_s rows]^T, slot columns / deg
 //   weight side  dW    = Mcat_t^T [K x n_dst]    . dY_t [n_dst x d_out]   (split over rows)
 //
-// bf16 mode: workgroup tile 256 x 256, eight waves in a 2 x 4 arrangement of 128 x 64, each
-// wave an 8 x 4 grid of 16 x 16 MFMA tiles.  These products are skinny (K and N of a few
-// hundred against up to millions of rows), so what limits them is how often the long
-// operand is re-read from L2: a 256-wide tile reads it half as often as a 128-wide one.
-// fp32 mode: 128 x 128, four waves of 64 x 64.
+// bf16 forward and weight side: workgroup tile 256 x 256, eight waves in a 2 x 4
+// arrangement of 128 x 64, each wave an 8 x 4 grid of 16 x 16 MFMA tiles.  These products
+// are skinny (K and N of a few hundred against up to millions of rows), so what limits
+// them is how often the long operand is re-read: a 256-wide tile reads it half as often as
+// a 128-wide one.  The input side (N = one or two slots of d_in columns) and fp32 mode:
+// 128 x 128, four waves of 64 x 64.
 //
 // LDS holds both operands K-contiguous ("row r, k..."), one row = BK elements of K + 16
 // bytes of padding; the row pitch is an odd number of 16-byte units, so the 16 rows a
@@ -28,7 +29,9 @@
 //
 // bf16 mode: v_mfma_f32_16x16x32_bf16, fp32 accumulation.  The fp32 output gradient dY
 // enters both backward products as a hi + lo pair of bf16 values (hi = bf16(x), lo =
-// bf16(x - hi)), which carries ~16 significant bits.  fp32 mode: v_mfma_f32_16x16x4_f32.
+// bf16(x - hi)), which carries ~16 significant bits: each fp32 tile is read from memory
+// once and written to LDS as two bf16 tiles, and every fragment of the other operand meets
+// both.  fp32 mode: v_mfma_f32_16x16x4_f32.
 #include <type_traits>
 
 #include "common.h"
@@ -150,6 +153,39 @@ struct MmaBf16Split {
     }
 };
 
+// A held as two bf16 tiles (hi at As, lo two tiles further, after B) of one fp32 operand:
+// acc += A_hi.B + A_lo.B, fp32 accumulation.
+template <class TL, int FM, int FN>
+struct MmaBf16SplitA {
+    using T = TL;
+    static constexpr int STAGE_BYTES = 3 * TL::BYTES;   // A_hi, B, A_lo
+    __device__ __forceinline__ static void run(const char *As, const char *Bs,
+                                               f32x4 (&acc)[FM][FN], int wm, int wn, int lane) {
+        const int r = lane & 15, q = lane >> 4;
+        const char *Al = As + 2 * TL::BYTES;
+#pragma unroll
+        for (int s = 0; s < TL::BK / 32; ++s) {
+            bf16x8 b[FN];
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+                b[i] = *(const bf16x8 *)(Bs + (wn * FN * 16 + i * 16 + r) * TL::PITCH + s * 64 + q * 16);
+#pragma unroll
+            for (int mi = 0; mi < FM; ++mi) {
+                const int ao = (wm * FM * 16 + mi * 16 + r) * TL::PITCH + s * 64 + q * 16;
+                const bf16x8 ah = *(const bf16x8 *)(As + ao);
+                const bf16x8 al = *(const bf16x8 *)(Al + ao);
+#pragma unroll
+                for (int ni = 0; ni < FN; ++ni) {
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b[ni], acc[mi][ni],
+                                                                          0, 0, 0);
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b[ni], acc[mi][ni],
+                                                                          0, 0, 0);
+                }
+            }
+        }
+    }
+};
+
 // fp32: lane group q holds k = 4q..4q+3 of its row; MFMA step s uses element s, so the
 // four steps together cover k = 0..15 (the sum over k is taken in a different order, not
 // a different set).
@@ -201,15 +237,13 @@ struct SlotRows {  // row n = (slot n / d_in, column c = n % d_in) of W_slot [d_
     }
 };
 
-// K-contiguous rows whose element type is the LDS type.  WRAP: the product's K is twice
-// the row length and k >= row length re-reads the row (used with LoadRowsF32Split).
-template <class TL, int NT, class RowPolicy, bool WRAP = false>
+// K-contiguous rows whose element type is the LDS type.
+template <class TL, int NT, class RowPolicy>
 struct LoadRows {
     static constexpr int NCH = TL::ROWS * TL::CPR / NT;
     static_assert(NCH * NT == TL::ROWS * TL::CPR, "threads must divide the tile's chunks");
     RowPolicy pol;
     int64_t kbytes;       // bytes of K per source row
-    int64_t wrap_bytes;
     struct State {
         const char *rp[NCH];
         bool rok[NCH];
@@ -230,8 +264,7 @@ struct LoadRows {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             const int64_t k = k0 + st.lq[c] * (16 / TL::ES);
-            int64_t kb = k * TL::ES;
-            if constexpr (WRAP) kb = kb >= wrap_bytes ? kb - wrap_bytes : kb;
+            const int64_t kb = k * TL::ES;
             const bool ok = st.rok[c] && kb < kbytes && k < kend;
             st.reg[c] = *(const u32x4 *)(ok ? st.rp[c] + kb : (const char *)g_zero16);
         }
@@ -243,13 +276,11 @@ struct LoadRows {
     }
 };
 
-// fp32 rows entering a bf16 product as two bf16 terms: chunk k < K holds the high part
-// hi = bf16(x) of element k, chunk K <= k < 2K the low part lo = bf16(x - hi) of element
-// k - K.  With the other operand read twice along K (LoadRows<..., true>) the product
-// accumulates hi.W + lo.W, which carries x to ~16 significant bits instead of 8.  K is a
-// multiple of 8, so a 16-byte chunk (8 values) never straddles the two halves.
-template <class TL, int NT>
-struct LoadRowsF32Split {
+// fp32 rows entering a bf16 product as a hi + lo pair read once: each 32-byte piece (8
+// values) goes to the hi tile at lds (hi = bf16(x)) and to the lo tile at lds + LO_OFF
+// (lo = bf16(x - hi)), for MmaBf16SplitA.
+template <class TL, int NT, int LO_OFF>
+struct LoadRowsF32HiLo {
     static constexpr int CPR = TL::BK / 8;        // 8 bf16 per 16-byte LDS chunk
     static constexpr int NCH = TL::ROWS * CPR / NT;
     static_assert(NCH * NT == TL::ROWS * CPR, "threads must divide the tile's chunks");
@@ -259,7 +290,6 @@ struct LoadRowsF32Split {
         const char *rp[NCH];
         bool rok[NCH];
         int lr[NCH], lq[NCH];
-        bool low[NCH];
         f32x4 reg[NCH][2];
     };
     __device__ __forceinline__ void init(State &st, int64_t row0) const {
@@ -275,30 +305,29 @@ struct LoadRowsF32Split {
     __device__ __forceinline__ void load(State &st, int64_t k0, int64_t kend) const {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-            int64_t k = k0 + st.lq[c] * 8;
-            const bool in = k < kend;
-            st.low[c] = k >= K;
-            k = st.low[c] ? k - K : k;
-            const bool ok = st.rok[c] && k < K && in;
+            const int64_t k = k0 + st.lq[c] * 8;
+            const bool ok = st.rok[c] && k < K && k < kend;
             const char *p = ok ? st.rp[c] + k * 4 : (const char *)g_zero16;
             st.reg[c][0] = *(const f32x4 *)p;
             st.reg[c][1] = *(const f32x4 *)(p + 16);
         }
     }
-    __device__ __forceinline__ static float part(float x, bool lo) {
-        return lo ? x - round_bf16(x) : x;
-    }
     __device__ __forceinline__ void store(const State &st, char *lds) const {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-            const bool lo = st.low[c];
             const f32x4 a = st.reg[c][0], b = st.reg[c][1];
-            u32x4 w;
-            w.x = pack_bf16x2(part(a.x, lo), part(a.y, lo));
-            w.y = pack_bf16x2(part(a.z, lo), part(a.w, lo));
-            w.z = pack_bf16x2(part(b.x, lo), part(b.y, lo));
-            w.w = pack_bf16x2(part(b.z, lo), part(b.w, lo));
-            *(u32x4 *)(lds + st.lr[c] * TL::PITCH + st.lq[c] * 16) = w;
+            u32x4 h, l;
+            h.x = pack_bf16x2(a.x, a.y);
+            h.y = pack_bf16x2(a.z, a.w);
+            h.z = pack_bf16x2(b.x, b.y);
+            h.w = pack_bf16x2(b.z, b.w);
+            l.x = pack_bf16x2(a.x - bf16_lo(h.x), a.y - bf16_hi(h.x));
+            l.y = pack_bf16x2(a.z - bf16_lo(h.y), a.w - bf16_hi(h.y));
+            l.z = pack_bf16x2(b.x - bf16_lo(h.z), b.y - bf16_hi(h.z));
+            l.w = pack_bf16x2(b.z - bf16_lo(h.w), b.w - bf16_hi(h.w));
+            char *d = lds + st.lr[c] * TL::PITCH + st.lq[c] * 16;
+            *(u32x4 *)d = h;
+            *(u32x4 *)(d + LO_OFF) = l;
         }
     }
 };
@@ -669,6 +698,15 @@ __global__ __launch_bounds__(kThreads) void k_zero_outputs(DwOut out, int d_in, 
 #ifndef RGCN_GEMM_RSTAGES
 #define RGCN_GEMM_RSTAGES 1
 #endif
+#ifndef RGCN_GEMM_DMS_STAGES
+#define RGCN_GEMM_DMS_STAGES 1
+#endif
+#ifndef RGCN_GEMM_DMS_R
+#define RGCN_GEMM_DMS_R 1
+#endif
+#ifndef RGCN_GEMM_DW_R
+#define RGCN_GEMM_DW_R 1
+#endif
 
 }  // namespace
 
@@ -679,18 +717,18 @@ hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
         using C = CfgFwd;
         using TL = TileBf16<C>;
         LoadRows<TL, C::NT, PlainRows> la{PlainRows{(const char *)a, (int64_t)K * 2, M},
-                                          (int64_t)K * 2, 0};
+                                          (int64_t)K * 2};
         LoadRows<TL, C::NT, PlainRows> lb{PlainRows{(const char *)wcat_t, (int64_t)K * 2, N},
-                                          (int64_t)K * 2, 0};
+                                          (int64_t)K * 2};
         return launch_gemm<C, MmaBf16<TL, C::FM, C::FN>, decltype(la), decltype(lb),
                            EpiForward<true>, 2, RGCN_GEMM_RSTAGES>(
             la, lb, EpiForward<true>{y, bias, M, N, relu}, M, N, K, 1, K, s);
     }
     using C = CfgF32;
     using TL = TileF32;
-    LoadRows<TL, C::NT, PlainRows> la{PlainRows{(const char *)a, (int64_t)K * 4, M}, (int64_t)K * 4, 0};
+    LoadRows<TL, C::NT, PlainRows> la{PlainRows{(const char *)a, (int64_t)K * 4, M}, (int64_t)K * 4};
     LoadRows<TL, C::NT, PlainRows> lb{PlainRows{(const char *)wcat_t, (int64_t)K * 4, N},
-                                      (int64_t)K * 4, 0};
+                                      (int64_t)K * 4};
     return launch_gemm<C, MmaF32<C::FM, C::FN>, decltype(la), decltype(lb), EpiForward<false>, 2, 2>(
         la, lb, EpiForward<false>{y, bias, M, N, relu}, M, N, K, 1, K, s);
 }
@@ -712,18 +750,19 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_
     for (int i = 0; i < kMaxSlots; ++i) epi.indptr[i] = i < slots.count ? slots.indptr[i] : nullptr;
     PlainRows pa{(const char *)dy, (int64_t)d_out * 4, M};
     if (dt == RGCN_BF16) {
-        // dY enters as hi + lo bf16 parts: K = 2 d_out, the weight rows read twice
+        // dY enters as hi + lo bf16 tiles from one read of each fp32 row; each weight
+        // fragment meets both
         using C = CfgDms;
         using TL = TileBf16<C>;
-        LoadRowsF32Split<TL, C::NT> la{pa, d_out};
-        LoadRows<TL, C::NT, SlotRows, true> lb{sr, (int64_t)d_out * 2, (int64_t)d_out * 2};
-        return launch_gemm<C, MmaBf16<TL, C::FM, C::FN>, decltype(la), decltype(lb), EpiDms, 2, 1>(
-            la, lb, epi, M, N, 2 * (int64_t)d_out, 1, 2 * (int64_t)d_out, s);
+        LoadRowsF32HiLo<TL, C::NT, 2 * TL::BYTES> la{pa, d_out};
+        LoadRows<TL, C::NT, SlotRows> lb{sr, (int64_t)d_out * 2};
+        return launch_gemm<C, MmaBf16SplitA<TL, C::FM, C::FN>, decltype(la), decltype(lb), EpiDms,
+                           RGCN_GEMM_DMS_STAGES, RGCN_GEMM_DMS_R>(la, lb, epi, M, N, d_out, 1, d_out, s);
     }
     using C = CfgF32;
     using TL = TileF32;
-    LoadRows<TL, C::NT, PlainRows> la{pa, (int64_t)d_out * 4, 0};
-    LoadRows<TL, C::NT, SlotRows> lb{sr, (int64_t)d_out * 4, 0};
+    LoadRows<TL, C::NT, PlainRows> la{pa, (int64_t)d_out * 4};
+    LoadRows<TL, C::NT, SlotRows> lb{sr, (int64_t)d_out * 4};
     return launch_gemm<C, MmaF32<C::FM, C::FN>, decltype(la), decltype(lb), EpiDms, 2, 2>(
         la, lb, epi, M, N, d_out, 1, d_out, s);
 }
@@ -758,7 +797,7 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
         LoadTransHalf<TL, C::NT, false, false> la{(const char *)mcat, (int64_t)Kcat * 2, M, Kcat};
         LoadTransHalf<TL, C::NT, true, true> lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
         RGCN_HIP_TRY((launch_gemm<C, MmaBf16Split<TL, C::FM, C::FN>, decltype(la), decltype(lb),
-                                  EpiPartial, 1, 1>(la, lb, epi, Kcat, d_out, M, splits, per, s)));
+                                  EpiPartial, 1, RGCN_GEMM_DW_R>(la, lb, epi, Kcat, d_out, M, splits, per, s)));
     } else {
         using C = CfgF32;
         LoadTransF32<C::NT> la{(const char *)mcat, (int64_t)Kcat * 4, M, Kcat};
