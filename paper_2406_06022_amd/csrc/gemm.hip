@@ -1,7 +1,8 @@
 // Dense transforms of the block on the CDNA4 matrix cores.
 //
-// One kernel body serves three products, differing only in how tiles reach LDS and how
-// results leave:
+// The bf16 forward product runs k_gemm_dl (both operands K-contiguous bf16 rows, loaded
+// straight into LDS).  One register-staged kernel body, k_gemm, serves the other products
+// (and fp32 mode), differing only in how tiles reach LDS and how results leave:
 //   forward      Y_t   = Mcat_t  [n_dst x K]      . WcatT_t^T  (+ bias, opt. ReLU)
 //                K = (1 + R_t) * d_in: the self-loop and every relation into t are one
 //                K-concatenated product, so the sum over relations is the K reduction.
@@ -647,6 +648,156 @@ __global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const 
     }
 }
 
+// ------------------------------------------------------------------ direct-load kernel
+// bf16 products whose operands are both K-contiguous rows (the forward transform).  Tiles
+// go from global memory straight into LDS (16 bytes per lane per instruction, lane L's
+// piece landing at base + 16 L), S stages deep, so no registers stage them and S - 1 K
+// steps are in flight while one is multiplied.  An LDS row is the BK elements of K of one
+// operand row (RB bytes, CPR 16-byte chunks); chunk c of row r sits in slot c ^ swz(r), so
+// the 16 rows an MFMA operand read touches fall in distinct bank groups.  A lane picks the
+// global chunk that belongs in its fixed LDS slot.  Rows past the end and K past the range
+// read the zero buffer.  Waits are explicit (vector-memory count, then a plain barrier).
+template <int BK_>
+struct DlGeom {
+    static constexpr int BK = BK_;
+    static constexpr int RB = BK * 2;             // bytes per LDS row
+    static constexpr int CPR = RB / 16;           // chunks per row
+    static constexpr int RPI = 64 / CPR;          // rows per wave instruction
+    static_assert(CPR == 4 || CPR == 8, "BK 32 or 64");
+    __device__ __forceinline__ static int swz(int r) { return CPR == 8 ? (r & 7) : ((r >> 1) & 3); }
+    __device__ __forceinline__ static int off(int r, int c) { return r * RB + ((c ^ swz(r)) << 4); }
+};
+
+__device__ __forceinline__ void lds_dma16(const char *g, char *l) {
+    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1))) *)g,
+                                     (void __attribute__((address_space(3))) *)l, 16, 0, 0);
+}
+// wait until at most n vector-memory operations of this wave are outstanding (other
+// counters untouched), then a workgroup barrier with no memory fence: the fence of
+// __syncthreads would wait for every LDS load in flight
+template <int N>
+__device__ __forceinline__ void vm_wait_barrier() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+template <class C, int BK, int S, class Epi>
+__global__ __launch_bounds__(C::NT) void k_gemm_dl(const char *__restrict__ a, int64_t lda,
+                                                   int64_t M, const char *__restrict__ b,
+                                                   int64_t ldb, int64_t N, int64_t K,
+                                                   const Epi epi, int64_t tiles_m,
+                                                   int64_t tiles_n) {
+    using Gm = DlGeom<BK>;
+    constexpr int FM = C::FM, FN = C::FN, NW = C::NT / 64;
+    constexpr int A_BYTES = C::TM * Gm::RB, B_BYTES = C::TN * Gm::RB;
+    constexpr int STAGE = A_BYTES + B_BYTES;
+    constexpr int IA = C::TM / Gm::RPI / NW, IB = C::TN / Gm::RPI / NW;   // loads per wave
+    static_assert(IA * Gm::RPI * NW == C::TM && IB * Gm::RPI * NW == C::TN, "whole instructions");
+    constexpr int LPS = IA + IB;                                          // per step
+    static_assert((S - 2) * LPS < 64 && S >= 2, "vmcnt range");
+    __shared__ __attribute__((aligned(1024))) char lds[S * STAGE];
+    static_assert(S * STAGE >= NW * 16 * kStagePitch * 4, "epilogue staging space");
+
+    const int64_t t = xcd_major_id(blockIdx.x, (int64_t)gridDim.x);
+    const int64_t tm = t / tiles_n, tn = t - tm * tiles_n;
+    const int64_t m0 = tm * C::TM, n0 = tn * C::TN;
+    const int lane = threadIdx.x & 63;
+    // the wave index is uniform; as a scalar it makes every LDS destination a scalar too
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int wm = wave / C::WN, wn = wave % C::WN;
+    const char *zp = (const char *)g_zero16;
+    asm volatile("" : "+v"(zp));   // computed once, kept in registers
+
+    // this lane's rows and chunks in each load instruction (fixed over K)
+    const int lr = lane / Gm::CPR, ls = lane % Gm::CPR;
+    const char *pa[IA];
+    const char *pb[IB];
+    int ca[IA], cb[IB];
+#pragma unroll
+    for (int j = 0; j < IA; ++j) {
+        const int r = (wave * IA + j) * Gm::RPI + lr;
+        ca[j] = ls ^ Gm::swz(r);
+        pa[j] = m0 + r < M ? a + (m0 + r) * lda : nullptr;
+    }
+#pragma unroll
+    for (int j = 0; j < IB; ++j) {
+        const int r = (wave * IB + j) * Gm::RPI + lr;
+        cb[j] = ls ^ Gm::swz(r);
+        pb[j] = n0 + r < N ? b + (n0 + r) * ldb : nullptr;
+    }
+    const int64_t nk = (K + BK - 1) / BK;
+    auto issue = [&](int64_t step) {
+        char *st = lds + (int)(step % S) * STAGE;
+        const int64_t k0 = step * BK;
+#pragma unroll
+        for (int j = 0; j < IA; ++j) {
+            const int64_t k = k0 + ca[j] * 8;
+            const char *g = (pa[j] && k < K) ? pa[j] + k * 2 : zp;
+            lds_dma16(g, st + (wave * IA + j) * 1024);
+        }
+#pragma unroll
+        for (int j = 0; j < IB; ++j) {
+            const int64_t k = k0 + cb[j] * 8;
+            const char *g = (pb[j] && k < K) ? pb[j] + k * 2 : zp;
+            lds_dma16(g, st + A_BYTES + (wave * IB + j) * 1024);
+        }
+    };
+
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int st = 0; st < S - 1; ++st) issue(st);
+    const int r16 = lane & 15, q = lane >> 4;
+    for (int64_t it = 0; it < nk; ++it) {
+        vm_wait_barrier<(S - 2) * LPS>();
+        issue(it + S - 1);
+        const char *As = lds + (int)(it % S) * STAGE;
+        const char *Bs = As + A_BYTES;
+#pragma unroll
+        for (int s = 0; s < BK / 32; ++s) {
+            bf16x8 bv[FN];
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+                bv[i] = *(const bf16x8 *)(Bs + Gm::off(wn * FN * 16 + i * 16 + r16, s * 4 + q));
+#pragma unroll
+            for (int mi = 0; mi < FM; ++mi) {
+                const bf16x8 av = *(const bf16x8 *)(As + Gm::off(wm * FM * 16 + mi * 16 + r16, s * 4 + q));
+#pragma unroll
+                for (int ni = 0; ni < FN; ++ni)
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv[ni], acc[mi][ni], 0, 0, 0);
+            }
+        }
+    }
+    vm_wait_barrier<0>();   // padded steps' loads landed; LDS free for the epilogue
+
+    float *stage = (float *)lds + wave * 16 * kStagePitch;
+    const int rq = lane >> 4, cc = lane & 15;
+#pragma unroll
+    for (int mi = 0; mi < FM; ++mi) {
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                stage[(4 * rq + v) * kStagePitch + ni * 16 + cc] = acc[mi][ni][v];
+        __syncthreads();
+        const int r = lane >> 2, c0 = (lane & 3) * 16;
+        float vals[16];
+#pragma unroll
+        for (int e = 0; e < 16; e += 4) {
+            const float4 x = *(const float4 *)(stage + r * kStagePitch + c0 + e);
+            vals[e] = x.x; vals[e + 1] = x.y; vals[e + 2] = x.z; vals[e + 3] = x.w;
+        }
+        epi(m0 + wm * FM * 16 + mi * 16 + r, n0 + wn * FN * 16 + c0, vals, 0);
+        __syncthreads();
+    }
+}
+
 template <class C, class Mma, class LA, class LB, class Epi, int STAGES, int R>
 hipError_t launch_gemm(const LA &la, const LB &lb, const Epi &epi, int64_t M, int64_t N,
                        int64_t K, int64_t splits, int64_t k_per_split, hipStream_t s) {
@@ -695,9 +846,6 @@ __global__ __launch_bounds__(kThreads) void k_zero_outputs(DwOut out, int d_in, 
     if (e < per && out.w[sl]) out.w[sl][e] = 0.f;
 }
 
-#ifndef RGCN_GEMM_RSTAGES
-#define RGCN_GEMM_RSTAGES 1
-#endif
 #ifndef RGCN_GEMM_DMS_STAGES
 #define RGCN_GEMM_DMS_STAGES 1
 #endif
@@ -715,14 +863,14 @@ hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
                         hipStream_t s) {
     if (dt == RGCN_BF16) {
         using C = CfgFwd;
-        using TL = TileBf16<C>;
-        LoadRows<TL, C::NT, PlainRows> la{PlainRows{(const char *)a, (int64_t)K * 2, M},
-                                          (int64_t)K * 2};
-        LoadRows<TL, C::NT, PlainRows> lb{PlainRows{(const char *)wcat_t, (int64_t)K * 2, N},
-                                          (int64_t)K * 2};
-        return launch_gemm<C, MmaBf16<TL, C::FM, C::FN>, decltype(la), decltype(lb),
-                           EpiForward<true>, 2, RGCN_GEMM_RSTAGES>(
-            la, lb, EpiForward<true>{y, bias, M, N, relu}, M, N, K, 1, K, s);
+        const int64_t tiles_m = cdiv(M, C::TM), tiles_n = cdiv(N, C::TN);
+        if (tiles_m == 0 || tiles_n == 0) return hipSuccess;
+        hipLaunchKernelGGL((k_gemm_dl<C, 64, 2, EpiForward<true>>),
+                           dim3((unsigned)(tiles_m * tiles_n)), dim3(C::NT), 0, s,
+                           (const char *)a, (int64_t)K * 2, M, (const char *)wcat_t,
+                           (int64_t)K * 2, (int64_t)N, (int64_t)K,
+                           EpiForward<true>{y, bias, M, N, relu}, tiles_m, tiles_n);
+        return hipGetLastError();
     }
     using C = CfgF32;
     using TL = TileF32;
