@@ -1,38 +1,32 @@
-// Dense transforms of the block on the CDNA4 matrix cores.
-//
-// The bf16 forward product runs k_gemm_dl (both operands K-contiguous bf16 rows, loaded
-// straight into LDS).  One register-staged kernel body, k_gemm, serves the other products
-// (and fp32 mode), differing only in how tiles reach LDS and how results leave:
+// Dense transforms of the block on the CDNA4 matrix cores:
 //   forward      Y_t   = Mcat_t  [n_dst x K]      . WcatT_t^T  (+ bias, opt. ReLU)
 //                K = (1 + R_t) * d_in: the self-loop and every relation into t are one
 //                K-concatenated product, so the sum over relations is the K reduction.
 //   input side   dMs_t = dY_t [n_dst x d_out]    . [W_s rows]^T, slot columns / deg
 //   weight side  dW    = Mcat_t^T [K x n_dst]    . dY_t [n_dst x d_out]   (split over rows)
 //
-// bf16 forward and weight side: workgroup tile 256 x 256, eight waves in a 2 x 4
-// arrangement of 128 x 64, each wave an 8 x 4 grid of 16 x 16 MFMA tiles.  These products
-// are skinny (K and N of a few hundred against up to millions of rows), so what limits
-// them is how often the long operand is re-read: a 256-wide tile reads it half as often as
-// a 128-wide one.  The input side (N = one or two slots of d_in columns) and fp32 mode:
-// 128 x 128, four waves of 64 x 64.
+// bf16 mode, v_mfma_f32_16x16x32_bf16 with fp32 accumulation, one kernel per product:
+//   k_gemm_dl   forward: both operands are K-contiguous bf16 rows, loaded straight from
+//               global memory into LDS, 256 x 256 tiles (8 waves of 128 x 64);
+//   k_gemm      input side: the register-staged kernel below with 128 x 128 tiles (N is
+//               one or two slots of d_in columns; a 256-wide tile would be half empty);
+//   k_gemm_dw2  weight side: reduces over the rows of both operands; 256 x 256 tiles whose
+//               operands sit in LDS as loaded (one row per m) and are read with the LDS
+//               transpose read.
+// These products are skinny (K and N of a few hundred against up to millions of rows), so
+// what limits them is how often the long operand is re-read: a 256-wide tile reads it half
+// as often as a 128-wide one.  The fp32 output gradient dY enters both backward products as
+// a hi + lo pair of bf16 values (hi = bf16(x), lo = bf16(x - hi)), ~16 significant bits:
+// each fp32 tile is read from memory once and written to LDS as two bf16 tiles, and every
+// fragment of the other operand meets both.
 //
-// LDS holds both operands K-contiguous ("row r, k..."), one row = BK elements of K + 16
-// bytes of padding; the row pitch is an odd number of 16-byte units, so the 16 rows a
-// 16-lane group reads for one MFMA operand fall in distinct bank groups.  Global loads
-// are staged through registers, issued in a fixed order and always unconditionally (rows
-// past the end and K past the range read a zero buffer), so each LDS store waits only for
-// its own loads.
-//
-// The weight-side product reduces over the rows of both operands, so its tiles are
-// transposed on the way to LDS: each thread loads half of an 8 x 8 block (4 rows x 16
-// bytes, row-contiguous global reads), transposes it in registers and writes eight 8-byte
-// LDS pieces; BK = 64 with a 144-byte pitch.
-//
-// bf16 mode: v_mfma_f32_16x16x32_bf16, fp32 accumulation.  The fp32 output gradient dY
-// enters both backward products as a hi + lo pair of bf16 values (hi = bf16(x), lo =
-// bf16(x - hi)), which carries ~16 significant bits: each fp32 tile is read from memory
-// once and written to LDS as two bf16 tiles, and every fragment of the other operand meets
-// both.  fp32 mode: v_mfma_f32_16x16x4_f32.
+// k_gemm (input side, and every product in fp32 mode with v_mfma_f32_16x16x4_f32): LDS
+// holds both operands K-contiguous ("row r, k..."), one row = BK elements of K + 16 bytes
+// of padding; the row pitch is an odd number of 16-byte units, so the 16 rows a 16-lane
+// group reads for one MFMA operand fall in distinct bank groups.  Global loads are staged
+// through registers, issued in a fixed order and always unconditionally (rows past the end
+// and K past the range read a zero buffer), so each LDS store waits only for its own
+// loads.  The fp32 weight side transposes its tiles on the way to LDS with scalar writes.
 #include <type_traits>
 
 #include "common.h"
@@ -54,19 +48,9 @@ struct Cfg {
 };
 using CfgWide = Cfg<256, 256, 2, 4>;
 using CfgNarrow = Cfg<128, 128, 2, 2>;
-#ifndef RGCN_GEMM_FWD_WIDE
-#define RGCN_GEMM_FWD_WIDE 1
-#endif
-#ifndef RGCN_GEMM_DMS_WIDE
-#define RGCN_GEMM_DMS_WIDE 0
-#endif
-#ifndef RGCN_GEMM_DW_WIDE
-#define RGCN_GEMM_DW_WIDE 1
-#endif
-template <bool W> using CfgSel = typename std::conditional<W, CfgWide, CfgNarrow>::type;
-using CfgFwd = CfgSel<RGCN_GEMM_FWD_WIDE>;
-using CfgDms = CfgSel<RGCN_GEMM_DMS_WIDE>;
-using CfgDw = CfgSel<RGCN_GEMM_DW_WIDE>;
+using CfgFwd = CfgWide;     // bf16 forward (k_gemm_dl)
+using CfgDms = CfgNarrow;   // bf16 input side: N is one or two slots of d_in columns
+using CfgDw = CfgWide;      // bf16 weight side (k_gemm_dw2)
 using CfgF32 = Cfg<128, 128, 2, 2>;
 
 template <int ROWS_, int BK_, int ES_>
@@ -113,43 +97,6 @@ struct MmaBf16 {
                 for (int ni = 0; ni < FN; ++ni)
                     acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], b[ni],
                                                                           acc[mi][ni], 0, 0, 0);
-        }
-    }
-};
-
-// B held as two bf16 tiles (hi, lo) of one fp32 operand, next to each other in LDS:
-// acc += A.B_hi + A.B_lo, fp32 accumulation.
-template <class TL, int FM, int FN>
-struct MmaBf16Split {
-    using T = TL;
-    static constexpr int STAGE_BYTES = 3 * TL::BYTES;   // A, B_hi, B_lo
-    __device__ __forceinline__ static void run(const char *As, const char *Bs,
-                                               f32x4 (&acc)[FM][FN], int wm, int wn, int lane) {
-        const int r = lane & 15, q = lane >> 4;
-        const char *Bl = Bs + TL::BYTES;
-        // B fragments (hi and lo) stay in registers for the step; A fragments are read one
-        // 16-row block at a time
-#pragma unroll
-        for (int s = 0; s < TL::BK / 32; ++s) {
-            bf16x8 bh[FN], bl[FN];
-#pragma unroll
-            for (int i = 0; i < FN; ++i) {
-                const int bo = (wn * FN * 16 + i * 16 + r) * TL::PITCH + s * 64 + q * 16;
-                bh[i] = *(const bf16x8 *)(Bs + bo);
-                bl[i] = *(const bf16x8 *)(Bl + bo);
-            }
-#pragma unroll
-            for (int mi = 0; mi < FM; ++mi) {
-                const bf16x8 a =
-                    *(const bf16x8 *)(As + (wm * FM * 16 + mi * 16 + r) * TL::PITCH + s * 64 + q * 16);
-#pragma unroll
-                for (int ni = 0; ni < FN; ++ni) {
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bh[ni], acc[mi][ni],
-                                                                          0, 0, 0);
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bl[ni], acc[mi][ni],
-                                                                          0, 0, 0);
-                }
-            }
         }
     }
 };
@@ -329,76 +276,6 @@ struct LoadRowsF32HiLo {
             char *d = lds + st.lr[c] * TL::PITCH + st.lq[c] * 16;
             *(u32x4 *)d = h;
             *(u32x4 *)(d + LO_OFF) = l;
-        }
-    }
-};
-
-// Weight-side operands (bf16 mode, BK = 64): source [ksrc rows x cols] row-major; LDS row
-// = source column (TL::ROWS from col0), LDS k = source row.  The tile is 8 x (ROWS / 8)
-// blocks of 8 x 8; thread t owns half a block: block b = t / 2 (source rows
-// k0 + 8*(b%8) + 4*(t%2) .. +3, columns col0 + 8*(b/8) .. +7).  Four row reads of 16 bytes
-// (bf16 source) or 32 bytes (fp32 source), a transpose in registers, eight 8-byte LDS
-// writes.  SPLIT (fp32 source): the values go to two bf16 tiles, hi = bf16(x) at lds and
-// lo = bf16(x - hi) at lds + tile bytes, for MmaBf16Split.
-template <class TL, int NT, bool SRC_F32, bool SPLIT>
-struct LoadTransHalf {
-    static_assert(TL::BK == 64 && NT == 2 * TL::ROWS, "one half block per thread");
-    static constexpr int SES = SRC_F32 ? 4 : 2;
-    static constexpr int NH = SRC_F32 ? 2 : 1;
-    const char *base;
-    int64_t ld_bytes;
-    int64_t ksrc;
-    int64_t cols;
-    struct State {
-        int64_t col0;
-        int ib, cb, hb;
-        u32x4 reg[4][NH];
-    };
-    __device__ __forceinline__ void init(State &st, int64_t c0) const {
-        st.col0 = c0;
-        const int b = (int)threadIdx.x >> 1;
-        st.hb = threadIdx.x & 1;
-        st.ib = b & 7;
-        st.cb = b >> 3;
-    }
-    __device__ __forceinline__ void load(State &st, int64_t k0, int64_t kend) const {
-        const int64_t col = st.col0 + (int64_t)st.cb * 8;
-        const bool colok = col < cols;
-        const int64_t lim = kend < ksrc ? kend : ksrc;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int64_t i = k0 + st.ib * 8 + st.hb * 4 + r;
-            const bool ok = colok && i < lim;
-            const char *p = ok ? base + i * ld_bytes + col * SES : (const char *)g_zero16;
-#pragma unroll
-            for (int h = 0; h < NH; ++h) st.reg[r][h] = *(const u32x4 *)(p + h * 16);
-        }
-    }
-    __device__ __forceinline__ void store(const State &st, char *lds) const {
-        const int off = st.ib * 16 + st.hb * 8;
-        const auto &rg = st.reg;
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-            uint32_t w[2], wl[2];
-#pragma unroll
-            for (int p = 0; p < 2; ++p) {
-                if constexpr (SRC_F32) {
-                    const float x0 = __uint_as_float(rg[2 * p][c >> 2][c & 3]);
-                    const float x1 = __uint_as_float(rg[2 * p + 1][c >> 2][c & 3]);
-                    w[p] = pack_bf16x2(x0, x1);
-                    if constexpr (SPLIT)
-                        wl[p] = pack_bf16x2(x0 - __uint_as_float(w[p] << 16),
-                                            x1 - __uint_as_float(w[p] & 0xffff0000u));
-                } else {
-                    const uint32_t a0 = rg[2 * p][0][c >> 1];
-                    const uint32_t a1 = rg[2 * p + 1][0][c >> 1];
-                    w[p] = (c & 1) ? ((a0 >> 16) | (a1 & 0xffff0000u))
-                                   : ((a0 & 0xffffu) | (a1 << 16));
-                }
-            }
-            char *dst = lds + (st.cb * 8 + c) * TL::PITCH + off;
-            *(uint2 *)dst = make_uint2(w[0], w[1]);
-            if constexpr (SPLIT) *(uint2 *)(dst + TL::BYTES) = make_uint2(wl[0], wl[1]);
         }
     }
 };
@@ -798,6 +675,185 @@ __global__ __launch_bounds__(C::NT) void k_gemm_dl(const char *__restrict__ a, i
     }
 }
 
+// ------------------------------------------------------------------ weight side
+// dW partial of one split: out[c][o] = sum over the split's rows m of Mcat[m][c] dY[m][o].
+// The reduction runs over rows of both operands, so both tiles sit in LDS as loaded (row
+// = one m, TM or TN consecutive columns) and the MFMA fragments, which want 8 consecutive
+// m per lane, are read with the LDS transpose read: a 16-lane group hands in sixteen
+// 8-byte pieces (four columns of one row each) and every lane gets one column of four
+// rows.  Mcat (bf16) goes straight into LDS; dY (fp32) goes through registers and is
+// written as a hi and a lo bf16 tile, so each dY element is read once and every Mcat
+// fragment meets both parts.  512-byte LDS rows, 16-byte chunk c of row r at slot
+// c ^ 2 (r & 3): the four rows of one transpose read hit distinct banks.
+template <int BK_>
+struct DwGeom {
+    static constexpr int BK = BK_;                 // rows (m) per K step
+    static constexpr int RB = 512;                 // bytes per LDS row (256 bf16)
+    static constexpr int TILE = BK * RB;
+    __device__ __forceinline__ static int slot(int r, int c) { return c ^ ((r & 3) << 1); }
+};
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ s16x4 lds_tr16(const char *p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((s16x4 __attribute__((address_space(3))) *)p);
+}
+// Fragment of 16 columns [col0, col0 + 16) x rows [k0, k0 + 8) of a DwGeom tile for the
+// calling lane (group q = lane / 16 takes rows k0 + 8 q' where k0 already includes 8 q).
+template <class Gm>
+__device__ __forceinline__ bf16x8 dw_frag(const char *tile, int row0, int col0, int j) {
+    const int col = col0 + 4 * (j & 3);
+    const int r0 = row0 + (j >> 2), r1 = r0 + 4;
+    const int c = col >> 3, byte = (col & 7) * 2;
+    const s16x4 lo = lds_tr16(tile + r0 * Gm::RB + (Gm::slot(r0, c) << 4) + byte);
+    const s16x4 hi = lds_tr16(tile + r1 * Gm::RB + (Gm::slot(r1, c) << 4) + byte);
+    const s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+template <class C, int BK>
+__global__ __launch_bounds__(C::NT) void k_gemm_dw2(const char *__restrict__ mcat, int64_t M,
+                                                    int64_t Kcat, const float *__restrict__ dy,
+                                                    int64_t d_out, int64_t tiles_m,
+                                                    int64_t tiles_n, int64_t per,
+                                                    const EpiPartial epi) {
+    using Gm = DwGeom<BK>;
+    static_assert(C::TM == 256 && C::TN == 256, "512-byte LDS rows");
+    constexpr int FM = C::FM, FN = C::FN, NW = C::NT / 64;
+    constexpr int STAGE = 3 * Gm::TILE;                      // A, B hi, B lo
+    constexpr int IA = BK * Gm::RB / 1024 / NW;              // A loads per wave per step
+    static_assert(IA * NW * 1024 == BK * Gm::RB, "whole A instructions");
+    constexpr int NB = BK * 32 / C::NT;                      // dY pieces (8 floats) per thread
+    static_assert(NB * C::NT == BK * 32, "whole B pieces");
+    __shared__ __attribute__((aligned(1024))) char lds[2 * STAGE];
+    static_assert(2 * STAGE >= NW * 16 * kStagePitch * 4, "epilogue staging space");
+
+    const int64_t logical = xcd_major_id(blockIdx.x, (int64_t)gridDim.x);
+    const int64_t tiles = tiles_m * tiles_n;
+    const int64_t split = logical / tiles;
+    const int64_t t = logical - split * tiles;
+    const int64_t tm = t / tiles_n, tn = t - tm * tiles_n;
+    const int64_t c0 = tm * C::TM, o0 = tn * C::TN;
+    const int64_t kb = split * per;
+    const int64_t ke = kb + per < M ? kb + per : M;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int wm = wave / C::WN, wn = wave % C::WN;
+    const char *zp = (const char *)g_zero16;
+    asm volatile("" : "+v"(zp));
+
+    // A (Mcat rows) straight into LDS: instruction j of this wave covers rows
+    // 2 (IA wave + j) and the next, lane L the slot L % 32 of row L / 32
+    const int ar = lane >> 5, as = lane & 31;
+    auto issue_a = [&](int64_t step, char *st) {
+        const int64_t m0 = kb + step * BK;
+#pragma unroll
+        for (int j = 0; j < IA; ++j) {
+            const int r = (wave * IA + j) * 2 + ar;
+            const int c = Gm::slot(r, as);                    // the chunk that lives in slot `as`
+            const int64_t m = m0 + r, col = c0 + c * 8;
+            const char *g = (m < ke && col < Kcat) ? mcat + m * Kcat * 2 + col * 2 : zp;
+            lds_dma16(g, st + (wave * IA + j) * 1024);
+        }
+    };
+    // B (dY) through registers: piece u of this thread = row p / 32, columns 8 (p % 32) ..
+    f32x4 bq[NB][2];
+    auto load_b = [&](int64_t step) {
+        const int64_t m0 = kb + step * BK;
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int p = (int)threadIdx.x + u * C::NT;
+            const int r = p >> 5, g = p & 31;
+            const int64_t m = m0 + r, col = o0 + g * 8;
+            // the zero buffer holds 32 bytes, so both halves stay in bounds either way
+            const char *src = (m < ke && col < d_out) ? (const char *)(dy + m * d_out + col) : zp;
+            const __attribute__((address_space(1))) f32x4 *gs =
+                (const __attribute__((address_space(1))) f32x4 *)src;
+            bq[u][0] = gs[0];
+            bq[u][1] = gs[1];
+        }
+    };
+    auto store_b = [&](char *st) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int p = (int)threadIdx.x + u * C::NT;
+            const int r = p >> 5, g = p & 31;
+            const f32x4 x = bq[u][0], y = bq[u][1];
+            u32x4 h, l;
+            h.x = pack_bf16x2(x.x, x.y); h.y = pack_bf16x2(x.z, x.w);
+            h.z = pack_bf16x2(y.x, y.y); h.w = pack_bf16x2(y.z, y.w);
+            l.x = pack_bf16x2(x.x - bf16_lo(h.x), x.y - bf16_hi(h.x));
+            l.y = pack_bf16x2(x.z - bf16_lo(h.y), x.w - bf16_hi(h.y));
+            l.z = pack_bf16x2(y.x - bf16_lo(h.z), y.y - bf16_hi(h.z));
+            l.w = pack_bf16x2(y.z - bf16_lo(h.w), y.w - bf16_hi(h.w));
+            const int off = r * Gm::RB + (Gm::slot(r, g) << 4);
+            *(u32x4 *)(st + Gm::TILE + off) = h;
+            *(u32x4 *)(st + 2 * Gm::TILE + off) = l;
+        }
+    };
+
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int64_t nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+    issue_a(0, lds);
+    load_b(0);
+    store_b(lds);
+    __syncthreads();
+    const int j16 = lane & 15, q = lane >> 4;
+    for (int64_t it = 0; it < nk; ++it) {
+        char *cur = lds + (int)(it & 1) * STAGE;
+        char *nxt = lds + (int)((it + 1) & 1) * STAGE;
+        // next step's tiles in flight while this one is multiplied (a step past the end
+        // loads zeros into the free stage)
+        issue_a(it + 1, nxt);
+        load_b(it + 1);
+#pragma unroll
+        for (int s = 0; s < BK / 32; ++s) {
+            bf16x8 bh[FN], bl[FN];
+#pragma unroll
+            for (int ni = 0; ni < FN; ++ni) {
+                bh[ni] = dw_frag<Gm>(cur + Gm::TILE, s * 32 + 8 * q, wn * FN * 16 + ni * 16, j16);
+                bl[ni] = dw_frag<Gm>(cur + 2 * Gm::TILE, s * 32 + 8 * q, wn * FN * 16 + ni * 16, j16);
+            }
+#pragma unroll
+            for (int mi = 0; mi < FM; ++mi) {
+                const bf16x8 av = dw_frag<Gm>(cur, s * 32 + 8 * q, wm * FM * 16 + mi * 16, j16);
+#pragma unroll
+                for (int ni = 0; ni < FN; ++ni) {
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bh[ni], acc[mi][ni], 0, 0, 0);
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bl[ni], acc[mi][ni], 0, 0, 0);
+                }
+            }
+        }
+        store_b(nxt);
+        __syncthreads();   // waits for this wave's A loads and LDS stores, then all waves
+    }
+
+    float *stage = (float *)lds + wave * 16 * kStagePitch;
+    const int rq = lane >> 4, cc = lane & 15;
+#pragma unroll
+    for (int mi = 0; mi < FM; ++mi) {
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                stage[(4 * rq + v) * kStagePitch + ni * 16 + cc] = acc[mi][ni][v];
+        __syncthreads();
+        const int r = lane >> 2, cq = (lane & 3) * 16;
+        float vals[16];
+#pragma unroll
+        for (int e = 0; e < 16; e += 4) {
+            const float4 x = *(const float4 *)(stage + r * kStagePitch + cq + e);
+            vals[e] = x.x; vals[e + 1] = x.y; vals[e + 2] = x.z; vals[e + 3] = x.w;
+        }
+        epi(c0 + wm * FM * 16 + mi * 16 + r, o0 + wn * FN * 16 + cq, vals, split);
+        __syncthreads();
+    }
+}
+
 template <class C, class Mma, class LA, class LB, class Epi, int STAGES, int R>
 hipError_t launch_gemm(const LA &la, const LB &lb, const Epi &epi, int64_t M, int64_t N,
                        int64_t K, int64_t splits, int64_t k_per_split, hipStream_t s) {
@@ -809,12 +865,14 @@ hipError_t launch_gemm(const LA &la, const LB &lb, const Epi &epi, int64_t M, in
     return hipGetLastError();
 }
 
-// Split of the weight-side reduction over rows: about two workgroups per CU in total, each
-// split a whole number of K steps and at least 8 of them.
+// Split of the weight-side reduction over rows: at most `target` workgroups in total (one
+// wave of them where a workgroup fills a CU, so no partial second wave trails), each split
+// a whole number of K steps and at least 8 of them.
 template <class C>
-void dw_split(int64_t M, int Kcat, int d_out, int bk, int64_t *splits, int64_t *per) {
+void dw_split(int64_t M, int Kcat, int d_out, int bk, int64_t target, int64_t *splits,
+              int64_t *per) {
     const int64_t tiles = cdiv(Kcat, C::TM) * cdiv(d_out, C::TN);
-    int64_t want = cdiv(512, tiles);
+    int64_t want = target / tiles;
     const int64_t max_by_len = cdiv(M, (int64_t)bk * 8);
     if (want > max_by_len) want = max_by_len;
     if (want < 1) want = 1;
@@ -846,14 +904,17 @@ __global__ __launch_bounds__(kThreads) void k_zero_outputs(DwOut out, int d_in, 
     if (e < per && out.w[sl]) out.w[sl][e] = 0.f;
 }
 
+constexpr int kDwBK = 32;   // rows per K step of the bf16 weight-side kernel
+// workgroups of one weight-side product: the bf16 kernel holds a CU by itself (96 KB of
+// LDS), so one per CU of the 256 (a 2.02-wave grid left most CUs idle behind its last
+// few workgroups); the fp32 kernel fits two per CU
+constexpr int64_t kDwTargetBf16 = 256;
+constexpr int64_t kDwTargetF32 = 512;
 #ifndef RGCN_GEMM_DMS_STAGES
 #define RGCN_GEMM_DMS_STAGES 1
 #endif
 #ifndef RGCN_GEMM_DMS_R
 #define RGCN_GEMM_DMS_R 1
-#endif
-#ifndef RGCN_GEMM_DW_R
-#define RGCN_GEMM_DW_R 1
 #endif
 
 }  // namespace
@@ -917,8 +978,8 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_
 
 size_t gemm_dw_partial_bytes(int64_t M, int Kcat, int d_out) {
     int64_t sp16, p16, sp64, p64;
-    dw_split<CfgF32>(M, Kcat, d_out, TileF32::BK, &sp16, &p16);
-    dw_split<CfgDw>(M, Kcat, d_out, TileBf16<CfgDw>::BK, &sp64, &p64);
+    dw_split<CfgF32>(M, Kcat, d_out, TileF32::BK, kDwTargetF32, &sp16, &p16);
+    dw_split<CfgDw>(M, Kcat, d_out, kDwBK, kDwTargetBf16, &sp64, &p64);
     const int64_t sp = sp16 > sp64 ? sp16 : sp64;
     return (size_t)(sp > 0 ? sp : 1) * Kcat * d_out * 4 + 256;
 }
@@ -929,9 +990,9 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
     const bool bf = dt == RGCN_BF16;
     int64_t splits, per;
     if (bf)
-        dw_split<CfgDw>(M, Kcat, d_out, TileBf16<CfgDw>::BK, &splits, &per);
+        dw_split<CfgDw>(M, Kcat, d_out, kDwBK, kDwTargetBf16, &splits, &per);
     else
-        dw_split<CfgF32>(M, Kcat, d_out, TileF32::BK, &splits, &per);
+        dw_split<CfgF32>(M, Kcat, d_out, TileF32::BK, kDwTargetF32, &splits, &per);
     if (splits == 0) {  // no rows: every requested gradient is zero
         hipLaunchKernelGGL(k_zero_outputs, dim3((unsigned)cdiv((int64_t)d_in * d_out, kThreads),
                            (unsigned)out.count), dim3(kThreads), 0, s, out, d_in, d_out);
@@ -939,13 +1000,12 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
     }
     EpiPartial epi{partial, Kcat, d_out};
     if (bf) {
-        // dY enters as hi + lo bf16 tiles (two MFMAs per operand pair, one load)
-        using C = CfgDw;
-        using TL = TileBf16<C>;
-        LoadTransHalf<TL, C::NT, false, false> la{(const char *)mcat, (int64_t)Kcat * 2, M, Kcat};
-        LoadTransHalf<TL, C::NT, true, true> lb{(const char *)dy, (int64_t)d_out * 4, M, d_out};
-        RGCN_HIP_TRY((launch_gemm<C, MmaBf16Split<TL, C::FM, C::FN>, decltype(la), decltype(lb),
-                                  EpiPartial, 1, RGCN_GEMM_DW_R>(la, lb, epi, Kcat, d_out, M, splits, per, s)));
+        using C = CfgWide;
+        const int64_t tiles_m = cdiv(Kcat, C::TM), tiles_n = cdiv(d_out, C::TN);
+        hipLaunchKernelGGL((k_gemm_dw2<C, kDwBK>), dim3((unsigned)(tiles_m * tiles_n * splits)),
+                           dim3(C::NT), 0, s, (const char *)mcat, M, (int64_t)Kcat, dy,
+                           (int64_t)d_out, tiles_m, tiles_n, per, epi);
+        RGCN_HIP_TRY(hipGetLastError());
     } else {
         using C = CfgF32;
         LoadTransF32<C::NT> la{(const char *)mcat, (int64_t)Kcat * 4, M, Kcat};
