@@ -62,6 +62,7 @@ struct Layout {
     // workspace offsets
     size_t off_slots = 0, off_fwd_order = 0, off_fwd_desc = 0, off_bwd_order = 0, off_err = 0;
     size_t off_fwd_chunks = 0;
+    size_t off_flags = 0;         // schedule flags: [0] forward, [1 + t] backward of type t
     int64_t nc_max = 0;           // chunk bound of the flattened forward stream
     size_t off_csc_indptr[kMaxRels], off_csc_dst[kMaxRels];
     // combined transpose of the relations leaving grad types
@@ -218,6 +219,7 @@ rgcn_status make_layout(const rgcn_block *b, const rgcn_params *p, Layout &L) {
     // persistent region
     size_t off = 0;
     L.off_err = off;                      off += 256;
+    L.off_flags = off;                    off += 256;
     L.off_slots = off;                    off += align256(sizeof(FwdSlot) * kMaxSlots);
     L.off_fwd_order = off;                off += align256((size_t)L.n_seg * 4 + 4);
     L.off_fwd_desc = off;                 off += align256((size_t)L.n_seg * sizeof(SegDesc) + 16);
@@ -401,8 +403,11 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
     if (L.nslots > 0)
         TRY_HIP(fill_words(ws + L.off_slots, L.slots, sizeof(FwdSlot) * L.nslots, stream),
                 "slot table");
-    TRY_HIP(fwd_schedule(L.slots, L.nslots, L.n_seg, (int32_t *)(ws + L.off_fwd_order), scratch,
-                         stream), "forward schedule");
+    uint32_t *sched_flag = (uint32_t *)(ws + L.off_flags);
+    {
+        const uint32_t zeros[1 + kMaxTypes] = {};
+        TRY_HIP(fill_words(sched_flag, zeros, sizeof zeros, stream), "schedule flags");
+    }
     {
         int64_t moff[kMaxTypes], mld[kMaxTypes];
         for (int t = 0; t < kMaxTypes; ++t) {
@@ -411,9 +416,9 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
         }
         // segment weights sit in the plan scratch after the chunk pass's own temporaries
         int32_t *weight = (int32_t *)(scratch + fwd_chunks_temp_bytes(L.n_seg));
-        TRY_HIP(fwd_descriptors(L.slots, L.nslots, (const int32_t *)(ws + L.off_fwd_order), L.n_seg,
-                                moff, mld, L.es, (SegDesc *)(ws + L.off_fwd_desc), weight, stream),
-                "forward descriptors");
+        TRY_HIP(fwd_plan(L.slots, L.nslots, L.n_seg, (int32_t *)(ws + L.off_fwd_order), moff, mld,
+                         L.es, (SegDesc *)(ws + L.off_fwd_desc), weight, sched_flag, scratch,
+                         stream), "forward schedule");
         TRY_HIP(fwd_chunks(weight, L.n_seg, L.nc_max, (int32_t *)(ws + L.off_fwd_chunks), scratch,
                            stream), "forward chunks");
     }
@@ -441,7 +446,7 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
             if (block->rels[r].src_type == t)
                 kr.csc_indptr[kr.count++] = (const int32_t *)(ws + L.off_csc_indptr[r]);
         TRY_HIP(bwd_schedule(kr, block->n_src[t], (int32_t *)(ws + L.off_bwd_order) + L.bwd_base[t],
-                             scratch, stream), "backward schedule");
+                             scratch, sched_flag + 1 + t, stream), "backward schedule");
     }
     return RGCN_OK;
 }

@@ -92,14 +92,13 @@ size_t scan_temp_bytes(int64_t n);
 hipError_t exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, void *temp,
                               hipStream_t s);
 size_t bucket_sort_temp_bytes(int64_t n, int nbuckets);
-hipError_t fwd_schedule(const FwdSlot *slots_dev, int nslots, int64_t n_seg, int32_t *order,
-                        void *temp, hipStream_t s);
-// Segment descriptors in schedule order; mcat_off[t]: byte offset of Mcat_t in the
-// workspace, mcat_ld[t]: its row length in elements, es: element size.
-// weight[p] = entries of segment p in the flattened forward stream (max(deg, 1)).
-hipError_t fwd_descriptors(const FwdSlot *slots_host, int nslots, const int32_t *order,
-                           int64_t n_seg, const int64_t *mcat_off, const int64_t *mcat_ld,
-                           int es, SegDesc *desc, int32_t *weight, hipStream_t s);
+// Forward schedule and segment descriptors in schedule order; mcat_off[t]: byte offset of
+// Mcat_t in the workspace, mcat_ld[t]: its row length in elements, es: element size.
+// weight[p] = entries of segment p in the flattened forward stream (max(deg, 1)).  *flag
+// (zero on entry) ends nonzero when some segment is heavy and the schedule was sorted.
+hipError_t fwd_plan(const FwdSlot *slots_host, int nslots, int64_t n_seg, int32_t *order,
+                    const int64_t *mcat_off, const int64_t *mcat_ld, int es, SegDesc *desc,
+                    int32_t *weight, uint32_t *flag, void *temp, hipStream_t s);
 // Flattened forward stream split into chunks of kFwdChunk entries (segments whole): cs has
 // nc_max + 2 entries, nc_max = fwd_chunk_bound(n_seg, sum of relation nnz); cs[c] = first
 // segment of chunk c, cs[nc_max + 1] = total entries.  temp: fwd_chunks_temp_bytes(n_seg);
@@ -128,8 +127,9 @@ struct BwdKeyRels {          // relations leaving one source type
     int32_t count;
     const int32_t *csc_indptr[kMaxRels];
 };
+// *flag (zero on entry) ends nonzero when some row is heavy and the schedule was sorted.
 hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, void *temp,
-                        hipStream_t s);
+                        uint32_t *flag, hipStream_t s);
 hipError_t fill_words(void *dst, const void *src_host, size_t bytes, hipStream_t s);
 
 // aggregate.hip

@@ -5,6 +5,10 @@
 #include "common.h"
 
 namespace rgcn {
+// exclusive scan whose kernels do nothing while *gate is zero (gate NULL: always run)
+hipError_t scan_gated(const int32_t *in, int32_t *out, int64_t n, void *temp,
+                      const uint32_t *gate, hipStream_t s);
+
 namespace {
 
 constexpr int kThreads = 256;
@@ -35,8 +39,12 @@ __device__ int wg_exclusive_scan(int v, int *total) {
 }
 
 // ---------------------------------------------------------------- scan (3 kernels)
+// A gate (NULL = none) is a device word: kernels given one do nothing while it is zero.
+__device__ __forceinline__ bool gated_off(const uint32_t *gate) { return gate && *gate == 0u; }
+
 __global__ __launch_bounds__(kThreads) void k_scan_reduce(const int32_t *in, int64_t n,
-                                                          int32_t *partial) {
+                                                          int32_t *partial, const uint32_t *gate) {
+    if (gated_off(gate)) return;
     const int64_t base = (int64_t)blockIdx.x * kScanTile;
     int sum = 0;
     for (int u = 0; u < kScanItems; ++u) {
@@ -48,7 +56,9 @@ __global__ __launch_bounds__(kThreads) void k_scan_reduce(const int32_t *in, int
     if (threadIdx.x == 0) partial[blockIdx.x] = total;
 }
 
-__global__ __launch_bounds__(kThreads) void k_scan_partials(int32_t *partial, int64_t nb) {
+__global__ __launch_bounds__(kThreads) void k_scan_partials(int32_t *partial, int64_t nb,
+                                                            const uint32_t *gate) {
+    if (gated_off(gate)) return;
     int carry = 0;
     for (int64_t c0 = 0; c0 < nb; c0 += kScanTile) {
         int v[kScanItems];
@@ -70,7 +80,9 @@ __global__ __launch_bounds__(kThreads) void k_scan_partials(int32_t *partial, in
 }
 
 __global__ __launch_bounds__(kThreads) void k_scan_apply(const int32_t *in, int32_t *out,
-                                                         int64_t n, const int32_t *partial) {
+                                                         int64_t n, const int32_t *partial,
+                                                         const uint32_t *gate) {
+    if (gated_off(gate)) return;
     const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
     int v[kScanItems];
     int sum = 0;
@@ -94,7 +106,8 @@ __global__ __launch_bounds__(kThreads) void k_scan_apply(const int32_t *in, int3
 // key in that order keeps the sort stable.
 template <int NB, class KeyFn>
 __global__ __launch_bounds__(kThreads) void k_bucket_hist(KeyFn kf, int64_t n, int32_t *hist,
-                                                          int32_t ntiles) {
+                                                          int32_t ntiles, const uint32_t *gate) {
+    if (gated_off(gate)) return;
     __shared__ int32_t h[NB];
     for (int b = threadIdx.x; b < NB; b += kThreads) h[b] = 0;
     __syncthreads();
@@ -111,7 +124,9 @@ __global__ __launch_bounds__(kThreads) void k_bucket_hist(KeyFn kf, int64_t n, i
 template <int NB, int BITS, class KeyFn, class PutFn>
 __global__ __launch_bounds__(kThreads) void k_bucket_scatter(KeyFn kf, PutFn put, int64_t n,
                                                              const int32_t *offs,
-                                                             int32_t ntiles) {
+                                                             int32_t ntiles,
+                                                             const uint32_t *gate) {
+    if (gated_off(gate)) return;
     __shared__ int32_t run[NB];
     __shared__ int32_t wcnt[kThreads / 64][NB];
     for (int b = threadIdx.x; b < NB; b += kThreads) {
@@ -155,17 +170,17 @@ __global__ __launch_bounds__(kThreads) void k_bucket_scatter(KeyFn kf, PutFn put
 
 template <int NB, int BITS, class KeyFn, class PutFn>
 hipError_t bucket_sort(const KeyFn &kf, const PutFn &put, int64_t n, void *temp,
-                       hipStream_t s) {
+                       hipStream_t s, const uint32_t *gate = nullptr) {
     if (n == 0) return hipSuccess;
     const int64_t ntiles = cdiv(n, kSortTile);
     int32_t *hist = (int32_t *)temp;
     void *scan_tmp = (char *)temp + align_up((size_t)NB * ntiles * 4, 256);
     hipLaunchKernelGGL((k_bucket_hist<NB, KeyFn>), dim3((unsigned)ntiles), dim3(kThreads), 0,
-                       s, kf, n, hist, (int32_t)ntiles);
+                       s, kf, n, hist, (int32_t)ntiles, gate);
     RGCN_HIP_TRY(hipGetLastError());
-    RGCN_HIP_TRY(exclusive_scan_i32(hist, hist, (int64_t)NB * ntiles, scan_tmp, s));
+    RGCN_HIP_TRY(scan_gated(hist, hist, (int64_t)NB * ntiles, scan_tmp, gate, s));
     hipLaunchKernelGGL((k_bucket_scatter<NB, BITS, KeyFn, PutFn>), dim3((unsigned)ntiles),
-                       dim3(kThreads), 0, s, kf, put, n, hist, (int32_t)ntiles);
+                       dim3(kThreads), 0, s, kf, put, n, hist, (int32_t)ntiles, gate);
     return hipGetLastError();
 }
 
@@ -274,12 +289,9 @@ struct DescArgs {
     int64_t mcat_ld[kMaxTypes];
     int32_t es;
 };
-__global__ __launch_bounds__(kThreads) void k_fwd_desc(DescArgs a, const int32_t *order,
-                                                       int64_t n_seg, SegDesc *desc,
-                                                       int32_t *weight) {
-    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (p >= n_seg) return;
-    const int64_t seg = order[p];
+// Descriptor of segment seg written at schedule position p; returns its degree.
+__device__ __forceinline__ int32_t desc_of(const DescArgs &a, int64_t seg, int64_t p,
+                                           SegDesc *desc, int32_t *weight) {
     int lo = 0, hi = a.nslots - 1;
     while (lo < hi) {
         int mid = (lo + hi + 1) >> 1;
@@ -300,7 +312,38 @@ __global__ __launch_bounds__(kThreads) void k_fwd_desc(DescArgs a, const int32_t
     d.info = (uint32_t)((out >> 32) & 0xffu) | ((uint32_t)lo << 8);
     desc[p] = d;
     weight[p] = d.deg > 0 ? d.deg : 1;
+    return d.deg;
 }
+
+// IDENT: schedule position p holds segment p; order[p] = p, and *flag is raised when some
+// segment is heavy (a schedule key other than the last), i.e. when the sorted schedule is
+// not the identity.  Otherwise (gated on that flag): segment order[p].
+template <bool IDENT>
+__global__ __launch_bounds__(kThreads) void k_fwd_desc(DescArgs a, int32_t *order,
+                                                       int64_t n_seg, SegDesc *desc,
+                                                       int32_t *weight, uint32_t *flag) {
+    if (!IDENT && *flag == 0u) return;
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const bool in = p < n_seg;
+    int64_t seg = p;
+    if (!IDENT && in) seg = order[p];
+    if (IDENT && in) order[p] = (int32_t)p;
+    bool heavy = false;
+    if (in) heavy = desc_of(a, seg, p, desc, weight) > 32;
+    if (IDENT && __ballot(heavy) != 0 && (threadIdx.x & 63) == 0) atomicOr(flag, 1u);
+}
+
+// Backward rows of one type in enumeration order (order[j] = j); *flag is raised when some
+// row is heavy, i.e. when the sorted schedule is not the identity.
+__global__ __launch_bounds__(kThreads) void k_bwd_ident(BwdKey kf, int64_t n, int32_t *order,
+                                                        uint32_t *flag) {
+    const int64_t j = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const bool in = j < n;
+    if (in) order[j] = (int32_t)j;
+    const bool heavy = in && kf(j) != kSchedBuckets - 1;
+    if (__ballot(heavy) != 0 && (threadIdx.x & 63) == 0) atomicOr(flag, 1u);
+}
+
 
 // Chunk starts of the flattened forward stream.  pre = exclusive prefix of the segment
 // weights (entries per segment).  Segment p belongs to chunk pre[p] / kFwdChunk; cs[c] is
@@ -333,18 +376,24 @@ __global__ void k_fill_words(uint32_t *dst, Words a) {
 
 size_t scan_temp_bytes(int64_t n) { return align_up((size_t)cdiv(n, kScanTile) * 4 + 4, 256); }
 
-hipError_t exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, void *temp,
-                              hipStream_t s) {
+hipError_t scan_gated(const int32_t *in, int32_t *out, int64_t n, void *temp,
+                      const uint32_t *gate, hipStream_t s) {
     if (n == 0) return hipSuccess;
     const int64_t nb = cdiv(n, kScanTile);
     int32_t *partial = (int32_t *)temp;
-    hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)nb), dim3(kThreads), 0, s, in, n, partial);
+    hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)nb), dim3(kThreads), 0, s, in, n, partial,
+                       gate);
     RGCN_HIP_TRY(hipGetLastError());
-    hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kThreads), 0, s, partial, nb);
+    hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kThreads), 0, s, partial, nb, gate);
     RGCN_HIP_TRY(hipGetLastError());
     hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)nb), dim3(kThreads), 0, s, in, out, n,
-                       partial);
+                       partial, gate);
     return hipGetLastError();
+}
+
+hipError_t exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, void *temp,
+                              hipStream_t s) {
+    return scan_gated(in, out, n, temp, nullptr, s);
 }
 
 size_t bucket_sort_temp_bytes(int64_t n, int nbuckets) {
@@ -353,26 +402,17 @@ size_t bucket_sort_temp_bytes(int64_t n, int nbuckets) {
            scan_temp_bytes((int64_t)nbuckets * ntiles);
 }
 
-hipError_t fwd_schedule(const FwdSlot *slots_host, int nslots, int64_t n_seg, int32_t *order,
-                        void *temp, hipStream_t s) {
-    FwdKey kf;
-    kf.nslots = nslots;
-    for (int i = 0; i < kMaxSlots; ++i) {
-        kf.base[i] = i < nslots ? slots_host[i].seg_base : 0;
-        kf.indptr[i] = i < nslots ? slots_host[i].indptr : nullptr;
-    }
-    return bucket_sort<kSchedBuckets, 5>(kf, PutIndex{order}, n_seg, temp, s);
-}
-
-hipError_t fwd_descriptors(const FwdSlot *slots_host, int nslots, const int32_t *order,
-                           int64_t n_seg, const int64_t *mcat_off, const int64_t *mcat_ld,
-                           int es, SegDesc *desc, int32_t *weight, hipStream_t s) {
+hipError_t fwd_plan(const FwdSlot *slots_host, int nslots, int64_t n_seg, int32_t *order,
+                    const int64_t *mcat_off, const int64_t *mcat_ld, int es, SegDesc *desc,
+                    int32_t *weight, uint32_t *flag, void *temp, hipStream_t s) {
     if (n_seg == 0) return hipSuccess;
     DescArgs a;
     a.nslots = nslots;
+    FwdKey kf;
+    kf.nslots = nslots;
     for (int i = 0; i < kMaxSlots; ++i) {
-        a.base[i] = i < nslots ? slots_host[i].seg_base : 0;
-        a.indptr[i] = i < nslots ? slots_host[i].indptr : nullptr;
+        a.base[i] = kf.base[i] = i < nslots ? slots_host[i].seg_base : 0;
+        a.indptr[i] = kf.indptr[i] = i < nslots ? slots_host[i].indptr : nullptr;
         a.dst[i] = (int16_t)(i < nslots ? slots_host[i].dst_type : 0);
         a.col_off[i] = i < nslots ? slots_host[i].col_off : 0;
     }
@@ -381,8 +421,15 @@ hipError_t fwd_descriptors(const FwdSlot *slots_host, int nslots, const int32_t 
         a.mcat_ld[t] = mcat_ld[t];
     }
     a.es = es;
-    hipLaunchKernelGGL(k_fwd_desc, dim3((unsigned)cdiv(n_seg, kThreads)), dim3(kThreads), 0, s, a,
-                       order, n_seg, desc, weight);
+    const dim3 grid((unsigned)cdiv(n_seg, kThreads));
+    // enumeration order first; the sort and the second descriptor pass run only when some
+    // segment is heavy (otherwise the stable sort by key is the identity)
+    hipLaunchKernelGGL(k_fwd_desc<true>, grid, dim3(kThreads), 0, s, a, order, n_seg, desc,
+                       weight, flag);
+    RGCN_HIP_TRY(hipGetLastError());
+    RGCN_HIP_TRY((bucket_sort<kSchedBuckets, 5>(kf, PutIndex{order}, n_seg, temp, s, flag)));
+    hipLaunchKernelGGL(k_fwd_desc<false>, grid, dim3(kThreads), 0, s, a, order, n_seg, desc,
+                       weight, flag);
     return hipGetLastError();
 }
 
@@ -406,8 +453,12 @@ hipError_t fwd_chunks(const int32_t *weight, int64_t n_seg, int64_t nc_max, int3
 }
 
 hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, void *temp,
-                        hipStream_t s) {
-    return bucket_sort<kSchedBuckets, 5>(BwdKey{rels}, PutIndex{order}, n_rows, temp, s);
+                        uint32_t *flag, hipStream_t s) {
+    if (n_rows == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_bwd_ident, dim3((unsigned)cdiv(n_rows, kThreads)), dim3(kThreads), 0, s,
+                       BwdKey{rels}, n_rows, order, flag);
+    RGCN_HIP_TRY(hipGetLastError());
+    return bucket_sort<kSchedBuckets, 5>(BwdKey{rels}, PutIndex{order}, n_rows, temp, s, flag);
 }
 
 // Digit plan of an LSD radix sort of keys < key_range: the fewest passes of at most 10
