@@ -166,9 +166,9 @@ struct GatherTabs {
 // Forward gather over the flattened stream of the schedule: every in-edge of a segment is
 // one entry, and a self-loop row or a segment of degree 0 is one entry as well.  The
 // stream is cut into balanced contiguous ranges of whole segments (chunks of kFwdChunk
-// entries, split evenly over the groups of the grid), so every group moves the same number
-// of rows whatever the degrees, and consecutive segments' indices and row ids are read by
-// the same group.
+// rows moved -- entries read plus one row written per segment -- split evenly over the
+// groups of the grid), so every group moves about the same number of rows whatever the
+// degrees, and consecutive segments' indices and row ids are read by the same group.
 //
 // A group of G lanes takes S = G entries per step.  A step's entries are resolved with one
 // entry per lane: the G segment descriptors from the step's first segment are loaded one
@@ -186,7 +186,8 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
                                                           int64_t nc_max,
                                                           const FwdSlot *__restrict__ slots,
                                                           int nslots, GatherTabs tabs,
-                                                          char *__restrict__ ws, int chunks) {
+                                                          char *__restrict__ ws, int chunks,
+                                                          uint32_t *claims) {
     constexpr int VEC = BF16 ? 8 : 4;
     constexpr int ES = BF16 ? 2 : 4;
     constexpr int S = G;
@@ -214,8 +215,19 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
     const int64_t gid = ((int64_t)blockIdx.x * W + wave) * GPW + lane / G;
     const int64_t total = cs[nc_max + 1];
     const int64_t nc = (total + kFwdChunk - 1) / kFwdChunk;
-    const int32_t s_lo = cs[gid * nc / ngroups];
-    const int32_t s_hi = cs[(gid + 1) * nc / ngroups];
+    // Work is claimed in runs of kFwdClaim chunks: run gid first, then runs from the shared
+    // counter (which starts at ngroups), each time this group's window stage reaches the
+    // end of its run, so the stream continues without a pipeline restart.  Costs per row
+    // differ between source tables (a row of the largest one costs more), which a static
+    // split cannot know.
+    auto run_of = [&](int64_t c, int32_t &lo, int32_t &hi) {
+        const int64_t a = c * kFwdClaim, b = a + kFwdClaim < nc ? a + kFwdClaim : nc;
+        lo = a < nc ? cs[a] : 0;
+        hi = a < nc ? cs[b] : 0;
+        return a < nc;
+    };
+    int32_t s_lo, s_hi;
+    bool live = run_of(gid, s_lo, s_hi);
     const char *zero = (const char *)g_zero;
     const int64_t zrow = (int64_t)(uintptr_t)g_zero_row;
 
@@ -302,13 +314,28 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
         return j < 0 ? zrow : (int64_t)(uintptr_t)s_tab[t].base + row * (s_tab[t].ld * ES);
     };
 
-    // pipeline prologue: steps 0, 1, 2
     int32_t sc = s_lo, e0 = 0;
+    // after a scan: at the end of the run, continue with the next claimed run
+    auto next_run = [&]() {
+        const bool need = live && sc >= s_hi;
+        uint32_t c = 0;
+        if (need && lg == 0) c = atomicAdd(claims, 1u);
+        c = __shfl(c, gb, 64);
+        if (need) {
+            live = run_of(c, s_lo, s_hi);
+            sc = live ? s_lo : sc;
+            e0 = 0;
+        }
+    };
+
+    // pipeline prologue: steps 0, 1, 2
     SegDesc dw = load_win(sc);
     Ent ez = scan(dw, sc, e0);
+    next_run();
     dw = load_win(sc);
     int32_t jz = load_src(ez);
     Ent ey = scan(dw, sc, e0);
+    next_run();
     dw = load_win(sc);
     int32_t jy = load_src(ey);
     int64_t az = load_addr(ez.slot, jz);
@@ -319,7 +346,9 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
 #pragma unroll
         for (int v = 0; v < VEC; ++v) acc[p][v] = 0.f;
 
-    while (__ballot(ez.kind != 0) != 0) {
+    // a step with no entries (the end of a run, an empty run) does not end a group: it
+    // ends when nothing is in flight and it can claim no more
+    while (__ballot(ez.kind != 0 || ey.kind != 0 || dw.deg >= 0 || live) != 0) {
         __builtin_amdgcn_wave_barrier();
         s_addr[wave][lane] = az;
         s_out[wave][lane] = ez.out;
@@ -344,6 +373,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
         // this step's first rows, then the later pipeline stages while they are in flight
         issue(0, v[0]);
         Ent ex = scan(dw, sc, e0);
+        next_run();
         dw = load_win(sc);
         const int32_t jx = load_src(ex);
         const int64_t ay = load_addr(ey.slot, jy);
@@ -816,41 +846,45 @@ int64_t resident_wgs(K kernel) {
 template <bool B, int G, int C, bool FULL>
 hipError_t launch_flat_k(const SegDesc *desc, const int32_t *cs, int64_t nc_max,
                          const FwdSlot *slots_dev, int nslots, const GatherTabs &tabs,
-                         char *ws_base, int chunks, hipStream_t s) {
+                         char *ws_base, int chunks, uint32_t *claims, hipStream_t s) {
     constexpr int U0 = RGCN_FLAT_ROWS / C > 0 ? RGCN_FLAT_ROWS / C : 1;
     constexpr int U = U0 < G ? U0 : G;
     const int64_t groups_per_wg = (int64_t)(kThreads / 64) * (64 / G);
-    int64_t wgs = cdiv(nc_max, groups_per_wg);
+    int64_t wgs = cdiv(cdiv(nc_max, kFwdClaim), groups_per_wg);
     const int64_t cap = resident_wgs(k_gather_flat<B, G, C, U, FULL>);
     if (wgs > cap) wgs = cap;
     if (wgs < 1) wgs = 1;
+    // the shared run counter starts past the runs the groups take first
+    const uint32_t first = (uint32_t)(wgs * groups_per_wg);
+    RGCN_HIP_TRY(fill_words(claims, &first, 4, s));
     hipLaunchKernelGGL((k_gather_flat<B, G, C, U, FULL>), dim3((unsigned)wgs), dim3(kThreads), 0,
-                       s, desc, cs, nc_max, slots_dev, nslots, tabs, ws_base, chunks);
+                       s, desc, cs, nc_max, slots_dev, nslots, tabs, ws_base, chunks, claims);
     return hipGetLastError();
 }
 template <bool B, int G, int C>
 hipError_t launch_flat(const SegDesc *desc, const int32_t *cs, int64_t nc_max,
                        const FwdSlot *slots_dev, int nslots, const GatherTabs &tabs,
-                       char *ws_base, int chunks, hipStream_t s) {
+                       char *ws_base, int chunks, uint32_t *claims, hipStream_t s) {
     // every lane of a group owns a chunk of the row: no per-lane range checks
     if (chunks == G * C)
         return launch_flat_k<B, G, C, true>(desc, cs, nc_max, slots_dev, nslots, tabs, ws_base,
-                                            chunks, s);
+                                            chunks, claims, s);
     return launch_flat_k<B, G, C, false>(desc, cs, nc_max, slots_dev, nslots, tabs, ws_base,
-                                         chunks, s);
+                                         chunks, claims, s);
 }
 
 template <bool B>
 hipError_t flat_dispatch(const SegDesc *desc, const int32_t *cs, int64_t nc_max,
                          const FwdSlot *slots_dev, int nslots, const GatherTabs &tabs,
-                         char *ws_base, int chunks, hipStream_t s) {
+                         char *ws_base, int chunks, uint32_t *claims, hipStream_t s) {
     // lanes per row: the next power of two >= chunks / chunks-per-lane, at least 4
     const int cpl = (int)cdiv(chunks, 64);
     const int need = (int)cdiv(chunks, cpl);
     int g = 4;
     while (g < need) g <<= 1;
 #define RGCN_FLAT(G_, C_) \
-    return launch_flat<B, G_, C_>(desc, cs, nc_max, slots_dev, nslots, tabs, ws_base, chunks, s)
+    return launch_flat<B, G_, C_>(desc, cs, nc_max, slots_dev, nslots, tabs, ws_base, chunks, \
+                                  claims, s)
     if (cpl == 1) {
         if (g == 4) RGCN_FLAT(4, 1);
         if (g == 8) RGCN_FLAT(8, 1);
@@ -866,16 +900,17 @@ hipError_t flat_dispatch(const SegDesc *desc, const int32_t *cs, int64_t nc_max,
 
 hipError_t gather_mean(rgcn_dtype dt, int d_in, const SegDesc *desc, int64_t n_seg,
                        const int32_t *chunk_starts, int64_t nc_max, const FwdSlot *slots_dev,
-                       int nslots, const TypeInput *in, char *ws_base, hipStream_t s) {
+                       int nslots, const TypeInput *in, char *ws_base, uint32_t *claims,
+                       hipStream_t s) {
     if (n_seg == 0) return hipSuccess;
     const bool bf = dt == RGCN_BF16;
     const int chunks = bf ? d_in / 8 : d_in / 4;
     GatherTabs tabs;
     for (int t = 0; t < kMaxTypes; ++t) tabs.in[t] = in[t];
     return bf ? flat_dispatch<true>(desc, chunk_starts, nc_max, slots_dev, nslots, tabs, ws_base,
-                                    chunks, s)
+                                    chunks, claims, s)
               : flat_dispatch<false>(desc, chunk_starts, nc_max, slots_dev, nslots, tabs, ws_base,
-                                     chunks, s);
+                                     chunks, claims, s);
 }
 
 template <bool B, int C>

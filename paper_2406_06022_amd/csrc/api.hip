@@ -9,6 +9,8 @@
 
 #include "common.h"
 
+constexpr int kGatherClaimWord = 32;
+
 using namespace rgcn;
 
 namespace {
@@ -62,7 +64,8 @@ struct Layout {
     // workspace offsets
     size_t off_slots = 0, off_fwd_order = 0, off_fwd_desc = 0, off_bwd_order = 0, off_err = 0;
     size_t off_fwd_chunks = 0;
-    size_t off_flags = 0;         // schedule flags: [0] forward, [1 + t] backward of type t
+    size_t off_flags = 0;         // schedule flags: [0] forward, [1 + t] backward of type t;
+                                  // [kGatherClaimWord] the gather's work counter
     int64_t nc_max = 0;           // chunk bound of the flattened forward stream
     size_t off_csc_indptr[kMaxRels], off_csc_dst[kMaxRels];
     // combined transpose of the relations leaving grad types
@@ -194,8 +197,8 @@ rgcn_status make_layout(const rgcn_block *b, const rgcn_params *p, Layout &L) {
         int64_t nnz_total = 0;
         for (int r = 0; r < L.R; ++r)
             if (b->n_dst[b->rels[r].dst_type] > 0) nnz_total += b->rels[r].nnz;
-        if (L.n_seg + nnz_total >= kI32Max)
-            return fail(RGCN_ERR_UNSUPPORTED, "edges plus forward segments of the block exceed 2^31");
+        if (2 * L.n_seg + nnz_total >= kI32Max)
+            return fail(RGCN_ERR_UNSUPPORTED, "edges plus twice the forward segments of the block exceed 2^31");
         L.nc_max = fwd_chunk_bound(L.n_seg, nnz_total);
     }
     // backward slots
@@ -468,7 +471,8 @@ rgcn_status rgcn_block_aggregate(const rgcn_block *block, const rgcn_input *in,
         tin[t] = t < L.T ? TypeInput{in[t].base, in[t].row_ids, in[t].ld} : TypeInput{nullptr, nullptr, 0};
     TRY_HIP(gather_mean(L.dt, L.d_in, (const SegDesc *)(ws + L.off_fwd_desc), L.n_seg,
                         (const int32_t *)(ws + L.off_fwd_chunks), L.nc_max,
-                        (const FwdSlot *)(ws + L.off_slots), L.nslots, tin, ws, stream),
+                        (const FwdSlot *)(ws + L.off_slots), L.nslots, tin, ws,
+                        (uint32_t *)(ws + L.off_flags) + kGatherClaimWord, stream),
             "gather mean");
     return RGCN_OK;
 }

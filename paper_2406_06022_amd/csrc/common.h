@@ -54,7 +54,11 @@ constexpr int kMaxTypes = RGCN_MAX_TYPES;
 constexpr int kMaxRels = RGCN_MAX_RELS;
 constexpr int kMaxSlots = RGCN_MAX_TYPES + RGCN_MAX_RELS;  // forward slots: self + relations
 constexpr int kSchedBuckets = 32;                          // schedule keys 0..31
-constexpr int kFwdChunk = 64;   // entries per chunk of the flattened forward stream
+constexpr int kFwdChunk = 64;   // weight per chunk of the flattened forward stream
+#ifndef RGCN_FWD_CLAIM
+#define RGCN_FWD_CLAIM 8
+#endif
+constexpr int kFwdClaim = RGCN_FWD_CLAIM;   // chunks per run a gather group claims at a time
 
 // A forward slot: the self-loop rows of a destination type, or the rows of one relation.
 struct FwdSlot {
@@ -94,14 +98,15 @@ hipError_t exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, void *
 size_t bucket_sort_temp_bytes(int64_t n, int nbuckets);
 // Forward schedule and segment descriptors in schedule order; mcat_off[t]: byte offset of
 // Mcat_t in the workspace, mcat_ld[t]: its row length in elements, es: element size.
-// weight[p] = entries of segment p in the flattened forward stream (max(deg, 1)).  *flag
+// weight[p] = balancing weight of segment p in the flattened forward stream: the rows it
+// moves, max(deg, 1) entries read plus one written.  *flag
 // (zero on entry) ends nonzero when some segment is heavy and the schedule was sorted.
 hipError_t fwd_plan(const FwdSlot *slots_host, int nslots, int64_t n_seg, int32_t *order,
                     const int64_t *mcat_off, const int64_t *mcat_ld, int es, SegDesc *desc,
                     int32_t *weight, uint32_t *flag, void *temp, hipStream_t s);
-// Flattened forward stream split into chunks of kFwdChunk entries (segments whole): cs has
+// Flattened forward stream split into chunks of kFwdChunk weight (segments whole): cs has
 // nc_max + 2 entries, nc_max = fwd_chunk_bound(n_seg, sum of relation nnz); cs[c] = first
-// segment of chunk c, cs[nc_max + 1] = total entries.  temp: fwd_chunks_temp_bytes(n_seg);
+// segment of chunk c, cs[nc_max + 1] = total weight.  temp: fwd_chunks_temp_bytes(n_seg);
 // `weight` may lie in temp past that size.
 int64_t fwd_chunk_bound(int64_t n_seg, int64_t nnz_total);
 size_t fwd_chunks_temp_bytes(int64_t n_seg);
@@ -133,9 +138,11 @@ hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, 
 hipError_t fill_words(void *dst, const void *src_host, size_t bytes, hipStream_t s);
 
 // aggregate.hip
+// claims: one device word, the gather's shared work counter (set by the launch)
 hipError_t gather_mean(rgcn_dtype dt, int d_in, const SegDesc *desc, int64_t n_seg,
                        const int32_t *chunk_starts, int64_t nc_max, const FwdSlot *slots_dev,
-                       int nslots, const TypeInput *in, char *ws_base, hipStream_t s);
+                       int nslots, const TypeInput *in, char *ws_base, uint32_t *claims,
+                       hipStream_t s);
 
 struct TsumRel {
     const int32_t *csc_indptr;

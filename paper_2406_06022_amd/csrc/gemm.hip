@@ -48,7 +48,10 @@ struct Cfg {
 };
 using CfgWide = Cfg<256, 256, 2, 4>;
 using CfgNarrow = Cfg<128, 128, 2, 2>;
-using CfgFwd = CfgWide;     // bf16 forward (k_gemm_dl)
+#ifndef RGCN_FWD_WAVES
+#define RGCN_FWD_WAVES 16
+#endif
+using CfgFwd = typename std::conditional<RGCN_FWD_WAVES == 16, Cfg<256, 256, 4, 4>, CfgWide>::type;
 using CfgDms = CfgNarrow;   // bf16 input side: N is one or two slots of d_in columns
 using CfgDw = CfgWide;      // bf16 weight side (k_gemm_dw2)
 using CfgF32 = Cfg<128, 128, 2, 2>;

@@ -311,7 +311,8 @@ __device__ __forceinline__ int32_t desc_of(const DescArgs &a, int64_t seg, int64
     d.out_lo = (uint32_t)out;
     d.info = (uint32_t)((out >> 32) & 0xffu) | ((uint32_t)lo << 8);
     desc[p] = d;
-    weight[p] = d.deg > 0 ? d.deg : 1;
+    // balancing weight: the rows a segment moves, its entries read plus the row it writes
+    weight[p] = (d.deg > 0 ? d.deg : 1) + 1;
     return d.deg;
 }
 
@@ -346,9 +347,9 @@ __global__ __launch_bounds__(kThreads) void k_bwd_ident(BwdKey kf, int64_t n, in
 
 
 // Chunk starts of the flattened forward stream.  pre = exclusive prefix of the segment
-// weights (entries per segment).  Segment p belongs to chunk pre[p] / kFwdChunk; cs[c] is
+// weights (rows a segment moves).  Segment p belongs to chunk pre[p] / kFwdChunk; cs[c] is
 // the first segment of chunk c or later (chunks no segment starts in are empty), for
-// c <= ceil(total / kFwdChunk); cs[nc_max + 1] = total entries.
+// c <= ceil(total / kFwdChunk); cs[nc_max + 1] = total weight.
 __global__ __launch_bounds__(kThreads) void k_chunk_starts(const int32_t *pre, const int32_t *weight,
                                                            int64_t n_seg, int64_t nc_max, int32_t *cs) {
     const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -434,7 +435,7 @@ hipError_t fwd_plan(const FwdSlot *slots_host, int nslots, int64_t n_seg, int32_
 }
 
 int64_t fwd_chunk_bound(int64_t n_seg, int64_t nnz_total) {
-    return cdiv(n_seg + nnz_total, kFwdChunk);
+    return cdiv(2 * n_seg + nnz_total, kFwdChunk);
 }
 
 size_t fwd_chunks_temp_bytes(int64_t n_seg) {
