@@ -187,7 +187,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
                                                           const FwdSlot *__restrict__ slots,
                                                           int nslots, GatherTabs tabs,
                                                           char *__restrict__ ws, int chunks,
-                                                          uint32_t *claims) {
+                                                          uint32_t *claims, int claim) {
     constexpr int VEC = BF16 ? 8 : 4;
     constexpr int ES = BF16 ? 2 : 4;
     constexpr int S = G;
@@ -215,13 +215,13 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
     const int64_t gid = ((int64_t)blockIdx.x * W + wave) * GPW + lane / G;
     const int64_t total = cs[nc_max + 1];
     const int64_t nc = (total + kFwdChunk - 1) / kFwdChunk;
-    // Work is claimed in runs of kFwdClaim chunks: run gid first, then runs from the shared
+    // Work is claimed in runs of `claim` chunks: run gid first, then runs from the shared
     // counter (which starts at ngroups), each time this group's window stage reaches the
     // end of its run, so the stream continues without a pipeline restart.  Costs per row
     // differ between source tables (a row of the largest one costs more), which a static
     // split cannot know.
     auto run_of = [&](int64_t c, int32_t &lo, int32_t &hi) {
-        const int64_t a = c * kFwdClaim, b = a + kFwdClaim < nc ? a + kFwdClaim : nc;
+        const int64_t a = c * claim, b = a + claim < nc ? a + claim : nc;
         lo = a < nc ? cs[a] : 0;
         hi = a < nc ? cs[b] : 0;
         return a < nc;
@@ -316,10 +316,12 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
 
     int32_t sc = s_lo, e0 = 0;
     // after a scan: at the end of the run, continue with the next claimed run
+    // with no more runs than groups every run is taken first and nobody claims
+    const bool shared = (nc + claim - 1) / claim > ngroups;
     auto next_run = [&]() {
         const bool need = live && sc >= s_hi;
-        uint32_t c = 0;
-        if (need && lg == 0) c = atomicAdd(claims, 1u);
+        uint32_t c = (uint32_t)ngroups;   // past the last run when nothing is shared
+        if (shared && need && lg == 0) c = atomicAdd(claims, 1u);
         c = __shfl(c, gb, 64);
         if (need) {
             live = run_of(c, s_lo, s_hi);
@@ -850,15 +852,20 @@ hipError_t launch_flat_k(const SegDesc *desc, const int32_t *cs, int64_t nc_max,
     constexpr int U0 = RGCN_FLAT_ROWS / C > 0 ? RGCN_FLAT_ROWS / C : 1;
     constexpr int U = U0 < G ? U0 : G;
     const int64_t groups_per_wg = (int64_t)(kThreads / 64) * (64 / G);
-    int64_t wgs = cdiv(cdiv(nc_max, kFwdClaim), groups_per_wg);
     const int64_t cap = resident_wgs(k_gather_flat<B, G, C, U, FULL>);
+    // runs of up to kFwdClaim chunks, fewer when that would leave about three runs or less
+    // per resident group (a small block then still spreads over the grid)
+    int64_t claim = nc_max / (3 * cap * groups_per_wg);
+    claim = claim < 1 ? 1 : (claim > kFwdClaim ? kFwdClaim : claim);
+    int64_t wgs = cdiv(cdiv(nc_max, claim), groups_per_wg);
     if (wgs > cap) wgs = cap;
     if (wgs < 1) wgs = 1;
     // the shared run counter starts past the runs the groups take first
     const uint32_t first = (uint32_t)(wgs * groups_per_wg);
     RGCN_HIP_TRY(fill_words(claims, &first, 4, s));
     hipLaunchKernelGGL((k_gather_flat<B, G, C, U, FULL>), dim3((unsigned)wgs), dim3(kThreads), 0,
-                       s, desc, cs, nc_max, slots_dev, nslots, tabs, ws_base, chunks, claims);
+                       s, desc, cs, nc_max, slots_dev, nslots, tabs, ws_base, chunks, claims,
+                       (int)claim);
     return hipGetLastError();
 }
 template <bool B, int G, int C>

@@ -55,10 +55,7 @@ constexpr int kMaxRels = RGCN_MAX_RELS;
 constexpr int kMaxSlots = RGCN_MAX_TYPES + RGCN_MAX_RELS;  // forward slots: self + relations
 constexpr int kSchedBuckets = 32;                          // schedule keys 0..31
 constexpr int kFwdChunk = 64;   // weight per chunk of the flattened forward stream
-#ifndef RGCN_FWD_CLAIM
-#define RGCN_FWD_CLAIM 8
-#endif
-constexpr int kFwdClaim = RGCN_FWD_CLAIM;   // chunks per run a gather group claims at a time
+constexpr int kFwdClaim = 8;    // most chunks per run a gather group claims at a time
 
 // A forward slot: the self-loop rows of a destination type, or the rows of one relation.
 struct FwdSlot {
