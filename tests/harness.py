@@ -98,6 +98,9 @@ class BlockRun:
         self.d_ids = [i.to(dev) if i is not None else None for i in self.ids]
         self.inputs = rgcn.Inputs(self.d_tables, self.d_ids)
         self.ws = rgcn.new_workspace(self.dblk, self.params, dev)
+        # every byte the library reads before writing would show up as NaN (0xFF bytes are
+        # NaN in fp32 and bf16)
+        self.ws.fill_(0xFF)
         tdt = synth.torch_dtype(self.dtype)
         f32 = torch.float32
         flags = rgcn.RGCN_VALIDATE_DEVICE if validate else 0

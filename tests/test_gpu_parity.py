@@ -42,6 +42,35 @@ def test_random_block_parity(name, blk, dtype, d_in, d_out):
     run.assert_parity()
 
 
+def _claimed_runs_block():
+    # Large enough that the gather's runs outnumber its resident lane groups (runs are then
+    # claimed from the shared counter), with forward segments heavy enough to span several
+    # runs, so some claimed runs hold no segment start at all.
+    rng = np.random.default_rng(4242)
+    n_src, n_dst = [300_000, 60_000], [90_000, 20_000]
+    rels = []
+    for s_t, d_t, mx in ((0, 0, 24), (1, 0, 8), (0, 1, 30)):
+        nd = n_dst[d_t]
+        deg = rng.integers(0, mx + 1, size=nd)
+        heavy = rng.choice(nd, size=6, replace=False)
+        deg[heavy] = rng.integers(3000, 9000, size=6)
+        indptr = np.zeros(nd + 1, dtype=np.int64)
+        np.cumsum(deg, out=indptr[1:])
+        idx = rng.integers(0, n_src[s_t], size=int(indptr[-1]))
+        rels.append(synth.Relation(s_t, d_t, indptr.astype(np.int32), idx.astype(np.int32)))
+    return synth.Block(n_src, n_dst, rels)
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("f32", 64)])
+def test_claimed_runs_and_heavy_segments(dtype, d):
+    blk = _claimed_runs_block()
+    print(f"claimed runs {dtype} d={d}: nnz {sum(r.nnz for r in blk.rels)}", flush=True)
+    run = BlockRun(blk, dtype, d, 64, seed=31, use_ids=True)
+    run.run_gpu(repeat=2)
+    run.run_oracle()
+    run.assert_parity()
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_relu_flags_and_embedding_scatter(dtype):
     rng = np.random.default_rng(77)
