@@ -35,7 +35,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp"
         subprocess.run(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fno-fast-math",
-                        "-ffp-contract=off", _SRC, "-o", tmp], check=True)
+                        "-ffp-contract=off", _SRC, "-o", tmp, "-lm"], check=True)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
 
@@ -68,6 +68,9 @@ def _load():
                                            vp, vp, vp, vp]
         lib.orc_block_backward.restype = ctypes.c_int
         lib.orc_scatter_add.argtypes = [i64, i64, vp, vp, vp]
+        lib.orc_sparse_adagrad.argtypes = [i64, i64, i64, vp, vp, vp, vp, ctypes.c_double,
+                                           ctypes.c_double]
+        lib.orc_sparse_adagrad.restype = ctypes.c_int
         lib.orc_csc.argtypes = [i64, i64, vp, vp, vp, vp, vp]
         lib.orc_csc.restype = ctypes.c_int
         lib.orc_stable_bucket_order.argtypes = [i64, vp, i32, vp]
@@ -199,6 +202,21 @@ def scatter_add(ids: np.ndarray, dh: np.ndarray, demb: np.ndarray) -> None:
         raise IndexError("oracle: scatter id out of range")
     _load().orc_scatter_add(ids.shape[0], dh.shape[1], ids.ctypes.data, dh.ctypes.data,
                             demb.ctypes.data)
+
+
+def sparse_adagrad(rows: np.ndarray, grad: np.ndarray, state: np.ndarray, table: np.ndarray,
+                   lr: float, eps: float) -> None:
+    """Sparse Adagrad step on the listed (distinct) rows, in place on float64 C-contiguous
+    state and table; grad is table-shaped float64."""
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    grad = np.ascontiguousarray(grad, dtype=np.float64)
+    for a in (state, table):
+        assert a.dtype == np.float64 and a.flags.c_contiguous and a.shape == grad.shape
+    rc = _load().orc_sparse_adagrad(rows.shape[0], grad.shape[1], grad.shape[0],
+                                    rows.ctypes.data, grad.ctypes.data, state.ctypes.data,
+                                    table.ctypes.data, float(lr), float(eps))
+    if rc != 0:
+        raise ValueError("oracle: adagrad rows out of range or repeated")
 
 
 def csc(n_src: int, indptr, indices):

@@ -31,8 +31,10 @@
  *      dE_t[ids_t[j]] += dH_t[j]                (embedding-gradient scatter-add)
  *
  *  and the integer plan (degrees, the degree-sorted schedules, and the CSC transpose
- *  of every relation as a stable counting sort of edge positions by source row).
+ *  of every relation as a stable counting sort of edge positions by source row), and a
+ *  sparse Adagrad step on the touched rows of a learnable table.
  */
+#include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -232,6 +234,39 @@ void orc_scatter_add(int64_t n, int64_t d, const int64_t *ids, const double *dh,
     for (int64_t j = 0; j < n; ++j)
         for (int64_t c = 0; c < d; ++c)
             demb[ids[j] * d + c] += dh[j * d + c];
+}
+
+/* Sparse Adagrad step on the rows of a learnable embedding table that a mini-batch
+ * touched (Sec. 3.3.2 trains such tables; the paper does not name the optimizer, and the
+ * reading here is the row-wise Adagrad rule applied to touched rows only).  For each
+ * listed row e, with g = grad[e] (the table-shaped gradient of the scatter-add above),
+ * elementwise:
+ *     state[e] <- state[e] + g * g
+ *     table[e] <- table[e] - lr * g / (sqrt(state[e]) + eps)
+ * Rows are listed at most once (the block's source ids of a type are distinct); rows not
+ * listed are left exactly as they were.  Returns 0, or -1 for an out-of-range or repeated
+ * row. */
+int orc_sparse_adagrad(int64_t n, int64_t d, int64_t num_rows, const int64_t *rows,
+                       const double *grad, double *state, double *table, double lr, double eps)
+{
+    unsigned char *seen = (unsigned char *)calloc((size_t)num_rows + 1, 1);
+    if (!seen) return -1;
+    for (int64_t i = 0; i < n; ++i) {
+        const int64_t e = rows[i];
+        if (e < 0 || e >= num_rows || seen[e]) { free(seen); return -1; }
+        seen[e] = 1;
+    }
+    free(seen);
+    for (int64_t i = 0; i < n; ++i) {
+        const int64_t e = rows[i];
+        for (int64_t c = 0; c < d; ++c) {
+            const double g = grad[e * d + c];
+            const double s = state[e * d + c] + g * g;
+            state[e * d + c] = s;
+            table[e * d + c] = table[e * d + c] - lr * g / (sqrt(s) + eps);
+        }
+    }
+    return 0;
 }
 
 /* CSC transpose of one relation as a stable counting sort of edge positions k by

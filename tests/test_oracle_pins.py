@@ -433,3 +433,67 @@ def test_forward_schedule_heavy_first_by_hand(orc):
     blk = _B([120], [6], [_R(0, 0, indptr, indices)])
     assert orc.forward_schedule(blk).tolist() == [9, 11, 7, 10, 0, 1, 2, 3, 4, 5, 6, 8]
     assert orc.backward_schedule(blk, [0])[:3].tolist() == [0, 1, 2]  # every source: degree <= 6
+
+
+# ---------------------------------------------------------------- sparse Adagrad step
+def test_sparse_adagrad_matches_torch_adagrad_when_every_row_is_touched(orc):
+    """With every row listed, the step is torch.optim.Adagrad's dense rule (no decay, zero
+    initial accumulator): state += g^2, w -= lr g / (sqrt(state) + eps); three steps."""
+    import torch
+    rng = np.random.default_rng(3)
+    w0 = rng.standard_normal((7, 5))
+    lr, eps = 0.05, 1e-10
+    w = torch.tensor(w0.copy(), dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.Adagrad([w], lr=lr, eps=eps)
+    table, state = w0.copy(), np.zeros_like(w0)
+    for step in range(3):
+        g = rng.standard_normal(w0.shape)
+        w.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        orc.sparse_adagrad(np.arange(7), g, state, table, lr, eps)
+        np.testing.assert_allclose(table, w.detach().numpy(), rtol=1e-14, atol=1e-15)
+        np.testing.assert_allclose(state, opt.state[w]["sum"].numpy(), rtol=1e-14, atol=0)
+
+
+def test_sparse_adagrad_first_step_closed_form_and_untouched_rows(orc):
+    """From a zero state the first step is w - lr g / (|g| + eps) = w - lr sign(g) (up to
+    eps); rows not listed keep their bits; a repeated row is rejected."""
+    rng = np.random.default_rng(5)
+    table0 = rng.standard_normal((10, 4))
+    g = np.zeros_like(table0)
+    rows = np.array([7, 2, 5])
+    g[rows] = np.array([[0.5, -2.0, 4.0, -0.25], [1.0, 1.0, -1.0, 8.0], [-3.0, 0.125, 2.0, -1.0]])
+    table, state = table0.copy(), np.zeros_like(table0)
+    orc.sparse_adagrad(rows, g, state, table, 0.1, 0.0)
+    np.testing.assert_array_equal(state[rows], g[rows] ** 2)
+    np.testing.assert_allclose(table[rows], table0[rows] - 0.1 * np.sign(g[rows]), rtol=0,
+                               atol=1e-15)
+    others = np.setdiff1d(np.arange(10), rows)
+    assert np.array_equal(table[others], table0[others]) and not state[others].any()
+    with pytest.raises(ValueError):
+        orc.sparse_adagrad(np.array([1, 1]), g, state, table, 0.1, 0.0)
+
+
+def test_sparse_adagrad_on_scattered_gradient_of_a_block(orc):
+    """The fused form (update each touched row from its own dH row) equals the two-pass form
+    (scatter-add dH into a zeroed table-shaped gradient, then step the listed rows) when the
+    block's source ids are distinct."""
+    rng = np.random.default_rng(8)
+    blk = synth.random_block(rng, [40, 30], [12, 9], [(0, 1), (1, 0), (0, 0)], 6)
+    d_in, d_out = 4, 3
+    h = [rng.standard_normal((n, d_in)) for n in blk.n_src]
+    w_rel = [rng.standard_normal((d_in, d_out)) for _ in blk.rels]
+    w_self = [rng.standard_normal((d_in, d_out)) for _ in blk.n_src]
+    dy = [rng.standard_normal((n, d_out)) for n in blk.n_dst]
+    g = orc.block_backward(blk, h, w_rel, w_self, dy)
+    ids = rng.permutation(100)[: blk.n_src[0]]
+    table0, state0 = rng.standard_normal((100, d_in)), rng.random((100, d_in))
+    dE = np.zeros((100, d_in))
+    orc.scatter_add(ids, g["dh_src"][0], dE)
+    t2, s2 = table0.copy(), state0.copy()
+    orc.sparse_adagrad(ids, dE, s2, t2, 0.02, 1e-8)
+    for j, e in enumerate(ids):   # per touched row, straight from dH
+        s = state0[e] + g["dh_src"][0][j] ** 2
+        np.testing.assert_allclose(s2[e], s, rtol=1e-15)
+        np.testing.assert_allclose(t2[e], table0[e] - 0.02 * g["dh_src"][0][j] / (np.sqrt(s) + 1e-8),
+                                   rtol=1e-15)
