@@ -43,6 +43,7 @@ _COMMON_INPUTS = ["paper_2406_06022_amd/csrc/common.h", "include/rgcn.h",
 KERNEL_SOURCES = {
     "k_gather_flat": ["paper_2406_06022_amd/csrc/aggregate.hip"] + _COMMON_INPUTS,
     "k_transpose_pipe": ["paper_2406_06022_amd/csrc/aggregate.hip"] + _COMMON_INPUTS,
+    "k_transpose_pipe_adagrad": ["paper_2406_06022_amd/csrc/aggregate.hip"] + _COMMON_INPUTS,
 }
 # Plain copy of known size run after the timed steps (an fp32 negation of a 1 GiB buffer:
 # one read and one write of every byte per dispatch).  Its time gives the box's attainable
@@ -140,10 +141,11 @@ def algorithmic_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
         for t in range(T):
             tot += blk.n_dst[t] * (2 * d_in * b + ids)
         return tot
-    if stage == "sparse":
+    if stage in ("sparse", "sparse_adagrad"):
         # per requested source type: transpose offsets + destination ids + one fp32 input-
         # side row per edge, the self-loop row, and the output row (a read-add-write of
-        # the embedding-gradient row at the input layer, else a write)
+        # the embedding-gradient row at the input layer, else a write); with the fused
+        # Adagrad step the read-add-write is of the fp32 state row and the table row
         tot = 0.0
         for s in range(T):
             if not (dev_blk.grad_src_types >> s & 1):
@@ -151,6 +153,8 @@ def algorithmic_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
             ns = blk.n_src[s]
             out = 2 if layer == 0 else 1
             tot += ns * d_in * 4 * out + blk.n_dst[s] * d_in * 4 + (layer == 0) * 8 * ns
+            if stage == "sparse_adagrad":
+                tot += ns * d_in * b * 2
             for rel in blk.rels:
                 if rel.src_type == s:
                     tot += 4 * (ns + 1) + len(rel.indices) * (4 + d_in * 4)
@@ -215,6 +219,12 @@ def _short_name(name: str) -> str:
     return name[:90]
 
 
+def _kernel_re(kernel: str) -> str:
+    """Pattern of one library kernel template by its exact name (so that
+    k_transpose_pipe does not also match k_transpose_pipe_adagrad)."""
+    return r"\b" + re.escape(kernel) + "<"
+
+
 def _dispatches(path: str, kernel_re: str, value_col=None, counter=None):
     """[(dispatch id, short name, value)] of the matching kernels, in dispatch order."""
     out = []
@@ -233,8 +243,12 @@ def _dispatches(path: str, kernel_re: str, value_col=None, counter=None):
     return out
 
 
-def _by_position(rows, per_step: int, skip_steps: int):
-    rows = rows[skip_steps * per_step:]
+def _by_position(rows, per_step: int, skip_steps: int, steps: int):
+    """Average of each launch position over the first phase of the run: its first
+    skip_steps + steps steps of per_step launches, the first skip_steps skipped (the
+    training steps with the fused optimizer that follow launch the plain transposed sum
+    once fewer per step, and are left out)."""
+    rows = rows[skip_steps * per_step:(skip_steps + steps) * per_step]
     if per_step <= 0 or len(rows) % per_step:
         raise SystemExit(f"{len(rows)} dispatches are not a whole number of steps of {per_step}")
     pos = []
@@ -254,15 +268,17 @@ def summarize_trace(args) -> str:
                 if "rgcn::" in r["Kernel_Name"] else other
             a[0] += 1
             a[1] += d
-    steps = args.steps + args.warmup
+    steps = 2 * (args.steps + args.warmup)
     lines = [f"# {args.kernel}: kernel trace", "", "Command:", "", "```", args.command, "```", "",
              f"Launches of {args.kernel} by position within a step ({args.launches_per_step} "
-             f"per step, first {args.warmup} steps skipped):", ""]
+             f"per step, first {args.warmup} of {args.warmup + args.steps} steps skipped):", ""]
     for p, (avg, n, name) in enumerate(_by_position(
-            _dispatches(args.summarize_trace, args.kernel), args.launches_per_step, args.warmup)):
+            _dispatches(args.summarize_trace, _kernel_re(args.kernel)), args.launches_per_step,
+            args.warmup, args.steps)):
         lines.append(f"- avg_us_pos{p}: {avg / 1e3:.1f} ({n} launches, {name})")
     ours = sum(v[1] for v in per.values())
-    lines += ["", f"Kernels of the library over the run's {steps} steps (warmup and timed): "
+    lines += ["", f"Kernels of the library over the run's {steps} steps (warmup and timed, "
+              f"then as many training steps with the fused optimizer): "
               f"{ours / 1e6:.3f} ms, {ours / steps / 1e6:.3f} ms per step.  Other kernels "
               f"(workload set-up: sampling, tables, weights): {other[0]} launches, "
               f"{other[1] / 1e6:.3f} ms.", "",
@@ -284,10 +300,11 @@ def summarize_pmc(args) -> str:
         raise SystemExit("no calibration copy dispatches in the counter files")
     f_scale = copy_bytes / (sum(cf) / len(cf) * 1024.0)
     w_scale = copy_bytes / (sum(cw) / len(cw) * 1024.0)
-    fpos = _by_position(_dispatches(fetch_csv, args.kernel, "Counter_Value", "FETCH_SIZE"),
-                        args.launches_per_step, args.warmup)
-    wpos = _by_position(_dispatches(write_csv, args.kernel, "Counter_Value", "WRITE_SIZE"),
-                        args.launches_per_step, args.warmup)
+    kre = _kernel_re(args.kernel)
+    fpos = _by_position(_dispatches(fetch_csv, kre, "Counter_Value", "FETCH_SIZE"),
+                        args.launches_per_step, args.warmup, args.steps)
+    wpos = _by_position(_dispatches(write_csv, kre, "Counter_Value", "WRITE_SIZE"),
+                        args.launches_per_step, args.warmup, args.steps)
     lines = [f"# {args.kernel}: HBM traffic per launch", "", "Commands:", "", "```",
              args.command, "```", "",
              f"Calibration: a plain copy of {COPY_BYTES >> 20} MiB (fp32 negation, kernel "
@@ -436,6 +453,31 @@ def main() -> int:
                          f"({s_rows} rows, {s_nnz} edges, full segments), fp64 forward + "
                          f"backward (weight grads, embedding-type input grad), {s_el:.1f}s"}
 
+    # the sparse optimizer step of the learnable tables fused into block 0's transposed sum:
+    # full training steps (plan, forward, backward, table update) after the others, since
+    # they change the tables
+    stack.attach_adagrad(lr=0.01, eps=1e-10)
+    ada_ev = []
+    for k in range(args.warmup + args.steps):
+        if k == args.warmup:
+            torch.cuda.synchronize()
+            a0 = time.perf_counter()
+        ada_ev.append({})
+        events.append(ada_ev[-1])
+        stack.step(dy, timer=timer)
+    torch.cuda.synchronize()
+    ada_ms = (time.perf_counter() - a0) / args.steps * 1e3
+    ada_sp = [e[("sparse", 0)][0].elapsed_time(e[("sparse", 0)][1]) for e in ada_ev[args.warmup:]]
+    ada_sp_ms = sum(ada_sp) / len(ada_sp)
+    ada_bytes = algorithmic_bytes(spec, mb.blocks[0], stack.blocks[0], "sparse_adagrad", 0)
+    ada_gbs = ada_bytes / (ada_sp_ms * 1e-3) / 1e9
+    adagrad = {"ms_per_train_step": round(ada_ms, 4),
+               "edges_per_s": nnz / (ada_ms / 1e3),
+               "sparse[0]": {"kernel": "k_transpose_pipe_adagrad", "ms": round(ada_sp_ms, 4),
+                             "bytes": ada_bytes, "GB/s": round(ada_gbs, 1),
+                             "frac": round(ada_gbs / HBM_PEAK_GBS, 4)},
+               "lr": 0.01, "eps": 1e-10}
+
     out = {
         "metric": METRIC,
         "value": value,
@@ -463,6 +505,7 @@ def main() -> int:
         "hbm_kernels": rooflines,
         "copy_probe_GBs": round(copy_gbs, 1),
         "mfma_transforms": mfma,
+        "train_step_sparse_adagrad": adagrad,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -64,6 +64,7 @@ typedef enum { RGCN_F32 = 0, RGCN_BF16 = 1 } rgcn_dtype;
                                      gradient is multiplied elementwise by [H > 0] */
 #define RGCN_IDS_UNIQUE      0x8u /* backward: the caller asserts row_ids are distinct per
                                      type, so demb rows are updated without atomics */
+#define RGCN_CLEAR_GRAD      0x10u /* rgcn_sparse_adagrad: zero the gradient rows it read */
 
 /* One relation (canonical edge type src_type -> dst_type) of a block, as a CSR over the
  * destination rows.  indptr[0] = 0, non-decreasing, indptr[n_dst] = nnz; indices are
@@ -200,6 +201,50 @@ rgcn_status rgcn_block_backward_sparse(const rgcn_block *block, const rgcn_input
                                        float *const *demb, void *workspace,
                                        size_t workspace_bytes, unsigned flags,
                                        hipStream_t stream);
+
+/* Sparse Adagrad step of learnable embedding tables (Sec. 3.3.2: the trainable rows of a
+ * featureless node type change only where a mini-batch used them; the paper does not
+ * name the optimizer, and the rule taken here is row-wise Adagrad with no decay):
+ *   state[r] += g[r]^2  (elementwise);   table[r] -= lr * g[r] / (sqrt(state[r]) + eps)
+ * computed in fp32; a bf16 table row is rounded to nearest even after the step. */
+typedef struct {
+    float lr;
+    float eps;
+    float *const *state;   /* [host][num_types]; entry t NULL, or fp32 [in[t].num_rows x d_in]
+                              row-major (ld = d_in), updated in place */
+    void *const *table;    /* [host][num_types]; for every t with state[t]: the writable
+                              table of in[t] (must equal in[t].base), updated in place */
+} rgcn_adagrad;
+
+/* rgcn_block_backward_sparse with the optimizer step fused into the transposed sum: for
+ * every type t with opt->state[t] set, the input gradient row dH_t[j] is applied at once to
+ * table row row_ids[j] (row j when row_ids is NULL) instead of being scatter-added.  The
+ * other types behave as in rgcn_block_backward_sparse (dh_src / demb).  Requires
+ * RGCN_IDS_UNIQUE (each table row then takes exactly one step; repeated ids would race),
+ * and, for the optimised types, bit t of grad_src_types, demb[t] NULL, a 16-byte aligned
+ * state and no RGCN_INPUT_RELU (a learnable table is not a ReLU output).  dh_src[t] may
+ * still be requested and is the gradient before the step.
+ * flags: RGCN_VALIDATE_DEVICE, RGCN_IDS_UNIQUE (required). */
+rgcn_status rgcn_block_backward_sparse_adagrad(const rgcn_block *block, const rgcn_input *in,
+                                               const rgcn_params *params,
+                                               float *const *dh_src, float *const *demb,
+                                               const rgcn_adagrad *opt /* [host] */,
+                                               void *workspace, size_t workspace_bytes,
+                                               unsigned flags, hipStream_t stream);
+
+/* The same Adagrad step as a pass of its own, for gradients gathered in a table-shaped
+ * buffer first (e.g. demb from rgcn_block_backward_sparse when ids repeat).  For each of
+ * the n listed rows r = rows[i]: grad row r (fp32 [num_rows x d], ld = d) and state row r
+ * (fp32 [num_rows x d]) are read, state and table row r (dtype, [num_rows x ld]) updated in
+ * place.  rows must be distinct (repeats race: any mix of the updates may result; no
+ * fault); rows outside [0, num_rows) are skipped, never read or written.  d a multiple of
+ * 8 (bf16) or 4 (fp32), ld >= d and a multiple of the same; all arrays 16-byte aligned.
+ * flags: RGCN_CLEAR_GRAD zeroes each grad row after reading it, leaving the buffer ready
+ * for the next scatter-add without a full clear. */
+rgcn_status rgcn_sparse_adagrad(int64_t n, const int64_t *rows, int64_t num_rows, int32_t d,
+                                float *grad, float *state, void *table, int64_t ld,
+                                rgcn_dtype dtype, float lr, float eps, unsigned flags,
+                                hipStream_t stream);
 
 /* Message for the last non-OK status returned on the calling thread ("" if none). */
 const char *rgcn_last_error(void);

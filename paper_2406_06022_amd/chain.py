@@ -6,7 +6,9 @@ blocks[i].  Between layers the output goes through a ReLU (fused into the produc
 transform); the last layer has no activation.  Backward runs from the last block to the
 first: block l+1's input gradient is block l's output gradient, masked by the ReLU.  At
 the first block the featureless node types read learnable embedding tables (Sec. 3.3.2)
-and their gradient is scatter-added into table-shaped buffers.
+and their gradient is scatter-added into table-shaped buffers, or, once an Adagrad state
+is attached, applied to the tables at once (the sparse optimizer step fused into the
+first block's transposed sum).
 
 This module only allocates buffers and sequences calls of the C ABI.
 """
@@ -74,6 +76,17 @@ class MiniBatchStack:
         for t in self.emb_types:
             tab = input_tables[t]
             self.demb[t] = torch.zeros((tab.shape[0], dims[0]), dtype=f32, device=device)
+        self.adagrad = None   # (lr, eps, state per type) once attached
+
+    def attach_adagrad(self, lr: float, eps: float) -> None:
+        """Zero Adagrad state per learnable table; from now on backward steps the tables
+        in place instead of filling demb."""
+        states = [None] * len(self.demb)
+        for t in self.emb_types:
+            tab = self.inputs[0].bases[t]
+            states[t] = torch.zeros((tab.shape[0], self.dims[0]), dtype=torch.float32,
+                                    device=self.device)
+        self.adagrad = (float(lr), float(eps), states)
 
     @property
     def nnz(self) -> int:
@@ -119,9 +132,20 @@ class MiniBatchStack:
                                            self.workspaces[l], f)
             _mark(timer, ("dense", l), 1)
             _mark(timer, ("sparse", l), 0)
-            rgcn.rgcn_block_backward_sparse(self.blocks[l], self.inputs[l], self.params[l], dh,
-                                            demb, self.workspaces[l], f)
+            if l == 0 and self.adagrad is not None and self.emb_types:
+                self.sparse_adagrad_first_block(f)
+            else:
+                rgcn.rgcn_block_backward_sparse(self.blocks[l], self.inputs[l], self.params[l],
+                                                dh, demb, self.workspaces[l], f)
             _mark(timer, ("sparse", l), 1)
+
+    def sparse_adagrad_first_block(self, flags: int = 0) -> None:
+        """First block's transposed sum with the Adagrad step of the learnable tables
+        (after its dense backward stage)."""
+        lr, eps, states = self.adagrad
+        rgcn.rgcn_block_backward_sparse_adagrad(self.blocks[0], self.inputs[0], self.params[0],
+                                                states, lr, eps, workspace=self.workspaces[0],
+                                                flags=flags | rgcn.RGCN_IDS_UNIQUE)
 
     def step(self, dy_top, timer=None) -> None:
         """One pass of the whole path: plan, forward, backward."""

@@ -433,18 +433,55 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
     }
 }
 
+// Stores of one 4-column chunk `res` of source row j's input gradient (global row grow):
+// the dh_src row, then one of
+//  - Adagrad mode: the table row takes one step, state += res^2 and
+//    w -= lr res / (sqrt(state) + eps), with `old` the state and `cur` the table values
+//    read before the sum (each row belongs to one group, so no other lane touches it);
+//  - demb += res, as a read-add-write of `old` when ids are unique, else by atomics.
+template <bool BF16IN, bool OPT>
+__device__ __forceinline__ void tsum_store(const TsumArgs &a, int64_t j, int64_t grow, int c,
+                                           f32x4 res, f32x4 old, f32x4 cur) {
+    if (a.dh) *(f32x4 *)(a.dh + j * a.d_in + (int64_t)c * 4) = res;
+    if constexpr (OPT) {
+        const f32x4 st = old + res * res;
+        f32x4 w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = cur[e] - a.lr * res[e] / (sqrtf(st[e]) + a.eps);
+        *(f32x4 *)(a.opt_state + grow * a.d_in + (int64_t)c * 4) = st;
+        char *tp = (char *)a.opt_table + (grow * a.in.ld + (int64_t)c * 4) * (BF16IN ? 2 : 4);
+        if constexpr (BF16IN) {
+            typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+            *(u2 *)tp = u2{pack_bf16x2(w[0], w[1]), pack_bf16x2(w[2], w[3])};
+        } else {
+            *(f32x4 *)tp = w;
+        }
+    } else if (a.demb) {
+        float *dp = a.demb + grow * a.d_in + (int64_t)c * 4;
+        if (a.ids_unique) {
+            *(f32x4 *)dp = old + res;
+        } else {
+            unsafeAtomicAdd(dp + 0, res[0]);
+            unsafeAtomicAdd(dp + 1, res[1]);
+            unsafeAtomicAdd(dp + 2, res[2]);
+            unsafeAtomicAdd(dp + 3, res[3]);
+        }
+    }
+}
+
 // Backward, one group per source row j of one node type, in schedule order:
 //   acc = [j < n_dst] dMs_self[j] + sum over relations leaving the type, over the
 //         transpose segment of j (ascending destination row), of dMs_r[i]
 // where dMs rows already carry the 1/deg factor.  Then the optional ReLU-input mask,
-// the dh_src store and the embedding scatter-add demb[row_ids[j]] += acc.
+// the dh_src store and the embedding scatter-add demb[row_ids[j]] += acc, or (OPT) the
+// Adagrad step of table row row_ids[j] with gradient acc.
 // Lanes first fetch the transpose offsets of up to G relations at once, then the
 // destination rows of up to G edges at once (flattened relation by relation), then walk
 // the edges broadcasting row addresses, U row loads in flight; the embedding-gradient
 // row and the ReLU mask input are requested before the walk.
-template <bool BF16IN, int CPL>
-__global__ __launch_bounds__(kThreads) void k_transpose_sum(TsumArgs a, int G, int gpw,
-                                                            int chunks) {
+template <bool BF16IN, int CPL, bool OPT>
+__device__ __forceinline__ void transpose_sum_body(const TsumArgs &a, int G, int gpw,
+                                                   int chunks) {
     constexpr int HES = BF16IN ? 2 : 4;  // element size of the block input (ReLU mask)
     constexpr int U = CPL == 1 ? 8 : 4;
     const int lane = threadIdx.x & 63;
@@ -458,7 +495,8 @@ __global__ __launch_bounds__(kThreads) void k_transpose_sum(TsumArgs a, int G, i
     const int64_t j = a.order[g];
     const int64_t grow = a.in.row_ids ? a.in.row_ids[j] : j;
 
-    // early requests: embedding-gradient row (read-add-write), ReLU mask input, self term
+    // early requests: embedding-gradient row (read-add-write) or Adagrad state, ReLU mask
+    // input or the table row the step updates, self term
     float4 old[CPL];
     float hm[CPL][4];
     float acc[CPL][4];
@@ -466,10 +504,10 @@ __global__ __launch_bounds__(kThreads) void k_transpose_sum(TsumArgs a, int G, i
     for (int p = 0; p < CPL; ++p) {
         const int c = lg + p * G;
         const bool okc = c < chunks;
-        old[p] = (a.demb && a.ids_unique && okc)
-                     ? *(const float4 *)(a.demb + grow * a.d_in + (int64_t)c * 4)
-                     : make_float4(0.f, 0.f, 0.f, 0.f);
-        if (a.input_relu && okc) {
+        const float *ob = OPT ? a.opt_state : (a.ids_unique ? a.demb : nullptr);
+        old[p] = (ob && okc) ? *(const float4 *)(ob + grow * a.d_in + (int64_t)c * 4)
+                             : make_float4(0.f, 0.f, 0.f, 0.f);
+        if ((a.input_relu || OPT) && okc) {
             const char *hp = (const char *)a.in.base + (grow * a.in.ld + (int64_t)c * 4) * HES;
             if constexpr (BF16IN) {
                 const uint2 hv = *(const uint2 *)hp;
@@ -549,20 +587,9 @@ __global__ __launch_bounds__(kThreads) void k_transpose_sum(TsumArgs a, int G, i
 #pragma unroll
             for (int e = 0; e < 4; ++e) acc[p][e] = hm[p][e] > 0.f ? acc[p][e] : 0.f;
         }
-        const float4 res = make_float4(acc[p][0], acc[p][1], acc[p][2], acc[p][3]);
-        if (a.dh) *(float4 *)(a.dh + j * a.d_in + (int64_t)c * 4) = res;
-        if (a.demb) {
-            float *dp = a.demb + grow * a.d_in + (int64_t)c * 4;
-            if (a.ids_unique) {
-                *(float4 *)dp = make_float4(old[p].x + res.x, old[p].y + res.y, old[p].z + res.z,
-                                            old[p].w + res.w);
-            } else {
-                unsafeAtomicAdd(dp + 0, res.x);
-                unsafeAtomicAdd(dp + 1, res.y);
-                unsafeAtomicAdd(dp + 2, res.z);
-                unsafeAtomicAdd(dp + 3, res.w);
-            }
-        }
+        tsum_store<BF16IN, OPT>(a, j, grow, c, f32x4{acc[p][0], acc[p][1], acc[p][2], acc[p][3]},
+                           f32x4{old[p].x, old[p].y, old[p].z, old[p].w},
+                           f32x4{hm[p][0], hm[p][1], hm[p][2], hm[p][3]});
     }
 }
 
@@ -570,7 +597,8 @@ __global__ __launch_bounds__(kThreads) void k_transpose_sum(TsumArgs a, int G, i
 // (used when the relations leaving the type fit in one group, nrel <= G).  A row takes
 // four dependent steps: its schedule entry j; the global row id and, on lane r, the
 // transpose offsets of relation r; on lane e, the destination row of flattened edge e
-// (with the embedding-gradient row, the ReLU-mask input and the self term); the dMs rows.
+// (with the embedding-gradient or Adagrad-state row, the ReLU-mask input or table row, and
+// the self term); the dMs rows.
 // While the rows of one source row are in flight, the earlier steps of the next three
 // rows are too.  Edges past the group width are resolved in place.  Every load is
 // unconditional (unused lanes read a zero word).
@@ -578,9 +606,9 @@ __global__ __launch_bounds__(kThreads) void k_transpose_sum(TsumArgs a, int G, i
 #define RGCN_TSUM_U1 4
 #endif
 
-template <bool BF16IN, int CPL>
-__global__ __launch_bounds__(kThreads) void k_transpose_pipe(TsumArgs a, int G, int gpw,
-                                                             int chunks) {
+template <bool BF16IN, int CPL, bool OPT>
+__device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, int gpw,
+                                                    int chunks) {
     constexpr int HES = BF16IN ? 2 : 4;
     constexpr int U = CPL == 1 ? RGCN_TSUM_U1 : 4;
     constexpr int W = kThreads / 64;
@@ -658,13 +686,18 @@ __global__ __launch_bounds__(kThreads) void k_transpose_pipe(TsumArgs a, int G, 
         for (int p = 0; p < CPL; ++p) {
             const int c = lg + p * G;
             const bool okc = c < chunks && m.j >= 0;
-            const bool ok_old = okc && a.demb != nullptr && a.ids_unique;
-            rw.old[p] = *gbl(ok_old ? (const f32x4 *)(a.demb + m.grow * a.d_in + (int64_t)c * 4)
+            // row read before the sum: Adagrad state, or the embedding gradient when ids
+            // are unique.  (Written this way, pointer chosen here and the flag test in the
+            // predicate: forms that pick the pointer once before the loop measured 9%
+            // slower at d = 128.)
+            const bool ok_old = OPT ? okc : (okc && a.demb != nullptr && a.ids_unique);
+            const float *ob = OPT ? a.opt_state : a.demb;
+            rw.old[p] = *gbl(ok_old ? (const f32x4 *)(ob + m.grow * a.d_in + (int64_t)c * 4)
                                     : (const f32x4 *)zero);
             const bool ok_self = okc && a.self_dms != nullptr && m.j < a.n_dst;
             rw.self[p] = *gbl(ok_self ? (const f32x4 *)(a.self_dms + m.j * a.self_ld + (int64_t)c * 4)
                                       : (const f32x4 *)zero);
-            const bool ok_h = okc && a.input_relu;
+            const bool ok_h = okc && (a.input_relu || OPT);
             const char *hp = ok_h ? (const char *)a.in.base + (m.grow * a.in.ld + (int64_t)c * 4) * HES
                                   : zero;
             if constexpr (BF16IN) {
@@ -710,18 +743,7 @@ __global__ __launch_bounds__(kThreads) void k_transpose_pipe(TsumArgs a, int G, 
 #pragma unroll
                 for (int e = 0; e < 4; ++e) res[e] = rw.hm[p][e] > 0.f ? res[e] : 0.f;
             }
-            if (a.dh) *(f32x4 *)(a.dh + (int64_t)rw.m.j * a.d_in + (int64_t)c * 4) = res;
-            if (a.demb) {
-                float *dp = a.demb + rw.m.grow * a.d_in + (int64_t)c * 4;
-                if (a.ids_unique) {
-                    *(f32x4 *)dp = rw.old[p] + res;
-                } else {
-                    unsafeAtomicAdd(dp + 0, res[0]);
-                    unsafeAtomicAdd(dp + 1, res[1]);
-                    unsafeAtomicAdd(dp + 2, res[2]);
-                    unsafeAtomicAdd(dp + 3, res[3]);
-                }
-            }
+            tsum_store<BF16IN, OPT>(a, rw.m.j, rw.m.grow, c, res, rw.old[p], rw.hm[p]);
         }
     };
 
@@ -743,6 +765,29 @@ __global__ __launch_bounds__(kThreads) void k_transpose_pipe(TsumArgs a, int G, 
         mn = mnn;
         jnn = jn3;
     }
+}
+
+// The transposed sums as kernels; the Adagrad forms carry a name of their own so that
+// traces and counters keep them apart.
+template <bool BF16IN, int CPL>
+__global__ __launch_bounds__(kThreads) void k_transpose_sum(TsumArgs a, int G, int gpw,
+                                                            int chunks) {
+    transpose_sum_body<BF16IN, CPL, false>(a, G, gpw, chunks);
+}
+template <bool BF16IN, int CPL>
+__global__ __launch_bounds__(kThreads) void k_transpose_sum_adagrad(TsumArgs a, int G, int gpw,
+                                                                    int chunks) {
+    transpose_sum_body<BF16IN, CPL, true>(a, G, gpw, chunks);
+}
+template <bool BF16IN, int CPL>
+__global__ __launch_bounds__(kThreads) void k_transpose_pipe(TsumArgs a, int G, int gpw,
+                                                             int chunks) {
+    transpose_pipe_body<BF16IN, CPL, false>(a, G, gpw, chunks);
+}
+template <bool BF16IN, int CPL>
+__global__ __launch_bounds__(kThreads) void k_transpose_pipe_adagrad(TsumArgs a, int G, int gpw,
+                                                                     int chunks) {
+    transpose_pipe_body<BF16IN, CPL, true>(a, G, gpw, chunks);
 }
 
 // WcatT[n][s*d_in + c] = W_s[c][n]: the forward transform's weights, K-contiguous.
@@ -920,42 +965,48 @@ hipError_t gather_mean(rgcn_dtype dt, int d_in, const SegDesc *desc, int64_t n_s
                                      chunks, claims, s);
 }
 
-template <bool B, int C>
+template <bool B, int C, bool O>
 hipError_t launch_transpose_pipe(const TsumArgs &a, const GroupShape &gs, int chunks,
                                  hipStream_t s) {
     const int64_t groups_per_wg = (int64_t)(kThreads / 64) * gs.gpw;
     int64_t wgs = cdiv(a.n_rows, groups_per_wg);
-    const int64_t cap = resident_wgs(k_transpose_pipe<B, C>);
+    auto kern = O ? k_transpose_pipe_adagrad<B, C> : k_transpose_pipe<B, C>;
+    const int64_t cap = resident_wgs(kern);
     if (wgs > cap) wgs = cap;
-    hipLaunchKernelGGL((k_transpose_pipe<B, C>), dim3((unsigned)wgs), dim3(kThreads), 0, s, a, gs.G,
-                       gs.gpw, chunks);
+    hipLaunchKernelGGL(kern, dim3((unsigned)wgs), dim3(kThreads), 0, s, a,
+                       gs.G, gs.gpw, chunks);
     return hipGetLastError();
+}
+
+template <bool B, int C, bool O>
+hipError_t launch_transpose(const TsumArgs &a, const GroupShape &gs, int chunks, hipStream_t s) {
+    if (a.nrel <= gs.G) return launch_transpose_pipe<B, C, O>(a, gs, chunks, s);
+    const int64_t waves = cdiv(a.n_rows, gs.gpw);
+    const dim3 grid((unsigned)cdiv(waves, kThreads / 64));
+    auto kern = O ? k_transpose_sum_adagrad<B, C> : k_transpose_sum<B, C>;
+    hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, a, gs.G, gs.gpw,
+                       chunks);
+    return hipGetLastError();
+}
+
+template <bool B, bool O>
+hipError_t launch_transpose_cpl(const TsumArgs &a, const GroupShape &gs, int chunks,
+                                hipStream_t s) {
+    if (gs.cpl == 1) return launch_transpose<B, 1, O>(a, gs, chunks, s);
+    if (gs.cpl == 2) return launch_transpose<B, 2, O>(a, gs, chunks, s);
+    if (gs.cpl <= 4) return launch_transpose<B, 4, O>(a, gs, chunks, s);
+    return hipErrorInvalidValue;
 }
 
 hipError_t transpose_sum(rgcn_dtype dt, const TsumArgs &a, hipStream_t s) {
     if (a.n_rows == 0) return hipSuccess;
     const int chunks = a.d_in / 4;
     const GroupShape gs = group_shape(chunks);
-    const bool bfp = dt == RGCN_BF16;
-    if (a.nrel <= gs.G) {
-        if (gs.cpl == 1) return bfp ? launch_transpose_pipe<true, 1>(a, gs, chunks, s)
-                                    : launch_transpose_pipe<false, 1>(a, gs, chunks, s);
-        if (gs.cpl == 2) return bfp ? launch_transpose_pipe<true, 2>(a, gs, chunks, s)
-                                    : launch_transpose_pipe<false, 2>(a, gs, chunks, s);
-        if (gs.cpl <= 4) return bfp ? launch_transpose_pipe<true, 4>(a, gs, chunks, s)
-                                    : launch_transpose_pipe<false, 4>(a, gs, chunks, s);
-    }
-    const int64_t waves = cdiv(a.n_rows, gs.gpw);
-    const dim3 grid((unsigned)cdiv(waves, kThreads / 64));
-    const bool bf = dt == RGCN_BF16;
-#define RGCN_TS(B, C) \
-    hipLaunchKernelGGL((k_transpose_sum<B, C>), grid, dim3(kThreads), 0, s, a, gs.G, gs.gpw, chunks)
-    if (gs.cpl == 1) { if (bf) RGCN_TS(true, 1); else RGCN_TS(false, 1); }
-    else if (gs.cpl == 2) { if (bf) RGCN_TS(true, 2); else RGCN_TS(false, 2); }
-    else if (gs.cpl <= 4) { if (bf) RGCN_TS(true, 4); else RGCN_TS(false, 4); }
-    else return hipErrorInvalidValue;
-#undef RGCN_TS
-    return hipGetLastError();
+    const bool bf = dt == RGCN_BF16, opt = a.opt_state != nullptr;
+    if (bf) return opt ? launch_transpose_cpl<true, true>(a, gs, chunks, s)
+                       : launch_transpose_cpl<true, false>(a, gs, chunks, s);
+    return opt ? launch_transpose_cpl<false, true>(a, gs, chunks, s)
+               : launch_transpose_cpl<false, false>(a, gs, chunks, s);
 }
 
 hipError_t pack_weights(rgcn_dtype dt, int d_in, int d_out, const void *const *w_slots,

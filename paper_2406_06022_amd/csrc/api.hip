@@ -615,16 +615,49 @@ rgcn_status rgcn_block_backward_dense(const rgcn_block *block, const rgcn_params
     return RGCN_OK;
 }
 
-rgcn_status rgcn_block_backward_sparse(const rgcn_block *block, const rgcn_input *in,
-                                       const rgcn_params *params, float *const *dh_src,
-                                       float *const *demb, void *workspace,
-                                       size_t workspace_bytes, unsigned flags,
-                                       hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Checks of the Adagrad mode of the transposed sum (types with opt->state[t] set).
+rgcn_status check_adagrad(const rgcn_block *block, const rgcn_input *in, const Layout &L,
+                          float *const *demb, const rgcn_adagrad *opt, unsigned flags) {
+    if (!opt) return fail(RGCN_ERR_INVALID_ARG, "opt is NULL");
+    if (!opt->state) return fail(RGCN_ERR_INVALID_ARG, "opt->state is NULL");
+    if (!(flags & RGCN_IDS_UNIQUE))
+        return fail(RGCN_ERR_INVALID_ARG, "the fused Adagrad step requires RGCN_IDS_UNIQUE");
+    if (!(opt->lr == opt->lr) || !(opt->eps == opt->eps))
+        return fail(RGCN_ERR_INVALID_ARG, "lr or eps is NaN");
+    for (int t = 0; t < L.T; ++t) {
+        if (!opt->state[t]) continue;
+        if (!(L.grad_mask >> t & 1u))
+            return fail(RGCN_ERR_INVALID_ARG, "Adagrad on type %d but bit %d of grad_src_types "
+                        "is clear", t, t);
+        if (flags & RGCN_INPUT_RELU)
+            return fail(RGCN_ERR_INVALID_ARG, "Adagrad on type %d with RGCN_INPUT_RELU", t);
+        if (demb && demb[t])
+            return fail(RGCN_ERR_INVALID_ARG, "type %d has both demb and an Adagrad state", t);
+        if (!aligned16(opt->state[t]))
+            return fail(RGCN_ERR_INVALID_ARG, "state[%d] not 16-byte aligned", t);
+        if (!opt->table || !opt->table[t] || !in || opt->table[t] != in[t].base)
+            return fail(RGCN_ERR_INVALID_ARG, "table[%d] must be the writable base of input %d",
+                        t, t);
+        if (block->n_src[t] > 0 && (!aligned16(in[t].base) || in[t].ld < L.d_in))
+            return fail(RGCN_ERR_INVALID_ARG, "table %d misaligned or ld < d_in", t);
+    }
+    return RGCN_OK;
+}
+
+rgcn_status backward_sparse(const rgcn_block *block, const rgcn_input *in,
+                            const rgcn_params *params, float *const *dh_src, float *const *demb,
+                            const rgcn_adagrad *opt, void *workspace, size_t workspace_bytes,
+                            unsigned flags, hipStream_t stream) {
     Layout L;
     rgcn_status st = make_layout(block, params, L);
     if (st != RGCN_OK) return st;
     if ((st = check_workspace(L, workspace, workspace_bytes)) != RGCN_OK) return st;
     if ((st = check_sparse_outputs(block, in, L, dh_src, demb, flags)) != RGCN_OK) return st;
+    if (opt && (st = check_adagrad(block, in, L, demb, opt, flags)) != RGCN_OK) return st;
     char *ws = (char *)workspace;
     if ((flags & RGCN_VALIDATE_DEVICE) && in) {
         if ((st = device_validate(block, in, L, ws, stream)) != RGCN_OK) return st;
@@ -633,7 +666,8 @@ rgcn_status rgcn_block_backward_sparse(const rgcn_block *block, const rgcn_input
     for (int s = 0; s < L.T; ++s) {
         float *dh = dh_src ? dh_src[s] : nullptr;
         float *de = demb ? demb[s] : nullptr;
-        if (!dh && !de) continue;
+        float *state = opt ? opt->state[s] : nullptr;
+        if (!dh && !de && !state) continue;
         TsumArgs a;
         memset(&a, 0, sizeof(a));
         a.order = (const int32_t *)(ws + L.off_bwd_order) + L.bwd_base[s];
@@ -648,6 +682,12 @@ rgcn_status rgcn_block_backward_sparse(const rgcn_block *block, const rgcn_input
         a.ids_unique = (flags & RGCN_IDS_UNIQUE) ? 1 : 0;
         a.dh = dh;
         a.demb = de;
+        if (state) {
+            a.opt_state = state;
+            a.opt_table = opt->table[s];
+            a.lr = opt->lr;
+            a.eps = opt->eps;
+        }
         a.d_in = L.d_in;
         for (int r = 0; r < L.R; ++r) {
             const rgcn_relation &rel = block->rels[r];
@@ -662,6 +702,53 @@ rgcn_status rgcn_block_backward_sparse(const rgcn_block *block, const rgcn_input
         }
         TRY_HIP(transpose_sum(L.dt, a, stream), "transposed sum");
     }
+    return RGCN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rgcn_status rgcn_block_backward_sparse(const rgcn_block *block, const rgcn_input *in,
+                                       const rgcn_params *params, float *const *dh_src,
+                                       float *const *demb, void *workspace,
+                                       size_t workspace_bytes, unsigned flags,
+                                       hipStream_t stream) {
+    return backward_sparse(block, in, params, dh_src, demb, nullptr, workspace, workspace_bytes,
+                           flags, stream);
+}
+
+rgcn_status rgcn_block_backward_sparse_adagrad(const rgcn_block *block, const rgcn_input *in,
+                                               const rgcn_params *params,
+                                               float *const *dh_src, float *const *demb,
+                                               const rgcn_adagrad *opt, void *workspace,
+                                               size_t workspace_bytes, unsigned flags,
+                                               hipStream_t stream) {
+    if (!opt) return fail(RGCN_ERR_INVALID_ARG, "opt is NULL");
+    return backward_sparse(block, in, params, dh_src, demb, opt, workspace, workspace_bytes,
+                           flags, stream);
+}
+
+rgcn_status rgcn_sparse_adagrad(int64_t n, const int64_t *rows, int64_t num_rows, int32_t d,
+                                float *grad, float *state, void *table, int64_t ld,
+                                rgcn_dtype dtype, float lr, float eps, unsigned flags,
+                                hipStream_t stream) {
+    if (dtype != RGCN_F32 && dtype != RGCN_BF16) return fail(RGCN_ERR_DTYPE, "unknown dtype");
+    const int vec = dtype == RGCN_BF16 ? 8 : 4;
+    if (n < 0 || num_rows < 0 || d < 0) return fail(RGCN_ERR_SHAPE, "negative size");
+    if (d % vec || ld < d || ld % vec)
+        return fail(RGCN_ERR_SHAPE, "d %d and ld %lld must be multiples of %d with ld >= d", d,
+                    (long long)ld, vec);
+    if (flags & ~(unsigned)RGCN_CLEAR_GRAD)
+        return fail(RGCN_ERR_INVALID_ARG, "unsupported flags 0x%x", flags);
+    if (!(lr == lr) || !(eps == eps)) return fail(RGCN_ERR_INVALID_ARG, "lr or eps is NaN");
+    if (n == 0 || d == 0) return RGCN_OK;
+    if (!rows || !grad || !state || !table)
+        return fail(RGCN_ERR_INVALID_ARG, "rows, grad, state or table is NULL");
+    if ((uintptr_t)rows % 8 || !aligned16(grad) || !aligned16(state) || !aligned16(table))
+        return fail(RGCN_ERR_INVALID_ARG, "misaligned array");
+    TRY_HIP(sparse_adagrad(dtype, n, rows, num_rows, d, grad, d, (flags & RGCN_CLEAR_GRAD) != 0,
+                           state, table, ld, lr, eps, stream), "sparse Adagrad");
     return RGCN_OK;
 }
 

@@ -158,11 +158,18 @@ struct TsumArgs {
     int32_t ids_unique;
     float *dh;               // [n_src x d_in] or NULL
     float *demb;             // table-shaped or NULL
+    float *opt_state;        // Adagrad mode: fp32 [num_rows x d_in] squared-gradient sums, or NULL
+    void *opt_table;         // Adagrad mode: the table of `in`, updated in place
+    float lr, eps;
     int32_t d_in;
     int32_t nrel;
     TsumRel rel[kMaxRels];
 };
 hipError_t transpose_sum(rgcn_dtype dt, const TsumArgs &a, hipStream_t s);
+hipError_t sparse_adagrad(rgcn_dtype dt, int64_t n, const int64_t *rows, int64_t num_rows,
+                          int32_t d, float *grad, int64_t grad_ld, bool clear_grad,
+                          float *state, void *table, int64_t ld, float lr, float eps,
+                          hipStream_t s);
 
 hipError_t pack_weights(rgcn_dtype dt, int d_in, int d_out, const void *const *w_slots,
                         int nslots, void *wcat_t, hipStream_t s);

@@ -23,13 +23,15 @@ RGCN_VALIDATE_DEVICE = 0x1
 RGCN_FUSE_RELU = 0x2
 RGCN_INPUT_RELU = 0x4
 RGCN_IDS_UNIQUE = 0x8
+RGCN_CLEAR_GRAD = 0x10
 STATUS_NAMES = {0: "RGCN_OK", 1: "RGCN_ERR_INVALID_ARG", 2: "RGCN_ERR_SHAPE",
                 3: "RGCN_ERR_DTYPE", 4: "RGCN_ERR_INDEX_OOB", 5: "RGCN_ERR_BAD_CSR",
                 6: "RGCN_ERR_WORKSPACE_TOO_SMALL", 7: "RGCN_ERR_UNSUPPORTED", 8: "RGCN_ERR_HIP"}
 EXPORTED = ("rgcn_block_workspace_size", "rgcn_block_plan_layout", "rgcn_block_plan",
             "rgcn_block_forward", "rgcn_block_backward", "rgcn_block_aggregate",
             "rgcn_block_transform", "rgcn_block_backward_dense", "rgcn_block_backward_sparse",
-            "rgcn_last_error", "rgcn_version")
+            "rgcn_block_backward_sparse_adagrad", "rgcn_sparse_adagrad", "rgcn_last_error",
+            "rgcn_version")
 
 
 class RgcnError(RuntimeError):
@@ -60,6 +62,12 @@ class _Params(ctypes.Structure):
                 ("w_rel", ctypes.POINTER(ctypes.c_void_p)),
                 ("w_self", ctypes.POINTER(ctypes.c_void_p)),
                 ("bias", ctypes.POINTER(ctypes.c_void_p))]
+
+
+class _Adagrad(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("eps", ctypes.c_float),
+                ("state", ctypes.POINTER(ctypes.c_void_p)),
+                ("table", ctypes.POINTER(ctypes.c_void_p))]
 
 
 class _PlanLayout(ctypes.Structure):
@@ -103,6 +111,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.rgcn_block_backward_sparse.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_size_t,
                                                    ctypes.c_uint, vp]
         lib.rgcn_block_backward_sparse.restype = st
+        lib.rgcn_block_backward_sparse_adagrad.argtypes = [vp, vp, vp, vp, vp, vp, vp,
+                                                           ctypes.c_size_t, ctypes.c_uint, vp]
+        lib.rgcn_block_backward_sparse_adagrad.restype = st
+        lib.rgcn_sparse_adagrad.argtypes = [ctypes.c_int64, vp, ctypes.c_int64, ctypes.c_int32,
+                                            vp, vp, vp, ctypes.c_int64, ctypes.c_int,
+                                            ctypes.c_float, ctypes.c_float, ctypes.c_uint, vp]
+        lib.rgcn_sparse_adagrad.restype = st
         lib.rgcn_last_error.restype = ctypes.c_char_p
         lib.rgcn_version.restype = ctypes.c_char_p
         _lib = lib
@@ -304,3 +319,35 @@ def rgcn_block_backward_sparse(block: DeviceBlock, inputs: Inputs, params: Param
     _check(load_library().rgcn_block_backward_sparse(
         ctypes.byref(block.c), inputs.c, ctypes.byref(params.c), *keep, workspace.data_ptr(),
         workspace.numel(), flags, _stream(stream)))
+
+
+def rgcn_block_backward_sparse_adagrad(block: DeviceBlock, inputs: Inputs, params: Params,
+                                       state: Sequence[Optional[torch.Tensor]], lr: float,
+                                       eps: float, dh_src=None, demb=None,
+                                       workspace: torch.Tensor = None, flags: int = 0,
+                                       stream=None) -> None:
+    """Transposed sum with the Adagrad step fused in: for every type t with state[t] given,
+    the table ``inputs.bases[t]`` and ``state[t]`` are updated in place."""
+    def arr(xs):
+        return None if xs is None else _ptr_array([_ptr(t) for t in xs])
+
+    states = list(state) + [None] * (block.num_types - len(state))
+    tables = [inputs.bases[t] if states[t] is not None else None for t in range(block.num_types)]
+    st_arr, tb_arr = arr(states), arr(tables)
+    opt = _Adagrad(float(lr), float(eps), st_arr, tb_arr)
+    keep = [arr(dh_src), arr(demb)]
+    _check(load_library().rgcn_block_backward_sparse_adagrad(
+        ctypes.byref(block.c), inputs.c, ctypes.byref(params.c), *keep, ctypes.byref(opt),
+        workspace.data_ptr(), workspace.numel(), flags, _stream(stream)))
+
+
+def rgcn_sparse_adagrad(rows: torch.Tensor, grad: torch.Tensor, state: torch.Tensor,
+                        table: torch.Tensor, lr: float, eps: float, flags: int = 0,
+                        stream=None) -> None:
+    """Adagrad step of the listed rows of ``table`` (rows int64; grad and state fp32
+    [num_rows x d]; table [num_rows x ld], bf16 or fp32), all updated in place."""
+    dt = RGCN_BF16 if table.dtype == torch.bfloat16 else RGCN_F32
+    _check(load_library().rgcn_sparse_adagrad(
+        int(rows.numel()), rows.data_ptr(), int(table.shape[0]), int(grad.shape[1]),
+        grad.data_ptr(), state.data_ptr(), table.data_ptr(), int(table.stride(0)), dt,
+        float(lr), float(eps), int(flags), _stream(stream)))

@@ -84,10 +84,10 @@ class BlockRun:
         self.device = device
 
     # ------------------------------------------------------------------ GPU
-    def run_gpu(self, validate: bool = False, repeat: int = 1):
+    def device_setup(self):
+        """Device copies of the block, weights, inputs and a NaN-filled workspace."""
         dev = self.device
         blk = self.blk
-        T = len(blk.n_src)
         self.dblk = rgcn.DeviceBlock(blk, self.mask, dev)
         d_wr = [w.to(dev) for w in self.w_rel]
         d_ws = [w.to(dev) for w in self.w_self]
@@ -101,6 +101,12 @@ class BlockRun:
         # every byte the library reads before writing would show up as NaN (0xFF bytes are
         # NaN in fp32 and bf16)
         self.ws.fill_(0xFF)
+
+    def run_gpu(self, validate: bool = False, repeat: int = 1):
+        dev = self.device
+        blk = self.blk
+        T = len(blk.n_src)
+        self.device_setup()
         tdt = synth.torch_dtype(self.dtype)
         f32 = torch.float32
         flags = rgcn.RGCN_VALIDATE_DEVICE if validate else 0

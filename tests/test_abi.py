@@ -111,3 +111,54 @@ def test_null_and_small_workspace_rejected(lib):
                                  dh, None, 0x100000, n, 0, None)
     assert st == 1
     assert "grad_src_types" in lib.rgcn_last_error().decode()
+
+
+def test_sparse_adagrad_host_validation(lib):
+    """The standalone step rejects bad sizes, dtypes, flags and pointers before any launch;
+    an empty row list is a no-op."""
+    f = lib.rgcn_sparse_adagrad
+    A, B, C, D = 0x100000, 0x200000, 0x300000, 0x400000
+    good = dict(n=4, rows=A, num_rows=10, d=8, grad=B, state=C, table=D, ld=8,
+                dtype=rgcn.RGCN_F32, lr=0.1, eps=1e-8, flags=0)
+
+    def call(**kw):
+        a = dict(good, **kw)
+        return f(a["n"], a["rows"], a["num_rows"], a["d"], a["grad"], a["state"], a["table"],
+                 a["ld"], a["dtype"], a["lr"], a["eps"], a["flags"], None)
+
+    assert call(n=0) == 0
+    cases = [(dict(dtype=5), 3), (dict(d=6), 2), (dict(ld=4), 2), (dict(dtype=rgcn.RGCN_BF16, d=4, ld=8), 2),
+             (dict(dtype=rgcn.RGCN_BF16, d=8, ld=12), 2), (dict(n=-1), 2), (dict(flags=0x1), 1),
+             (dict(lr=float("nan")), 1), (dict(rows=None), 1), (dict(table=None), 1),
+             (dict(rows=A + 4), 1), (dict(state=C + 8), 1)]
+    for kw, want in cases:
+        assert call(**kw) == want, (kw, lib.rgcn_last_error())
+        assert lib.rgcn_last_error()
+
+
+def test_fused_adagrad_host_validation(lib):
+    """The fused step needs RGCN_IDS_UNIQUE, a table equal to the input base, the type's
+    gradient bit, no ReLU-input flag and no demb for the same type."""
+    blk = _FakeBlock([20], [10], [(0, 0, 30)], grad=1)
+    p = _params()
+    _, n = _ws_size(lib, blk, p)
+    inp = (rgcn._Input * 1)(rgcn._Input(0x40000, None, 20, 8))
+    f = lib.rgcn_block_backward_sparse_adagrad
+
+    def call(state=0x50000, table=0x40000, flags=rgcn.RGCN_IDS_UNIQUE, demb=None, block=blk,
+             opt=True, eps=1e-8):
+        st = (ctypes.c_void_p * 1)(state)
+        tb = (ctypes.c_void_p * 1)(table)
+        o = rgcn._Adagrad(0.1, eps, st, tb)
+        de = None if demb is None else (ctypes.c_void_p * 1)(demb)
+        return f(ctypes.byref(block.c), inp, ctypes.byref(p), None, de,
+                 ctypes.byref(o) if opt else None, 0x100000, n, flags, None)
+
+    cases = [(dict(opt=False), "opt is NULL"), (dict(flags=0), "RGCN_IDS_UNIQUE"),
+             (dict(flags=rgcn.RGCN_IDS_UNIQUE | rgcn.RGCN_INPUT_RELU), "RGCN_INPUT_RELU"),
+             (dict(table=0x60000), "writable base"), (dict(demb=0x70000), "both demb"),
+             (dict(state=0x50004), "aligned"), (dict(eps=float("nan")), "NaN"),
+             (dict(block=_FakeBlock([20], [10], [(0, 0, 30)], grad=0)), "grad_src_types")]
+    for kw, msg in cases:
+        assert call(**kw) == 1, kw
+        assert msg in lib.rgcn_last_error().decode(), (kw, lib.rgcn_last_error())
