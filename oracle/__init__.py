@@ -21,6 +21,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "rgcn_oracle.c")
+_SRC_SAMPLE = os.path.join(_HERE, "sample_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
@@ -35,7 +36,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp"
         subprocess.run(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fno-fast-math",
-                        "-ffp-contract=off", _SRC, "-o", tmp, "-lm"], check=True)
+                        "-ffp-contract=off", _SRC, _SRC_SAMPLE, "-o", tmp, "-lm"], check=True)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
 
@@ -75,6 +76,15 @@ def _load():
         lib.orc_csc.restype = ctypes.c_int
         lib.orc_stable_bucket_order.argtypes = [i64, vp, i32, vp]
         lib.orc_stable_bucket_order.restype = ctypes.c_int
+        u64 = ctypes.c_uint64
+        lib.orc_philox4x64.argtypes = [vp, vp, vp]
+        lib.orc_sample_draw.argtypes = [u64, u64, u64, u64, u64]
+        lib.orc_sample_draw.restype = u64
+        lib.orc_sample_segment.argtypes = [i64, i64, u64, i32, i64, i32, vp]
+        lib.orc_sample_segment.restype = i64
+        lib.orc_sample_block.argtypes = [i32, i32, vp, vp, vp, vp, vp, vp, vp, i64, u64, i32,
+                                         vp, vp, vp, vp]
+        lib.orc_sample_block.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -352,3 +362,77 @@ def sub_block(block, dst_rows):
                             local.astype(np.int32)))
     sub = _SubBlock([int(m.size) for m in src_map], [int(k.size) for k in keep], rels)
     return sub, src_map
+
+
+# ------------------------------------------------------------------------------------
+# Neighbour sampling and block construction (sample_oracle.c states the reading)
+# ------------------------------------------------------------------------------------
+def philox4x64(ctr, key) -> np.ndarray:
+    """The Philox4x64-10 block function: 4 counter words, 2 key words -> 4 words."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint64)
+    k = np.ascontiguousarray(key, dtype=np.uint64)
+    out = np.zeros(4, dtype=np.uint64)
+    _load().orc_philox4x64(c.ctypes.data, k.ctypes.data, out.ctypes.data)
+    return out
+
+
+def sample_draw(seed: int, layer: int, v: int, r: int, k: int) -> int:
+    return int(_load().orc_sample_draw(seed, layer, v, r, k))
+
+
+def sample_segment(n: int, fanout: int, seed: int, layer: int, v: int, r: int) -> np.ndarray:
+    """Positions (ascending) taken from a segment of n in-edges."""
+    pos = np.zeros(max(min(n, fanout), 1), dtype=np.int64)
+    c = _load().orc_sample_segment(n, fanout, seed, layer, v, r, pos.ctypes.data)
+    return pos[:c]
+
+
+class SampledBlock:
+    def __init__(self, n_src, n_dst, rels, src_ids):
+        self.n_src, self.n_dst, self.rels, self.src_ids = n_src, n_dst, rels, src_ids
+
+
+class _SRel:
+    def __init__(self, src_type, dst_type, indptr, indices):
+        self.src_type, self.dst_type, self.indptr, self.indices = src_type, dst_type, indptr, indices
+
+
+def sample_block(graph, dst_ids: Sequence[np.ndarray], fanout: int, seed: int,
+                 layer: int) -> SampledBlock:
+    """One layer's block sampled from ``graph`` (``num_nodes`` per type; ``rels`` with
+    ``src_type``, ``dst_type`` and the in-edge CSR ``indptr``/``indices``, int64 global
+    ids) for the destination nodes ``dst_ids`` (per type, distinct)."""
+    T, R = len(graph.num_nodes), len(graph.rels)
+    dst = [np.ascontiguousarray(x, dtype=np.int64) for x in dst_ids]
+    n_dst = np.array([x.shape[0] for x in dst], dtype=np.int64)
+    num_nodes = np.ascontiguousarray(graph.num_nodes, dtype=np.int64)
+    rel_src = np.array([r.src_type for r in graph.rels], dtype=np.int32)
+    rel_dst = np.array([r.dst_type for r in graph.rels], dtype=np.int32)
+    gi = [np.ascontiguousarray(r.indptr, dtype=np.int64) for r in graph.rels]
+    gx = [np.ascontiguousarray(r.indices, dtype=np.int64) for r in graph.rels]
+    out_ip = [np.zeros(n_dst[rel_dst[r]] + 1, dtype=np.int32) for r in range(R)]
+    out_ix = [np.zeros(max(int(n_dst[rel_dst[r]]) * fanout, 1), dtype=np.int32) for r in range(R)]
+    cap = [int(n_dst[t]) + sum(int(n_dst[rel_dst[r]]) * fanout for r in range(R)
+                               if rel_src[r] == t) for t in range(T)]
+    out_src = [np.zeros(max(c, 1), dtype=np.int64) for c in cap]
+    counts = np.zeros(R + T, dtype=np.int64)
+
+    def parr(xs):
+        a = (ctypes.c_void_p * max(len(xs), 1))()
+        for i, x in enumerate(xs):
+            a[i] = x.ctypes.data
+        return a
+
+    rc = _load().orc_sample_block(T, R, rel_src.ctypes.data, rel_dst.ctypes.data, parr(gi),
+                                  parr(gx), num_nodes.ctypes.data, parr(dst),
+                                  n_dst.ctypes.data, fanout, seed, layer, parr(out_ip),
+                                  parr(out_ix), parr(out_src), counts.ctypes.data)
+    if rc == -1:
+        raise ValueError("destination id out of range")
+    if rc == -2:
+        raise ValueError("repeated destination ids")
+    rels = [_SRel(int(rel_src[r]), int(rel_dst[r]), out_ip[r], out_ix[r][:counts[r]])
+            for r in range(R)]
+    src_ids = [out_src[t][:counts[R + t]] for t in range(T)]
+    return SampledBlock([int(x.shape[0]) for x in src_ids], [int(x) for x in n_dst], rels,
+                        src_ids)

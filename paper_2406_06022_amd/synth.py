@@ -350,6 +350,72 @@ def random_block(rng: np.random.Generator, n_src: Sequence[int], n_dst: Sequence
 
 
 # --------------------------------------------------------------------------------------
+# Full graphs to sample from (in-edge CSR per relation, global ids)
+# --------------------------------------------------------------------------------------
+@dataclasses.dataclass
+class GraphRel:
+    src_type: int
+    dst_type: int
+    indptr: object    # int64 [num_nodes[dst_type] + 1] (numpy array or torch tensor)
+    indices: object   # int64 [nnz] global source ids of type src_type
+
+
+@dataclasses.dataclass
+class Graph:
+    num_nodes: List[int]
+    rels: List[GraphRel]
+
+    @property
+    def nnz(self) -> int:
+        return sum(int(r.indices.shape[0]) for r in self.rels)
+
+
+def random_graph(rng: np.random.Generator, num_nodes: Sequence[int],
+                 rels: Sequence[Tuple[int, int]], mean_deg: float, heavy: int = 0,
+                 heavy_deg: int = 0) -> Graph:
+    """A small full graph for tests: in-degrees Poisson(mean_deg) (zeros included), plus
+    ``heavy`` destination nodes per relation with ``heavy_deg`` in-edges; sources uniform
+    (repeats allowed, as in a multigraph)."""
+    out = []
+    for (s, t) in rels:
+        n = int(num_nodes[t])
+        deg = rng.poisson(mean_deg, size=n).astype(np.int64)
+        if heavy and n:
+            deg[rng.choice(n, size=min(heavy, n), replace=False)] = heavy_deg
+        if num_nodes[s] == 0:
+            deg[:] = 0
+        indptr = np.zeros(n + 1, dtype=np.int64)
+        np.cumsum(deg, out=indptr[1:])
+        idx = rng.integers(0, max(int(num_nodes[s]), 1), size=int(indptr[-1]), dtype=np.int64)
+        out.append(GraphRel(s, t, indptr, idx))
+    return Graph([int(x) for x in num_nodes], out)
+
+
+def device_graph(spec: WorkloadSpec, mean_deg: float = 5.0, max_deg: int = 100_000,
+                 device="cuda", node_scale: float = 1.0) -> Graph:
+    """The full graph behind a workload's mini-batches, drawn on ``device``: node counts of
+    the spec's types (times ``node_scale``), and per relation in-degrees
+    floor(Pareto(alpha = 2, x_m = (mean_deg + 0.5) / 2)) (mean about ``mean_deg``, power-law
+    tail, capped at ``max_deg``), sources uniform over the source type.  Seeded by the
+    spec."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(spec.seed * 31 + 7)
+    nodes = [max(1, int(round(n * node_scale))) for n in spec.type_rows]
+    out = []
+    for (s, t) in spec.rels:
+        n = nodes[t]
+        u = torch.rand(n, generator=gen, device=device, dtype=torch.float64)
+        deg = torch.floor(((mean_deg + 0.5) / 2.0) / torch.sqrt(1.0 - u)).clamp_(max=max_deg)
+        indptr = torch.zeros(n + 1, dtype=torch.int64, device=device)
+        torch.cumsum(deg.to(torch.int64), 0, out=indptr[1:])
+        nnz = int(indptr[-1])
+        idx = torch.randint(0, nodes[s], (nnz,), generator=gen, device=device, dtype=torch.int64)
+        out.append(GraphRel(s, t, indptr, idx))
+    return Graph(nodes, out)
+
+
+# --------------------------------------------------------------------------------------
 # Values
 # --------------------------------------------------------------------------------------
 def torch_dtype(name: str):
