@@ -289,6 +289,29 @@ def summarize_trace(args) -> str:
     return "\n".join(lines) + "\n"
 
 
+def summarize_kernels(args) -> str:
+    """Calls, total and average time of the kernels matching a pattern in a rocprofv3
+    kernel_stats.csv, totals also divided by --per repetitions."""
+    path, pat = args.summarize_kernels
+    rows = []
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            if re.search(pat, r["Name"]):
+                rows.append((_short_name(r["Name"]), int(r["Calls"]),
+                             float(r["TotalDurationNs"]), float(r["AverageNs"])))
+    rows.sort(key=lambda x: -x[2])
+    tot = sum(x[2] for x in rows)
+    lines = [f"# kernels matching `{pat}`", "", "Command:", "", "```", args.command, "```", "",
+             f"Total {tot / 1e6:.3f} ms, {tot / args.per / 1e6:.3f} ms per repetition "
+             f"({args.per} repetitions).", "",
+             "| kernel | calls | total ms | avg us | ms per repetition |",
+             "|---|---:|---:|---:|---:|"]
+    for name, n, t, a in rows:
+        lines.append(f"| `{name}` | {n} | {t / 1e6:.3f} | {a / 1e3:.1f} | "
+                     f"{t / args.per / 1e6:.3f} |")
+    return "\n".join(lines) + "\n"
+
+
 def summarize_pmc(args) -> str:
     """Per-launch HBM traffic of --kernel from FETCH_SIZE and WRITE_SIZE runs, each scaled
     by what the same counter reads for the plain copy of --copy-probe-mib MiB."""
@@ -322,6 +345,92 @@ def summarize_pmc(args) -> str:
     return "\n".join(lines) + "\n"
 
 
+def measure_sampling(spec, dev, args):
+    """On-device mini-batch sampling from the workload's full graph: each mini-batch is
+    the three layers top-down from 4,096 seeds (host reads of the counts between layers
+    included), timed over several mini-batches with distinct random streams; the oracle
+    samples the seed-adjacent layer on the host for a CPU rate."""
+    import numpy as np
+    import torch
+
+    from paper_2406_06022_amd import rgcn, sampler, synth
+
+    t0 = time.perf_counter()
+    g = synth.device_graph(spec, device=dev)
+    dg = rgcn.DeviceGraph(g)
+    torch.cuda.synchronize()
+    log(f"full graph: nodes {g.num_nodes}, {g.nnz} edges in {time.perf_counter() - t0:.1f}s")
+    gen = torch.Generator(device="cpu").manual_seed(spec.seed + 5)
+    T = len(g.num_nodes)
+    seeds = [torch.zeros(0, dtype=torch.int64, device=dev) for _ in range(T)]
+    for t in spec.seed_types:
+        seeds[t] = torch.randperm(g.num_nodes[t], generator=gen)[: spec.n_seeds].to(dev)
+    runs, edges, per_layer = [], [], []
+    n_batches = 10
+    for k in range(2 + n_batches):
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        blocks, _ = sampler.sample_minibatch(dg, seeds, spec.fanouts, seed=1000 + k)
+        torch.cuda.synchronize()
+        b = time.perf_counter()
+        if k >= 2:
+            runs.append((b - a) * 1e3)
+            edges.append(sum(x.nnz for x in blocks))
+            per_layer.append([x.nnz for x in blocks])
+    ms = sum(runs) / len(runs)
+    ne = sum(edges) / len(edges)
+    out = {"graph": {"num_nodes": g.num_nodes, "edges": g.nnz,
+                     "in_degree": "floor(Pareto(2, x_m = 2.75)), mean ~5 per relation, cap 1e5"},
+           "seeds": spec.n_seeds, "fanouts": list(spec.fanouts),
+           "ms_per_minibatch": round(ms, 3), "sampled_edges_per_minibatch": int(ne),
+           "sampled_edges_per_layer": per_layer[0],
+           "edges_per_s": ne / (ms * 1e-3), "minibatches": n_batches}
+    if args.cpu_budget > 0:
+        import oracle
+
+        # host copy of the relations into the seed type (all the seed-adjacent layer reads)
+        class _G:
+            pass
+        hg = _G()
+        hg.num_nodes = g.num_nodes
+        hg.rels = []
+        seed_t = spec.seed_types[0]
+        for r, (s_t, d_t) in enumerate(spec.rels):
+            x = _G()
+            x.src_type, x.dst_type = s_t, d_t
+            if d_t == seed_t:
+                x.indptr = g.rels[r].indptr.cpu().numpy()
+                x.indices = g.rels[r].indices.cpu().numpy()
+            else:
+                x.indptr = np.zeros(g.num_nodes[d_t] + 1, dtype=np.int64)
+                x.indices = np.zeros(1, dtype=np.int64)
+            hg.rels.append(x)
+        host_seeds = [x.cpu().numpy() for x in seeds]
+        c0 = time.perf_counter()
+        n_cpu, e_cpu = 0, 0
+        while time.perf_counter() - c0 < min(args.cpu_budget, 10.0) or n_cpu == 0:
+            blk = oracle.sample_block(hg, host_seeds, spec.fanouts[-1], 1000 + n_cpu,
+                                      len(spec.fanouts) - 1)
+            e_cpu += sum(int(r.indices.shape[0]) for r in blk.rels)
+            n_cpu += 1
+        el = time.perf_counter() - c0
+        out["cpu_baseline"] = {"value": e_cpu / el, "unit": "sampled edges/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"{n_cpu} seed-adjacent blocks ({spec.n_seeds} seeds, "
+                                         f"fanout {spec.fanouts[-1]}, {e_cpu} edges), {el:.1f}s"}
+        # the GPU rate of the same seed-adjacent layer
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        for k in range(20):
+            ip, ix, src, counts = rgcn.rgcn_sample_block(dg, seeds, spec.fanouts[-1], 2000 + k,
+                                                         len(spec.fanouts) - 1)
+        torch.cuda.synchronize()
+        out["seed_layer_gpu_ms"] = round((time.perf_counter() - a) * 1e3 / 20, 4)
+    del dg, g
+    torch.cuda.empty_cache()
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -335,6 +444,14 @@ def main() -> int:
                          "WRITE_SIZE) into the per-launch HBM traffic summary and exit")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="reduce a rocprofv3 kernel_trace.csv into a per-kernel summary and exit")
+    ap.add_argument("--summarize-kernels", nargs=2, metavar=("KERNEL_STATS_CSV", "REGEX"),
+                    help="reduce a rocprofv3 kernel_stats.csv to the kernels matching REGEX "
+                         "and exit")
+    ap.add_argument("--per", type=int, default=1,
+                    help="with --summarize-kernels: divide totals by this many repetitions")
+    ap.add_argument("--sampling-only", action="store_true",
+                    help="run only the on-device mini-batch sampling measurement (12 "
+                         "mini-batches of the workload) and print its JSON object")
     ap.add_argument("--kernel", default="k_gather_flat")
     ap.add_argument("--launches-per-step", type=int, default=3,
                     help="launches of --kernel per step (summaries split them by position)")
@@ -345,6 +462,9 @@ def main() -> int:
         return 0
     if args.summarize_trace:
         print(summarize_trace(args), end="")
+        return 0
+    if args.summarize_kernels:
+        print(summarize_kernels(args), end="")
         return 0
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for --gpus {args.gpus}); the multi-GPU "
@@ -357,6 +477,10 @@ def main() -> int:
     dev = "cuda:0"
     torch.cuda.set_device(0)
     rgcn.load_library()
+    if args.sampling_only:
+        from paper_2406_06022_amd import synth
+        print(json.dumps(measure_sampling(synth.config(args.config), dev, args)), flush=True)
+        return 0
     spec, mb, tables, ids, weights, stack, dy = build_stack(args.config, dev)
     log(f"workspace bytes per block {[int(w.numel()) for w in stack.workspaces]}")
 
@@ -478,6 +602,8 @@ def main() -> int:
                              "frac": round(ada_gbs / HBM_PEAK_GBS, 4)},
                "lr": 0.01, "eps": 1e-10}
 
+    sampling = measure_sampling(spec, dev, args)
+
     out = {
         "metric": METRIC,
         "value": value,
@@ -506,6 +632,7 @@ def main() -> int:
         "copy_probe_GBs": round(copy_gbs, 1),
         "mfma_transforms": mfma,
         "train_step_sparse_adagrad": adagrad,
+        "sampling": sampling,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

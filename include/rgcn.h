@@ -246,6 +246,66 @@ rgcn_status rgcn_sparse_adagrad(int64_t n, const int64_t *rows, int64_t num_rows
                                 rgcn_dtype dtype, float lr, float eps, unsigned flags,
                                 hipStream_t stream);
 
+/* ---------------------------------------------------------------- neighbour sampling
+ * One layer of on-the-fly mini-batch sampling (Sec. 3.1.1 and 3.1.4: neighbourhoods are
+ * sampled per mini-batch with a fanout per layer, one block per GNN layer, top-down from
+ * the seeds).  The paper leaves the sampler unspecified; the rule implemented:
+ *  - for each destination node v of type dst(r) and each relation r: every in-edge of v
+ *    in r when its in-degree is at most `fanout`, else `fanout` distinct in-edges, each
+ *    subset equally likely (Floyd's algorithm), listed in the graph's CSR order;
+ *  - draw k of (v, r) is word k mod 4 of Philox4x64-10 at counter (v, r, k/4, 0) and key
+ *    (seed, layer); a uniform integer in [0, m) is the high word of draw * m (results
+ *    are a function of the inputs, bit for bit);
+ *  - the block's source nodes of type t are its destination nodes (in the given order),
+ *    then the sampled sources in order of first appearance (relations in order,
+ *    destination rows in order, edges in order); indices are those block-local rows.
+ * The output is a block in the form rgcn_block expects (its source ids are the next
+ * layer's destination ids, and at the input layer the row ids of the tables). */
+typedef struct {
+    int32_t src_type;
+    int32_t dst_type;
+    const int64_t *indptr;    /* [num_nodes[dst_type] + 1] in-edge CSR offsets */
+    const int64_t *indices;   /* [indptr[num_nodes[dst_type]]] global source ids */
+} rgcn_graph_relation;
+
+typedef struct {
+    int32_t num_types;                /* 1 .. RGCN_MAX_TYPES */
+    int32_t num_rels;                 /* 0 .. RGCN_MAX_RELS */
+    const int64_t *num_nodes;         /* [host][num_types], each below 2^59 */
+    const rgcn_graph_relation *rels;  /* [host][num_rels] */
+} rgcn_graph;
+
+#define RGCN_MAX_FANOUT 64
+
+/* Workspace bytes for rgcn_sample_block with these destination counts (host only). */
+rgcn_status rgcn_sample_workspace_size(const rgcn_graph *graph,
+                                       const int64_t *n_dst /* [host][num_types] */,
+                                       int32_t fanout, size_t *bytes /* [host] */);
+
+/* Sample one layer's block for the destination nodes dst_ids[t] (device int64 [n_dst[t]],
+ * distinct per type).  fanout in [1, RGCN_MAX_FANOUT].  Outputs (device, caller-owned,
+ * overwritten):
+ *   out_indptr[r]:  int32 [n_dst[dst(r)] + 1]
+ *   out_indices[r]: int32, capacity n_dst[dst(r)] * fanout (block-local source rows)
+ *   out_src_ids[t]: int64, capacity n_dst[t] + sum over r with src(r) = t of
+ *                   n_dst[dst(r)] * fanout (global ids of the block's source nodes)
+ *   counts:         int64 [num_rels + num_types]: sampled edges per relation, then source
+ *                   nodes per type (read it after the stream completes to size the block)
+ * Entries for relations or types whose capacity is zero may be NULL.  Capacities must
+ * stay below 2^31 in total (RGCN_ERR_UNSUPPORTED otherwise).  Invalid device data (an id
+ * out of range, repeated destination ids, an in-degree of 2^32 or more) is never read
+ * out of bounds; it leaves the outputs unspecified and is reported only with
+ * RGCN_VALIDATE_DEVICE, which synchronises after the work: RGCN_ERR_INDEX_OOB (an id out
+ * of range), RGCN_ERR_INVALID_ARG (repeated destination ids), RGCN_ERR_UNSUPPORTED
+ * (degree).  flags: RGCN_VALIDATE_DEVICE. */
+rgcn_status rgcn_sample_block(const rgcn_graph *graph, const int64_t *const *dst_ids /* [host] */,
+                              const int64_t *n_dst /* [host] */, int32_t fanout, uint64_t seed,
+                              int32_t layer, int32_t *const *out_indptr /* [host] */,
+                              int32_t *const *out_indices /* [host] */,
+                              int64_t *const *out_src_ids /* [host] */, int64_t *counts,
+                              void *workspace, size_t workspace_bytes, unsigned flags,
+                              hipStream_t stream);
+
 /* Message for the last non-OK status returned on the calling thread ("" if none). */
 const char *rgcn_last_error(void);
 

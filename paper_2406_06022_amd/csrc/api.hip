@@ -778,3 +778,117 @@ rgcn_status rgcn_block_backward(const rgcn_block *block, const rgcn_input *in,
 }
 
 }  // extern "C"
+
+namespace {
+
+rgcn_status sample_tab(const rgcn_graph *g, const int64_t *n_dst, int32_t fanout,
+                       SampleTab &T, SampleLayout &L) {
+    if (!g || !n_dst) return fail(RGCN_ERR_INVALID_ARG, "graph or n_dst is NULL");
+    if (g->num_types < 1 || g->num_types > kMaxTypes)
+        return fail(RGCN_ERR_INVALID_ARG, "num_types %d outside [1, %d]", g->num_types, kMaxTypes);
+    if (g->num_rels < 0 || g->num_rels > kMaxRels)
+        return fail(RGCN_ERR_INVALID_ARG, "num_rels %d outside [0, %d]", g->num_rels, kMaxRels);
+    if (!g->num_nodes || (g->num_rels > 0 && !g->rels))
+        return fail(RGCN_ERR_INVALID_ARG, "num_nodes or rels is NULL");
+    if (fanout < 1 || fanout > kMaxFanout)
+        return fail(RGCN_ERR_UNSUPPORTED, "fanout %d outside [1, %d]", fanout, kMaxFanout);
+    memset(&T, 0, sizeof(T));
+    T.ntypes = g->num_types;
+    T.nrel = g->num_rels;
+    T.fanout = fanout;
+    for (int t = 0; t < T.ntypes; ++t) {
+        if (g->num_nodes[t] < 0 || g->num_nodes[t] >= (int64_t)1 << 59)
+            return fail(RGCN_ERR_SHAPE, "num_nodes[%d] outside [0, 2^59)", t);
+        if (n_dst[t] < 0) return fail(RGCN_ERR_SHAPE, "n_dst[%d] negative", t);
+        T.num_nodes[t] = g->num_nodes[t];
+        T.n_dst[t] = n_dst[t];
+    }
+    for (int r = 0; r < T.nrel; ++r) {
+        const rgcn_graph_relation &rel = g->rels[r];
+        if (rel.src_type < 0 || rel.src_type >= T.ntypes || rel.dst_type < 0 ||
+            rel.dst_type >= T.ntypes)
+            return fail(RGCN_ERR_INVALID_ARG, "relation %d: bad node type", r);
+        if (!rel.indptr || !rel.indices || ((uintptr_t)rel.indptr | (uintptr_t)rel.indices) & 7u)
+            return fail(RGCN_ERR_INVALID_ARG, "relation %d: indptr/indices NULL or misaligned", r);
+        T.src_type[r] = rel.src_type;
+        T.dst_type[r] = rel.dst_type;
+        T.g_indptr[r] = rel.indptr;
+        T.g_indices[r] = rel.indices;
+    }
+    if (!sample_layout(T, L))
+        return fail(RGCN_ERR_UNSUPPORTED, "sampling capacity %lld exceeds 2^31",
+                    (long long)T.cap_total);
+    return RGCN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rgcn_status rgcn_sample_workspace_size(const rgcn_graph *graph, const int64_t *n_dst,
+                                       int32_t fanout, size_t *bytes) {
+    if (!bytes) return fail(RGCN_ERR_INVALID_ARG, "bytes is NULL");
+    SampleTab T;
+    SampleLayout L;
+    rgcn_status st = sample_tab(graph, n_dst, fanout, T, L);
+    if (st != RGCN_OK) return st;
+    *bytes = L.total;
+    return RGCN_OK;
+}
+
+rgcn_status rgcn_sample_block(const rgcn_graph *graph, const int64_t *const *dst_ids,
+                              const int64_t *n_dst, int32_t fanout, uint64_t seed,
+                              int32_t layer, int32_t *const *out_indptr,
+                              int32_t *const *out_indices, int64_t *const *out_src_ids,
+                              int64_t *counts, void *workspace, size_t workspace_bytes,
+                              unsigned flags, hipStream_t stream) {
+    SampleTab T;
+    SampleLayout L;
+    rgcn_status st = sample_tab(graph, n_dst, fanout, T, L);
+    if (st != RGCN_OK) return st;
+    if (flags & ~(unsigned)RGCN_VALIDATE_DEVICE)
+        return fail(RGCN_ERR_INVALID_ARG, "unsupported flags 0x%x", flags);
+    if (!workspace || ((uintptr_t)workspace & 255u))
+        return fail(RGCN_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
+    if (workspace_bytes < L.total)
+        return fail(RGCN_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu",
+                    workspace_bytes, L.total);
+    if (!counts || ((uintptr_t)counts & 7u))
+        return fail(RGCN_ERR_INVALID_ARG, "counts NULL or misaligned");
+    if (!dst_ids || !out_indptr || !out_indices || !out_src_ids)
+        return fail(RGCN_ERR_INVALID_ARG, "an array argument is NULL");
+    T.seed = seed;
+    T.layer = layer;
+    for (int t = 0; t < T.ntypes; ++t) {
+        if (T.n_dst[t] > 0 && (!dst_ids[t] || ((uintptr_t)dst_ids[t] & 7u)))
+            return fail(RGCN_ERR_INVALID_ARG, "dst_ids[%d] NULL or misaligned", t);
+        if (T.type_cap[t] > 0 && (!out_src_ids[t] || ((uintptr_t)out_src_ids[t] & 7u)))
+            return fail(RGCN_ERR_INVALID_ARG, "out_src_ids[%d] NULL or misaligned", t);
+        T.dst_ids[t] = dst_ids[t];
+        T.out_src_ids[t] = out_src_ids[t];
+    }
+    for (int r = 0; r < T.nrel; ++r) {
+        const int64_t cap = T.n_dst[T.dst_type[r]] * (int64_t)fanout;
+        if (!out_indptr[r] || ((uintptr_t)out_indptr[r] & 3u))
+            return fail(RGCN_ERR_INVALID_ARG, "out_indptr[%d] NULL or misaligned", r);
+        if (cap > 0 && (!out_indices[r] || ((uintptr_t)out_indices[r] & 3u)))
+            return fail(RGCN_ERR_INVALID_ARG, "out_indices[%d] NULL or misaligned", r);
+        T.out_indptr[r] = out_indptr[r];
+        T.out_indices[r] = out_indices[r];
+    }
+    char *ws = (char *)workspace;
+    TRY_HIP(sample_block(T, L, ws, counts, stream), "sampling");
+    if (flags & RGCN_VALIDATE_DEVICE) {
+        uint32_t host = 0;
+        TRY_HIP(hipMemcpyAsync(&host, ws + L.off_err, 4, hipMemcpyDeviceToHost, stream),
+                "validate copy");
+        TRY_HIP(hipStreamSynchronize(stream), "validate sync");
+        if (host & 1u) return fail(RGCN_ERR_INDEX_OOB, "a destination id is out of range");
+        if (host & 8u) return fail(RGCN_ERR_INDEX_OOB, "a graph source id is out of range");
+        if (host & 2u) return fail(RGCN_ERR_INVALID_ARG, "repeated destination ids");
+        if (host & 4u) return fail(RGCN_ERR_UNSUPPORTED, "an in-degree of 2^32 or more");
+    }
+    return RGCN_OK;
+}
+
+}  // extern "C"

@@ -171,6 +171,36 @@ hipError_t sparse_adagrad(rgcn_dtype dt, int64_t n, const int64_t *rows, int64_t
                           float *state, void *table, int64_t ld, float lr, float eps,
                           hipStream_t s);
 
+// sample.hip: one layer's neighbour sampling and block construction (tables in the
+// workspace; see the file for the method)
+constexpr int kMaxFanout = 64;
+struct SampleTab {
+    int32_t ntypes, nrel, fanout, layer;
+    uint64_t seed;
+    int64_t n_seg, cap_total;
+    int64_t num_nodes[kMaxTypes], n_dst[kMaxTypes], type_base[kMaxTypes], type_cap[kMaxTypes];
+    int64_t node_base[kMaxTypes];   // prefix of num_nodes (the per-node first-position words)
+    const int64_t *dst_ids[kMaxTypes];
+    int64_t *out_src_ids[kMaxTypes];
+    int32_t src_type[kMaxRels], dst_type[kMaxRels];
+    int64_t seg_base[kMaxRels], cand_base[kMaxRels];
+    const int64_t *g_indptr[kMaxRels];
+    const int64_t *g_indices[kMaxRels];
+    int32_t *out_indptr[kMaxRels];
+    int32_t *out_indices[kMaxRels];
+};
+struct SampleLayout {
+    size_t off_err, off_tab, off_seg, off_scan, off_cand, off_flag, off_first, total;
+    int64_t nodes;
+};
+// Fills the derived fields of T (segments, candidate regions) and the workspace layout;
+// false when positions would not fit int32.
+bool sample_layout(SampleTab &T, SampleLayout &L);
+// Error word bits (at ws + L.off_err): 1 destination id out of range, 2 repeated
+// destination ids, 4 in-degree of 2^32 or more, 8 graph source id out of range.
+hipError_t sample_block(const SampleTab &T, const SampleLayout &L, char *ws, int64_t *counts,
+                        hipStream_t s);
+
 hipError_t pack_weights(rgcn_dtype dt, int d_in, int d_out, const void *const *w_slots,
                         int nslots, void *wcat_t, hipStream_t s);
 hipError_t column_sums(const float *dy, int64_t rows, int cols, float *out, float *partial,

@@ -30,8 +30,10 @@ STATUS_NAMES = {0: "RGCN_OK", 1: "RGCN_ERR_INVALID_ARG", 2: "RGCN_ERR_SHAPE",
 EXPORTED = ("rgcn_block_workspace_size", "rgcn_block_plan_layout", "rgcn_block_plan",
             "rgcn_block_forward", "rgcn_block_backward", "rgcn_block_aggregate",
             "rgcn_block_transform", "rgcn_block_backward_dense", "rgcn_block_backward_sparse",
-            "rgcn_block_backward_sparse_adagrad", "rgcn_sparse_adagrad", "rgcn_last_error",
+            "rgcn_block_backward_sparse_adagrad", "rgcn_sparse_adagrad",
+            "rgcn_sample_workspace_size", "rgcn_sample_block", "rgcn_last_error",
             "rgcn_version")
+RGCN_MAX_FANOUT = 64
 
 
 class RgcnError(RuntimeError):
@@ -68,6 +70,16 @@ class _Adagrad(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("eps", ctypes.c_float),
                 ("state", ctypes.POINTER(ctypes.c_void_p)),
                 ("table", ctypes.POINTER(ctypes.c_void_p))]
+
+
+class _GraphRel(ctypes.Structure):
+    _fields_ = [("src_type", ctypes.c_int32), ("dst_type", ctypes.c_int32),
+                ("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p)]
+
+
+class _Graph(ctypes.Structure):
+    _fields_ = [("num_types", ctypes.c_int32), ("num_rels", ctypes.c_int32),
+                ("num_nodes", ctypes.POINTER(ctypes.c_int64)), ("rels", ctypes.POINTER(_GraphRel))]
 
 
 class _PlanLayout(ctypes.Structure):
@@ -118,6 +130,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                             vp, vp, vp, ctypes.c_int64, ctypes.c_int,
                                             ctypes.c_float, ctypes.c_float, ctypes.c_uint, vp]
         lib.rgcn_sparse_adagrad.restype = st
+        lib.rgcn_sample_workspace_size.argtypes = [vp, vp, ctypes.c_int32, vp]
+        lib.rgcn_sample_workspace_size.restype = st
+        lib.rgcn_sample_block.argtypes = [vp, vp, vp, ctypes.c_int32, ctypes.c_uint64,
+                                          ctypes.c_int32, vp, vp, vp, vp, vp, ctypes.c_size_t,
+                                          ctypes.c_uint, vp]
+        lib.rgcn_sample_block.restype = st
         lib.rgcn_last_error.restype = ctypes.c_char_p
         lib.rgcn_version.restype = ctypes.c_char_p
         _lib = lib
@@ -184,6 +202,54 @@ class DeviceBlock:
     @property
     def nnz(self) -> int:
         return sum(x[2] for x in self.types)
+
+
+class DeviceBlockView(DeviceBlock):
+    """A block whose CSR arrays are already device tensors (e.g. from rgcn_sample_block):
+    rels = [(src_type, dst_type, indptr int32, indices int32)]."""
+
+    def __init__(self, n_src, n_dst, rels, grad_src_types: int = 0):
+        self.n_src = [int(x) for x in n_src]
+        self.n_dst = [int(x) for x in n_dst]
+        self.num_types = len(self.n_src)
+        self.grad_src_types = int(grad_src_types)
+        self.indptr = [r[2] for r in rels]
+        self.indices = [r[3] for r in rels]
+        self.types = [(int(r[0]), int(r[1]), int(r[3].numel())) for r in rels]
+        self.num_rels = len(self.types)
+        self._n_src = (ctypes.c_int64 * self.num_types)(*self.n_src)
+        self._n_dst = (ctypes.c_int64 * self.num_types)(*self.n_dst)
+        self._rels = (_Relation * max(self.num_rels, 1))()
+        for r, (s, t, nnz) in enumerate(self.types):
+            self._rels[r] = _Relation(s, t, nnz, self.indptr[r].data_ptr(),
+                                      self.indices[r].data_ptr())
+        self.c = _Block(self.num_types, self.num_rels, self._n_src, self._n_dst, self._rels,
+                        self.grad_src_types)
+
+
+class DeviceGraph:
+    """A full graph in device memory (in-edge CSR per relation, int64) plus its C mirror.
+    ``graph`` has ``num_nodes`` and ``rels`` (``src_type``, ``dst_type``, ``indptr``,
+    ``indices``; numpy arrays or torch tensors)."""
+
+    def __init__(self, graph, device="cuda"):
+        self.num_nodes = [int(x) for x in graph.num_nodes]
+        self.num_types = len(self.num_nodes)
+        self.indptr, self.indices, self.types = [], [], []
+        for rel in graph.rels:
+            ip = torch.as_tensor(rel.indptr).to(device=device, dtype=torch.int64)
+            ix = torch.as_tensor(rel.indices).to(device=device, dtype=torch.int64)
+            if ix.numel() == 0:
+                ix = torch.zeros(1, dtype=torch.int64, device=device)
+            self.indptr.append(ip.contiguous())
+            self.indices.append(ix.contiguous())
+            self.types.append((int(rel.src_type), int(rel.dst_type)))
+        self.num_rels = len(self.types)
+        self._nodes = (ctypes.c_int64 * self.num_types)(*self.num_nodes)
+        self._rels = (_GraphRel * max(self.num_rels, 1))()
+        for r, (s, t) in enumerate(self.types):
+            self._rels[r] = _GraphRel(s, t, self.indptr[r].data_ptr(), self.indices[r].data_ptr())
+        self.c = _Graph(self.num_types, self.num_rels, self._nodes, self._rels)
 
 
 class Params:
@@ -351,3 +417,40 @@ def rgcn_sparse_adagrad(rows: torch.Tensor, grad: torch.Tensor, state: torch.Ten
         int(rows.numel()), rows.data_ptr(), int(table.shape[0]), int(grad.shape[1]),
         grad.data_ptr(), state.data_ptr(), table.data_ptr(), int(table.stride(0)), dt,
         float(lr), float(eps), int(flags), _stream(stream)))
+
+
+def rgcn_sample_workspace_size(graph: DeviceGraph, n_dst: Sequence[int], fanout: int) -> int:
+    out = ctypes.c_size_t(0)
+    nd = (ctypes.c_int64 * graph.num_types)(*[int(x) for x in n_dst])
+    _check(load_library().rgcn_sample_workspace_size(ctypes.byref(graph.c), nd, int(fanout),
+                                                     ctypes.byref(out)))
+    return int(out.value)
+
+
+def rgcn_sample_block(graph: DeviceGraph, dst_ids: Sequence[torch.Tensor], fanout: int,
+                      seed: int, layer: int, workspace: Optional[torch.Tensor] = None,
+                      flags: int = 0, stream=None):
+    """One layer's block for destination ids ``dst_ids[t]`` (device int64).  Returns
+    (out_indptr, out_indices, out_src_ids, counts): capacity-sized device tensors and the
+    device int64 counts [num_rels + num_types]."""
+    T, R = graph.num_types, graph.num_rels
+    dev = graph.indptr[0].device if R else dst_ids[0].device
+    n_dst = [int(x.numel()) for x in dst_ids]
+    if workspace is None:
+        workspace = torch.empty(rgcn_sample_workspace_size(graph, n_dst, fanout),
+                                dtype=torch.uint8, device=dev)
+    out_ip = [torch.empty(n_dst[t] + 1, dtype=torch.int32, device=dev) for (_, t) in graph.types]
+    out_ix = [torch.empty(max(n_dst[t] * fanout, 1), dtype=torch.int32, device=dev)
+              for (_, t) in graph.types]
+    cap = [n_dst[t] + sum(n_dst[d] * fanout for (s, d) in graph.types if s == t) for t in range(T)]
+    out_src = [torch.empty(max(c, 1), dtype=torch.int64, device=dev) for c in cap]
+    counts = torch.zeros(R + T, dtype=torch.int64, device=dev)
+    ids = [x.contiguous() for x in dst_ids]
+    keep = [_ptr_array([_ptr(x) for x in ids]), _ptr_array([_ptr(x) for x in out_ip]),
+            _ptr_array([_ptr(x) for x in out_ix]), _ptr_array([_ptr(x) for x in out_src])]
+    nd = (ctypes.c_int64 * T)(*n_dst)
+    _check(load_library().rgcn_sample_block(
+        ctypes.byref(graph.c), keep[0], nd, int(fanout), int(seed), int(layer), keep[1],
+        keep[2], keep[3], counts.data_ptr(), workspace.data_ptr(), workspace.numel(), flags,
+        _stream(stream)))
+    return out_ip, out_ix, out_src, counts

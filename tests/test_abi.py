@@ -162,3 +162,41 @@ def test_fused_adagrad_host_validation(lib):
     for kw, msg in cases:
         assert call(**kw) == 1, kw
         assert msg in lib.rgcn_last_error().decode(), (kw, lib.rgcn_last_error())
+
+
+def test_sampling_host_validation(lib):
+    """Sampling rejects bad graphs, fanouts and arrays before any launch."""
+    nodes = (ctypes.c_int64 * 2)(100, 50)
+    rels = (rgcn._GraphRel * 2)(rgcn._GraphRel(0, 1, 0x10000, 0x20000),
+                                rgcn._GraphRel(1, 0, 0x30000, 0x40000))
+    g = rgcn._Graph(2, 2, nodes, rels)
+    nd = (ctypes.c_int64 * 2)(10, 5)
+    out = ctypes.c_size_t(0)
+    assert lib.rgcn_sample_workspace_size(ctypes.byref(g), nd, 8, ctypes.byref(out)) == 0
+    assert out.value > 0
+    for fo in (0, 65):
+        assert lib.rgcn_sample_workspace_size(ctypes.byref(g), nd, fo, ctypes.byref(out)) == 7
+    bad = rgcn._Graph(2, 2, nodes, (rgcn._GraphRel * 2)(rgcn._GraphRel(0, 2, 0x10000, 0x20000),
+                                                        rgcn._GraphRel(1, 0, 0x30000, 0x40000)))
+    assert lib.rgcn_sample_workspace_size(ctypes.byref(bad), nd, 8, ctypes.byref(out)) == 1
+    neg = (ctypes.c_int64 * 2)(-1, 5)
+    assert lib.rgcn_sample_workspace_size(ctypes.byref(g), neg, 8, ctypes.byref(out)) == 2
+    huge = (ctypes.c_int64 * 2)(1 << 27, 1 << 27)
+    assert lib.rgcn_sample_workspace_size(ctypes.byref(g), huge, 64, ctypes.byref(out)) == 7
+    ws = out.value
+    lib.rgcn_sample_workspace_size(ctypes.byref(g), nd, 8, ctypes.byref(out))
+    p2 = (ctypes.c_void_p * 2)(0x50000, 0x60000)
+    p3 = (ctypes.c_void_p * 2)(0x70000, 0x80000)
+    f = lib.rgcn_sample_block
+    # workspace too small, misaligned workspace, NULL counts, NULL destination ids
+    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, 0x90000, 0x100000, 16, 0, None) == 6
+    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, 0x90000, 0x100010, out.value, 0,
+             None) == 1
+    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, None, 0x100000, out.value, 0,
+             None) == 1
+    nul = (ctypes.c_void_p * 2)(None, 0x60000)
+    assert f(ctypes.byref(g), nul, nd, 8, 1, 0, p3, p3, p2, 0x90000, 0x100000, out.value, 0,
+             None) == 1
+    assert "dst_ids[0]" in lib.rgcn_last_error().decode()
+    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, 0x90000, 0x100000, out.value, 0x4,
+             None) == 1
