@@ -22,6 +22,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "rgcn_oracle.c")
 _SRC_SAMPLE = os.path.join(_HERE, "sample_oracle.c")
+_SRC_LP = os.path.join(_HERE, "lp_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
@@ -36,7 +37,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp"
         subprocess.run(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fno-fast-math",
-                        "-ffp-contract=off", _SRC, _SRC_SAMPLE, "-o", tmp, "-lm"], check=True)
+                        "-ffp-contract=off", _SRC, _SRC_SAMPLE, _SRC_LP, "-o", tmp, "-lm"], check=True)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
 
@@ -85,6 +86,10 @@ def _load():
         lib.orc_sample_block.argtypes = [i32, i32, vp, vp, vp, vp, vp, vp, vp, i64, u64, i32,
                                          vp, vp, vp, vp]
         lib.orc_sample_block.restype = ctypes.c_int
+        lib.orc_lp_loss.argtypes = [i64, i64, vp, vp, i32, i32, i64, vp, vp, i64, vp, vp, vp, vp,
+                                    vp, vp, vp]
+        lib.orc_lp_loss.restype = ctypes.c_int
+        lib.orc_lp_negatives.argtypes = [i32, i64, i64, u64, vp]
         _lib = lib
     return _lib
 
@@ -436,3 +441,43 @@ def sample_block(graph, dst_ids: Sequence[np.ndarray], fanout: int, seed: int,
     src_ids = [out_src[t][:counts[R + t]] for t in range(T)]
     return SampledBlock([int(x.shape[0]) for x in src_ids], [int(x) for x in n_dst], rels,
                         src_ids)
+
+
+# ------------------------------------------------------------------------------------
+# Link-prediction decoder (lp_oracle.c states the readings)
+# ------------------------------------------------------------------------------------
+NEG_PER_EDGE, NEG_JOINT, NEG_IN_BATCH = 0, 1, 2
+LOSS_CE, LOSS_WEIGHTED_CE, LOSS_CONTRASTIVE = 0, 1, 2
+
+
+def lp_loss(emb: np.ndarray, rel: Optional[np.ndarray], neg_mode: int, loss_kind: int,
+            src, dst, k: int = 0, neg=None, pos_weight=None, grads: bool = True) -> dict:
+    """Scores, loss and gradients of one batch of positive edges (rows of ``emb``)."""
+    emb = np.ascontiguousarray(emb, dtype=np.float64)
+    n, d = emb.shape
+    src = np.ascontiguousarray(src, dtype=np.int64)
+    dst = np.ascontiguousarray(dst, dtype=np.int64)
+    B = src.shape[0]
+    nn = B - 1 if neg_mode == NEG_IN_BATCH else k
+    negv = np.ascontiguousarray(neg if neg is not None else np.zeros(1), dtype=np.int64)
+    relv = None if rel is None else np.ascontiguousarray(rel, dtype=np.float64)
+    w = None if pos_weight is None else np.ascontiguousarray(pos_weight, dtype=np.float64)
+    loss = np.zeros(1)
+    pos = np.zeros(max(B, 1))
+    negs = np.zeros(max(B * nn, 1))
+    d_emb = np.zeros((n, d)) if grads else None
+    d_rel = np.zeros(d) if (grads and rel is not None) else None
+    rc = _load().orc_lp_loss(n, d, emb.ctypes.data, _ptr(relv), neg_mode, loss_kind, B,
+                             src.ctypes.data, dst.ctypes.data, k, negv.ctypes.data, _ptr(w),
+                             loss.ctypes.data, pos.ctypes.data, negs.ctypes.data, _ptr(d_emb),
+                             _ptr(d_rel))
+    if rc != 0:
+        raise ValueError("invalid link-prediction batch")
+    return {"loss": float(loss[0]), "pos_score": pos[:B], "neg_score": negs[:B * nn].reshape(B, nn),
+            "d_emb": d_emb, "d_rel": d_rel}
+
+
+def lp_negatives(neg_mode: int, slots: int, num_nodes: int, seed: int) -> np.ndarray:
+    out = np.zeros(max(slots, 1), dtype=np.int64)
+    _load().orc_lp_negatives(neg_mode, slots, num_nodes, seed, out.ctypes.data)
+    return out[:slots]
