@@ -312,6 +312,46 @@ def summarize_kernels(args) -> str:
     return "\n".join(lines) + "\n"
 
 
+LP_SETTINGS = ["contrastive / in-batch, B 1024", "cross entropy / in-batch, B 1024",
+               "contrastive / joint-32, B 1024", "cross entropy / joint-32, B 1024",
+               "contrastive / uniform-32, B 1024", "cross entropy / uniform-32, B 1024",
+               "contrastive / uniform-32, B 65536 over 4M rows"]
+
+
+def summarize_lp(args) -> str:
+    """Kernel time per decoder call for each setting measure_lp runs (3 untimed and 50
+    timed calls per B 1024 setting, 3 and 10 for the large batch, in that order; a call
+    starts with its k_lp_scores launch)."""
+    calls, cur = [], []
+    for _, name, v in _dispatches(args.summarize_lp, r"rgcn::.*k_lp_"):
+        base = re.sub(r"<.*$", "", name)
+        if base == "k_lp_scores" and cur:
+            calls.append(cur)
+            cur = []
+        cur.append((base, v / 1e3))
+    calls.append(cur)
+    keys = [("scores", ["k_lp_scores"]), ("gather", ["k_lp_gather"]), ("gemm (3)", ["k_lp_gemm"]),
+            ("loss", ["k_lp_loss"]), ("sum", ["k_lp_sum"]), ("scatter", ["k_lp_scatter_cols"]),
+            ("finish", ["k_lp_finish"]), ("d_rel", ["k_lp_rel_partial", "k_lp_rel_final"])]
+    lines = ["# k_lp: decoder kernels per call", "", "Command:", "", "```", args.command, "```",
+             "", "Per call, us (averages over the timed calls of each setting):", "",
+             "| setting | " + " | ".join(k for k, _ in keys) + " | total |",
+             "|---|" + "---:|" * (len(keys) + 1)]
+    idx = 0
+    for si, setting in enumerate(LP_SETTINGS):
+        reps, warm = (53, 3) if si < 6 else (13, 3)
+        grp = calls[idx + warm: idx + reps]
+        idx += reps
+        agg = {}
+        for c in grp:
+            for n, t in c:
+                agg[n] = agg.get(n, 0.0) + t
+        vals = [sum(agg.get(x, 0.0) for x in names) / max(len(grp), 1) for _, names in keys]
+        lines.append(f"| {setting} | " + " | ".join(f"{v:.1f}" for v in vals) +
+                     f" | {sum(vals):.1f} |")
+    return "\n".join(lines) + "\n"
+
+
 def summarize_pmc(args) -> str:
     """Per-launch HBM traffic of --kernel from FETCH_SIZE and WRITE_SIZE runs, each scaled
     by what the same counter reads for the plain copy of --copy-probe-mib MiB."""
@@ -431,6 +471,100 @@ def measure_sampling(spec, dev, args):
     return out
 
 
+def lp_bytes(B: int, nn: int, d: int, esize: int, mode: int) -> float:
+    """Algorithmic bytes of one decoder call (scores, loss and gradients): the source,
+    destination and negative rows read once for the scores (shared negatives once per
+    group), again for the gradients, u_i and its gradient written and read in fp32, the
+    scores and their derivatives, and the gradient rows added into d_emb (read and
+    written) for every row touched."""
+    rows = 2 * B + (B * nn if mode == 0 else (((B + nn - 1) // max(nn, 1)) * nn if mode == 1 else 0))
+    emb = rows * d * esize * 2
+    u = B * d * 4 * 3
+    sc = B * nn * 4 * 3 + B * 4 * 3
+    grad = rows * d * 4 * 2
+    return float(emb + u + sc + grad)
+
+
+def measure_lp(dev, args):
+    """The link-prediction decoder (scores, loss, gradients in one call): the paper's
+    settings (local batch 1,024, in-batch / joint-32 / uniform-32 negatives, contrastive
+    and cross entropy) at d = 512 bf16, and a large per-edge batch for the rate of the
+    row gathers."""
+    import numpy as np
+    import torch
+
+    from paper_2406_06022_amd import rgcn
+
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(4242)
+    d = 512
+    out = {"d": d, "dtype": "bf16", "score": "DistMult"}
+
+    def setup(n_rows, B, k, mode):
+        emb = (torch.randn((n_rows, d), generator=gen, device=dev) * 0.1).to(torch.bfloat16)
+        rel = torch.randn(d, generator=gen, device=dev).to(torch.bfloat16)
+        src = torch.randint(0, n_rows, (B,), generator=gen, device=dev, dtype=torch.int32)
+        dst = torch.randint(0, n_rows, (B,), generator=gen, device=dev, dtype=torch.int32)
+        nneg = B * k if mode == 0 else (((B + k - 1) // k) * k if mode == 1 else 0)
+        neg = torch.randint(0, n_rows, (max(nneg, 1),), generator=gen, device=dev,
+                            dtype=torch.int32)
+        return emb, rel, src, dst, neg
+
+    def time_call(emb, rel, src, dst, neg, mode, kind, k, reps):
+        b = rgcn.lp_batch(emb, rel, mode, kind, src, dst, k, neg)
+        ws = torch.empty(rgcn.rgcn_lp_workspace_size(b), dtype=torch.uint8, device=dev)
+        loss = torch.zeros(1, device=dev)
+        d_emb = torch.zeros((emb.shape[0], d), device=dev)
+        d_rel = torch.zeros(d, device=dev)
+        for _ in range(3):
+            rgcn.rgcn_lp_loss(b, loss, None, None, d_emb, d_rel, ws)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            rgcn.rgcn_lp_loss(b, loss, None, None, d_emb, d_rel, ws)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    paper = {}
+    B = 1024
+    for name, mode, k in (("in-batch", 2, 0), ("joint-32", 1, 32), ("uniform-32", 0, 32)):
+        n_rows = 2 * B + (B * k if mode == 0 else k * (B // max(k, 1)) if mode == 1 else 0)
+        t = setup(n_rows, B, k, mode)
+        for lname, kind in (("contrastive", 2), ("cross-entropy", 0)):
+            paper[f"{lname}/{name}"] = round(time_call(*t, mode, kind, k, 50), 4)
+    out["paper_batch_1024_ms"] = paper
+    # large per-edge batch: 65,536 positives x 32 negatives over 4M rows (4 GB)
+    B, k, n_rows = 65536, 32, 4_000_000
+    t = setup(n_rows, B, k, 0)
+    ms = time_call(*t, 0, 2, k, 10)
+    byts = lp_bytes(B, k, d, 2, 0)
+    gbs = byts / (ms * 1e-3) / 1e9
+    out["large_uniform"] = {"batch": B, "negatives": k, "rows": n_rows, "ms": round(ms, 4),
+                            "bytes": byts, "GB/s": round(gbs, 1),
+                            "frac": round(gbs / HBM_PEAK_GBS, 4),
+                            "scored_edges_per_s": B * (k + 1) / (ms * 1e-3)}
+    del t
+    if args.cpu_budget > 0:
+        import oracle
+        rng = np.random.default_rng(3)
+        n_rows, B, k = 2 * 1024 + 1024 * 32, 1024, 32
+        emb = rng.standard_normal((n_rows, d)) * 0.1
+        rel = rng.standard_normal(d)
+        src, dst = rng.integers(0, n_rows, B), rng.integers(0, n_rows, B)
+        neg = rng.integers(0, n_rows, B * k)
+        c0, n = time.perf_counter(), 0
+        while time.perf_counter() - c0 < min(args.cpu_budget, 5.0) or n == 0:
+            oracle.lp_loss(emb, rel, 0, 2, src, dst, k, neg)
+            n += 1
+        el = time.perf_counter() - c0
+        out["cpu_baseline"] = {"value": n * B * (k + 1) / el, "unit": "scored edges/s",
+                               "cores": 1, "kind": "oracle",
+                               "sample": f"{n} calls of the uniform-32 contrastive batch of "
+                                         f"1,024 positives, d {d}, fp64, {el:.1f}s"}
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -447,11 +581,16 @@ def main() -> int:
     ap.add_argument("--summarize-kernels", nargs=2, metavar=("KERNEL_STATS_CSV", "REGEX"),
                     help="reduce a rocprofv3 kernel_stats.csv to the kernels matching REGEX "
                          "and exit")
+    ap.add_argument("--summarize-lp", metavar="KERNEL_TRACE_CSV",
+                    help="per-setting kernel breakdown of a rocprofv3 kernel_trace.csv of "
+                         "`bench.py --lp-only` and exit")
     ap.add_argument("--per", type=int, default=1,
                     help="with --summarize-kernels: divide totals by this many repetitions")
     ap.add_argument("--sampling-only", action="store_true",
                     help="run only the on-device mini-batch sampling measurement (12 "
                          "mini-batches of the workload) and print its JSON object")
+    ap.add_argument("--lp-only", action="store_true",
+                    help="run only the link-prediction decoder measurement and print its JSON")
     ap.add_argument("--kernel", default="k_gather_flat")
     ap.add_argument("--launches-per-step", type=int, default=3,
                     help="launches of --kernel per step (summaries split them by position)")
@@ -466,6 +605,9 @@ def main() -> int:
     if args.summarize_kernels:
         print(summarize_kernels(args), end="")
         return 0
+    if args.summarize_lp:
+        print(summarize_lp(args), end="")
+        return 0
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for --gpus {args.gpus}); the multi-GPU "
               "sharding of this path is a design note, not an implementation.", file=sys.stderr)
@@ -477,6 +619,9 @@ def main() -> int:
     dev = "cuda:0"
     torch.cuda.set_device(0)
     rgcn.load_library()
+    if args.lp_only:
+        print(json.dumps(measure_lp(dev, args)), flush=True)
+        return 0
     if args.sampling_only:
         from paper_2406_06022_amd import synth
         print(json.dumps(measure_sampling(synth.config(args.config), dev, args)), flush=True)
@@ -603,6 +748,7 @@ def main() -> int:
                "lr": 0.01, "eps": 1e-10}
 
     sampling = measure_sampling(spec, dev, args)
+    link_prediction = measure_lp(dev, args)
 
     out = {
         "metric": METRIC,
@@ -633,6 +779,7 @@ def main() -> int:
         "mfma_transforms": mfma,
         "train_step_sparse_adagrad": adagrad,
         "sampling": sampling,
+        "link_prediction": link_prediction,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

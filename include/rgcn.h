@@ -306,6 +306,68 @@ rgcn_status rgcn_sample_block(const rgcn_graph *graph, const int64_t *const *dst
                               void *workspace, size_t workspace_bytes, unsigned flags,
                               hipStream_t stream);
 
+/* ---------------------------------------------------------------- link prediction
+ * The link-prediction decoder of the paper's appendix on score and loss functions,
+ * applied to a batch of B positive edges (src_i, dst_i), rows of the GNN's output
+ * embedding matrix, and their negatives, which keep src_i and replace dst_i:
+ *   scores:    dot product sum_c h_u[c] h_v[c], or DistMult sum_c h_u[c] r[c] h_v[c] with r
+ *              the edge type's embedding (the printed dot product reuses the node index
+ *              as the summation index: the sum runs over the embedding dimension);
+ *   negatives: RGCN_LP_NEG_PER_EDGE (uniform): K rows per positive, neg[i*K + k];
+ *              RGCN_LP_NEG_JOINT: positives i of group g = i / K share neg[g*K + k];
+ *              RGCN_LP_NEG_IN_BATCH: the destinations of the other positives, dst_j for
+ *              j != i in ascending j (B - 1 negatives), as in the appendix's example;
+ *   losses:    RGCN_LP_CE: binary cross entropy on sigmoid(score), label 1 for positives
+ *              and 0 for negatives, averaged over all B (1 + K) scored edges (the printed
+ *              formula misplaces a sign and a bracket);
+ *              RGCN_LP_WEIGHTED_CE: the same with weight pos_weight[i] on positive i and
+ *              1 on negatives;
+ *              RGCN_LP_CONTRASTIVE: per positive, -log(exp(s_pos) / (exp(s_pos) +
+ *              sum_k exp(s_k))) (the positive is in the denominator), averaged over B. */
+typedef enum { RGCN_LP_NEG_PER_EDGE = 0, RGCN_LP_NEG_JOINT = 1, RGCN_LP_NEG_IN_BATCH = 2 } rgcn_lp_neg;
+typedef enum { RGCN_LP_CE = 0, RGCN_LP_WEIGHTED_CE = 1, RGCN_LP_CONTRASTIVE = 2 } rgcn_lp_loss_kind;
+
+typedef struct {
+    rgcn_dtype dtype;
+    int32_t d;                  /* embedding width, a multiple of 8 (bf16) or 4 (fp32), <= 2048 (bf16) / 1024 (fp32) */
+    int64_t n_rows;             /* rows of emb */
+    int64_t ld;                 /* row stride of emb in elements, >= d, a multiple of 8 / 4 */
+    const void *emb;            /* [n_rows x ld] in dtype, 16-byte aligned */
+    const void *rel;            /* DistMult: [d] in dtype, 16-byte aligned; NULL: dot product */
+    int32_t neg_mode;           /* rgcn_lp_neg */
+    int32_t loss;               /* rgcn_lp_loss_kind */
+    int64_t batch;              /* B */
+    const int32_t *src;         /* [B] rows of emb */
+    const int32_t *dst;         /* [B] rows of emb */
+    int32_t k;                  /* negatives per positive (per edge, joint); in-batch: ignored */
+    const int32_t *neg;         /* per edge: [B x K] rows; joint: [ceil(B / K) x K]; in-batch: NULL */
+    const float *pos_weight;    /* weighted CE: [B]; otherwise ignored */
+} rgcn_lp_batch;
+
+/* Workspace bytes of rgcn_lp_loss for this batch (host only).  It holds the B x N scores
+ * and their derivatives (N = K, or B - 1 in-batch); B x N must stay below 2^31. */
+rgcn_status rgcn_lp_workspace_size(const rgcn_lp_batch *batch, size_t *bytes /* [host] */);
+
+/* Loss of one batch, its scores and gradients.  Outputs (device, fp32; NULL skips):
+ *   loss:      [1] the averaged loss (overwritten);
+ *   pos_score: [B]; neg_score: [B x N] in positive-major order (overwritten);
+ *   d_emb:     [n_rows x d], row-major: the gradient of the loss with respect to each
+ *              embedding row is ADDED (caller-initialised; rows never used untouched;
+ *              fp32 atomics, so the order of additions varies);
+ *   d_rel:     [d] the gradient with respect to rel (DistMult; overwritten).
+ * Rows outside [0, n_rows) are the caller's error: checked only with RGCN_VALIDATE_DEVICE
+ * (before any other work; synchronises; RGCN_ERR_INDEX_OOB).  flags: RGCN_VALIDATE_DEVICE. */
+rgcn_status rgcn_lp_loss(const rgcn_lp_batch *batch, float *loss, float *pos_score,
+                         float *neg_score, float *d_emb, float *d_rel, void *workspace,
+                         size_t workspace_bytes, unsigned flags, hipStream_t stream);
+
+/* Negative node ids for the per-edge (slots = B * K) or joint (slots = ceil(B / K) * K)
+ * modes: slot q is the high word of draw * num_nodes, the draw being word q mod 4 of
+ * Philox4x64-10 at counter (q / 4, neg_mode, 0, 0) and key (seed, 0x6e6567); uniform over
+ * [0, num_nodes) and a function of the arguments only.  out: device int64 [slots]. */
+rgcn_status rgcn_lp_negatives(int32_t neg_mode, int64_t slots, int64_t num_nodes, uint64_t seed,
+                              int64_t *out, hipStream_t stream);
+
 /* Message for the last non-OK status returned on the calling thread ("" if none). */
 const char *rgcn_last_error(void);
 

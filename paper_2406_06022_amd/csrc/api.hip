@@ -892,3 +892,112 @@ rgcn_status rgcn_sample_block(const rgcn_graph *graph, const int64_t *const *dst
 }
 
 }  // extern "C"
+
+namespace {
+
+rgcn_status lp_args(const rgcn_lp_batch *b, LpArgs &a) {
+    if (!b) return fail(RGCN_ERR_INVALID_ARG, "batch is NULL");
+    if (b->dtype != RGCN_F32 && b->dtype != RGCN_BF16) return fail(RGCN_ERR_DTYPE, "unknown dtype");
+    const int vec = b->dtype == RGCN_BF16 ? 8 : 4;
+    if (b->d <= 0 || b->d % vec || b->d > 256 * vec)
+        return fail(RGCN_ERR_UNSUPPORTED, "d %d must be a positive multiple of %d, at most %d",
+                    b->d, vec, 256 * vec);
+    if (b->ld < b->d || b->ld % vec || b->n_rows < 0)
+        return fail(RGCN_ERR_SHAPE, "ld %lld must be >= d and a multiple of %d",
+                    (long long)b->ld, vec);
+    if (b->neg_mode < 0 || b->neg_mode > 2) return fail(RGCN_ERR_INVALID_ARG, "unknown neg_mode");
+    if (b->loss < 0 || b->loss > 2) return fail(RGCN_ERR_INVALID_ARG, "unknown loss");
+    if (b->batch < 0) return fail(RGCN_ERR_SHAPE, "negative batch");
+    if (b->neg_mode != RGCN_LP_NEG_IN_BATCH && b->k < 1)
+        return fail(RGCN_ERR_SHAPE, "k must be at least 1");
+    memset(&a, 0, sizeof(a));
+    a.dtype = b->dtype;
+    a.d = b->d;
+    a.ld = b->ld;
+    a.n_rows = b->n_rows;
+    a.emb = b->emb;
+    a.rel = b->rel;
+    a.neg_mode = b->neg_mode;
+    a.loss = b->loss;
+    a.batch = b->batch;
+    a.k = b->neg_mode == RGCN_LP_NEG_IN_BATCH ? 0 : b->k;
+    a.nn = b->neg_mode == RGCN_LP_NEG_IN_BATCH ? (b->batch > 0 ? b->batch - 1 : 0) : b->k;
+    a.src = b->src;
+    a.dst = b->dst;
+    a.neg = b->neg;
+    a.pos_weight = b->pos_weight;
+    if ((double)a.batch * (double)(a.nn > 0 ? a.nn : 1) >= 2147483647.0 ||
+        (double)a.batch * a.d >= 2147483647.0)
+        return fail(RGCN_ERR_UNSUPPORTED, "batch x negatives or batch x d reaches 2^31");
+    if (a.batch > 0) {
+        if (!a.emb || !aligned16(a.emb)) return fail(RGCN_ERR_INVALID_ARG, "emb NULL or misaligned");
+        if (a.rel && !aligned16(a.rel)) return fail(RGCN_ERR_INVALID_ARG, "rel misaligned");
+        if (!a.src || !a.dst || !aligned4(a.src) || !aligned4(a.dst))
+            return fail(RGCN_ERR_INVALID_ARG, "src or dst NULL or misaligned");
+        if (a.neg_mode != RGCN_LP_NEG_IN_BATCH && (!a.neg || !aligned4(a.neg)))
+            return fail(RGCN_ERR_INVALID_ARG, "neg NULL or misaligned");
+        if (a.loss == RGCN_LP_WEIGHTED_CE && (!a.pos_weight || !aligned4(a.pos_weight)))
+            return fail(RGCN_ERR_INVALID_ARG, "pos_weight NULL or misaligned");
+    }
+    return RGCN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rgcn_status rgcn_lp_workspace_size(const rgcn_lp_batch *batch, size_t *bytes) {
+    if (!bytes) return fail(RGCN_ERR_INVALID_ARG, "bytes is NULL");
+    LpArgs a;
+    rgcn_status st = lp_args(batch, a);
+    if (st != RGCN_OK) return st;
+    *bytes = lp_layout(a).total;
+    return RGCN_OK;
+}
+
+rgcn_status rgcn_lp_loss(const rgcn_lp_batch *batch, float *loss, float *pos_score,
+                         float *neg_score, float *d_emb, float *d_rel, void *workspace,
+                         size_t workspace_bytes, unsigned flags, hipStream_t stream) {
+    LpArgs a;
+    rgcn_status st = lp_args(batch, a);
+    if (st != RGCN_OK) return st;
+    if (flags & ~(unsigned)RGCN_VALIDATE_DEVICE)
+        return fail(RGCN_ERR_INVALID_ARG, "unsupported flags 0x%x", flags);
+    const LpLayout L = lp_layout(a);
+    if (!workspace || ((uintptr_t)workspace & 255u))
+        return fail(RGCN_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
+    if (workspace_bytes < L.total)
+        return fail(RGCN_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu",
+                    workspace_bytes, L.total);
+    if (!loss || !aligned4(loss)) return fail(RGCN_ERR_INVALID_ARG, "loss NULL or misaligned");
+    if ((pos_score && !aligned4(pos_score)) || (neg_score && !aligned4(neg_score)) ||
+        (d_emb && !aligned4(d_emb)) || (d_rel && !aligned4(d_rel)))
+        return fail(RGCN_ERR_INVALID_ARG, "an output is misaligned");
+    if (d_rel && !a.rel) return fail(RGCN_ERR_INVALID_ARG, "d_rel requested for a dot product");
+    char *ws = (char *)workspace;
+    if ((flags & RGCN_VALIDATE_DEVICE) && a.batch > 0) {
+        uint32_t *err = (uint32_t *)(ws + L.off_err);
+        const uint32_t zero = 0;
+        TRY_HIP(fill_words(err, &zero, 4, stream), "validate");
+        TRY_HIP(lp_validate(a, err, stream), "validate");
+        uint32_t host = 0;
+        TRY_HIP(hipMemcpyAsync(&host, err, 4, hipMemcpyDeviceToHost, stream), "validate copy");
+        TRY_HIP(hipStreamSynchronize(stream), "validate sync");
+        if (host) return fail(RGCN_ERR_INDEX_OOB, "a row index is outside [0, n_rows)");
+    }
+    TRY_HIP(lp_loss(a, L, ws, loss, pos_score, neg_score, d_emb, d_rel, stream), "link prediction");
+    return RGCN_OK;
+}
+
+rgcn_status rgcn_lp_negatives(int32_t neg_mode, int64_t slots, int64_t num_nodes, uint64_t seed,
+                              int64_t *out, hipStream_t stream) {
+    if (neg_mode != RGCN_LP_NEG_PER_EDGE && neg_mode != RGCN_LP_NEG_JOINT)
+        return fail(RGCN_ERR_INVALID_ARG, "negative ids are drawn for per-edge or joint modes");
+    if (slots < 0 || num_nodes < 1) return fail(RGCN_ERR_SHAPE, "slots < 0 or num_nodes < 1");
+    if (slots > 0 && (!out || ((uintptr_t)out & 7u)))
+        return fail(RGCN_ERR_INVALID_ARG, "out NULL or misaligned");
+    TRY_HIP(lp_negatives(neg_mode, slots, num_nodes, seed, out, stream), "negatives");
+    return RGCN_OK;
+}
+
+}  // extern "C"

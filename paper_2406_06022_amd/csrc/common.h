@@ -32,6 +32,24 @@ __device__ __forceinline__ float round_bf16(float x) {
     return __uint_as_float(pack_bf16x2(x, 0.f) << 16);
 }
 
+// Philox4x64-10 block function (Salmon, Moraes, Dror and Shaw, SC 2011): 10 rounds of
+// two 64x64 -> 128-bit products of words 0 and 2 by fixed odd constants, the high halves
+// mixed into words 1 and 3 with the key, the key advanced by two Weyl constants between
+// rounds.  c: counter in, output out.
+__device__ __forceinline__ void philox4x64(uint64_t c[4], uint64_t k0, uint64_t k1) {
+    const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int round = 0; round < 10; ++round) {
+        const uint64_t hi0 = __umul64hi(M0, c[0]), lo0 = M0 * c[0];
+        const uint64_t hi1 = __umul64hi(M1, c[2]), lo1 = M1 * c[2];
+        const uint64_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+        c[0] = n0; c[1] = lo1; c[2] = n2; c[3] = lo0;
+        k0 += W0;
+        k1 += W1;
+    }
+}
+
 // Number of set bits of `mask` below the calling lane (wave64).
 __device__ __forceinline__ int lanes_below(uint64_t mask) {
     return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
@@ -200,6 +218,30 @@ bool sample_layout(SampleTab &T, SampleLayout &L);
 // destination ids, 4 in-degree of 2^32 or more, 8 graph source id out of range.
 hipError_t sample_block(const SampleTab &T, const SampleLayout &L, char *ws, int64_t *counts,
                         hipStream_t s);
+
+// lp.hip: link-prediction decoder (see the file for the passes)
+struct LpArgs {
+    rgcn_dtype dtype;
+    int32_t d;
+    int64_t ld, n_rows;
+    const void *emb;
+    const void *rel;          // [d] (DistMult) or NULL (dot product)
+    int32_t neg_mode, loss;
+    int64_t batch, k, nn;     // nn: negatives per positive
+    const int32_t *src, *dst, *neg;
+    const float *pos_weight;
+};
+struct LpLayout {
+    size_t off_pos, off_gpos, off_lossp, off_S, off_G, off_U, off_P, off_dU, off_Hn, off_dHn,
+        off_colsum, off_err, total;
+};
+LpLayout lp_layout(const LpArgs &a);
+hipError_t lp_loss(const LpArgs &a, const LpLayout &L, char *ws, float *loss, float *pos_score,
+                   float *neg_score, float *d_emb, float *d_rel, hipStream_t s);
+// error bit 1 at *err when a row is outside [0, n_rows)
+hipError_t lp_validate(const LpArgs &a, uint32_t *err, hipStream_t s);
+hipError_t lp_negatives(int32_t neg_mode, int64_t slots, int64_t num_nodes, uint64_t seed,
+                        int64_t *out, hipStream_t s);
 
 hipError_t pack_weights(rgcn_dtype dt, int d_in, int d_out, const void *const *w_slots,
                         int nslots, void *wcat_t, hipStream_t s);

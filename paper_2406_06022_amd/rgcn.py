@@ -31,8 +31,10 @@ EXPORTED = ("rgcn_block_workspace_size", "rgcn_block_plan_layout", "rgcn_block_p
             "rgcn_block_forward", "rgcn_block_backward", "rgcn_block_aggregate",
             "rgcn_block_transform", "rgcn_block_backward_dense", "rgcn_block_backward_sparse",
             "rgcn_block_backward_sparse_adagrad", "rgcn_sparse_adagrad",
-            "rgcn_sample_workspace_size", "rgcn_sample_block", "rgcn_last_error",
-            "rgcn_version")
+            "rgcn_sample_workspace_size", "rgcn_sample_block", "rgcn_lp_workspace_size",
+            "rgcn_lp_loss", "rgcn_lp_negatives", "rgcn_last_error", "rgcn_version")
+RGCN_LP_NEG_PER_EDGE, RGCN_LP_NEG_JOINT, RGCN_LP_NEG_IN_BATCH = 0, 1, 2
+RGCN_LP_CE, RGCN_LP_WEIGHTED_CE, RGCN_LP_CONTRASTIVE = 0, 1, 2
 RGCN_MAX_FANOUT = 64
 
 
@@ -80,6 +82,14 @@ class _GraphRel(ctypes.Structure):
 class _Graph(ctypes.Structure):
     _fields_ = [("num_types", ctypes.c_int32), ("num_rels", ctypes.c_int32),
                 ("num_nodes", ctypes.POINTER(ctypes.c_int64)), ("rels", ctypes.POINTER(_GraphRel))]
+
+
+class _LpBatch(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int), ("d", ctypes.c_int32), ("n_rows", ctypes.c_int64),
+                ("ld", ctypes.c_int64), ("emb", ctypes.c_void_p), ("rel", ctypes.c_void_p),
+                ("neg_mode", ctypes.c_int32), ("loss", ctypes.c_int32), ("batch", ctypes.c_int64),
+                ("src", ctypes.c_void_p), ("dst", ctypes.c_void_p), ("k", ctypes.c_int32),
+                ("neg", ctypes.c_void_p), ("pos_weight", ctypes.c_void_p)]
 
 
 class _PlanLayout(ctypes.Structure):
@@ -136,6 +146,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                           ctypes.c_int32, vp, vp, vp, vp, vp, ctypes.c_size_t,
                                           ctypes.c_uint, vp]
         lib.rgcn_sample_block.restype = st
+        lib.rgcn_lp_workspace_size.argtypes = [vp, vp]
+        lib.rgcn_lp_workspace_size.restype = st
+        lib.rgcn_lp_loss.argtypes = [vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, ctypes.c_uint, vp]
+        lib.rgcn_lp_loss.restype = st
+        lib.rgcn_lp_negatives.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
+                                          ctypes.c_uint64, vp, vp]
+        lib.rgcn_lp_negatives.restype = st
         lib.rgcn_last_error.restype = ctypes.c_char_p
         lib.rgcn_version.restype = ctypes.c_char_p
         _lib = lib
@@ -454,3 +471,38 @@ def rgcn_sample_block(graph: DeviceGraph, dst_ids: Sequence[torch.Tensor], fanou
         keep[2], keep[3], counts.data_ptr(), workspace.data_ptr(), workspace.numel(), flags,
         _stream(stream)))
     return out_ip, out_ix, out_src, counts
+
+
+def lp_batch(emb: torch.Tensor, rel: Optional[torch.Tensor], neg_mode: int, loss_kind: int,
+             src: torch.Tensor, dst: torch.Tensor, k: int = 0, neg: Optional[torch.Tensor] = None,
+             pos_weight: Optional[torch.Tensor] = None, d: Optional[int] = None):
+    """The C description of a link-prediction batch (tensors must stay alive)."""
+    dt = RGCN_BF16 if emb.dtype == torch.bfloat16 else RGCN_F32
+    return _LpBatch(dt, int(d if d is not None else emb.shape[1]), int(emb.shape[0]),
+                    int(emb.stride(0)), emb.data_ptr(), _ptr(rel), int(neg_mode), int(loss_kind),
+                    int(src.numel()), src.data_ptr(), dst.data_ptr(), int(k), _ptr(neg),
+                    _ptr(pos_weight))
+
+
+def rgcn_lp_workspace_size(batch: "_LpBatch") -> int:
+    out = ctypes.c_size_t(0)
+    _check(load_library().rgcn_lp_workspace_size(ctypes.byref(batch), ctypes.byref(out)))
+    return int(out.value)
+
+
+def rgcn_lp_loss(batch: "_LpBatch", loss: torch.Tensor, pos_score=None, neg_score=None,
+                 d_emb=None, d_rel=None, workspace: Optional[torch.Tensor] = None, flags: int = 0,
+                 stream=None) -> None:
+    if workspace is None:
+        workspace = torch.empty(rgcn_lp_workspace_size(batch), dtype=torch.uint8,
+                                device=loss.device)
+    _check(load_library().rgcn_lp_loss(ctypes.byref(batch), loss.data_ptr(), _ptr(pos_score),
+                                       _ptr(neg_score), _ptr(d_emb), _ptr(d_rel),
+                                       workspace.data_ptr(), workspace.numel(), flags,
+                                       _stream(stream)))
+
+
+def rgcn_lp_negatives(neg_mode: int, slots: int, num_nodes: int, seed: int, out: torch.Tensor,
+                      stream=None) -> None:
+    _check(load_library().rgcn_lp_negatives(int(neg_mode), int(slots), int(num_nodes), int(seed),
+                                            out.data_ptr(), _stream(stream)))

@@ -200,3 +200,44 @@ def test_sampling_host_validation(lib):
     assert "dst_ids[0]" in lib.rgcn_last_error().decode()
     assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, 0x90000, 0x100000, out.value, 0x4,
              None) == 1
+
+
+def test_link_prediction_host_validation(lib):
+    """The decoder rejects bad widths, modes, strides and pointers before any launch."""
+    def batch(**kw):
+        a = dict(dtype=rgcn.RGCN_BF16, d=64, n_rows=100, ld=64, emb=0x100000, rel=0x200000,
+                 neg_mode=0, loss=2, batch=8, src=0x300000, dst=0x400000, k=4, neg=0x500000,
+                 pos_weight=None)
+        a.update(kw)
+        return rgcn._LpBatch(a["dtype"], a["d"], a["n_rows"], a["ld"], a["emb"], a["rel"],
+                             a["neg_mode"], a["loss"], a["batch"], a["src"], a["dst"], a["k"],
+                             a["neg"], a["pos_weight"])
+    out = ctypes.c_size_t(0)
+    assert lib.rgcn_lp_workspace_size(ctypes.byref(batch()), ctypes.byref(out)) == 0
+    cases = [(dict(dtype=9), 3), (dict(d=60), 7), (dict(d=4096), 7), (dict(ld=32), 2),
+             (dict(neg_mode=3), 1), (dict(loss=5), 1), (dict(k=0), 2), (dict(batch=-1), 2),
+             (dict(emb=0x100008), 1), (dict(neg=None), 1), (dict(loss=1), 1),
+             (dict(neg_mode=2, batch=50000), 7)]
+    for kw, want in cases:
+        # pointer checks run in the workspace query too
+        got = lib.rgcn_lp_workspace_size(ctypes.byref(batch(**kw)), ctypes.byref(out))
+        assert got == want, (kw, got, lib.rgcn_last_error())
+    # in-batch needs no negative array
+    assert lib.rgcn_lp_workspace_size(ctypes.byref(batch(neg_mode=2, neg=None)),
+                                      ctypes.byref(out)) == 0
+    b = batch()
+    lib.rgcn_lp_workspace_size(ctypes.byref(b), ctypes.byref(out))
+    f = lib.rgcn_lp_loss
+    assert f(ctypes.byref(b), None, None, None, None, None, 0x600000, out.value, 0, None) == 1
+    assert f(ctypes.byref(b), 0x700000, None, None, None, None, 0x600000, 16, 0, None) == 6
+    assert f(ctypes.byref(b), 0x700000, None, None, None, None, 0x600000, out.value, 0x8,
+             None) == 1
+    nodot = batch(rel=None)
+    lib.rgcn_lp_workspace_size(ctypes.byref(nodot), ctypes.byref(out))
+    assert f(ctypes.byref(nodot), 0x700000, None, None, None, 0x800000, 0x600000, out.value, 0,
+             None) == 1
+    assert "d_rel" in lib.rgcn_last_error().decode()
+    g = lib.rgcn_lp_negatives
+    assert g(2, 10, 100, 1, 0x900000, None) == 1
+    assert g(0, 10, 0, 1, 0x900000, None) == 2
+    assert g(0, 0, 10, 1, None, None) == 0
