@@ -23,6 +23,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "rgcn_oracle.c")
 _SRC_SAMPLE = os.path.join(_HERE, "sample_oracle.c")
 _SRC_LP = os.path.join(_HERE, "lp_oracle.c")
+_SRC_FEAT = os.path.join(_HERE, "feature_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
@@ -37,7 +38,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp"
         subprocess.run(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fno-fast-math",
-                        "-ffp-contract=off", _SRC, _SRC_SAMPLE, _SRC_LP, "-o", tmp, "-lm"], check=True)
+                        "-ffp-contract=off", _SRC, _SRC_SAMPLE, _SRC_LP, _SRC_FEAT, "-o", tmp, "-lm"], check=True)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
 
@@ -90,6 +91,8 @@ def _load():
                                     vp, vp, vp]
         lib.orc_lp_loss.restype = ctypes.c_int
         lib.orc_lp_negatives.argtypes = [i32, i64, i64, u64, vp]
+        lib.orc_featureless_mean.argtypes = [i32, vp, vp, vp, vp, i64, i64, vp]
+        lib.orc_featureless_mean.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -481,3 +484,31 @@ def lp_negatives(neg_mode: int, slots: int, num_nodes: int, seed: int) -> np.nda
     out = np.zeros(max(slots, 1), dtype=np.int64)
     _load().orc_lp_negatives(neg_mode, slots, num_nodes, seed, out.ctypes.data)
     return out[:slots]
+
+
+# ------------------------------------------------------------------------------------
+# Feature construction for featureless nodes (feature_oracle.c states the reading)
+# ------------------------------------------------------------------------------------
+def featureless_mean(rels, num_nodes: int) -> np.ndarray:
+    """rels: list of (indptr int64 [num_nodes + 1], indices int64, source features
+    [rows x d]).  Returns the mean of each node's in-neighbours' features (fp64)."""
+    R = len(rels)
+    d = int(rels[0][2].shape[1]) if R else 0
+    ips = [np.ascontiguousarray(r[0], dtype=np.int64) for r in rels]
+    ixs = [np.ascontiguousarray(r[1] if len(r[1]) else np.zeros(1), dtype=np.int64) for r in rels]
+    fts = [np.ascontiguousarray(r[2], dtype=np.float64) for r in rels]
+    rows = np.array([f.shape[0] for f in fts], dtype=np.int64)
+    out = np.zeros((num_nodes, d))
+
+    def parr(xs):
+        a = (ctypes.c_void_p * max(len(xs), 1))()
+        for i, x in enumerate(xs):
+            a[i] = x.ctypes.data
+        return a
+
+    rc = _load().orc_featureless_mean(R, parr(ips), parr(ixs), parr(fts),
+                                      rows.ctypes.data if R else None, num_nodes, d,
+                                      out.ctypes.data)
+    if rc != 0:
+        raise ValueError("neighbour index out of range")
+    return out
