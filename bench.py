@@ -385,7 +385,19 @@ def summarize_pmc(args) -> str:
     return "\n".join(lines) + "\n"
 
 
-def measure_sampling(spec, dev, args):
+def full_graph(spec, dev):
+    import torch
+
+    from paper_2406_06022_amd import synth
+
+    t0 = time.perf_counter()
+    g = synth.device_graph(spec, device=dev)
+    torch.cuda.synchronize()
+    log(f"full graph: nodes {g.num_nodes}, {g.nnz} edges in {time.perf_counter() - t0:.1f}s")
+    return g
+
+
+def measure_sampling(spec, g, dev, args):
     """On-device mini-batch sampling from the workload's full graph: each mini-batch is
     the three layers top-down from 4,096 seeds (host reads of the counts between layers
     included), timed over several mini-batches with distinct random streams; the oracle
@@ -393,13 +405,9 @@ def measure_sampling(spec, dev, args):
     import numpy as np
     import torch
 
-    from paper_2406_06022_amd import rgcn, sampler, synth
+    from paper_2406_06022_amd import rgcn, sampler
 
-    t0 = time.perf_counter()
-    g = synth.device_graph(spec, device=dev)
     dg = rgcn.DeviceGraph(g)
-    torch.cuda.synchronize()
-    log(f"full graph: nodes {g.num_nodes}, {g.nnz} edges in {time.perf_counter() - t0:.1f}s")
     gen = torch.Generator(device="cpu").manual_seed(spec.seed + 5)
     T = len(g.num_nodes)
     seeds = [torch.zeros(0, dtype=torch.int64, device=dev) for _ in range(T)]
@@ -466,9 +474,76 @@ def measure_sampling(spec, dev, args):
                                                          len(spec.fanouts) - 1)
         torch.cuda.synchronize()
         out["seed_layer_gpu_ms"] = round((time.perf_counter() - a) * 1e3 / 20, 4)
-    del dg, g
+    del dg
     torch.cuda.empty_cache()
     return out
+
+
+def measure_featureless(spec, g, tables, dev, args):
+    """Feature construction for the featureless type over the workload's whole graph: the
+    mean of every node's featured in-neighbours (all relations into the type whose source
+    type has a feature table), one call over all its nodes; the oracle runs the same
+    construction for the first nodes of the type on the host."""
+    import numpy as np
+    import torch
+
+    from paper_2406_06022_amd import rgcn
+
+    T = len(g.num_nodes)
+    fl = [t for t in range(T) if spec.featureless[t]]
+    if not fl:
+        return None
+    t0 = fl[0]
+    into = [r for r in g.rels if r.dst_type == t0 and not spec.featureless[r.src_type]]
+    if not into:
+        return None
+    rels = [(r.indptr, r.indices, tables[r.src_type]) for r in into]
+    n = g.num_nodes[t0]
+    d = int(tables[into[0].src_type].shape[1])
+    out_t = torch.empty((n, d), dtype=tables[into[0].src_type].dtype, device=dev)
+    ws = torch.empty(rgcn.RGCN_FEATURELESS_WORKSPACE, dtype=torch.uint8, device=dev)
+    esize = out_t.element_size()
+    nnz = sum(int(r.indices.shape[0]) for r in into)
+    byts = float(len(into) * 8 * (n + 1) + nnz * (8 + d * esize) + n * d * esize)
+    rgcn.rgcn_featureless_mean(rels, n, out_t, ws)
+    reps = 3
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        rgcn.rgcn_featureless_mean(rels, n, out_t, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    gbs = byts / (ms * 1e-3) / 1e9
+    res = {"type": spec.ntype_names[t0], "nodes": n, "d": d, "dtype": spec.dtype,
+           "relations": [spec.ntype_names[r.src_type] for r in into], "edges": nnz,
+           "kernel": "k_feature_mean", "ms": round(ms, 3), "bytes": byts,
+           "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
+           "edges_per_s": nnz / (ms * 1e-3)}
+    if args.cpu_budget > 0:
+        import oracle
+        # the first nodes of the type with all their in-edges, copied to the host
+        k = 100_000
+        sub = []
+        for r in into:
+            ip = r.indptr[: k + 1].cpu().numpy()
+            ix = r.indices[: int(ip[-1])].cpu().numpy()
+            rows = np.unique(ix)
+            feat = tables[r.src_type][torch.as_tensor(rows, device=dev)].float().cpu().numpy()
+            sub.append((ip, np.searchsorted(rows, ix), feat))
+        e_sub = sum(int(x[0][-1]) for x in sub)
+        c0, reps_cpu = time.perf_counter(), 0
+        while time.perf_counter() - c0 < min(args.cpu_budget, 5.0) or reps_cpu == 0:
+            oracle.featureless_mean(sub, k)
+            reps_cpu += 1
+        el = time.perf_counter() - c0
+        res["cpu_baseline"] = {"value": reps_cpu * e_sub / el, "unit": "edges/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"the first {k} nodes of the type ({e_sub} edges), "
+                                         f"{reps_cpu} run(s), fp64, {el:.1f}s"}
+    del out_t
+    torch.cuda.empty_cache()
+    return res
 
 
 def lp_bytes(B: int, nn: int, d: int, esize: int, mode: int) -> float:
@@ -589,6 +664,8 @@ def main() -> int:
     ap.add_argument("--sampling-only", action="store_true",
                     help="run only the on-device mini-batch sampling measurement (12 "
                          "mini-batches of the workload) and print its JSON object")
+    ap.add_argument("--featureless-only", action="store_true",
+                    help="time only the featureless-type feature construction")
     ap.add_argument("--lp-only", action="store_true",
                     help="run only the link-prediction decoder measurement and print its JSON")
     ap.add_argument("--kernel", default="k_gather_flat")
@@ -624,7 +701,18 @@ def main() -> int:
         return 0
     if args.sampling_only:
         from paper_2406_06022_amd import synth
-        print(json.dumps(measure_sampling(synth.config(args.config), dev, args)), flush=True)
+        spec = synth.config(args.config)
+        print(json.dumps(measure_sampling(spec, full_graph(spec, dev), dev, args)), flush=True)
+        return 0
+    if args.featureless_only:
+        from paper_2406_06022_amd import synth
+        spec = synth.config(args.config)
+        g = full_graph(spec, dev)
+        tables = [synth.normal_table(spec.type_rows[t], spec.dims[0],
+                                     synth.torch_dtype(spec.dtype), spec.seed * 10 + t,
+                                     device=dev) if not spec.featureless[t] else None
+                  for t in range(len(spec.type_rows))]
+        print(json.dumps(measure_featureless(spec, g, tables, dev, args)), flush=True)
         return 0
     spec, mb, tables, ids, weights, stack, dy = build_stack(args.config, dev)
     log(f"workspace bytes per block {[int(w.numel()) for w in stack.workspaces]}")
@@ -747,7 +835,11 @@ def main() -> int:
                              "frac": round(ada_gbs / HBM_PEAK_GBS, 4)},
                "lr": 0.01, "eps": 1e-10}
 
-    sampling = measure_sampling(spec, dev, args)
+    g = full_graph(spec, dev)
+    sampling = measure_sampling(spec, g, dev, args)
+    featureless = measure_featureless(spec, g, tables, dev, args)
+    del g
+    torch.cuda.empty_cache()
     link_prediction = measure_lp(dev, args)
 
     out = {
@@ -779,6 +871,7 @@ def main() -> int:
         "mfma_transforms": mfma,
         "train_step_sparse_adagrad": adagrad,
         "sampling": sampling,
+        "featureless_features": featureless,
         "link_prediction": link_prediction,
         "cpu_baseline": cpu,
     }

@@ -368,6 +368,33 @@ rgcn_status rgcn_lp_loss(const rgcn_lp_batch *batch, float *loss, float *pos_sco
 rgcn_status rgcn_lp_negatives(int32_t neg_mode, int64_t slots, int64_t num_nodes, uint64_t seed,
                               int64_t *out, hipStream_t stream);
 
+/* ---------------------------------------------------------------- featureless nodes
+ * Feature construction for a node type without features (Sec. 3.3.2, eq. 1, with f the
+ * average): over the whole graph, for every node i of the type,
+ *   F'_i = mean of F_{src(r)}[j] over the in-edges (j -> i) of the given relations,
+ * each relation's source type having a feature table; an edge listed twice counts twice;
+ * F'_i = 0 when i has no such in-edge.  fp32 accumulation; bf16 output rounded to nearest
+ * even. */
+typedef struct {
+    const int64_t *indptr;     /* [num_nodes + 1] in-edge CSR over the featureless type */
+    const int64_t *indices;    /* [indptr[num_nodes]] rows of `features` */
+    const void *features;      /* [rows x ld] source feature table in the dtype, 16-byte aligned */
+    int64_t rows;
+    int64_t ld;                /* >= d, a multiple of 8 (bf16) or 4 (fp32) */
+} rgcn_feature_relation;
+
+#define RGCN_FEATURELESS_WORKSPACE 256   /* bytes of device workspace (a work counter) */
+
+/* out: [num_nodes x out_ld] in dtype (written).  d a multiple of 8 (bf16) or 4 (fp32), at
+ * most 2048 / 1024.  rels: [host][num_rels], 1 <= num_rels <= RGCN_MAX_RELS.  workspace:
+ * RGCN_FEATURELESS_WORKSPACE bytes, 256-byte aligned.  Neighbour indices outside
+ * [0, rows) are skipped (never read); with RGCN_VALIDATE_DEVICE (synchronises after the
+ * work) they are reported as RGCN_ERR_INDEX_OOB.  flags: RGCN_VALIDATE_DEVICE. */
+rgcn_status rgcn_featureless_mean(int32_t num_rels, const rgcn_feature_relation *rels,
+                                  int64_t num_nodes, int32_t d, rgcn_dtype dtype, void *out,
+                                  int64_t out_ld, void *workspace, unsigned flags,
+                                  hipStream_t stream);
+
 /* Message for the last non-OK status returned on the calling thread ("" if none). */
 const char *rgcn_last_error(void);
 

@@ -70,13 +70,6 @@ __device__ __forceinline__ uint4 ld16(const char *p) {
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-// Broadcast a 64-bit value from absolute lane `src` of the wave.
-__device__ __forceinline__ int64_t shfl64(int64_t v, int src) {
-    const int lo = __shfl((int)(uint32_t)v, src, 64);
-    const int hi = __shfl((int)(uint32_t)((uint64_t)v >> 32), src, 64);
-    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
-}
-
 // Forward segments in schedule order (heaviest first), one group of G lanes per segment,
 // persistent: group q handles segments q, q + ngroups, ...  A segment is the self-loop
 // row of a destination (copied) or the sampled in-edges of a destination row in one

@@ -1001,3 +1001,56 @@ rgcn_status rgcn_lp_negatives(int32_t neg_mode, int64_t slots, int64_t num_nodes
 }
 
 }  // extern "C"
+
+extern "C" {
+
+rgcn_status rgcn_featureless_mean(int32_t num_rels, const rgcn_feature_relation *rels,
+                                  int64_t num_nodes, int32_t d, rgcn_dtype dtype, void *out,
+                                  int64_t out_ld, void *workspace, unsigned flags,
+                                  hipStream_t stream) {
+    if (dtype != RGCN_F32 && dtype != RGCN_BF16) return fail(RGCN_ERR_DTYPE, "unknown dtype");
+    const int vec = dtype == RGCN_BF16 ? 8 : 4;
+    if (num_rels < 1 || num_rels > kMaxRels || !rels)
+        return fail(RGCN_ERR_INVALID_ARG, "num_rels %d outside [1, %d] or rels NULL", num_rels,
+                    kMaxRels);
+    if (d <= 0 || d % vec || d > 256 * vec)
+        return fail(RGCN_ERR_UNSUPPORTED, "d %d must be a positive multiple of %d, at most %d", d,
+                    vec, 256 * vec);
+    if (num_nodes < 0 || out_ld < d || out_ld % vec)
+        return fail(RGCN_ERR_SHAPE, "num_nodes negative or out_ld %lld bad", (long long)out_ld);
+    if (flags & ~(unsigned)RGCN_VALIDATE_DEVICE)
+        return fail(RGCN_ERR_INVALID_ARG, "unsupported flags 0x%x", flags);
+    if (num_nodes > 0 && (!out || !aligned16(out)))
+        return fail(RGCN_ERR_INVALID_ARG, "out NULL or not 16-byte aligned");
+    if (!workspace || ((uintptr_t)workspace & 255u))
+        return fail(RGCN_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
+    FeatArgs a;
+    memset(&a, 0, sizeof(a));
+    for (int r = 0; r < num_rels; ++r) {
+        const rgcn_feature_relation &x = rels[r];
+        if (!x.indptr || !x.indices || ((uintptr_t)x.indptr | (uintptr_t)x.indices) & 7u)
+            return fail(RGCN_ERR_INVALID_ARG, "relation %d: indptr/indices NULL or misaligned", r);
+        if (x.rows < 0 || x.ld < d || x.ld % vec || (x.rows > 0 && (!x.features ||
+                                                                    !aligned16(x.features))))
+            return fail(RGCN_ERR_SHAPE, "relation %d: feature table misaligned or ld < d", r);
+        a.rel[r] = FeatRel{x.indptr, x.indices, x.features, x.rows, x.ld};
+    }
+    a.nrel = num_rels;
+    a.d = d;
+    a.num_nodes = num_nodes;
+    a.out_ld = out_ld;
+    a.out = out;
+    a.dtype = dtype;
+    uint32_t *words = (uint32_t *)workspace;
+    TRY_HIP(featureless_mean(a, words, stream), "featureless mean");
+    if ((flags & RGCN_VALIDATE_DEVICE) && num_nodes > 0) {
+        uint32_t host = 0;
+        TRY_HIP(hipMemcpyAsync(&host, words + 1, 4, hipMemcpyDeviceToHost, stream),
+                "validate copy");
+        TRY_HIP(hipStreamSynchronize(stream), "validate sync");
+        if (host & 1u) return fail(RGCN_ERR_INDEX_OOB, "a neighbour index is out of range");
+    }
+    return RGCN_OK;
+}
+
+}  // extern "C"

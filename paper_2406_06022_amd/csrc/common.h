@@ -50,6 +50,13 @@ __device__ __forceinline__ void philox4x64(uint64_t c[4], uint64_t k0, uint64_t 
     }
 }
 
+// Broadcast a 64-bit value from absolute lane `src` of the wave.
+__device__ __forceinline__ int64_t shfl64(int64_t v, int src) {
+    const int lo = __shfl((int)(uint32_t)v, src, 64);
+    const int hi = __shfl((int)(uint32_t)((uint64_t)v >> 32), src, 64);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
 // Number of set bits of `mask` below the calling lane (wave64).
 __device__ __forceinline__ int lanes_below(uint64_t mask) {
     return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
@@ -242,6 +249,24 @@ hipError_t lp_loss(const LpArgs &a, const LpLayout &L, char *ws, float *loss, fl
 hipError_t lp_validate(const LpArgs &a, uint32_t *err, hipStream_t s);
 hipError_t lp_negatives(int32_t neg_mode, int64_t slots, int64_t num_nodes, uint64_t seed,
                         int64_t *out, hipStream_t s);
+
+// feature.hip: mean of the featured in-neighbours of every node of a featureless type
+struct FeatRel {
+    const int64_t *indptr;    // [num_nodes + 1]
+    const int64_t *indices;   // global rows of the source feature table
+    const void *feat;         // [rows x ld] in the dtype
+    int64_t rows, ld;
+};
+struct FeatArgs {
+    FeatRel rel[kMaxRels];
+    int32_t nrel, d;
+    int64_t num_nodes, out_ld;
+    void *out;
+    rgcn_dtype dtype;
+};
+// words: two device words (the work counter and the error word: bit 1 = an index out of
+// range, skipped)
+hipError_t featureless_mean(const FeatArgs &a, uint32_t *words, hipStream_t s);
 
 hipError_t pack_weights(rgcn_dtype dt, int d_in, int d_out, const void *const *w_slots,
                         int nslots, void *wcat_t, hipStream_t s);

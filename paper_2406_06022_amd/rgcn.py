@@ -32,7 +32,9 @@ EXPORTED = ("rgcn_block_workspace_size", "rgcn_block_plan_layout", "rgcn_block_p
             "rgcn_block_transform", "rgcn_block_backward_dense", "rgcn_block_backward_sparse",
             "rgcn_block_backward_sparse_adagrad", "rgcn_sparse_adagrad",
             "rgcn_sample_workspace_size", "rgcn_sample_block", "rgcn_lp_workspace_size",
-            "rgcn_lp_loss", "rgcn_lp_negatives", "rgcn_last_error", "rgcn_version")
+            "rgcn_lp_loss", "rgcn_lp_negatives", "rgcn_featureless_mean", "rgcn_last_error",
+            "rgcn_version")
+RGCN_FEATURELESS_WORKSPACE = 256
 RGCN_LP_NEG_PER_EDGE, RGCN_LP_NEG_JOINT, RGCN_LP_NEG_IN_BATCH = 0, 1, 2
 RGCN_LP_CE, RGCN_LP_WEIGHTED_CE, RGCN_LP_CONTRASTIVE = 0, 1, 2
 RGCN_MAX_FANOUT = 64
@@ -90,6 +92,11 @@ class _LpBatch(ctypes.Structure):
                 ("neg_mode", ctypes.c_int32), ("loss", ctypes.c_int32), ("batch", ctypes.c_int64),
                 ("src", ctypes.c_void_p), ("dst", ctypes.c_void_p), ("k", ctypes.c_int32),
                 ("neg", ctypes.c_void_p), ("pos_weight", ctypes.c_void_p)]
+
+
+class _FeatureRel(ctypes.Structure):
+    _fields_ = [("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p),
+                ("features", ctypes.c_void_p), ("rows", ctypes.c_int64), ("ld", ctypes.c_int64)]
 
 
 class _PlanLayout(ctypes.Structure):
@@ -153,6 +160,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.rgcn_lp_negatives.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
                                           ctypes.c_uint64, vp, vp]
         lib.rgcn_lp_negatives.restype = st
+        lib.rgcn_featureless_mean.argtypes = [ctypes.c_int32, vp, ctypes.c_int64, ctypes.c_int32,
+                                              ctypes.c_int, vp, ctypes.c_int64, vp, ctypes.c_uint,
+                                              vp]
+        lib.rgcn_featureless_mean.restype = st
         lib.rgcn_last_error.restype = ctypes.c_char_p
         lib.rgcn_version.restype = ctypes.c_char_p
         _lib = lib
@@ -506,3 +517,20 @@ def rgcn_lp_negatives(neg_mode: int, slots: int, num_nodes: int, seed: int, out:
                       stream=None) -> None:
     _check(load_library().rgcn_lp_negatives(int(neg_mode), int(slots), int(num_nodes), int(seed),
                                             out.data_ptr(), _stream(stream)))
+
+
+def rgcn_featureless_mean(rels, num_nodes: int, out: torch.Tensor,
+                          workspace: Optional[torch.Tensor] = None, flags: int = 0,
+                          stream=None) -> None:
+    """rels: list of (indptr int64, indices int64, features [rows x ld]) device tensors;
+    out: [num_nodes x >= d] in the features' dtype (d = out.shape[1])."""
+    dt = RGCN_BF16 if out.dtype == torch.bfloat16 else RGCN_F32
+    arr = (_FeatureRel * max(len(rels), 1))()
+    for i, (ip, ix, f) in enumerate(rels):
+        arr[i] = _FeatureRel(ip.data_ptr(), ix.data_ptr(), f.data_ptr(), int(f.shape[0]),
+                             int(f.stride(0)))
+    if workspace is None:
+        workspace = torch.empty(RGCN_FEATURELESS_WORKSPACE, dtype=torch.uint8, device=out.device)
+    _check(load_library().rgcn_featureless_mean(len(rels), arr, int(num_nodes), int(out.shape[1]),
+                                                dt, out.data_ptr(), int(out.stride(0)),
+                                                workspace.data_ptr(), int(flags), _stream(stream)))
