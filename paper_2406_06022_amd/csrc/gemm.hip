@@ -5,11 +5,15 @@
 //   input side   dMs_t = dY_t [n_dst x d_out]    . [W_s rows]^T, slot columns / deg
 //   weight side  dW    = Mcat_t^T [K x n_dst]    . dY_t [n_dst x d_out]   (split over rows)
 //
-// bf16 mode, v_mfma_f32_16x16x32_bf16 with fp32 accumulation, one kernel per product:
+// bf16 mode, fp32 accumulation, one kernel per product:
 //   k_gemm_dl   forward: both operands are K-contiguous bf16 rows, loaded straight from
-//               global memory into LDS, 256 x 256 tiles (8 waves of 128 x 64);
+//               global memory into LDS, 256 x 256 tiles (16 waves of 64 x 64),
+//               v_mfma_f32_16x16x32_bf16; the epilogue's bias is loaded once per tile,
+//               before the K loop;
 //   k_gemm      input side: the register-staged kernel below with 128 x 128 tiles (N is
-//               one or two slots of d_in columns; a 256-wide tile would be half empty);
+//               one or two slots of d_in columns; a 256-wide tile would be half empty),
+//               on v_mfma_f32_32x32x16_bf16 (the 16 x 16 x 32 form issues at half its
+//               rate on gfx950);
 //   k_gemm_dw2  weight side: reduces over the rows of both operands; 256 x 256 tiles whose
 //               operands sit in LDS as loaded (one row per m) and are read with the LDS
 //               transpose read.
@@ -81,6 +85,8 @@ __device__ u32x4 g_zero16[2];
 template <class TL, int FM, int FN>
 struct MmaBf16 {
     using T = TL;
+    using Acc = f32x4;                                  // one 16 x 16 accumulator
+    static constexpr int AM = FM, AN = FN;
     static constexpr int STAGE_BYTES = 2 * TL::BYTES;   // A, B
     __device__ __forceinline__ static void run(const char *As, const char *Bs,
                                                f32x4 (&acc)[FM][FN], int wm, int wn, int lane) {
@@ -109,6 +115,8 @@ struct MmaBf16 {
 template <class TL, int FM, int FN>
 struct MmaBf16SplitA {
     using T = TL;
+    using Acc = f32x4;
+    static constexpr int AM = FM, AN = FN;
     static constexpr int STAGE_BYTES = 3 * TL::BYTES;   // A_hi, B, A_lo
     __device__ __forceinline__ static void run(const char *As, const char *Bs,
                                                f32x4 (&acc)[FM][FN], int wm, int wn, int lane) {
@@ -137,12 +145,53 @@ struct MmaBf16SplitA {
     }
 };
 
+// The same split product on 32 x 32 x 16 MFMA tiles (twice the issue rate of 16 x 16 x 32
+// on gfx950): the wave's 16 x 16 grid of FM x FN fragments becomes (FM / 2) x (FN / 2)
+// accumulators of 32 x 32.  Lane l reads row l % 32 of the operand tile at K chunk
+// 2 s + l / 32 of K sub-step s (16 elements); it holds column l % 32 of each accumulator
+// and rows 8 (e / 4) + 4 (l / 32) + e % 4 for its 16 values e.
+template <class TL, int FM, int FN>
+struct MmaBf16SplitA32 {
+    using T = TL;
+    using Acc = f32x16;
+    static constexpr int AM = FM / 2, AN = FN / 2;
+    static_assert(AM * 2 == FM && AN * 2 == FN, "pairs of 16 x 16 fragments");
+    static constexpr int STAGE_BYTES = 3 * TL::BYTES;   // A_hi, B, A_lo
+    __device__ __forceinline__ static void run(const char *As, const char *Bs,
+                                               f32x16 (&acc)[AM][AN], int wm, int wn, int lane) {
+        const int r = lane & 31, h = lane >> 5;
+        const char *Al = As + 2 * TL::BYTES;
+#pragma unroll
+        for (int s = 0; s < TL::BK / 16; ++s) {
+            bf16x8 b[AN];
+#pragma unroll
+            for (int i = 0; i < AN; ++i)
+                b[i] = *(const bf16x8 *)(Bs + (wn * AN * 32 + i * 32 + r) * TL::PITCH + s * 32 + h * 16);
+#pragma unroll
+            for (int mi = 0; mi < AM; ++mi) {
+                const int ao = (wm * AM * 32 + mi * 32 + r) * TL::PITCH + s * 32 + h * 16;
+                const bf16x8 ah = *(const bf16x8 *)(As + ao);
+                const bf16x8 al = *(const bf16x8 *)(Al + ao);
+#pragma unroll
+                for (int ni = 0; ni < AN; ++ni) {
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b[ni], acc[mi][ni],
+                                                                          0, 0, 0);
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b[ni], acc[mi][ni],
+                                                                          0, 0, 0);
+                }
+            }
+        }
+    }
+};
+
 // fp32: lane group q holds k = 4q..4q+3 of its row; MFMA step s uses element s, so the
 // four steps together cover k = 0..15 (the sum over k is taken in a different order, not
 // a different set).
 template <int FM, int FN>
 struct MmaF32 {
     using T = TileF32;
+    using Acc = f32x4;
+    static constexpr int AM = FM, AN = FN;
     static constexpr int STAGE_BYTES = 2 * T::BYTES;
     __device__ __forceinline__ static void run(const char *As, const char *Bs,
                                                f32x4 (&acc)[FM][FN], int wm, int wn, int lane) {
@@ -341,26 +390,27 @@ struct EpiForward {
     __device__ __forceinline__ void operator()(int64_t m, int64_t n0, const float *v, int64_t) const {
         if (m >= M) return;
         // N is a multiple of 4: each group of 4 columns is either whole or absent.  The
-        // bias loads are issued together (clamped, then zeroed) before any is used.
-        float bq[4][4];
+        // bias loads are issued together (clamped, then zeroed) before any is used; with no
+        // bias (a uniform test) nothing is loaded.
+        float bq[4][4] = {};
+        if (bias != nullptr) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int64_t n = n0 + 4 * q;
-            const bool ok = bias != nullptr && n < N;
-            if constexpr (OUT_BF16) {
-                const uint2 w = *(const uint2 *)((const uint16_t *)(ok ? bias : (const void *)y) +
-                                                 (ok ? n : 0));
-                bq[q][0] = ok ? bf16_lo(w.x) : 0.f;
-                bq[q][1] = ok ? bf16_hi(w.x) : 0.f;
-                bq[q][2] = ok ? bf16_lo(w.y) : 0.f;
-                bq[q][3] = ok ? bf16_hi(w.y) : 0.f;
-            } else {
-                const float4 w = *(const float4 *)((const float *)(ok ? bias : (const void *)y) +
-                                                   (ok ? n : 0));
-                bq[q][0] = ok ? w.x : 0.f;
-                bq[q][1] = ok ? w.y : 0.f;
-                bq[q][2] = ok ? w.z : 0.f;
-                bq[q][3] = ok ? w.w : 0.f;
+            for (int q = 0; q < 4; ++q) {
+                const int64_t n = n0 + 4 * q;
+                const bool ok = n < N;
+                if constexpr (OUT_BF16) {
+                    const uint2 w = *(const uint2 *)((const uint16_t *)bias + (ok ? n : 0));
+                    bq[q][0] = ok ? bf16_lo(w.x) : 0.f;
+                    bq[q][1] = ok ? bf16_hi(w.x) : 0.f;
+                    bq[q][2] = ok ? bf16_lo(w.y) : 0.f;
+                    bq[q][3] = ok ? bf16_hi(w.y) : 0.f;
+                } else {
+                    const float4 w = *(const float4 *)((const float *)bias + (ok ? n : 0));
+                    bq[q][0] = ok ? w.x : 0.f;
+                    bq[q][1] = ok ? w.y : 0.f;
+                    bq[q][2] = ok ? w.z : 0.f;
+                    bq[q][3] = ok ? w.w : 0.f;
+                }
             }
         }
 #pragma unroll
@@ -381,6 +431,52 @@ struct EpiForward {
             } else {
                 *(float4 *)((float *)y + m * N + n) = make_float4(r[0], r[1], r[2], r[3]);
             }
+        }
+    }
+};
+
+// The forward epilogue of the direct-load kernel: a lane's 16 columns are the same for
+// every row it writes, so their bias is loaded once per tile, before the K loop (and not
+// at all without a bias).
+struct EpiForwardBf16 {
+    void *y;
+    const void *bias;    // bf16 [N] or NULL
+    int64_t M;
+    int32_t N;
+    int32_t relu;
+    __device__ __forceinline__ void load_bias(int64_t n0, float *bq) const {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) bq[e] = 0.f;
+        if (bias == nullptr) return;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t n = n0 + 4 * q;
+            if (n < N) {   // N is a multiple of 4
+                const uint2 w = *(const uint2 *)((const uint16_t *)bias + n);
+                bq[4 * q] = bf16_lo(w.x);
+                bq[4 * q + 1] = bf16_hi(w.x);
+                bq[4 * q + 2] = bf16_lo(w.y);
+                bq[4 * q + 3] = bf16_hi(w.y);
+            }
+        }
+    }
+    __device__ __forceinline__ void store(int64_t m, int64_t n0, const float *v,
+                                          const float *bq) const {
+        if (m >= M) return;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t n = n0 + 4 * q;
+            if (n >= N) return;
+            float r[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                r[e] = v[4 * q + e] + bq[4 * q + e];
+                if (relu) r[e] = r[e] > 0.f ? r[e] : 0.f;
+            }
+            uint2 w;
+            w.x = pack_bf16x2(r[0], r[1]);
+            w.y = pack_bf16x2(r[2], r[3]);
+            *(uint2 *)((uint16_t *)y + m * N + n) = w;
         }
     }
 };
@@ -468,11 +564,16 @@ __global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const 
         la.init(sa[r], m0);
         lb.init(sb[r], n0);
     }
-    f32x4 acc[FM][FN];
+    using Acc = typename Mma::Acc;
+    constexpr int AM = Mma::AM, AN = Mma::AN;
+    constexpr int AV = (int)(sizeof(Acc) / sizeof(float));   // values per lane per accumulator
+    Acc acc[AM][AN];
 #pragma unroll
-    for (int mi = 0; mi < FM; ++mi)
+    for (int mi = 0; mi < AM; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int ni = 0; ni < AN; ++ni)
+#pragma unroll
+            for (int e = 0; e < AV; ++e) acc[mi][ni][e] = 0.f;
 
     // Steps are padded to a multiple of R and every load is issued unconditionally
     // (steps past the range load zero tiles), so all paths through the loop have the same
@@ -505,26 +606,49 @@ __global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const 
     }
     __syncthreads();
 
-    // epilogue: per wave, 16 rows at a time through LDS, then 16 contiguous columns/lane
+    // epilogue: per wave, 16 rows at a time through the wave's own LDS area, then 16
+    // contiguous columns per lane
     float *stage = (float *)lds + wave * 16 * kStagePitch;
-    const int rq = lane >> 4, cc = lane & 15;
-#pragma unroll
-    for (int mi = 0; mi < FM; ++mi) {
-#pragma unroll
-        for (int ni = 0; ni < FN; ++ni)
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-                stage[(4 * rq + v) * kStagePitch + ni * 16 + cc] = acc[mi][ni][v];
-        __syncthreads();
-        const int r = lane >> 2, c0 = (lane & 3) * 16;
+    const int er = lane >> 2, ec = (lane & 3) * 16;
+    auto emit = [&](int64_t row) {
+        __builtin_amdgcn_wave_barrier();
         float vals[16];
 #pragma unroll
         for (int e = 0; e < 16; e += 4) {
-            const float4 x = *(const float4 *)(stage + r * kStagePitch + c0 + e);
+            const float4 x = *(const float4 *)(stage + er * kStagePitch + ec + e);
             vals[e] = x.x; vals[e + 1] = x.y; vals[e + 2] = x.z; vals[e + 3] = x.w;
         }
-        epi(m0 + wm * FM * 16 + mi * 16 + r, n0 + wn * FN * 16 + c0, vals, split);
-        __syncthreads();
+        __builtin_amdgcn_wave_barrier();
+        epi(row + er, n0 + wn * FN * 16 + ec, vals, split);
+    };
+    if constexpr (AV == 4) {
+        const int rq = lane >> 4, cc = lane & 15;
+#pragma unroll
+        for (int mi = 0; mi < AM; ++mi) {
+#pragma unroll
+            for (int ni = 0; ni < AN; ++ni)
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    stage[(4 * rq + v) * kStagePitch + ni * 16 + cc] = acc[mi][ni][v];
+            emit(m0 + wm * FM * 16 + mi * 16);
+        }
+    } else {
+        // 32 x 32 accumulators: values e = 8 hh .. 8 hh + 7 are rows 16 hh + 8 (e / 4 % 2)
+        // + 4 (lane / 32) + e % 4 of the 32-row slice
+        const int h = lane >> 5, r32 = lane & 31;
+#pragma unroll
+        for (int mi = 0; mi < AM; ++mi) {
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+                for (int ni = 0; ni < AN; ++ni)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        stage[(8 * (e / 4) + 4 * h + (e % 4)) * kStagePitch + ni * 32 + r32] =
+                            acc[mi][ni][8 * hh + e];
+                emit(m0 + wm * FM * 16 + mi * 32 + hh * 16);
+            }
+        }
     }
 }
 
@@ -564,8 +688,9 @@ __device__ __forceinline__ void vm_wait_barrier() {
     asm volatile("" ::: "memory");
 }
 
+// a 16-wave workgroup fills a CU (4 waves per SIMD, 128 registers each)
 template <class C, int BK, int S, class Epi>
-__global__ __launch_bounds__(C::NT) void k_gemm_dl(const char *__restrict__ a, int64_t lda,
+__global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_dl(const char *__restrict__ a, int64_t lda,
                                                    int64_t M, const char *__restrict__ b,
                                                    int64_t ldb, int64_t N, int64_t K,
                                                    const Epi epi, int64_t tiles_m,
@@ -633,6 +758,11 @@ __global__ __launch_bounds__(C::NT) void k_gemm_dl(const char *__restrict__ a, i
         for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     for (int st = 0; st < S - 1; ++st) issue(st);
+    // this lane's epilogue row offset and 16 columns, and their bias (its latency hidden
+    // behind the K loop)
+    const int er = lane >> 2, ec = (lane & 3) * 16;
+    float bq[16];
+    epi.load_bias(n0 + wn * FN * 16 + ec, bq);
     const int r16 = lane & 15, q = lane >> 4;
     for (int64_t it = 0; it < nk; ++it) {
         vm_wait_barrier<(S - 2) * LPS>();
@@ -654,8 +784,15 @@ __global__ __launch_bounds__(C::NT) void k_gemm_dl(const char *__restrict__ a, i
             }
         }
     }
-    vm_wait_barrier<0>();   // padded steps' loads landed; LDS free for the epilogue
+    // padded steps' loads landed and every wave's fragment reads done: LDS is free for the
+    // epilogue
+    __builtin_amdgcn_s_waitcnt(0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
 
+    // each wave transposes its 16-row slices through a staging area of its own, so only
+    // the wave's own lanes need to agree on it (LDS operations of a wave run in order)
     float *stage = (float *)lds + wave * 16 * kStagePitch;
     const int rq = lane >> 4, cc = lane & 15;
 #pragma unroll
@@ -665,16 +802,15 @@ __global__ __launch_bounds__(C::NT) void k_gemm_dl(const char *__restrict__ a, i
 #pragma unroll
             for (int v = 0; v < 4; ++v)
                 stage[(4 * rq + v) * kStagePitch + ni * 16 + cc] = acc[mi][ni][v];
-        __syncthreads();
-        const int r = lane >> 2, c0 = (lane & 3) * 16;
+        __builtin_amdgcn_wave_barrier();
         float vals[16];
 #pragma unroll
         for (int e = 0; e < 16; e += 4) {
-            const float4 x = *(const float4 *)(stage + r * kStagePitch + c0 + e);
+            const float4 x = *(const float4 *)(stage + er * kStagePitch + ec + e);
             vals[e] = x.x; vals[e + 1] = x.y; vals[e + 2] = x.z; vals[e + 3] = x.w;
         }
-        epi(m0 + wm * FM * 16 + mi * 16 + r, n0 + wn * FN * 16 + c0, vals, 0);
-        __syncthreads();
+        __builtin_amdgcn_wave_barrier();
+        epi.store(m0 + wm * FM * 16 + mi * 16 + er, n0 + wn * FN * 16 + ec, vals, bq);
     }
 }
 
@@ -913,6 +1049,16 @@ constexpr int kDwBK = 32;   // rows per K step of the bf16 weight-side kernel
 // few workgroups); the fp32 kernel fits two per CU
 constexpr int64_t kDwTargetBf16 = 256;
 constexpr int64_t kDwTargetF32 = 512;
+// forward transform: K step (elements) and LDS stages of k_gemm_dl
+#ifndef RGCN_FWD_BK
+#define RGCN_FWD_BK 64
+#endif
+#ifndef RGCN_FWD_STAGES
+#define RGCN_FWD_STAGES 2
+#endif
+#ifndef RGCN_DMS_MFMA32
+#define RGCN_DMS_MFMA32 1
+#endif
 #ifndef RGCN_GEMM_DMS_STAGES
 #define RGCN_GEMM_DMS_STAGES 1
 #endif
@@ -929,11 +1075,11 @@ hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
         using C = CfgFwd;
         const int64_t tiles_m = cdiv(M, C::TM), tiles_n = cdiv(N, C::TN);
         if (tiles_m == 0 || tiles_n == 0) return hipSuccess;
-        hipLaunchKernelGGL((k_gemm_dl<C, 64, 2, EpiForward<true>>),
+        hipLaunchKernelGGL((k_gemm_dl<C, RGCN_FWD_BK, RGCN_FWD_STAGES, EpiForwardBf16>),
                            dim3((unsigned)(tiles_m * tiles_n)), dim3(C::NT), 0, s,
                            (const char *)a, (int64_t)K * 2, M, (const char *)wcat_t,
                            (int64_t)K * 2, (int64_t)N, (int64_t)K,
-                           EpiForward<true>{y, bias, M, N, relu}, tiles_m, tiles_n);
+                           EpiForwardBf16{y, bias, M, N, relu}, tiles_m, tiles_n);
         return hipGetLastError();
     }
     using C = CfgF32;
@@ -968,8 +1114,13 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_
         using TL = TileBf16<C>;
         LoadRowsF32HiLo<TL, C::NT, 2 * TL::BYTES> la{pa, d_out};
         LoadRows<TL, C::NT, SlotRows> lb{sr, (int64_t)d_out * 2};
-        return launch_gemm<C, MmaBf16SplitA<TL, C::FM, C::FN>, decltype(la), decltype(lb), EpiDms,
-                           RGCN_GEMM_DMS_STAGES, RGCN_GEMM_DMS_R>(la, lb, epi, M, N, d_out, 1, d_out, s);
+#if RGCN_DMS_MFMA32
+        using Core = MmaBf16SplitA32<TL, C::FM, C::FN>;
+#else
+        using Core = MmaBf16SplitA<TL, C::FM, C::FN>;
+#endif
+        return launch_gemm<C, Core, decltype(la), decltype(lb), EpiDms, RGCN_GEMM_DMS_STAGES,
+                           RGCN_GEMM_DMS_R>(la, lb, epi, M, N, d_out, 1, d_out, s);
     }
     using C = CfgF32;
     using TL = TileF32;

@@ -273,6 +273,122 @@ __global__ __launch_bounds__(kThreads) void k_expand_edges(CscRels a, int64_t to
     }
 }
 
+// ---------------------------------------------------------------- CSC by placement
+// The per-key offsets are known from the counts, so each edge takes a slot of its key's
+// segment with one atomic decrement of the key's remaining count (cur, which returns to
+// zero), and the segment is then sorted by value.  Within a key the stable order is
+// ascending edge position, i.e. ascending destination row (a relation's edges are listed
+// by destination row), and edges with the same destination row have equal values, so the
+// sorted segment is the stable result whatever order the slots were taken in.
+__global__ __launch_bounds__(kThreads) void k_csc_place(const uint32_t *keys, const int32_t *vals,
+                                                        int64_t nnz, const int32_t *ip,
+                                                        int32_t *cur, int32_t *csd) {
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e >= nnz) return;
+    const uint32_t k = keys[e];
+    const int32_t slot = atomicSub(&cur[k], 1) - 1;
+    csd[ip[k] + slot] = vals[e];
+}
+
+constexpr int kSegNet = 16;        // segments up to this length: a sorting network per thread
+constexpr int kSegLds = 16384;     // longer ones up to this length: a workgroup sort in LDS
+
+__device__ __forceinline__ void cswap(int32_t &a, int32_t &b) {
+    const int32_t lo = a < b ? a : b, hi = a < b ? b : a;
+    a = lo;
+    b = hi;
+}
+
+// One thread per key: segments of 2..kSegNet values sorted in registers (bitonic network
+// over 16 slots, unused slots +inf); longer segments are queued for k_csc_sort_long.
+__global__ __launch_bounds__(kThreads) void k_csc_sort_short(const int32_t *ip, int64_t nkeys,
+                                                             int32_t *csd, int32_t *long_keys,
+                                                             uint32_t *long_count) {
+    const int64_t k = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (k >= nkeys) return;
+    const int32_t b = ip[k], n = ip[k + 1] - b;
+    if (n <= 1) return;
+    if (n == 2) {
+        int32_t x = csd[b], y = csd[b + 1];
+        if (y < x) {
+            csd[b] = y;
+            csd[b + 1] = x;
+        }
+        return;
+    }
+    if (n > kSegNet) {
+        long_keys[atomicAdd(long_count, 1u)] = (int32_t)k;
+        return;
+    }
+    int32_t v[kSegNet];
+#pragma unroll
+    for (int i = 0; i < kSegNet; ++i) v[i] = i < n ? csd[b + i] : INT32_MAX;
+#pragma unroll
+    for (int sz = 2; sz <= kSegNet; sz <<= 1)
+#pragma unroll
+        for (int st = sz >> 1; st > 0; st >>= 1)
+#pragma unroll
+            for (int i = 0; i < kSegNet; ++i) {
+                const int j = i ^ st;
+                if (j > i) {
+                    if ((i & sz) == 0) cswap(v[i], v[j]);
+                    else cswap(v[j], v[i]);
+                }
+            }
+#pragma unroll
+    for (int i = 0; i < kSegNet; ++i)
+        if (i < n) csd[b + i] = v[i];
+}
+
+// One workgroup per queued segment (grid-stride over the queue): bitonic sort of up to
+// kSegLds values in LDS.  A longer segment raises *overflow, which runs the radix sort
+// of all edges instead.
+__global__ __launch_bounds__(kThreads) void k_csc_sort_long(const int32_t *ip, int32_t *csd,
+                                                            const int32_t *long_keys,
+                                                            const uint32_t *long_count,
+                                                            uint32_t *overflow) {
+    __shared__ int32_t buf[kSegLds];
+    const uint32_t total = *long_count;
+    for (uint32_t q = blockIdx.x; q < total; q += gridDim.x) {
+        const int32_t k = long_keys[q];
+        const int32_t b = ip[k], n = ip[k + 1] - b;
+        if (n > kSegLds) {
+            if (threadIdx.x == 0) atomicOr(overflow, 1u);
+            continue;
+        }
+        int P = 1;
+        while (P < n) P <<= 1;
+        __syncthreads();
+        for (int i = threadIdx.x; i < P; i += kThreads) buf[i] = i < n ? csd[b + i] : INT32_MAX;
+        __syncthreads();
+        for (int sz = 2; sz <= P; sz <<= 1) {
+            for (int st = sz >> 1; st > 0; st >>= 1) {
+                for (int i = threadIdx.x; i < P; i += kThreads) {
+                    const int j = i ^ st;
+                    if (j > i) {
+                        const int32_t x = buf[i], y = buf[j];
+                        const bool up = (i & sz) == 0;
+                        if (up ? y < x : x < y) {
+                            buf[i] = y;
+                            buf[j] = x;
+                        }
+                    }
+                }
+                __syncthreads();
+            }
+        }
+        for (int i = threadIdx.x; i < n; i += kThreads) csd[b + i] = buf[i];
+    }
+}
+
+// dst[i] = src[i] for i < n, only when *gate is raised
+__global__ __launch_bounds__(kThreads) void k_copy_i32_gated(const int32_t *src, int32_t *dst,
+                                                             int64_t n, const uint32_t *gate) {
+    if (*gate == 0u) return;
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < n) dst[i] = src[i];
+}
+
 __global__ __launch_bounds__(kThreads) void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
     const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (i < n) p[i] = v;
@@ -477,47 +593,78 @@ size_t csc_temp_bytes(int64_t nnz, int64_t key_range) {
     const int nbk = bits <= 8 ? 256 : (1 << bits);
     const size_t sort = bucket_sort_temp_bytes(nnz, nbk);
     const size_t scan = scan_temp_bytes(key_range + 1);
-    return 3 * align_up((size_t)nnz * 4 + 4, 256) + (sort > scan ? sort : scan);
+    // values, two key buffers, sort / scan scratch, then the per-key cursors and two
+    // words (queue length, overflow flag)
+    return 3 * align_up((size_t)nnz * 4 + 4, 256) + align_up(sort > scan ? sort : scan, 256) +
+           align_up((size_t)(key_range + 3) * 4, 256);
 }
 
+// The transpose: (key, value) pairs of every edge (k_expand_edges, which also counts edges
+// per key), offsets by an exclusive scan of the counts, each edge placed in its key's
+// segment, segments sorted by value.  If some segment is longer than kSegLds, the LSD
+// radix sort of all pairs (stable, digits of at most 10 bits) runs instead, gated on a
+// device flag so the host never waits.
 hipError_t csc_build_all(const CscRels &rels, int64_t total_rows, int64_t nnz,
                          int64_t key_range, int32_t *ip, int32_t *csd, void *temp,
                          hipStream_t s) {
-    // counts per key -> exclusive scan = offsets (ip[key_range] = nnz)
-    hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)cdiv(key_range + 1, kThreads)), dim3(kThreads), 0,
-                       s, ip, key_range + 1, 0);
-    RGCN_HIP_TRY(hipGetLastError());
     int passes, bits;
     radix_plan(key_range, &passes, &bits);
     if (nnz == 0) passes = 0;
+    const int nbk = bits <= 8 ? 256 : (1 << bits);
+    const size_t sort = bucket_sort_temp_bytes(nnz, nbk);
+    const size_t scan = scan_temp_bytes(key_range + 1);
     const size_t arr = align_up((size_t)nnz * 4 + 4, 256);
     int32_t *tmp_vals = (int32_t *)temp;
     uint32_t *kb[2] = {(uint32_t *)((char *)temp + arr), (uint32_t *)((char *)temp + 2 * arr)};
-    void *sort_tmp = (char *)temp + 3 * arr;
-    int32_t *vb[2];
-    vb[passes % 2] = csd;
-    vb[(passes + 1) % 2] = tmp_vals;
+    void *sort_tmp = (char *)temp + 3 * arr;   // also the scan's scratch
+    int32_t *cur = (int32_t *)((char *)sort_tmp + align_up(sort > scan ? sort : scan, 256));
+    uint32_t *words = (uint32_t *)(cur + key_range + 1);   // queue length, overflow
+    int32_t *long_keys = (int32_t *)kb[0];                 // at most nnz / (kSegNet + 1)
+
+    // cursors and the two words start at zero
+    hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)cdiv(key_range + 3, kThreads)), dim3(kThreads),
+                       0, s, cur, key_range + 3, 0);
+    RGCN_HIP_TRY(hipGetLastError());
     if (total_rows > 0 && nnz > 0) {
         hipLaunchKernelGGL(k_expand_edges, dim3((unsigned)cdiv(total_rows, kThreads)),
-                           dim3(kThreads), 0, s, rels, total_rows, kb[1], vb[0], ip);
+                           dim3(kThreads), 0, s, rels, total_rows, kb[1], tmp_vals, cur);
         RGCN_HIP_TRY(hipGetLastError());
     }
-    void *scan_tmp = (char *)temp + 3 * arr;  // free until the radix passes start
-    RGCN_HIP_TRY(exclusive_scan_i32(ip, ip, key_range + 1, scan_tmp, s));
+    RGCN_HIP_TRY(exclusive_scan_i32(cur, ip, key_range + 1, sort_tmp, s));
+    if (nnz == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_csc_place, dim3((unsigned)cdiv(nnz, kThreads)), dim3(kThreads), 0, s,
+                       kb[1], tmp_vals, nnz, ip, cur, csd);
+    RGCN_HIP_TRY(hipGetLastError());
+    hipLaunchKernelGGL(k_csc_sort_short, dim3((unsigned)cdiv(key_range, kThreads)), dim3(kThreads),
+                       0, s, ip, key_range, csd, long_keys, words);
+    RGCN_HIP_TRY(hipGetLastError());
+    hipLaunchKernelGGL(k_csc_sort_long, dim3(512), dim3(kThreads), 0, s, ip, csd, long_keys,
+                       words, words + 1);
+    RGCN_HIP_TRY(hipGetLastError());
+
+    // fallback, gated on the overflow word: values ping-pong between tmp_vals and csd
+    // from tmp_vals; with an even number of passes they end in tmp_vals and are copied
+    const uint32_t *gate = words + 1;
     const uint32_t *keys = kb[1];
     const uint32_t mask = bits ? (uint32_t)((1u << bits) - 1u) : 0u;
+    int32_t *vb[2] = {tmp_vals, csd};
     for (int p = 0; p < passes; ++p) {
         RadixKey kf{keys, bits * p, mask};
         uint32_t *kout = kb[p % 2] == keys ? kb[(p + 1) % 2] : kb[p % 2];
         RadixPut put{keys, vb[p % 2], kout, vb[(p + 1) % 2]};
         if (bits <= 8) {
-            RGCN_HIP_TRY((bucket_sort<256, 8>(kf, put, nnz, sort_tmp, s)));
+            RGCN_HIP_TRY((bucket_sort<256, 8>(kf, put, nnz, sort_tmp, s, gate)));
         } else if (bits == 9) {
-            RGCN_HIP_TRY((bucket_sort<512, 9>(kf, put, nnz, sort_tmp, s)));
+            RGCN_HIP_TRY((bucket_sort<512, 9>(kf, put, nnz, sort_tmp, s, gate)));
         } else {
-            RGCN_HIP_TRY((bucket_sort<1024, 10>(kf, put, nnz, sort_tmp, s)));
+            RGCN_HIP_TRY((bucket_sort<1024, 10>(kf, put, nnz, sort_tmp, s, gate)));
         }
         keys = kout;
+    }
+    if (passes % 2 == 0) {
+        hipLaunchKernelGGL(k_copy_i32_gated, dim3((unsigned)cdiv(nnz, kThreads)), dim3(kThreads),
+                           0, s, tmp_vals, csd, nnz, gate);
+        RGCN_HIP_TRY(hipGetLastError());
     }
     return hipSuccess;
 }

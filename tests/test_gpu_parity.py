@@ -159,6 +159,36 @@ def test_plan_skewed_sources_bit_exact():
     assert longest > 20  # hub sources exist
 
 
+@pytest.mark.parametrize("n_src", [900, 5000, 1_200_000])
+def test_plan_csc_hubs_beyond_lds(n_src):
+    """Transpose segments of every length class: 2, up to 16, up to 16384 (sorted in LDS)
+    and one hub source with more than 16384 edges, which sends the whole transpose down the
+    radix-sort path; source counts giving 1, 2 and 3 radix passes."""
+    rng = np.random.default_rng(n_src)
+    n_dst = min(n_src, 20000)
+    per_row = max(1, -(-17000 // n_dst))          # hub-0 edges per destination row
+    rows = []
+    for i in range(n_dst):
+        e = [0] * per_row
+        if i % 4 == 0:
+            e.append(1)                            # hub 1: ~n_dst / 4 edges
+        e += rng.integers(2, n_src, size=int(rng.integers(0, 6))).tolist()
+        rng.shuffle(e)
+        rows.append(e)
+    indptr = np.zeros(n_dst + 1, dtype=np.int32)
+    np.cumsum([len(e) for e in rows], out=indptr[1:])
+    indices = np.concatenate([np.asarray(e, dtype=np.int32) for e in rows])
+    blk = synth.Block([n_src], [n_dst], [synth.Relation(0, 0, indptr, indices)])
+    print(f"case csc hubs n_src {n_src} nnz {len(indices)}", flush=True)
+    run = BlockRun(blk, "f32", 4, 8, seed=5, grad_types=[0])
+    run.run_gpu()
+    _, _, csc = _plan_arrays(run)
+    cip, cdst = csc[0]
+    want_ip, want_dst, _ = oracle.csc(n_src, indptr, indices)
+    assert int(np.diff(want_ip).max()) > 16384
+    assert np.array_equal(cip, want_ip) and np.array_equal(cdst, want_dst)
+
+
 def test_index_probe_is_exact():
     """fp32 integer features encoding the global id bytes; W_self = 0 and W_r = I, so every
     output is a gathered-row sum divided by the degree; times the degree it must equal the
