@@ -260,14 +260,25 @@ def _by_position(rows, per_step: int, skip_steps: int, steps: int):
 
 def summarize_trace(args) -> str:
     """Per-kernel time of a kernel-trace run, and the launches of --kernel by position."""
-    per, other = {}, [0, 0.0]
+    per, other, legs = {}, [0, 0.0], [0, 0.0]
     with open(args.summarize_trace, newline="") as f:
-        for r in csv.DictReader(f):
-            d = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
-            a = per.setdefault(_short_name(r["Kernel_Name"]), [0, 0.0]) \
-                if "rgcn::" in r["Kernel_Name"] else other
-            a[0] += 1
-            a[1] += d
+        rows = list(csv.DictReader(f))
+    # the measurement legs after the training steps (sampling, featureless features, link
+    # prediction) begin with the first of their kernels; library launches from then on are
+    # not part of a step
+    leg_re = re.compile(r"k_sample|k_dedup|k_fill_first|k_feature_mean|k_lp_")
+    starts = [float(r["Start_Timestamp"]) for r in rows if leg_re.search(r["Kernel_Name"])]
+    cut = min(starts) if starts else float("inf")
+    for r in rows:
+        d = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+        if "rgcn::" not in r["Kernel_Name"]:
+            a = other
+        elif float(r["Start_Timestamp"]) >= cut:
+            a = legs
+        else:
+            a = per.setdefault(_short_name(r["Kernel_Name"]), [0, 0.0])
+        a[0] += 1
+        a[1] += d
     steps = 2 * (args.steps + args.warmup)
     lines = [f"# {args.kernel}: kernel trace", "", "Command:", "", "```", args.command, "```", "",
              f"Launches of {args.kernel} by position within a step ({args.launches_per_step} "
@@ -279,7 +290,9 @@ def summarize_trace(args) -> str:
     ours = sum(v[1] for v in per.values())
     lines += ["", f"Kernels of the library over the run's {steps} steps (warmup and timed, "
               f"then as many training steps with the fused optimizer): "
-              f"{ours / 1e6:.3f} ms, {ours / steps / 1e6:.3f} ms per step.  Other kernels "
+              f"{ours / 1e6:.3f} ms, {ours / steps / 1e6:.3f} ms per step.  Library kernels "
+              f"of the measurement legs after the steps (sampling, featureless features, link "
+              f"prediction): {legs[0]} launches, {legs[1] / 1e6:.3f} ms.  Other kernels "
               f"(workload set-up: sampling, tables, weights): {other[0]} launches, "
               f"{other[1] / 1e6:.3f} ms.", "",
               "| kernel | calls | total ms | avg us | ms per step |", "|---|---:|---:|---:|---:|"]

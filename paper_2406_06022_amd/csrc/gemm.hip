@@ -849,7 +849,10 @@ __device__ __forceinline__ bf16x8 dw_frag(const char *tile, int row0, int col0, 
     return __builtin_bit_cast(bf16x8, v);
 }
 
-template <class C, int BK>
+// MFMA32: 32 x 32 x 16 tiles instead of 16 x 16 x 32 (see the input-side core): the
+// 16-lane group g of a fragment read takes columns 16 (g % 2) .. of the 32 and rows
+// 8 (g / 2) .. of the 16-row K sub-step.
+template <class C, int BK, bool MFMA32>
 __global__ __launch_bounds__(C::NT) void k_gemm_dw2(const char *__restrict__ mcat, int64_t M,
                                                     int64_t Kcat, const float *__restrict__ dy,
                                                     int64_t d_out, int64_t tiles_m,
@@ -930,11 +933,16 @@ __global__ __launch_bounds__(C::NT) void k_gemm_dw2(const char *__restrict__ mca
         }
     };
 
-    f32x4 acc[FM][FN];
+    using Acc = typename std::conditional<MFMA32, f32x16, f32x4>::type;
+    constexpr int AM = MFMA32 ? FM / 2 : FM, AN = MFMA32 ? FN / 2 : FN;
+    constexpr int AV = MFMA32 ? 16 : 4;
+    Acc acc[AM][AN];
 #pragma unroll
-    for (int mi = 0; mi < FM; ++mi)
+    for (int mi = 0; mi < AM; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int ni = 0; ni < AN; ++ni)
+#pragma unroll
+            for (int e = 0; e < AV; ++e) acc[mi][ni][e] = 0.f;
 
     const int64_t nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
     issue_a(0, lds);
@@ -949,21 +957,43 @@ __global__ __launch_bounds__(C::NT) void k_gemm_dw2(const char *__restrict__ mca
         // loads zeros into the free stage)
         issue_a(it + 1, nxt);
         load_b(it + 1);
+        if constexpr (MFMA32) {
+            const int gc = 16 * (q & 1), gr = 8 * (q >> 1);
 #pragma unroll
-        for (int s = 0; s < BK / 32; ++s) {
-            bf16x8 bh[FN], bl[FN];
+            for (int s = 0; s < BK / 16; ++s) {
+                bf16x8 bh[AN], bl[AN];
 #pragma unroll
-            for (int ni = 0; ni < FN; ++ni) {
-                bh[ni] = dw_frag<Gm>(cur + Gm::TILE, s * 32 + 8 * q, wn * FN * 16 + ni * 16, j16);
-                bl[ni] = dw_frag<Gm>(cur + 2 * Gm::TILE, s * 32 + 8 * q, wn * FN * 16 + ni * 16, j16);
+                for (int ni = 0; ni < AN; ++ni) {
+                    bh[ni] = dw_frag<Gm>(cur + Gm::TILE, s * 16 + gr, wn * FN * 16 + ni * 32 + gc, j16);
+                    bl[ni] = dw_frag<Gm>(cur + 2 * Gm::TILE, s * 16 + gr, wn * FN * 16 + ni * 32 + gc, j16);
+                }
+#pragma unroll
+                for (int mi = 0; mi < AM; ++mi) {
+                    const bf16x8 av = dw_frag<Gm>(cur, s * 16 + gr, wm * FM * 16 + mi * 32 + gc, j16);
+#pragma unroll
+                    for (int ni = 0; ni < AN; ++ni) {
+                        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bh[ni], acc[mi][ni], 0, 0, 0);
+                        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bl[ni], acc[mi][ni], 0, 0, 0);
+                    }
+                }
             }
+        } else {
 #pragma unroll
-            for (int mi = 0; mi < FM; ++mi) {
-                const bf16x8 av = dw_frag<Gm>(cur, s * 32 + 8 * q, wm * FM * 16 + mi * 16, j16);
+            for (int s = 0; s < BK / 32; ++s) {
+                bf16x8 bh[FN], bl[FN];
 #pragma unroll
                 for (int ni = 0; ni < FN; ++ni) {
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bh[ni], acc[mi][ni], 0, 0, 0);
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bl[ni], acc[mi][ni], 0, 0, 0);
+                    bh[ni] = dw_frag<Gm>(cur + Gm::TILE, s * 32 + 8 * q, wn * FN * 16 + ni * 16, j16);
+                    bl[ni] = dw_frag<Gm>(cur + 2 * Gm::TILE, s * 32 + 8 * q, wn * FN * 16 + ni * 16, j16);
+                }
+#pragma unroll
+                for (int mi = 0; mi < FM; ++mi) {
+                    const bf16x8 av = dw_frag<Gm>(cur, s * 32 + 8 * q, wm * FM * 16 + mi * 16, j16);
+#pragma unroll
+                    for (int ni = 0; ni < FN; ++ni) {
+                        acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bh[ni], acc[mi][ni], 0, 0, 0);
+                        acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bl[ni], acc[mi][ni], 0, 0, 0);
+                    }
                 }
             }
         }
@@ -971,25 +1001,47 @@ __global__ __launch_bounds__(C::NT) void k_gemm_dw2(const char *__restrict__ mca
         __syncthreads();   // waits for this wave's A loads and LDS stores, then all waves
     }
 
+    // epilogue: per wave, 16 rows at a time through the wave's own LDS area (the loop's
+    // last barrier has released the stages)
     float *stage = (float *)lds + wave * 16 * kStagePitch;
-    const int rq = lane >> 4, cc = lane & 15;
-#pragma unroll
-    for (int mi = 0; mi < FM; ++mi) {
-#pragma unroll
-        for (int ni = 0; ni < FN; ++ni)
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-                stage[(4 * rq + v) * kStagePitch + ni * 16 + cc] = acc[mi][ni][v];
-        __syncthreads();
-        const int r = lane >> 2, cq = (lane & 3) * 16;
+    const int er = lane >> 2, ec = (lane & 3) * 16;
+    auto emit = [&](int64_t row) {
+        __builtin_amdgcn_wave_barrier();
         float vals[16];
 #pragma unroll
         for (int e = 0; e < 16; e += 4) {
-            const float4 x = *(const float4 *)(stage + r * kStagePitch + cq + e);
+            const float4 x = *(const float4 *)(stage + er * kStagePitch + ec + e);
             vals[e] = x.x; vals[e + 1] = x.y; vals[e + 2] = x.z; vals[e + 3] = x.w;
         }
-        epi(c0 + wm * FM * 16 + mi * 16 + r, o0 + wn * FN * 16 + cq, vals, split);
-        __syncthreads();
+        __builtin_amdgcn_wave_barrier();
+        epi(row + er, o0 + wn * FN * 16 + ec, vals, split);
+    };
+    if constexpr (MFMA32) {
+        const int h = lane >> 5, r32 = lane & 31;
+#pragma unroll
+        for (int mi = 0; mi < AM; ++mi) {
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+                for (int ni = 0; ni < AN; ++ni)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        stage[(8 * (e / 4) + 4 * h + (e % 4)) * kStagePitch + ni * 32 + r32] =
+                            acc[mi][ni][8 * hh + e];
+                emit(c0 + wm * FM * 16 + mi * 32 + hh * 16);
+            }
+        }
+    } else {
+        const int rq = lane >> 4, cc = lane & 15;
+#pragma unroll
+        for (int mi = 0; mi < FM; ++mi) {
+#pragma unroll
+            for (int ni = 0; ni < FN; ++ni)
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    stage[(4 * rq + v) * kStagePitch + ni * 16 + cc] = acc[mi][ni][v];
+            emit(c0 + wm * FM * 16 + mi * 16);
+        }
     }
 }
 
@@ -1055,6 +1107,9 @@ constexpr int64_t kDwTargetF32 = 512;
 #endif
 #ifndef RGCN_FWD_STAGES
 #define RGCN_FWD_STAGES 2
+#endif
+#ifndef RGCN_DW_MFMA32
+#define RGCN_DW_MFMA32 1
 #endif
 #ifndef RGCN_DMS_MFMA32
 #define RGCN_DMS_MFMA32 1
@@ -1156,7 +1211,8 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
     if (bf) {
         using C = CfgWide;
         const int64_t tiles_m = cdiv(Kcat, C::TM), tiles_n = cdiv(d_out, C::TN);
-        hipLaunchKernelGGL((k_gemm_dw2<C, kDwBK>), dim3((unsigned)(tiles_m * tiles_n * splits)),
+        hipLaunchKernelGGL((k_gemm_dw2<C, kDwBK, RGCN_DW_MFMA32 != 0>),
+                           dim3((unsigned)(tiles_m * tiles_n * splits)),
                            dim3(C::NT), 0, s, (const char *)mcat, M, (int64_t)Kcat, dy,
                            (int64_t)d_out, tiles_m, tiles_n, per, epi);
         RGCN_HIP_TRY(hipGetLastError());

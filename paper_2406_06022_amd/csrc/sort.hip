@@ -250,27 +250,66 @@ struct RadixPut {
 // Edges of every relation taking part in the combined transpose, as (key, value) pairs:
 // key = koff_r + source row (disjoint key ranges per relation), value = destination row;
 // relation r's edges occupy positions [E_r, E_r + nnz_r) in input order.  Also counts the
-// edges per key.  One thread per destination row of the concatenated relations.
+// edges per key.  The relations' destination rows are concatenated, and so are their
+// edges, in the same order, so the edges of 64 consecutive rows are one contiguous range:
+// a wave takes 64 rows (lane l: row x0 + l, its relation and first edge), then walks the
+// range 64 edges at a time, lane l on edge g, whose row it finds by a binary search over
+// the lanes' first edges (wave shuffles).  Index reads and key / value writes are
+// contiguous across the wave.
 __global__ __launch_bounds__(kThreads) void k_expand_edges(CscRels a, int64_t total_rows,
                                                            uint32_t *keys, int32_t *vals,
                                                            int32_t *cnt) {
-    const int64_t x = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (x >= total_rows) return;
-    int lo = 0, hi = a.count - 1;
-    while (lo < hi) {
-        int mid = (lo + hi + 1) >> 1;
-        if (a.row_base[mid] <= x) lo = mid; else hi = mid - 1;
+    __shared__ const int32_t *s_ix[kMaxRels];
+    __shared__ const int32_t *s_ip[kMaxRels];
+    __shared__ int64_t s_koff[kMaxRels], s_e0[kMaxRels], s_rb[kMaxRels];
+    for (int r = threadIdx.x; r < a.count; r += kThreads) {
+        s_ix[r] = a.indices[r];
+        s_ip[r] = a.indptr[r];
+        s_koff[r] = a.koff[r];
+        s_e0[r] = a.e0[r];
+        s_rb[r] = a.row_base[r];
     }
-    const int64_t i = x - a.row_base[lo];
-    const int32_t *ip = a.indptr[lo];
-    const int32_t *ix = a.indices[lo];
-    const int64_t koff = a.koff[lo], e0 = a.e0[lo];
-    for (int64_t k = ip[i]; k < ip[i + 1]; ++k) {
-        const uint32_t key = (uint32_t)(koff + ix[k]);
-        keys[e0 + k] = key;
-        vals[e0 + k] = (int32_t)i;
-        atomicAdd(&cnt[key], 1);
+    __syncthreads();
+    const int lane = threadIdx.x & 63;
+    const int64_t x0 = ((int64_t)blockIdx.x * kThreads + (threadIdx.x & ~63));
+    if (x0 >= total_rows) return;                       // whole wave
+    const int64_t x = x0 + lane;
+    const bool live = x < total_rows;
+    // this lane's row: relation c (last with row_base <= x), local row i, first edge eb
+    int c = 0;
+    for (int r = 1; r < a.count; ++r)
+        if (s_rb[r] <= x) c = r;
+    const int64_t i = live ? x - s_rb[c] : 0;
+    const int32_t *ip = s_ip[c];
+    const int32_t eb = live ? (int32_t)(s_e0[c] + ip[i]) : 0;
+    const int32_t ee = live ? (int32_t)(s_e0[c] + ip[i + 1]) : 0;
+    // the wave's edge range [E0, E1): first edge of row x0, end of its last live row
+    const int last = (int)((total_rows - x0 < 64 ? total_rows - x0 : 64) - 1);
+    const int32_t E0 = __shfl(eb, 0, 64), E1 = __shfl(ee, last, 64);
+    const int32_t ebs = live ? eb : INT32_MAX;          // dead lanes never match
+    for (int32_t g0 = E0; g0 < E1; g0 += 64) {
+        const int32_t g = g0 + lane;
+        int lo = 0;
+#pragma unroll
+        for (int step = 32; step >= 1; step >>= 1) {
+            const int cand = lo + step;
+            const int32_t v = __shfl(ebs, cand, 64);
+            if (v <= g) lo = cand;
+        }
+        const int cg = __shfl(c, lo, 64);
+        const int32_t ig = (int32_t)__shfl((int)i, lo, 64);
+        if (g < E1) {
+            const uint32_t key = (uint32_t)(s_koff[cg] + s_ix[cg][g - s_e0[cg]]);
+            keys[g] = key;
+            vals[g] = ig;
+            atomicAdd(&cnt[key], 1);
+        }
     }
+}
+
+__global__ __launch_bounds__(kThreads) void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < n) p[i] = v;
 }
 
 // ---------------------------------------------------------------- CSC by placement
@@ -389,10 +428,6 @@ __global__ __launch_bounds__(kThreads) void k_copy_i32_gated(const int32_t *src,
     if (i < n) dst[i] = src[i];
 }
 
-__global__ __launch_bounds__(kThreads) void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
-    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (i < n) p[i] = v;
-}
 
 // Descriptor of the segment at schedule position p (see SegDesc).
 struct DescArgs {
