@@ -59,6 +59,29 @@ def test_matches_oracle(dtype, d):
     assert torch.isnan(out_full[:, d:]).all()      # the padding is not written
 
 
+def test_many_relations():
+    """20 relations into the type (more than the 2 chunks of a 16-wide bf16 row), so the
+    lane group is as wide as the relation count; some sources with no rows at all."""
+    rng = np.random.default_rng(20)
+    srcs = [int(x) for x in rng.integers(0, 400, size=20)]
+    srcs[3] = 0
+    g = synth.random_graph(rng, [1500] + srcs, [(1 + k, 0) for k in range(20)], 0.8,
+                           heavy=2, heavy_deg=300)
+    gen = torch.Generator().manual_seed(20)
+    feats = [torch.randn((max(n, 0), 16), generator=gen).to(torch.bfloat16) for n in srcs]
+    # the library takes non-NULL index arrays: an edgeless relation passes one dummy entry
+    rels = [(torch.as_tensor(r.indptr).cuda(),
+             torch.as_tensor(r.indices if len(r.indices) else np.zeros(1, np.int64)).cuda(),
+             feats[k].cuda()) for k, r in enumerate(g.rels)]
+    out = torch.full((1500, 16), float("nan"), dtype=torch.bfloat16, device="cuda")
+    print("case featureless 20 relations", flush=True)
+    rgcn.rgcn_featureless_mean(rels, 1500, out, flags=rgcn.RGCN_VALIDATE_DEVICE)
+    torch.cuda.synchronize()
+    want = oracle.featureless_mean([(r.indptr, r.indices, to64(feats[k]) if srcs[k] else
+                                     np.zeros((0, 16))) for k, r in enumerate(g.rels)], 1500)
+    _compare(to64(out), want, "bf16")
+
+
 def test_out_of_range_reported_and_skipped():
     ip = torch.tensor([0, 2, 3], dtype=torch.int64, device="cuda")
     ix = torch.tensor([1, 7, 0], dtype=torch.int64, device="cuda")
