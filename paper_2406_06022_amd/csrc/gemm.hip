@@ -382,6 +382,7 @@ struct LoadTransF32 {
 // Each call gets 16 consecutive columns of one row.
 template <bool OUT_BF16>
 struct EpiForward {
+    static constexpr bool kPrefetch = false;
     void *y;
     const void *bias;    // block dtype, [N] or NULL
     int64_t M;
@@ -481,26 +482,33 @@ struct EpiForwardBf16 {
     }
 };
 
+// dMs rows divided by the segment's degree.  The degrees a lane's epilogue needs are read
+// before the K loop (deg_of), so the epilogue waits for no load (store).
 struct EpiDms {
+    static constexpr bool kPrefetch = true;
     float *out;
     int64_t M;
     int32_t N;
     int32_t d_in;
     const int32_t *indptr[kMaxSlots];
-    __device__ __forceinline__ void operator()(int64_t m, int64_t n0, const float *v, int64_t) const {
+    // degree of row m in the slot of column n; -1 where the slot has none (scale 1) or the
+    // element is outside the output
+    __device__ __forceinline__ int32_t deg_of(int64_t m, int64_t n) const {
+        if (m >= M || n >= N) return -1;
+        const int sl = (int)(n / d_in);
+        if (!indptr[sl]) return -1;
+        return indptr[sl][m + 1] - indptr[sl][m];
+    }
+    // columns n0 + 4 q .. + 3 take degree deg[q]
+    __device__ __forceinline__ void store(int64_t m, int64_t n0, const float *v,
+                                          const int32_t *deg) const {
         if (m >= M) return;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int64_t n = n0 + 4 * q;
             if (n >= N) return;
-            const int sl = (int)(n / d_in);
-            float scale = 1.f;
-            bool zero = false;
-            if (indptr[sl]) {
-                const int32_t deg = indptr[sl][m + 1] - indptr[sl][m];
-                zero = deg == 0;
-                scale = (float)deg;
-            }
+            const bool zero = deg[q] == 0;
+            const float scale = deg[q] > 0 ? (float)deg[q] : 1.f;
             float4 r;
             r.x = zero ? 0.f : v[4 * q + 0] / scale;
             r.y = zero ? 0.f : v[4 * q + 1] / scale;
@@ -512,6 +520,7 @@ struct EpiDms {
 };
 
 struct EpiPartial {
+    static constexpr bool kPrefetch = false;
     float *out;          // [splits][M][N]
     int64_t M;
     int32_t N;
@@ -575,6 +584,20 @@ __global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const 
 #pragma unroll
             for (int e = 0; e < AV; ++e) acc[mi][ni][e] = 0.f;
 
+    // the epilogue's per-row data (EpiDms: degrees), read before the tiles so the loads
+    // are long done when the epilogue needs them; slice e of the wave covers rows
+    // m0 + wm FM 16 + 16 e + er, the lane columns n0 + wn FN 16 + ec + 4 q
+    const int er = lane >> 2, ec = (lane & 3) * 16;
+    int32_t pdeg[FM][4];
+    if constexpr (Epi::kPrefetch) {
+#pragma unroll
+        for (int e = 0; e < FM; ++e)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                pdeg[e][q] = epi.deg_of(m0 + wm * FM * 16 + 16 * e + er,
+                                        n0 + wn * FN * 16 + ec + 4 * q);
+    }
+
     // Steps are padded to a multiple of R and every load is issued unconditionally
     // (steps past the range load zero tiles), so all paths through the loop have the same
     // loads in flight and the waits before each LDS store cover only its own register set.
@@ -609,8 +632,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const 
     // epilogue: per wave, 16 rows at a time through the wave's own LDS area, then 16
     // contiguous columns per lane
     float *stage = (float *)lds + wave * 16 * kStagePitch;
-    const int er = lane >> 2, ec = (lane & 3) * 16;
-    auto emit = [&](int64_t row) {
+    auto emit = [&](int64_t row, int slice) {
         __builtin_amdgcn_wave_barrier();
         float vals[16];
 #pragma unroll
@@ -619,7 +641,10 @@ __global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const 
             vals[e] = x.x; vals[e + 1] = x.y; vals[e + 2] = x.z; vals[e + 3] = x.w;
         }
         __builtin_amdgcn_wave_barrier();
-        epi(row + er, n0 + wn * FN * 16 + ec, vals, split);
+        if constexpr (Epi::kPrefetch)
+            epi.store(row + er, n0 + wn * FN * 16 + ec, vals, pdeg[slice]);
+        else
+            epi(row + er, n0 + wn * FN * 16 + ec, vals, split);
     };
     if constexpr (AV == 4) {
         const int rq = lane >> 4, cc = lane & 15;
@@ -630,7 +655,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const 
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
                     stage[(4 * rq + v) * kStagePitch + ni * 16 + cc] = acc[mi][ni][v];
-            emit(m0 + wm * FM * 16 + mi * 16);
+            emit(m0 + wm * FM * 16 + mi * 16, mi);
         }
     } else {
         // 32 x 32 accumulators: values e = 8 hh .. 8 hh + 7 are rows 16 hh + 8 (e / 4 % 2)
@@ -646,7 +671,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const 
                     for (int e = 0; e < 8; ++e)
                         stage[(8 * (e / 4) + 4 * h + (e % 4)) * kStagePitch + ni * 32 + r32] =
                             acc[mi][ni][8 * hh + e];
-                emit(m0 + wm * FM * 16 + mi * 32 + hh * 16);
+                emit(m0 + wm * FM * 16 + mi * 32 + hh * 16, 2 * mi + hh);
             }
         }
     }
