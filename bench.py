@@ -143,7 +143,8 @@ def algorithmic_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
         return tot
     if stage in ("sparse", "sparse_adagrad"):
         # per requested source type: transpose offsets + destination ids + one fp32 input-
-        # side row per edge, the self-loop row, and the output row (a read-add-write of
+        # side row per edge, the fp32 self-loop row, the ReLU-mask input row above the input
+        # layer (the block input, block dtype), and the fp32 output row (a read-add-write of
         # the embedding-gradient row at the input layer, else a write); with the fused
         # Adagrad step the read-add-write is of the fp32 state row and the table row
         tot = 0.0
@@ -153,6 +154,7 @@ def algorithmic_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
             ns = blk.n_src[s]
             out = 2 if layer == 0 else 1
             tot += ns * d_in * 4 * out + blk.n_dst[s] * d_in * 4 + (layer == 0) * 8 * ns
+            tot += (layer > 0) * ns * d_in * b
             if stage == "sparse_adagrad":
                 tot += ns * d_in * b * 2
             for rel in blk.rels:
