@@ -16,7 +16,7 @@
 //               rate on gfx950);
 //   k_gemm_dw2  weight side: reduces over the rows of both operands; 256 x 256 tiles whose
 //               operands sit in LDS as loaded (one row per m) and are read with the LDS
-//               transpose read.
+//               transpose read, on v_mfma_f32_32x32x16_bf16.
 // These products are skinny (K and N of a few hundred against up to millions of rows), so
 // what limits them is how often the long operand is re-read: a 256-wide tile reads it half
 // as often as a 128-wide one.  The fp32 output gradient dY enters both backward products as
@@ -82,74 +82,12 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ u32x4 g_zero16[2];
 
 // ------------------------------------------------------------------ MFMA cores
-template <class TL, int FM, int FN>
-struct MmaBf16 {
-    using T = TL;
-    using Acc = f32x4;                                  // one 16 x 16 accumulator
-    static constexpr int AM = FM, AN = FN;
-    static constexpr int STAGE_BYTES = 2 * TL::BYTES;   // A, B
-    __device__ __forceinline__ static void run(const char *As, const char *Bs,
-                                               f32x4 (&acc)[FM][FN], int wm, int wn, int lane) {
-        const int r = lane & 15, q = lane >> 4;
-#pragma unroll
-        for (int s = 0; s < TL::BK / 32; ++s) {
-            bf16x8 a[FM], b[FN];
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-                a[i] = *(const bf16x8 *)(As + (wm * FM * 16 + i * 16 + r) * TL::PITCH + s * 64 + q * 16);
-#pragma unroll
-            for (int i = 0; i < FN; ++i)
-                b[i] = *(const bf16x8 *)(Bs + (wn * FN * 16 + i * 16 + r) * TL::PITCH + s * 64 + q * 16);
-#pragma unroll
-            for (int mi = 0; mi < FM; ++mi)
-#pragma unroll
-                for (int ni = 0; ni < FN; ++ni)
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], b[ni],
-                                                                          acc[mi][ni], 0, 0, 0);
-        }
-    }
-};
-
 // A held as two bf16 tiles (hi at As, lo two tiles further, after B) of one fp32 operand:
-// acc += A_hi.B + A_lo.B, fp32 accumulation.
-template <class TL, int FM, int FN>
-struct MmaBf16SplitA {
-    using T = TL;
-    using Acc = f32x4;
-    static constexpr int AM = FM, AN = FN;
-    static constexpr int STAGE_BYTES = 3 * TL::BYTES;   // A_hi, B, A_lo
-    __device__ __forceinline__ static void run(const char *As, const char *Bs,
-                                               f32x4 (&acc)[FM][FN], int wm, int wn, int lane) {
-        const int r = lane & 15, q = lane >> 4;
-        const char *Al = As + 2 * TL::BYTES;
-#pragma unroll
-        for (int s = 0; s < TL::BK / 32; ++s) {
-            bf16x8 b[FN];
-#pragma unroll
-            for (int i = 0; i < FN; ++i)
-                b[i] = *(const bf16x8 *)(Bs + (wn * FN * 16 + i * 16 + r) * TL::PITCH + s * 64 + q * 16);
-#pragma unroll
-            for (int mi = 0; mi < FM; ++mi) {
-                const int ao = (wm * FM * 16 + mi * 16 + r) * TL::PITCH + s * 64 + q * 16;
-                const bf16x8 ah = *(const bf16x8 *)(As + ao);
-                const bf16x8 al = *(const bf16x8 *)(Al + ao);
-#pragma unroll
-                for (int ni = 0; ni < FN; ++ni) {
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b[ni], acc[mi][ni],
-                                                                          0, 0, 0);
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b[ni], acc[mi][ni],
-                                                                          0, 0, 0);
-                }
-            }
-        }
-    }
-};
-
-// The same split product on 32 x 32 x 16 MFMA tiles (twice the issue rate of 16 x 16 x 32
-// on gfx950): the wave's 16 x 16 grid of FM x FN fragments becomes (FM / 2) x (FN / 2)
-// accumulators of 32 x 32.  Lane l reads row l % 32 of the operand tile at K chunk
-// 2 s + l / 32 of K sub-step s (16 elements); it holds column l % 32 of each accumulator
-// and rows 8 (e / 4) + 4 (l / 32) + e % 4 for its 16 values e.
+// acc += A_hi.B + A_lo.B, fp32 accumulation, on 32 x 32 x 16 MFMA tiles (the 16 x 16 x 32
+// form issues at half the rate on gfx950): the wave's 16 x 16 grid of FM x FN fragments
+// is (FM / 2) x (FN / 2) accumulators of 32 x 32.  Lane l reads row l % 32 of the operand
+// tile at K chunk 2 s + l / 32 of K sub-step s (16 elements); it holds column l % 32 of
+// each accumulator and rows 8 (e / 4) + 4 (l / 32) + e % 4 for its 16 values e.
 template <class TL, int FM, int FN>
 struct MmaBf16SplitA32 {
     using T = TL;
@@ -874,10 +812,9 @@ __device__ __forceinline__ bf16x8 dw_frag(const char *tile, int row0, int col0, 
     return __builtin_bit_cast(bf16x8, v);
 }
 
-// MFMA32: 32 x 32 x 16 tiles instead of 16 x 16 x 32 (see the input-side core): the
-// 16-lane group g of a fragment read takes columns 16 (g % 2) .. of the 32 and rows
-// 8 (g / 2) .. of the 16-row K sub-step.
-template <class C, int BK, bool MFMA32>
+// 32 x 32 x 16 MFMA tiles (see the input-side core): the 16-lane group g of a fragment
+// read takes columns 16 (g % 2) .. of the 32 and rows 8 (g / 2) .. of the 16-row K sub-step.
+template <class C, int BK>
 __global__ __launch_bounds__(C::NT) void k_gemm_dw2(const char *__restrict__ mcat, int64_t M,
                                                     int64_t Kcat, const float *__restrict__ dy,
                                                     int64_t d_out, int64_t tiles_m,
@@ -958,16 +895,14 @@ __global__ __launch_bounds__(C::NT) void k_gemm_dw2(const char *__restrict__ mca
         }
     };
 
-    using Acc = typename std::conditional<MFMA32, f32x16, f32x4>::type;
-    constexpr int AM = MFMA32 ? FM / 2 : FM, AN = MFMA32 ? FN / 2 : FN;
-    constexpr int AV = MFMA32 ? 16 : 4;
-    Acc acc[AM][AN];
+    constexpr int AM = FM / 2, AN = FN / 2;
+    f32x16 acc[AM][AN];
 #pragma unroll
     for (int mi = 0; mi < AM; ++mi)
 #pragma unroll
         for (int ni = 0; ni < AN; ++ni)
 #pragma unroll
-            for (int e = 0; e < AV; ++e) acc[mi][ni][e] = 0.f;
+            for (int e = 0; e < 16; ++e) acc[mi][ni][e] = 0.f;
 
     const int64_t nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
     issue_a(0, lds);
@@ -982,43 +917,22 @@ __global__ __launch_bounds__(C::NT) void k_gemm_dw2(const char *__restrict__ mca
         // loads zeros into the free stage)
         issue_a(it + 1, nxt);
         load_b(it + 1);
-        if constexpr (MFMA32) {
-            const int gc = 16 * (q & 1), gr = 8 * (q >> 1);
+        const int gc = 16 * (q & 1), gr = 8 * (q >> 1);
 #pragma unroll
-            for (int s = 0; s < BK / 16; ++s) {
-                bf16x8 bh[AN], bl[AN];
+        for (int s = 0; s < BK / 16; ++s) {
+            bf16x8 bh[AN], bl[AN];
+#pragma unroll
+            for (int ni = 0; ni < AN; ++ni) {
+                bh[ni] = dw_frag<Gm>(cur + Gm::TILE, s * 16 + gr, wn * FN * 16 + ni * 32 + gc, j16);
+                bl[ni] = dw_frag<Gm>(cur + 2 * Gm::TILE, s * 16 + gr, wn * FN * 16 + ni * 32 + gc, j16);
+            }
+#pragma unroll
+            for (int mi = 0; mi < AM; ++mi) {
+                const bf16x8 av = dw_frag<Gm>(cur, s * 16 + gr, wm * FM * 16 + mi * 32 + gc, j16);
 #pragma unroll
                 for (int ni = 0; ni < AN; ++ni) {
-                    bh[ni] = dw_frag<Gm>(cur + Gm::TILE, s * 16 + gr, wn * FN * 16 + ni * 32 + gc, j16);
-                    bl[ni] = dw_frag<Gm>(cur + 2 * Gm::TILE, s * 16 + gr, wn * FN * 16 + ni * 32 + gc, j16);
-                }
-#pragma unroll
-                for (int mi = 0; mi < AM; ++mi) {
-                    const bf16x8 av = dw_frag<Gm>(cur, s * 16 + gr, wm * FM * 16 + mi * 32 + gc, j16);
-#pragma unroll
-                    for (int ni = 0; ni < AN; ++ni) {
-                        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bh[ni], acc[mi][ni], 0, 0, 0);
-                        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bl[ni], acc[mi][ni], 0, 0, 0);
-                    }
-                }
-            }
-        } else {
-#pragma unroll
-            for (int s = 0; s < BK / 32; ++s) {
-                bf16x8 bh[FN], bl[FN];
-#pragma unroll
-                for (int ni = 0; ni < FN; ++ni) {
-                    bh[ni] = dw_frag<Gm>(cur + Gm::TILE, s * 32 + 8 * q, wn * FN * 16 + ni * 16, j16);
-                    bl[ni] = dw_frag<Gm>(cur + 2 * Gm::TILE, s * 32 + 8 * q, wn * FN * 16 + ni * 16, j16);
-                }
-#pragma unroll
-                for (int mi = 0; mi < FM; ++mi) {
-                    const bf16x8 av = dw_frag<Gm>(cur, s * 32 + 8 * q, wm * FM * 16 + mi * 16, j16);
-#pragma unroll
-                    for (int ni = 0; ni < FN; ++ni) {
-                        acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bh[ni], acc[mi][ni], 0, 0, 0);
-                        acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bl[ni], acc[mi][ni], 0, 0, 0);
-                    }
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bh[ni], acc[mi][ni], 0, 0, 0);
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bl[ni], acc[mi][ni], 0, 0, 0);
                 }
             }
         }
@@ -1041,31 +955,18 @@ __global__ __launch_bounds__(C::NT) void k_gemm_dw2(const char *__restrict__ mca
         __builtin_amdgcn_wave_barrier();
         epi(row + er, o0 + wn * FN * 16 + ec, vals, split);
     };
-    if constexpr (MFMA32) {
-        const int h = lane >> 5, r32 = lane & 31;
+    const int h = lane >> 5, r32 = lane & 31;
 #pragma unroll
-        for (int mi = 0; mi < AM; ++mi) {
+    for (int mi = 0; mi < AM; ++mi) {
 #pragma unroll
-            for (int hh = 0; hh < 2; ++hh) {
+        for (int hh = 0; hh < 2; ++hh) {
 #pragma unroll
-                for (int ni = 0; ni < AN; ++ni)
+            for (int ni = 0; ni < AN; ++ni)
 #pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        stage[(8 * (e / 4) + 4 * h + (e % 4)) * kStagePitch + ni * 32 + r32] =
-                            acc[mi][ni][8 * hh + e];
-                emit(c0 + wm * FM * 16 + mi * 32 + hh * 16);
-            }
-        }
-    } else {
-        const int rq = lane >> 4, cc = lane & 15;
-#pragma unroll
-        for (int mi = 0; mi < FM; ++mi) {
-#pragma unroll
-            for (int ni = 0; ni < FN; ++ni)
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    stage[(4 * rq + v) * kStagePitch + ni * 16 + cc] = acc[mi][ni][v];
-            emit(c0 + wm * FM * 16 + mi * 16);
+                for (int e = 0; e < 8; ++e)
+                    stage[(8 * (e / 4) + 4 * h + (e % 4)) * kStagePitch + ni * 32 + r32] =
+                        acc[mi][ni][8 * hh + e];
+            emit(c0 + wm * FM * 16 + mi * 32 + hh * 16);
         }
     }
 }
@@ -1133,12 +1034,6 @@ constexpr int64_t kDwTargetF32 = 512;
 #ifndef RGCN_FWD_STAGES
 #define RGCN_FWD_STAGES 2
 #endif
-#ifndef RGCN_DW_MFMA32
-#define RGCN_DW_MFMA32 1
-#endif
-#ifndef RGCN_DMS_MFMA32
-#define RGCN_DMS_MFMA32 1
-#endif
 #ifndef RGCN_GEMM_DMS_STAGES
 #define RGCN_GEMM_DMS_STAGES 1
 #endif
@@ -1194,11 +1089,7 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_
         using TL = TileBf16<C>;
         LoadRowsF32HiLo<TL, C::NT, 2 * TL::BYTES> la{pa, d_out};
         LoadRows<TL, C::NT, SlotRows> lb{sr, (int64_t)d_out * 2};
-#if RGCN_DMS_MFMA32
         using Core = MmaBf16SplitA32<TL, C::FM, C::FN>;
-#else
-        using Core = MmaBf16SplitA<TL, C::FM, C::FN>;
-#endif
         return launch_gemm<C, Core, decltype(la), decltype(lb), EpiDms, RGCN_GEMM_DMS_STAGES,
                            RGCN_GEMM_DMS_R>(la, lb, epi, M, N, d_out, 1, d_out, s);
     }
@@ -1236,7 +1127,7 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
     if (bf) {
         using C = CfgWide;
         const int64_t tiles_m = cdiv(Kcat, C::TM), tiles_n = cdiv(d_out, C::TN);
-        hipLaunchKernelGGL((k_gemm_dw2<C, kDwBK, RGCN_DW_MFMA32 != 0>),
+        hipLaunchKernelGGL((k_gemm_dw2<C, kDwBK>),
                            dim3((unsigned)(tiles_m * tiles_n * splits)),
                            dim3(C::NT), 0, s, (const char *)mcat, M, (int64_t)Kcat, dy,
                            (int64_t)d_out, tiles_m, tiles_n, per, epi);
