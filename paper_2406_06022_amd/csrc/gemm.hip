@@ -6,10 +6,10 @@
 //   weight side  dW    = Mcat_t^T [K x n_dst]    . dY_t [n_dst x d_out]   (split over rows)
 //
 // bf16 mode, fp32 accumulation, one kernel per product:
-//   k_gemm_dl   forward: both operands are K-contiguous bf16 rows, loaded straight from
+//   k_gemm_fwd  forward: both operands are K-contiguous bf16 rows, loaded straight from
 //               global memory into LDS, 256 x 256 tiles (16 waves of 64 x 64),
-//               v_mfma_f32_16x16x32_bf16; the epilogue's bias is loaded once per tile,
-//               before the K loop;
+//               v_mfma_f32_16x16x32_bf16; persistent, one K-step pipeline across a
+//               workgroup's tiles, epilogue stored from registers;
 //   k_gemm      input side: the register-staged kernel below with 128 x 128 tiles (N is
 //               one or two slots of d_in columns; a 256-wide tile would be half empty),
 //               on v_mfma_f32_32x32x16_bf16 (the 16 x 16 x 32 form issues at half its
@@ -374,49 +374,35 @@ struct EpiForward {
     }
 };
 
-// The forward epilogue of the direct-load kernel: a lane's 16 columns are the same for
-// every row it writes, so their bias is loaded once per tile, before the K loop (and not
-// at all without a bias).
+// The forward epilogue of the persistent kernel: 4 consecutive columns of one row per call,
+// their bias loaded only when there is one.
 struct EpiForwardBf16 {
     void *y;
     const void *bias;    // bf16 [N] or NULL
     int64_t M;
     int32_t N;
     int32_t relu;
-    __device__ __forceinline__ void load_bias(int64_t n0, float *bq) const {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) bq[e] = 0.f;
-        if (bias == nullptr) return;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int64_t n = n0 + 4 * q;
-            if (n < N) {   // N is a multiple of 4
-                const uint2 w = *(const uint2 *)((const uint16_t *)bias + n);
-                bq[4 * q] = bf16_lo(w.x);
-                bq[4 * q + 1] = bf16_hi(w.x);
-                bq[4 * q + 2] = bf16_lo(w.y);
-                bq[4 * q + 3] = bf16_hi(w.y);
-            }
-        }
+    // 4 columns from n (N is a multiple of 4: whole or absent)
+    __device__ __forceinline__ void load_bias4(int64_t n, float *bq) const {
+        bq[0] = bq[1] = bq[2] = bq[3] = 0.f;
+        if (bias == nullptr || n >= N) return;
+        const uint2 w = *(const uint2 *)((const uint16_t *)bias + n);
+        bq[0] = bf16_lo(w.x);
+        bq[1] = bf16_hi(w.x);
+        bq[2] = bf16_lo(w.y);
+        bq[3] = bf16_hi(w.y);
     }
-    __device__ __forceinline__ void store(int64_t m, int64_t n0, const float *v,
-                                          const float *bq) const {
-        if (m >= M) return;
+    __device__ __forceinline__ void store4(int64_t m, int64_t n, const f32x4 v,
+                                           const float *bq) const {
+        if (m >= M || n >= N) return;
+        float r[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int64_t n = n0 + 4 * q;
-            if (n >= N) return;
-            float r[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                r[e] = v[4 * q + e] + bq[4 * q + e];
-                if (relu) r[e] = r[e] > 0.f ? r[e] : 0.f;
-            }
-            uint2 w;
-            w.x = pack_bf16x2(r[0], r[1]);
-            w.y = pack_bf16x2(r[2], r[3]);
-            *(uint2 *)((uint16_t *)y + m * N + n) = w;
+        for (int e = 0; e < 4; ++e) {
+            r[e] = v[e] + bq[e];
+            if (relu) r[e] = r[e] > 0.f ? r[e] : 0.f;
         }
+        *(uint2 *)((uint16_t *)y + m * N + n) = make_uint2(pack_bf16x2(r[0], r[1]),
+                                                            pack_bf16x2(r[2], r[3]));
     }
 };
 
@@ -651,86 +637,106 @@ __device__ __forceinline__ void vm_wait_barrier() {
     asm volatile("" ::: "memory");
 }
 
-// a 16-wave workgroup fills a CU (4 waves per SIMD, 128 registers each)
-template <class C, int BK, int S, class Epi>
-__global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_dl(const char *__restrict__ a, int64_t lda,
-                                                   int64_t M, const char *__restrict__ b,
-                                                   int64_t ldb, int64_t N, int64_t K,
-                                                   const Epi epi, int64_t tiles_m,
-                                                   int64_t tiles_n) {
+// The forward product as a persistent kernel: one workgroup per CU walks a sequence of
+// output tiles with one K-step pipeline across them, so the first steps of the next tile
+// are in flight while the current tile's epilogue stores its results.  XCD x (workgroups
+// b with b % 8 == x) takes a contiguous range of the tiles, its workgroups the tiles
+// lo + j, lo + j + (workgroups per XCD), ..., so the two column halves of a row block are
+// worked on at the same time on the same XCD and share its L2.  The MFMA operands are
+// swapped (weights as the first operand), which leaves each lane 4 consecutive output
+// columns of one row: the epilogue stores straight from registers, and LDS holds only the
+// pipeline stages.  Steps past the last tile load zero tiles, so every step issues the
+// same loads; everything lands before a workgroup exits.
+template <class C, int BK, int S>
+__global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
+    const char *__restrict__ a, int64_t lda, int64_t M, const char *__restrict__ b,
+    int64_t ldb, int64_t N, int64_t K, const EpiForwardBf16 epi, int64_t tiles_m,
+    int64_t tiles_n) {
     using Gm = DlGeom<BK>;
     constexpr int FM = C::FM, FN = C::FN, NW = C::NT / 64;
     constexpr int A_BYTES = C::TM * Gm::RB, B_BYTES = C::TN * Gm::RB;
     constexpr int STAGE = A_BYTES + B_BYTES;
-    constexpr int IA = C::TM / Gm::RPI / NW, IB = C::TN / Gm::RPI / NW;   // loads per wave
+    constexpr int IA = C::TM / Gm::RPI / NW, IB = C::TN / Gm::RPI / NW;
     static_assert(IA * Gm::RPI * NW == C::TM && IB * Gm::RPI * NW == C::TN, "whole instructions");
-    constexpr int LPS = IA + IB;                                          // per step
+    constexpr int LPS = IA + IB;
     static_assert((S - 2) * LPS < 64 && S >= 2, "vmcnt range");
     __shared__ __attribute__((aligned(1024))) char lds[S * STAGE];
-    static_assert(S * STAGE >= NW * 16 * kStagePitch * 4, "epilogue staging space");
 
-    const int64_t t = xcd_major_id(blockIdx.x, (int64_t)gridDim.x);
-    const int64_t tm = t / tiles_n, tn = t - tm * tiles_n;
-    const int64_t m0 = tm * C::TM, n0 = tn * C::TN;
+    const int64_t T = tiles_m * tiles_n;
+    const int64_t wpx = (int64_t)gridDim.x / 8;          // workgroups per XCD (grid % 8 == 0)
+    const int64_t per = (T + 7) / 8;
+    const int64_t x = blockIdx.x % 8, jx = blockIdx.x / 8;
+    const int64_t lo = x * per + jx, hi = (x + 1) * per < T ? (x + 1) * per : T;
+    const int64_t ntile = lo < hi ? (hi - lo + wpx - 1) / wpx : 0;
+    const int64_t nk = (K + BK - 1) / BK;
+    const int64_t nsteps = ntile * nk;
+
     const int lane = threadIdx.x & 63;
-    // the wave index is uniform; as a scalar it makes every LDS destination a scalar too
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int wm = wave / C::WN, wn = wave % C::WN;
     const char *zp = (const char *)g_zero16;
-    asm volatile("" : "+v"(zp));   // computed once, kept in registers
-
-    // this lane's rows and chunks in each load instruction (fixed over K)
+    asm volatile("" : "+v"(zp));
     const int lr = lane / Gm::CPR, ls = lane % Gm::CPR;
-    const char *pa[IA];
-    const char *pb[IB];
-    int ca[IA], cb[IB];
+    int ra[IA], rb[IB], ca[IA], cb[IB];
 #pragma unroll
     for (int j = 0; j < IA; ++j) {
-        const int r = (wave * IA + j) * Gm::RPI + lr;
-        ca[j] = ls ^ Gm::swz(r);
-        pa[j] = m0 + r < M ? a + (m0 + r) * lda : nullptr;
+        ra[j] = (wave * IA + j) * Gm::RPI + lr;
+        ca[j] = ls ^ Gm::swz(ra[j]);
     }
 #pragma unroll
     for (int j = 0; j < IB; ++j) {
-        const int r = (wave * IB + j) * Gm::RPI + lr;
-        cb[j] = ls ^ Gm::swz(r);
-        pb[j] = n0 + r < N ? b + (n0 + r) * ldb : nullptr;
+        rb[j] = (wave * IB + j) * Gm::RPI + lr;
+        cb[j] = ls ^ Gm::swz(rb[j]);
     }
-    const int64_t nk = (K + BK - 1) / BK;
-    auto issue = [&](int64_t step) {
-        char *st = lds + (int)(step % S) * STAGE;
-        const int64_t k0 = step * BK;
+    // issue cursor: the step the next issue() loads (tile it_t, K step it_k)
+    int64_t it_t = 0, it_k = 0, im0 = 0, in0 = 0;
+    auto tile_origin = [&](int64_t ti, int64_t &m0, int64_t &n0) {
+        const int64_t t = lo + ti * wpx;
+        const int64_t tm = t / tiles_n;
+        m0 = tm * C::TM;
+        n0 = (t - tm * tiles_n) * C::TN;
+    };
+    if (ntile > 0) tile_origin(0, im0, in0);
+    int64_t gs_issue = 0;
+    auto issue = [&]() {
+        char *st = lds + (int)(gs_issue % S) * STAGE;
+        const bool live = it_t < ntile;
+        const int64_t k0 = it_k * BK;
 #pragma unroll
         for (int j = 0; j < IA; ++j) {
-            const int64_t k = k0 + ca[j] * 8;
-            const char *g = (pa[j] && k < K) ? pa[j] + k * 2 : zp;
+            const int64_t k = k0 + ca[j] * 8, m = im0 + ra[j];
+            const char *g = (live && m < M && k < K) ? a + m * lda + k * 2 : zp;
             lds_dma16(g, st + (wave * IA + j) * 1024);
         }
 #pragma unroll
         for (int j = 0; j < IB; ++j) {
-            const int64_t k = k0 + cb[j] * 8;
-            const char *g = (pb[j] && k < K) ? pb[j] + k * 2 : zp;
+            const int64_t k = k0 + cb[j] * 8, n = in0 + rb[j];
+            const char *g = (live && n < N && k < K) ? b + n * ldb + k * 2 : zp;
             lds_dma16(g, st + A_BYTES + (wave * IB + j) * 1024);
+        }
+        ++gs_issue;
+        if (++it_k == nk) {
+            it_k = 0;
+            ++it_t;
+            if (it_t < ntile) tile_origin(it_t, im0, in0);
         }
     };
 
     f32x4 acc[FM][FN];
-#pragma unroll
-    for (int mi = 0; mi < FM; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    for (int st = 0; st < S - 1; ++st) issue(st);
-    // this lane's epilogue row offset and 16 columns, and their bias (its latency hidden
-    // behind the K loop)
-    const int er = lane >> 2, ec = (lane & 3) * 16;
-    float bq[16];
-    epi.load_bias(n0 + wn * FN * 16 + ec, bq);
+    for (int st = 0; st < S - 1; ++st) issue();
     const int r16 = lane & 15, q = lane >> 4;
-    for (int64_t it = 0; it < nk; ++it) {
+    int64_t m0 = 0, n0 = 0, ti = 0, kk = 0;
+    for (int64_t gs = 0; gs < nsteps; ++gs) {
+        if (kk == 0) {
+            tile_origin(ti, m0, n0);
+#pragma unroll
+            for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
         vm_wait_barrier<(S - 2) * LPS>();
-        issue(it + S - 1);
-        const char *As = lds + (int)(it % S) * STAGE;
+        issue();
+        const char *As = lds + (int)(gs % S) * STAGE;
         const char *Bs = As + A_BYTES;
 #pragma unroll
         for (int s = 0; s < BK / 32; ++s) {
@@ -743,38 +749,28 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_dl(const char *__re
                 const bf16x8 av = *(const bf16x8 *)(As + Gm::off(wm * FM * 16 + mi * 16 + r16, s * 4 + q));
 #pragma unroll
                 for (int ni = 0; ni < FN; ++ni)
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv[ni], acc[mi][ni], 0, 0, 0);
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bv[ni], av, acc[mi][ni], 0, 0, 0);
             }
         }
-    }
-    // padded steps' loads landed and every wave's fragment reads done: LDS is free for the
-    // epilogue
-    __builtin_amdgcn_s_waitcnt(0);
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-
-    // each wave transposes its 16-row slices through a staging area of its own, so only
-    // the wave's own lanes need to agree on it (LDS operations of a wave run in order)
-    float *stage = (float *)lds + wave * 16 * kStagePitch;
-    const int rq = lane >> 4, cc = lane & 15;
+        if (kk == nk - 1) {
+            // lane: row m0 + wm FM 16 + 16 mi + (lane % 16), columns n0 + wn FN 16 + 16 ni +
+            // 4 (lane / 16) .. + 3
 #pragma unroll
-    for (int mi = 0; mi < FM; ++mi) {
+            for (int ni = 0; ni < FN; ++ni) {
+                const int64_t n = n0 + wn * FN * 16 + ni * 16 + 4 * q;
+                float bq[4];
+                epi.load_bias4(n, bq);
 #pragma unroll
-        for (int ni = 0; ni < FN; ++ni)
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-                stage[(4 * rq + v) * kStagePitch + ni * 16 + cc] = acc[mi][ni][v];
-        __builtin_amdgcn_wave_barrier();
-        float vals[16];
-#pragma unroll
-        for (int e = 0; e < 16; e += 4) {
-            const float4 x = *(const float4 *)(stage + er * kStagePitch + ec + e);
-            vals[e] = x.x; vals[e + 1] = x.y; vals[e + 2] = x.z; vals[e + 3] = x.w;
+                for (int mi = 0; mi < FM; ++mi)
+                    epi.store4(m0 + wm * FM * 16 + mi * 16 + r16, n, acc[mi][ni], bq);
+            }
         }
-        __builtin_amdgcn_wave_barrier();
-        epi.store(m0 + wm * FM * 16 + mi * 16 + er, n0 + wn * FN * 16 + ec, vals, bq);
+        if (++kk == nk) {
+            kk = 0;
+            ++ti;
+        }
     }
+    __builtin_amdgcn_s_waitcnt(0);   // padded steps' loads landed before the workgroup exits
 }
 
 // ------------------------------------------------------------------ weight side
@@ -1027,7 +1023,21 @@ constexpr int kDwBK = 32;   // rows per K step of the bf16 weight-side kernel
 // few workgroups); the fp32 kernel fits two per CU
 constexpr int64_t kDwTargetBf16 = 256;
 constexpr int64_t kDwTargetF32 = 512;
-// forward transform: K step (elements) and LDS stages of k_gemm_dl
+// compute units of the current device (cached per device)
+int64_t device_cus() {
+    static int64_t cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cache[dev] == 0) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            cus = 256;
+        cache[dev] = cus;
+    }
+    return cache[dev];
+}
+// forward transform: K step (elements) and LDS stages of k_gemm_fwd
 #ifndef RGCN_FWD_BK
 #define RGCN_FWD_BK 64
 #endif
@@ -1050,10 +1060,14 @@ hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
         using C = CfgFwd;
         const int64_t tiles_m = cdiv(M, C::TM), tiles_n = cdiv(N, C::TN);
         if (tiles_m == 0 || tiles_n == 0) return hipSuccess;
-        hipLaunchKernelGGL((k_gemm_dl<C, RGCN_FWD_BK, RGCN_FWD_STAGES, EpiForwardBf16>),
-                           dim3((unsigned)(tiles_m * tiles_n)), dim3(C::NT), 0, s,
-                           (const char *)a, (int64_t)K * 2, M, (const char *)wcat_t,
-                           (int64_t)K * 2, (int64_t)N, (int64_t)K,
+        // one workgroup per CU (a multiple of 8 so every XCD has the same count)
+        int64_t P = tiles_m * tiles_n;
+        const int64_t cus = device_cus();
+        if (P > cus) P = cus;
+        P = (P + 7) / 8 * 8;
+        hipLaunchKernelGGL((k_gemm_fwd<C, RGCN_FWD_BK, RGCN_FWD_STAGES>), dim3((unsigned)P),
+                           dim3(C::NT), 0, s, (const char *)a, (int64_t)K * 2, M,
+                           (const char *)wcat_t, (int64_t)K * 2, (int64_t)N, (int64_t)K,
                            EpiForwardBf16{y, bias, M, N, relu}, tiles_m, tiles_n);
         return hipGetLastError();
     }
