@@ -219,9 +219,11 @@ __global__ __launch_bounds__(kThreads) void k_lp_sum(const float *lossp, int64_t
 // Shared negatives as dense products, per group of positives (joint: K positives and
 // their K shared rows; in-batch: all B positives and the B destination rows):
 //   S_g = U_g Hn_g^T,  dU_g = G_g Hn_g,  dHn_g = G_g^T U_g.
-// A generic batched fp32 tile product C = A B^T over strided operands: 64 x 64 tiles,
-// K steps of 16 through LDS, 4 x 4 outputs per thread.  Rows of A (or the reduction, for
-// dHn) that lie past the batch in a group's last tile are left out.
+// A generic batched fp32 tile product C = A B^T over strided operands: 32 x 32 tiles, one
+// wave each (a batch of 1,024 positives makes 1,024 tiles, four per CU), K steps of 16
+// through LDS, fp32 MFMA.  Rows of A (or the reduction, for dHn) that lie past the batch
+// in a group's last tile are left out.
+constexpr int kLpTile = 32;
 struct LpGemm {
     const float *A, *B;
     float *C;
@@ -232,7 +234,7 @@ struct LpGemm {
     int32_t pos_dim;   // 0: M counts positives; 2: K counts positives; -1: neither
 };
 
-__global__ __launch_bounds__(kThreads) void k_lp_gemm(LpGemm g) {
+__global__ __launch_bounds__(64) void k_lp_gemm(LpGemm g) {
     const int64_t grp = blockIdx.z;
     int64_t M = g.M, K = g.K;
     if (g.pos_dim >= 0) {
@@ -240,46 +242,53 @@ __global__ __launch_bounds__(kThreads) void k_lp_gemm(LpGemm g) {
         const int64_t lim = rest < g.pos_per_group ? rest : g.pos_per_group;
         if (g.pos_dim == 0) M = lim; else K = lim;
     }
-    const int64_t m0 = (int64_t)blockIdx.y * 64, n0 = (int64_t)blockIdx.x * 64;
+    const int64_t m0 = (int64_t)blockIdx.y * kLpTile, n0 = (int64_t)blockIdx.x * kLpTile;
     if (m0 >= M) return;   // the whole workgroup leaves together
     const float *A = g.A + grp * g.bsa;
     const float *B = g.B + grp * g.bsb;
     float *C = g.C + grp * g.bsc;
-    __shared__ float As[16][65], Bs[16][65];
-    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-    float acc[4][4] = {};
-    for (int64_t k0 = 0; k0 < K; k0 += 16) {
+    __shared__ float As[16][kLpTile + 1], Bs[16][kLpTile + 1];
+    // one wave per 32 x 32 tile on fp32 MFMA tiles of 32 x 32 x 2: lane l supplies row
+    // l % 32 of the A slice and column l % 32 of the B slice at k = l / 32, and holds
+    // column l % 32, rows 8 (e / 4) + 4 (l / 32) + e % 4 of the result.  The next K step's
+    // operands are loaded into registers while the current one is multiplied.
+    const int lane = threadIdx.x, l32 = lane & 31, kh = lane >> 5;
+    float ra[8], rb[8];
+    auto load = [&](int64_t k0) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int idx = threadIdx.x + q * kThreads;
+        for (int q = 0; q < 8; ++q) {
+            const int idx = lane + q * 64;
             const int r = idx >> 4, kk = idx & 15;
             const int64_t m = m0 + r, n = n0 + r, k = k0 + kk;
-            As[kk][r] = (m < M && k < K) ? A[m * g.sam + k * g.sak] : 0.f;
-            Bs[kk][r] = (n < g.N && k < K) ? B[n * g.sbn + k * g.sbk] : 0.f;
+            ra[q] = (m < M && k < K) ? A[m * g.sam + k * g.sak] : 0.f;
+            rb[q] = (n < g.N && k < K) ? B[n * g.sbn + k * g.sbk] : 0.f;
+        }
+    };
+    f32x16 acc;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+    load(0);
+    for (int64_t k0 = 0; k0 < K; k0 += 16) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int idx = lane + q * 64;
+            As[idx & 15][idx >> 4] = ra[q];
+            Bs[idx & 15][idx >> 4] = rb[q];
         }
         __syncthreads();
+        if (k0 + 16 < K) load(k0 + 16);
 #pragma unroll
-        for (int kk = 0; kk < 16; ++kk) {
-            float av[4], bv[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                av[u] = As[kk][ty * 4 + u];
-                bv[u] = Bs[kk][tx * 4 + u];
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) acc[u][v] += av[u] * bv[v];
-        }
+        for (int kp = 0; kp < 8; ++kp)
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[2 * kp + kh][l32], Bs[2 * kp + kh][l32],
+                                                       acc, 0, 0, 0);
         __syncthreads();
     }
+    const int64_t n = n0 + l32;
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int64_t m = m0 + ty * 4 + u, n = n0 + tx * 4 + v;
-            if (m < M && n < g.N) C[m * g.scm + n * g.scn] = acc[u][v];
-        }
+    for (int e = 0; e < 16; ++e) {
+        const int64_t m = m0 + 8 * (e / 4) + 4 * kh + (e % 4);
+        if (m < M && n < g.N) C[m * g.scm + n * g.scn] = acc[e];
+    }
 }
 
 // Row of shared-negative column c: joint neg[c], in-batch dst[c].
@@ -510,8 +519,8 @@ hipError_t dispatch_finish(const LpArgs &a, const float *gpos, const float *Gm, 
 
 hipError_t gemm(const LpGemm &g, int64_t groups, hipStream_t s) {
     if (groups == 0 || g.M == 0 || g.N == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_lp_gemm, dim3((unsigned)cdiv(g.N, 64), (unsigned)cdiv(g.M, 64),
-                                       (unsigned)groups), dim3(kThreads), 0, s, g);
+    hipLaunchKernelGGL(k_lp_gemm, dim3((unsigned)cdiv(g.N, kLpTile), (unsigned)cdiv(g.M, kLpTile),
+                                       (unsigned)groups), dim3(64), 0, s, g);
     return hipGetLastError();
 }
 
