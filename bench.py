@@ -175,6 +175,23 @@ def transform_flops(spec, blk, layer: int) -> float:
     return tot
 
 
+def backward_flops(spec, blk, grad_src_types: int, layer: int) -> float:
+    """Flops of a block's dense backward products as the method defines them: the weight
+    gradients (the forward product's flops) and the input-side products dMs = dY W^T for the
+    self slot of every type whose input gradient is requested and every relation whose
+    source type's is (the hi / lo split of dY doubles the MFMA work; it is not counted)."""
+    d_in, d_out = spec.dims[layer], spec.dims[layer + 1]
+    tot = transform_flops(spec, blk, layer)
+    for t in range(len(blk.n_src)):
+        if blk.n_dst[t] == 0:
+            continue
+        slots = 1 if grad_src_types >> t & 1 else 0
+        slots += sum(1 for rel in blk.rels
+                     if rel.dst_type == t and grad_src_types >> rel.src_type & 1)
+        tot += 2.0 * blk.n_dst[t] * slots * d_in * d_out
+    return tot
+
+
 def cpu_baseline(spec, mb, tables, ids, weights, budget_s: float):
     """The CPU oracle (single thread, fp64) on a bounded sample of block 0: the first n
     destination rows of every type with their full sampled segments, forward + backward
@@ -802,6 +819,12 @@ def main() -> int:
         tf = fl / (avg[("transform", l)] * 1e-3) / 1e12
         mfma[f"transform[{l}]"] = {"ms": round(avg[("transform", l)], 4), "TFLOP/s": round(tf, 1),
                                    "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)}
+    mfma_bwd = {}
+    for l in range(stack.L):
+        fl = backward_flops(spec, mb.blocks[l], stack.blocks[l].grad_src_types, l)
+        tf = fl / (avg[("dense", l)] * 1e-3) / 1e12
+        mfma_bwd[f"dense[{l}]"] = {"ms": round(avg[("dense", l)], 4), "TFLOP/s": round(tf, 1),
+                                   "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)}
 
     # attainable streaming bandwidth of this machine: a plain 1 GiB fp32 copy (read + write)
     src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
@@ -884,6 +907,7 @@ def main() -> int:
         "hbm_kernels": rooflines,
         "copy_probe_GBs": round(copy_gbs, 1),
         "mfma_transforms": mfma,
+        "mfma_backward": mfma_bwd,
         "train_step_sparse_adagrad": adagrad,
         "sampling": sampling,
         "featureless_features": featureless,
