@@ -57,7 +57,10 @@ using CfgNarrow = Cfg<128, 128, 2, 2>;
 #endif
 using CfgFwd = typename std::conditional<RGCN_FWD_WAVES == 16, Cfg<256, 256, 4, 4>, CfgWide>::type;
 using CfgDms = CfgNarrow;   // bf16 input side: N is one or two slots of d_in columns
-using CfgDw = CfgWide;      // bf16 weight side (k_gemm_dw2)
+// bf16 weight side (k_gemm_dw2): 256 x 256 tiles of 8 waves, one workgroup per CU (128 x
+// 128 tiles of 4 waves, three per CU, measured the same)
+using CfgDw = CfgWide;
+constexpr int kDwMinWaves = 2;   // per SIMD
 using CfgF32 = Cfg<128, 128, 2, 2>;
 
 template <int ROWS_, int BK_, int ES_>
@@ -783,11 +786,14 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
 // written as a hi and a lo bf16 tile, so each dY element is read once and every Mcat
 // fragment meets both parts.  512-byte LDS rows, 16-byte chunk c of row r at slot
 // c ^ 2 (r & 3): the four rows of one transpose read hit distinct banks.
-template <int BK_>
+template <int BK_, int COLS>
 struct DwGeom {
     static constexpr int BK = BK_;                 // rows (m) per K step
-    static constexpr int RB = 512;                 // bytes per LDS row (256 bf16)
+    static constexpr int RB = COLS * 2;            // bytes per LDS row (COLS bf16)
+    static constexpr int CPR = RB / 16;            // 16-byte chunks per row
+    static constexpr int RPI = 1024 / RB;          // rows per wave load instruction
     static constexpr int TILE = BK * RB;
+    static_assert(CPR >= 8, "the slot swizzle needs 8 chunks per row");
     __device__ __forceinline__ static int slot(int r, int c) { return c ^ ((r & 3) << 1); }
 };
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -810,20 +816,21 @@ __device__ __forceinline__ bf16x8 dw_frag(const char *tile, int row0, int col0, 
 
 // 32 x 32 x 16 MFMA tiles (see the input-side core): the 16-lane group g of a fragment
 // read takes columns 16 (g % 2) .. of the 32 and rows 8 (g / 2) .. of the 16-row K sub-step.
-template <class C, int BK>
-__global__ __launch_bounds__(C::NT) void k_gemm_dw2(const char *__restrict__ mcat, int64_t M,
+template <class C, int BK, int MINW>
+__global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw2(const char *__restrict__ mcat, int64_t M,
                                                     int64_t Kcat, const float *__restrict__ dy,
                                                     int64_t d_out, int64_t tiles_m,
                                                     int64_t tiles_n, int64_t per,
                                                     const EpiPartial epi) {
-    using Gm = DwGeom<BK>;
-    static_assert(C::TM == 256 && C::TN == 256, "512-byte LDS rows");
+    using Gm = DwGeom<BK, C::TM>;
+    static_assert(C::TM == C::TN, "one row geometry for both operand tiles");
     constexpr int FM = C::FM, FN = C::FN, NW = C::NT / 64;
     constexpr int STAGE = 3 * Gm::TILE;                      // A, B hi, B lo
     constexpr int IA = BK * Gm::RB / 1024 / NW;              // A loads per wave per step
     static_assert(IA * NW * 1024 == BK * Gm::RB, "whole A instructions");
-    constexpr int NB = BK * 32 / C::NT;                      // dY pieces (8 floats) per thread
-    static_assert(NB * C::NT == BK * 32, "whole B pieces");
+    constexpr int PPR = C::TN / 8;                           // dY pieces (8 floats) per row
+    constexpr int NB = BK * PPR / C::NT;                     // dY pieces per thread
+    static_assert(NB * C::NT == BK * PPR, "whole B pieces");
     __shared__ __attribute__((aligned(1024))) char lds[2 * STAGE];
     static_assert(2 * STAGE >= NW * 16 * kStagePitch * 4, "epilogue staging space");
 
@@ -842,27 +849,27 @@ __global__ __launch_bounds__(C::NT) void k_gemm_dw2(const char *__restrict__ mca
     asm volatile("" : "+v"(zp));
 
     // A (Mcat rows) straight into LDS: instruction j of this wave covers rows
-    // 2 (IA wave + j) and the next, lane L the slot L % 32 of row L / 32
-    const int ar = lane >> 5, as = lane & 31;
+    // RPI (IA wave + j) .. + RPI - 1, lane L the slot L % CPR of row L / CPR
+    const int ar = lane / Gm::CPR, as = lane % Gm::CPR;
     auto issue_a = [&](int64_t step, char *st) {
         const int64_t m0 = kb + step * BK;
 #pragma unroll
         for (int j = 0; j < IA; ++j) {
-            const int r = (wave * IA + j) * 2 + ar;
+            const int r = (wave * IA + j) * Gm::RPI + ar;
             const int c = Gm::slot(r, as);                    // the chunk that lives in slot `as`
             const int64_t m = m0 + r, col = c0 + c * 8;
             const char *g = (m < ke && col < Kcat) ? mcat + m * Kcat * 2 + col * 2 : zp;
             lds_dma16(g, st + (wave * IA + j) * 1024);
         }
     };
-    // B (dY) through registers: piece u of this thread = row p / 32, columns 8 (p % 32) ..
+    // B (dY) through registers: piece u of this thread = row p / PPR, columns 8 (p % PPR) ..
     f32x4 bq[NB][2];
     auto load_b = [&](int64_t step) {
         const int64_t m0 = kb + step * BK;
 #pragma unroll
         for (int u = 0; u < NB; ++u) {
             const int p = (int)threadIdx.x + u * C::NT;
-            const int r = p >> 5, g = p & 31;
+            const int r = p / PPR, g = p % PPR;
             const int64_t m = m0 + r, col = o0 + g * 8;
             // the zero buffer holds 32 bytes, so both halves stay in bounds either way
             const char *src = (m < ke && col < d_out) ? (const char *)(dy + m * d_out + col) : zp;
@@ -876,7 +883,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm_dw2(const char *__restrict__ mca
 #pragma unroll
         for (int u = 0; u < NB; ++u) {
             const int p = (int)threadIdx.x + u * C::NT;
-            const int r = p >> 5, g = p & 31;
+            const int r = p / PPR, g = p % PPR;
             const f32x4 x = bq[u][0], y = bq[u][1];
             u32x4 h, l;
             h.x = pack_bf16x2(x.x, x.y); h.y = pack_bf16x2(x.z, x.w);
@@ -1139,9 +1146,9 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
     }
     EpiPartial epi{partial, Kcat, d_out};
     if (bf) {
-        using C = CfgWide;
+        using C = CfgDw;
         const int64_t tiles_m = cdiv(Kcat, C::TM), tiles_n = cdiv(d_out, C::TN);
-        hipLaunchKernelGGL((k_gemm_dw2<C, kDwBK>),
+        hipLaunchKernelGGL((k_gemm_dw2<C, kDwBK, kDwMinWaves>),
                            dim3((unsigned)(tiles_m * tiles_n * splits)),
                            dim3(C::NT), 0, s, (const char *)mcat, M, (int64_t)Kcat, dy,
                            (int64_t)d_out, tiles_m, tiles_n, per, epi);
