@@ -14,15 +14,15 @@
 //               one or two slots of d_in columns; a 256-wide tile would be half empty),
 //               on v_mfma_f32_32x32x16_bf16 (the 16 x 16 x 32 form issues at half its
 //               rate on gfx950);
-//   k_gemm_dw2  weight side: reduces over the rows of both operands; 256 x 256 tiles whose
-//               operands sit in LDS as loaded (one row per m) and are read with the LDS
-//               transpose read, on v_mfma_f32_32x32x16_bf16.
+//   k_gemm_dw   weight side: reduces over the rows of both operands; 256 x 256 tiles whose
+//               operands are loaded straight into LDS (one row per m) and read down the
+//               columns, on v_mfma_f32_32x32x16_bf16.
 // These products are skinny (K and N of a few hundred against up to millions of rows), so
 // what limits them is how often the long operand is re-read: a 256-wide tile reads it half
 // as often as a 128-wide one.  The fp32 output gradient dY enters both backward products as
 // a hi + lo pair of bf16 values (hi = bf16(x), lo = bf16(x - hi)), ~16 significant bits:
-// each fp32 tile is read from memory once and written to LDS as two bf16 tiles, and every
-// fragment of the other operand meets both.
+// each fp32 tile is read from memory once and split on the way to the MFMA operands, and
+// every fragment of the other operand meets both parts.
 //
 // k_gemm (input side, and every product in fp32 mode with v_mfma_f32_16x16x4_f32): LDS
 // holds both operands K-contiguous ("row r, k..."), one row = BK elements of K + 16 bytes
@@ -57,10 +57,13 @@ using CfgNarrow = Cfg<128, 128, 2, 2>;
 #endif
 using CfgFwd = typename std::conditional<RGCN_FWD_WAVES == 16, Cfg<256, 256, 4, 4>, CfgWide>::type;
 using CfgDms = CfgNarrow;   // bf16 input side: N is one or two slots of d_in columns
-// bf16 weight side (k_gemm_dw2): 256 x 256 tiles of 8 waves, one workgroup per CU (128 x
-// 128 tiles of 4 waves, three per CU, measured the same)
-using CfgDw = CfgWide;
-constexpr int kDwMinWaves = 2;   // per SIMD
+// bf16 weight side (k_gemm_dw): 256 x 256 tiles of 8 waves, one workgroup per CU (16
+// waves of 64 x 64 measured 1 % slower)
+#ifndef RGCN_DW_WAVES
+#define RGCN_DW_WAVES 8
+#endif
+using CfgDw = typename std::conditional<RGCN_DW_WAVES == 16, Cfg<256, 256, 4, 4>, CfgWide>::type;
+constexpr int kDwMinWaves = RGCN_DW_WAVES / 4;   // per SIMD
 using CfgF32 = Cfg<128, 128, 2, 2>;
 
 template <int ROWS_, int BK_, int ES_>
@@ -780,12 +783,12 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
 // dW partial of one split: out[c][o] = sum over the split's rows m of Mcat[m][c] dY[m][o].
 // The reduction runs over rows of both operands, so both tiles sit in LDS as loaded (row
 // = one m, TM or TN consecutive columns) and the MFMA fragments, which want 8 consecutive
-// m per lane, are read with the LDS transpose read: a 16-lane group hands in sixteen
-// 8-byte pieces (four columns of one row each) and every lane gets one column of four
-// rows.  Mcat (bf16) goes straight into LDS; dY (fp32) goes through registers and is
-// written as a hi and a lo bf16 tile, so each dY element is read once and every Mcat
-// fragment meets both parts.  512-byte LDS rows, 16-byte chunk c of row r at slot
-// c ^ 2 (r & 3): the four rows of one transpose read hit distinct banks.
+// m per lane, are read down the columns: the bf16 Mcat tile with the LDS transpose read (a
+// 16-lane group hands in sixteen 8-byte pieces, four columns of one row each, and every
+// lane gets one column of four rows), the fp32 dY tile one row at a time.  Mcat tile:
+// 512-byte LDS rows, 16-byte chunk c of row r at slot c ^ SWZ (r & 3).  A transpose read
+// of 32 lanes takes 64 bytes of each of four rows; with SWZ = 4 the four rows fall in
+// distinct 64-byte bank windows.
 template <int BK_, int COLS>
 struct DwGeom {
     static constexpr int BK = BK_;                 // rows (m) per K step
@@ -793,46 +796,100 @@ struct DwGeom {
     static constexpr int CPR = RB / 16;            // 16-byte chunks per row
     static constexpr int RPI = 1024 / RB;          // rows per wave load instruction
     static constexpr int TILE = BK * RB;
-    static_assert(CPR >= 8, "the slot swizzle needs 8 chunks per row");
-    __device__ __forceinline__ static int slot(int r, int c) { return c ^ ((r & 3) << 1); }
+#ifndef RGCN_DW_SWZ
+#define RGCN_DW_SWZ 4
+#endif
+    static constexpr int SWZ = RGCN_DW_SWZ;
+    static_assert(CPR >= 4 * SWZ, "the slot swizzle stays within a row");
+    __device__ __forceinline__ static int slot(int r, int c) { return c ^ ((r & 3) * SWZ); }
 };
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
-__device__ __forceinline__ s16x4 lds_tr16(const char *p) {
-    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((s16x4 __attribute__((address_space(3))) *)p);
+// LDS transpose read from inline assembly.  Before the builtin form of this read the
+// compiler waits for every direct-to-LDS load in flight (vmcnt(0)), since it cannot tell
+// which LDS bytes they write; in a pipelined loop that stalls each step on the loads just
+// issued for the steps ahead.  The compiler does not track these reads: lds_reads_done must
+// run on the fragment before it is used.
+__device__ __forceinline__ s16x4 lds_tr16_untracked(const char *p) {
+    s16x4 v;
+    const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char *)p;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(a));
+    return v;
 }
-// Fragment of 16 columns [col0, col0 + 16) x rows [k0, k0 + 8) of a DwGeom tile for the
-// calling lane (group q = lane / 16 takes rows k0 + 8 q' where k0 already includes 8 q).
+// Fragment of 16 columns [col0, col0 + 16) x rows [row0, row0 + 8) of a DwGeom tile for
+// lane j of a 16-lane group.
 template <class Gm>
-__device__ __forceinline__ bf16x8 dw_frag(const char *tile, int row0, int col0, int j) {
+__device__ __forceinline__ bf16x8 dw_frag_untracked(const char *tile, int row0, int col0, int j) {
     const int col = col0 + 4 * (j & 3);
     const int r0 = row0 + (j >> 2), r1 = r0 + 4;
     const int c = col >> 3, byte = (col & 7) * 2;
-    const s16x4 lo = lds_tr16(tile + r0 * Gm::RB + (Gm::slot(r0, c) << 4) + byte);
-    const s16x4 hi = lds_tr16(tile + r1 * Gm::RB + (Gm::slot(r1, c) << 4) + byte);
+    const s16x4 lo = lds_tr16_untracked(tile + r0 * Gm::RB + (Gm::slot(r0, c) << 4) + byte);
+    const s16x4 hi = lds_tr16_untracked(tile + r1 * Gm::RB + (Gm::slot(r1, c) << 4) + byte);
     const s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     return __builtin_bit_cast(bf16x8, v);
 }
+// Waits until every LDS read of the wave has returned; `v` depends on the wait, so no use
+// of it is scheduled before it.
+__device__ __forceinline__ void lds_reads_done(bf16x8 &v) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v));
+}
 
-// 32 x 32 x 16 MFMA tiles (see the input-side core): the 16-lane group g of a fragment
-// read takes columns 16 (g % 2) .. of the 32 and rows 8 (g / 2) .. of the 16-row K sub-step.
-template <class C, int BK, int MINW>
-__global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw2(const char *__restrict__ mcat, int64_t M,
+// fp32 dY tile of k_gemm_dw: BK rows of COLS floats as loaded, 16-byte chunk c of row r in
+// slot c ^ 8 ((r / 8) % 2).  A fragment read takes rows r and r + 8 of the same 32 columns
+// in its two half-waves; the slot flip puts them 128 bytes apart, on disjoint banks.
+template <int BK_, int COLS>
+struct DwRawGeom {
+    static constexpr int BK = BK_;
+    static constexpr int RB = COLS * 4;            // bytes per LDS row
+    static constexpr int CPR = RB / 16;            // 16-byte chunks per row
+    static constexpr int RPI = 1024 / RB;          // rows per wave load instruction
+    static constexpr int TILE = BK * RB;
+    static_assert(CPR >= 16 && RPI >= 1, "the slot flip needs 16 chunks per row");
+    __device__ __forceinline__ static int slot(int r, int c) { return c ^ (((r >> 3) & 1) << 3); }
+};
+// B fragment of a 32 x 32 x 16 product from an fp32 tile: column `col`, rows row0 .. + 7
+// (row0 a multiple of 8), split into hi = bf16(x) and lo = bf16(x - hi) for the two
+// products that carry dY's 16 significant bits.
+template <class Gr>
+__device__ __forceinline__ void dw_raw_frag(const char *tile, int row0, int col, bf16x8 &hi,
+                                            bf16x8 &lo) {
+    const char *p = tile + row0 * Gr::RB + (Gr::slot(row0, col >> 2) << 4) + (col & 3) * 4;
+    float x[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = *(const float *)(p + i * Gr::RB);
+    u32x4 h, l;
+    h.x = pack_bf16x2(x[0], x[1]); h.y = pack_bf16x2(x[2], x[3]);
+    h.z = pack_bf16x2(x[4], x[5]); h.w = pack_bf16x2(x[6], x[7]);
+    l.x = pack_bf16x2(x[0] - bf16_lo(h.x), x[1] - bf16_hi(h.x));
+    l.y = pack_bf16x2(x[2] - bf16_lo(h.y), x[3] - bf16_hi(h.y));
+    l.z = pack_bf16x2(x[4] - bf16_lo(h.z), x[5] - bf16_hi(h.z));
+    l.w = pack_bf16x2(x[6] - bf16_lo(h.w), x[7] - bf16_hi(h.w));
+    hi = __builtin_bit_cast(bf16x8, h);
+    lo = __builtin_bit_cast(bf16x8, l);
+}
+
+// The weight-side product with both operands loaded straight into LDS (no register
+// staging), S stages deep: the loads of the next S - 1 steps are in flight while a step is
+// multiplied.  dY stays fp32 in LDS and each fragment is split into its hi and lo bf16
+// parts in registers.  32 x 32 x 16 MFMA tiles (see the input-side core): the 16-lane
+// group g of a fragment read takes columns 16 (g % 2) .. of the 32 and rows 8 (g / 2) ..
+// of the 16-row K sub-step.
+template <class C, int BK, int S, int MINW>
+__global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw(const char *__restrict__ mcat, int64_t M,
                                                     int64_t Kcat, const float *__restrict__ dy,
                                                     int64_t d_out, int64_t tiles_m,
                                                     int64_t tiles_n, int64_t per,
                                                     const EpiPartial epi) {
-    using Gm = DwGeom<BK, C::TM>;
-    static_assert(C::TM == C::TN, "one row geometry for both operand tiles");
+    using Ga = DwGeom<BK, C::TM>;
+    using Gb = DwRawGeom<BK, C::TN>;
     constexpr int FM = C::FM, FN = C::FN, NW = C::NT / 64;
-    constexpr int STAGE = 3 * Gm::TILE;                      // A, B hi, B lo
-    constexpr int IA = BK * Gm::RB / 1024 / NW;              // A loads per wave per step
-    static_assert(IA * NW * 1024 == BK * Gm::RB, "whole A instructions");
-    constexpr int PPR = C::TN / 8;                           // dY pieces (8 floats) per row
-    constexpr int NB = BK * PPR / C::NT;                     // dY pieces per thread
-    static_assert(NB * C::NT == BK * PPR, "whole B pieces");
-    __shared__ __attribute__((aligned(1024))) char lds[2 * STAGE];
-    static_assert(2 * STAGE >= NW * 16 * kStagePitch * 4, "epilogue staging space");
+    constexpr int STAGE = Ga::TILE + Gb::TILE;
+    constexpr int IA = BK / Ga::RPI / NW, IB = BK / Gb::RPI / NW;   // loads per wave per step
+    static_assert(IA * Ga::RPI * NW == BK && IB * Gb::RPI * NW == BK, "whole instructions");
+    constexpr int LPS = IA + IB;
+    static_assert(S >= 2 && (S - 2) * LPS < 64, "vmcnt range");
+    __shared__ __attribute__((aligned(1024))) char lds[S * STAGE];
+    static_assert(S * STAGE >= NW * 16 * kStagePitch * 4, "epilogue staging space");
 
     const int64_t logical = xcd_major_id(blockIdx.x, (int64_t)gridDim.x);
     const int64_t tiles = tiles_m * tiles_n;
@@ -848,53 +905,25 @@ __global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw2(const char *__restrict
     const char *zp = (const char *)g_zero16;
     asm volatile("" : "+v"(zp));
 
-    // A (Mcat rows) straight into LDS: instruction j of this wave covers rows
-    // RPI (IA wave + j) .. + RPI - 1, lane L the slot L % CPR of row L / CPR
-    const int ar = lane / Gm::CPR, as = lane % Gm::CPR;
-    auto issue_a = [&](int64_t step, char *st) {
+    // instruction j of this wave: A rows RPI (IA wave + j) .., B rows RPI (IB wave + j) ..;
+    // lane L fills slot L % CPR of row L / CPR with the chunk that belongs there
+    const int64_t nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+    auto issue = [&](int64_t step) {
+        char *st = lds + (int)(step % S) * STAGE;
         const int64_t m0 = kb + step * BK;
 #pragma unroll
         for (int j = 0; j < IA; ++j) {
-            const int r = (wave * IA + j) * Gm::RPI + ar;
-            const int c = Gm::slot(r, as);                    // the chunk that lives in slot `as`
-            const int64_t m = m0 + r, col = c0 + c * 8;
+            const int r = (wave * IA + j) * Ga::RPI + lane / Ga::CPR;
+            const int64_t m = m0 + r, col = c0 + Ga::slot(r, lane % Ga::CPR) * 8;
             const char *g = (m < ke && col < Kcat) ? mcat + m * Kcat * 2 + col * 2 : zp;
             lds_dma16(g, st + (wave * IA + j) * 1024);
         }
-    };
-    // B (dY) through registers: piece u of this thread = row p / PPR, columns 8 (p % PPR) ..
-    f32x4 bq[NB][2];
-    auto load_b = [&](int64_t step) {
-        const int64_t m0 = kb + step * BK;
 #pragma unroll
-        for (int u = 0; u < NB; ++u) {
-            const int p = (int)threadIdx.x + u * C::NT;
-            const int r = p / PPR, g = p % PPR;
-            const int64_t m = m0 + r, col = o0 + g * 8;
-            // the zero buffer holds 32 bytes, so both halves stay in bounds either way
-            const char *src = (m < ke && col < d_out) ? (const char *)(dy + m * d_out + col) : zp;
-            const __attribute__((address_space(1))) f32x4 *gs =
-                (const __attribute__((address_space(1))) f32x4 *)src;
-            bq[u][0] = gs[0];
-            bq[u][1] = gs[1];
-        }
-    };
-    auto store_b = [&](char *st) {
-#pragma unroll
-        for (int u = 0; u < NB; ++u) {
-            const int p = (int)threadIdx.x + u * C::NT;
-            const int r = p / PPR, g = p % PPR;
-            const f32x4 x = bq[u][0], y = bq[u][1];
-            u32x4 h, l;
-            h.x = pack_bf16x2(x.x, x.y); h.y = pack_bf16x2(x.z, x.w);
-            h.z = pack_bf16x2(y.x, y.y); h.w = pack_bf16x2(y.z, y.w);
-            l.x = pack_bf16x2(x.x - bf16_lo(h.x), x.y - bf16_hi(h.x));
-            l.y = pack_bf16x2(x.z - bf16_lo(h.y), x.w - bf16_hi(h.y));
-            l.z = pack_bf16x2(y.x - bf16_lo(h.z), y.y - bf16_hi(h.z));
-            l.w = pack_bf16x2(y.z - bf16_lo(h.w), y.w - bf16_hi(h.w));
-            const int off = r * Gm::RB + (Gm::slot(r, g) << 4);
-            *(u32x4 *)(st + Gm::TILE + off) = h;
-            *(u32x4 *)(st + 2 * Gm::TILE + off) = l;
+        for (int j = 0; j < IB; ++j) {
+            const int r = (wave * IB + j) * Gb::RPI + lane / Gb::CPR;
+            const int64_t m = m0 + r, col = o0 + Gb::slot(r, lane % Gb::CPR) * 4;
+            const char *g = (m < ke && col < d_out) ? (const char *)(dy + m * d_out + col) : zp;
+            lds_dma16(g, st + Ga::TILE + (wave * IB + j) * 1024);
         }
     };
 
@@ -907,44 +936,47 @@ __global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw2(const char *__restrict
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[mi][ni][e] = 0.f;
 
-    const int64_t nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
-    issue_a(0, lds);
-    load_b(0);
-    store_b(lds);
-    __syncthreads();
+    for (int st = 0; st < S - 1; ++st)
+        if (st < nk) issue(st);
     const int j16 = lane & 15, q = lane >> 4;
+    const int gc = 16 * (q & 1), gr = 8 * (q >> 1);
     for (int64_t it = 0; it < nk; ++it) {
-        char *cur = lds + (int)(it & 1) * STAGE;
-        char *nxt = lds + (int)((it + 1) & 1) * STAGE;
-        // next step's tiles in flight while this one is multiplied (a step past the end
-        // loads zeros into the free stage)
-        issue_a(it + 1, nxt);
-        load_b(it + 1);
-        const int gc = 16 * (q & 1), gr = 8 * (q >> 1);
+        // this step's tiles have landed in every wave, and every wave is done with the stage
+        // the next issue overwrites (the loads of later steps stay in flight)
+        if (it + S - 2 < nk)
+            vm_wait_barrier<(S - 2) * LPS>();
+        else
+            vm_wait_barrier<0>();
+        if (it + S - 1 < nk) issue(it + S - 1);
+        const char *As = lds + (int)(it % S) * STAGE;
+        const char *Bs = As + Ga::TILE;
 #pragma unroll
         for (int s = 0; s < BK / 16; ++s) {
             bf16x8 bh[AN], bl[AN];
 #pragma unroll
-            for (int ni = 0; ni < AN; ++ni) {
-                bh[ni] = dw_frag<Gm>(cur + Gm::TILE, s * 16 + gr, wn * FN * 16 + ni * 32 + gc, j16);
-                bl[ni] = dw_frag<Gm>(cur + 2 * Gm::TILE, s * 16 + gr, wn * FN * 16 + ni * 32 + gc, j16);
-            }
+            for (int ni = 0; ni < AN; ++ni)
+                dw_raw_frag<Gb>(Bs, s * 16 + 8 * (lane >> 5), wn * FN * 16 + ni * 32 + (lane & 31),
+                                bh[ni], bl[ni]);
+            bf16x8 av[AM];
+#pragma unroll
+            for (int mi = 0; mi < AM; ++mi)
+                av[mi] = dw_frag_untracked<Ga>(As, s * 16 + gr, wm * FM * 16 + mi * 32 + gc, j16);
+#pragma unroll
+            for (int mi = 0; mi < AM; ++mi) lds_reads_done(av[mi]);
 #pragma unroll
             for (int mi = 0; mi < AM; ++mi) {
-                const bf16x8 av = dw_frag<Gm>(cur, s * 16 + gr, wm * FM * 16 + mi * 32 + gc, j16);
 #pragma unroll
                 for (int ni = 0; ni < AN; ++ni) {
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bh[ni], acc[mi][ni], 0, 0, 0);
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bl[ni], acc[mi][ni], 0, 0, 0);
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[mi], bh[ni], acc[mi][ni], 0, 0, 0);
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[mi], bl[ni], acc[mi][ni], 0, 0, 0);
                 }
             }
         }
-        store_b(nxt);
-        __syncthreads();   // waits for this wave's A loads and LDS stores, then all waves
     }
+    // every load has landed (the last steps wait for all) and every wave is done with the
+    // stages before the epilogue reuses them
+    __syncthreads();
 
-    // epilogue: per wave, 16 rows at a time through the wave's own LDS area (the loop's
-    // last barrier has released the stages)
     float *stage = (float *)lds + wave * 16 * kStagePitch;
     const int er = lane >> 2, ec = (lane & 3) * 16;
     auto emit = [&](int64_t row) {
@@ -1025,6 +1057,9 @@ __global__ __launch_bounds__(kThreads) void k_zero_outputs(DwOut out, int d_in, 
 }
 
 constexpr int kDwBK = 32;   // rows per K step of the bf16 weight-side kernel
+#ifndef RGCN_DW_STAGES
+#define RGCN_DW_STAGES 2     // LDS stages of k_gemm_dw (three measured 2 % slower)
+#endif
 // workgroups of one weight-side product: the bf16 kernel holds a CU by itself (96 KB of
 // LDS), so one per CU of the 256 (a 2.02-wave grid left most CUs idle behind its last
 // few workgroups); the fp32 kernel fits two per CU
@@ -1148,7 +1183,7 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
     if (bf) {
         using C = CfgDw;
         const int64_t tiles_m = cdiv(Kcat, C::TM), tiles_n = cdiv(d_out, C::TN);
-        hipLaunchKernelGGL((k_gemm_dw2<C, kDwBK, kDwMinWaves>),
+        hipLaunchKernelGGL((k_gemm_dw<C, kDwBK, RGCN_DW_STAGES, kDwMinWaves>),
                            dim3((unsigned)(tiles_m * tiles_n * splits)),
                            dim3(C::NT), 0, s, (const char *)mcat, M, (int64_t)Kcat, dy,
                            (int64_t)d_out, tiles_m, tiles_n, per, epi);
