@@ -65,6 +65,8 @@ typedef enum { RGCN_F32 = 0, RGCN_BF16 = 1 } rgcn_dtype;
 #define RGCN_IDS_UNIQUE      0x8u /* backward: the caller asserts row_ids are distinct per
                                      type, so demb rows are updated without atomics */
 #define RGCN_CLEAR_GRAD      0x10u /* rgcn_sparse_adagrad: zero the gradient rows it read */
+#define RGCN_PLAN_FORWARD    0x20u /* rgcn_block_plan: only the part the forward stages read */
+#define RGCN_PLAN_BACKWARD   0x40u /* rgcn_block_plan: only the part only the backward reads */
 
 /* One relation (canonical edge type src_type -> dst_type) of a block, as a CSR over the
  * destination rows.  indptr[0] = 0, non-decreasing, indptr[n_dst] = nnz; indices are
@@ -140,7 +142,15 @@ rgcn_status rgcn_block_plan_layout(const rgcn_block *block, const rgcn_params *p
  *  - the backward schedule: for each type in grad_src_types (ascending), a section
  *    holding that type's rows (local ids) stably sorted by 63 - min(d, 63), d the row's
  *    in-degree in the transpose summed over the relations leaving the type.
- * Only structural arrays are read.  flags: RGCN_VALIDATE_DEVICE. */
+ * Only structural arrays are read.  flags: RGCN_VALIDATE_DEVICE, RGCN_PLAN_FORWARD,
+ * RGCN_PLAN_BACKWARD.  With neither (or both) of the last two the whole plan is built.
+ * RGCN_PLAN_FORWARD builds the slot table and the forward schedule, all that
+ * rgcn_block_aggregate / rgcn_block_transform read; RGCN_PLAN_BACKWARD builds the CSC
+ * transpose and the backward schedule.  The two parts share the workspace's temporary
+ * region, so the backward part must be ordered after the forward part (same stream, or an
+ * event); the forward stages do not touch that region or anything the backward part
+ * writes, so the backward part may run on another stream while they run.  The backward
+ * stages need both parts complete. */
 rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
                             void *workspace, size_t workspace_bytes, unsigned flags,
                             hipStream_t stream);

@@ -77,6 +77,7 @@ class MiniBatchStack:
             tab = input_tables[t]
             self.demb[t] = torch.zeros((tab.shape[0], dims[0]), dtype=f32, device=device)
         self.adagrad = None   # (lr, eps, state per type) once attached
+        self._side = None     # stream of the overlapped backward plans (created on first use)
 
     def attach_adagrad(self, lr: float, eps: float) -> None:
         """Zero Adagrad state per learnable table; from now on backward steps the tables
@@ -98,14 +99,19 @@ class MiniBatchStack:
             rgcn.rgcn_block_plan(b, p, ws, flags)
             _mark(timer, ("plan", l), 1)
 
-    def forward(self, flags: int = 0, timer=None) -> List[Optional[torch.Tensor]]:
-        """Forward through all blocks (each as its aggregate and transform stages)."""
+    def forward(self, flags: int = 0, timer=None, after_first_aggregate=None
+                ) -> List[Optional[torch.Tensor]]:
+        """Forward through all blocks (each as its aggregate and transform stages).
+        after_first_aggregate, if given, is called once the first block's aggregate stage is
+        enqueued."""
         for l in range(self.L):
             f = flags | (rgcn.RGCN_FUSE_RELU if l < self.L - 1 else 0)
             _mark(timer, ("aggregate", l), 0)
             rgcn.rgcn_block_aggregate(self.blocks[l], self.inputs[l], self.params[l],
                                       self.workspaces[l], f)
             _mark(timer, ("aggregate", l), 1)
+            if l == 0 and after_first_aggregate is not None:
+                after_first_aggregate()
             _mark(timer, ("transform", l), 0)
             rgcn.rgcn_block_transform(self.blocks[l], self.params[l], self.y[l],
                                       self.workspaces[l], f & ~rgcn.RGCN_VALIDATE_DEVICE)
@@ -147,10 +153,33 @@ class MiniBatchStack:
                                                 states, lr, eps, workspace=self.workspaces[0],
                                                 flags=flags | rgcn.RGCN_IDS_UNIQUE)
 
-    def step(self, dy_top, timer=None) -> None:
-        """One pass of the whole path: plan, forward, backward."""
-        self.plan(timer=timer)
-        self.forward(timer=timer)
+    def step(self, dy_top, timer=None, overlap_plan: bool = True) -> None:
+        """One pass of the whole path: plan, forward, backward.
+
+        With overlap_plan the plan is split: the forward part of every block runs first;
+        the backward part (CSC transposes and backward schedules) runs on a second stream
+        from the end of the first block's aggregate stage, next to the MFMA-bound transforms,
+        and the backward waits for it.  Same work and results as the serial order."""
+        if not overlap_plan:
+            self.plan(timer=timer)
+            self.forward(timer=timer)
+            self.backward(dy_top, timer=timer)
+            return
+        if self._side is None:
+            self._side = torch.cuda.Stream(device=self.device)
+        main = torch.cuda.current_stream(self.device)
+
+        def backward_plans():
+            self._side.wait_stream(main)
+            with torch.cuda.stream(self._side):
+                for l, (b, p, ws) in enumerate(zip(self.blocks, self.params, self.workspaces)):
+                    _mark(timer, ("plan_bwd", l), 0)
+                    rgcn.rgcn_block_plan(b, p, ws, rgcn.RGCN_PLAN_BACKWARD)
+                    _mark(timer, ("plan_bwd", l), 1)
+
+        self.plan(rgcn.RGCN_PLAN_FORWARD, timer=timer)
+        self.forward(timer=timer, after_first_aggregate=backward_plans)
+        main.wait_stream(self._side)
         self.backward(dy_top, timer=timer)
 
 

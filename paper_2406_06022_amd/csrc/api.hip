@@ -403,15 +403,21 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
         if ((st = device_validate(block, nullptr, L, ws, stream)) != RGCN_OK) return st;
     }
     char *scratch = ws + L.off_scratch;
-    if (L.nslots > 0)
-        TRY_HIP(fill_words(ws + L.off_slots, L.slots, sizeof(FwdSlot) * L.nslots, stream),
-                "slot table");
+    unsigned parts = flags & (RGCN_PLAN_FORWARD | RGCN_PLAN_BACKWARD);
+    if (parts == 0) parts = RGCN_PLAN_FORWARD | RGCN_PLAN_BACKWARD;
+    // flag word 0 belongs to the forward schedule, words 1 + t to the backward ones
     uint32_t *sched_flag = (uint32_t *)(ws + L.off_flags);
-    {
-        const uint32_t zeros[1 + kMaxTypes] = {};
-        TRY_HIP(fill_words(sched_flag, zeros, sizeof zeros, stream), "schedule flags");
+    const uint32_t zeros[1 + kMaxTypes] = {};
+    if (parts & RGCN_PLAN_FORWARD) {
+        if (L.nslots > 0)
+            TRY_HIP(fill_words(ws + L.off_slots, L.slots, sizeof(FwdSlot) * L.nslots, stream),
+                    "slot table");
+        TRY_HIP(fill_words(sched_flag, zeros, sizeof(uint32_t), stream), "schedule flags");
     }
-    {
+    if (parts & RGCN_PLAN_BACKWARD)
+        TRY_HIP(fill_words(sched_flag + 1, zeros, sizeof(uint32_t) * kMaxTypes, stream),
+                "schedule flags");
+    if (parts & RGCN_PLAN_FORWARD) {
         int64_t moff[kMaxTypes], mld[kMaxTypes];
         for (int t = 0; t < kMaxTypes; ++t) {
             moff[t] = (t < L.T && L.off_mcat[t] != SIZE_MAX) ? (int64_t)L.off_mcat[t] : 0;
@@ -425,6 +431,7 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
         TRY_HIP(fwd_chunks(weight, L.n_seg, L.nc_max, (int32_t *)(ws + L.off_fwd_chunks), scratch,
                            stream), "forward chunks");
     }
+    if (!(parts & RGCN_PLAN_BACKWARD)) return RGCN_OK;
     if (L.key_range > 0) {
         CscRels cr{};
         int64_t rows = 0;
