@@ -241,3 +241,18 @@ def test_link_prediction_host_validation(lib):
     assert g(2, 10, 100, 1, 0x900000, None) == 1
     assert g(0, 10, 0, 1, 0x900000, None) == 2
     assert g(0, 0, 10, 1, None, None) == 0
+
+
+def test_binding_constants_match_header():
+    """Every numeric #define of the C header that the binding also names has the same value
+    there (flags, limits, workspace sizes)."""
+    import os
+    import re
+    from paper_2406_06022_amd import rgcn
+    hdr = open(os.path.join(os.path.dirname(__file__), "..", "include", "rgcn.h")).read()
+    seen = 0
+    for name, val in re.findall(r"^#define\s+(RGCN_\w+)\s+\(?(0x[0-9a-fA-F]+|\d+)u?\)?", hdr, re.M):
+        if hasattr(rgcn, name):
+            assert getattr(rgcn, name) == int(val, 0), name
+            seen += 1
+    assert seen >= 8 and rgcn.RGCN_PLAN_FORWARD != rgcn.RGCN_PLAN_BACKWARD
