@@ -67,6 +67,9 @@ typedef enum { RGCN_F32 = 0, RGCN_BF16 = 1 } rgcn_dtype;
 #define RGCN_CLEAR_GRAD      0x10u /* rgcn_sparse_adagrad: zero the gradient rows it read */
 #define RGCN_PLAN_FORWARD    0x20u /* rgcn_block_plan: only the part the forward stages read */
 #define RGCN_PLAN_BACKWARD   0x40u /* rgcn_block_plan: only the part only the backward reads */
+#define RGCN_PLAN_ENUMERATION_ORDER 0x80u /* rgcn_block_plan: keep both schedules in
+                                     enumeration order (no degree sort); every result is
+                                     bit-identical, only the processing order changes */
 
 /* One relation (canonical edge type src_type -> dst_type) of a block, as a CSR over the
  * destination rows.  indptr[0] = 0, non-decreasing, indptr[n_dst] = nnz; indices are
@@ -113,7 +116,8 @@ typedef struct {
  * An offset of SIZE_MAX means "not built". */
 typedef struct {
     int64_t n_fwd_segments;                 /* forward segments (self-loop + relation rows) */
-    size_t fwd_order;                       /* int32 [n_fwd_segments]: segment ids, heaviest first */
+    size_t fwd_order;                       /* int32 [n_fwd_segments]: segment ids in processing
+                                               order (a permutation; see rgcn_block_plan) */
     int64_t n_bwd_rows;                     /* source rows of the types in grad_src_types */
     size_t bwd_order;                       /* int32 [n_bwd_rows] */
     size_t csc_indptr[RGCN_MAX_RELS];       /* int32 [n_src[src_type] + 1]: csc_indptr[j+1] -
@@ -134,16 +138,26 @@ rgcn_status rgcn_block_plan_layout(const rgcn_block *block, const rgcn_params *p
                                    rgcn_plan_layout *layout /* [host] */);
 
 /* Integer plan of a block (exact, deterministic):
- *  - the forward schedule: segments (self-loop rows, then each relation's rows, type by
- *    type) as a stable counting sort by degree key 63 - min(deg, 63), heaviest first;
  *  - for every relation whose source type is in grad_src_types, the CSC transpose:
  *    csc_indptr and csc_dst, a stable sort of edges by source row (ascending edge
- *    position inside a source row);
- *  - the backward schedule: for each type in grad_src_types (ascending), a section
- *    holding that type's rows (local ids) stably sorted by 63 - min(d, 63), d the row's
- *    in-degree in the transpose summed over the relations leaving the type.
+ *    position inside a source row) -- the transposed adjacency the backward of the
+ *    segmented mean runs over;
+ *  - two schedules, the order in which the kernels visit work items.  They are library
+ *    policy for load balance, not part of the method: no passage of the paper defines
+ *    them, every order gives the same results bit for bit, and RGCN_PLAN_ENUMERATION_ORDER
+ *    keeps both in enumeration order.  The forward schedule is a permutation of the
+ *    forward segments, enumerated type by type (ascending): the type's self-loop rows,
+ *    then each relation into the type (ascending relation index), rows ascending.  The
+ *    backward schedule holds, for each type in grad_src_types (ascending), a section that
+ *    is a permutation of that type's rows (local ids).  The key of an item of degree d
+ *    (a segment's edge count; for a backward row, its in-degree in the transpose summed
+ *    over the relations leaving the type) is 31 for d <= 32 and max(0, 30 - (floor(log2 d)
+ *    - 5)) above; a schedule is the stable sort by ascending key, so items of more than 32
+ *    edges come first, the heaviest power of two first, and every lighter item keeps its
+ *    enumeration order.
  * Only structural arrays are read.  flags: RGCN_VALIDATE_DEVICE, RGCN_PLAN_FORWARD,
- * RGCN_PLAN_BACKWARD.  With neither (or both) of the last two the whole plan is built.
+ * RGCN_PLAN_BACKWARD, RGCN_PLAN_ENUMERATION_ORDER.  With neither (or both) of
+ * RGCN_PLAN_FORWARD and RGCN_PLAN_BACKWARD the whole plan is built.
  * RGCN_PLAN_FORWARD builds the slot table and the forward schedule, all that
  * rgcn_block_aggregate / rgcn_block_transform read; RGCN_PLAN_BACKWARD builds the CSC
  * transpose and the backward schedule.  The two parts share the workspace's temporary

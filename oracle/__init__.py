@@ -6,9 +6,10 @@ import this package.  It shares no code with the HIP library: the arithmetic liv
 arrays into it.  Block objects are duck-typed: anything with ``n_src``, ``n_dst`` and
 ``rels`` (each with ``src_type``, ``dst_type``, ``indptr``, ``indices``) is accepted.
 
-Which passage each function follows is stated in ``rgcn_oracle.c``.  The degree-sorted
-schedules are the library's documented ordering rule (a stable counting sort of
-segments by a degree key), restated here from that rule.
+Which passage each function follows is stated in ``rgcn_oracle.c``.  The order in which
+the library processes segments is library policy, not the method's arithmetic, so it has
+no counterpart here: the tests check that the library's schedules are permutations and that
+results do not depend on them.
 """
 from __future__ import annotations
 
@@ -27,18 +28,24 @@ _SRC_FEAT = os.path.join(_HERE, "feature_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
-# Schedule keys: segments of at most 32 edges share the last key; heavier segments get one
-# key per power of two of their degree, heaviest first; a stable ascending sort by key
-# lists the heavy segments first and leaves the rest in enumeration order.
-SCHED_BUCKETS = 32
+
+def _flags():
+    """gcc flags of the oracle: plain IEEE double (no fast-math, no contraction into fused
+    multiply-adds), OpenMP for the loops that hand whole output elements to one thread.
+    ORACLE_SANITIZE=1 adds AddressSanitizer and UndefinedBehaviorSanitizer (host code)."""
+    f = ["-O2", "-std=c99", "-fno-fast-math", "-ffp-contract=off", "-fopenmp"]
+    if os.environ.get("ORACLE_SANITIZE") == "1":
+        f += ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+              "-fno-omit-frame-pointer", "-g"]
+    return f
 
 
 def build(force: bool = True) -> str:
     """Compile the oracle with the host C compiler (plain IEEE double, no fast-math)."""
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp"
-        subprocess.run(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fno-fast-math",
-                        "-ffp-contract=off", _SRC, _SRC_SAMPLE, _SRC_LP, _SRC_FEAT, "-o", tmp, "-lm"], check=True)
+        subprocess.run(["gcc", *_flags(), "-fPIC", "-shared", _SRC, _SRC_SAMPLE, _SRC_LP,
+                        _SRC_FEAT, "-o", tmp, "-lm"], check=True)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
 
@@ -61,6 +68,8 @@ def _load():
             build(force=False)
         lib = ctypes.CDLL(_LIB_PATH)
         vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        lib.orc_set_threads.argtypes = [ctypes.c_int]
+        lib.orc_get_threads.restype = ctypes.c_int
         lib.orc_check_block.argtypes = [vp]
         lib.orc_check_block.restype = ctypes.c_int
         lib.orc_degrees.argtypes = [vp, i64, vp]
@@ -76,8 +85,6 @@ def _load():
         lib.orc_sparse_adagrad.restype = ctypes.c_int
         lib.orc_csc.argtypes = [i64, i64, vp, vp, vp, vp, vp]
         lib.orc_csc.restype = ctypes.c_int
-        lib.orc_stable_bucket_order.argtypes = [i64, vp, i32, vp]
-        lib.orc_stable_bucket_order.restype = ctypes.c_int
         u64 = ctypes.c_uint64
         lib.orc_philox4x64.argtypes = [vp, vp, vp]
         lib.orc_sample_draw.argtypes = [u64, u64, u64, u64, u64]
@@ -95,6 +102,15 @@ def _load():
         lib.orc_featureless_mean.restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def set_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops (results do not depend on it)."""
+    _load().orc_set_threads(int(n))
+
+
+def get_threads() -> int:
+    return int(_load().orc_get_threads())
 
 
 def _ptr(a: Optional[np.ndarray]) -> Optional[int]:
@@ -251,75 +267,6 @@ def csc(n_src: int, indptr, indices):
     if rc != 0:
         raise MemoryError
     return cip, cd[:nnz], ce[:nnz]
-
-
-def stable_bucket_order(key: np.ndarray, nbuckets: int) -> np.ndarray:
-    k = np.ascontiguousarray(key, dtype=np.int32)
-    n = k.shape[0]
-    out = np.zeros(max(n, 1), dtype=np.int32)
-    k1 = k if n else np.zeros(1, dtype=np.int32)
-    if _load().orc_stable_bucket_order(n, k1.ctypes.data, nbuckets, out.ctypes.data) != 0:
-        raise ValueError("oracle: bucket key out of range")
-    return out[:n]
-
-
-def degree_key(deg: np.ndarray) -> np.ndarray:
-    """Schedule key of a segment of degree deg: SCHED_BUCKETS - 1 for deg <= 32, else
-    SCHED_BUCKETS - 2 - (floor(log2 deg) - 5), at least 0."""
-    d = np.asarray(deg, dtype=np.int64)
-    out = np.full(d.shape, SCHED_BUCKETS - 1, dtype=np.int64)
-    heavy = d > 32
-    lg = np.floor(np.log2(np.where(heavy, d, 1).astype(np.float64))).astype(np.int64)
-    out[heavy] = np.maximum(SCHED_BUCKETS - 2 - (lg[heavy] - 5), 0)
-    return out.astype(np.int32)
-
-
-def forward_segments(block):
-    """Forward segments of a block in enumeration order.
-
-    Slots are listed destination type by destination type (ascending); each type with
-    n_dst[t] > 0 contributes its self-loop slot first (degree 1), then one slot per relation
-    into t in ascending relation order.  A segment is (slot, destination row); segment ids
-    run slot by slot, rows ascending.  Returns (slot_type, slot_rel (-1 for self),
-    slot_base, degrees) where degrees is the per-segment degree array.
-    """
-    slot_type, slot_rel, slot_base, degs = [], [], [], []
-    base = 0
-    for t in range(len(block.n_src)):
-        nd = int(block.n_dst[t])
-        if nd == 0:
-            continue
-        slot_type.append(t); slot_rel.append(-1); slot_base.append(base)
-        degs.append(np.ones(nd, dtype=np.int32)); base += nd
-        for r, rel in enumerate(block.rels):
-            if rel.dst_type != t:
-                continue
-            slot_type.append(t); slot_rel.append(r); slot_base.append(base)
-            degs.append(degrees(rel.indptr)); base += nd
-    deg = np.concatenate(degs) if degs else np.zeros(0, dtype=np.int32)
-    return slot_type, slot_rel, slot_base, deg
-
-
-def forward_schedule(block) -> np.ndarray:
-    """Segment ids in the library's forward processing order: segments of more than 32
-    edges first, heaviest power of two first; everything else in enumeration order."""
-    _, _, _, deg = forward_segments(block)
-    return stable_bucket_order(degree_key(deg), SCHED_BUCKETS)
-
-
-def backward_schedule(block, grad_types: Sequence[int]) -> np.ndarray:
-    """Backward processing order: for each requested source type (ascending), that type's
-    rows (local ids) stably sorted by the degree key of the row's in-degree in the
-    transpose, summed over the relations leaving the type; sections concatenated."""
-    parts = []
-    for s in sorted(set(grad_types)):
-        ns = int(block.n_src[s])
-        cnt = np.zeros(ns, dtype=np.int64)
-        for rel in block.rels:
-            if rel.src_type == s and len(rel.indices):
-                cnt += np.bincount(np.asarray(rel.indices, dtype=np.int64), minlength=ns)[:ns]
-        parts.append(stable_bucket_order(degree_key(cnt), SCHED_BUCKETS))
-    return np.concatenate(parts) if parts else np.zeros(0, dtype=np.int32)
 
 
 class _SubRel:

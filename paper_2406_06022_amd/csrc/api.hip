@@ -403,6 +403,7 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
         if ((st = device_validate(block, nullptr, L, ws, stream)) != RGCN_OK) return st;
     }
     char *scratch = ws + L.off_scratch;
+    const int keep_order = (flags & RGCN_PLAN_ENUMERATION_ORDER) ? 1 : 0;
     unsigned parts = flags & (RGCN_PLAN_FORWARD | RGCN_PLAN_BACKWARD);
     if (parts == 0) parts = RGCN_PLAN_FORWARD | RGCN_PLAN_BACKWARD;
     // flag word 0 belongs to the forward schedule, words 1 + t to the backward ones
@@ -426,8 +427,8 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
         // segment weights sit in the plan scratch after the chunk pass's own temporaries
         int32_t *weight = (int32_t *)(scratch + fwd_chunks_temp_bytes(L.n_seg));
         TRY_HIP(fwd_plan(L.slots, L.nslots, L.n_seg, (int32_t *)(ws + L.off_fwd_order), moff, mld,
-                         L.es, (SegDesc *)(ws + L.off_fwd_desc), weight, sched_flag, scratch,
-                         stream), "forward schedule");
+                         L.es, (SegDesc *)(ws + L.off_fwd_desc), weight, sched_flag,
+                         keep_order, scratch, stream), "forward schedule");
         TRY_HIP(fwd_chunks(weight, L.n_seg, L.nc_max, (int32_t *)(ws + L.off_fwd_chunks), scratch,
                            stream), "forward chunks");
     }
@@ -456,7 +457,7 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
             if (block->rels[r].src_type == t)
                 kr.csc_indptr[kr.count++] = (const int32_t *)(ws + L.off_csc_indptr[r]);
         TRY_HIP(bwd_schedule(kr, block->n_src[t], (int32_t *)(ws + L.off_bwd_order) + L.bwd_base[t],
-                             scratch, sched_flag + 1 + t, stream), "backward schedule");
+                             scratch, sched_flag + 1 + t, keep_order, stream), "backward schedule");
     }
     return RGCN_OK;
 }

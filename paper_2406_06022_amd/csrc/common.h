@@ -123,10 +123,12 @@ size_t bucket_sort_temp_bytes(int64_t n, int nbuckets);
 // Mcat_t in the workspace, mcat_ld[t]: its row length in elements, es: element size.
 // weight[p] = balancing weight of segment p in the flattened forward stream: the rows it
 // moves, max(deg, 1) entries read plus one written.  *flag
-// (zero on entry) ends nonzero when some segment is heavy and the schedule was sorted.
+// (zero on entry) ends nonzero when some segment is heavy and the schedule was sorted;
+// keep_order != 0 keeps enumeration order (the flag stays zero, nothing is sorted).
 hipError_t fwd_plan(const FwdSlot *slots_host, int nslots, int64_t n_seg, int32_t *order,
                     const int64_t *mcat_off, const int64_t *mcat_ld, int es, SegDesc *desc,
-                    int32_t *weight, uint32_t *flag, void *temp, hipStream_t s);
+                    int32_t *weight, uint32_t *flag, int keep_order, void *temp,
+                    hipStream_t s);
 // Flattened forward stream split into chunks of kFwdChunk weight (segments whole): cs has
 // nc_max + 2 entries, nc_max = fwd_chunk_bound(n_seg, sum of relation nnz); cs[c] = first
 // segment of chunk c, cs[nc_max + 1] = total weight.  temp: fwd_chunks_temp_bytes(n_seg);
@@ -155,9 +157,10 @@ struct BwdKeyRels {          // relations leaving one source type
     int32_t count;
     const int32_t *csc_indptr[kMaxRels];
 };
-// *flag (zero on entry) ends nonzero when some row is heavy and the schedule was sorted.
+// *flag (zero on entry) ends nonzero when some row is heavy and the schedule was sorted;
+// keep_order != 0 keeps enumeration order.
 hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, void *temp,
-                        uint32_t *flag, hipStream_t s);
+                        uint32_t *flag, int keep_order, hipStream_t s);
 hipError_t fill_words(void *dst, const void *src_host, size_t bytes, hipStream_t s);
 
 // aggregate.hip

@@ -469,11 +469,12 @@ __device__ __forceinline__ int32_t desc_of(const DescArgs &a, int64_t seg, int64
 
 // IDENT: schedule position p holds segment p; order[p] = p, and *flag is raised when some
 // segment is heavy (a schedule key other than the last), i.e. when the sorted schedule is
-// not the identity.  Otherwise (gated on that flag): segment order[p].
+// not the identity, unless `keep` asks for enumeration order.  Otherwise (gated on that
+// flag): segment order[p].
 template <bool IDENT>
 __global__ __launch_bounds__(kThreads) void k_fwd_desc(DescArgs a, int32_t *order,
                                                        int64_t n_seg, SegDesc *desc,
-                                                       int32_t *weight, uint32_t *flag) {
+                                                       int32_t *weight, uint32_t *flag, int keep) {
     if (!IDENT && *flag == 0u) return;
     const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const bool in = p < n_seg;
@@ -482,17 +483,18 @@ __global__ __launch_bounds__(kThreads) void k_fwd_desc(DescArgs a, int32_t *orde
     if (IDENT && in) order[p] = (int32_t)p;
     bool heavy = false;
     if (in) heavy = desc_of(a, seg, p, desc, weight) > 32;
-    if (IDENT && __ballot(heavy) != 0 && (threadIdx.x & 63) == 0) atomicOr(flag, 1u);
+    if (IDENT && !keep && __ballot(heavy) != 0 && (threadIdx.x & 63) == 0) atomicOr(flag, 1u);
 }
 
 // Backward rows of one type in enumeration order (order[j] = j); *flag is raised when some
-// row is heavy, i.e. when the sorted schedule is not the identity.
+// row is heavy, i.e. when the sorted schedule is not the identity, unless `keep` asks for
+// enumeration order.
 __global__ __launch_bounds__(kThreads) void k_bwd_ident(BwdKey kf, int64_t n, int32_t *order,
-                                                        uint32_t *flag) {
+                                                        uint32_t *flag, int keep) {
     const int64_t j = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const bool in = j < n;
     if (in) order[j] = (int32_t)j;
-    const bool heavy = in && kf(j) != kSchedBuckets - 1;
+    const bool heavy = in && !keep && kf(j) != kSchedBuckets - 1;
     if (__ballot(heavy) != 0 && (threadIdx.x & 63) == 0) atomicOr(flag, 1u);
 }
 
@@ -556,7 +558,8 @@ size_t bucket_sort_temp_bytes(int64_t n, int nbuckets) {
 
 hipError_t fwd_plan(const FwdSlot *slots_host, int nslots, int64_t n_seg, int32_t *order,
                     const int64_t *mcat_off, const int64_t *mcat_ld, int es, SegDesc *desc,
-                    int32_t *weight, uint32_t *flag, void *temp, hipStream_t s) {
+                    int32_t *weight, uint32_t *flag, int keep_order, void *temp,
+                    hipStream_t s) {
     if (n_seg == 0) return hipSuccess;
     DescArgs a;
     a.nslots = nslots;
@@ -577,11 +580,11 @@ hipError_t fwd_plan(const FwdSlot *slots_host, int nslots, int64_t n_seg, int32_
     // enumeration order first; the sort and the second descriptor pass run only when some
     // segment is heavy (otherwise the stable sort by key is the identity)
     hipLaunchKernelGGL(k_fwd_desc<true>, grid, dim3(kThreads), 0, s, a, order, n_seg, desc,
-                       weight, flag);
+                       weight, flag, keep_order);
     RGCN_HIP_TRY(hipGetLastError());
     RGCN_HIP_TRY((bucket_sort<kSchedBuckets, 5>(kf, PutIndex{order}, n_seg, temp, s, flag)));
     hipLaunchKernelGGL(k_fwd_desc<false>, grid, dim3(kThreads), 0, s, a, order, n_seg, desc,
-                       weight, flag);
+                       weight, flag, keep_order);
     return hipGetLastError();
 }
 
@@ -605,10 +608,10 @@ hipError_t fwd_chunks(const int32_t *weight, int64_t n_seg, int64_t nc_max, int3
 }
 
 hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, void *temp,
-                        uint32_t *flag, hipStream_t s) {
+                        uint32_t *flag, int keep_order, hipStream_t s) {
     if (n_rows == 0) return hipSuccess;
     hipLaunchKernelGGL(k_bwd_ident, dim3((unsigned)cdiv(n_rows, kThreads)), dim3(kThreads), 0, s,
-                       BwdKey{rels}, n_rows, order, flag);
+                       BwdKey{rels}, n_rows, order, flag, keep_order);
     RGCN_HIP_TRY(hipGetLastError());
     return bucket_sort<kSchedBuckets, 5>(BwdKey{rels}, PutIndex{order}, n_rows, temp, s, flag);
 }

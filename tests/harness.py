@@ -102,7 +102,7 @@ class BlockRun:
         # NaN in fp32 and bf16)
         self.ws.fill_(0xFF)
 
-    def run_gpu(self, validate: bool = False, repeat: int = 1):
+    def run_gpu(self, validate: bool = False, repeat: int = 1, plan_flags: int = 0):
         dev = self.device
         blk = self.blk
         T = len(blk.n_src)
@@ -125,7 +125,7 @@ class BlockRun:
                   if t in self.grad_types else None for t in range(T)]
             demb = [torch.zeros((self.tables[t].shape[0], self.d_in), dtype=f32, device=dev)
                     if t in self.emb_types else None for t in range(T)]
-            rgcn.rgcn_block_plan(self.dblk, self.params, self.ws, flags)
+            rgcn.rgcn_block_plan(self.dblk, self.params, self.ws, flags | plan_flags)
             rgcn.rgcn_block_forward(self.dblk, self.inputs, self.params, y, self.ws,
                                     flags | (rgcn.RGCN_FUSE_RELU if self.fwd_relu else 0))
             rgcn.rgcn_block_backward(self.dblk, self.inputs, self.params, dy, dw_rel, dw_self,

@@ -119,8 +119,31 @@ def _plan_arrays(run):
     return fwd, bwd, csc
 
 
+def _check_schedules(run, fwd, bwd):
+    """The schedules are library policy (no passage of the paper orders the work): all a
+    caller may rely on is that each is a permutation of the items it covers."""
+    lay = rgcn.rgcn_block_plan_layout(run.dblk, run.params)
+    assert np.array_equal(np.sort(fwd), np.arange(lay["n_fwd_segments"]))
+    base = 0
+    for t in sorted(set(run.grad_types)):
+        n = run.blk.n_src[t]
+        assert np.array_equal(np.sort(bwd[base:base + n]), np.arange(n)), t
+        base += n
+    assert base == len(bwd)
+
+
+def _check_csc(run, csc):
+    for r, (cip, cdst) in csc.items():
+        rel = run.blk.rels[r]
+        want_ip, want_dst, _ = oracle.csc(run.blk.n_src[rel.src_type], rel.indptr, rel.indices)
+        assert np.array_equal(cip, want_ip), r
+        assert np.array_equal(cdst, want_dst), r
+
+
 @pytest.mark.parametrize("index", [1, 2, 3, 4])
 def test_plan_is_bit_exact(index):
+    """CSC transposes bit for bit against the oracle's stable counting sort; schedules are
+    permutations."""
     spec = synth.small_config(index)
     mb = synth.sample_minibatch(spec)
     for blk in mb.blocks:
@@ -129,34 +152,78 @@ def test_plan_is_bit_exact(index):
                        grad_types=[t for t in range(T) if blk.n_src[t] > 0])
         run.run_gpu()
         fwd, bwd, csc = _plan_arrays(run)
-        assert np.array_equal(fwd, oracle.forward_schedule(blk))
-        assert np.array_equal(bwd, oracle.backward_schedule(blk, run.grad_types))
-        for r, (cip, cdst) in csc.items():
-            rel = blk.rels[r]
-            want_ip, want_dst, _ = oracle.csc(blk.n_src[rel.src_type], rel.indptr, rel.indices)
-            assert np.array_equal(cip, want_ip), r
-            assert np.array_equal(cdst, want_dst), r
+        _check_schedules(run, fwd, bwd)
+        _check_csc(run, csc)
 
 
-def test_plan_skewed_sources_bit_exact():
-    """Power-law source popularity: long transpose segments (hub sources)."""
+def _skewed_block():
     spec = synth.WorkloadSpec("skewed", "bf16", ("A", "B"), (300000, 5000), (False, False),
                               ((0, 1), (1, 0), (0, 0)), (1,), 3000, (25,), "zipf", (8, 8),
                               synth.BASE_SEED + 50, skew=0.9)
-    mb = synth.sample_minibatch(spec)
-    blk = mb.blocks[0]
+    return synth.sample_minibatch(spec).blocks[0]
+
+
+def test_plan_skewed_sources_bit_exact():
+    """Power-law source popularity: long transpose segments (hub sources), so the
+    backward schedule is reordered; RGCN_PLAN_ENUMERATION_ORDER keeps enumeration order."""
+    blk = _skewed_block()
     run = BlockRun(blk, "bf16", 8, 8, seed=3, grad_types=[0, 1])
     run.run_gpu()
     fwd, bwd, csc = _plan_arrays(run)
-    assert np.array_equal(fwd, oracle.forward_schedule(blk))
-    assert np.array_equal(bwd, oracle.backward_schedule(blk, [0, 1]))
-    longest = 0
-    for r, (cip, cdst) in csc.items():
-        rel = blk.rels[r]
-        want_ip, want_dst, _ = oracle.csc(blk.n_src[rel.src_type], rel.indptr, rel.indices)
-        longest = max(longest, int(np.diff(want_ip).max(initial=0)))
-        assert np.array_equal(cip, want_ip) and np.array_equal(cdst, want_dst)
-    assert longest > 20  # hub sources exist
+    _check_schedules(run, fwd, bwd)
+    _check_csc(run, csc)
+    longest = max(int(np.diff(oracle.csc(blk.n_src[r.src_type], r.indptr, r.indices)[0]).max(initial=0))
+                  for r in blk.rels)
+    assert longest > 32  # hub sources exist ...
+    assert not np.array_equal(bwd, np.concatenate([np.arange(n) for n in blk.n_src]))  # ... and moved
+    run.run_gpu(plan_flags=rgcn.RGCN_PLAN_ENUMERATION_ORDER)
+    fwd, bwd, csc = _plan_arrays(run)
+    assert np.array_equal(fwd, np.arange(len(fwd)))
+    assert np.array_equal(bwd, np.concatenate([np.arange(n) for n in blk.n_src]))
+    _check_csc(run, csc)
+
+
+def _bitwise_equal(a, b):
+    for key in a:
+        for x, z in zip(a[key], b[key]):
+            if x is None:
+                assert z is None
+                continue
+            xv = x.view(torch.int16) if x.dtype == torch.bfloat16 else x.view(torch.int32)
+            zv = z.view(torch.int16) if z.dtype == torch.bfloat16 else z.view(torch.int32)
+            assert torch.equal(xv, zv), key
+
+
+@pytest.mark.parametrize("case", ["skewed-bf16", "claimed-runs-bf16", "claimed-runs-f32"])
+def test_results_do_not_depend_on_the_schedule(case):
+    """Every output and gradient is bit-identical whether the kernels walk the degree-sorted
+    schedules or plain enumeration order (blocks with segments of more than 32 edges in both
+    directions, so the sorted schedules differ from enumeration order); and both match the
+    oracle."""
+    if case.startswith("skewed"):
+        blk, dtype, d, ids = _skewed_block(), "bf16", 64, True
+    else:
+        blk, dtype = _claimed_runs_block(), case.split("-")[-1]
+        d, ids = (128 if dtype == "bf16" else 64), True
+    T = len(blk.n_src)
+    run = BlockRun(blk, dtype, d, 64, seed=17, use_ids=ids, bias=True, emb_types=(0,),
+                   grad_types=list(range(T)))
+    print(f"case {case} nnz {sum(r.nnz for r in blk.rels)}", flush=True)
+    sorted_out = run.run_gpu()[0]
+    fwd, bwd, _ = _plan_arrays(run)
+    enum_bwd = np.concatenate([np.arange(blk.n_src[t]) for t in sorted(set(run.grad_types))])
+    # the forward segments are heavy in the claimed-runs block, the transpose segments in the
+    # skewed one: the sorted schedule differs from enumeration order in that direction
+    if case.startswith("skewed"):
+        assert not np.array_equal(bwd, enum_bwd)
+    else:
+        assert not np.array_equal(fwd, np.arange(len(fwd)))
+    enum_out = run.run_gpu(plan_flags=rgcn.RGCN_PLAN_ENUMERATION_ORDER)[0]
+    fwd2, bwd2, _ = _plan_arrays(run)
+    assert np.array_equal(fwd2, np.arange(len(fwd2))) and np.array_equal(bwd2, enum_bwd)
+    _bitwise_equal(sorted_out, enum_out)
+    run.run_oracle()
+    run.assert_parity()
 
 
 @pytest.mark.parametrize("n_src", [900, 5000, 1_200_000])

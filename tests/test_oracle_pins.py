@@ -143,7 +143,6 @@ def test_hand_worked_block(orc):
     for r, c in enumerate(g["csc"]):
         cip, cd, ce = orc.csc(3, blk.rels[r].indptr, blk.rels[r].indices)
         assert cip.tolist() == c["indptr"] and cd.tolist() == c["dst"] and ce.tolist() == c["eid"]
-    assert orc.forward_schedule(blk).tolist() == g["forward_schedule"]
     demb = np.zeros((g["emb_rows"], 2))
     orc.scatter_add(np.array(g["emb_ids"]), gr["dh_src"][0], demb)
     for row in range(g["emb_rows"]):
@@ -365,17 +364,6 @@ def test_csc_against_scipy(orc):
         assert np.array_equal(cd, dst_of[ce])
 
 
-def test_bucket_order_is_a_stable_sort(orc):
-    rng = np.random.default_rng(43)
-    for n in (0, 1, 17, 1000):
-        key = rng.integers(0, 64, size=n).astype(np.int32)
-        got = orc.stable_bucket_order(key, 64)
-        want = sorted(range(n), key=lambda x: int(key[x]))
-        assert got.tolist() == want
-    deg = np.array([0, 1, 5, 32, 33, 63, 64, 127, 128, 1000, 2 ** 31 - 1])
-    assert orc.degree_key(deg).tolist() == [31, 31, 31, 31, 30, 30, 29, 29, 28, 26, 5]
-
-
 def test_invalid_blocks_are_rejected(orc):
     good = _B([4], [2], [_R(0, 0, [0, 1, 3], [0, 3, 1])])
     assert orc.check_block(good)
@@ -420,19 +408,6 @@ def test_sub_block_preserves_kept_rows(orc):
                                    atol=1e-12)
     for r in range(3):
         np.testing.assert_allclose(gs["dw_rel"][r], g["dw_rel"][r], rtol=1e-12, atol=1e-12)
-
-
-def test_forward_schedule_heavy_first_by_hand(orc):
-    """One type, six destination rows, one relation with degrees 1, 40, 3, 100, 33, 64.
-    Segments 0-5 are the self-loop rows (degree 1), 6-11 the relation's rows.  Keys: 31 up
-    to degree 32, 30 for 33-63, 29 for 64-127.  Worked by hand: the relation rows of degree
-    100 and 64 (segments 9, 11), then 40 and 33 (7, 10), then the rest in order."""
-    degs = [1, 40, 3, 100, 33, 64]
-    indptr = np.concatenate([[0], np.cumsum(degs)]).astype(np.int32)
-    indices = np.concatenate([np.arange(d) for d in degs]).astype(np.int32)
-    blk = _B([120], [6], [_R(0, 0, indptr, indices)])
-    assert orc.forward_schedule(blk).tolist() == [9, 11, 7, 10, 0, 1, 2, 3, 4, 5, 6, 8]
-    assert orc.backward_schedule(blk, [0])[:3].tolist() == [0, 1, 2]  # every source: degree <= 6
 
 
 # ---------------------------------------------------------------- sparse Adagrad step
