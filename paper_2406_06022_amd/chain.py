@@ -81,12 +81,22 @@ class MiniBatchStack:
 
     def attach_adagrad(self, lr: float, eps: float) -> None:
         """Zero Adagrad state per learnable table; from now on backward steps the tables
-        in place instead of filling demb."""
+        in place instead of filling demb.  With distinct row ids (ids_unique) the step is
+        fused into the first block's transposed sum; with repeated ids the gradient is
+        first scatter-added into demb (cleared here) and the standalone step then runs once
+        over the distinct rows, clearing the gradient rows it reads."""
         states = [None] * len(self.demb)
+        self._ada_rows = [None] * len(self.demb)
         for t in self.emb_types:
             tab = self.inputs[0].bases[t]
             states[t] = torch.zeros((tab.shape[0], self.dims[0]), dtype=torch.float32,
                                     device=self.device)
+            if not self.ids_unique:
+                self.demb[t].zero_()
+                ids = self.inputs[0].row_ids[t]
+                self._ada_rows[t] = (torch.unique(ids) if ids is not None else
+                                     torch.arange(self.blocks[0].n_src[t], dtype=torch.int64,
+                                                  device=self.device))
         self.adagrad = (float(lr), float(eps), states)
 
     @property
@@ -149,9 +159,19 @@ class MiniBatchStack:
         """First block's transposed sum with the Adagrad step of the learnable tables
         (after its dense backward stage)."""
         lr, eps, states = self.adagrad
-        rgcn.rgcn_block_backward_sparse_adagrad(self.blocks[0], self.inputs[0], self.params[0],
-                                                states, lr, eps, workspace=self.workspaces[0],
-                                                flags=flags | rgcn.RGCN_IDS_UNIQUE)
+        if self.ids_unique:
+            rgcn.rgcn_block_backward_sparse_adagrad(self.blocks[0], self.inputs[0],
+                                                    self.params[0], states, lr, eps,
+                                                    workspace=self.workspaces[0],
+                                                    flags=flags | rgcn.RGCN_IDS_UNIQUE)
+            return
+        # repeated ids: the fused step would race on a row listed twice
+        rgcn.rgcn_block_backward_sparse(self.blocks[0], self.inputs[0], self.params[0], None,
+                                        self.demb, self.workspaces[0],
+                                        flags & ~rgcn.RGCN_IDS_UNIQUE)
+        for t in self.emb_types:
+            rgcn.rgcn_sparse_adagrad(self._ada_rows[t], self.demb[t], states[t],
+                                     self.inputs[0].bases[t], lr, eps, rgcn.RGCN_CLEAR_GRAD)
 
     def step(self, dy_top, timer=None, overlap_plan: bool = True) -> None:
         """One pass of the whole path: plan, forward, backward.

@@ -120,6 +120,15 @@ def config(index: int) -> WorkloadSpec:
     return CONFIGS[index]()
 
 
+def skewed_config(index: int, skew: float = 0.8) -> WorkloadSpec:
+    """The workload with sources drawn by popularity rank, p(rank k) proportional to
+    (k + 1)^-skew, mapped to ids by a fixed bijection: power-law source degrees, so the
+    backward's transpose segments are uncapped (hub sources with tens of thousands of
+    edges)."""
+    spec = config(index)
+    return dataclasses.replace(spec, name=f"{spec.name}_skewed", skew=skew)
+
+
 def small_config(index: int) -> WorkloadSpec:
     """Each configuration's structure at a size the oracle evaluates in seconds.
 

@@ -194,3 +194,53 @@ def test_standalone_adagrad_matches_oracle(dtype, d, n, num_rows, clear):
     else:
         assert np.array_equal(got_g[listed], grad0.double().numpy()[listed])
     assert np.array_equal(got_g[~listed], grad0.double().numpy()[~listed])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_chain_adagrad_with_repeated_ids(dtype):
+    """The chain driver declared with repeated input ids (ids_unique=False): the embedding
+    gradient is scatter-added with atomics, then each distinct table row takes one step
+    from the summed gradient (the fused step, which would race, is not used).  Rows named
+    twice or more must have stepped on their summed gradient, rows never named keep their
+    bits, and the gradient buffer is left cleared for the next step."""
+    from paper_2406_06022_amd import chain
+
+    blk, _ = _adagrad_block("mixed")
+    T, R = len(blk.n_src), len(blk.rels)
+    d_in, d_out = 32, 48
+    tdt = synth.torch_dtype(dtype)
+    gen = torch.Generator().manual_seed(71)
+    rows0 = blk.n_src[0] // 2 + 5
+    ids = [torch.randint(0, rows0, (blk.n_src[0],), generator=gen),      # repeats
+           torch.randperm(blk.n_src[1] + 40, generator=gen)[: blk.n_src[1]]]
+    assert torch.unique(ids[0]).numel() < blk.n_src[0]
+    tables = [torch.randn((rows0, d_in), generator=gen).to(tdt),
+              torch.randn((blk.n_src[1] + 40, d_in), generator=gen).to(tdt)]
+    w_rel, w_self, _ = synth.block_weights(T, R, d_in, d_out, tdt, 19)
+    dy = [torch.randn((n, d_out), generator=gen) for n in blk.n_dst]
+    dev = "cuda"
+    d_tables = [x.to(dev) for x in tables]
+    stack = chain.MiniBatchStack([blk], d_tables, [x.to(dev) for x in ids],
+                                 [([w.to(dev) for w in w_rel], [w.to(dev) for w in w_self], None)],
+                                 dtype, [d_in, d_out], emb_types=[0], device=dev,
+                                 ids_unique=False)
+    stack.attach_adagrad(LR, EPS)
+    stack.step([x.to(dev) for x in dy])
+    torch.cuda.synchronize()
+
+    h = [to64(tables[t])[ids[t].numpy()] for t in range(T)]
+    g = oracle.block_backward(blk, h, [to64(w) for w in w_rel], [to64(w) for w in w_self],
+                              [to64(x) for x in dy], want_dh=[True, False])
+    grad = np.zeros((rows0, d_in))
+    oracle.scatter_add(ids[0].numpy(), g["dh_src"][0], grad)
+    rows = np.unique(ids[0].numpy())
+    w0 = to64(tables[0])
+    got_w = to64(d_tables[0])
+    got_s = to64(stack.adagrad[2][0])
+    named = np.zeros(rows0, dtype=bool)
+    named[rows] = True
+    assert np.array_equal(got_w[~named], w0[~named])
+    assert not got_s[~named].any()
+    assert not to64(stack.demb[0]).any()          # cleared by the step
+    _check_steps(grad[rows], np.zeros((rows.size, d_in)), w0[rows], got_s[rows], got_w[rows], 1,
+                 TOL[dtype], dtype, f"repeated ids {dtype}")

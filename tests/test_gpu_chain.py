@@ -52,7 +52,7 @@ def _margin_biases(blocks, h0, w64, T, seed, quant):
     return biases, ys
 
 
-@pytest.mark.parametrize("index", [2, 4])
+@pytest.mark.parametrize("index", [1, 2, 4])
 def test_chain_matches_layerwise_oracle(index):
     spec = synth.small_config(index)
     mb = synth.sample_minibatch(spec)
@@ -124,11 +124,43 @@ def test_chain_matches_layerwise_oracle(index):
     assert not bad, f"chain parity failures (tol {tol}): {bad}"
 
 
-@pytest.mark.parametrize("index", [2, 4])
+def poison_stack(stack):
+    """Fill every workspace with 0xFF bytes (NaN in fp32 and bf16, -1 as int32) and every
+    output buffer with NaN, so that nothing a step reads before writing survives from an
+    earlier step."""
+    for ws in stack.workspaces:
+        ws.fill_(0xFF)
+    for l in range(stack.L):
+        for x in stack.y[l]:
+            if x is not None:
+                x.fill_(float("nan"))
+        for grp in (stack.dw_rel[l], stack.dw_self[l], stack.dbias[l]):
+            for x in grp or []:
+                if x is not None:
+                    x.fill_(float("nan"))
+        if stack.dh[l] is not None:
+            for x in stack.dh[l]:
+                if x is not None:
+                    x.fill_(float("nan"))
+
+
+def step_outputs(stack, emb):
+    out = [x.clone() for x in stack.y[-1] if x is not None]
+    for l in range(stack.L):
+        out += [x.clone() for x in stack.dw_rel[l]] + [x.clone() for x in stack.dw_self[l]]
+        if stack.dh[l] is not None:
+            out += [x.clone() for x in stack.dh[l] if x is not None]
+    out += [stack.demb[t].clone() for t in emb]
+    return out
+
+
+@pytest.mark.parametrize("index", [1, 2, 4])
 def test_overlapped_plan_matches_serial_step(index):
     """The step with the backward half of the plan on a second stream (from the end of the
-    first aggregate stage) gives bit-identical outputs and gradients to the serial order,
-    on two steps in a row (the second re-plans into the same workspaces)."""
+    first aggregate stage) gives bit-identical outputs and gradients to the serial order.
+    Every step starts from poisoned workspaces and outputs, and the overlapped step runs
+    first, so a backward that read a transpose or schedule the side stream had not yet
+    written (a missing wait, a plan part skipped) would show."""
     spec = synth.small_config(index)
     mb = synth.sample_minibatch(spec)
     T, R, L = len(spec.ntype_names), len(spec.rels), spec.num_layers
@@ -148,19 +180,18 @@ def test_overlapped_plan_matches_serial_step(index):
           for n in mb.blocks[-1].n_dst]
 
     def run(overlap):
+        poison_stack(stack)
         for t in emb:
             stack.demb[t].zero_()
         stack.step(dy, overlap_plan=overlap)
         torch.cuda.synchronize()
-        out = [x.clone() for x in stack.y[-1] if x is not None]
-        for l in range(L):
-            out += [x.clone() for x in stack.dw_rel[l]] + [x.clone() for x in stack.dw_self[l]]
-        out += [stack.demb[t].clone() for t in emb]
-        return out
+        return step_outputs(stack, emb)
 
+    first = run(True)
     want = run(False)
-    for rep in range(2):
-        got = run(True)
+    second = run(True)
+    for rep, got in enumerate((first, second)):
         assert len(got) == len(want)
         for i, (g, w_) in enumerate(zip(got, want)):
-            assert torch.equal(g, w_), f"step {rep}: output {i} differs"
+            assert not torch.isnan(w_).any(), f"serial output {i} left unwritten"
+            assert torch.equal(g, w_), f"overlapped step {rep}: output {i} differs"

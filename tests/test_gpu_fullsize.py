@@ -1,10 +1,10 @@
-"""Parity at the workloads' full sizes, in the launch configuration the benchmark times.
+"""Parity at the workloads' full sizes.
 
-Every block of each workload runs through the C ABI with the benchmark's flags (fused ReLU
-below the last layer, ReLU-input mask above the first, unique ids and the embedding
-gradient at the first).  Inputs are seeded: the input layer reads the full feature and
-embedding tables by global row id; higher layers read a seeded ReLU'd dense input of the
-right shape.  The oracle then recomputes sampled outputs one by one:
+Every block of each workload runs through the C ABI stage by stage, on one stream, with the
+benchmark's flags (fused ReLU below the last layer, ReLU-input mask above the first, unique
+ids and the embedding gradient at the first).  Inputs are seeded: the input layer reads the
+full feature and embedding tables by global row id; higher layers read a seeded ReLU'd
+dense input of the right shape.  The oracle then recomputes sampled outputs one by one:
 
 * output rows of sampled destination rows (heaviest, zero-degree, first, last, random):
   the forward of the sub-block that determines them;
@@ -13,6 +13,12 @@ right shape.  The oracle then recomputes sampled outputs one by one:
 * weight and bias gradients on a sampled set of (input, output) columns, reduced over all
   rows of the block;
 * embedding-gradient rows the block never touches stay zero.
+
+The same checks run on the first block of the billion-edge workload with power-law
+(popularity-skewed) sources, whose hub sources take the long-segment paths of the
+transpose.  The benchmark's own launch configuration -- the chain driver's step with the
+backward half of the plan on a second stream -- is checked at the billion-edge workload's
+full size bit for bit against the serial order of the same stages.
 """
 import numpy as np
 import pytest
@@ -84,144 +90,224 @@ def _check(name, got, want, tol, errs):
     return e <= tol
 
 
-@pytest.mark.parametrize("index", range(5))
-def test_full_size_sampled_parity(index):
-    spec = synth.config(index)
-    torch.manual_seed(0)
-    mb = synth.sample_minibatch(spec, device=DEV)
+def _block_parity(spec, mb, index, l, rng, bad):
+    """Run block l of the mini-batch through the C ABI with the benchmark's flags and check
+    sampled outputs against the oracle; failures go into ``bad``."""
     tdt = synth.torch_dtype(spec.dtype)
     tol = TOL[spec.dtype]
     T = len(spec.ntype_names)
     R = len(spec.rels)
     L = spec.num_layers
     emb = [t for t in range(T) if spec.featureless[t]]
+    blk = mb.blocks[l]
+    print(f"[fullsize] {spec.name} block {l}: nnz {blk.nnz}", flush=True)
+    d_in, d_out = spec.dims[l], spec.dims[l + 1]
+    first, last = l == 0, l == L - 1
+    # ---- seeded inputs
+    if first:
+        tables = [synth.normal_table(spec.type_rows[t], d_in, tdt, 7000 + 10 * index + t,
+                                     device=DEV) for t in range(T)]
+        ids = [torch.as_tensor(mb.input_ids[t]).to(DEV) for t in range(T)]
+    else:
+        tables = [torch.relu(synth.normal_table(max(blk.n_src[t], 1), d_in, tdt,
+                                                8000 + 100 * index + 10 * l + t, device=DEV))
+                  for t in range(T)]
+        ids = [None] * T
+    w_rel, w_self, _ = synth.block_weights(T, R, d_in, d_out, tdt, 900 + 10 * index + l)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(5000 + 10 * index + l)
+    dy = [torch.randn((n, d_out), generator=gen, device=DEV, dtype=torch.float32)
+          for n in blk.n_dst]
+    if first:
+        grad_types = [t for t in emb if blk.n_src[t] > 0]
+    else:
+        grad_types = [t for t in range(T) if blk.n_src[t] > 0]
+    mask = 0
+    for t in grad_types:
+        mask |= 1 << t
+    # ---- GPU, benchmark flags
+    dblk = rgcn.DeviceBlock(blk, mask, DEV)
+    params = rgcn.Params(spec.dtype, d_in, d_out, [w.to(DEV) for w in w_rel],
+                         [w.to(DEV) for w in w_self])
+    ws = rgcn.new_workspace(dblk, params, DEV)
+    inputs = rgcn.Inputs(tables, ids)
+    y = [torch.empty((n, d_out), dtype=tdt, device=DEV) if n > 0 else None for n in blk.n_dst]
+    f32 = torch.float32
+    dw_rel = [torch.empty((d_in, d_out), dtype=f32, device=DEV) for _ in range(R)]
+    dw_self = [torch.empty((d_in, d_out), dtype=f32, device=DEV) for _ in range(T)]
+    dh = [None] * T
+    demb = None
+    if first:
+        demb = [torch.zeros((spec.type_rows[t], d_in), dtype=f32, device=DEV)
+                if t in grad_types else None for t in range(T)]
+        if not grad_types:
+            demb = None
+    else:
+        dh = [torch.empty((blk.n_src[t], d_in), dtype=f32, device=DEV)
+              if t in grad_types else None for t in range(T)]
+    fwd_flags = 0 if last else rgcn.RGCN_FUSE_RELU
+    bwd_flags = rgcn.RGCN_IDS_UNIQUE if first else rgcn.RGCN_INPUT_RELU
+    rgcn.rgcn_block_plan(dblk, params, ws)
+    rgcn.rgcn_block_aggregate(dblk, inputs, params, ws, fwd_flags)
+    rgcn.rgcn_block_transform(dblk, params, y, ws, fwd_flags)
+    rgcn.rgcn_block_backward_dense(dblk, params, dy, dw_rel, dw_self, None, ws, bwd_flags)
+    rgcn.rgcn_block_backward_sparse(dblk, inputs, params, dh, demb, ws, bwd_flags)
+    torch.cuda.synchronize()
+
+    w_rel64 = [to64(w) for w in w_rel]
+    w_self64 = [to64(w) for w in w_self]
+    errs = {}
+    # ---- sampled output rows
+    keep = [_dst_sample(blk, t, rng) for t in range(T)]
+    sub, src_map = oracle.sub_block(blk, keep)
+    h_sub = [_input_rows(tables, ids, t, src_map[t]) for t in range(T)]
+    y_ref = oracle.block_forward(sub, h_sub, w_rel64, w_self64, relu=not last)
+    for t in range(T):
+        if keep[t].size:
+            got = to64(y[t].index_select(0, torch.as_tensor(keep[t], device=DEV)))
+            if not _check(f"y[{t}]", got, y_ref[t], tol, errs):
+                bad[f"block{l} y[{t}]"] = errs[f"y[{t}]"]
+    # ---- sampled input / embedding gradient rows
+    for s in grad_types:
+        srows = _src_sample(blk, s, rng)
+        keep_b = _rows_referencing(blk, s, srows)
+        sub_b, map_b = oracle.sub_block(blk, keep_b)
+        h_b = [_input_rows(tables, ids, t, map_b[t]) for t in range(T)]
+        dy_b = [to64(dy[t].index_select(0, torch.as_tensor(keep_b[t], device=DEV)))
+                for t in range(T)]
+        want = [t == s for t in range(T)]
+        g = oracle.block_backward(sub_b, h_b, w_rel64, w_self64, dy_b,
+                                  input_relu=not first, want_dh=want, want_dw=False)
+        order = np.argsort(map_b[s], kind="stable")
+        pos = order[np.searchsorted(map_b[s][order], srows)]
+        ref_rows = g["dh_src"][s][pos]
+        if first:
+            gid = ids[s].index_select(0, torch.as_tensor(srows, device=DEV))
+            got = to64(demb[s].index_select(0, gid))
+            name = f"demb[{s}]"
+        else:
+            got = to64(dh[s].index_select(0, torch.as_tensor(srows, device=DEV)))
+            name = f"dh[{s}]"
+        if not _check(name, got, ref_rows, tol, errs):
+            bad[f"block{l} {name}"] = errs[name]
+        if first:
+            # rows of the table the block never references stay zero
+            probe = rng.integers(0, spec.type_rows[s], size=4096)
+            probe = probe[~np.isin(probe, mb.input_ids[s])]
+            zrows = demb[s].index_select(0, torch.as_tensor(probe, device=DEV))
+            assert torch.count_nonzero(zrows).item() == 0, f"block{l} demb[{s}] untouched rows"
+    # ---- weight gradients on sampled columns, reduced over every row
+    cols = np.sort(rng.choice(d_in, size=2, replace=False))
+    outs = np.sort(rng.choice(d_out, size=16, replace=False))
+    c_t = torch.as_tensor(cols, device=DEV)
+    o_t = torch.as_tensor(outs, device=DEV)
+    h_c = []
+    for t in range(T):
+        if blk.n_src[t] == 0:
+            h_c.append(np.zeros((0, cols.size)))
+            continue
+        narrow = tables[t].index_select(1, c_t)
+        if ids[t] is not None:
+            narrow = narrow.index_select(0, ids[t])
+        h_c.append(narrow[: blk.n_src[t]].to(torch.float64).cpu().numpy())
+    dy_c = [to64(dy[t].index_select(1, o_t)) for t in range(T)]
+    g = oracle.block_backward(blk, h_c, [w[np.ix_(cols, outs)] for w in w_rel64],
+                              [w[np.ix_(cols, outs)] for w in w_self64], dy_c,
+                              want_dh=[False] * T, want_dw=True)
+    for r in range(R):
+        got = to64(dw_rel[r].index_select(0, c_t).index_select(1, o_t))
+        if not _check(f"dw_rel[{r}]", got, g["dw_rel"][r], tol, errs):
+            bad[f"block{l} dw_rel[{r}]"] = errs[f"dw_rel[{r}]"]
+    for t in range(T):
+        got = to64(dw_self[t].index_select(0, c_t).index_select(1, o_t))
+        if not _check(f"dw_self[{t}]", got, g["dw_self"][t], tol, errs):
+            bad[f"block{l} dw_self[{t}]"] = errs[f"dw_self[{t}]"]
+    print(f"[fullsize] {spec.name} block {l}: worst {max(errs.values()):.3g} "
+          f"({max(errs, key=errs.get)})", flush=True)
+    del tables, ids, ws, y, dy, dw_rel, dw_self, dh, demb, inputs
+    torch.cuda.empty_cache()
+    return blk
+
+
+@pytest.mark.parametrize("index", range(5))
+def test_full_size_sampled_parity(index):
+    spec = synth.config(index)
+    torch.manual_seed(0)
+    mb = synth.sample_minibatch(spec, device=DEV)
     rng = np.random.default_rng(1000 + index)
     bad = {}
-    for l, blk in enumerate(mb.blocks):
-        print(f"[fullsize] {spec.name} block {l}: nnz {blk.nnz}", flush=True)
-        d_in, d_out = spec.dims[l], spec.dims[l + 1]
-        first, last = l == 0, l == L - 1
-        # ---- seeded inputs
-        if first:
-            tables = [synth.normal_table(spec.type_rows[t], d_in, tdt, 7000 + 10 * index + t,
-                                         device=DEV) for t in range(T)]
-            ids = [torch.as_tensor(mb.input_ids[t]).to(DEV) for t in range(T)]
-        else:
-            tables = [torch.relu(synth.normal_table(max(blk.n_src[t], 1), d_in, tdt,
-                                                    8000 + 100 * index + 10 * l + t, device=DEV))
-                      for t in range(T)]
-            ids = [None] * T
-        w_rel, w_self, _ = synth.block_weights(T, R, d_in, d_out, tdt, 900 + 10 * index + l)
-        gen = torch.Generator(device=DEV)
-        gen.manual_seed(5000 + 10 * index + l)
-        dy = [torch.randn((n, d_out), generator=gen, device=DEV, dtype=torch.float32)
-              for n in blk.n_dst]
-        if first:
-            grad_types = [t for t in emb if blk.n_src[t] > 0]
-        else:
-            grad_types = [t for t in range(T) if blk.n_src[t] > 0]
-        mask = 0
-        for t in grad_types:
-            mask |= 1 << t
-        # ---- GPU, benchmark flags
-        dblk = rgcn.DeviceBlock(blk, mask, DEV)
-        params = rgcn.Params(spec.dtype, d_in, d_out, [w.to(DEV) for w in w_rel],
-                             [w.to(DEV) for w in w_self])
-        ws = rgcn.new_workspace(dblk, params, DEV)
-        inputs = rgcn.Inputs(tables, ids)
-        y = [torch.empty((n, d_out), dtype=tdt, device=DEV) if n > 0 else None for n in blk.n_dst]
-        f32 = torch.float32
-        dw_rel = [torch.empty((d_in, d_out), dtype=f32, device=DEV) for _ in range(R)]
-        dw_self = [torch.empty((d_in, d_out), dtype=f32, device=DEV) for _ in range(T)]
-        dh = [None] * T
-        demb = None
-        if first:
-            demb = [torch.zeros((spec.type_rows[t], d_in), dtype=f32, device=DEV)
-                    if t in grad_types else None for t in range(T)]
-            if not grad_types:
-                demb = None
-        else:
-            dh = [torch.empty((blk.n_src[t], d_in), dtype=f32, device=DEV)
-                  if t in grad_types else None for t in range(T)]
-        fwd_flags = 0 if last else rgcn.RGCN_FUSE_RELU
-        bwd_flags = rgcn.RGCN_IDS_UNIQUE if first else rgcn.RGCN_INPUT_RELU
-        rgcn.rgcn_block_plan(dblk, params, ws)
-        rgcn.rgcn_block_aggregate(dblk, inputs, params, ws, fwd_flags)
-        rgcn.rgcn_block_transform(dblk, params, y, ws, fwd_flags)
-        rgcn.rgcn_block_backward_dense(dblk, params, dy, dw_rel, dw_self, None, ws, bwd_flags)
-        rgcn.rgcn_block_backward_sparse(dblk, inputs, params, dh, demb, ws, bwd_flags)
-        torch.cuda.synchronize()
+    for l in range(spec.num_layers):
+        _block_parity(spec, mb, index, l, rng, bad)
+    assert not bad, f"full-size parity failures (tol {TOL[spec.dtype]}): {bad}"
 
-        w_rel64 = [to64(w) for w in w_rel]
-        w_self64 = [to64(w) for w in w_self]
-        errs = {}
-        # ---- sampled output rows
-        keep = [_dst_sample(blk, t, rng) for t in range(T)]
-        sub, src_map = oracle.sub_block(blk, keep)
-        h_sub = [_input_rows(tables, ids, t, src_map[t]) for t in range(T)]
-        y_ref = oracle.block_forward(sub, h_sub, w_rel64, w_self64, relu=not last)
-        for t in range(T):
-            if keep[t].size:
-                got = to64(y[t].index_select(0, torch.as_tensor(keep[t], device=DEV)))
-                if not _check(f"y[{t}]", got, y_ref[t], tol, errs):
-                    bad[f"block{l} y[{t}]"] = errs[f"y[{t}]"]
-        # ---- sampled input / embedding gradient rows
-        for s in grad_types:
-            srows = _src_sample(blk, s, rng)
-            keep_b = _rows_referencing(blk, s, srows)
-            sub_b, map_b = oracle.sub_block(blk, keep_b)
-            h_b = [_input_rows(tables, ids, t, map_b[t]) for t in range(T)]
-            dy_b = [to64(dy[t].index_select(0, torch.as_tensor(keep_b[t], device=DEV)))
-                    for t in range(T)]
-            want = [t == s for t in range(T)]
-            g = oracle.block_backward(sub_b, h_b, w_rel64, w_self64, dy_b,
-                                      input_relu=not first, want_dh=want, want_dw=False)
-            order = np.argsort(map_b[s], kind="stable")
-            pos = order[np.searchsorted(map_b[s][order], srows)]
-            ref_rows = g["dh_src"][s][pos]
-            if first:
-                gid = ids[s].index_select(0, torch.as_tensor(srows, device=DEV))
-                got = to64(demb[s].index_select(0, gid))
-                name = f"demb[{s}]"
-            else:
-                got = to64(dh[s].index_select(0, torch.as_tensor(srows, device=DEV)))
-                name = f"dh[{s}]"
-            if not _check(name, got, ref_rows, tol, errs):
-                bad[f"block{l} {name}"] = errs[name]
-            if first:
-                # rows of the table the block never references stay zero
-                probe = rng.integers(0, spec.type_rows[s], size=4096)
-                probe = probe[~np.isin(probe, mb.input_ids[s])]
-                zrows = demb[s].index_select(0, torch.as_tensor(probe, device=DEV))
-                assert torch.count_nonzero(zrows).item() == 0, f"block{l} demb[{s}] untouched rows"
-        # ---- weight gradients on sampled columns, reduced over every row
-        cols = np.sort(rng.choice(d_in, size=2, replace=False))
-        outs = np.sort(rng.choice(d_out, size=16, replace=False))
-        c_t = torch.as_tensor(cols, device=DEV)
-        o_t = torch.as_tensor(outs, device=DEV)
-        h_c = []
-        for t in range(T):
-            if blk.n_src[t] == 0:
-                h_c.append(np.zeros((0, cols.size)))
-                continue
-            narrow = tables[t].index_select(1, c_t)
-            if ids[t] is not None:
-                narrow = narrow.index_select(0, ids[t])
-            h_c.append(narrow[: blk.n_src[t]].to(torch.float64).cpu().numpy())
-        dy_c = [to64(dy[t].index_select(1, o_t)) for t in range(T)]
-        g = oracle.block_backward(blk, h_c, [w[np.ix_(cols, outs)] for w in w_rel64],
-                                  [w[np.ix_(cols, outs)] for w in w_self64], dy_c,
-                                  want_dh=[False] * T, want_dw=True)
-        for r in range(R):
-            got = to64(dw_rel[r].index_select(0, c_t).index_select(1, o_t))
-            if not _check(f"dw_rel[{r}]", got, g["dw_rel"][r], tol, errs):
-                bad[f"block{l} dw_rel[{r}]"] = errs[f"dw_rel[{r}]"]
-        for t in range(T):
-            got = to64(dw_self[t].index_select(0, c_t).index_select(1, o_t))
-            if not _check(f"dw_self[{t}]", got, g["dw_self"][t], tol, errs):
-                bad[f"block{l} dw_self[{t}]"] = errs[f"dw_self[{t}]"]
-        print(f"[fullsize] {spec.name} block {l}: worst {max(errs.values()):.3g} "
-              f"({max(errs, key=errs.get)})", flush=True)
-        del tables, ids, ws, y, dy, dw_rel, dw_self, dh, demb, inputs
-        torch.cuda.empty_cache()
-    assert not bad, f"full-size parity failures (tol {tol}): {bad}"
+
+def test_full_size_skewed_first_block():
+    """Block 0 of the billion-edge workload with power-law sources (p(rank k) proportional
+    to (k + 1)^-0.8): the 25.6 GB learnable table, hub sources with transpose segments of
+    thousands of edges (the LDS bitonic sort of the plan at its upper end) and a reordered
+    backward schedule."""
+    spec = synth.skewed_config(4)
+    mb = synth.sample_minibatch(spec, device=DEV)
+    blk = mb.blocks[0]
+    longest = 0
+    for rel in blk.rels:
+        if rel.src_type == 0 and rel.nnz:
+            longest = max(longest, int(np.bincount(np.asarray(rel.indices)).max()))
+    print(f"[fullsize] skewed block 0: longest transpose segment {longest}", flush=True)
+    assert longest > 4096
+    rng = np.random.default_rng(4242)
+    bad = {}
+    _block_parity(spec, mb, 9, 0, rng, bad)
+    assert not bad, f"skewed full-size parity failures (tol {TOL[spec.dtype]}): {bad}"
+
+
+def test_full_size_benchmark_step_overlap_is_bitwise_serial():
+    """The billion-edge workload through the chain driver exactly as the benchmark steps it
+    (forward plans first, the backward plans on a second stream from the end of block 0's
+    aggregate stage), from poisoned workspaces, against the serial order of the same calls:
+    every output and gradient bit for bit, including the embedding gradient of every table
+    row the block names."""
+    from paper_2406_06022_amd import chain
+    from tests.test_gpu_chain import poison_stack
+
+    spec = synth.config(4)
+    mb = synth.sample_minibatch(spec, device=DEV)
+    tdt = synth.torch_dtype(spec.dtype)
+    T, R, L = len(spec.ntype_names), len(spec.rels), spec.num_layers
+    tables = [synth.normal_table(spec.type_rows[t], spec.dims[0], tdt, spec.seed * 10 + t,
+                                 device=DEV) for t in range(T)]
+    ids = [torch.as_tensor(mb.input_ids[t]).to(DEV) for t in range(T)]
+    weights = []
+    for l in range(L):
+        w_rel, w_self, _ = synth.block_weights(T, R, spec.dims[l], spec.dims[l + 1], tdt,
+                                               spec.seed * 100 + l)
+        weights.append(([w.to(DEV) for w in w_rel], [w.to(DEV) for w in w_self], None))
+    emb = [t for t in range(T) if spec.featureless[t]]
+    stack = chain.MiniBatchStack(mb.blocks, tables, ids, weights, spec.dtype, spec.dims,
+                                 emb_types=emb, device=DEV)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(spec.seed + 1)
+    dy = [torch.randn((n, spec.dims[-1]), generator=gen, device=DEV, dtype=torch.float32)
+          if n > 0 else None for n in mb.blocks[-1].n_dst]
+
+    def run(overlap):
+        poison_stack(stack)
+        for t in emb:
+            stack.demb[t].zero_()
+        print(f"[fullsize] benchmark step, overlapped plan {overlap}", flush=True)
+        stack.step(dy, overlap_plan=overlap)
+        torch.cuda.synchronize()
+        out = [x.clone() for x in stack.y[-1] if x is not None]
+        for l in range(L):
+            out += [x.clone() for x in stack.dw_rel[l]] + [x.clone() for x in stack.dw_self[l]]
+            if stack.dh[l] is not None:
+                out += [x.clone() for x in stack.dh[l] if x is not None]
+        out += [stack.demb[t].index_select(0, ids[t]) for t in emb]
+        return out
+
+    got = run(True)
+    want = run(False)
+    assert len(got) == len(want)
+    for i, (g, w_) in enumerate(zip(got, want)):
+        assert not torch.isnan(w_).any(), f"serial output {i} left unwritten"
+        assert torch.equal(g, w_), f"output {i} differs between the overlapped and serial step"
