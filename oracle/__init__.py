@@ -25,7 +25,10 @@ _SRC = os.path.join(_HERE, "rgcn_oracle.c")
 _SRC_SAMPLE = os.path.join(_HERE, "sample_oracle.c")
 _SRC_LP = os.path.join(_HERE, "lp_oracle.c")
 _SRC_FEAT = os.path.join(_HERE, "feature_oracle.c")
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# ORACLE_SANITIZE=1 selects an AddressSanitizer / UndefinedBehaviorSanitizer build of the
+# same sources (host code; loading it needs the ASan runtime preloaded)
+_LIB_PATH = os.path.join(_HERE, "liboracle_san.so" if os.environ.get("ORACLE_SANITIZE") == "1"
+                         else "liboracle.so")
 _lib = None
 
 

@@ -30,14 +30,39 @@
  *                   + [j < n_dst[s]] dY_s[j] W_self_s^T
  *      dE_t[ids_t[j]] += dH_t[j]                (embedding-gradient scatter-add)
  *
- *  and the integer plan (degrees, the degree-sorted schedules, and the CSC transpose
- *  of every relation as a stable counting sort of edge positions by source row), and a
- *  sparse Adagrad step on the touched rows of a learnable table.
+ *  and the integer plan (degrees, and the CSC transpose of every relation as a stable
+ *  counting sort of edge positions by source row), and a sparse Adagrad step on the
+ *  touched rows of a learnable table.  The order in which a GPU processes segments is
+ *  not part of the method (any order gives the same sums) and is not modelled here.
  */
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* Threads of the loops below.  Each loop marked "omp" hands whole output elements to one
+ * thread, which computes them in exactly the order written, so every result is the same
+ * bit for bit whatever the thread count. */
+void orc_set_threads(int n)
+{
+#ifdef _OPENMP
+    omp_set_num_threads(n > 0 ? n : 1);
+#else
+    (void)n;
+#endif
+}
+
+int orc_get_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
 
 typedef struct {
     int32_t src_type;
@@ -84,6 +109,7 @@ void orc_degrees(const int32_t *indptr, int64_t n_dst, int32_t *deg)
 void orc_mean_aggregate(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
                         const double *h_src, int64_t d, double *m)
 {
+#pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < n_dst; ++i) {
         int64_t deg = indptr[i + 1] - indptr[i];
         for (int64_t c = 0; c < d; ++c) {
@@ -109,6 +135,7 @@ int orc_block_forward(const orc_block *b, int64_t d_in, int64_t d_out,
         if (nd == 0) continue;
         double *yt = y[t];
         /* self-loop term (and bias) */
+#pragma omp parallel for schedule(static)
         for (int64_t i = 0; i < nd; ++i)
             for (int64_t o = 0; o < d_out; ++o) {
                 double acc = bias && bias[t] ? bias[t][o] : 0.0;
@@ -123,6 +150,7 @@ int orc_block_forward(const orc_block *b, int64_t d_in, int64_t d_out,
             double *m = (double *)malloc((size_t)(nd * d_in) * sizeof(double));
             if (!m) return -1;
             orc_mean_aggregate(rel->indptr, rel->indices, nd, h_src[rel->src_type], d_in, m);
+#pragma omp parallel for schedule(static)
             for (int64_t i = 0; i < nd; ++i)
                 for (int64_t o = 0; o < d_out; ++o) {
                     double acc = 0.0;
@@ -155,12 +183,14 @@ int orc_block_backward(const orc_block *b, int64_t d_in, int64_t d_out,
     for (int t = 0; t < b->num_types; ++t) {
         int64_t nd = b->n_dst[t];
         if (dbias && dbias[t])
+#pragma omp parallel for schedule(static)
             for (int64_t o = 0; o < d_out; ++o) {
                 double acc = 0.0;
                 for (int64_t i = 0; i < nd; ++i) acc += dy[t][i * d_out + o];
                 dbias[t][o] = acc;
             }
         if (dw_self && dw_self[t])
+#pragma omp parallel for schedule(static)
             for (int64_t c = 0; c < d_in; ++c)
                 for (int64_t o = 0; o < d_out; ++o) {
                     double acc = 0.0;
@@ -178,6 +208,7 @@ int orc_block_backward(const orc_block *b, int64_t d_in, int64_t d_out,
             double *m = (double *)malloc((size_t)(nd * d_in + 1) * sizeof(double));
             if (!m) return -1;
             orc_mean_aggregate(rel->indptr, rel->indices, nd, h_src[rel->src_type], d_in, m);
+#pragma omp parallel for schedule(static)
             for (int64_t c = 0; c < d_in; ++c)
                 for (int64_t o = 0; o < d_out; ++o) {
                     double acc = 0.0;
@@ -195,6 +226,7 @@ int orc_block_backward(const orc_block *b, int64_t d_in, int64_t d_out,
             double *g = dh_src[s];
             for (int64_t e = 0; e < ns * d_in; ++e) g[e] = 0.0;
             /* self-loop: rows j < n_dst[s] receive dY_s[j] W_self_s^T */
+#pragma omp parallel for schedule(static)
             for (int64_t j = 0; j < nds; ++j)
                 for (int64_t c = 0; c < d_in; ++c) {
                     double acc = 0.0;
@@ -202,23 +234,24 @@ int orc_block_backward(const orc_block *b, int64_t d_in, int64_t d_out,
                         acc += dy[s][j * d_out + o] * w_self[s][c * d_out + o];
                     g[j * d_in + c] += acc;
                 }
-            /* every edge (i <- j) of a relation leaving s sends dY[i] W_r^T / deg_r(i) */
+            /* every edge (i <- j) of a relation leaving s sends dY[i] W_r^T / deg_r(i);
+             * column c of every row takes its terms in ascending (r, i, k) order */
             for (int r = 0; r < b->num_rels; ++r) {
                 const orc_relation *rel = &b->rels[r];
                 if (rel->src_type != s) continue;
                 int t = rel->dst_type;
-                for (int64_t i = 0; i < b->n_dst[t]; ++i) {
-                    int64_t deg = rel->indptr[i + 1] - rel->indptr[i];
-                    for (int64_t k = rel->indptr[i]; k < rel->indptr[i + 1]; ++k) {
-                        int64_t j = rel->indices[k];
-                        for (int64_t c = 0; c < d_in; ++c) {
+#pragma omp parallel for schedule(static)
+                for (int64_t c = 0; c < d_in; ++c)
+                    for (int64_t i = 0; i < b->n_dst[t]; ++i) {
+                        int64_t deg = rel->indptr[i + 1] - rel->indptr[i];
+                        for (int64_t k = rel->indptr[i]; k < rel->indptr[i + 1]; ++k) {
+                            int64_t j = rel->indices[k];
                             double acc = 0.0;
                             for (int64_t o = 0; o < d_out; ++o)
                                 acc += dy[t][i * d_out + o] * w_rel[r][c * d_out + o];
                             g[j * d_in + c] += acc / (double)deg;
                         }
                     }
-                }
             }
             if (input_relu)
                 for (int64_t e = 0; e < ns * d_in; ++e)
@@ -290,21 +323,5 @@ int orc_csc(int64_t n_src, int64_t n_dst, const int32_t *indptr, const int32_t *
             csc_eid[p] = (int32_t)k;
         }
     free(fill);
-    return 0;
-}
-
-/* Stable counting sort of n items by key in [0, nbuckets): order[p] = item index of the
- * p-th item when items are listed bucket by bucket, ascending item index inside a bucket. */
-int orc_stable_bucket_order(int64_t n, const int32_t *key, int32_t nbuckets, int32_t *order)
-{
-    int64_t *start = (int64_t *)calloc((size_t)nbuckets + 1, sizeof(int64_t));
-    if (!start) return -1;
-    for (int64_t x = 0; x < n; ++x) {
-        if (key[x] < 0 || key[x] >= nbuckets) { free(start); return -1; }
-        start[key[x] + 1] += 1;
-    }
-    for (int32_t q = 0; q < nbuckets; ++q) start[q + 1] += start[q];
-    for (int64_t x = 0; x < n; ++x) order[start[key[x]]++] = (int32_t)x;
-    free(start);
     return 0;
 }

@@ -37,6 +37,18 @@ rgcn_status hip_fail(hipError_t e, const char *what) {
         if (_e != hipSuccess) return hip_fail(_e, what); \
     } while (0)
 
+// A dtype field of a caller's struct read as the integer it holds: a caller may store any
+// value there, and loading a value outside the enumeration as the enum type is undefined.
+inline int32_t dtype_code(const rgcn_dtype *p) {
+    int32_t v;
+    memcpy(&v, p, sizeof(v));
+    return v;
+}
+inline bool dtype_known(const rgcn_dtype *p) {
+    const int32_t v = dtype_code(p);
+    return v == RGCN_F32 || v == RGCN_BF16;
+}
+
 inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 inline bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 inline bool aligned4(const void *p) { return ((uintptr_t)p & 3u) == 0; }
@@ -117,8 +129,8 @@ rgcn_status check_block(const rgcn_block *b) {
 
 rgcn_status check_params(const rgcn_block *b, const rgcn_params *p) {
     if (!p) return fail(RGCN_ERR_INVALID_ARG, "params is NULL");
-    if (p->dtype != RGCN_F32 && p->dtype != RGCN_BF16)
-        return fail(RGCN_ERR_DTYPE, "unknown dtype %d", (int)p->dtype);
+    if (!dtype_known(&p->dtype))
+        return fail(RGCN_ERR_DTYPE, "unknown dtype %d", (int)dtype_code(&p->dtype));
     const int vec = p->dtype == RGCN_BF16 ? 8 : 4;
     if (p->d_in <= 0 || p->d_out <= 0)
         return fail(RGCN_ERR_INVALID_ARG, "d_in / d_out must be positive");
@@ -741,7 +753,7 @@ rgcn_status rgcn_sparse_adagrad(int64_t n, const int64_t *rows, int64_t num_rows
                                 float *grad, float *state, void *table, int64_t ld,
                                 rgcn_dtype dtype, float lr, float eps, unsigned flags,
                                 hipStream_t stream) {
-    if (dtype != RGCN_F32 && dtype != RGCN_BF16) return fail(RGCN_ERR_DTYPE, "unknown dtype");
+    if (!dtype_known(&dtype)) return fail(RGCN_ERR_DTYPE, "unknown dtype");
     const int vec = dtype == RGCN_BF16 ? 8 : 4;
     if (n < 0 || num_rows < 0 || d < 0) return fail(RGCN_ERR_SHAPE, "negative size");
     if (d % vec || ld < d || ld % vec)
@@ -905,7 +917,7 @@ namespace {
 
 rgcn_status lp_args(const rgcn_lp_batch *b, LpArgs &a) {
     if (!b) return fail(RGCN_ERR_INVALID_ARG, "batch is NULL");
-    if (b->dtype != RGCN_F32 && b->dtype != RGCN_BF16) return fail(RGCN_ERR_DTYPE, "unknown dtype");
+    if (!dtype_known(&b->dtype)) return fail(RGCN_ERR_DTYPE, "unknown dtype");
     const int vec = b->dtype == RGCN_BF16 ? 8 : 4;
     if (b->d <= 0 || b->d % vec || b->d > 256 * vec)
         return fail(RGCN_ERR_UNSUPPORTED, "d %d must be a positive multiple of %d, at most %d",
@@ -1016,7 +1028,7 @@ rgcn_status rgcn_featureless_mean(int32_t num_rels, const rgcn_feature_relation 
                                   int64_t num_nodes, int32_t d, rgcn_dtype dtype, void *out,
                                   int64_t out_ld, void *workspace, unsigned flags,
                                   hipStream_t stream) {
-    if (dtype != RGCN_F32 && dtype != RGCN_BF16) return fail(RGCN_ERR_DTYPE, "unknown dtype");
+    if (!dtype_known(&dtype)) return fail(RGCN_ERR_DTYPE, "unknown dtype");
     const int vec = dtype == RGCN_BF16 ? 8 : 4;
     if (num_rels < 1 || num_rels > kMaxRels || !rels)
         return fail(RGCN_ERR_INVALID_ARG, "num_rels %d outside [1, %d] or rels NULL", num_rels,

@@ -15,7 +15,10 @@ import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "librgcn.so")
+# RGCN_LIB_SANITIZE=1 loads the host-sanitized build of the same sources (CPU-side checks
+# of the argument validation; needs the ASan runtime preloaded)
+LIB_PATH = os.path.join(_HERE, "librgcn_san.so" if os.environ.get("RGCN_LIB_SANITIZE") == "1"
+                        else "librgcn.so")
 
 RGCN_F32, RGCN_BF16 = 0, 1
 RGCN_MAX_TYPES, RGCN_MAX_RELS = 16, 64

@@ -472,3 +472,27 @@ def test_sparse_adagrad_on_scattered_gradient_of_a_block(orc):
         np.testing.assert_allclose(s2[e], s, rtol=1e-15)
         np.testing.assert_allclose(t2[e], table0[e] - 0.02 * g["dh_src"][0][j] / (np.sqrt(s) + 1e-8),
                                    rtol=1e-15)
+
+
+def test_results_do_not_depend_on_the_thread_count(orc):
+    """The oracle's parallel loops give every output element to one thread, which adds its
+    terms in the written order: forward and backward are bit-identical on 1 and 5 threads."""
+    rng = np.random.default_rng(77)
+    blk = synth.random_block(rng, [300, 200], [120, 80], [(0, 1), (1, 0), (0, 0), (1, 1)], 9)
+    h, w_rel, w_self, b, dy = _rand_inputs(rng, blk, 6, 5)
+    before = orc.get_threads()
+    runs = []
+    try:
+        for n in (1, 5):
+            orc.set_threads(n)
+            y = orc.block_forward(blk, h, w_rel, w_self, b)
+            g = orc.block_backward(blk, h, w_rel, w_self, dy, input_relu=True)
+            runs.append((y, g))
+    finally:
+        orc.set_threads(before)
+    (y1, g1), (y5, g5) = runs
+    for a, c in zip(y1, y5):
+        assert np.array_equal(a, c)
+    for key in ("dw_rel", "dw_self", "dbias", "dh_src"):
+        for a, c in zip(g1[key], g5[key]):
+            assert np.array_equal(a, c), key
