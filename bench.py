@@ -123,8 +123,47 @@ def build_stack(index: int, device: str):
     return spec, mb, tables, ids, weights, stack, dy
 
 
+def survey_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
+    """Algorithmic bytes of one launch of a stage's kernel as the method defines them (no
+    cache reuse), the figures the roofline fractions use:
+      aggregate (gather + segmented mean): per relation 4 (n_dst + 1) offsets, 4 nnz source
+        indices, nnz gathered rows of d_in b bytes and one aggregate row of d_in b bytes per
+        destination row written; at the input layer 8 bytes of global id per source row;
+      sparse (transposed sum, embedding scatter-add): per relation leaving a type whose
+        gradient is requested, one fp32 row of d_in per edge plus 8 bytes of transpose
+        entry; per source row one fp32 gradient row written, and at the input layer, where
+        the scatter-add into the embedding gradient is fused with the sum (distinct ids),
+        that row read once more (the read half of its read-add-write)."""
+    b = 2 if spec.dtype == "bf16" else 4
+    d_in = spec.dims[layer]
+    T = len(blk.n_src)
+    if stage == "aggregate":
+        tot = 0.0
+        for rel in blk.rels:
+            nd = blk.n_dst[rel.dst_type]
+            nnz = len(rel.indices)
+            tot += 4 * (nd + 1) + 4 * nnz + nnz * d_in * b + nd * d_in * b
+        if layer == 0:
+            tot += 8 * sum(blk.n_src)
+        return tot
+    if stage == "sparse":
+        tot = 0.0
+        for s in range(T):
+            if not (dev_blk.grad_src_types >> s & 1) or blk.n_src[s] == 0:
+                continue
+            for rel in blk.rels:
+                if rel.src_type == s and blk.n_dst[rel.dst_type] > 0:
+                    tot += len(rel.indices) * (d_in * 4 + 8)
+            tot += blk.n_src[s] * d_in * 4 * (2 if layer == 0 else 1)
+        return tot
+    raise ValueError(stage)
+
+
 def algorithmic_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
-    """Bytes the method must move for one launch of a stage's kernel (no cache reuse)."""
+    """Bytes one launch of a stage's kernel moves in this implementation's data layout (no
+    cache reuse): the method's bytes (survey_bytes) plus what the layout adds -- the
+    self-loop rows copied into the K-concatenated operand, an 8-byte id per gathered edge,
+    the fp32 self-loop input-side rows and the ReLU-mask input rows of the backward."""
     b = 2 if spec.dtype == "bf16" else 4
     d_in = spec.dims[layer]
     T = len(blk.n_src)
@@ -192,15 +231,43 @@ def backward_flops(spec, blk, grad_src_types: int, layer: int) -> float:
     return tot
 
 
-def cpu_baseline(spec, mb, tables, ids, weights, budget_s: float):
-    """The CPU oracle (single thread, fp64) on a bounded sample of block 0: the first n
-    destination rows of every type with their full sampled segments, forward + backward
-    (weight gradients and the embedding-type input gradient).  n grows until the run
-    takes about budget_s seconds.  Returns edges/s of the sample."""
+def host_info() -> dict:
+    """The host the CPU baseline ran on."""
+    info = {"nproc": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0))}
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    info["cpu_model"] = line.split(":", 1)[1].strip()
+                    break
+        with open("/proc/meminfo") as f:
+            for line in f:
+                if line.startswith("MemTotal"):
+                    info["ram_gib"] = round(int(line.split()[1]) / (1 << 20), 1)
+                    break
+    except OSError:
+        pass
+    return info
+
+
+def oracle_threads() -> int:
+    """Threads for the all-cores oracle run: the CPUs this process may use, at most 16 (a
+    one-GPU machine's share of its host)."""
+    return max(1, min(len(os.sched_getaffinity(0)), 16))
+
+
+def cpu_baseline(spec, mb, tables, ids, weights, budget_s: float, threads: int):
+    """The CPU oracle (fp64) on a bounded sample of block 0: the first n destination rows
+    of every type with their full sampled segments, forward + backward (weight gradients
+    and the embedding-type input gradient), on `threads` threads (the oracle's loops hand
+    whole output elements to one thread, so results do not depend on it).  n grows until
+    the run takes about budget_s seconds.  Returns edges/s of the sample."""
     import numpy as np
     import torch
 
     import oracle
+
+    oracle.set_threads(threads)
 
     blk = mb.blocks[0]
     T = len(blk.n_src)
@@ -224,7 +291,7 @@ def cpu_baseline(spec, mb, tables, ids, weights, budget_s: float):
         el = time.perf_counter() - t0
         nnz = sum(len(r.indices) for r in sub.rels)
         result = (nnz / el, nnz, el, sum(sub.n_dst))
-        if el > budget_s / 3 or n >= 1 << 16:
+        if el > budget_s / 3 or n >= 1 << 20:
             break
         n = int(n * max(2.0, min(8.0, budget_s / 2 / max(el, 1e-3))))
     return result
@@ -672,6 +739,171 @@ def measure_lp(dev, args):
     return out
 
 
+def time_steps(stack, dy, steps: int, warmup: int) -> dict:
+    """warmup untimed steps, then `steps` steps timed by the wall clock (synchronised on
+    both sides) and by HIP events: one pair around each whole step on the stream the
+    library launches on (the plan's second stream joins it before the step ends), and one
+    pair around each stage.  Returns the wall ms per step, per-step event statistics and
+    the mean ms of every (stage, block)."""
+    import statistics
+
+    import torch
+
+    for _ in range(warmup):
+        stack.step(dy)
+    torch.cuda.synchronize()
+    events = []
+
+    def timer(tag, edge):
+        ev = torch.cuda.Event(enable_timing=True)
+        ev.record()
+        events[-1].setdefault(tag, [None, None])[edge] = ev
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        events.append({})
+        timer("step", 0)
+        stack.step(dy, timer=timer)
+        timer("step", 1)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps * 1e3
+    stage = {}
+    for ev in events:
+        for tag, (a, b) in ev.items():
+            stage.setdefault(tag, []).append(a.elapsed_time(b))
+    per_step = stage.pop("step")
+    q = sorted(per_step)
+    stats = {"median": round(statistics.median(q), 4), "mean": round(statistics.fmean(q), 4),
+             "min": round(q[0], 4), "max": round(q[-1], 4),
+             "stdev": round(statistics.pstdev(q), 4), "n": len(q)}
+    return {"wall_ms": wall, "step_stats": stats,
+            "stage_avg": {tag: sum(v) / len(v) for tag, v in stage.items()}}
+
+
+def block_ms(stack, avg) -> list:
+    return [round(sum(avg.get((s, l), 0.0)
+                      for s in ("plan", "aggregate", "transform", "dense", "sparse")), 4)
+            for l in range(stack.L)]
+
+
+def stage_rooflines(spec, mb, stack, avg) -> dict:
+    """Every aggregate and sparse stage: its time, the method's bytes (survey_bytes) and
+    the fraction of the 8 TB/s peak they make, and this layout's bytes beside them."""
+    out = {}
+    for l in range(stack.L):
+        for s in ("aggregate", "sparse"):
+            if (s, l) not in avg:
+                continue
+            t_ms = avg[(s, l)]
+            byts = survey_bytes(spec, mb.blocks[l], stack.blocks[l], s, l)
+            impl = algorithmic_bytes(spec, mb.blocks[l], stack.blocks[l], s, l)
+            gbs = byts / (t_ms * 1e-3) / 1e9
+            out[f"{s}[{l}]"] = {"ms": round(t_ms, 4), "bytes": byts, "GB/s": round(gbs, 1),
+                                "frac": round(gbs / HBM_PEAK_GBS, 4), "impl_bytes": impl,
+                                "impl_GB/s": round(impl / (t_ms * 1e-3) / 1e9, 1)}
+    return out
+
+
+def mfma_stages(spec, mb, stack, avg):
+    mfma, mfma_bwd = {}, {}
+    for l in range(stack.L):
+        fl = transform_flops(spec, mb.blocks[l], l)
+        tf = fl / (avg[("transform", l)] * 1e-3) / 1e12
+        mfma[f"transform[{l}]"] = {"ms": round(avg[("transform", l)], 4), "TFLOP/s": round(tf, 1),
+                                   "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)}
+        fl = backward_flops(spec, mb.blocks[l], stack.blocks[l].grad_src_types, l)
+        tf = fl / (avg[("dense", l)] * 1e-3) / 1e12
+        mfma_bwd[f"dense[{l}]"] = {"ms": round(avg[("dense", l)], 4), "TFLOP/s": round(tf, 1),
+                                   "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)}
+    return mfma, mfma_bwd
+
+
+def measure_skewed(args, tables, dev):
+    """The billion-edge workload with power-law sources (p(rank k) proportional to
+    (k + 1)^-0.8 through a fixed id bijection), the backward's load-balance stress: the
+    same tables and weights, a mini-batch sampled with skewed sources, full steps timed as
+    the main workload is."""
+    import numpy as np
+    import torch
+
+    from paper_2406_06022_amd import chain, synth
+
+    spec = synth.skewed_config(args.config)
+    t0 = time.perf_counter()
+    mb = synth.sample_minibatch(spec, device=dev)
+    log(f"sampled {spec.name}: blocks nnz {[b.nnz for b in mb.blocks]} in "
+        f"{time.perf_counter() - t0:.1f}s")
+    T = len(spec.ntype_names)
+    tdt = synth.torch_dtype(spec.dtype)
+    ids = [torch.as_tensor(mb.input_ids[t]).to(dev) for t in range(T)]
+    weights = []
+    for l in range(spec.num_layers):
+        w_rel, w_self, _ = synth.block_weights(T, len(spec.rels), spec.dims[l],
+                                               spec.dims[l + 1], tdt, spec.seed * 100 + l)
+        weights.append(([w.to(dev) for w in w_rel], [w.to(dev) for w in w_self], None))
+    emb = [t for t in range(T) if spec.featureless[t]]
+    stack = chain.MiniBatchStack(mb.blocks, tables, ids, weights, spec.dtype, spec.dims,
+                                 emb_types=emb, device=dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(spec.seed + 1)
+    dy = [torch.randn((n, spec.dims[-1]), generator=gen, device=dev, dtype=torch.float32)
+          if n > 0 else None for n in mb.blocks[-1].n_dst]
+    steps = max(3, args.steps // 2)
+    run = time_steps(stack, dy, steps, min(args.warmup, 3))
+    avg = run["stage_avg"]
+    blk = mb.blocks[0]
+    longest, hubs = 0, 0
+    for rel in blk.rels:
+        if stack.blocks[0].grad_src_types >> rel.src_type & 1 and rel.nnz:
+            cnt = np.bincount(np.asarray(rel.indices))
+            longest = max(longest, int(cnt.max()))
+            hubs += int((cnt > 32).sum())
+    roof = stage_rooflines(spec, mb, stack, avg)
+    out = {"workload": spec.name, "skew": spec.skew, "blocks_nnz": [b.nnz for b in mb.blocks],
+           "ms_per_step": round(run["wall_ms"], 4), "step_ms_events": run["step_stats"],
+           "edges_per_s": stack.nnz / (run["wall_ms"] / 1e3),
+           "ms_per_block": block_ms(stack, avg),
+           "plan[0]": round(avg[("plan", 0)], 4), "plan_bwd[0]": round(avg[("plan_bwd", 0)], 4),
+           "sparse[0]": dict(roof["sparse[0]"], kernel="k_transpose_pipe"),
+           "aggregate[0]": roof["aggregate[0]"],
+           "largest_transpose_degree": longest, "sources_over_32_edges": hubs,
+           "csc_radix_path": longest > 16384}
+    del stack
+    torch.cuda.empty_cache()
+    return out
+
+
+def measure_configs(args, dev):
+    """The other workloads (the parity configurations at full size): per-block ms of a
+    full step and the gather's fraction of the HBM peak by the method's bytes."""
+    import torch
+
+    out = {}
+    for index in range(5):
+        if index == args.config:
+            continue
+        spec, mb, tables, ids, weights, stack, dy = build_stack(index, dev)
+        run = time_steps(stack, dy, max(5, args.steps // 2), min(args.warmup, 3))
+        avg = run["stage_avg"]
+        roof = stage_rooflines(spec, mb, stack, avg)
+        mf, mb_ = mfma_stages(spec, mb, stack, avg)
+        out[spec.name] = {"blocks_nnz": [b.nnz for b in mb.blocks],
+                          "ms_per_step": round(run["wall_ms"], 4),
+                          "step_ms_median": run["step_stats"]["median"],
+                          "edges_per_s": stack.nnz / (run["wall_ms"] / 1e3),
+                          "ms_per_block": block_ms(stack, avg),
+                          "aggregate_frac": {k: v["frac"] for k, v in roof.items()
+                                             if k.startswith("aggregate")},
+                          "sparse_frac": {k: v["frac"] for k, v in roof.items()
+                                          if k.startswith("sparse")},
+                          "transform_frac": {k: v["frac"] for k, v in mf.items()},
+                          "dense_frac": {k: v["frac"] for k, v in mb_.items()}}
+        del stack, tables, ids, weights, dy, mb
+        torch.cuda.empty_cache()
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -748,56 +980,20 @@ def main() -> int:
         return 0
     spec, mb, tables, ids, weights, stack, dy = build_stack(args.config, dev)
     log(f"workspace bytes per block {[int(w.numel()) for w in stack.workspaces]}")
-
-    for _ in range(args.warmup):
-        stack.step(dy)
-    torch.cuda.synchronize()
-    log(f"warmup {args.warmup} steps done")
-
-    events = []  # per step: {tag: [start_event, end_event]}
-
-    def timer(tag, edge):
-        ev = torch.cuda.Event(enable_timing=True)
-        ev.record()
-        events[-1].setdefault(tag, [None, None])[edge] = ev
-
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        events.append({})
-        stack.step(dy, timer=timer)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    ms = elapsed / args.steps * 1e3
+    run = time_steps(stack, dy, args.steps, args.warmup)
+    log(f"warmup {args.warmup} and {args.steps} timed steps done")
+    ms = run["wall_ms"]
     nnz = stack.nnz
     value = nnz / (ms / 1e3)
+    avg = run["stage_avg"]
+    per_block = block_ms(stack, avg)
 
-    stage_ms = {}
-    for step_ev in events:
-        for tag, (a, b) in step_ev.items():
-            stage_ms.setdefault(tag, []).append(a.elapsed_time(b))
-    avg = {tag: sum(v) / len(v) for tag, v in stage_ms.items()}
-    per_block = []
-    for l in range(stack.L):
-        per_block.append(round(sum(avg.get((s, l), 0.0)
-                                   for s in ("plan", "aggregate", "transform", "dense", "sparse")), 4))
-
+    rooflines = stage_rooflines(spec, mb, stack, avg)
     # dominant single-kernel stage: the aggregate or sparse stage with the largest time
-    cands = []
-    for l in range(stack.L):
-        for s in ("aggregate", "sparse"):
-            if (s, l) in avg:
-                cands.append((avg[(s, l)], s, l))
-    cands.sort(reverse=True)
-    _, dom_stage, dom_layer = cands[0]
+    dom_key = max(rooflines, key=lambda k: rooflines[k]["ms"])
+    dom = rooflines[dom_key]
+    dom_stage, dom_layer = dom_key.split("[")[0], int(dom_key.split("[")[1][:-1])
     kernel_name = {"aggregate": "k_gather_flat", "sparse": "k_transpose_pipe"}[dom_stage]
-    rooflines = {}
-    for t_ms, s, l in cands:
-        byts = algorithmic_bytes(spec, mb.blocks[l], stack.blocks[l], s, l)
-        gbs = byts / (t_ms * 1e-3) / 1e9
-        rooflines[f"{s}[{l}]"] = {"ms": round(t_ms, 4), "bytes": byts, "GB/s": round(gbs, 1),
-                                  "frac": round(gbs / HBM_PEAK_GBS, 4)}
-    dom = rooflines[f"{dom_stage}[{dom_layer}]"]
     # launch position of the dominant stage within a step's launches of its kernel: the
     # gather runs once per block, input side first; the transposed sum once per requested
     # source type, output side first
@@ -813,18 +1009,7 @@ def main() -> int:
                 break
             position += n
     traffic = read_traffic(kernel_name, spec.name, position)
-    mfma = {}
-    for l in range(stack.L):
-        fl = transform_flops(spec, mb.blocks[l], l)
-        tf = fl / (avg[("transform", l)] * 1e-3) / 1e12
-        mfma[f"transform[{l}]"] = {"ms": round(avg[("transform", l)], 4), "TFLOP/s": round(tf, 1),
-                                   "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)}
-    mfma_bwd = {}
-    for l in range(stack.L):
-        fl = backward_flops(spec, mb.blocks[l], stack.blocks[l].grad_src_types, l)
-        tf = fl / (avg[("dense", l)] * 1e-3) / 1e12
-        mfma_bwd[f"dense[{l}]"] = {"ms": round(avg[("dense", l)], 4), "TFLOP/s": round(tf, 1),
-                                   "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)}
+    mfma, mfma_bwd = mfma_stages(spec, mb, stack, avg)
 
     # attainable streaming bandwidth of this machine: a plain 1 GiB fp32 copy (read + write)
     src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
@@ -841,29 +1026,29 @@ def main() -> int:
 
     cpu = None
     if args.cpu_budget > 0:
-        log("timing the CPU oracle on a sample of block 0")
-        eps, s_nnz, s_el, s_rows = cpu_baseline(spec, mb, tables, ids, weights, args.cpu_budget)
-        cpu = {"value": eps, "unit": "edges/s", "cores": 1, "kind": "oracle",
-               "sample": f"block 0 restricted to its first destination rows per type "
-                         f"({s_rows} rows, {s_nnz} edges, full segments), fp64 forward + "
-                         f"backward (weight grads, embedding-type input grad), {s_el:.1f}s"}
+        host = host_info()
+        nt = oracle_threads()
+        log(f"timing the CPU oracle on a sample of block 0 ({nt} threads, then 1)")
+        res = {}
+        for th in (nt, 1):
+            eps, s_nnz, s_el, s_rows = cpu_baseline(spec, mb, tables, ids, weights,
+                                                    args.cpu_budget, th)
+            res[th] = {"value": eps, "unit": "edges/s", "cores": th, "kind": "oracle",
+                       "sample": f"block 0 restricted to its first destination rows per type "
+                                 f"({s_rows} rows, {s_nnz} edges, full segments), fp64 "
+                                 f"forward + backward (weight grads, embedding-type input "
+                                 f"grad), {th} thread(s), {s_el:.1f}s"}
+        cpu = dict(res[nt])
+        cpu["host"] = host
+        cpu["one_thread"] = {k: res[1][k] for k in ("value", "cores", "sample")}
 
     # the sparse optimizer step of the learnable tables fused into block 0's transposed sum:
     # full training steps (plan, forward, backward, table update) after the others, since
     # they change the tables
     stack.attach_adagrad(lr=0.01, eps=1e-10)
-    ada_ev = []
-    for k in range(args.warmup + args.steps):
-        if k == args.warmup:
-            torch.cuda.synchronize()
-            a0 = time.perf_counter()
-        ada_ev.append({})
-        events.append(ada_ev[-1])
-        stack.step(dy, timer=timer)
-    torch.cuda.synchronize()
-    ada_ms = (time.perf_counter() - a0) / args.steps * 1e3
-    ada_sp = [e[("sparse", 0)][0].elapsed_time(e[("sparse", 0)][1]) for e in ada_ev[args.warmup:]]
-    ada_sp_ms = sum(ada_sp) / len(ada_sp)
+    ada = time_steps(stack, dy, args.steps, args.warmup)
+    ada_ms = ada["wall_ms"]
+    ada_sp_ms = ada["stage_avg"][("sparse", 0)]
     ada_bytes = algorithmic_bytes(spec, mb.blocks[0], stack.blocks[0], "sparse_adagrad", 0)
     ada_gbs = ada_bytes / (ada_sp_ms * 1e-3) / 1e9
     adagrad = {"ms_per_train_step": round(ada_ms, 4),
@@ -872,6 +1057,13 @@ def main() -> int:
                              "bytes": ada_bytes, "GB/s": round(ada_gbs, 1),
                              "frac": round(ada_gbs / HBM_PEAK_GBS, 4)},
                "lr": 0.01, "eps": 1e-10}
+    del stack
+    torch.cuda.empty_cache()
+
+    skewed = measure_skewed(args, tables, dev)
+    torch.cuda.empty_cache()
+    configs = measure_configs(args, dev)
+    torch.cuda.empty_cache()
 
     g = full_graph(spec, dev)
     sampling = measure_sampling(spec, g, dev, args)
@@ -899,16 +1091,23 @@ def main() -> int:
                    "table_rows": list(spec.type_rows),
                    "learnable_tables": [spec.ntype_names[t] for t in range(len(spec.ntype_names))
                                         if spec.featureless[t]]},
+        "step_ms_events": run["step_stats"],
         "ms_per_block": per_block,
         "stage_ms": {f"{s}[{l}]": round(v, 4) for (s, l), v in sorted(avg.items(), key=lambda x: (x[0][1], x[0][0]))},
-        "roofline": {"bound": "hbm", "kernel": kernel_name, "stage": f"{dom_stage}[{dom_layer}]",
+        "roofline": {"bound": "hbm", "kernel": kernel_name, "stage": dom_key,
                      "achieved": dom["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": dom["frac"], "traffic": traffic, "launch_position": position},
+                     "frac": dom["frac"], "traffic": traffic,
+                     "traffic_over_bytes": (round(traffic / dom["bytes"], 3)
+                                            if traffic is not None else None),
+                     "bytes": dom["bytes"], "impl_bytes": dom["impl_bytes"],
+                     "launch_position": position},
         "hbm_kernels": rooflines,
         "copy_probe_GBs": round(copy_gbs, 1),
         "mfma_transforms": mfma,
         "mfma_backward": mfma_bwd,
         "train_step_sparse_adagrad": adagrad,
+        "skewed": skewed,
+        "configs": configs,
         "sampling": sampling,
         "featureless_features": featureless,
         "link_prediction": link_prediction,
@@ -916,7 +1115,6 @@ def main() -> int:
     }
     print(json.dumps(out), flush=True)
     return 0
-
 
 if __name__ == "__main__":
     sys.exit(main())
