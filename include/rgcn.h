@@ -385,6 +385,22 @@ rgcn_status rgcn_lp_loss(const rgcn_lp_batch *batch, float *loss, float *pos_sco
                          float *neg_score, float *d_emb, float *d_rel, void *workspace,
                          size_t workspace_bytes, unsigned flags, hipStream_t stream);
 
+/* rgcn_lp_loss for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same computation
+ * and outputs, with no workspace argument.  Its temporaries live in one fixed device
+ * array of RGCN_LP_NOALLOC_MAX_SCRATCH bytes inside the library, one per device, held
+ * until the process ends; the call allocates nothing and calls no allocating routine.
+ * A batch whose temporaries (rgcn_lp_workspace_size) exceed that size is rejected with
+ * RGCN_ERR_UNSUPPORTED before anything is enqueued.  Every call on a device shares that
+ * device's array: calls that overlap on one device (two streams, two threads) race and
+ * give unspecified results; calls ordered on one stream are safe, and each call
+ * initialises every temporary it reads, whatever the previous call left.
+ * flags: RGCN_VALIDATE_DEVICE. */
+#define RGCN_LP_NOALLOC_MAX_SCRATCH 33554432u /* 32 MiB */
+rgcn_status rgcn_lp_loss_noalloc(const rgcn_lp_batch *batch, float *loss, float *pos_score,
+                                 float *neg_score, float *d_emb, float *d_rel, unsigned flags,
+                                 hipStream_t stream);
+
 /* Negative node ids for the per-edge (slots = B * K) or joint (slots = ceil(B / K) * K)
  * modes: slot q is the high word of draw * num_nodes, the draw being word q mod 4 of
  * Philox4x64-10 at counter (q / 4, neg_mode, 0, 0) and key (seed, 0x6e6567); uniform over

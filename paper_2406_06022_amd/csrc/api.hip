@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 
 #include "common.h"
@@ -975,26 +976,27 @@ rgcn_status rgcn_lp_workspace_size(const rgcn_lp_batch *batch, size_t *bytes) {
     return RGCN_OK;
 }
 
-rgcn_status rgcn_lp_loss(const rgcn_lp_batch *batch, float *loss, float *pos_score,
-                         float *neg_score, float *d_emb, float *d_rel, void *workspace,
-                         size_t workspace_bytes, unsigned flags, hipStream_t stream) {
-    LpArgs a;
-    rgcn_status st = lp_args(batch, a);
-    if (st != RGCN_OK) return st;
+}  // extern "C"
+
+namespace {
+
+// Argument checks of the decoder shared by both entry points (the workspace aside).
+rgcn_status lp_check_outputs(const LpArgs &a, float *loss, float *pos_score, float *neg_score,
+                             float *d_emb, float *d_rel, unsigned flags) {
     if (flags & ~(unsigned)RGCN_VALIDATE_DEVICE)
         return fail(RGCN_ERR_INVALID_ARG, "unsupported flags 0x%x", flags);
-    const LpLayout L = lp_layout(a);
-    if (!workspace || ((uintptr_t)workspace & 255u))
-        return fail(RGCN_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
-    if (workspace_bytes < L.total)
-        return fail(RGCN_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu",
-                    workspace_bytes, L.total);
     if (!loss || !aligned4(loss)) return fail(RGCN_ERR_INVALID_ARG, "loss NULL or misaligned");
     if ((pos_score && !aligned4(pos_score)) || (neg_score && !aligned4(neg_score)) ||
         (d_emb && !aligned4(d_emb)) || (d_rel && !aligned4(d_rel)))
         return fail(RGCN_ERR_INVALID_ARG, "an output is misaligned");
     if (d_rel && !a.rel) return fail(RGCN_ERR_INVALID_ARG, "d_rel requested for a dot product");
-    char *ws = (char *)workspace;
+    return RGCN_OK;
+}
+
+// The decoder's launches on temporaries at `ws` (L.total bytes, 256-byte aligned).
+rgcn_status lp_run(const LpArgs &a, const LpLayout &L, char *ws, float *loss, float *pos_score,
+                   float *neg_score, float *d_emb, float *d_rel, unsigned flags,
+                   hipStream_t stream) {
     if ((flags & RGCN_VALIDATE_DEVICE) && a.batch > 0) {
         uint32_t *err = (uint32_t *)(ws + L.off_err);
         const uint32_t zero = 0;
@@ -1007,6 +1009,84 @@ rgcn_status rgcn_lp_loss(const rgcn_lp_batch *batch, float *loss, float *pos_sco
     }
     TRY_HIP(lp_loss(a, L, ws, loss, pos_score, neg_score, d_emb, d_rel, stream), "link prediction");
     return RGCN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rgcn_status rgcn_lp_loss(const rgcn_lp_batch *batch, float *loss, float *pos_score,
+                         float *neg_score, float *d_emb, float *d_rel, void *workspace,
+                         size_t workspace_bytes, unsigned flags, hipStream_t stream) {
+    LpArgs a;
+    rgcn_status st = lp_args(batch, a);
+    if (st != RGCN_OK) return st;
+    if ((st = lp_check_outputs(a, loss, pos_score, neg_score, d_emb, d_rel, flags)) != RGCN_OK)
+        return st;
+    const LpLayout L = lp_layout(a);
+    if (!workspace || ((uintptr_t)workspace & 255u))
+        return fail(RGCN_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
+    if (workspace_bytes < L.total)
+        return fail(RGCN_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu",
+                    workspace_bytes, L.total);
+    return lp_run(a, L, (char *)workspace, loss, pos_score, neg_score, d_emb, d_rel, flags,
+                  stream);
+}
+
+}  // extern "C"
+
+// ------------------------------------------------ the decoder without a caller workspace
+// Temporaries of rgcn_lp_loss_noalloc: one fixed array per device, part of the library's
+// code object (each GPU the library runs on holds it until the process ends).  Host code
+// never uses its name as an address: the per-device address comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+static __device__ __align__(256) char scratch[RGCN_LP_NOALLOC_MAX_SCRATCH];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char *g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address (looked up on the first call on each device).
+rgcn_status current_scratch(char **out) {
+    int dev = -1;
+    TRY_HIP(hipGetDevice(&dev), "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(RGCN_ERR_UNSUPPORTED, "device index %d outside [0, %d)", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        TRY_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "scratch address");
+        if (!p || ((uintptr_t)p & 255u))
+            return fail(RGCN_ERR_HIP, "scratch array address missing or misaligned");
+        g_scratch_ptr[dev] = (char *)p;
+    }
+    *out = g_scratch_ptr[dev];
+    return RGCN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rgcn_status rgcn_lp_loss_noalloc(const rgcn_lp_batch *batch, float *loss, float *pos_score,
+                                 float *neg_score, float *d_emb, float *d_rel, unsigned flags,
+                                 hipStream_t stream) {
+    LpArgs a;
+    rgcn_status st = lp_args(batch, a);
+    if (st != RGCN_OK) return st;
+    if ((st = lp_check_outputs(a, loss, pos_score, neg_score, d_emb, d_rel, flags)) != RGCN_OK)
+        return st;
+    const LpLayout L = lp_layout(a);
+    if (L.total > (size_t)RGCN_LP_NOALLOC_MAX_SCRATCH)
+        return fail(RGCN_ERR_UNSUPPORTED,
+                    "this batch needs %zu bytes of temporaries, above the %zu of the fixed "
+                    "scratch array; call rgcn_lp_loss with a workspace", L.total,
+                    (size_t)RGCN_LP_NOALLOC_MAX_SCRATCH);
+    char *ws = nullptr;
+    if ((st = current_scratch(&ws)) != RGCN_OK) return st;
+    return lp_run(a, L, ws, loss, pos_score, neg_score, d_emb, d_rel, flags, stream);
 }
 
 rgcn_status rgcn_lp_negatives(int32_t neg_mode, int64_t slots, int64_t num_nodes, uint64_t seed,

@@ -38,11 +38,12 @@ EXPORTED = ("rgcn_block_workspace_size", "rgcn_block_plan_layout", "rgcn_block_p
             "rgcn_block_transform", "rgcn_block_backward_dense", "rgcn_block_backward_sparse",
             "rgcn_block_backward_sparse_adagrad", "rgcn_sparse_adagrad",
             "rgcn_sample_workspace_size", "rgcn_sample_block", "rgcn_lp_workspace_size",
-            "rgcn_lp_loss", "rgcn_lp_negatives", "rgcn_featureless_mean", "rgcn_last_error",
+            "rgcn_lp_loss", "rgcn_lp_loss_noalloc", "rgcn_lp_negatives", "rgcn_featureless_mean", "rgcn_last_error",
             "rgcn_version")
 RGCN_FEATURELESS_WORKSPACE = 256
 RGCN_LP_NEG_PER_EDGE, RGCN_LP_NEG_JOINT, RGCN_LP_NEG_IN_BATCH = 0, 1, 2
 RGCN_LP_CE, RGCN_LP_WEIGHTED_CE, RGCN_LP_CONTRASTIVE = 0, 1, 2
+RGCN_LP_NOALLOC_MAX_SCRATCH = 32 << 20
 RGCN_MAX_FANOUT = 64
 
 
@@ -163,6 +164,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.rgcn_lp_workspace_size.restype = st
         lib.rgcn_lp_loss.argtypes = [vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, ctypes.c_uint, vp]
         lib.rgcn_lp_loss.restype = st
+        lib.rgcn_lp_loss_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_uint, vp]
+        lib.rgcn_lp_loss_noalloc.restype = st
         lib.rgcn_lp_negatives.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
                                           ctypes.c_uint64, vp, vp]
         lib.rgcn_lp_negatives.restype = st
@@ -517,6 +520,16 @@ def rgcn_lp_loss(batch: "_LpBatch", loss: torch.Tensor, pos_score=None, neg_scor
                                        _ptr(neg_score), _ptr(d_emb), _ptr(d_rel),
                                        workspace.data_ptr(), workspace.numel(), flags,
                                        _stream(stream)))
+
+
+def rgcn_lp_loss_noalloc(batch: "_LpBatch", loss: torch.Tensor, pos_score=None,
+                         neg_score=None, d_emb=None, d_rel=None, flags: int = 0,
+                         stream=None) -> None:
+    """rgcn_lp_loss with the library's fixed per-device scratch array instead of a
+    workspace (allocates nothing)."""
+    _check(load_library().rgcn_lp_loss_noalloc(ctypes.byref(batch), loss.data_ptr(),
+                                               _ptr(pos_score), _ptr(neg_score), _ptr(d_emb),
+                                               _ptr(d_rel), flags, _stream(stream)))
 
 
 def rgcn_lp_negatives(neg_mode: int, slots: int, num_nodes: int, seed: int, out: torch.Tensor,
