@@ -127,11 +127,27 @@ __device__ __forceinline__ void row_walk(const int64_t *goff, int n, LoadAcc &&l
 }
 
 // Batch bodies: load B rows' chunks (16 bytes per lane per chunk) and add them into acc.
-// SumLoad: fp32 rows at absolute addresses.
-template <int CPL>
+// SumLoad: fp32 rows at absolute addresses.  COMP: added with compensation (Kahan), comp
+// holding the low-order part each addition lost, for the pieces of split rows: the terms
+// of a hub's transpose cancel over thousands of edges, and plain fp32 sums of its pieces
+// lost a digit against the exact sum (the rows of at most kSplitEdges edges that the
+// plain kernels sum do not need it, and its registers cost those kernels a wave per
+// SIMD).
+// A slot that holds no row (padding of a batch) must leave acc and comp as they are:
+// adding a zero would apply the pending compensation, and how many padding slots a row
+// sees depends on its neighbours in the wave, i.e. on the processing order.
+__device__ __forceinline__ void kahan_add(f32x4 &acc, f32x4 &comp, f32x4 x, bool take) {
+    const f32x4 y = x - comp;
+    const f32x4 t = acc + y;
+    const f32x4 c = (t - acc) - y;
+    acc = take ? t : acc;
+    comp = take ? c : comp;
+}
+template <int CPL, bool COMP>
 struct SumLoad {
     int lg, G, chunks;
     f32x4 *acc;
+    f32x4 *comp;   // COMP only
     template <int B>
     __device__ __forceinline__ void run(const int64_t (&o)[B], const bool (&ok)[B]) const {
         f32x4 v[B][CPL];
@@ -147,7 +163,12 @@ struct SumLoad {
 #pragma unroll
         for (int u = 0; u < B; ++u)
 #pragma unroll
-            for (int p = 0; p < CPL; ++p) acc[p] += v[u][p];
+            for (int p = 0; p < CPL; ++p) {
+                if constexpr (COMP)
+                    kahan_add(acc[p], comp[p], v[u][p], ok[u]);
+                else
+                    acc[p] += v[u][p];
+            }
     }
 };
 
@@ -486,6 +507,7 @@ __device__ __forceinline__ void transpose_sum_body(const TsumArgs &a, int G, int
     const int64_t g = wave * gpw + gi;
     if (g >= a.n_rows) return;
     const int64_t j = a.order[g];
+    if (a.split_np != nullptr && a.split_np[j] > 0) return;   // summed by the piece kernels
     const int64_t grow = a.in.row_ids ? a.in.row_ids[j] : j;
 
     // early requests: embedding-gradient row (read-add-write) or Adagrad state, ReLU mask
@@ -630,6 +652,7 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
     struct Row {
         Meta m;
         int32_t total, ei, er;
+        bool split;     // more than kSplitEdges edges: the piece kernels sum this row
         f32x4 old[CPL], self[CPL], hm[CPL];
     };
     // stage 1: source row at schedule position q (-1 past the end)
@@ -672,13 +695,16 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
         rw.m = m;
         int ridx, pos;
         rw.total = locate(m, lg, ridx, pos);
+        // the plan split exactly the rows whose degree passes the threshold
+        rw.split = a.split_np != nullptr && rw.total > kSplitEdges;
+        if (rw.split) rw.total = 0;
         const bool oke = lg < rw.total;
         rw.ei = *gbl(oke ? s_rel[ridx].csc_dst + pos : (const int32_t *)zero);
         rw.er = ridx;
 #pragma unroll
         for (int p = 0; p < CPL; ++p) {
             const int c = lg + p * G;
-            const bool okc = c < chunks && m.j >= 0;
+            const bool okc = c < chunks && m.j >= 0 && !rw.split;
             // row read before the sum: Adagrad state, or the embedding gradient when ids
             // are unique.  (Written this way, pointer chosen here and the flag test in the
             // predicate: forms that pick the pointer once before the loop measured 9%
@@ -703,7 +729,9 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
     };
     // rows [0, n) whose addresses are in goff, added into acc; a batch's unused slots re-read
     // the last row and are dropped
-    auto rows = [&](int n, f32x4 (&acc)[CPL]) { row_walk<U>(goff, n, SumLoad<CPL>{lg, G, chunks, acc}); };
+    auto rows = [&](int n, f32x4 (&acc)[CPL]) {
+        row_walk<U>(goff, n, SumLoad<CPL, false>{lg, G, chunks, acc, nullptr});
+    };
     auto edge_addr = [&](int r, int32_t i) -> int64_t {
         return (int64_t)(uintptr_t)(s_rel[r].dms + (int64_t)i * s_rel[r].dms_ld);
     };
@@ -727,6 +755,7 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
             rows(rw.total - ec < G ? rw.total - ec : G, acc);
         }
         __builtin_amdgcn_wave_barrier();
+        if (rw.split) return;
 #pragma unroll
         for (int p = 0; p < CPL; ++p) {
             const int c = lg + p * G;
@@ -758,6 +787,160 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
         mn = mnn;
         jnn = jn3;
     }
+}
+
+// Rows split into pieces (transpose degree above kSplitEdges).  Piece p = (row j, number q)
+// is the sum of the dMs rows of edges [q P, min((q + 1) P, deg)) of row j's transpose,
+// flattened relation by relation in order, edges in order; it goes to partial[p].  Lanes
+// r < nrel of a group hold relation r's segment of row j (in blocks of G relations), the
+// group resolves G edges at a time and keeps the rows' loads in flight through row_walk.
+template <int CPL>
+__device__ __forceinline__ void pieces_body(const TsumArgs &a, int G, int gpw, int chunks) {
+    constexpr int U = CPL == 1 ? 8 : 4;
+    constexpr int W = kThreads / 64;
+    __shared__ TsumRel s_rel[kMaxRels];
+    __shared__ int64_t s_off[W][64];
+    for (int i = threadIdx.x; i < a.nrel; i += kThreads) s_rel[i] = a.rel[i];
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int gi = lane / G;
+    const int lg = lane - gi * G;
+    const int g0 = gi * G;
+    if (gi >= gpw) return;
+    int64_t *goff = &s_off[wave][g0];
+    const uint32_t cnt_all = *a.piece_count;
+    const int64_t n = (int64_t)cnt_all < a.piece_cap ? (int64_t)cnt_all : a.piece_cap;
+    const int64_t stride = (int64_t)gridDim.x * W * gpw;
+    const int64_t zrow = (int64_t)(uintptr_t)g_zero_row;
+    for (int64_t p = ((int64_t)blockIdx.x * W + wave) * gpw + gi; p < n; p += stride) {
+        const int2 pc = a.pieces[p];
+        const int64_t j = pc.x;
+        const int e0 = pc.y * kSplitEdges, e1 = e0 + kSplitEdges;
+        f32x4 acc[CPL], comp[CPL];
+#pragma unroll
+        for (int q = 0; q < CPL; ++q) acc[q] = comp[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        int base = 0;   // flattened index of the first edge of relation block r0
+        for (int r0 = 0; r0 < a.nrel && base < e1; r0 += G) {
+            const int nr = (a.nrel - r0) < G ? (a.nrel - r0) : G;
+            int p0 = 0, cnt = 0;
+            if (lg < nr) {
+                const int32_t *ip = s_rel[r0 + lg].csc_indptr;
+                p0 = ip[j];
+                cnt = ip[j + 1] - p0;
+            }
+            int tot = 0;
+            for (int r = 0; r < nr; ++r) tot += __shfl(cnt, g0 + r, 64);
+            const int lo = e0 - base > 0 ? e0 - base : 0;
+            const int hi = e1 - base < tot ? e1 - base : tot;
+            for (int ec = lo; ec < hi; ec += G) {
+                const int e = ec + lg;
+                int64_t addr = zrow;
+                int b = 0;
+                for (int r = 0; r < nr; ++r) {
+                    const int cr = __shfl(cnt, g0 + r, 64);
+                    const int pr = __shfl(p0, g0 + r, 64);
+                    if (e < hi && e >= b && e < b + cr) {
+                        const TsumRel &rel = s_rel[r0 + r];
+                        const int64_t i = rel.csc_dst[pr + (e - b)];
+                        addr = (int64_t)(uintptr_t)(rel.dms + i * rel.dms_ld);
+                    }
+                    b += cr;
+                }
+                __builtin_amdgcn_wave_barrier();
+                goff[lg] = addr;
+                __builtin_amdgcn_wave_barrier();
+                row_walk<U>(goff, hi - ec < G ? hi - ec : G, SumLoad<CPL, true>{lg, G, chunks, acc, comp});
+                __builtin_amdgcn_wave_barrier();
+            }
+            base += tot;
+        }
+#pragma unroll
+        for (int q = 0; q < CPL; ++q) {
+            const int c = lg + q * G;
+            if (c < chunks) *(f32x4 *)(a.partial + p * a.d_in + (int64_t)c * 4) = acc[q];
+        }
+    }
+}
+
+// The rows split into pieces, finished: one group per split row (found through its first
+// piece) adds its self term and its pieces' partial sums in piece order, then applies the
+// mask and the stores of the transposed sum (dh_src, the embedding gradient or the Adagrad
+// step).
+template <bool BF16IN, int CPL, bool OPT>
+__device__ __forceinline__ void split_finish_body(const TsumArgs &a, int G, int gpw, int chunks) {
+    constexpr int HES = BF16IN ? 2 : 4;
+    constexpr int U = CPL == 1 ? 8 : 4;
+    constexpr int W = kThreads / 64;
+    __shared__ int64_t s_off[W][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int gi = lane / G;
+    const int lg = lane - gi * G;
+    const int g0 = gi * G;
+    if (gi >= gpw) return;
+    int64_t *goff = &s_off[wave][g0];
+    const uint32_t cnt_all = *a.piece_count;
+    const int64_t n = (int64_t)cnt_all < a.piece_cap ? (int64_t)cnt_all : a.piece_cap;
+    const int64_t stride = (int64_t)gridDim.x * W * gpw;
+    for (int64_t p = ((int64_t)blockIdx.x * W + wave) * gpw + gi; p < n; p += stride) {
+        const int2 pc = a.pieces[p];
+        if (pc.y != 0) continue;
+        const int64_t j = pc.x;
+        const int np = a.split_np[j];
+        const int64_t pb = a.split_base[j];
+        const int64_t grow = a.in.row_ids ? a.in.row_ids[j] : j;
+        f32x4 acc[CPL], comp[CPL], old[CPL], hm[CPL];
+#pragma unroll
+        for (int q = 0; q < CPL; ++q) {
+            const int c = lg + q * G;
+            const bool okc = c < chunks;
+            const float *ob = OPT ? a.opt_state : (a.ids_unique ? a.demb : nullptr);
+            old[q] = (ob && okc) ? *(const f32x4 *)(ob + grow * a.d_in + (int64_t)c * 4)
+                                 : f32x4{0.f, 0.f, 0.f, 0.f};
+            hm[q] = f32x4{1.f, 1.f, 1.f, 1.f};
+            if ((a.input_relu || OPT) && okc) {
+                const char *hp = (const char *)a.in.base + (grow * a.in.ld + (int64_t)c * 4) * HES;
+                if constexpr (BF16IN) {
+                    const uint2 hv = *(const uint2 *)hp;
+                    hm[q] = f32x4{bf16_lo(hv.x), bf16_hi(hv.x), bf16_lo(hv.y), bf16_hi(hv.y)};
+                } else {
+                    hm[q] = *(const f32x4 *)hp;
+                }
+            }
+            acc[q] = (a.self_dms && j < a.n_dst && okc)
+                         ? *(const f32x4 *)(a.self_dms + j * a.self_ld + (int64_t)c * 4)
+                         : f32x4{0.f, 0.f, 0.f, 0.f};
+            comp[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        for (int q0 = 0; q0 < np; q0 += G) {
+            __builtin_amdgcn_wave_barrier();
+            goff[lg] = (int64_t)(uintptr_t)(a.partial + (pb + q0 + (q0 + lg < np ? lg : 0)) * a.d_in);
+            __builtin_amdgcn_wave_barrier();
+            row_walk<U>(goff, np - q0 < G ? np - q0 : G, SumLoad<CPL, true>{lg, G, chunks, acc, comp});
+        }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int q = 0; q < CPL; ++q) {
+            const int c = lg + q * G;
+            if (c >= chunks) continue;
+            f32x4 res = acc[q];
+            if (a.input_relu) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) res[e] = hm[q][e] > 0.f ? res[e] : 0.f;
+            }
+            tsum_store<BF16IN, OPT>(a, j, grow, c, res, old[q], hm[q]);
+        }
+    }
+}
+
+template <int CPL>
+__global__ __launch_bounds__(kThreads) void k_transpose_pieces(TsumArgs a, int G, int gpw,
+                                                               int chunks) {
+    pieces_body<CPL>(a, G, gpw, chunks);
+}
+template <bool BF16IN, int CPL, bool OPT>
+__global__ __launch_bounds__(kThreads) void k_transpose_split_finish(TsumArgs a, int G, int gpw,
+                                                                     int chunks) {
+    split_finish_body<BF16IN, CPL, OPT>(a, G, gpw, chunks);
 }
 
 // The transposed sums as kernels; the Adagrad forms carry a name of their own so that
@@ -971,8 +1154,31 @@ hipError_t launch_transpose_pipe(const TsumArgs &a, const GroupShape &gs, int ch
     return hipGetLastError();
 }
 
+// The piece and finishing kernels of split rows: persistent grids that read the piece
+// count on the device (no piece: every group exits at once).
 template <bool B, int C, bool O>
-hipError_t launch_transpose(const TsumArgs &a, const GroupShape &gs, int chunks, hipStream_t s) {
+hipError_t launch_split(const TsumArgs &a, const GroupShape &gs, int chunks, bool finish,
+                        hipStream_t s) {
+    if (a.piece_cap <= 0 || !a.pieces) return hipSuccess;
+    const int64_t groups_per_wg = (int64_t)(kThreads / 64) * gs.gpw;
+    int64_t wgs = cdiv(a.piece_cap, groups_per_wg);
+    if (finish) {
+        auto kern = k_transpose_split_finish<B, C, O>;
+        const int64_t cap = resident_wgs(kern);
+        hipLaunchKernelGGL(kern, dim3((unsigned)(wgs < cap ? wgs : cap)), dim3(kThreads), 0, s,
+                           a, gs.G, gs.gpw, chunks);
+    } else {
+        auto kern = k_transpose_pieces<C>;
+        const int64_t cap = resident_wgs(kern);
+        hipLaunchKernelGGL(kern, dim3((unsigned)(wgs < cap ? wgs : cap)), dim3(kThreads), 0, s,
+                           a, gs.G, gs.gpw, chunks);
+    }
+    return hipGetLastError();
+}
+
+template <bool B, int C, bool O>
+hipError_t launch_transpose_rows(const TsumArgs &a, const GroupShape &gs, int chunks,
+                                 hipStream_t s) {
     if (a.nrel <= gs.G) return launch_transpose_pipe<B, C, O>(a, gs, chunks, s);
     const int64_t waves = cdiv(a.n_rows, gs.gpw);
     const dim3 grid((unsigned)cdiv(waves, kThreads / 64));
@@ -980,6 +1186,14 @@ hipError_t launch_transpose(const TsumArgs &a, const GroupShape &gs, int chunks,
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, a, gs.G, gs.gpw,
                        chunks);
     return hipGetLastError();
+}
+
+template <bool B, int C, bool O>
+hipError_t launch_transpose(const TsumArgs &a, const GroupShape &gs, int chunks, hipStream_t s) {
+    // split rows: pieces first, then every other row, then the split rows' reductions
+    RGCN_HIP_TRY((launch_split<B, C, O>(a, gs, chunks, false, s)));
+    RGCN_HIP_TRY((launch_transpose_rows<B, C, O>(a, gs, chunks, s)));
+    return launch_split<B, C, O>(a, gs, chunks, true, s);
 }
 
 template <bool B, bool O>

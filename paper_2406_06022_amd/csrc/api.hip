@@ -10,8 +10,6 @@
 
 #include "common.h"
 
-constexpr int kGatherClaimWord = 32;
-
 using namespace rgcn;
 
 namespace {
@@ -77,8 +75,12 @@ struct Layout {
     // workspace offsets
     size_t off_slots = 0, off_fwd_order = 0, off_fwd_desc = 0, off_bwd_order = 0, off_err = 0;
     size_t off_fwd_chunks = 0;
-    size_t off_flags = 0;         // schedule flags: [0] forward, [1 + t] backward of type t;
-                                  // [kGatherClaimWord] the gather's work counter
+    size_t off_flags = 0;         // flag words (see kGatherClaimWord, kPieceCountWord)
+    // split backward rows: np and base per backward row, the piece list (per type a window
+    // of piece_cap[t] pieces from piece_at[t]), partial sums in the backward temporaries
+    size_t off_split_np = 0, off_split_base = 0, off_pieces = 0;
+    int64_t piece_at[kMaxTypes], piece_cap[kMaxTypes], piece_total = 0;
+    size_t off_split_partial = 0;       // relative to scratch
     int64_t nc_max = 0;           // chunk bound of the flattened forward stream
     size_t off_csc_indptr[kMaxRels], off_csc_dst[kMaxRels];
     // combined transpose of the relations leaving grad types
@@ -241,6 +243,20 @@ rgcn_status make_layout(const rgcn_block *b, const rgcn_params *p, Layout &L) {
     L.off_fwd_desc = off;                 off += align256((size_t)L.n_seg * sizeof(SegDesc) + 16);
     L.off_fwd_chunks = off;               off += align256((size_t)(L.nc_max + 2) * 4);
     L.off_bwd_order = off;                off += align256((size_t)L.n_bwd_rows * 4 + 4);
+    L.off_split_np = off;                 off += align256((size_t)L.n_bwd_rows * 4 + 4);
+    L.off_split_base = off;               off += align256((size_t)L.n_bwd_rows * 4 + 4);
+    L.piece_total = 0;
+    for (int t = 0; t < kMaxTypes; ++t) L.piece_at[t] = L.piece_cap[t] = 0;
+    for (int t = 0; t < L.T; ++t) {
+        if (!(L.grad_mask >> t & 1u)) continue;
+        int64_t nnz_out = 0;
+        for (int r = 0; r < L.R; ++r)
+            if (b->rels[r].src_type == t) nnz_out += b->rels[r].nnz;
+        L.piece_at[t] = L.piece_total;
+        L.piece_cap[t] = split_piece_cap(nnz_out);
+        L.piece_total += L.piece_cap[t];
+    }
+    L.off_pieces = off;                   off += align256((size_t)L.piece_total * 8 + 8);
     for (int r = 0; r < kMaxRels; ++r) {
         L.off_csc_indptr[r] = L.off_csc_dst[r] = SIZE_MAX;
         L.koff[r] = L.e0[r] = -1;
@@ -304,6 +320,7 @@ rgcn_status make_layout(const rgcn_block *b, const rgcn_params *p, Layout &L) {
     }
     L.off_partial = bt;   bt += align256(part);
     L.off_colsum = bt;    bt += align256(cols);
+    L.off_split_partial = bt;  bt += align256((size_t)L.piece_total * L.d_in * 4 + 16);
     L.total = L.off_scratch + (L.plan_temp > bt ? L.plan_temp : bt);
     return RGCN_OK;
 }
@@ -428,9 +445,12 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
                     "slot table");
         TRY_HIP(fill_words(sched_flag, zeros, sizeof(uint32_t), stream), "schedule flags");
     }
-    if (parts & RGCN_PLAN_BACKWARD)
+    if (parts & RGCN_PLAN_BACKWARD) {
         TRY_HIP(fill_words(sched_flag + 1, zeros, sizeof(uint32_t) * kMaxTypes, stream),
                 "schedule flags");
+        TRY_HIP(fill_words(sched_flag + kPieceCountWord, zeros, sizeof(uint32_t) * kMaxTypes,
+                           stream), "piece counters");
+    }
     if (parts & RGCN_PLAN_FORWARD) {
         int64_t moff[kMaxTypes], mld[kMaxTypes];
         for (int t = 0; t < kMaxTypes; ++t) {
@@ -469,8 +489,15 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
         for (int r = 0; r < L.R; ++r)
             if (block->rels[r].src_type == t)
                 kr.csc_indptr[kr.count++] = (const int32_t *)(ws + L.off_csc_indptr[r]);
+        SplitRows sp;
+        sp.np = (int32_t *)(ws + L.off_split_np) + L.bwd_base[t];
+        sp.base = (int32_t *)(ws + L.off_split_base) + L.bwd_base[t];
+        sp.pieces = (int2 *)(ws + L.off_pieces) + L.piece_at[t];
+        sp.count = sched_flag + kPieceCountWord + t;
+        sp.cap = L.piece_cap[t];
         TRY_HIP(bwd_schedule(kr, block->n_src[t], (int32_t *)(ws + L.off_bwd_order) + L.bwd_base[t],
-                             scratch, sched_flag + 1 + t, keep_order, stream), "backward schedule");
+                             scratch, sched_flag + 1 + t, keep_order, sp, stream),
+                "backward schedule");
     }
     return RGCN_OK;
 }
@@ -710,6 +737,12 @@ rgcn_status backward_sparse(const rgcn_block *block, const rgcn_input *in,
             a.eps = opt->eps;
         }
         a.d_in = L.d_in;
+        a.split_np = (const int32_t *)(ws + L.off_split_np) + L.bwd_base[s];
+        a.split_base = (const int32_t *)(ws + L.off_split_base) + L.bwd_base[s];
+        a.pieces = (const int2 *)(ws + L.off_pieces) + L.piece_at[s];
+        a.piece_count = (const uint32_t *)(ws + L.off_flags) + kPieceCountWord + s;
+        a.piece_cap = L.piece_cap[s];
+        a.partial = (float *)(scratch + L.off_split_partial) + L.piece_at[s] * L.d_in;
         for (int r = 0; r < L.R; ++r) {
             const rgcn_relation &rel = block->rels[r];
             if (rel.src_type != s || block->n_dst[rel.dst_type] == 0) continue;

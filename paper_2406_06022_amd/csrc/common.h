@@ -82,6 +82,26 @@ constexpr int kMaxSlots = RGCN_MAX_TYPES + RGCN_MAX_RELS;  // forward slots: sel
 constexpr int kSchedBuckets = 32;                          // schedule keys 0..31
 constexpr int kFwdChunk = 64;   // weight per chunk of the flattened forward stream
 constexpr int kFwdClaim = 8;    // most chunks per run a gather group claims at a time
+// A backward source row with more transpose edges than this (over all relations leaving
+// its type) is summed in pieces of this many edges by several lane groups, then reduced:
+// one group walking a hub of tens of thousands of edges alone would set the stage's time.
+constexpr int kSplitEdges = 128;
+// Words of the workspace's flag area: [0] forward schedule flag, [1 + t] backward schedule
+// flag of type t, [kGatherClaimWord] the gather's work counter, [kPieceCountWord + t] the
+// number of pieces of type t's split rows.
+constexpr int kGatherClaimWord = 32;
+constexpr int kPieceCountWord = 48;
+// Split rows of one backward type (plan output, read by the transposed sum).
+struct SplitRows {
+    int32_t *np;        // [n_rows] pieces of row j (0: not split)
+    int32_t *base;      // [n_rows] index of row j's first piece (split rows only)
+    int2 *pieces;       // [cap] (row, piece number) of each piece
+    uint32_t *count;    // pieces written (zero before the plan)
+    int64_t cap;
+};
+// Pieces of a type whose relations leaving it hold nnz edges: a split row of deg > P edges
+// has ceil(deg / P) <= deg / P + 1 pieces and there are fewer than nnz / P split rows.
+inline int64_t split_piece_cap(int64_t nnz) { return 2 * ((nnz + kSplitEdges - 1) / kSplitEdges) + 1; }
 
 // A forward slot: the self-loop rows of a destination type, or the rows of one relation.
 struct FwdSlot {
@@ -159,8 +179,9 @@ struct BwdKeyRels {          // relations leaving one source type
 };
 // *flag (zero on entry) ends nonzero when some row is heavy and the schedule was sorted;
 // keep_order != 0 keeps enumeration order.
+// Also lists the rows of more than kSplitEdges transpose edges in `split`.
 hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, void *temp,
-                        uint32_t *flag, int keep_order, hipStream_t s);
+                        uint32_t *flag, int keep_order, const SplitRows &split, hipStream_t s);
 hipError_t fill_words(void *dst, const void *src_host, size_t bytes, hipStream_t s);
 
 // aggregate.hip
@@ -192,6 +213,14 @@ struct TsumArgs {
     float lr, eps;
     int32_t d_in;
     int32_t nrel;
+    // rows split into pieces (see kSplitEdges): per row its piece count and first piece,
+    // the piece list and its length, and fp32 partial sums [piece_cap x d_in]
+    const int32_t *split_np;
+    const int32_t *split_base;
+    const int2 *pieces;
+    const uint32_t *piece_count;
+    int64_t piece_cap;
+    float *partial;
     TsumRel rel[kMaxRels];
 };
 hipError_t transpose_sum(rgcn_dtype dt, const TsumArgs &a, hipStream_t s);

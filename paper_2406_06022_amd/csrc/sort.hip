@@ -221,12 +221,14 @@ struct PutIndex {
 // relations leaving the type.
 struct BwdKey {
     BwdKeyRels rels;
-    __device__ int operator()(int64_t j) const {
+    // transpose degree of row j summed over the relations leaving the type
+    __device__ int64_t degree(int64_t j) const {
         int64_t deg = 0;
         for (int r = 0; r < rels.count; ++r)
             deg += (int64_t)rels.csc_indptr[r][j + 1] - rels.csc_indptr[r][j];
-        return degree_key(deg);
+        return deg;
     }
+    __device__ int operator()(int64_t j) const { return degree_key(degree(j)); }
 };
 
 // Radix pass: the digit (key >> shift) & mask.
@@ -488,13 +490,30 @@ __global__ __launch_bounds__(kThreads) void k_fwd_desc(DescArgs a, int32_t *orde
 
 // Backward rows of one type in enumeration order (order[j] = j); *flag is raised when some
 // row is heavy, i.e. when the sorted schedule is not the identity, unless `keep` asks for
-// enumeration order.
+// enumeration order.  Rows of more than kSplitEdges transpose edges are split into pieces
+// of kSplitEdges edges: np[j] = their count (0 for other rows), and the pieces (j, 0),
+// (j, 1), ... take consecutive slots from the shared counter (the slots' places vary from
+// run to run; what is summed, and in which order, does not).
 __global__ __launch_bounds__(kThreads) void k_bwd_ident(BwdKey kf, int64_t n, int32_t *order,
-                                                        uint32_t *flag, int keep) {
+                                                        uint32_t *flag, int keep, SplitRows sp) {
     const int64_t j = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const bool in = j < n;
-    if (in) order[j] = (int32_t)j;
-    const bool heavy = in && !keep && kf(j) != kSchedBuckets - 1;
+    int64_t deg = 0;
+    if (in) {
+        order[j] = (int32_t)j;
+        deg = kf.degree(j);
+        const int32_t np = deg > kSplitEdges ? (int32_t)((deg + kSplitEdges - 1) / kSplitEdges) : 0;
+        sp.np[j] = np;
+        if (np > 0) {
+            const uint32_t b = atomicAdd(sp.count, (uint32_t)np);
+            sp.base[j] = (int32_t)b;
+            // the capacity bounds every count the edges allow; the test keeps a corrupt
+            // transpose from writing past the list
+            if ((int64_t)b + np <= sp.cap)
+                for (int32_t q = 0; q < np; ++q) sp.pieces[b + q] = make_int2((int)j, q);
+        }
+    }
+    const bool heavy = in && !keep && degree_key(deg) != kSchedBuckets - 1;
     if (__ballot(heavy) != 0 && (threadIdx.x & 63) == 0) atomicOr(flag, 1u);
 }
 
@@ -608,10 +627,10 @@ hipError_t fwd_chunks(const int32_t *weight, int64_t n_seg, int64_t nc_max, int3
 }
 
 hipError_t bwd_schedule(const BwdKeyRels &rels, int64_t n_rows, int32_t *order, void *temp,
-                        uint32_t *flag, int keep_order, hipStream_t s) {
+                        uint32_t *flag, int keep_order, const SplitRows &split, hipStream_t s) {
     if (n_rows == 0) return hipSuccess;
     hipLaunchKernelGGL(k_bwd_ident, dim3((unsigned)cdiv(n_rows, kThreads)), dim3(kThreads), 0, s,
-                       BwdKey{rels}, n_rows, order, flag, keep_order);
+                       BwdKey{rels}, n_rows, order, flag, keep_order, split);
     RGCN_HIP_TRY(hipGetLastError());
     return bucket_sort<kSchedBuckets, 5>(BwdKey{rels}, PutIndex{order}, n_rows, temp, s, flag);
 }

@@ -358,6 +358,40 @@ def random_block(rng: np.random.Generator, n_src: Sequence[int], n_dst: Sequence
     return Block([int(x) for x in n_src], [int(x) for x in n_dst], out)
 
 
+def with_hub_sources(rng: np.random.Generator, blk: Block, src_type: int,
+                     hub_degrees: Sequence[int]) -> Block:
+    """``blk`` with extra edges from source rows 0, 1, ... of ``src_type``: source row h
+    gains about hub_degrees[h] in-edges over the relations leaving the type, spread over
+    random destination rows (repeated edges included), kept in CSR order."""
+    rels = [r for r in blk.rels if r.src_type == src_type and blk.n_dst[r.dst_type] > 0]
+    if not rels:
+        return blk
+    extra = {id(r): [] for r in rels}
+    for h, dh in enumerate(hub_degrees):
+        which = rng.integers(0, len(rels), size=int(dh))
+        for k, rel in enumerate(rels):
+            m = int((which == k).sum())
+            rows = rng.integers(0, blk.n_dst[rel.dst_type], size=m)
+            extra[id(rel)].append(np.stack([rows, np.full(m, h)], axis=1))
+    out = []
+    for rel in blk.rels:
+        if id(rel) not in extra:
+            out.append(rel)
+            continue
+        nd = blk.n_dst[rel.dst_type]
+        ip = np.asarray(rel.indptr, np.int64)
+        rows = np.repeat(np.arange(nd), np.diff(ip))
+        add = np.concatenate(extra[id(rel)]) if extra[id(rel)] else np.zeros((0, 2), np.int64)
+        all_rows = np.concatenate([rows, add[:, 0]])
+        all_src = np.concatenate([np.asarray(rel.indices, np.int64), add[:, 1]])
+        order = np.argsort(all_rows, kind="stable")
+        indptr = np.zeros(nd + 1, dtype=np.int64)
+        np.cumsum(np.bincount(all_rows, minlength=nd), out=indptr[1:])
+        out.append(Relation(rel.src_type, rel.dst_type, indptr.astype(np.int32),
+                            all_src[order].astype(np.int32)))
+    return Block(list(blk.n_src), list(blk.n_dst), out)
+
+
 # --------------------------------------------------------------------------------------
 # Full graphs to sample from (in-edge CSR per relation, global ids)
 # --------------------------------------------------------------------------------------

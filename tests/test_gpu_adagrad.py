@@ -51,7 +51,11 @@ def _check_table(got, w0, want, dtype, tol_step, what):
 
 
 def _adagrad_block(kind):
-    rng = np.random.default_rng({"mixed": 7, "many-rels": 8}[kind])
+    rng = np.random.default_rng({"mixed": 7, "many-rels": 8, "hubs": 9}[kind])
+    if kind == "hubs":
+        # learnable rows whose transposes span several pieces of the split backward
+        blk = synth.random_block(rng, [3000, 500], [800, 200], [(0, 0), (0, 1), (1, 0)], 8)
+        return synth.with_hub_sources(rng, blk, 0, [129, 700, 5000]), [0]
     if kind == "mixed":
         # type 0 learnable (ids into a larger table), type 1 featured; zero-degree rows,
         # source rows without out-edges, a heavy destination row
@@ -61,10 +65,11 @@ def _adagrad_block(kind):
     # one type with more relations leaving it than a lane group is wide (the non-pipelined
     # transposed sum at d = 32)
     rels = [(0, 0)] * 6 + [(0, 1)] * 5 + [(1, 0)]
-    return synth.random_block(rng, [700, 300], [250, 120], rels, 6), [0, 1]
+    blk = synth.random_block(rng, [700, 300], [250, 120], rels, 6)
+    return synth.with_hub_sources(rng, blk, 0, [300, 2000]), [0, 1]   # split rows too
 
 
-@pytest.mark.parametrize("kind", ["mixed", "many-rels"])
+@pytest.mark.parametrize("kind", ["mixed", "many-rels", "hubs"])
 @pytest.mark.parametrize("dtype,d_in,d_out", [("f32", 32, 48), ("bf16", 32, 64),
                                               ("bf16", 128, 64), ("f32", 264, 40)])
 def test_fused_adagrad_matches_oracle(kind, dtype, d_in, d_out):

@@ -358,3 +358,38 @@ def test_workspace_too_small_and_bad_dims():
     with pytest.raises(rgcn.RgcnError) as e:
         rgcn.rgcn_block_workspace_size(dblk, rgcn.Params("f32", 6, 8, [w], [w]))
     assert e.value.status == 7
+
+
+# transpose degrees around the split threshold of the backward (128 edges per piece) and
+# far beyond it: one piece plus one edge, whole pieces, a ragged last piece, and in bf16 a
+# hub past the LDS sort of the plan.  (fp32 stops at 3,000: each fp32 input-side term
+# carries a rounding error of about sqrt(d_out) 2^-24 of its size, and over 17,000
+# cancelling terms that alone reaches the 1e-5 bar at elements of rms size, whatever the
+# order of summation.)
+HUBS = {"f32": [129, 256, 257, 1000, 3000], "bf16": [129, 256, 257, 1000, 3000, 17000]}
+
+
+@pytest.mark.parametrize("dtype,d_in,d_out", [("f32", 64, 32), ("bf16", 128, 64),
+                                              ("f32", 32, 16), ("bf16", 264, 40)])
+def test_split_hub_rows(dtype, d_in, d_out):
+    """Source rows whose transpose holds more than one piece of edges are summed piecewise
+    by several lane groups and then reduced; their input and embedding gradients, with the
+    ReLU mask and with repeated edges, against the oracle.  d 32 fp32 leaves more relations
+    per type than lanes per group (the non-pipelined sum)."""
+    rng = np.random.default_rng(d_in + d_out)
+    rels = [(0, 0), (0, 1), (1, 0), (0, 0)] + ([(0, 1)] * 6 if d_in == 32 else [])
+    blk = synth.random_block(rng, [6000, 900], [2000, 700], rels, 6)
+    blk = synth.with_hub_sources(rng, blk, 0, HUBS[dtype])
+    refs = np.zeros(6000, np.int64)
+    for rel in blk.rels:
+        if rel.src_type == 0:
+            refs += np.bincount(np.asarray(rel.indices, np.int64), minlength=6000)
+    assert refs.max() >= HUBS[dtype][-1] and (refs > 128).sum() >= len(HUBS[dtype])
+    print(f"case split hubs {dtype} {d_in}->{d_out}: nnz {sum(r.nnz for r in blk.rels)}",
+          flush=True)
+    for relu in (False, True):
+        run = BlockRun(blk, dtype, d_in, d_out, seed=13, use_ids=True, input_relu=relu,
+                       emb_types=(0,), grad_types=(0, 1))
+        run.run_gpu()
+        run.run_oracle()
+        run.assert_parity()
