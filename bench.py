@@ -819,6 +819,34 @@ def mfma_stages(spec, mb, stack, avg):
     return mfma, mfma_bwd
 
 
+def gather_by_ids(spec, mb, stack, reps: int = 10) -> dict:
+    """Block 0's gather when each edge's table row is resolved through the block's row ids
+    (indices -> ids -> row, a dependent random 8-byte read per edge) instead of read from
+    the sampler's per-edge rows as the timed steps do: same segments, same bytes by the
+    method's count, the id lookup on the critical path."""
+    import torch
+
+    from paper_2406_06022_amd import rgcn
+
+    blk = mb.blocks[0]
+    db = rgcn.DeviceBlock(blk, stack.blocks[0].grad_src_types, stack.device)
+    p, ws, inp = stack.params[0], stack.workspaces[0], stack.inputs[0]
+    rgcn.rgcn_block_plan(db, p, ws, rgcn.RGCN_PLAN_FORWARD)
+    for _ in range(2):
+        rgcn.rgcn_block_aggregate(db, inp, p, ws)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        rgcn.rgcn_block_aggregate(db, inp, p, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    byts = survey_bytes(spec, blk, stack.blocks[0], "aggregate", 0)
+    gbs = byts / (ms * 1e-3) / 1e9
+    return {"ms": round(ms, 4), "bytes": byts, "GB/s": round(gbs, 1),
+            "frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+
 def measure_skewed(args, tables, dev):
     """The billion-edge workload with power-law sources (p(rank k) proportional to
     (k + 1)^-0.8 through a fixed id bijection), the backward's load-balance stress: the
@@ -1010,6 +1038,7 @@ def main() -> int:
             position += n
     traffic = read_traffic(kernel_name, spec.name, position)
     mfma, mfma_bwd = mfma_stages(spec, mb, stack, avg)
+    gather_ids = gather_by_ids(spec, mb, stack)
 
     # attainable streaming bandwidth of this machine: a plain 1 GiB fp32 copy (read + write)
     src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
@@ -1102,6 +1131,7 @@ def main() -> int:
                      "bytes": dom["bytes"], "impl_bytes": dom["impl_bytes"],
                      "launch_position": position},
         "hbm_kernels": rooflines,
+        "aggregate[0]_rows_by_id_lookup": gather_ids,
         "copy_probe_GBs": round(copy_gbs, 1),
         "mfma_transforms": mfma,
         "mfma_backward": mfma_bwd,

@@ -73,13 +73,22 @@ typedef enum { RGCN_F32 = 0, RGCN_BF16 = 1 } rgcn_dtype;
 
 /* One relation (canonical edge type src_type -> dst_type) of a block, as a CSR over the
  * destination rows.  indptr[0] = 0, non-decreasing, indptr[n_dst] = nnz; indices are
- * block-local source rows in [0, n_src[src_type]); repeats allowed. */
+ * block-local source rows in [0, n_src[src_type]); repeats allowed.
+ * src_rows (optional, NULL = not given): the input-table row of each edge's source,
+ * src_rows[k] = in[src_type].row_ids[indices[k]] (indices[k] when the input has no row
+ * ids), as a sampler that drew the edges from the graph already holds it (the global id
+ * of each sampled in-edge's source, before relabelling).  When given, the forward gather
+ * reads each edge's table row from it instead of resolving indices[k] through row_ids,
+ * which spares a dependent random 8-byte read per edge.  The caller guarantees the
+ * equality; RGCN_VALIDATE_DEVICE checks it (RGCN_ERR_INDEX_OOB otherwise).  Everything
+ * else (the transpose, the backward, the embedding scatter) uses indices and row_ids. */
 typedef struct {
     int32_t src_type;
     int32_t dst_type;
     int64_t nnz;
     const int32_t *indptr;    /* [n_dst[dst_type] + 1] */
     const int32_t *indices;   /* [nnz] */
+    const int64_t *src_rows;  /* [nnz] or NULL */
 } rgcn_relation;
 
 /* A block: node-type counts and relations.  grad_src_types has bit t set when backward
@@ -313,6 +322,10 @@ rgcn_status rgcn_sample_workspace_size(const rgcn_graph *graph,
  *   out_indices[r]: int32, capacity n_dst[dst(r)] * fanout (block-local source rows)
  *   out_src_ids[t]: int64, capacity n_dst[t] + sum over r with src(r) = t of
  *                   n_dst[dst(r)] * fanout (global ids of the block's source nodes)
+ *   out_src_rows:   NULL, or per relation NULL or int64 with the capacity of
+ *                   out_indices[r]: the global id of each sampled edge's source, in edge
+ *                   order (out_src_ids[src(r)][out_indices[r][k]]; at the input layer the
+ *                   rgcn_relation.src_rows of the block)
  *   counts:         int64 [num_rels + num_types]: sampled edges per relation, then source
  *                   nodes per type (read it after the stream completes to size the block)
  * Entries for relations or types whose capacity is zero may be NULL.  Capacities must
@@ -326,7 +339,8 @@ rgcn_status rgcn_sample_block(const rgcn_graph *graph, const int64_t *const *dst
                               const int64_t *n_dst /* [host] */, int32_t fanout, uint64_t seed,
                               int32_t layer, int32_t *const *out_indptr /* [host] */,
                               int32_t *const *out_indices /* [host] */,
-                              int64_t *const *out_src_ids /* [host] */, int64_t *counts,
+                              int64_t *const *out_src_ids /* [host] */,
+                              int64_t *const *out_src_rows /* [host] or NULL */, int64_t *counts,
                               void *workspace, size_t workspace_bytes, unsigned flags,
                               hipStream_t stream);
 

@@ -25,10 +25,14 @@ class MiniBatchStack:
     def __init__(self, blocks, input_tables: Sequence[Optional[torch.Tensor]],
                  input_ids: Sequence[Optional[torch.Tensor]], weights, dtype: str,
                  dims: Sequence[int], emb_types: Sequence[int] = (), device="cuda",
-                 want_weight_grads: bool = True, ids_unique: bool = True):
+                 want_weight_grads: bool = True, ids_unique: bool = True,
+                 edge_rows: bool = True):
         """blocks: host blocks (blocks[0] nearest the input); input_tables[t] / input_ids[t]:
         layer-0 table and int64 global row ids of each type; weights[l] = (w_rel, w_self,
-        bias) device tensors of layer l; emb_types: types whose table is learnable."""
+        bias) device tensors of layer l; emb_types: types whose table is learnable.
+        edge_rows: give the first block's per-edge source rows (``rel.src_rows``, the
+        sampler's global source ids) to the library when the blocks carry them and every
+        type has row ids, so its gather reads each edge's table row directly."""
         self.L = len(blocks)
         self.dtype = dtype
         self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
@@ -37,6 +41,7 @@ class MiniBatchStack:
         self.emb_types = list(emb_types)
         self.ids_unique = ids_unique
         self.blocks: List[rgcn.DeviceBlock] = []
+        rows0 = edge_rows and all(x is not None for x in input_ids)
         for l, blk in enumerate(blocks):
             if l == 0:
                 mask = 0
@@ -47,7 +52,7 @@ class MiniBatchStack:
                 for t in range(len(blk.n_src)):
                     if blk.n_src[t] > 0:
                         mask |= 1 << t
-            self.blocks.append(rgcn.DeviceBlock(blk, mask, device))
+            self.blocks.append(rgcn.DeviceBlock(blk, mask, device, src_rows=rows0 and l == 0))
         self.params = [rgcn.Params(dtype, dims[l], dims[l + 1], *weights[l]) for l in range(self.L)]
         self.workspaces = [rgcn.new_workspace(b, p, device) for b, p in zip(self.blocks, self.params)]
         # activations: y[l][t] = output of block l, [n_dst x d_{l+1}]

@@ -210,6 +210,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
     constexpr int NB = S / U;
     static_assert(S % U == 0 && (G & (G - 1)) == 0, "power-of-two groups, whole batches");
     __shared__ const int32_t *s_idx[kMaxSlots];
+    __shared__ const int64_t *s_rows[kMaxSlots];
     __shared__ int32_t s_src[kMaxSlots];
     __shared__ TypeInput s_tab[kMaxTypes];
     __shared__ int64_t s_addr[W][64];
@@ -217,6 +218,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
     __shared__ int32_t s_deg[W][64];
     for (int i = threadIdx.x; i < nslots; i += kThreads) {
         s_idx[i] = slots[i].indices;
+        s_rows[i] = slots[i].rows;
         s_src[i] = slots[i].src_type;
     }
     for (int i = threadIdx.x; i < kMaxTypes; i += kThreads) s_tab[i] = tabs.in[i];
@@ -311,20 +313,27 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
         }
         return e;
     };
-    // source row (index within its type) of an entry; -1 for none
-    auto load_src = [&](const Ent &e) -> int32_t {
+    // source of an entry: its row within its type, or, for an edge of a relation whose
+    // table rows are given per edge, that table row; -1 for none
+    auto load_src = [&](const Ent &e) -> int64_t {
         const bool edge = e.kind == 3;
-        const int32_t *p = edge ? s_idx[e.slot] + e.k : (const int32_t *)zero;
-        const int32_t v = *gbl(p);
-        return edge ? v : (e.kind == 2 ? e.k : -1);
+        const int64_t *pr = s_rows[e.slot];
+        int64_t v;
+        if (pr != nullptr) {
+            v = *gbl(edge ? pr + e.k : (const int64_t *)zero);
+        } else {
+            v = *gbl(edge ? s_idx[e.slot] + e.k : (const int32_t *)zero);
+        }
+        return edge ? v : (e.kind == 2 ? (int64_t)e.k : -1);
     };
-    // absolute address of that row (the zero row for none)
-    auto load_addr = [&](int slot, int32_t j) -> int64_t {
+    // absolute address of that row (the zero row for none): a row within the type goes
+    // through the type's row ids, a per-edge table row is used as it is
+    auto load_addr = [&](int slot, int64_t j) -> int64_t {
         const int t = s_src[slot];
         const int64_t *rid = s_tab[t].row_ids;
-        const bool look = j >= 0 && rid != nullptr;
-        const int64_t v = *gbl(look ? rid + j : (const int64_t *)zero);
-        const int64_t row = rid != nullptr ? v : (int64_t)j;
+        const bool ids = rid != nullptr && s_rows[slot] == nullptr;
+        const int64_t v = *gbl((j >= 0 && ids) ? rid + j : (const int64_t *)zero);
+        const int64_t row = ids ? v : j;
         return j < 0 ? zrow : (int64_t)(uintptr_t)s_tab[t].base + row * (s_tab[t].ld * ES);
     };
 
@@ -349,11 +358,11 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
     Ent ez = scan(dw, sc, e0);
     next_run();
     dw = load_win(sc);
-    int32_t jz = load_src(ez);
+    int64_t jz = load_src(ez);
     Ent ey = scan(dw, sc, e0);
     next_run();
     dw = load_win(sc);
-    int32_t jy = load_src(ey);
+    int64_t jy = load_src(ey);
     int64_t az = load_addr(ez.slot, jz);
 
     float acc[CPL][VEC];
@@ -391,7 +400,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
         Ent ex = scan(dw, sc, e0);
         next_run();
         dw = load_win(sc);
-        const int32_t jx = load_src(ex);
+        const int64_t jx = load_src(ex);
         const int64_t ay = load_addr(ey.slot, jy);
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
@@ -1263,6 +1272,27 @@ hipError_t validate_csr(const int32_t *indptr, const int32_t *indices, int64_t n
                         int64_t nnz, int64_t n_src, uint32_t *err, hipStream_t s) {
     hipLaunchKernelGGL(k_validate_csr, dim3((unsigned)cdiv(n_dst + 1, kThreads)), dim3(kThreads),
                        0, s, indptr, indices, n_dst, nnz, n_src, err);
+    return hipGetLastError();
+}
+
+// Per-edge table rows must be those the indices and row ids name (and inside the table).
+__global__ __launch_bounds__(kThreads) void k_validate_src_rows(const int32_t *indices,
+                                                                const int64_t *rows, int64_t nnz,
+                                                                int64_t n_src, const int64_t *ids,
+                                                                int64_t num_rows, uint32_t *err) {
+    const int64_t k = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (k >= nnz) return;
+    const int64_t j = indices[k], x = rows[k];
+    if (j < 0 || j >= n_src) return;   // reported by the CSR check
+    const int64_t want = ids ? ids[j] : j;
+    if (x != want || x < 0 || x >= num_rows) atomicOr(err, 2u);
+}
+hipError_t validate_src_rows(const int32_t *indices, const int64_t *rows, int64_t nnz,
+                             int64_t n_src, const int64_t *ids, int64_t num_rows, uint32_t *err,
+                             hipStream_t s) {
+    if (nnz == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_validate_src_rows, dim3((unsigned)cdiv(nnz, kThreads)), dim3(kThreads), 0,
+                       s, indices, rows, nnz, n_src, ids, num_rows, err);
     return hipGetLastError();
 }
 

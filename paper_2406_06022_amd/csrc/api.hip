@@ -126,6 +126,8 @@ rgcn_status check_block(const rgcn_block *b) {
             return fail(RGCN_ERR_INVALID_ARG, "relation %d: indices NULL or misaligned", r);
         if (rel.nnz > 0 && b->n_src[rel.src_type] == 0)
             return fail(RGCN_ERR_SHAPE, "relation %d: edges into an empty source type", r);
+        if (rel.src_rows && ((uintptr_t)rel.src_rows & 7u))
+            return fail(RGCN_ERR_INVALID_ARG, "relation %d: src_rows misaligned", r);
     }
     return RGCN_OK;
 }
@@ -196,6 +198,7 @@ rgcn_status make_layout(const rgcn_block *b, const rgcn_params *p, Layout &L) {
             s.seg_base = L.n_seg;
             s.indptr = b->rels[r].indptr;
             s.indices = b->rels[r].indices;
+            s.rows = b->rels[r].nnz > 0 ? b->rels[r].src_rows : nullptr;
             s.src_type = b->rels[r].src_type;
             s.dst_type = t;
             s.col_off = pos * L.d_in;
@@ -371,11 +374,20 @@ rgcn_status device_validate(const rgcn_block *b, const rgcn_input *in, const Lay
         TRY_HIP(validate_csr(rel.indptr, rel.indices, b->n_dst[rel.dst_type], rel.nnz,
                              b->n_src[rel.src_type], err, s), "validate_csr");
     }
-    if (in)
+    if (in) {
         for (int t = 0; t < L.T; ++t)
             if (in[t].row_ids)
                 TRY_HIP(validate_ids(in[t].row_ids, b->n_src[t], in[t].num_rows, err, s),
                         "validate_ids");
+        for (int r = 0; r < L.R; ++r) {
+            const rgcn_relation &rel = b->rels[r];
+            if (rel.src_rows && rel.nnz > 0)
+                TRY_HIP(validate_src_rows(rel.indices, rel.src_rows, rel.nnz,
+                                          b->n_src[rel.src_type], in[rel.src_type].row_ids,
+                                          in[rel.src_type].num_rows, err, s),
+                        "validate_src_rows");
+        }
+    }
     uint32_t host = 0;
     TRY_HIP(hipMemcpyAsync(&host, err, 4, hipMemcpyDeviceToHost, s), "validate copy");
     TRY_HIP(hipStreamSynchronize(s), "validate sync");
@@ -894,8 +906,8 @@ rgcn_status rgcn_sample_block(const rgcn_graph *graph, const int64_t *const *dst
                               const int64_t *n_dst, int32_t fanout, uint64_t seed,
                               int32_t layer, int32_t *const *out_indptr,
                               int32_t *const *out_indices, int64_t *const *out_src_ids,
-                              int64_t *counts, void *workspace, size_t workspace_bytes,
-                              unsigned flags, hipStream_t stream) {
+                              int64_t *const *out_src_rows, int64_t *counts, void *workspace,
+                              size_t workspace_bytes, unsigned flags, hipStream_t stream) {
     SampleTab T;
     SampleLayout L;
     rgcn_status st = sample_tab(graph, n_dst, fanout, T, L);
@@ -929,6 +941,10 @@ rgcn_status rgcn_sample_block(const rgcn_graph *graph, const int64_t *const *dst
             return fail(RGCN_ERR_INVALID_ARG, "out_indices[%d] NULL or misaligned", r);
         T.out_indptr[r] = out_indptr[r];
         T.out_indices[r] = out_indices[r];
+        int64_t *rows = out_src_rows ? out_src_rows[r] : nullptr;
+        if (rows && ((uintptr_t)rows & 7u))
+            return fail(RGCN_ERR_INVALID_ARG, "out_src_rows[%d] misaligned", r);
+        T.out_src_rows[r] = cap > 0 ? rows : nullptr;
     }
     char *ws = (char *)workspace;
     TRY_HIP(sample_block(T, L, ws, counts, stream), "sampling");

@@ -108,6 +108,7 @@ struct FwdSlot {
     int64_t seg_base;        // first segment id of this slot
     const int32_t *indptr;   // NULL: self-loop slot (every row has degree 1)
     const int32_t *indices;
+    const int64_t *rows;     // table row of each edge's source, or NULL (resolve indices)
     int32_t src_type;
     int32_t dst_type;
     int32_t col_off;         // element offset of this slot inside a row of Mcat_t
@@ -246,6 +247,7 @@ struct SampleTab {
     const int64_t *g_indices[kMaxRels];
     int32_t *out_indptr[kMaxRels];
     int32_t *out_indices[kMaxRels];
+    int64_t *out_src_rows[kMaxRels];   // global source id per sampled edge, or NULL
 };
 struct SampleLayout {
     size_t off_err, off_tab, off_seg, off_scan, off_cand, off_flag, off_first, total;
@@ -310,6 +312,9 @@ hipError_t validate_csr(const int32_t *indptr, const int32_t *indices, int64_t n
                         int64_t nnz, int64_t n_src, uint32_t *err, hipStream_t s);
 hipError_t validate_ids(const int64_t *ids, int64_t n, int64_t num_rows, uint32_t *err,
                         hipStream_t s);
+hipError_t validate_src_rows(const int32_t *indices, const int64_t *rows, int64_t nnz,
+                             int64_t n_src, const int64_t *ids, int64_t num_rows, uint32_t *err,
+                             hipStream_t s);
 
 // gemm.hip
 // Forward: Y = A W + bias (opt. ReLU); A [M x K] row-major (ld K), wcat_t [N x K].

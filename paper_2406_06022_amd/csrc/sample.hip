@@ -265,6 +265,7 @@ __global__ __launch_bounds__(kThreads) void k_dedup_emit(const SampleTab *tab, c
         const int32_t loc = rank[f] - rank[T.type_base[t]];
         if (f == (int32_t)p) T.out_src_ids[t][loc] = id;
         if (r >= 0) T.out_indices[r][e] = loc;
+        if (r >= 0 && T.out_src_rows[r]) T.out_src_rows[r][e] = id;
     }
 }
 

@@ -56,7 +56,7 @@ class RgcnError(RuntimeError):
 class _Relation(ctypes.Structure):
     _fields_ = [("src_type", ctypes.c_int32), ("dst_type", ctypes.c_int32),
                 ("nnz", ctypes.c_int64), ("indptr", ctypes.c_void_p),
-                ("indices", ctypes.c_void_p)]
+                ("indices", ctypes.c_void_p), ("src_rows", ctypes.c_void_p)]
 
 
 class _Block(ctypes.Structure):
@@ -157,8 +157,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.rgcn_sample_workspace_size.argtypes = [vp, vp, ctypes.c_int32, vp]
         lib.rgcn_sample_workspace_size.restype = st
         lib.rgcn_sample_block.argtypes = [vp, vp, vp, ctypes.c_int32, ctypes.c_uint64,
-                                          ctypes.c_int32, vp, vp, vp, vp, vp, ctypes.c_size_t,
-                                          ctypes.c_uint, vp]
+                                          ctypes.c_int32, vp, vp, vp, vp, vp, vp,
+                                          ctypes.c_size_t, ctypes.c_uint, vp]
         lib.rgcn_sample_block.restype = st
         lib.rgcn_lp_workspace_size.argtypes = [vp, vp]
         lib.rgcn_lp_workspace_size.restype = st
@@ -209,15 +209,18 @@ class DeviceBlock:
 
     ``blk`` is anything with ``n_src``, ``n_dst`` and ``rels`` (each relation with
     ``src_type``, ``dst_type``, ``indptr`` and ``indices``); arrays are copied to
-    ``device`` as int32."""
+    ``device`` as int32.  With ``src_rows`` the relations' per-edge input-table rows
+    (``rel.src_rows``, int64, the sampler's global source ids) go along too (the input
+    layer only: they must equal row_ids[indices])."""
 
-    def __init__(self, blk, grad_src_types: int = 0, device="cuda"):
+    def __init__(self, blk, grad_src_types: int = 0, device="cuda", src_rows: bool = False):
         self.n_src = [int(x) for x in blk.n_src]
         self.n_dst = [int(x) for x in blk.n_dst]
         self.num_types = len(self.n_src)
         self.grad_src_types = int(grad_src_types)
         self.indptr: List[torch.Tensor] = []
         self.indices: List[torch.Tensor] = []
+        self.src_rows: List[Optional[torch.Tensor]] = []
         self.types = []
         for rel in blk.rels:
             ip = torch.as_tensor(np.ascontiguousarray(rel.indptr, dtype=np.int32)).to(device)
@@ -225,6 +228,12 @@ class DeviceBlock:
             ix = (ix if ix.numel() else torch.zeros(1, dtype=torch.int32)).to(device)
             self.indptr.append(ip)
             self.indices.append(ix)
+            sr = getattr(rel, "src_rows", None) if src_rows else None
+            if sr is not None and len(rel.indices):
+                sr = torch.as_tensor(np.ascontiguousarray(sr, dtype=np.int64)).to(device)
+            else:
+                sr = None
+            self.src_rows.append(sr)
             self.types.append((int(rel.src_type), int(rel.dst_type), int(len(rel.indices))))
         self.num_rels = len(self.types)
         self._n_src = (ctypes.c_int64 * self.num_types)(*self.n_src)
@@ -232,7 +241,7 @@ class DeviceBlock:
         self._rels = (_Relation * max(self.num_rels, 1))()
         for r, (s, t, nnz) in enumerate(self.types):
             self._rels[r] = _Relation(s, t, nnz, self.indptr[r].data_ptr(),
-                                      self.indices[r].data_ptr())
+                                      self.indices[r].data_ptr(), _ptr(self.src_rows[r]))
         self.c = _Block(self.num_types, self.num_rels, self._n_src, self._n_dst, self._rels,
                         self.grad_src_types)
 
@@ -243,7 +252,7 @@ class DeviceBlock:
 
 class DeviceBlockView(DeviceBlock):
     """A block whose CSR arrays are already device tensors (e.g. from rgcn_sample_block):
-    rels = [(src_type, dst_type, indptr int32, indices int32)]."""
+    rels = [(src_type, dst_type, indptr int32, indices int32[, src_rows int64 or None])]."""
 
     def __init__(self, n_src, n_dst, rels, grad_src_types: int = 0):
         self.n_src = [int(x) for x in n_src]
@@ -252,6 +261,7 @@ class DeviceBlockView(DeviceBlock):
         self.grad_src_types = int(grad_src_types)
         self.indptr = [r[2] for r in rels]
         self.indices = [r[3] for r in rels]
+        self.src_rows = [r[4] if len(r) > 4 else None for r in rels]
         self.types = [(int(r[0]), int(r[1]), int(r[3].numel())) for r in rels]
         self.num_rels = len(self.types)
         self._n_src = (ctypes.c_int64 * self.num_types)(*self.n_src)
@@ -259,7 +269,7 @@ class DeviceBlockView(DeviceBlock):
         self._rels = (_Relation * max(self.num_rels, 1))()
         for r, (s, t, nnz) in enumerate(self.types):
             self._rels[r] = _Relation(s, t, nnz, self.indptr[r].data_ptr(),
-                                      self.indices[r].data_ptr())
+                                      self.indices[r].data_ptr(), _ptr(self.src_rows[r]))
         self.c = _Block(self.num_types, self.num_rels, self._n_src, self._n_dst, self._rels,
                         self.grad_src_types)
 
@@ -466,10 +476,11 @@ def rgcn_sample_workspace_size(graph: DeviceGraph, n_dst: Sequence[int], fanout:
 
 def rgcn_sample_block(graph: DeviceGraph, dst_ids: Sequence[torch.Tensor], fanout: int,
                       seed: int, layer: int, workspace: Optional[torch.Tensor] = None,
-                      flags: int = 0, stream=None):
+                      flags: int = 0, stream=None, src_rows: bool = False):
     """One layer's block for destination ids ``dst_ids[t]`` (device int64).  Returns
-    (out_indptr, out_indices, out_src_ids, counts): capacity-sized device tensors and the
-    device int64 counts [num_rels + num_types]."""
+    (out_indptr, out_indices, out_src_ids, counts) -- capacity-sized device tensors and the
+    device int64 counts [num_rels + num_types] -- and, with ``src_rows``, a fifth element:
+    the global source id of every sampled edge per relation."""
     T, R = graph.num_types, graph.num_rels
     dev = graph.indptr[0].device if R else dst_ids[0].device
     n_dst = [int(x.numel()) for x in dst_ids]
@@ -481,15 +492,20 @@ def rgcn_sample_block(graph: DeviceGraph, dst_ids: Sequence[torch.Tensor], fanou
               for (_, t) in graph.types]
     cap = [n_dst[t] + sum(n_dst[d] * fanout for (s, d) in graph.types if s == t) for t in range(T)]
     out_src = [torch.empty(max(c, 1), dtype=torch.int64, device=dev) for c in cap]
+    out_rows = ([torch.empty(max(n_dst[t] * fanout, 1), dtype=torch.int64, device=dev)
+                 for (_, t) in graph.types] if src_rows else None)
     counts = torch.zeros(R + T, dtype=torch.int64, device=dev)
     ids = [x.contiguous() for x in dst_ids]
     keep = [_ptr_array([_ptr(x) for x in ids]), _ptr_array([_ptr(x) for x in out_ip]),
-            _ptr_array([_ptr(x) for x in out_ix]), _ptr_array([_ptr(x) for x in out_src])]
+            _ptr_array([_ptr(x) for x in out_ix]), _ptr_array([_ptr(x) for x in out_src]),
+            _ptr_array([_ptr(x) for x in out_rows]) if src_rows else None]
     nd = (ctypes.c_int64 * T)(*n_dst)
     _check(load_library().rgcn_sample_block(
         ctypes.byref(graph.c), keep[0], nd, int(fanout), int(seed), int(layer), keep[1],
-        keep[2], keep[3], counts.data_ptr(), workspace.data_ptr(), workspace.numel(), flags,
-        _stream(stream)))
+        keep[2], keep[3], keep[4], counts.data_ptr(), workspace.data_ptr(), workspace.numel(),
+        flags, _stream(stream)))
+    if src_rows:
+        return out_ip, out_ix, out_src, counts, out_rows
     return out_ip, out_ix, out_src, counts
 
 

@@ -13,20 +13,24 @@ from . import rgcn
 
 def sample_minibatch(graph: "rgcn.DeviceGraph", seeds: Sequence[torch.Tensor],
                      fanouts: Sequence[int], seed: int, grad_src_types=None,
-                     flags: int = 0, stream=None):
+                     flags: int = 0, stream=None, src_rows: bool = False):
     """Blocks (blocks[0] nearest the input, fanouts[l] for block l, as DeviceBlockView) and
     the input layer's source ids per type.  ``seeds[t]``: device int64 ids (may be empty).
-    ``grad_src_types[l]``: the grad mask given to block l (default 0)."""
+    ``grad_src_types[l]``: the grad mask given to block l (default 0).  With ``src_rows``
+    the input-side block also carries each edge's global source id (its table row)."""
     T = graph.num_types
     L = len(fanouts)
     frontier = [x.to(torch.int64).contiguous() for x in seeds]
     blocks: List[rgcn.DeviceBlockView] = []
     for layer in reversed(range(L)):
-        ip, ix, src, counts = rgcn.rgcn_sample_block(graph, frontier, fanouts[layer], seed,
-                                                     layer, flags=flags, stream=stream)
+        want_rows = src_rows and layer == 0
+        out = rgcn.rgcn_sample_block(graph, frontier, fanouts[layer], seed, layer, flags=flags,
+                                     stream=stream, src_rows=want_rows)
+        ip, ix, src, counts = out[:4]
         c = counts.cpu().tolist()   # synchronises: the block's sizes
         R = graph.num_rels
-        rels = [(graph.types[r][0], graph.types[r][1], ip[r], ix[r][: c[r]])
+        rels = [(graph.types[r][0], graph.types[r][1], ip[r], ix[r][: c[r]],
+                 out[4][r][: c[r]] if want_rows and c[r] > 0 else None)
                 for r in range(R)]
         n_src = c[R:R + T]
         n_dst = [int(x.numel()) for x in frontier]

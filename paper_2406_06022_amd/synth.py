@@ -156,6 +156,9 @@ class Relation:
     dst_type: int
     indptr: np.ndarray    # int32 [n_dst[dst_type] + 1]
     indices: np.ndarray   # int32 [nnz], local source rows in [0, n_src[src_type])
+    # int64 [nnz] global id of each edge's source as drawn (the sampler's output before
+    # relabelling: the input-table row of the source at the input layer), or None
+    src_rows: Optional[np.ndarray] = None
 
     @property
     def nnz(self) -> int:
@@ -327,7 +330,8 @@ def sample_minibatch(spec: WorkloadSpec, seed_ids: Optional[List[np.ndarray]] = 
                 local = _relabel(torch.as_tensor(src, device=device), src_t[s]).cpu().numpy()
             else:
                 local = np.zeros(0, np.int64)
-            rels.append(Relation(s, t, indptr.astype(np.int32), local.astype(np.int32)))
+            rels.append(Relation(s, t, indptr.astype(np.int32), local.astype(np.int32),
+                                 np.asarray(src, dtype=np.int64)))
         src_ids = [x.cpu().numpy().astype(np.int64) for x in src_t]
         blocks.insert(0, Block([int(x.shape[0]) for x in src_ids],
                                [int(x.shape[0]) for x in dst_ids], rels))

@@ -46,7 +46,8 @@ class BlockRun:
     def __init__(self, blk, dtype: str, d_in: int, d_out: int, seed: int, *,
                  grad_types=None, use_ids: bool = False, bias: bool = False,
                  input_relu: bool = False, fwd_relu: bool = False, emb_types=(),
-                 ids_unique: bool = True, dup_ids: bool = False, device="cuda"):
+                 ids_unique: bool = True, dup_ids: bool = False, device="cuda",
+                 edge_rows: bool = False):
         self.blk, self.dtype, self.d_in, self.d_out = blk, dtype, d_in, d_out
         T, R = len(blk.n_src), len(blk.rels)
         tdt = synth.torch_dtype(dtype)
@@ -82,13 +83,26 @@ class BlockRun:
             rgcn.RGCN_IDS_UNIQUE if ids_unique else 0)
         self.mask = mask
         self.device = device
+        # give the library each edge's table row (ids[src][indices]) as a sampler would
+        self.edge_rows = edge_rows
 
     # ------------------------------------------------------------------ GPU
     def device_setup(self):
         """Device copies of the block, weights, inputs and a NaN-filled workspace."""
         dev = self.device
         blk = self.blk
-        self.dblk = rgcn.DeviceBlock(blk, self.mask, dev)
+        if self.edge_rows:
+            rels = []
+            for rel in blk.rels:
+                ix = np.asarray(rel.indices, dtype=np.int64)
+                ids = self.ids[rel.src_type]
+                rows = ids.numpy()[ix] if ids is not None else ix
+                rels.append(synth.Relation(rel.src_type, rel.dst_type, rel.indptr, rel.indices,
+                                           rows))
+            self.dblk = rgcn.DeviceBlock(synth.Block(list(blk.n_src), list(blk.n_dst), rels),
+                                         self.mask, dev, src_rows=True)
+        else:
+            self.dblk = rgcn.DeviceBlock(blk, self.mask, dev)
         d_wr = [w.to(dev) for w in self.w_rel]
         d_ws = [w.to(dev) for w in self.w_self]
         d_b = [x.to(dev) if x is not None else None for x in self.bias]

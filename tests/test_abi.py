@@ -189,16 +189,20 @@ def test_sampling_host_validation(lib):
     p3 = (ctypes.c_void_p * 2)(0x70000, 0x80000)
     f = lib.rgcn_sample_block
     # workspace too small, misaligned workspace, NULL counts, NULL destination ids
-    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, 0x90000, 0x100000, 16, 0, None) == 6
-    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, 0x90000, 0x100010, out.value, 0,
+    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, None, 0x90000, 0x100000, 16, 0, None) == 6
+    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, None, 0x90000, 0x100010, out.value, 0,
              None) == 1
-    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, None, 0x100000, out.value, 0,
+    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, None, None, 0x100000, out.value, 0,
              None) == 1
     nul = (ctypes.c_void_p * 2)(None, 0x60000)
-    assert f(ctypes.byref(g), nul, nd, 8, 1, 0, p3, p3, p2, 0x90000, 0x100000, out.value, 0,
+    assert f(ctypes.byref(g), nul, nd, 8, 1, 0, p3, p3, p2, None, 0x90000, 0x100000, out.value, 0,
              None) == 1
     assert "dst_ids[0]" in lib.rgcn_last_error().decode()
-    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, 0x90000, 0x100000, out.value, 0x4,
+    odd = (ctypes.c_void_p * 2)(0x90004, None)     # per-edge source ids misaligned
+    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, odd, 0x90000, 0x100000, out.value, 0,
+             None) == 1
+    assert "out_src_rows[0]" in lib.rgcn_last_error().decode()
+    assert f(ctypes.byref(g), p2, nd, 8, 1, 0, p3, p3, p2, None, 0x90000, 0x100000, out.value, 0x4,
              None) == 1
 
 

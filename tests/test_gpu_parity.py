@@ -393,3 +393,33 @@ def test_split_hub_rows(dtype, d_in, d_out):
         run.run_gpu()
         run.run_oracle()
         run.assert_parity()
+
+
+@pytest.mark.parametrize("index", [1, 2, 3, 4])
+def test_per_edge_source_rows_match_id_resolution(index):
+    """The input layer given each edge's table row (as the sampler emits it) gathers the
+    same rows in the same order as resolving indices through the row ids: every output and
+    gradient bit for bit, and both at the oracle's bar; a wrong per-edge row is reported
+    under device validation."""
+    spec = synth.small_config(index)
+    blk = synth.sample_minibatch(spec).blocks[0]
+    T = len(spec.ntype_names)
+    emb = [t for t in range(T) if spec.featureless[t]]
+    run = BlockRun(blk, spec.dtype, spec.dims[0], spec.dims[1], seed=300 + index, use_ids=True,
+                   emb_types=emb, grad_types=emb)
+    print(f"case per-edge rows {spec.name} nnz {blk.nnz}", flush=True)
+    by_ids = run.run_gpu()[0]
+    run.edge_rows = True
+    by_rows = run.run_gpu(validate=True)[0]
+    _bitwise_equal(by_ids, by_rows)
+    run.run_oracle()
+    run.assert_parity()
+    # corrupt one per-edge row: validation reports it
+    r = next(i for i, rel in enumerate(blk.rels) if len(rel.indices))
+    run.device_setup()
+    run.dblk.src_rows[r][0] += 1
+    with pytest.raises(rgcn.RgcnError) as e:
+        rgcn.rgcn_block_plan(run.dblk, run.params, run.ws, rgcn.RGCN_VALIDATE_DEVICE)
+        rgcn.rgcn_block_aggregate(run.dblk, run.inputs, run.params, run.ws,
+                                  rgcn.RGCN_VALIDATE_DEVICE)
+    assert e.value.status == 4

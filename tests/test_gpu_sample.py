@@ -29,14 +29,18 @@ def _seeds(rng, nodes, counts):
             for n, c in zip(nodes, counts)]
 
 
-def _gpu_block(dg, dst, fanout, seed, layer, flags=0):
-    ip, ix, src, counts = rgcn.rgcn_sample_block(dg, [torch.as_tensor(x).cuda() for x in dst],
-                                                 fanout, seed, layer, flags=flags)
+def _gpu_block(dg, dst, fanout, seed, layer, flags=0, rows=False):
+    out = rgcn.rgcn_sample_block(dg, [torch.as_tensor(x).cuda() for x in dst], fanout, seed,
+                                 layer, flags=flags, src_rows=rows)
+    ip, ix, src, counts = out[:4]
     torch.cuda.synchronize()
     c = counts.cpu().numpy()
     R, T = dg.num_rels, dg.num_types
-    return ([x.cpu().numpy() for x in ip], [ix[r][: c[r]].cpu().numpy() for r in range(R)],
-            [src[t][: c[R + t]].cpu().numpy() for t in range(T)], c)
+    res = ([x.cpu().numpy() for x in ip], [ix[r][: c[r]].cpu().numpy() for r in range(R)],
+           [src[t][: c[R + t]].cpu().numpy() for t in range(T)], c)
+    if rows:
+        return res + ([out[4][r][: c[r]].cpu().numpy() for r in range(R)],)
+    return res
 
 
 @pytest.mark.parametrize("fanout", [1, 3, 10, 25, 64])
@@ -46,12 +50,15 @@ def test_one_layer_bit_exact(fanout):
     rng = np.random.default_rng(100 + fanout)
     dst = _seeds(rng, g.num_nodes, [400, 0, 250])   # a type without destinations
     print(f"case sample one layer fanout={fanout}", flush=True)
-    ip, ix, src, c = _gpu_block(dg, dst, fanout, seed=2024 + fanout, layer=1)
+    ip, ix, src, c, rows = _gpu_block(dg, dst, fanout, seed=2024 + fanout, layer=1, rows=True)
     ref = oracle.sample_block(g, dst, fanout, 2024 + fanout, 1)
     for r in range(len(RELS)):
         assert np.array_equal(ip[r], ref.rels[r].indptr), r
         assert np.array_equal(ix[r], ref.rels[r].indices), r
         assert c[r] == ref.rels[r].indices.shape[0]
+        # each sampled edge's global source id, as the block's input layer reads it
+        s = RELS[r][0]
+        assert np.array_equal(rows[r], ref.src_ids[s][ref.rels[r].indices]), r
     for t in range(3):
         assert np.array_equal(src[t], ref.src_ids[t]), t
         assert c[len(RELS) + t] == ref.n_src[t]
