@@ -451,6 +451,82 @@ def summarize_lp(args) -> str:
     return "\n".join(lines) + "\n"
 
 
+def summarize_counters(args) -> str:
+    """Per-dispatch averages of hardware counters for the kernels matching each pattern,
+    over the timed steps' launches (the first --warmup steps' launches skipped), from one
+    or more rocprofv3 --pmc counter_collection.csv files, with derived ratios."""
+    files = args.summarize_counters
+    pats = [p for p in args.kernels.split(",") if p]
+    per = {}   # pattern -> counter -> list of per-dispatch values
+    names = {}
+    for path in files:
+        with open(path, newline="") as f:
+            rows = list(csv.DictReader(f))
+        for pat in pats:
+            kre = _kernel_re(pat) if re.match(r"^\w+$", pat) else pat
+            by_counter = {}
+            for r in rows:
+                if not re.search(kre, r["Kernel_Name"]):
+                    continue
+                names.setdefault(pat, _short_name(r["Kernel_Name"]))
+                by_counter.setdefault(r["Counter_Name"], {}).setdefault(
+                    int(r["Dispatch_Id"]), 0.0)
+                by_counter[r["Counter_Name"]][int(r["Dispatch_Id"])] += float(r["Counter_Value"])
+            for cn, d in by_counter.items():
+                vals = [v for _, v in sorted(d.items())]
+                skip = len(vals) * args.warmup // (args.warmup + args.steps)
+                vals = vals[skip:] or vals
+                per.setdefault(pat, {})[cn] = sum(vals) / len(vals)
+    lines = [f"# hardware counters of {', '.join(pats)}", "", "Commands:", "", "```",
+             args.command, "```", "",
+             "Per-dispatch averages over the timed steps' launches (the warm-up steps' "
+             "launches dropped).  Derived: `gpu_cycles` = GRBM_GUI_ACTIVE / 8 (the counter "
+             "reads the sum over the 8 XCDs: 8x the kernel's cycles at the clock the trace "
+             "durations imply); `mfma_busy` = SQ_VALU_MFMA_BUSY_CYCLES / (gpu_cycles x 256 "
+             "CUs x 4 SIMDs); `valu_per_mfma` = SQ_INSTS_VALU / "
+             "SQ_INSTS_MFMA (SQ_INSTS_VALU includes the MFMA instructions); `wait_share` = "
+             "SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES (wave cycles spent waiting on "
+             "s_waitcnt); `lds_conflict_per_lds_inst` = SQ_LDS_BANK_CONFLICT / "
+             "SQ_INSTS_LDS; `fetch_GB`, `write_GB` = FETCH_SIZE and WRITE_SIZE (KiB) "
+             "scaled as the plain copy calibrates them.", ""]
+    f_scale = w_scale = None
+    for path in files:
+        with open(path, newline="") as f:
+            rows = list(csv.DictReader(f))
+        cf = [float(r["Counter_Value"]) for r in rows
+              if re.search(COPY_KERNEL, r["Kernel_Name"]) and r["Counter_Name"] == "FETCH_SIZE"]
+        cw = [float(r["Counter_Value"]) for r in rows
+              if re.search(COPY_KERNEL, r["Kernel_Name"]) and r["Counter_Name"] == "WRITE_SIZE"]
+        if cf:
+            f_scale = COPY_BYTES / (sum(cf) / len(cf) * 1024.0)
+        if cw:
+            w_scale = COPY_BYTES / (sum(cw) / len(cw) * 1024.0)
+    for pat in pats:
+        c = per.get(pat, {})
+        lines.append(f"## `{names.get(pat, pat)}`")
+        lines.append("")
+        for cn in sorted(c):
+            lines.append(f"- {cn}: {c[cn]:.6g}")
+        der = {}
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in c and c.get("GRBM_GUI_ACTIVE"):
+            der["gpu_cycles"] = c["GRBM_GUI_ACTIVE"] / 8
+            der["mfma_busy"] = c["SQ_VALU_MFMA_BUSY_CYCLES"] / (der["gpu_cycles"] * 256 * 4)
+        if c.get("SQ_INSTS_MFMA"):
+            der["valu_per_mfma"] = c.get("SQ_INSTS_VALU", 0.0) / c["SQ_INSTS_MFMA"]
+        if c.get("SQ_WAVE_CYCLES"):
+            der["wait_share"] = c.get("SQ_WAIT_INST_ANY", 0.0) / c["SQ_WAVE_CYCLES"]
+        if c.get("SQ_INSTS_LDS"):
+            der["lds_conflict_per_lds_inst"] = c.get("SQ_LDS_BANK_CONFLICT", 0.0) / c["SQ_INSTS_LDS"]
+        if "FETCH_SIZE" in c and f_scale:
+            der["fetch_GB"] = c["FETCH_SIZE"] * 1024.0 * f_scale / 1e9
+        if "WRITE_SIZE" in c and w_scale:
+            der["write_GB"] = c["WRITE_SIZE"] * 1024.0 * w_scale / 1e9
+        for k, v in der.items():
+            lines.append(f"- {k}: {v:.4g}")
+        lines.append("")
+    return "\n".join(lines) + "\n"
+
+
 def summarize_pmc(args) -> str:
     """Per-launch HBM traffic of --kernel from FETCH_SIZE and WRITE_SIZE runs, each scaled
     by what the same counter reads for the plain copy of --copy-probe-mib MiB."""
@@ -932,6 +1008,45 @@ def measure_configs(args, dev):
     return out
 
 
+def other_legs(args, spec, mb, tables, stack, dy, nnz, dev):
+    """The measurement legs after the main steps: training steps with the fused sparse
+    optimizer, the power-law-source workload, the other workloads, sampling, featureless
+    feature construction and the link-prediction decoder."""
+    import torch
+
+    # the sparse optimizer step of the learnable tables fused into block 0's transposed sum:
+    # full training steps (plan, forward, backward, table update) after the others, since
+    # they change the tables
+    stack.attach_adagrad(lr=0.01, eps=1e-10)
+    ada = time_steps(stack, dy, args.steps, args.warmup)
+    ada_ms = ada["wall_ms"]
+    ada_sp_ms = ada["stage_avg"][("sparse", 0)]
+    ada_bytes = algorithmic_bytes(spec, mb.blocks[0], stack.blocks[0], "sparse_adagrad", 0)
+    ada_gbs = ada_bytes / (ada_sp_ms * 1e-3) / 1e9
+    adagrad = {"ms_per_train_step": round(ada_ms, 4),
+               "edges_per_s": nnz / (ada_ms / 1e3),
+               "sparse[0]": {"kernel": "k_transpose_pipe_adagrad", "ms": round(ada_sp_ms, 4),
+                             "bytes": ada_bytes, "GB/s": round(ada_gbs, 1),
+                             "frac": round(ada_gbs / HBM_PEAK_GBS, 4)},
+               "lr": 0.01, "eps": 1e-10}
+    stack.release()
+    torch.cuda.empty_cache()
+
+    skewed = measure_skewed(args, tables, dev)
+    torch.cuda.empty_cache()
+    configs = measure_configs(args, dev)
+    torch.cuda.empty_cache()
+
+    g = full_graph(spec, dev)
+    sampling = measure_sampling(spec, g, dev, args)
+    featureless = measure_featureless(spec, g, tables, dev, args)
+    del g
+    torch.cuda.empty_cache()
+    link_prediction = measure_lp(dev, args)
+
+    return adagrad, skewed, configs, sampling, featureless, link_prediction
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -943,6 +1058,14 @@ def main() -> int:
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="reduce two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, "
                          "WRITE_SIZE) into the per-launch HBM traffic summary and exit")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="COUNTER_CSV",
+                    help="reduce rocprofv3 --pmc counter_collection.csv files to per-dispatch "
+                         "counter averages of the kernels in --kernels and exit")
+    ap.add_argument("--kernels", default="k_gemm_dw,k_gemm_fwd,LoadRowsF32HiLo",
+                    help="with --summarize-counters: comma-separated kernel names or patterns")
+    ap.add_argument("--main-only", action="store_true",
+                    help="time the main workload's steps (and the calibration copy) only: no "
+                         "CPU baseline, training steps or other measurement legs")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="reduce a rocprofv3 kernel_trace.csv into a per-kernel summary and exit")
     ap.add_argument("--summarize-kernels", nargs=2, metavar=("KERNEL_STATS_CSV", "REGEX"),
@@ -967,6 +1090,9 @@ def main() -> int:
     args = ap.parse_args()
     if args.summarize_pmc:
         print(summarize_pmc(args), end="")
+        return 0
+    if args.summarize_counters:
+        print(summarize_counters(args), end="")
         return 0
     if args.summarize_trace:
         print(summarize_trace(args), end="")
@@ -1053,8 +1179,8 @@ def main() -> int:
     copy_gbs = 2.0 * src.numel() * 4 * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del src, dst
 
-    cpu = None
-    if args.cpu_budget > 0:
+    cpu = adagrad = skewed = configs = sampling = featureless = link_prediction = None
+    if args.cpu_budget > 0 and not args.main_only:
         host = host_info()
         nt = oracle_threads()
         log(f"timing the CPU oracle on a sample of block 0 ({nt} threads, then 1)")
@@ -1074,32 +1200,9 @@ def main() -> int:
     # the sparse optimizer step of the learnable tables fused into block 0's transposed sum:
     # full training steps (plan, forward, backward, table update) after the others, since
     # they change the tables
-    stack.attach_adagrad(lr=0.01, eps=1e-10)
-    ada = time_steps(stack, dy, args.steps, args.warmup)
-    ada_ms = ada["wall_ms"]
-    ada_sp_ms = ada["stage_avg"][("sparse", 0)]
-    ada_bytes = algorithmic_bytes(spec, mb.blocks[0], stack.blocks[0], "sparse_adagrad", 0)
-    ada_gbs = ada_bytes / (ada_sp_ms * 1e-3) / 1e9
-    adagrad = {"ms_per_train_step": round(ada_ms, 4),
-               "edges_per_s": nnz / (ada_ms / 1e3),
-               "sparse[0]": {"kernel": "k_transpose_pipe_adagrad", "ms": round(ada_sp_ms, 4),
-                             "bytes": ada_bytes, "GB/s": round(ada_gbs, 1),
-                             "frac": round(ada_gbs / HBM_PEAK_GBS, 4)},
-               "lr": 0.01, "eps": 1e-10}
-    del stack
-    torch.cuda.empty_cache()
-
-    skewed = measure_skewed(args, tables, dev)
-    torch.cuda.empty_cache()
-    configs = measure_configs(args, dev)
-    torch.cuda.empty_cache()
-
-    g = full_graph(spec, dev)
-    sampling = measure_sampling(spec, g, dev, args)
-    featureless = measure_featureless(spec, g, tables, dev, args)
-    del g
-    torch.cuda.empty_cache()
-    link_prediction = measure_lp(dev, args)
+    if not args.main_only:
+        adagrad, skewed, configs, sampling, featureless, link_prediction = other_legs(
+            args, spec, mb, tables, stack, dy, nnz, dev)
 
     out = {
         "metric": METRIC,

@@ -104,6 +104,16 @@ class MiniBatchStack:
                                                   device=self.device))
         self.adagrad = (float(lr), float(eps), states)
 
+    def release(self) -> None:
+        """Drop every buffer the stack allocated (workspaces, activations, gradients,
+        optimizer state); the stack cannot step afterwards."""
+        self.workspaces = []
+        self.y = []
+        self.dh = []
+        self.dw_rel = self.dw_self = self.dbias = []
+        self.demb = []
+        self.adagrad = None
+
     @property
     def nnz(self) -> int:
         return sum(b.nnz for b in self.blocks)

@@ -51,18 +51,11 @@ __device__ __forceinline__ const __attribute__((address_space(1))) T *gbl(const 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-#ifndef RGCN_ROWS_NT
-#define RGCN_ROWS_NT 1
-#endif
 // Gathered rows are read once (no locality over a table of many GB): streaming loads, so
 // they do not push the index, row-id and descriptor lines out of L2.
 __device__ __forceinline__ u32x4 ld_row(const char *p) {
     const __attribute__((address_space(1))) u32x4 *g = (const __attribute__((address_space(1))) u32x4 *)p;
-#if RGCN_ROWS_NT
     return __builtin_nontemporal_load(g);
-#else
-    return *g;
-#endif
 }
 // 16-byte global load
 __device__ __forceinline__ uint4 ld16(const char *p) {
@@ -626,15 +619,12 @@ __device__ __forceinline__ void transpose_sum_body(const TsumArgs &a, int G, int
 // While the rows of one source row are in flight, the earlier steps of the next three
 // rows are too.  Edges past the group width are resolved in place.  Every load is
 // unconditional (unused lanes read a zero word).
-#ifndef RGCN_TSUM_U1
-#define RGCN_TSUM_U1 4
-#endif
 
 template <bool BF16IN, int CPL, bool OPT>
 __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, int gpw,
                                                     int chunks) {
     constexpr int HES = BF16IN ? 2 : 4;
-    constexpr int U = CPL == 1 ? RGCN_TSUM_U1 : 4;
+    constexpr int U = 4;   // rows in flight per lane
     constexpr int W = kThreads / 64;
     __shared__ TsumRel s_rel[kMaxRels];
     __shared__ int64_t s_off[W][64];
@@ -1071,15 +1061,14 @@ int64_t resident_wgs(K kernel) {
     return (int64_t)per_cu * cus;
 }
 
-#ifndef RGCN_FLAT_ROWS
-#define RGCN_FLAT_ROWS 8
-#endif
+// rows in flight per lane in the gather (for one chunk per lane)
+constexpr int kFlatRows = 8;
 
 template <bool B, int G, int C, bool FULL>
 hipError_t launch_flat_k(const SegDesc *desc, const int32_t *cs, int64_t nc_max,
                          const FwdSlot *slots_dev, int nslots, const GatherTabs &tabs,
                          char *ws_base, int chunks, uint32_t *claims, hipStream_t s) {
-    constexpr int U0 = RGCN_FLAT_ROWS / C > 0 ? RGCN_FLAT_ROWS / C : 1;
+    constexpr int U0 = kFlatRows / C > 0 ? kFlatRows / C : 1;
     constexpr int U = U0 < G ? U0 : G;
     const int64_t groups_per_wg = (int64_t)(kThreads / 64) * (64 / G);
     const int64_t cap = resident_wgs(k_gather_flat<B, G, C, U, FULL>);

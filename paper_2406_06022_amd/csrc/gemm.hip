@@ -52,18 +52,12 @@ struct Cfg {
 };
 using CfgWide = Cfg<256, 256, 2, 4>;
 using CfgNarrow = Cfg<128, 128, 2, 2>;
-#ifndef RGCN_FWD_WAVES
-#define RGCN_FWD_WAVES 16
-#endif
-using CfgFwd = typename std::conditional<RGCN_FWD_WAVES == 16, Cfg<256, 256, 4, 4>, CfgWide>::type;
+using CfgFwd = Cfg<256, 256, 4, 4>;   // bf16 forward: 16 waves of 64 x 64
 using CfgDms = CfgNarrow;   // bf16 input side: N is one or two slots of d_in columns
 // bf16 weight side (k_gemm_dw): 256 x 256 tiles of 8 waves, one workgroup per CU (16
 // waves of 64 x 64 measured 1 % slower)
-#ifndef RGCN_DW_WAVES
-#define RGCN_DW_WAVES 8
-#endif
-using CfgDw = typename std::conditional<RGCN_DW_WAVES == 16, Cfg<256, 256, 4, 4>, CfgWide>::type;
-constexpr int kDwMinWaves = RGCN_DW_WAVES / 4;   // per SIMD
+using CfgDw = CfgWide;
+constexpr int kDwMinWaves = CfgDw::NT / 64 / 4;   // waves per SIMD
 using CfgF32 = Cfg<128, 128, 2, 2>;
 
 template <int ROWS_, int BK_, int ES_>
@@ -796,10 +790,7 @@ struct DwGeom {
     static constexpr int CPR = RB / 16;            // 16-byte chunks per row
     static constexpr int RPI = 1024 / RB;          // rows per wave load instruction
     static constexpr int TILE = BK * RB;
-#ifndef RGCN_DW_SWZ
-#define RGCN_DW_SWZ 4
-#endif
-    static constexpr int SWZ = RGCN_DW_SWZ;
+    static constexpr int SWZ = 4;
     static_assert(CPR >= 4 * SWZ, "the slot swizzle stays within a row");
     __device__ __forceinline__ static int slot(int r, int c) { return c ^ ((r & 3) * SWZ); }
 };
@@ -1057,9 +1048,7 @@ __global__ __launch_bounds__(kThreads) void k_zero_outputs(DwOut out, int d_in, 
 }
 
 constexpr int kDwBK = 32;   // rows per K step of the bf16 weight-side kernel
-#ifndef RGCN_DW_STAGES
-#define RGCN_DW_STAGES 2     // LDS stages of k_gemm_dw (three measured 2 % slower)
-#endif
+constexpr int kDwStages = 2;   // LDS stages of k_gemm_dw (three measured 2 % slower)
 // workgroups of one weight-side product: the bf16 kernel holds a CU by itself (96 KB of
 // LDS), so one per CU of the 256 (a 2.02-wave grid left most CUs idle behind its last
 // few workgroups); the fp32 kernel fits two per CU
@@ -1080,18 +1069,11 @@ int64_t device_cus() {
     return cache[dev];
 }
 // forward transform: K step (elements) and LDS stages of k_gemm_fwd
-#ifndef RGCN_FWD_BK
-#define RGCN_FWD_BK 64
-#endif
-#ifndef RGCN_FWD_STAGES
-#define RGCN_FWD_STAGES 2
-#endif
-#ifndef RGCN_GEMM_DMS_STAGES
-#define RGCN_GEMM_DMS_STAGES 1
-#endif
-#ifndef RGCN_GEMM_DMS_R
-#define RGCN_GEMM_DMS_R 1
-#endif
+constexpr int kFwdBK = 64;
+constexpr int kFwdStages = 2;
+// input side: one LDS stage (two workgroups share a CU), one register stage
+constexpr int kDmsStages = 1;
+constexpr int kDmsRegStages = 1;
 
 }  // namespace
 
@@ -1107,7 +1089,7 @@ hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
         const int64_t cus = device_cus();
         if (P > cus) P = cus;
         P = (P + 7) / 8 * 8;
-        hipLaunchKernelGGL((k_gemm_fwd<C, RGCN_FWD_BK, RGCN_FWD_STAGES>), dim3((unsigned)P),
+        hipLaunchKernelGGL((k_gemm_fwd<C, kFwdBK, kFwdStages>), dim3((unsigned)P),
                            dim3(C::NT), 0, s, (const char *)a, (int64_t)K * 2, M,
                            (const char *)wcat_t, (int64_t)K * 2, (int64_t)N, (int64_t)K,
                            EpiForwardBf16{y, bias, M, N, relu}, tiles_m, tiles_n);
@@ -1146,8 +1128,8 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_
         LoadRowsF32HiLo<TL, C::NT, 2 * TL::BYTES> la{pa, d_out};
         LoadRows<TL, C::NT, SlotRows> lb{sr, (int64_t)d_out * 2};
         using Core = MmaBf16SplitA32<TL, C::FM, C::FN>;
-        return launch_gemm<C, Core, decltype(la), decltype(lb), EpiDms, RGCN_GEMM_DMS_STAGES,
-                           RGCN_GEMM_DMS_R>(la, lb, epi, M, N, d_out, 1, d_out, s);
+        return launch_gemm<C, Core, decltype(la), decltype(lb), EpiDms, kDmsStages,
+                           kDmsRegStages>(la, lb, epi, M, N, d_out, 1, d_out, s);
     }
     using C = CfgF32;
     using TL = TileF32;
@@ -1183,7 +1165,7 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
     if (bf) {
         using C = CfgDw;
         const int64_t tiles_m = cdiv(Kcat, C::TM), tiles_n = cdiv(d_out, C::TN);
-        hipLaunchKernelGGL((k_gemm_dw<C, kDwBK, RGCN_DW_STAGES, kDwMinWaves>),
+        hipLaunchKernelGGL((k_gemm_dw<C, kDwBK, kDwStages, kDwMinWaves>),
                            dim3((unsigned)(tiles_m * tiles_n * splits)),
                            dim3(C::NT), 0, s, (const char *)mcat, M, (int64_t)Kcat, dy,
                            (int64_t)d_out, tiles_m, tiles_n, per, epi);
