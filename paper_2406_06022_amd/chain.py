@@ -218,6 +218,25 @@ class MiniBatchStack:
         self.backward(dy_top, timer=timer)
 
 
+    def capture_step(self, dy_top, overlap_plan: bool = True) -> "torch.cuda.CUDAGraph":
+        """Record one step (plan, forward, backward, and the optimizer step when attached)
+        into a HIP graph; ``graph.replay()`` then reruns it with one launch from the host.
+        Every buffer the step touches is allocated already, the library allocates nothing
+        and clears no memory with memset nodes (its counters are cleared by kernels), and a
+        step has no host synchronisation, so the recorded launches are the step.  One eager
+        step on a side stream comes first (it creates the plan's second stream)."""
+        side = torch.cuda.Stream(device=self.device)
+        side.wait_stream(torch.cuda.current_stream(self.device))
+        with torch.cuda.stream(side):
+            self.step(dy_top, overlap_plan=overlap_plan)
+        torch.cuda.current_stream(self.device).wait_stream(side)
+        torch.cuda.synchronize(self.device)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, capture_error_mode="thread_local"):
+            self.step(dy_top, overlap_plan=overlap_plan)
+        return graph
+
+
 def _mark(timer, tag, edge: int) -> None:
     if timer is not None:
         timer(tag, edge)
