@@ -348,42 +348,40 @@ def _by_position(rows, per_step: int, skip_steps: int, steps: int):
 
 
 def summarize_trace(args) -> str:
-    """Per-kernel time of a kernel-trace run, and the launches of --kernel by position."""
-    per, other, legs = {}, [0, 0.0], [0, 0.0]
+    """Per-kernel time of a kernel-trace run over the eagerly launched steps (warm-up and
+    timed), and the launches of --kernel by position within a step.  The steps' window ends
+    where the step after them starts: the gather launch that follows the last step's
+    (--blocks launches per step)."""
+    per, rest = {}, [0, 0.0]
     with open(args.summarize_trace, newline="") as f:
-        rows = list(csv.DictReader(f))
-    # the measurement legs after the training steps (sampling, featureless features, link
-    # prediction) begin with the first of their kernels; library launches from then on are
-    # not part of a step
-    leg_re = re.compile(r"k_sample|k_dedup|k_fill_first|k_feature_mean|k_lp_")
-    starts = [float(r["Start_Timestamp"]) for r in rows if leg_re.search(r["Kernel_Name"])]
-    cut = min(starts) if starts else float("inf")
+        rows = sorted(csv.DictReader(f), key=lambda r: float(r["Start_Timestamp"]))
+    steps = args.steps + args.warmup
+    gathers = [r for r in rows if re.search(_kernel_re("k_gather_flat"), r["Kernel_Name"])]
+    lo = float(gathers[0]["Start_Timestamp"]) if gathers else 0.0
+    hi = (float(gathers[steps * args.blocks]["Start_Timestamp"])
+          if len(gathers) > steps * args.blocks else float("inf"))
     for r in rows:
-        d = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
-        if "rgcn::" not in r["Kernel_Name"]:
-            a = other
-        elif float(r["Start_Timestamp"]) >= cut:
-            a = legs
-        else:
+        t0 = float(r["Start_Timestamp"])
+        d = float(r["End_Timestamp"]) - t0
+        if "rgcn::" in r["Kernel_Name"] and lo <= t0 < hi:
             a = per.setdefault(_short_name(r["Kernel_Name"]), [0, 0.0])
+        else:
+            a = rest
         a[0] += 1
         a[1] += d
-    steps = 2 * (args.steps + args.warmup)
     lines = [f"# {args.kernel}: kernel trace", "", "Command:", "", "```", args.command, "```", "",
              f"Launches of {args.kernel} by position within a step ({args.launches_per_step} "
-             f"per step, first {args.warmup} of {args.warmup + args.steps} steps skipped):", ""]
+             f"per step, first {args.warmup} of {steps} steps skipped):", ""]
     for p, (avg, n, name) in enumerate(_by_position(
             _dispatches(args.summarize_trace, _kernel_re(args.kernel)), args.launches_per_step,
             args.warmup, args.steps)):
         lines.append(f"- avg_us_pos{p}: {avg / 1e3:.1f} ({n} launches, {name})")
     ours = sum(v[1] for v in per.values())
-    lines += ["", f"Kernels of the library over the run's {steps} steps (warmup and timed, "
-              f"then as many training steps with the fused optimizer): "
-              f"{ours / 1e6:.3f} ms, {ours / steps / 1e6:.3f} ms per step.  Library kernels "
-              f"of the measurement legs after the steps (sampling, featureless features, link "
-              f"prediction): {legs[0]} launches, {legs[1] / 1e6:.3f} ms.  Other kernels "
-              f"(workload set-up: sampling, tables, weights): {other[0]} launches, "
-              f"{other[1] / 1e6:.3f} ms.", "",
+    lines += ["", f"Library kernels of the {steps} eagerly launched steps (warm-up and timed): "
+              f"{ours / 1e6:.3f} ms, {ours / steps / 1e6:.3f} ms per step (kernel time summed "
+              f"over both streams: the plan's backward part runs beside the transforms).  "
+              f"Everything else in the run (workload set-up, the graph-replayed steps, other "
+              f"measurements): {rest[0]} launches, {rest[1] / 1e6:.3f} ms.", "",
               "| kernel | calls | total ms | avg us | ms per step |", "|---|---:|---:|---:|---:|"]
     for name, (n, tot) in sorted(per.items(), key=lambda x: -x[1][1]):
         lines.append(f"| `{name}` | {n} | {tot / 1e6:.3f} | {tot / n / 1e3:.1f} | "
@@ -1117,6 +1115,8 @@ def main() -> int:
     ap.add_argument("--lp-only", action="store_true",
                     help="run only the link-prediction decoder measurement and print its JSON")
     ap.add_argument("--kernel", default="k_gather_flat")
+    ap.add_argument("--blocks", type=int, default=3,
+                    help="with --summarize-trace: blocks (gather launches) per step")
     ap.add_argument("--launches-per-step", type=int, default=3,
                     help="launches of --kernel per step (summaries split them by position)")
     ap.add_argument("--command", default="", help="command line recorded in a summary")
