@@ -463,25 +463,35 @@ def summarize_counters(args) -> str:
     for path in files:
         with open(path, newline="") as f:
             rows = list(csv.DictReader(f))
+        # the timed eager steps: from the first gather launch of the first timed step to the
+        # gather launch that follows the last step (--blocks gather launches per step)
+        gstarts = sorted({float(r["Start_Timestamp"]) for r in rows
+                          if re.search(_kernel_re("k_gather_flat"), r["Kernel_Name"])})
+        nb = args.blocks
+        lo = gstarts[args.warmup * nb] if len(gstarts) > args.warmup * nb else 0.0
+        end_i = (args.warmup + args.steps) * nb
+        hi = gstarts[end_i] if len(gstarts) > end_i else float("inf")
         for pat in pats:
             kre = _kernel_re(pat) if re.match(r"^\w+$", pat) else pat
             by_counter = {}
             for r in rows:
                 if not re.search(kre, r["Kernel_Name"]):
                     continue
+                if not lo <= float(r["Start_Timestamp"]) < hi:
+                    continue
                 names.setdefault(pat, _short_name(r["Kernel_Name"]))
                 by_counter.setdefault(r["Counter_Name"], {}).setdefault(
                     int(r["Dispatch_Id"]), 0.0)
                 by_counter[r["Counter_Name"]][int(r["Dispatch_Id"])] += float(r["Counter_Value"])
             for cn, d in by_counter.items():
-                vals = [v for _, v in sorted(d.items())]
-                skip = len(vals) * args.warmup // (args.warmup + args.steps)
-                vals = vals[skip:] or vals
+                vals = list(d.values())
                 per.setdefault(pat, {})[cn] = sum(vals) / len(vals)
+                per[pat]["launches"] = len(vals)
     lines = [f"# hardware counters of {', '.join(pats)}", "", "Commands:", "", "```",
              args.command, "```", "",
-             "Per-dispatch averages over the timed steps' launches (the warm-up steps' "
-             "launches dropped).  Derived: `gpu_cycles` = GRBM_GUI_ACTIVE / 8 (the counter "
+             "Per-dispatch averages over the launches of the timed, eagerly launched steps "
+             "(between the first gather launch of the first timed step and the gather launch "
+             "after the last step), all blocks and node types of a step together.  Derived: `gpu_cycles` = GRBM_GUI_ACTIVE / 8 (the counter "
              "reads the sum over the 8 XCDs: 8x the kernel's cycles at the clock the trace "
              "durations imply); `mfma_busy` = SQ_VALU_MFMA_BUSY_CYCLES / (gpu_cycles x 256 "
              "CUs x 4 SIMDs); `valu_per_mfma` = SQ_INSTS_VALU / "
