@@ -10,10 +10,13 @@
 //               global memory into LDS, 256 x 256 tiles (16 waves of 64 x 64),
 //               v_mfma_f32_16x16x32_bf16; persistent, one K-step pipeline across a
 //               workgroup's tiles, epilogue stored from registers;
-//   k_gemm      input side: the register-staged kernel below with 128 x 128 tiles (N is
-//               one or two slots of d_in columns; a 256-wide tile would be half empty),
-//               on v_mfma_f32_32x32x16_bf16 (the 16 x 16 x 32 form issues at half its
-//               rate on gfx950);
+//   k_dms_stream input side with at most 128 output columns and d_out 256 or 512 (the
+//               input layer's embedding slots): K split over the waves, the weights held
+//               in registers, dY read once in whole rows, partial sums met in LDS;
+//   k_gemm      input side otherwise: the register-staged kernel below with 128 x 128
+//               tiles (N is one or two slots of d_in columns; a 256-wide tile would be half
+//               empty), on v_mfma_f32_32x32x16_bf16 (the 16 x 16 x 32 form issues at half
+//               its rate on gfx950);
 //   k_gemm_dw   weight side: reduces over the rows of both operands; 256 x 256 tiles whose
 //               operands are loaded straight into LDS (one row per m) and read down the
 //               columns, on v_mfma_f32_32x32x16_bf16.
@@ -997,6 +1000,149 @@ __global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw(const char *__restrict_
     }
 }
 
+// ------------------------------------------------------------------ input side, streamed
+// dMs with at most 128 output columns (one slot of d_in <= 128, or a few narrower ones),
+// d_out a multiple of 256 up to 512: K (= d_out) is split over the 8 waves of a workgroup.
+// Each wave keeps its K slice of the weights of all 128 columns in registers and the
+// workgroup walks blocks of 16 dY rows: every wave reads its slice of the 16 rows straight
+// into registers (so the workgroup reads the 16 rows whole, at once), splits each fp32
+// value into its hi and lo bf16 parts, multiplies both against its weights, and leaves its
+// partial products in LDS; the waves then sum the 8 partials of 2 rows each, divide by the
+// degree and store whole rows.  dY is read exactly once, in whole rows; the register-
+// staged kernel reads it in 256-byte row pieces, once per column tile.
+// v_mfma_f32_16x16x32_bf16 with the weights as the first operand: lane l supplies weight
+// row 16 t + l % 16 and dY row m0 + l % 16, K group q = l / 16, and holds output row
+// m0 + l % 16, columns 16 t + 4 q .. + 3.  Wave w's slice is K values [KW w, KW w + KW),
+// KW = d_out / 8; MFMA step s gives group q the 8 values at KW w + 8 (S q + s) (S = KW / 32
+// steps), so each lane reads 32 S contiguous bytes of its row.  Partial row r, 4-column
+// piece c sits at slot c ^ (2 r) of the row's 512 bytes.  Two LDS buffers alternate
+// between row blocks (one barrier per block); each wave's register copies of the next NB
+// blocks are in flight while it multiplies one.
+constexpr int kDmsStreamCols = 128;                  // output columns
+constexpr int kDmsStreamWaves = 8;
+constexpr int kDmsStreamPart = 16 * kDmsStreamCols * 4;   // one wave's partial block
+struct DmsStream {
+    const void *w[kMaxSlots];          // W_slot [d_in x d_out] bf16
+    const int32_t *indptr[kMaxSlots];  // relation slot: degrees; NULL: the self slot
+    float *out;                        // [M x N]
+    int32_t N;
+    int32_t d_in;
+};
+template <int S, int NB>
+__global__ __launch_bounds__(kDmsStreamWaves * 64, 1) void k_dms_stream(
+    const float *__restrict__ dy, int64_t M, const DmsStream p) {
+    constexpr int KW = 32 * S;                       // K values per wave
+    constexpr int D = KW * kDmsStreamWaves;          // d_out
+    __shared__ __attribute__((aligned(16))) char lds[2 * kDmsStreamWaves * kDmsStreamPart];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int r16 = lane & 15, q = lane >> 4;
+    // weight fragments: tile t, step s: row n = 16 t + r16 (W_{n / d_in} row n % d_in, zero
+    // past N), K values KW wave + 8 (S q + s) ..
+    bf16x8 wf[8][S];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        const int n = t * 16 + r16;
+        const int sl = n < p.N ? n / p.d_in : 0;
+        const char *wr = (const char *)p.w[sl] + (int64_t)(n < p.N ? n - sl * p.d_in : 0) * D * 2 +
+                         (wave * KW + q * 8 * S) * 2;
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            u32x4 v = *(const u32x4 *)(wr + s * 16);
+            if (n >= p.N) v = u32x4{0u, 0u, 0u, 0u};
+            wf[t][s] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
+    const int64_t nblocks = (M + 15) / 16;
+    const int64_t P = gridDim.x;
+    const int nmine = blockIdx.x < nblocks ? (int)((nblocks - blockIdx.x + P - 1) / P) : 0;
+    const float *zp = (const float *)g_zero16;
+    // summing role: row rr of the block, columns 4 cq .. + 3 (slot cq 4 / d_in)
+    const int rr = 2 * wave + (lane >> 5), cq = lane & 31;
+    const bool col_ok = cq * 4 < p.N;
+    const int32_t *ipc = col_ok ? p.indptr[cq * 4 / p.d_in] : nullptr;
+    // block bi of this workgroup: rows 16 (blockIdx.x + bi P) ..; the lane's slice of its
+    // row, and indptr[m], indptr[m + 1] of its summing row and slot (the self slot and
+    // rows past M read the zero buffer).  Loads are issued unconditionally (blocks past the
+    // last read the zero buffer), so every path has the same loads in flight.
+    struct Blk {
+        f32x4 v[2 * S];
+        int32_t i0, i1;
+    };
+    auto load = [&](int bi, Blk &b) {
+        const bool live = bi < nmine;
+        const int64_t m0 = ((int64_t)blockIdx.x + (int64_t)(live ? bi : 0) * P) * 16;
+        const int64_t m = m0 + r16;
+        const bool ok = live && m < M;
+        const float *src = ok ? dy + m * D + wave * KW + q * 8 * S : zp;
+        const int st = ok ? 4 : 0;
+#pragma unroll
+        for (int i = 0; i < 2 * S; ++i) b.v[i] = *(const f32x4 *)(src + i * st);
+        const int64_t mr = m0 + rr;
+        const int32_t *d = (live && ipc != nullptr && mr < M) ? ipc + mr : (const int32_t *)zp;
+        b.i0 = d[0];
+        b.i1 = d[1];
+    };
+    Blk bufs[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) load(b, bufs[b]);
+    for (int bi0 = 0; bi0 < nmine; bi0 += NB) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int bi = bi0 + b;
+            if (bi >= nmine) break;
+            f32x4 acc[8];
+#pragma unroll
+            for (int t = 0; t < 8; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < S; ++s) {
+                const f32x4 a = bufs[b].v[2 * s], c = bufs[b].v[2 * s + 1];
+                u32x4 hv, lv;
+                hv.x = pack_bf16x2(a.x, a.y);
+                hv.y = pack_bf16x2(a.z, a.w);
+                hv.z = pack_bf16x2(c.x, c.y);
+                hv.w = pack_bf16x2(c.z, c.w);
+                lv.x = pack_bf16x2(a.x - bf16_lo(hv.x), a.y - bf16_hi(hv.x));
+                lv.y = pack_bf16x2(a.z - bf16_lo(hv.y), a.w - bf16_hi(hv.y));
+                lv.z = pack_bf16x2(c.x - bf16_lo(hv.z), c.y - bf16_hi(hv.z));
+                lv.w = pack_bf16x2(c.z - bf16_lo(hv.w), c.w - bf16_hi(hv.w));
+                const bf16x8 bh = __builtin_bit_cast(bf16x8, hv), bl = __builtin_bit_cast(bf16x8, lv);
+#pragma unroll
+                for (int t = 0; t < 8; ++t) {
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[t][s], bh, acc[t], 0, 0, 0);
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[t][s], bl, acc[t], 0, 0, 0);
+                }
+            }
+            const int32_t i0 = bufs[b].i0, i1 = bufs[b].i1;
+            char *part = lds + (bi & 1) * (kDmsStreamWaves * kDmsStreamPart);
+            char *mine = part + wave * kDmsStreamPart;
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+                *(f32x4 *)(mine + r16 * 512 + (((4 * t + q) ^ (2 * r16)) * 16)) = acc[t];
+            load(bi + NB, bufs[b]);
+            // every wave's partials of this block are in LDS; the buffer written next was
+            // last read before this barrier
+            __syncthreads();
+            f32x4 sum = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int w = 0; w < kDmsStreamWaves; ++w)
+                sum += *(const f32x4 *)(part + w * kDmsStreamPart + rr * 512 + ((cq ^ (2 * rr)) * 16));
+            const int64_t m = ((int64_t)blockIdx.x + (int64_t)bi * P) * 16 + rr;
+            if (col_ok && m < M) {
+                const int32_t deg = i1 - i0;
+                const bool zero = ipc != nullptr && deg == 0;
+                const float scale = ipc != nullptr && deg > 0 ? (float)deg : 1.f;
+                f32x4 r;
+                r.x = zero ? 0.f : sum.x / scale;
+                r.y = zero ? 0.f : sum.y / scale;
+                r.z = zero ? 0.f : sum.z / scale;
+                r.w = zero ? 0.f : sum.w / scale;
+                *(f32x4 *)(p.out + m * p.N + cq * 4) = r;
+            }
+        }
+    }
+}
+
 template <class C, class Mma, class LA, class LB, class Epi, int STAGES, int R>
 hipError_t launch_gemm(const LA &la, const LB &lb, const Epi &epi, int64_t M, int64_t N,
                        int64_t K, int64_t splits, int64_t k_per_split, hipStream_t s) {
@@ -1120,6 +1266,30 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_
     epi.d_in = d_in;
     for (int i = 0; i < kMaxSlots; ++i) epi.indptr[i] = i < slots.count ? slots.indptr[i] : nullptr;
     PlainRows pa{(const char *)dy, (int64_t)d_out * 4, M};
+    if (dt == RGCN_BF16 && N <= kDmsStreamCols && d_in % 16 == 0 &&
+        (d_out == 256 || d_out == 512)) {
+        if (M == 0) return hipSuccess;
+        DmsStream ps{};
+        for (int i = 0; i < kMaxSlots; ++i) {
+            ps.w[i] = sr.w[i];
+            ps.indptr[i] = epi.indptr[i];
+        }
+        ps.out = dms;
+        ps.N = (int32_t)N;
+        ps.d_in = d_in;
+        // one workgroup per CU (128 KB of LDS), no more than there are 16-row blocks
+        int64_t P = cdiv(M, 16);
+        const int64_t cus = device_cus();
+        if (P > cus) P = cus;
+        // register blocks in flight per wave: as many as fit beside the weights
+        if (d_out == 512)
+            hipLaunchKernelGGL((k_dms_stream<2, 5>), dim3((unsigned)P), dim3(kDmsStreamWaves * 64),
+                               0, s, dy, M, ps);
+        else
+            hipLaunchKernelGGL((k_dms_stream<1, 8>), dim3((unsigned)P), dim3(kDmsStreamWaves * 64),
+                               0, s, dy, M, ps);
+        return hipGetLastError();
+    }
     if (dt == RGCN_BF16) {
         // dY enters as hi + lo bf16 tiles from one read of each fp32 row; each weight
         // fragment meets both

@@ -42,6 +42,33 @@ def test_random_block_parity(name, blk, dtype, d_in, d_out):
     run.assert_parity()
 
 
+# Destination types whose input-side product has at most 128 gradient columns (one slot of
+# d_in <= 128, or two to four narrower ones) take, in bf16 with d_out 256 or 512, the
+# streamed kernel that splits K over the waves of a workgroup (other d_out: the
+# register-staged kernel).  Type 0 has a gradient and only its self slot (no degree
+# division); type 1 takes k relation slots from type 0 (divided by the degree, zero-degree
+# rows included).  Row counts cover a few 16-row blocks, a ragged last block, and many
+# blocks per workgroup (past the register prefetch depth); N = 96 leaves 16-column tiles
+# empty.
+@pytest.mark.parametrize("d_in,d_out,n0,n1,k", [(128, 512, 2_500, 2_500, 1),
+                                                (32, 512, 25_001, 25_000, 4),
+                                                (64, 256, 40_000, 3_000, 2),
+                                                (32, 512, 77, 77, 4),
+                                                (96, 256, 2_500, 2_500, 1),
+                                                (128, 64, 66_000, 700, 1),
+                                                (64, 192, 4_133, 4_133, 2),
+                                                (32, 128, 1_000, 1_000, 1)])
+def test_input_side_narrow_slots(d_in, d_out, n0, n1, k):
+    rng = np.random.default_rng(d_in * 7 + d_out + k)
+    rels = [(0, 1)] * k + [(1, 0), (1, 1)]
+    blk = synth.random_block(rng, [n0 + 40, n1 + n1 // 3 + 5], [n0, n1], rels, 6, zero_frac=0.3)
+    print(f"case narrow input side {d_in}->{d_out} rows {n0}, {n1} slots {k}", flush=True)
+    run = BlockRun(blk, "bf16", d_in, d_out, seed=d_out + k, use_ids=True, grad_types=(0,))
+    run.run_gpu()
+    run.run_oracle()
+    run.assert_parity()
+
+
 def _claimed_runs_block():
     # Large enough that the gather's runs outnumber its resident lane groups (runs are then
     # claimed from the shared counter), with forward segments heavy enough to span several
