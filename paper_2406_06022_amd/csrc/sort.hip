@@ -12,44 +12,68 @@ hipError_t scan_gated(const int32_t *in, int32_t *out, int64_t n, void *temp,
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kScanItems = 8;
-constexpr int kScanTile = kThreads * kScanItems;     // 2048
+constexpr int kScanRounds = 4;                        // int4 per thread per round
+constexpr int kScanTile = kThreads * 4 * kScanRounds;  // 4096
 constexpr int kSortItems = 16;
 constexpr int kSortTile = kThreads * kSortItems;     // 4096
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// Exclusive scan of one value per thread over a 256-thread workgroup.
+// Exclusive scan of one value per thread over a 256-thread workgroup: inclusive scans
+// within the waves (shuffles), then the four wave totals through LDS (two barriers).
 __device__ int wg_exclusive_scan(int v, int *total) {
-    __shared__ int buf[kThreads];
-    const int t = threadIdx.x;
-    buf[t] = v;
-    __syncthreads();
-    for (int off = 1; off < kThreads; off <<= 1) {
-        int x = t >= off ? buf[t - off] : 0;
-        __syncthreads();
-        buf[t] += x;
-        __syncthreads();
+    __shared__ int wsum[kThreads / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
     }
-    int incl = buf[t];
-    *total = buf[kThreads - 1];
+    if (lane == 63) wsum[wave] = x;
     __syncthreads();
-    return incl - v;
+    int below = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) {
+        const int t = wsum[w];
+        below += w < wave ? t : 0;
+        all += t;
+    }
+    __syncthreads();   // wsum is rewritten by the next call
+    *total = all;
+    return below + x - v;
 }
 
 // ---------------------------------------------------------------- scan (3 kernels)
 // A gate (NULL = none) is a device word: kernels given one do nothing while it is zero.
+// Tiles of 4096 values: in round u thread t holds values 4 (256 u + t) .. + 3 (one 16-byte
+// access when the arrays are 16-byte aligned, VEC), so every access of a round is
+// contiguous across the workgroup.
 __device__ __forceinline__ bool gated_off(const uint32_t *gate) { return gate && *gate == 0u; }
 
+template <bool VEC>
+__device__ __forceinline__ void scan_load4(const int32_t *in, int64_t i, int64_t n, int v[4]) {
+    if (VEC && i + 4 <= n) {
+        const int4 q = *(const int4 *)(in + i);
+        v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+        return;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = i + e < n ? in[i + e] : 0;
+}
+
+template <bool VEC>
 __global__ __launch_bounds__(kThreads) void k_scan_reduce(const int32_t *in, int64_t n,
                                                           int32_t *partial, const uint32_t *gate) {
     if (gated_off(gate)) return;
     const int64_t base = (int64_t)blockIdx.x * kScanTile;
     int sum = 0;
-    for (int u = 0; u < kScanItems; ++u) {
-        int64_t i = base + (int64_t)u * kThreads + threadIdx.x;
-        if (i < n) sum += in[i];
+#pragma unroll
+    for (int u = 0; u < kScanRounds; ++u) {
+        int v[4];
+        scan_load4<VEC>(in, base + 4 * ((int64_t)u * kThreads + threadIdx.x), n, v);
+        sum += v[0] + v[1] + v[2] + v[3];
     }
     int total;
     wg_exclusive_scan(sum, &total);
@@ -59,19 +83,20 @@ __global__ __launch_bounds__(kThreads) void k_scan_reduce(const int32_t *in, int
 __global__ __launch_bounds__(kThreads) void k_scan_partials(int32_t *partial, int64_t nb,
                                                             const uint32_t *gate) {
     if (gated_off(gate)) return;
+    constexpr int kItems = kScanTile / kThreads;
     int carry = 0;
     for (int64_t c0 = 0; c0 < nb; c0 += kScanTile) {
-        int v[kScanItems];
+        int v[kItems];
         int sum = 0;
-        for (int u = 0; u < kScanItems; ++u) {
-            int64_t i = c0 + (int64_t)threadIdx.x * kScanItems + u;
+        for (int u = 0; u < kItems; ++u) {
+            int64_t i = c0 + (int64_t)threadIdx.x * kItems + u;
             v[u] = i < nb ? partial[i] : 0;
             sum += v[u];
         }
         int total;
         int pre = wg_exclusive_scan(sum, &total) + carry;
-        for (int u = 0; u < kScanItems; ++u) {
-            int64_t i = c0 + (int64_t)threadIdx.x * kScanItems + u;
+        for (int u = 0; u < kItems; ++u) {
+            int64_t i = c0 + (int64_t)threadIdx.x * kItems + u;
             if (i < nb) partial[i] = pre;
             pre += v[u];
         }
@@ -79,24 +104,31 @@ __global__ __launch_bounds__(kThreads) void k_scan_partials(int32_t *partial, in
     }
 }
 
+// partial NULL: a single tile (offset 0).  in may equal out: every value of a round is
+// read before that round's values are written.
+template <bool VEC>
 __global__ __launch_bounds__(kThreads) void k_scan_apply(const int32_t *in, int32_t *out,
                                                          int64_t n, const int32_t *partial,
                                                          const uint32_t *gate) {
     if (gated_off(gate)) return;
-    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
-    int v[kScanItems];
-    int sum = 0;
-    for (int u = 0; u < kScanItems; ++u) {
-        int64_t i = base + u;
-        v[u] = i < n ? in[i] : 0;
-        sum += v[u];
-    }
-    int total;
-    int pre = wg_exclusive_scan(sum, &total) + partial[blockIdx.x];
-    for (int u = 0; u < kScanItems; ++u) {
-        int64_t i = base + u;
-        if (i < n) out[i] = pre;
-        pre += v[u];
+    const int64_t base = (int64_t)blockIdx.x * kScanTile;
+    int carry = partial ? partial[blockIdx.x] : 0;
+#pragma unroll
+    for (int u = 0; u < kScanRounds; ++u) {
+        const int64_t i = base + 4 * ((int64_t)u * kThreads + threadIdx.x);
+        int v[4];
+        scan_load4<VEC>(in, i, n, v);
+        int total;
+        const int pre = wg_exclusive_scan(v[0] + v[1] + v[2] + v[3], &total) + carry;
+        const int o[4] = {pre, pre + v[0], pre + v[0] + v[1], pre + v[0] + v[1] + v[2]};
+        if (VEC && i + 4 <= n) {
+            *(int4 *)(out + i) = make_int4(o[0], o[1], o[2], o[3]);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (i + e < n) out[i + e] = o[e];
+        }
+        carry += total;
     }
 }
 
@@ -222,10 +254,21 @@ struct PutIndex {
 struct BwdKey {
     BwdKeyRels rels;
     // transpose degree of row j summed over the relations leaving the type
+    // (four relations' loads in flight at a time: past the last relation the first one is
+    // read again and not counted, so the loads need no branch)
     __device__ int64_t degree(int64_t j) const {
         int64_t deg = 0;
-        for (int r = 0; r < rels.count; ++r)
-            deg += (int64_t)rels.csc_indptr[r][j + 1] - rels.csc_indptr[r][j];
+        for (int r0 = 0; r0 < rels.count; r0 += 4) {
+            int32_t a[4], b[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int32_t *ip = rels.csc_indptr[r0 + i < rels.count ? r0 + i : 0] + j;
+                a[i] = ip[0];
+                b[i] = ip[1];
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) deg += r0 + i < rels.count ? (int64_t)b[i] - a[i] : 0;
+        }
         return deg;
     }
     __device__ int operator()(int64_t j) const { return degree_key(degree(j)); }
@@ -309,9 +352,15 @@ __global__ __launch_bounds__(kThreads) void k_expand_edges(CscRels a, int64_t to
     }
 }
 
+// p[0, n) = v; 16-byte stores over the grid (p 16-byte aligned), a grid-stride loop
 __global__ __launch_bounds__(kThreads) void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
-    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (i < n) p[i] = v;
+    const int64_t n4 = n / 4;
+    const int4 q = make_int4(v, v, v, v);
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n4; i += stride)
+        ((int4 *)p)[i] = q;
+    const int64_t t = 4 * n4 + (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (t < n) p[t] = v;
 }
 
 // ---------------------------------------------------------------- CSC by placement
@@ -553,14 +602,32 @@ hipError_t scan_gated(const int32_t *in, int32_t *out, int64_t n, void *temp,
                       const uint32_t *gate, hipStream_t s) {
     if (n == 0) return hipSuccess;
     const int64_t nb = cdiv(n, kScanTile);
+    const bool vec = ((uintptr_t)in % 16) == 0 && ((uintptr_t)out % 16) == 0;
+    if (nb == 1) {   // one tile: the apply pass alone
+        if (vec)
+            hipLaunchKernelGGL(k_scan_apply<true>, dim3(1), dim3(kThreads), 0, s, in, out, n,
+                               (const int32_t *)nullptr, gate);
+        else
+            hipLaunchKernelGGL(k_scan_apply<false>, dim3(1), dim3(kThreads), 0, s, in, out, n,
+                               (const int32_t *)nullptr, gate);
+        return hipGetLastError();
+    }
     int32_t *partial = (int32_t *)temp;
-    hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)nb), dim3(kThreads), 0, s, in, n, partial,
-                       gate);
+    if (vec)
+        hipLaunchKernelGGL(k_scan_reduce<true>, dim3((unsigned)nb), dim3(kThreads), 0, s, in, n,
+                           partial, gate);
+    else
+        hipLaunchKernelGGL(k_scan_reduce<false>, dim3((unsigned)nb), dim3(kThreads), 0, s, in, n,
+                           partial, gate);
     RGCN_HIP_TRY(hipGetLastError());
     hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kThreads), 0, s, partial, nb, gate);
     RGCN_HIP_TRY(hipGetLastError());
-    hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)nb), dim3(kThreads), 0, s, in, out, n,
-                       partial, gate);
+    if (vec)
+        hipLaunchKernelGGL(k_scan_apply<true>, dim3((unsigned)nb), dim3(kThreads), 0, s, in, out,
+                           n, (const int32_t *)partial, gate);
+    else
+        hipLaunchKernelGGL(k_scan_apply<false>, dim3((unsigned)nb), dim3(kThreads), 0, s, in, out,
+                           n, (const int32_t *)partial, gate);
     return hipGetLastError();
 }
 
@@ -679,8 +746,12 @@ hipError_t csc_build_all(const CscRels &rels, int64_t total_rows, int64_t nnz,
     int32_t *long_keys = (int32_t *)kb[0];                 // at most nnz / (kSegNet + 1)
 
     // cursors and the two words start at zero
-    hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)cdiv(key_range + 3, kThreads)), dim3(kThreads),
-                       0, s, cur, key_range + 3, 0);
+    {
+        int64_t blocks = cdiv(cdiv(key_range + 3, 4), kThreads);
+        blocks = blocks < 1 ? 1 : (blocks > 2048 ? 2048 : blocks);
+        hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)blocks), dim3(kThreads), 0, s, cur,
+                           key_range + 3, 0);
+    }
     RGCN_HIP_TRY(hipGetLastError());
     if (total_rows > 0 && nnz > 0) {
         hipLaunchKernelGGL(k_expand_edges, dim3((unsigned)cdiv(total_rows, kThreads)),
