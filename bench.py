@@ -166,7 +166,7 @@ def algorithmic_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
     """Bytes one launch of a stage's kernel moves in this implementation's data layout (no
     cache reuse): the method's bytes (survey_bytes) plus what the layout adds -- the
     self-loop rows copied into the K-concatenated operand, an 8-byte id per gathered edge,
-    the fp32 self-loop input-side rows and the ReLU-mask input rows of the backward."""
+    the fp32 self-loop input-side rows and the ReLU sign bits the backward reads."""
     b = 2 if spec.dtype == "bf16" else 4
     d_in = spec.dims[layer]
     T = len(blk.n_src)
@@ -185,10 +185,11 @@ def algorithmic_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
         return tot
     if stage in ("sparse", "sparse_adagrad"):
         # per requested source type: transpose offsets + destination ids + one fp32 input-
-        # side row per edge, the fp32 self-loop row, the ReLU-mask input row above the input
-        # layer (the block input, block dtype), and the fp32 output row (a read-add-write of
-        # the embedding-gradient row at the input layer, else a write); with the fused
-        # Adagrad step the read-add-write is of the fp32 state row and the table row
+        # side row per edge, the fp32 self-loop row, the ReLU mask above the input layer
+        # (the sign bits the producing transform wrote: ceil(d_in / 64) words per row),
+        # and the fp32 output row (a read-add-write of the embedding-gradient row at the
+        # input layer, else a write); with the fused Adagrad step the read-add-write is of
+        # the fp32 state row and the table row
         tot = 0.0
         for s in range(T):
             if not (dev_blk.grad_src_types >> s & 1):
@@ -196,7 +197,7 @@ def algorithmic_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
             ns = blk.n_src[s]
             out = 2 if layer == 0 else 1
             tot += ns * d_in * 4 * out + blk.n_dst[s] * d_in * 4 + (layer == 0) * 8 * ns
-            tot += (layer > 0) * ns * d_in * b
+            tot += (layer > 0) * ns * 8 * ((d_in + 63) // 64)
             if stage == "sparse_adagrad":
                 tot += ns * d_in * b * 2
             for rel in blk.rels:

@@ -103,12 +103,20 @@ typedef struct {
 } rgcn_block;
 
 /* Input rows of one node type: H[j] = base[row_ids[j] * ld + 0 .. d_in) (row_ids NULL:
- * H[j] = base[j * ld ...]).  base has num_rows rows of the block's dtype. */
+ * H[j] = base[j * ld ...]).  base has num_rows rows of the block's dtype.
+ * relu_mask (optional, read only by the backward under RGCN_INPUT_RELU): the signs of
+ * the input as bits, [num_rows x ceil(d_in / 64)] uint64 words, 8-byte aligned, row r's
+ * words at relu_mask + r * ceil(d_in / 64), bit c % 64 of word c / 64 set exactly when
+ * element c of table row r is positive (rows addressed like base).  The forward of the
+ * block that produced the input writes it (rgcn_block_forward's relu_mask); with it the
+ * backward reads 1 bit per element instead of the input row.  NULL: the input rows are
+ * read. */
 typedef struct {
     const void *base;
     const int64_t *row_ids;   /* [n_src[t]] or NULL */
     int64_t num_rows;
     int64_t ld;
+    const uint64_t *relu_mask;   /* or NULL */
 } rgcn_input;
 
 /* Weights of one block in the block's dtype, row-major [d_in x d_out]. */
@@ -180,9 +188,15 @@ rgcn_status rgcn_block_plan(const rgcn_block *block, const rgcn_params *params,
 
 /* Forward: y[t] (device [n_dst[t] x d_out], block dtype, row-major) for every type with
  * n_dst[t] > 0; entries for other types are ignored.  in: [host][num_types].
+ * relu_mask ([host][num_types] or NULL; entries may be NULL): with RGCN_FUSE_RELU,
+ * relu_mask[t] receives the signs of y[t] as bits, [n_dst[t] x ceil(d_out / 64)] uint64
+ * words, 8-byte aligned, bit c % 64 of word c / 64 of row i set exactly when the stored
+ * y[t][i][c] is positive (bits past d_out zero) -- the relu_mask of rgcn_input for the
+ * next block's backward.  A non-NULL entry without RGCN_FUSE_RELU is an error.
  * flags: RGCN_VALIDATE_DEVICE, RGCN_FUSE_RELU.  Requires rgcn_block_plan first. */
 rgcn_status rgcn_block_forward(const rgcn_block *block, const rgcn_input *in,
                                const rgcn_params *params, void *const *y /* [host] */,
+                               uint64_t *const *relu_mask /* [host] or NULL */,
                                void *workspace, size_t workspace_bytes, unsigned flags,
                                hipStream_t stream);
 
@@ -208,13 +222,16 @@ rgcn_status rgcn_block_backward(const rgcn_block *block, const rgcn_input *in,
  *   flags: RGCN_VALIDATE_DEVICE.  Requires rgcn_block_plan first.
  * rgcn_block_transform: the per-destination-type transform
  *   Y_t = [H_t | M_r ...] [W_self_t; W_r ...] (+ b_t) on the matrix cores, reading the
- *   aggregates left by rgcn_block_aggregate.  flags: RGCN_FUSE_RELU. */
+ *   aggregates left by rgcn_block_aggregate; relu_mask as in rgcn_block_forward.
+ *   flags: RGCN_FUSE_RELU. */
 rgcn_status rgcn_block_aggregate(const rgcn_block *block, const rgcn_input *in,
                                  const rgcn_params *params, void *workspace,
                                  size_t workspace_bytes, unsigned flags, hipStream_t stream);
 rgcn_status rgcn_block_transform(const rgcn_block *block, const rgcn_params *params,
-                                 void *const *y /* [host] */, void *workspace,
-                                 size_t workspace_bytes, unsigned flags, hipStream_t stream);
+                                 void *const *y /* [host] */,
+                                 uint64_t *const *relu_mask /* [host] or NULL */,
+                                 void *workspace, size_t workspace_bytes, unsigned flags,
+                                 hipStream_t stream);
 
 /* The two stages of rgcn_block_backward.
  * rgcn_block_backward_dense: weight and bias gradients (dw_rel, dw_self, dbias as in

@@ -26,13 +26,15 @@ class MiniBatchStack:
                  input_ids: Sequence[Optional[torch.Tensor]], weights, dtype: str,
                  dims: Sequence[int], emb_types: Sequence[int] = (), device="cuda",
                  want_weight_grads: bool = True, ids_unique: bool = True,
-                 edge_rows: bool = True):
+                 edge_rows: bool = True, relu_masks: bool = True):
         """blocks: host blocks (blocks[0] nearest the input); input_tables[t] / input_ids[t]:
         layer-0 table and int64 global row ids of each type; weights[l] = (w_rel, w_self,
         bias) device tensors of layer l; emb_types: types whose table is learnable.
         edge_rows: give the first block's per-edge source rows (``rel.src_rows``, the
         sampler's global source ids) to the library when the blocks carry them and every
-        type has row ids, so its gather reads each edge's table row directly."""
+        type has row ids, so its gather reads each edge's table row directly.
+        relu_masks: the transforms followed by a ReLU also write the signs of their output
+        as bits, and the next block's backward reads those instead of the activation rows."""
         self.L = len(blocks)
         self.dtype = dtype
         self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
@@ -58,9 +60,14 @@ class MiniBatchStack:
         # activations: y[l][t] = output of block l, [n_dst x d_{l+1}]
         self.y = [[torch.empty((n, dims[l + 1]), dtype=self.tdtype, device=device) if n > 0 else None
                    for n in b.n_dst] for l, b in enumerate(self.blocks)]
+        # ReLU sign bits of y[l] for l < L - 1 (the inputs of the next block's backward)
+        words = [rgcn.relu_mask_words(dims[l + 1]) for l in range(self.L)]
+        self.y_mask = [[torch.empty((n, words[l]), dtype=torch.int64, device=device)
+                        if n > 0 and relu_masks and l < self.L - 1 else None
+                        for n in b.n_dst] for l, b in enumerate(self.blocks)]
         self.inputs = [rgcn.Inputs(list(input_tables), list(input_ids))]
         for l in range(1, self.L):
-            self.inputs.append(rgcn.Inputs(self.y[l - 1], None))
+            self.inputs.append(rgcn.Inputs(self.y[l - 1], None, self.y_mask[l - 1]))
         # gradients
         f32 = torch.float32
         self.want_weight_grads = want_weight_grads
@@ -109,6 +116,8 @@ class MiniBatchStack:
         optimizer state); the stack cannot step afterwards."""
         self.workspaces = []
         self.y = []
+        self.y_mask = []
+        self.inputs = []
         self.dh = []
         self.dw_rel = self.dw_self = self.dbias = []
         self.demb = []
@@ -139,7 +148,8 @@ class MiniBatchStack:
                 after_first_aggregate()
             _mark(timer, ("transform", l), 0)
             rgcn.rgcn_block_transform(self.blocks[l], self.params[l], self.y[l],
-                                      self.workspaces[l], f & ~rgcn.RGCN_VALIDATE_DEVICE)
+                                      self.workspaces[l], f & ~rgcn.RGCN_VALIDATE_DEVICE,
+                                      relu_mask=self.y_mask[l] if l < self.L - 1 else None)
             _mark(timer, ("transform", l), 1)
         return self.y[-1]
 

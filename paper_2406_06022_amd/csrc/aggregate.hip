@@ -48,6 +48,17 @@ __device__ __forceinline__ const __attribute__((address_space(1))) T *gbl(const 
     return (const __attribute__((address_space(1))) T *)p;
 }
 
+// ReLU mask of the block input at chunk c (columns 4 c .. 4 c + 3) of input row grow, as
+// 1 / 0 per column, from the sign bits the caller passed (bit c' % 64 of word c' / 64 of
+// the row): one 8-byte word read, shared by the 16 chunks it covers.  !ok reads `zero`.
+__device__ __forceinline__ f32x4 relu_bits4(const uint64_t *mask, int64_t ld, int64_t grow, int c,
+                                            bool ok, const char *zero) {
+    const uint64_t w = *gbl(ok ? mask + grow * ld + (c >> 4) : (const uint64_t *)zero);
+    const uint32_t b = (uint32_t)(w >> (4 * (c & 15)));
+    return f32x4{(b & 1u) ? 1.f : 0.f, (b & 2u) ? 1.f : 0.f, (b & 4u) ? 1.f : 0.f,
+                 (b & 8u) ? 1.f : 0.f};
+}
+
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
@@ -495,7 +506,7 @@ __device__ __forceinline__ void tsum_store(const TsumArgs &a, int64_t j, int64_t
 // destination rows of up to G edges at once (flattened relation by relation), then walk
 // the edges broadcasting row addresses, U row loads in flight; the embedding-gradient
 // row and the ReLU mask input are requested before the walk.
-template <bool BF16IN, int CPL, bool OPT>
+template <bool BF16IN, int CPL, bool OPT, bool MASK>
 __device__ __forceinline__ void transpose_sum_body(const TsumArgs &a, int G, int gpw,
                                                    int chunks) {
     constexpr int HES = BF16IN ? 2 : 4;  // element size of the block input (ReLU mask)
@@ -524,7 +535,10 @@ __device__ __forceinline__ void transpose_sum_body(const TsumArgs &a, int G, int
         const float *ob = OPT ? a.opt_state : (a.ids_unique ? a.demb : nullptr);
         old[p] = (ob && okc) ? *(const float4 *)(ob + grow * a.d_in + (int64_t)c * 4)
                              : make_float4(0.f, 0.f, 0.f, 0.f);
-        if ((a.input_relu || OPT) && okc) {
+        if constexpr (MASK) {
+            const f32x4 b = relu_bits4(a.relu_mask, a.mask_ld, grow, c, okc, (const char *)g_zero);
+            hm[p][0] = b[0]; hm[p][1] = b[1]; hm[p][2] = b[2]; hm[p][3] = b[3];
+        } else if ((a.input_relu || OPT) && okc) {
             const char *hp = (const char *)a.in.base + (grow * a.in.ld + (int64_t)c * 4) * HES;
             if constexpr (BF16IN) {
                 const uint2 hv = *(const uint2 *)hp;
@@ -620,7 +634,7 @@ __device__ __forceinline__ void transpose_sum_body(const TsumArgs &a, int G, int
 // rows are too.  Edges past the group width are resolved in place.  Every load is
 // unconditional (unused lanes read a zero word).
 
-template <bool BF16IN, int CPL, bool OPT>
+template <bool BF16IN, int CPL, bool OPT, bool MASK>
 __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, int gpw,
                                                     int chunks) {
     constexpr int HES = BF16IN ? 2 : 4;
@@ -653,6 +667,7 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
         int32_t total, ei, er;
         bool split;     // more than kSplitEdges edges: the piece kernels sum this row
         f32x4 old[CPL], self[CPL], hm[CPL];
+        uint32_t hb[CPL];   // MASK: the 4 sign bits of each chunk (hm unused)
     };
     // stage 1: source row at schedule position q (-1 past the end)
     auto s1 = [&](int64_t q) -> int32_t {
@@ -716,13 +731,20 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
             rw.self[p] = *gbl(ok_self ? (const f32x4 *)(a.self_dms + m.j * a.self_ld + (int64_t)c * 4)
                                       : (const f32x4 *)zero);
             const bool ok_h = okc && (a.input_relu || OPT);
-            const char *hp = ok_h ? (const char *)a.in.base + (m.grow * a.in.ld + (int64_t)c * 4) * HES
-                                  : zero;
-            if constexpr (BF16IN) {
-                const u32x2 hv = *gbl((const u32x2 *)hp);
-                rw.hm[p] = f32x4{bf16_lo(hv.x), bf16_hi(hv.x), bf16_lo(hv.y), bf16_hi(hv.y)};
+            if constexpr (MASK) {
+                const uint64_t w = *gbl(ok_h ? a.relu_mask + m.grow * a.mask_ld + (c >> 4)
+                                             : (const uint64_t *)zero);
+                rw.hb[p] = (uint32_t)(w >> (4 * (c & 15))) & 0xFu;
             } else {
-                rw.hm[p] = *gbl((const f32x4 *)hp);
+                const char *hp = ok_h ? (const char *)a.in.base +
+                                            (m.grow * a.in.ld + (int64_t)c * 4) * HES
+                                      : zero;
+                if constexpr (BF16IN) {
+                    const u32x2 hv = *gbl((const u32x2 *)hp);
+                    rw.hm[p] = f32x4{bf16_lo(hv.x), bf16_hi(hv.x), bf16_lo(hv.y), bf16_hi(hv.y)};
+                } else {
+                    rw.hm[p] = *gbl((const f32x4 *)hp);
+                }
             }
         }
     };
@@ -760,11 +782,15 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
             const int c = lg + p * G;
             if (c >= chunks) continue;
             f32x4 res = acc[p];
-            if (a.input_relu) {
+            if constexpr (MASK) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) res[e] = (rw.hb[p] >> e) & 1u ? res[e] : 0.f;
+            } else if (a.input_relu) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) res[e] = rw.hm[p][e] > 0.f ? res[e] : 0.f;
             }
-            tsum_store<BF16IN, OPT>(a, rw.m.j, rw.m.grow, c, res, rw.old[p], rw.hm[p]);
+            tsum_store<BF16IN, OPT>(a, rw.m.j, rw.m.grow, c, res, rw.old[p],
+                                    MASK ? f32x4{0.f, 0.f, 0.f, 0.f} : rw.hm[p]);
         }
     };
 
@@ -865,7 +891,7 @@ __device__ __forceinline__ void pieces_body(const TsumArgs &a, int G, int gpw, i
 // piece) adds its self term and its pieces' partial sums in piece order, then applies the
 // mask and the stores of the transposed sum (dh_src, the embedding gradient or the Adagrad
 // step).
-template <bool BF16IN, int CPL, bool OPT>
+template <bool BF16IN, int CPL, bool OPT, bool MASK>
 __device__ __forceinline__ void split_finish_body(const TsumArgs &a, int G, int gpw, int chunks) {
     constexpr int HES = BF16IN ? 2 : 4;
     constexpr int U = CPL == 1 ? 8 : 4;
@@ -896,7 +922,9 @@ __device__ __forceinline__ void split_finish_body(const TsumArgs &a, int G, int 
             old[q] = (ob && okc) ? *(const f32x4 *)(ob + grow * a.d_in + (int64_t)c * 4)
                                  : f32x4{0.f, 0.f, 0.f, 0.f};
             hm[q] = f32x4{1.f, 1.f, 1.f, 1.f};
-            if ((a.input_relu || OPT) && okc) {
+            if constexpr (MASK) {
+                hm[q] = relu_bits4(a.relu_mask, a.mask_ld, grow, c, okc, (const char *)g_zero);
+            } else if ((a.input_relu || OPT) && okc) {
                 const char *hp = (const char *)a.in.base + (grow * a.in.ld + (int64_t)c * 4) * HES;
                 if constexpr (BF16IN) {
                     const uint2 hv = *(const uint2 *)hp;
@@ -936,33 +964,33 @@ __global__ __launch_bounds__(kThreads) void k_transpose_pieces(TsumArgs a, int G
                                                                int chunks) {
     pieces_body<CPL>(a, G, gpw, chunks);
 }
-template <bool BF16IN, int CPL, bool OPT>
+template <bool BF16IN, int CPL, bool OPT, bool MASK>
 __global__ __launch_bounds__(kThreads) void k_transpose_split_finish(TsumArgs a, int G, int gpw,
                                                                      int chunks) {
-    split_finish_body<BF16IN, CPL, OPT>(a, G, gpw, chunks);
+    split_finish_body<BF16IN, CPL, OPT, MASK>(a, G, gpw, chunks);
 }
 
 // The transposed sums as kernels; the Adagrad forms carry a name of their own so that
 // traces and counters keep them apart.
-template <bool BF16IN, int CPL>
+template <bool BF16IN, int CPL, bool MASK>
 __global__ __launch_bounds__(kThreads) void k_transpose_sum(TsumArgs a, int G, int gpw,
                                                             int chunks) {
-    transpose_sum_body<BF16IN, CPL, false>(a, G, gpw, chunks);
+    transpose_sum_body<BF16IN, CPL, false, MASK>(a, G, gpw, chunks);
 }
 template <bool BF16IN, int CPL>
 __global__ __launch_bounds__(kThreads) void k_transpose_sum_adagrad(TsumArgs a, int G, int gpw,
                                                                     int chunks) {
-    transpose_sum_body<BF16IN, CPL, true>(a, G, gpw, chunks);
+    transpose_sum_body<BF16IN, CPL, true, false>(a, G, gpw, chunks);
 }
-template <bool BF16IN, int CPL>
+template <bool BF16IN, int CPL, bool MASK>
 __global__ __launch_bounds__(kThreads) void k_transpose_pipe(TsumArgs a, int G, int gpw,
                                                              int chunks) {
-    transpose_pipe_body<BF16IN, CPL, false>(a, G, gpw, chunks);
+    transpose_pipe_body<BF16IN, CPL, false, MASK>(a, G, gpw, chunks);
 }
 template <bool BF16IN, int CPL>
 __global__ __launch_bounds__(kThreads) void k_transpose_pipe_adagrad(TsumArgs a, int G, int gpw,
                                                                      int chunks) {
-    transpose_pipe_body<BF16IN, CPL, true>(a, G, gpw, chunks);
+    transpose_pipe_body<BF16IN, CPL, true, false>(a, G, gpw, chunks);
 }
 
 // WcatT[n][s*d_in + c] = W_s[c][n]: the forward transform's weights, K-contiguous.
@@ -1139,12 +1167,12 @@ hipError_t gather_mean(rgcn_dtype dt, int d_in, const SegDesc *desc, int64_t n_s
                                      chunks, claims, s);
 }
 
-template <bool B, int C, bool O>
+template <bool B, int C, bool O, bool K>
 hipError_t launch_transpose_pipe(const TsumArgs &a, const GroupShape &gs, int chunks,
                                  hipStream_t s) {
     const int64_t groups_per_wg = (int64_t)(kThreads / 64) * gs.gpw;
     int64_t wgs = cdiv(a.n_rows, groups_per_wg);
-    auto kern = O ? k_transpose_pipe_adagrad<B, C> : k_transpose_pipe<B, C>;
+    auto kern = O ? k_transpose_pipe_adagrad<B, C> : k_transpose_pipe<B, C, K>;
     const int64_t cap = resident_wgs(kern);
     if (wgs > cap) wgs = cap;
     hipLaunchKernelGGL(kern, dim3((unsigned)wgs), dim3(kThreads), 0, s, a,
@@ -1154,14 +1182,14 @@ hipError_t launch_transpose_pipe(const TsumArgs &a, const GroupShape &gs, int ch
 
 // The piece and finishing kernels of split rows: persistent grids that read the piece
 // count on the device (no piece: every group exits at once).
-template <bool B, int C, bool O>
+template <bool B, int C, bool O, bool K>
 hipError_t launch_split(const TsumArgs &a, const GroupShape &gs, int chunks, bool finish,
                         hipStream_t s) {
     if (a.piece_cap <= 0 || !a.pieces) return hipSuccess;
     const int64_t groups_per_wg = (int64_t)(kThreads / 64) * gs.gpw;
     int64_t wgs = cdiv(a.piece_cap, groups_per_wg);
     if (finish) {
-        auto kern = k_transpose_split_finish<B, C, O>;
+        auto kern = k_transpose_split_finish<B, C, O, K>;
         const int64_t cap = resident_wgs(kern);
         hipLaunchKernelGGL(kern, dim3((unsigned)(wgs < cap ? wgs : cap)), dim3(kThreads), 0, s,
                            a, gs.G, gs.gpw, chunks);
@@ -1174,44 +1202,51 @@ hipError_t launch_split(const TsumArgs &a, const GroupShape &gs, int chunks, boo
     return hipGetLastError();
 }
 
-template <bool B, int C, bool O>
+template <bool B, int C, bool O, bool K>
 hipError_t launch_transpose_rows(const TsumArgs &a, const GroupShape &gs, int chunks,
                                  hipStream_t s) {
-    if (a.nrel <= gs.G) return launch_transpose_pipe<B, C, O>(a, gs, chunks, s);
+    if (a.nrel <= gs.G) return launch_transpose_pipe<B, C, O, K>(a, gs, chunks, s);
     const int64_t waves = cdiv(a.n_rows, gs.gpw);
     const dim3 grid((unsigned)cdiv(waves, kThreads / 64));
-    auto kern = O ? k_transpose_sum_adagrad<B, C> : k_transpose_sum<B, C>;
+    auto kern = O ? k_transpose_sum_adagrad<B, C> : k_transpose_sum<B, C, K>;
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, a, gs.G, gs.gpw,
                        chunks);
     return hipGetLastError();
 }
 
-template <bool B, int C, bool O>
+template <bool B, int C, bool O, bool K>
 hipError_t launch_transpose(const TsumArgs &a, const GroupShape &gs, int chunks, hipStream_t s) {
     // split rows: pieces first, then every other row, then the split rows' reductions
-    RGCN_HIP_TRY((launch_split<B, C, O>(a, gs, chunks, false, s)));
-    RGCN_HIP_TRY((launch_transpose_rows<B, C, O>(a, gs, chunks, s)));
-    return launch_split<B, C, O>(a, gs, chunks, true, s);
+    RGCN_HIP_TRY((launch_split<B, C, O, K>(a, gs, chunks, false, s)));
+    RGCN_HIP_TRY((launch_transpose_rows<B, C, O, K>(a, gs, chunks, s)));
+    return launch_split<B, C, O, K>(a, gs, chunks, true, s);
 }
 
-template <bool B, bool O>
+template <bool B, bool O, bool K>
 hipError_t launch_transpose_cpl(const TsumArgs &a, const GroupShape &gs, int chunks,
                                 hipStream_t s) {
-    if (gs.cpl == 1) return launch_transpose<B, 1, O>(a, gs, chunks, s);
-    if (gs.cpl == 2) return launch_transpose<B, 2, O>(a, gs, chunks, s);
-    if (gs.cpl <= 4) return launch_transpose<B, 4, O>(a, gs, chunks, s);
+    if (gs.cpl == 1) return launch_transpose<B, 1, O, K>(a, gs, chunks, s);
+    if (gs.cpl == 2) return launch_transpose<B, 2, O, K>(a, gs, chunks, s);
+    if (gs.cpl <= 4) return launch_transpose<B, 4, O, K>(a, gs, chunks, s);
     return hipErrorInvalidValue;
+}
+
+// kernel forms: the block dtype (B), Adagrad (O), the input's ReLU signs read as bits (K;
+// never with O: a learnable table is not a ReLU output)
+template <bool B>
+hipError_t transpose_sum_dt(const TsumArgs &a, const GroupShape &gs, int chunks, hipStream_t s) {
+    if (a.opt_state != nullptr) return launch_transpose_cpl<B, true, false>(a, gs, chunks, s);
+    if (a.input_relu && a.relu_mask != nullptr)
+        return launch_transpose_cpl<B, false, true>(a, gs, chunks, s);
+    return launch_transpose_cpl<B, false, false>(a, gs, chunks, s);
 }
 
 hipError_t transpose_sum(rgcn_dtype dt, const TsumArgs &a, hipStream_t s) {
     if (a.n_rows == 0) return hipSuccess;
     const int chunks = a.d_in / 4;
     const GroupShape gs = group_shape(chunks);
-    const bool bf = dt == RGCN_BF16, opt = a.opt_state != nullptr;
-    if (bf) return opt ? launch_transpose_cpl<true, true>(a, gs, chunks, s)
-                       : launch_transpose_cpl<true, false>(a, gs, chunks, s);
-    return opt ? launch_transpose_cpl<false, true>(a, gs, chunks, s)
-               : launch_transpose_cpl<false, false>(a, gs, chunks, s);
+    return dt == RGCN_BF16 ? transpose_sum_dt<true>(a, gs, chunks, s)
+                           : transpose_sum_dt<false>(a, gs, chunks, s);
 }
 
 hipError_t pack_weights(rgcn_dtype dt, int d_in, int d_out, const void *const *w_slots,

@@ -537,17 +537,32 @@ rgcn_status rgcn_block_aggregate(const rgcn_block *block, const rgcn_input *in,
     return RGCN_OK;
 }
 
+// The forward outputs: y[t] for every type with rows, and the optional sign masks (only
+// with RGCN_FUSE_RELU, 8-byte aligned).
+static rgcn_status check_forward_outputs(const rgcn_block *block, int T, void *const *y,
+                                         uint64_t *const *relu_mask, unsigned flags) {
+    if (!y) return fail(RGCN_ERR_INVALID_ARG, "y is NULL");
+    for (int t = 0; t < T; ++t) {
+        if (block->n_dst[t] > 0 && (!y[t] || !aligned16(y[t])))
+            return fail(RGCN_ERR_INVALID_ARG, "y[%d] NULL or not 16-byte aligned", t);
+        if (relu_mask && relu_mask[t]) {
+            if (!(flags & RGCN_FUSE_RELU))
+                return fail(RGCN_ERR_INVALID_ARG, "relu_mask[%d] given without RGCN_FUSE_RELU", t);
+            if ((uintptr_t)relu_mask[t] % 8)
+                return fail(RGCN_ERR_INVALID_ARG, "relu_mask[%d] not 8-byte aligned", t);
+        }
+    }
+    return RGCN_OK;
+}
+
 rgcn_status rgcn_block_transform(const rgcn_block *block, const rgcn_params *params,
-                                 void *const *y, void *workspace, size_t workspace_bytes,
-                                 unsigned flags, hipStream_t stream) {
+                                 void *const *y, uint64_t *const *relu_mask, void *workspace,
+                                 size_t workspace_bytes, unsigned flags, hipStream_t stream) {
     Layout L;
     rgcn_status st = make_layout(block, params, L);
     if (st != RGCN_OK) return st;
     if ((st = check_workspace(L, workspace, workspace_bytes)) != RGCN_OK) return st;
-    if (!y) return fail(RGCN_ERR_INVALID_ARG, "y is NULL");
-    for (int t = 0; t < L.T; ++t)
-        if (block->n_dst[t] > 0 && (!y[t] || !aligned16(y[t])))
-            return fail(RGCN_ERR_INVALID_ARG, "y[%d] NULL or not 16-byte aligned", t);
+    if ((st = check_forward_outputs(block, L.T, y, relu_mask, flags)) != RGCN_OK) return st;
     char *ws = (char *)workspace;
     for (int t = 0; t < L.T; ++t) {
         if (block->n_dst[t] == 0) continue;
@@ -561,24 +576,26 @@ rgcn_status rgcn_block_transform(const rgcn_block *block, const rgcn_params *par
         const void *bias = params->bias ? params->bias[t] : nullptr;
         TRY_HIP(gemm_forward(L.dt, ws + L.off_mcat[t], block->n_dst[t], L.d_out, (int)L.K[t],
                              ws + L.off_wcat[t], bias, (flags & RGCN_FUSE_RELU) ? 1 : 0, y[t],
-                             stream), "forward transform");
+                             relu_mask ? relu_mask[t] : nullptr, stream),
+                "forward transform");
     }
     return RGCN_OK;
 }
 
 rgcn_status rgcn_block_forward(const rgcn_block *block, const rgcn_input *in,
-                               const rgcn_params *params, void *const *y, void *workspace,
+                               const rgcn_params *params, void *const *y,
+                               uint64_t *const *relu_mask, void *workspace,
                                size_t workspace_bytes, unsigned flags, hipStream_t stream) {
     // check everything the second stage needs before enqueueing the first
     if (!y) return fail(RGCN_ERR_INVALID_ARG, "y is NULL");
-    if (block && block->n_dst && block->num_types > 0 && block->num_types <= kMaxTypes)
-        for (int t = 0; t < block->num_types; ++t)
-            if (block->n_dst[t] > 0 && (!y[t] || !aligned16(y[t])))
-                return fail(RGCN_ERR_INVALID_ARG, "y[%d] NULL or not 16-byte aligned", t);
+    if (block && block->n_dst && block->num_types > 0 && block->num_types <= kMaxTypes) {
+        rgcn_status st = check_forward_outputs(block, block->num_types, y, relu_mask, flags);
+        if (st != RGCN_OK) return st;
+    }
     rgcn_status st = rgcn_block_aggregate(block, in, params, workspace, workspace_bytes, flags,
                                           stream);
     if (st != RGCN_OK) return st;
-    return rgcn_block_transform(block, params, y, workspace, workspace_bytes,
+    return rgcn_block_transform(block, params, y, relu_mask, workspace, workspace_bytes,
                                 flags & ~RGCN_VALIDATE_DEVICE, stream);
 }
 
@@ -605,6 +622,8 @@ static rgcn_status check_sparse_outputs(const rgcn_block *block, const rgcn_inpu
         if (want && block->n_src[t] > 0 && (!in || !in[t].base ||
                                             ((flags & RGCN_INPUT_RELU) && !aligned16(in[t].base))))
             return fail(RGCN_ERR_INVALID_ARG, "input %d needed for its gradient", t);
+        if (want && in && in[t].relu_mask && (uintptr_t)in[t].relu_mask % 8)
+            return fail(RGCN_ERR_INVALID_ARG, "input %d: relu_mask not 8-byte aligned", t);
     }
     return RGCN_OK;
 }
@@ -739,6 +758,10 @@ rgcn_status backward_sparse(const rgcn_block *block, const rgcn_input *in,
         }
         a.in = TypeInput{in[s].base, in[s].row_ids, in[s].ld};
         a.input_relu = (flags & RGCN_INPUT_RELU) ? 1 : 0;
+        if (a.input_relu && in[s].relu_mask) {   // the input's signs as bits
+            a.relu_mask = in[s].relu_mask;
+            a.mask_ld = (L.d_in + 63) / 64;
+        }
         a.ids_unique = (flags & RGCN_IDS_UNIQUE) ? 1 : 0;
         a.dh = dh;
         a.demb = de;

@@ -205,6 +205,8 @@ struct TsumArgs {
     const float *self_dms;   // dY_s W_self_s^T rows (NULL if n_dst == 0)
     int64_t self_ld;
     TypeInput in;            // block input of type s (for the ReLU mask and row ids)
+    const uint64_t *relu_mask;   // the input's sign bits, [num_rows x mask_ld], or NULL
+    int64_t mask_ld;
     int32_t input_relu;
     int32_t ids_unique;
     float *dh;               // [n_src x d_in] or NULL
@@ -318,9 +320,10 @@ hipError_t validate_src_rows(const int32_t *indices, const int64_t *rows, int64_
 
 // gemm.hip
 // Forward: Y = A W + bias (opt. ReLU); A [M x K] row-major (ld K), wcat_t [N x K].
+// mask (or NULL): the positive bits of the stored Y, [M x ceil(N / 64)] words.
 hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
                         const void *wcat_t, const void *bias, int relu, void *y,
-                        hipStream_t s);
+                        uint64_t *mask, hipStream_t s);
 // Backward input side: C[m][n] = (sum_k dy[m][k] W_slot(n)[c(n)][k]) / deg_slot(n)(m);
 // slot(n) = n / d_in, c(n) = n % d_in; indptr[slot] NULL: no scaling (self-loop slot).
 struct DmsSlots {

@@ -321,16 +321,33 @@ struct LoadTransF32 {
 
 // ------------------------------------------------------------------ epilogues
 // Each call gets 16 consecutive columns of one row.
+// ReLU sign words: bit c % 64 of word c / 64 of row m is set when the stored value (m, c)
+// is positive.  A lane hands in the bits of its own columns, already shifted to their place
+// in the 64-column word of its wave; the lanes that share a row OR theirs together (xor
+// shuffles over `span` lanes at stride `step`) and the first of them stores the word.
+struct ReluMask {
+    uint64_t *w;         // [M x ld] or NULL
+    int64_t ld;
+    __device__ __forceinline__ void put(int64_t m, int64_t M, int64_t col0, int64_t N,
+                                        uint64_t bits, int step, int span, bool first) const {
+        for (int o = step; o < step * span; o <<= 1) bits |= (uint64_t)shfl64((int64_t)bits, (int)(__lane_id() ^ o));
+        if (first && m < M && col0 < N) w[m * ld + col0 / 64] = bits;
+    }
+};
+
 template <bool OUT_BF16>
 struct EpiForward {
     static constexpr bool kPrefetch = false;
+    static constexpr bool kMask = true;
     void *y;
     const void *bias;    // block dtype, [N] or NULL
     int64_t M;
     int32_t N;
     int32_t relu;
-    __device__ __forceinline__ void operator()(int64_t m, int64_t n0, const float *v, int64_t) const {
-        if (m >= M) return;
+    ReluMask mask;
+    // returns the positive bits of the 16 columns n0 .. n0 + 15 (bit k: column n0 + k)
+    __device__ __forceinline__ uint32_t operator()(int64_t m, int64_t n0, const float *v, int64_t) const {
+        if (m >= M) return 0u;
         // N is a multiple of 4: each group of 4 columns is either whole or absent.  The
         // bias loads are issued together (clamped, then zeroed) before any is used; with no
         // bias (a uniform test) nothing is loaded.
@@ -355,10 +372,11 @@ struct EpiForward {
                 }
             }
         }
+        uint32_t bits = 0u;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int64_t n = n0 + 4 * q;
-            if (n >= N) return;
+            if (n >= N) break;
             float r[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -370,10 +388,16 @@ struct EpiForward {
                 w.x = pack_bf16x2(r[0], r[1]);
                 w.y = pack_bf16x2(r[2], r[3]);
                 *(uint2 *)((uint16_t *)y + m * N + n) = w;
+                bits |= (uint32_t)(((w.x & 0xffffu) != 0u) | (((w.x >> 16) != 0u) << 1) |
+                                   (((w.y & 0xffffu) != 0u) << 2) | (((w.y >> 16) != 0u) << 3))
+                        << (4 * q);
             } else {
                 *(float4 *)((float *)y + m * N + n) = make_float4(r[0], r[1], r[2], r[3]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) bits |= (uint32_t)(r[e] > 0.f) << (4 * q + e);
             }
         }
+        return bits;
     }
 };
 
@@ -385,6 +409,7 @@ struct EpiForwardBf16 {
     int64_t M;
     int32_t N;
     int32_t relu;
+    ReluMask mask;
     // 4 columns from n (N is a multiple of 4: whole or absent)
     __device__ __forceinline__ void load_bias4(int64_t n, float *bq) const {
         bq[0] = bq[1] = bq[2] = bq[3] = 0.f;
@@ -395,17 +420,20 @@ struct EpiForwardBf16 {
         bq[2] = bf16_lo(w.y);
         bq[3] = bf16_hi(w.y);
     }
-    __device__ __forceinline__ void store4(int64_t m, int64_t n, const f32x4 v,
-                                           const float *bq) const {
-        if (m >= M || n >= N) return;
+    // returns the positive bits of the 4 stored values (bit e: column n + e)
+    __device__ __forceinline__ uint32_t store4(int64_t m, int64_t n, const f32x4 v,
+                                               const float *bq) const {
+        if (m >= M || n >= N) return 0u;
         float r[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             r[e] = v[e] + bq[e];
             if (relu) r[e] = r[e] > 0.f ? r[e] : 0.f;
         }
-        *(uint2 *)((uint16_t *)y + m * N + n) = make_uint2(pack_bf16x2(r[0], r[1]),
-                                                            pack_bf16x2(r[2], r[3]));
+        const uint32_t lo = pack_bf16x2(r[0], r[1]), hi = pack_bf16x2(r[2], r[3]);
+        *(uint2 *)((uint16_t *)y + m * N + n) = make_uint2(lo, hi);
+        return (uint32_t)((lo & 0xffffu) != 0u) | ((uint32_t)((lo >> 16) != 0u) << 1) |
+               ((uint32_t)((hi & 0xffffu) != 0u) << 2) | ((uint32_t)((hi >> 16) != 0u) << 3);
     }
 };
 
@@ -413,6 +441,7 @@ struct EpiForwardBf16 {
 // before the K loop (deg_of), so the epilogue waits for no load (store).
 struct EpiDms {
     static constexpr bool kPrefetch = true;
+    static constexpr bool kMask = false;
     float *out;
     int64_t M;
     int32_t N;
@@ -448,6 +477,7 @@ struct EpiDms {
 
 struct EpiPartial {
     static constexpr bool kPrefetch = false;
+    static constexpr bool kMask = false;
     float *out;          // [splits][M][N]
     int64_t M;
     int32_t N;
@@ -568,10 +598,17 @@ __global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const 
             vals[e] = x.x; vals[e + 1] = x.y; vals[e + 2] = x.z; vals[e + 3] = x.w;
         }
         __builtin_amdgcn_wave_barrier();
-        if constexpr (Epi::kPrefetch)
+        if constexpr (Epi::kPrefetch) {
             epi.store(row + er, n0 + wn * FN * 16 + ec, vals, pdeg[slice]);
-        else
+        } else if constexpr (Epi::kMask) {
+            // the 4 lanes of a row hold its 64 columns, 16 each
+            const uint32_t bits = epi(row + er, n0 + wn * FN * 16 + ec, vals, split);
+            if (epi.mask.w != nullptr)
+                epi.mask.put(row + er, epi.M, n0 + wn * FN * 16, epi.N, (uint64_t)bits << ec, 1,
+                             4, (lane & 3) == 0);
+        } else {
             epi(row + er, n0 + wn * FN * 16 + ec, vals, split);
+        }
     };
     if constexpr (AV == 4) {
         const int rq = lane >> 4, cc = lane & 15;
@@ -757,7 +794,13 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
         }
         if (kk == nk - 1) {
             // lane: row m0 + wm FM 16 + 16 mi + (lane % 16), columns n0 + wn FN 16 + 16 ni +
-            // 4 (lane / 16) .. + 3
+            // 4 (lane / 16) .. + 3; the wave's 64 columns are one word of the sign mask, of
+            // which the lane holds bits 16 ni + 4 (lane / 16) + e, kept packed as bits
+            // 16 (mi % 2) + 4 ni + e of word mi / 2 while the results are stored
+            static_assert(FM % 2 == 0 && FN == 4, "packed sign bits");
+            uint32_t pk[FM / 2];
+#pragma unroll
+            for (int i = 0; i < FM / 2; ++i) pk[i] = 0u;
 #pragma unroll
             for (int ni = 0; ni < FN; ++ni) {
                 const int64_t n = n0 + wn * FN * 16 + ni * 16 + 4 * q;
@@ -765,7 +808,20 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
                 epi.load_bias4(n, bq);
 #pragma unroll
                 for (int mi = 0; mi < FM; ++mi)
-                    epi.store4(m0 + wm * FM * 16 + mi * 16 + r16, n, acc[mi][ni], bq);
+                    pk[mi / 2] |= epi.store4(m0 + wm * FM * 16 + mi * 16 + r16, n, acc[mi][ni], bq)
+                                  << (16 * (mi % 2) + 4 * ni);
+            }
+            if (epi.mask.w != nullptr) {
+#pragma unroll
+                for (int mi = 0; mi < FM; ++mi) {
+                    const uint32_t c16 = pk[mi / 2] >> (16 * (mi % 2));
+                    uint64_t bits = 0u;
+#pragma unroll
+                    for (int ni = 0; ni < FN; ++ni)
+                        bits |= (uint64_t)((c16 >> (4 * ni)) & 0xFu) << (16 * ni + 4 * q);
+                    epi.mask.put(m0 + wm * FM * 16 + mi * 16 + r16, epi.M, n0 + wn * FN * 16,
+                                 epi.N, bits, 16, 4, q == 0);
+                }
             }
         }
         if (++kk == nk) {
@@ -1225,7 +1281,8 @@ constexpr int kDmsRegStages = 1;
 
 hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
                         const void *wcat_t, const void *bias, int relu, void *y,
-                        hipStream_t s) {
+                        uint64_t *mask, hipStream_t s) {
+    const ReluMask rm{mask, (int64_t)(N + 63) / 64};
     if (dt == RGCN_BF16) {
         using C = CfgFwd;
         const int64_t tiles_m = cdiv(M, C::TM), tiles_n = cdiv(N, C::TN);
@@ -1238,7 +1295,7 @@ hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
         hipLaunchKernelGGL((k_gemm_fwd<C, kFwdBK, kFwdStages>), dim3((unsigned)P),
                            dim3(C::NT), 0, s, (const char *)a, (int64_t)K * 2, M,
                            (const char *)wcat_t, (int64_t)K * 2, (int64_t)N, (int64_t)K,
-                           EpiForwardBf16{y, bias, M, N, relu}, tiles_m, tiles_n);
+                           EpiForwardBf16{y, bias, M, N, relu, rm}, tiles_m, tiles_n);
         return hipGetLastError();
     }
     using C = CfgF32;
@@ -1247,7 +1304,7 @@ hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
     LoadRows<TL, C::NT, PlainRows> lb{PlainRows{(const char *)wcat_t, (int64_t)K * 4, N},
                                       (int64_t)K * 4};
     return launch_gemm<C, MmaF32<C::FM, C::FN>, decltype(la), decltype(lb), EpiForward<false>, 2, 2>(
-        la, lb, EpiForward<false>{y, bias, M, N, relu}, M, N, K, 1, K, s);
+        la, lb, EpiForward<false>{y, bias, M, N, relu, rm}, M, N, K, 1, K, s);
 }
 
 hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_in,

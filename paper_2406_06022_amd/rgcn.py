@@ -67,7 +67,8 @@ class _Block(ctypes.Structure):
 
 class _Input(ctypes.Structure):
     _fields_ = [("base", ctypes.c_void_p), ("row_ids", ctypes.c_void_p),
-                ("num_rows", ctypes.c_int64), ("ld", ctypes.c_int64)]
+                ("num_rows", ctypes.c_int64), ("ld", ctypes.c_int64),
+                ("relu_mask", ctypes.c_void_p)]
 
 
 class _Params(ctypes.Structure):
@@ -132,14 +133,16 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.rgcn_block_plan_layout.restype = st
         lib.rgcn_block_plan.argtypes = [vp, vp, vp, ctypes.c_size_t, ctypes.c_uint, vp]
         lib.rgcn_block_plan.restype = st
-        lib.rgcn_block_forward.argtypes = [vp, vp, vp, vp, vp, ctypes.c_size_t, ctypes.c_uint, vp]
+        lib.rgcn_block_forward.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_size_t, ctypes.c_uint,
+                                           vp]
         lib.rgcn_block_forward.restype = st
         lib.rgcn_block_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                             ctypes.c_size_t, ctypes.c_uint, vp]
         lib.rgcn_block_backward.restype = st
         lib.rgcn_block_aggregate.argtypes = [vp, vp, vp, vp, ctypes.c_size_t, ctypes.c_uint, vp]
         lib.rgcn_block_aggregate.restype = st
-        lib.rgcn_block_transform.argtypes = [vp, vp, vp, vp, ctypes.c_size_t, ctypes.c_uint, vp]
+        lib.rgcn_block_transform.argtypes = [vp, vp, vp, vp, vp, ctypes.c_size_t, ctypes.c_uint,
+                                             vp]
         lib.rgcn_block_transform.restype = st
         lib.rgcn_block_backward_dense.argtypes = [vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t,
                                                   ctypes.c_uint, vp]
@@ -315,18 +318,24 @@ class Params:
 
 
 class Inputs:
-    """Per-type input rows: (base table, optional int64 row ids) with base [rows x ld]."""
+    """Per-type input rows: (base table, optional int64 row ids) with base [rows x ld], and
+    optionally the tables' ReLU sign bits (uint64 / int64 [rows x ceil(d / 64)], as
+    rgcn_block_forward writes them)."""
 
     def __init__(self, bases: Sequence[Optional[torch.Tensor]],
-                 row_ids: Optional[Sequence[Optional[torch.Tensor]]] = None):
+                 row_ids: Optional[Sequence[Optional[torch.Tensor]]] = None,
+                 relu_masks: Optional[Sequence[Optional[torch.Tensor]]] = None):
         self.bases = list(bases)
         self.row_ids = list(row_ids) if row_ids is not None else [None] * len(self.bases)
+        self.relu_masks = (list(relu_masks) if relu_masks is not None
+                           else [None] * len(self.bases))
         self.c = (_Input * max(len(self.bases), 1))()
-        for t, (b, ids) in enumerate(zip(self.bases, self.row_ids)):
+        for t, (b, ids, mk) in enumerate(zip(self.bases, self.row_ids, self.relu_masks)):
             if b is None:
-                self.c[t] = _Input(None, None, 0, 0)
+                self.c[t] = _Input(None, None, 0, 0, None)
             else:
-                self.c[t] = _Input(b.data_ptr(), _ptr(ids), int(b.shape[0]), int(b.stride(0)))
+                self.c[t] = _Input(b.data_ptr(), _ptr(ids), int(b.shape[0]), int(b.stride(0)),
+                                   _ptr(mk))
 
 
 # ------------------------------------------------------------------------------------
@@ -368,12 +377,19 @@ def rgcn_block_plan(block: DeviceBlock, params: Params, workspace: torch.Tensor,
                                           _stream(stream)))
 
 
+def relu_mask_words(d: int) -> int:
+    """uint64 words per row of a ReLU sign mask of width d."""
+    return (d + 63) // 64
+
+
 def rgcn_block_forward(block: DeviceBlock, inputs: Inputs, params: Params,
                        y: Sequence[Optional[torch.Tensor]], workspace: torch.Tensor,
-                       flags: int = 0, stream=None) -> None:
+                       flags: int = 0, stream=None,
+                       relu_mask: Optional[Sequence[Optional[torch.Tensor]]] = None) -> None:
     ys = _ptr_array([_ptr(t) for t in y])
+    ms = None if relu_mask is None else _ptr_array([_ptr(t) for t in relu_mask])
     _check(load_library().rgcn_block_forward(ctypes.byref(block.c), inputs.c,
-                                             ctypes.byref(params.c), ys, workspace.data_ptr(),
+                                             ctypes.byref(params.c), ys, ms, workspace.data_ptr(),
                                              workspace.numel(), flags, _stream(stream)))
 
 
@@ -402,10 +418,12 @@ def rgcn_block_aggregate(block: DeviceBlock, inputs: Inputs, params: Params,
 
 
 def rgcn_block_transform(block: DeviceBlock, params: Params, y: Sequence[Optional[torch.Tensor]],
-                         workspace: torch.Tensor, flags: int = 0, stream=None) -> None:
+                         workspace: torch.Tensor, flags: int = 0, stream=None,
+                         relu_mask: Optional[Sequence[Optional[torch.Tensor]]] = None) -> None:
     ys = _ptr_array([_ptr(t) for t in y])
+    ms = None if relu_mask is None else _ptr_array([_ptr(t) for t in relu_mask])
     _check(load_library().rgcn_block_transform(ctypes.byref(block.c), ctypes.byref(params.c), ys,
-                                               workspace.data_ptr(), workspace.numel(), flags,
+                                               ms, workspace.data_ptr(), workspace.numel(), flags,
                                                _stream(stream)))
 
 

@@ -33,6 +33,18 @@ def rel_err(got, want) -> float:
     return float(np.max(np.abs(got - want) / den))
 
 
+def sign_words(t: torch.Tensor) -> torch.Tensor:
+    """ReLU sign bits of a [rows x d] table as the library lays them out: int64 words
+    [rows x ceil(d / 64)], bit c % 64 of word c / 64 set where element c is positive."""
+    pos = (t.detach().to("cpu").to(torch.float32) > 0).numpy().astype(np.uint8)
+    rows, d = pos.shape
+    w = (d + 63) // 64
+    pad = np.zeros((rows, w * 64), dtype=np.uint8)
+    pad[:, :d] = pos
+    by = np.packbits(pad.reshape(rows, w, 64), axis=2, bitorder="little")
+    return torch.from_numpy(np.ascontiguousarray(by).view("<u8").reshape(rows, w).view(np.int64))
+
+
 def gather_rows(table64: np.ndarray, ids) -> np.ndarray:
     """Input rows H[j] = table[ids[j]] (the oracle's first step at the input layer)."""
     if ids is None:
@@ -47,7 +59,7 @@ class BlockRun:
                  grad_types=None, use_ids: bool = False, bias: bool = False,
                  input_relu: bool = False, fwd_relu: bool = False, emb_types=(),
                  ids_unique: bool = True, dup_ids: bool = False, device="cuda",
-                 edge_rows: bool = False):
+                 edge_rows: bool = False, mask_in: bool = False, mask_out: bool = False):
         self.blk, self.dtype, self.d_in, self.d_out = blk, dtype, d_in, d_out
         T, R = len(blk.n_src), len(blk.rels)
         tdt = synth.torch_dtype(dtype)
@@ -85,6 +97,9 @@ class BlockRun:
         self.device = device
         # give the library each edge's table row (ids[src][indices]) as a sampler would
         self.edge_rows = edge_rows
+        # mask_in: the backward reads the input's ReLU signs as bits (from the tables);
+        # mask_out: the forward also writes the signs of y (with fwd_relu)
+        self.mask_in, self.mask_out = mask_in, mask_out
 
     # ------------------------------------------------------------------ GPU
     def device_setup(self):
@@ -110,7 +125,8 @@ class BlockRun:
                                   d_b if any(x is not None for x in d_b) else None)
         self.d_tables = [t.to(dev) for t in self.tables]
         self.d_ids = [i.to(dev) if i is not None else None for i in self.ids]
-        self.inputs = rgcn.Inputs(self.d_tables, self.d_ids)
+        masks = [sign_words(t).to(dev) for t in self.tables] if self.mask_in else None
+        self.inputs = rgcn.Inputs(self.d_tables, self.d_ids, masks)
         self.ws = rgcn.new_workspace(self.dblk, self.params, dev)
         # every byte the library reads before writing would show up as NaN (0xFF bytes are
         # NaN in fp32 and bf16)
@@ -139,9 +155,14 @@ class BlockRun:
                   if t in self.grad_types else None for t in range(T)]
             demb = [torch.zeros((self.tables[t].shape[0], self.d_in), dtype=f32, device=dev)
                     if t in self.emb_types else None for t in range(T)]
+            # sign words start as all ones (0xFF bytes): every word must be written
+            ym = ([torch.full((n, rgcn.relu_mask_words(self.d_out)), -1, dtype=torch.int64,
+                              device=dev) if n > 0 else None for n in blk.n_dst]
+                  if self.mask_out else None)
             rgcn.rgcn_block_plan(self.dblk, self.params, self.ws, flags | plan_flags)
             rgcn.rgcn_block_forward(self.dblk, self.inputs, self.params, y, self.ws,
-                                    flags | (rgcn.RGCN_FUSE_RELU if self.fwd_relu else 0))
+                                    flags | (rgcn.RGCN_FUSE_RELU if self.fwd_relu else 0),
+                                    relu_mask=ym)
             rgcn.rgcn_block_backward(self.dblk, self.inputs, self.params, dy, dw_rel, dw_self,
                                      dbias, dh, demb if self.emb_types else None, self.ws,
                                      flags | self.flags_bwd)
@@ -151,7 +172,9 @@ class BlockRun:
                          "dw_self": [x.cpu() for x in dw_self],
                          "dbias": [x.cpu() if x is not None else None for x in dbias],
                          "dh": [x.cpu() if x is not None else None for x in dh],
-                         "demb": [x.cpu() if x is not None else None for x in demb]})
+                         "demb": [x.cpu() if x is not None else None for x in demb],
+                         "y_mask": ([x.cpu() if x is not None else None for x in ym]
+                                    if ym is not None else None)})
         self.gpu = outs[0]
         return outs
 

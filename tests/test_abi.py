@@ -92,18 +92,30 @@ def test_null_and_small_workspace_rejected(lib):
     assert st == 1  # misaligned
     _, n = _ws_size(lib, blk, p)
     # forward: NULL inputs, then NULL outputs
-    st = lib.rgcn_block_forward(ctypes.byref(blk.c), None, ctypes.byref(p), None, 0x100000, n,
-                                0, None)
+    st = lib.rgcn_block_forward(ctypes.byref(blk.c), None, ctypes.byref(p), None, None,
+                                0x100000, n, 0, None)
     assert st == 1
     inp = (rgcn._Input * 1)(rgcn._Input(0x40000, None, 20, 8))
-    st = lib.rgcn_block_forward(ctypes.byref(blk.c), inp, ctypes.byref(p), None, 0x100000, n, 0,
-                                None)
+    st = lib.rgcn_block_forward(ctypes.byref(blk.c), inp, ctypes.byref(p), None, None, 0x100000,
+                                n, 0, None)
     assert st == 1
     bad_ld = (rgcn._Input * 1)(rgcn._Input(0x40000, None, 20, 6))
     y = (ctypes.c_void_p * 1)(0x80000)
-    st = lib.rgcn_block_forward(ctypes.byref(blk.c), bad_ld, ctypes.byref(p), y, 0x100000, n, 0,
-                                None)
+    st = lib.rgcn_block_forward(ctypes.byref(blk.c), bad_ld, ctypes.byref(p), y, None, 0x100000,
+                                n, 0, None)
     assert st == 2
+    # sign-mask outputs: only with RGCN_FUSE_RELU, and 8-byte aligned
+    mask = (ctypes.c_void_p * 1)(0xA0000)
+    st = lib.rgcn_block_forward(ctypes.byref(blk.c), inp, ctypes.byref(p), y, mask, 0x100000, n,
+                                0, None)
+    assert st == 1 and "RGCN_FUSE_RELU" in lib.rgcn_last_error().decode()
+    st = lib.rgcn_block_transform(ctypes.byref(blk.c), ctypes.byref(p), y, mask, 0x100000, n, 0,
+                                  None)
+    assert st == 1 and "RGCN_FUSE_RELU" in lib.rgcn_last_error().decode()
+    odd = (ctypes.c_void_p * 1)(0xA0004)
+    st = lib.rgcn_block_forward(ctypes.byref(blk.c), inp, ctypes.byref(p), y, odd, 0x100000, n,
+                                rgcn.RGCN_FUSE_RELU, None)
+    assert st == 1 and "8-byte" in lib.rgcn_last_error().decode()
     # backward: a gradient of a type that is not in grad_src_types
     dy = (ctypes.c_void_p * 1)(0x80000)
     dh = (ctypes.c_void_p * 1)(0x90000)

@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import oracle
-from harness import BlockRun, TOL, rel_err, to64
+from harness import BlockRun, sign_words, TOL, rel_err, to64
 from paper_2406_06022_amd import rgcn, synth
 
 pytestmark = pytest.mark.gpu
@@ -109,6 +109,40 @@ def test_relu_flags_and_embedding_scatter(dtype):
         run.run_gpu()
         run.run_oracle()
         run.assert_parity()
+
+
+# ReLU sign bits: the forward writes them beside y (bit-exact against y > 0 on the stored
+# values, words fully written, bits past d_out zero), and a backward that reads them gives
+# bit for bit the results of one that reads the input rows (and matches the oracle).
+# d_out 40 and 136 leave a part-filled last word; 512 is whole words in every tile.
+@pytest.mark.parametrize("dtype,d_in,d_out", [("bf16", 64, 40), ("bf16", 128, 136),
+                                              ("bf16", 128, 512), ("f32", 32, 40),
+                                              ("f32", 64, 136)])
+def test_relu_sign_bits(dtype, d_in, d_out):
+    rng = np.random.default_rng(d_in + d_out)
+    blk = synth.random_block(rng, [700, 333], [517, 100], [(0, 1), (1, 0), (0, 0)], 9)
+    print(f"case relu sign bits {dtype} {d_in}->{d_out}", flush=True)
+    fwd = BlockRun(blk, dtype, d_in, d_out, seed=11, use_ids=True, fwd_relu=True, bias=True,
+                   mask_out=True)
+    fwd.run_gpu()
+    for t, y in enumerate(fwd.gpu["y"]):
+        if y is None:
+            continue
+        want = sign_words(y)
+        got = fwd.gpu["y_mask"][t]
+        assert torch.equal(got, want), f"type {t}: sign words differ"
+    runs = []
+    for mask_in in (False, True):
+        run = BlockRun(blk, dtype, d_in, d_out, seed=12, use_ids=True, input_relu=True,
+                       grad_types=(0, 1), emb_types=(0,), mask_in=mask_in)
+        run.run_gpu()
+        runs.append(run)
+    runs[1].run_oracle()
+    runs[1].assert_parity()
+    for key in ("dh", "demb"):
+        for a, b in zip(runs[0].gpu[key], runs[1].gpu[key]):
+            if a is not None:
+                assert torch.equal(a, b), f"{key} differs when read through the sign bits"
 
 
 @pytest.mark.parametrize("index", range(5))
@@ -212,13 +246,17 @@ def test_plan_skewed_sources_bit_exact():
 
 def _bitwise_equal(a, b):
     for key in a:
+        if a[key] is None:
+            assert b[key] is None, key
+            continue
         for x, z in zip(a[key], b[key]):
             if x is None:
                 assert z is None
                 continue
-            xv = x.view(torch.int16) if x.dtype == torch.bfloat16 else x.view(torch.int32)
-            zv = z.view(torch.int16) if z.dtype == torch.bfloat16 else z.view(torch.int32)
-            assert torch.equal(xv, zv), key
+            if x.dtype in (torch.bfloat16, torch.float32):
+                x = x.view(torch.int16) if x.dtype == torch.bfloat16 else x.view(torch.int32)
+                z = z.view(torch.int16) if z.dtype == torch.bfloat16 else z.view(torch.int32)
+            assert torch.equal(x, z), key
 
 
 @pytest.mark.parametrize("case", ["skewed-bf16", "claimed-runs-bf16", "claimed-runs-f32"])
