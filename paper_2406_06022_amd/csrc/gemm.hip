@@ -441,7 +441,6 @@ struct EpiForwardBf16 {
 // before the K loop (deg_of), so the epilogue waits for no load (store).
 struct EpiDms {
     static constexpr bool kPrefetch = true;
-    static constexpr bool kMask = false;
     float *out;
     int64_t M;
     int32_t N;
