@@ -420,20 +420,29 @@ struct EpiForwardBf16 {
         bq[2] = bf16_lo(w.y);
         bq[3] = bf16_hi(w.y);
     }
-    // returns the positive bits of the 4 stored values (bit e: column n + e)
-    __device__ __forceinline__ uint32_t store4(int64_t m, int64_t n, const f32x4 v,
-                                               const float *bq) const {
-        if (m >= M || n >= N) return 0u;
+    // the 4 values of columns n .. n + 3 with bias (and ReLU) as bf16 pairs lo, hi; returns
+    // their positive bits (bit e: column n + e), none outside the output.  No branches: the
+    // callers exchange the results between lanes.
+    __device__ __forceinline__ uint32_t pack4(int64_t m, int64_t n, const f32x4 v,
+                                              const float *bq, uint32_t &lo,
+                                              uint32_t &hi) const {
         float r[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             r[e] = v[e] + bq[e];
             if (relu) r[e] = r[e] > 0.f ? r[e] : 0.f;
         }
-        const uint32_t lo = pack_bf16x2(r[0], r[1]), hi = pack_bf16x2(r[2], r[3]);
-        *(uint2 *)((uint16_t *)y + m * N + n) = make_uint2(lo, hi);
-        return (uint32_t)((lo & 0xffffu) != 0u) | ((uint32_t)((lo >> 16) != 0u) << 1) |
-               ((uint32_t)((hi & 0xffffu) != 0u) << 2) | ((uint32_t)((hi >> 16) != 0u) << 3);
+        lo = pack_bf16x2(r[0], r[1]);
+        hi = pack_bf16x2(r[2], r[3]);
+        const uint32_t bits = (uint32_t)((lo & 0xffffu) != 0u) |
+                              ((uint32_t)((lo >> 16) != 0u) << 1) |
+                              ((uint32_t)((hi & 0xffffu) != 0u) << 2) |
+                              ((uint32_t)((hi >> 16) != 0u) << 3);
+        return m < M && n < N ? bits : 0u;
+    }
+    // 8 bf16 at columns n .. n + 7 of row m (N is a multiple of 8: whole or absent)
+    __device__ __forceinline__ void store8(int64_t m, int64_t n, uint4 v) const {
+        if (m < M && n < N) *(uint4 *)((uint16_t *)y + m * N + n) = v;
     }
 };
 
@@ -796,19 +805,35 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
             // 4 (lane / 16) .. + 3; the wave's 64 columns are one word of the sign mask, of
             // which the lane holds bits 16 ni + 4 (lane / 16) + e, kept packed as bits
             // 16 (mi % 2) + 4 ni + e of word mi / 2 while the results are stored
+            // The packed bf16 results of fragments 2 p and 2 p + 1 are exchanged between the
+            // lane rows (16 lanes) 0 and 1, and 2 and 3, of the wave: lane row q then holds
+            // 8 consecutive columns, 16 (q % 2) + 8 (q / 2) .. of the pair's 32, and the 4
+            // lanes of an output row store 64 contiguous bytes.
             static_assert(FM % 2 == 0 && FN == 4, "packed sign bits");
             uint32_t pk[FM / 2];
 #pragma unroll
             for (int i = 0; i < FM / 2; ++i) pk[i] = 0u;
+            const int cofs = 16 * (q & 1) + 8 * (q >> 1);
 #pragma unroll
-            for (int ni = 0; ni < FN; ++ni) {
-                const int64_t n = n0 + wn * FN * 16 + ni * 16 + 4 * q;
-                float bq[4];
-                epi.load_bias4(n, bq);
+            for (int p = 0; p < FN / 2; ++p) {
+                const int64_t na = n0 + wn * FN * 16 + p * 32 + 4 * q, nb = na + 16;
+                const int64_t ns = n0 + wn * FN * 16 + p * 32 + cofs;
+                float ba[4], bb[4];
+                epi.load_bias4(na, ba);
+                epi.load_bias4(nb, bb);
 #pragma unroll
-                for (int mi = 0; mi < FM; ++mi)
-                    pk[mi / 2] |= epi.store4(m0 + wm * FM * 16 + mi * 16 + r16, n, acc[mi][ni], bq)
-                                  << (16 * (mi % 2) + 4 * ni);
+                for (int mi = 0; mi < FM; ++mi) {
+                    const int64_t m = m0 + wm * FM * 16 + mi * 16 + r16;
+                    uint32_t a0, a1, b0, b1;
+                    const uint32_t bits = epi.pack4(m, na, acc[mi][2 * p], ba, a0, a1) |
+                                          (epi.pack4(m, nb, acc[mi][2 * p + 1], bb, b0, b1) << 4);
+                    pk[mi / 2] |= bits << (16 * (mi % 2) + 8 * p);
+                    // odd lane rows of the first operand trade places with even lane rows
+                    // of the second
+                    const auto s0 = __builtin_amdgcn_permlane16_swap(a0, b0, false, false);
+                    const auto s1 = __builtin_amdgcn_permlane16_swap(a1, b1, false, false);
+                    epi.store8(m, ns, make_uint4(s0[0], s1[0], s0[1], s1[1]));
+                }
             }
             if (epi.mask.w != nullptr) {
 #pragma unroll
