@@ -345,7 +345,8 @@ struct EpiForward {
     int32_t N;
     int32_t relu;
     ReluMask mask;
-    // returns the positive bits of the 16 columns n0 .. n0 + 15 (bit k: column n0 + k)
+    // v: columns n0 + 16 q .. + 3 for q = 0 .. 3; returns their positive bits (bit 4 q + e:
+    // column n0 + 16 q + e)
     __device__ __forceinline__ uint32_t operator()(int64_t m, int64_t n0, const float *v, int64_t) const {
         if (m >= M) return 0u;
         // N is a multiple of 4: each group of 4 columns is either whole or absent.  The
@@ -355,7 +356,7 @@ struct EpiForward {
         if (bias != nullptr) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const int64_t n = n0 + 4 * q;
+                const int64_t n = n0 + 16 * q;
                 const bool ok = n < N;
                 if constexpr (OUT_BF16) {
                     const uint2 w = *(const uint2 *)((const uint16_t *)bias + (ok ? n : 0));
@@ -375,7 +376,7 @@ struct EpiForward {
         uint32_t bits = 0u;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const int64_t n = n0 + 4 * q;
+            const int64_t n = n0 + 16 * q;
             if (n >= N) break;
             float r[4];
 #pragma unroll
@@ -463,13 +464,13 @@ struct EpiDms {
         if (!indptr[sl]) return -1;
         return indptr[sl][m + 1] - indptr[sl][m];
     }
-    // columns n0 + 4 q .. + 3 take degree deg[q]
+    // v: columns n0 + 16 q .. + 3, which take degree deg[q]
     __device__ __forceinline__ void store(int64_t m, int64_t n0, const float *v,
                                           const int32_t *deg) const {
         if (m >= M) return;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const int64_t n = n0 + 4 * q;
+            const int64_t n = n0 + 16 * q;
             if (n >= N) return;
             const bool zero = deg[q] == 0;
             const float scale = deg[q] > 0 ? (float)deg[q] : 1.f;
@@ -495,7 +496,7 @@ struct EpiPartial {
         float *o = out + split * M * N + m * N;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const int64_t n = n0 + 4 * q;
+            const int64_t n = n0 + 16 * q;   // v: columns n0 + 16 q .. + 3
             if (n >= N) return;
             *(float4 *)(o + n) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
         }
@@ -551,8 +552,8 @@ __global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const 
 
     // the epilogue's per-row data (EpiDms: degrees), read before the tiles so the loads
     // are long done when the epilogue needs them; slice e of the wave covers rows
-    // m0 + wm FM 16 + 16 e + er, the lane columns n0 + wn FN 16 + ec + 4 q
-    const int er = lane >> 2, ec = (lane & 3) * 16;
+    // m0 + wm FM 16 + 16 e + er, the lane columns n0 + wn FN 16 + ec + 16 q
+    const int er = lane & 15, ec = 4 * (lane >> 4);
     int32_t pdeg[FM][4];
     if constexpr (Epi::kPrefetch) {
 #pragma unroll
@@ -560,7 +561,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const 
 #pragma unroll
             for (int q = 0; q < 4; ++q)
                 pdeg[e][q] = epi.deg_of(m0 + wm * FM * 16 + 16 * e + er,
-                                        n0 + wn * FN * 16 + ec + 4 * q);
+                                        n0 + wn * FN * 16 + ec + 16 * q);
     }
 
     // Steps are padded to a multiple of R and every load is issued unconditionally
@@ -594,26 +595,30 @@ __global__ __launch_bounds__(C::NT) void k_gemm(const LA la, const LB lb, const 
     }
     __syncthreads();
 
-    // epilogue: per wave, 16 rows at a time through the wave's own LDS area, then 16
-    // contiguous columns per lane
+    // epilogue: per wave, 16 rows at a time through the wave's own LDS area; lane L takes
+    // row L % 16 and columns 4 (L / 16) + 16 q .. + 3 (q = 0 .. 3), so the 4 lanes of a row
+    // store 64 contiguous bytes in each store instruction
     float *stage = (float *)lds + wave * 16 * kStagePitch;
     auto emit = [&](int64_t row, int slice) {
         __builtin_amdgcn_wave_barrier();
         float vals[16];
 #pragma unroll
-        for (int e = 0; e < 16; e += 4) {
-            const float4 x = *(const float4 *)(stage + er * kStagePitch + ec + e);
-            vals[e] = x.x; vals[e + 1] = x.y; vals[e + 2] = x.z; vals[e + 3] = x.w;
+        for (int q = 0; q < 4; ++q) {
+            const float4 x = *(const float4 *)(stage + er * kStagePitch + ec + 16 * q);
+            vals[4 * q] = x.x; vals[4 * q + 1] = x.y; vals[4 * q + 2] = x.z; vals[4 * q + 3] = x.w;
         }
         __builtin_amdgcn_wave_barrier();
         if constexpr (Epi::kPrefetch) {
             epi.store(row + er, n0 + wn * FN * 16 + ec, vals, pdeg[slice]);
         } else if constexpr (Epi::kMask) {
-            // the 4 lanes of a row hold its 64 columns, 16 each
+            // the 4 lanes of a row (L, L + 16, L + 32, L + 48) hold its 64 columns
             const uint32_t bits = epi(row + er, n0 + wn * FN * 16 + ec, vals, split);
-            if (epi.mask.w != nullptr)
-                epi.mask.put(row + er, epi.M, n0 + wn * FN * 16, epi.N, (uint64_t)bits << ec, 1,
-                             4, (lane & 3) == 0);
+            if (epi.mask.w != nullptr) {
+                uint64_t b64 = 0u;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) b64 |= (uint64_t)((bits >> (4 * q)) & 0xFu) << (ec + 16 * q);
+                epi.mask.put(row + er, epi.M, n0 + wn * FN * 16, epi.N, b64, 16, 4, (lane >> 4) == 0);
+            }
         } else {
             epi(row + er, n0 + wn * FN * 16 + ec, vals, split);
         }
@@ -1051,15 +1056,16 @@ __global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw(const char *__restrict_
     // stages before the epilogue reuses them
     __syncthreads();
 
+    // lane L: row L % 16, columns 4 (L / 16) + 16 q .. + 3 of the staged 16 x 64 slice
     float *stage = (float *)lds + wave * 16 * kStagePitch;
-    const int er = lane >> 2, ec = (lane & 3) * 16;
+    const int er = lane & 15, ec = 4 * (lane >> 4);
     auto emit = [&](int64_t row) {
         __builtin_amdgcn_wave_barrier();
         float vals[16];
 #pragma unroll
-        for (int e = 0; e < 16; e += 4) {
-            const float4 x = *(const float4 *)(stage + er * kStagePitch + ec + e);
-            vals[e] = x.x; vals[e + 1] = x.y; vals[e + 2] = x.z; vals[e + 3] = x.w;
+        for (int q = 0; q < 4; ++q) {
+            const float4 x = *(const float4 *)(stage + er * kStagePitch + ec + 16 * q);
+            vals[4 * q] = x.x; vals[4 * q + 1] = x.y; vals[4 * q + 2] = x.z; vals[4 * q + 3] = x.w;
         }
         __builtin_amdgcn_wave_barrier();
         epi(row + er, o0 + wn * FN * 16 + ec, vals, split);
