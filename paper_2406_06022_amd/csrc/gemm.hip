@@ -1099,8 +1099,9 @@ __global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw(const char *__restrict_
 // v_mfma_f32_16x16x32_bf16 with the weights as the first operand: lane l supplies weight
 // row 16 t + l % 16 and dY row m0 + l % 16, K group q = l / 16, and holds output row
 // m0 + l % 16, columns 16 t + 4 q .. + 3.  Wave w's slice is K values [KW w, KW w + KW),
-// KW = d_out / 8; MFMA step s gives group q the 8 values at KW w + 8 (S q + s) (S = KW / 32
-// steps), so each lane reads 32 S contiguous bytes of its row.  Partial row r, 4-column
+// KW = d_out / 8; MFMA step s gives group q the 8 values at KW w + 32 s + 8 q (S = KW / 32
+// steps), so the 4 groups of a step read 128 contiguous bytes of each row and every load
+// instruction stays within one 128-byte window per row.  Partial row r, 4-column
 // piece c sits at slot c ^ (2 r) of the row's 512 bytes.  Two LDS buffers alternate
 // between row blocks (one barrier per block); each wave's register copies of the next NB
 // blocks are in flight while it multiplies one.
@@ -1124,17 +1125,17 @@ __global__ __launch_bounds__(kDmsStreamWaves * 64, 1) void k_dms_stream(
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int r16 = lane & 15, q = lane >> 4;
     // weight fragments: tile t, step s: row n = 16 t + r16 (W_{n / d_in} row n % d_in, zero
-    // past N), K values KW wave + 8 (S q + s) ..
+    // past N), K values KW wave + 32 s + 8 q ..
     bf16x8 wf[8][S];
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
         const int n = t * 16 + r16;
         const int sl = n < p.N ? n / p.d_in : 0;
         const char *wr = (const char *)p.w[sl] + (int64_t)(n < p.N ? n - sl * p.d_in : 0) * D * 2 +
-                         (wave * KW + q * 8 * S) * 2;
+                         (wave * KW + q * 8) * 2;
 #pragma unroll
         for (int s = 0; s < S; ++s) {
-            u32x4 v = *(const u32x4 *)(wr + s * 16);
+            u32x4 v = *(const u32x4 *)(wr + s * 64);
             if (n >= p.N) v = u32x4{0u, 0u, 0u, 0u};
             wf[t][s] = __builtin_bit_cast(bf16x8, v);
         }
@@ -1160,10 +1161,10 @@ __global__ __launch_bounds__(kDmsStreamWaves * 64, 1) void k_dms_stream(
         const int64_t m0 = ((int64_t)blockIdx.x + (int64_t)(live ? bi : 0) * P) * 16;
         const int64_t m = m0 + r16;
         const bool ok = live && m < M;
-        const float *src = ok ? dy + m * D + wave * KW + q * 8 * S : zp;
-        const int st = ok ? 4 : 0;
+        const float *src = ok ? dy + m * D + wave * KW + q * 8 : zp;
+        const int st = ok ? 1 : 0;
 #pragma unroll
-        for (int i = 0; i < 2 * S; ++i) b.v[i] = *(const f32x4 *)(src + i * st);
+        for (int i = 0; i < 2 * S; ++i) b.v[i] = *(const f32x4 *)(src + (32 * (i / 2) + 4 * (i % 2)) * st);
         const int64_t mr = m0 + rr;
         const int32_t *d = (live && ipc != nullptr && mr < M) ? ipc + mr : (const int32_t *)zp;
         b.i0 = d[0];
