@@ -1102,9 +1102,10 @@ __global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw(const char *__restrict_
 // KW = d_out / 8; MFMA step s gives group q the 8 values at KW w + 32 s + 8 q (S = KW / 32
 // steps), so the 4 groups of a step read 128 contiguous bytes of each row and every load
 // instruction stays within one 128-byte window per row.  Partial row r, 4-column
-// piece c sits at slot c ^ (2 r) of the row's 512 bytes.  Two LDS buffers alternate
-// between row blocks (one barrier per block); each wave's register copies of the next NB
-// blocks are in flight while it multiplies one.
+// piece c sits at slot c ^ r of the row's 512 bytes, so the 16 rows a partial store
+// writes and the 32 pieces a summing read takes fall in distinct banks.  Two LDS buffers
+// alternate between row blocks (one barrier per block); each wave's register copies of
+// the next NB blocks are in flight while it multiplies one.
 constexpr int kDmsStreamCols = 128;                  // output columns
 constexpr int kDmsStreamWaves = 8;
 constexpr int kDmsStreamPart = 16 * kDmsStreamCols * 4;   // one wave's partial block
@@ -1205,7 +1206,7 @@ __global__ __launch_bounds__(kDmsStreamWaves * 64, 1) void k_dms_stream(
             char *mine = part + wave * kDmsStreamPart;
 #pragma unroll
             for (int t = 0; t < 8; ++t)
-                *(f32x4 *)(mine + r16 * 512 + (((4 * t + q) ^ (2 * r16)) * 16)) = acc[t];
+                *(f32x4 *)(mine + r16 * 512 + (((4 * t + q) ^ r16) * 16)) = acc[t];
             load(bi + NB, bufs[b]);
             // every wave's partials of this block are in LDS; the buffer written next was
             // last read before this barrier
@@ -1213,7 +1214,7 @@ __global__ __launch_bounds__(kDmsStreamWaves * 64, 1) void k_dms_stream(
             f32x4 sum = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int w = 0; w < kDmsStreamWaves; ++w)
-                sum += *(const f32x4 *)(part + w * kDmsStreamPart + rr * 512 + ((cq ^ (2 * rr)) * 16));
+                sum += *(const f32x4 *)(part + w * kDmsStreamPart + rr * 512 + ((cq ^ rr) * 16));
             const int64_t m = ((int64_t)blockIdx.x + (int64_t)bi * P) * 16 + rr;
             if (col_ok && m < M) {
                 const int32_t deg = i1 - i0;
