@@ -466,10 +466,20 @@ __global__ __launch_bounds__(kThreads) void k_gather_flat(const SegDesc *__restr
 //    w -= lr res / (sqrt(state) + eps), with `old` the state and `cur` the table values
 //    read before the sum (each row belongs to one group, so no other lane touches it);
 //  - demb += res, as a read-add-write of `old` when ids are unique, else by atomics.
-template <bool BF16IN, bool OPT>
+// OFF_HERE: the lane's byte offset is formed at the store (kept across the row loop as
+// part of a 64-bit address it costs two registers for the whole kernel, which the bit
+// form at two chunks per lane cannot spare)
+template <bool BF16IN, bool OPT, bool OFF_HERE = false>
 __device__ __forceinline__ void tsum_store(const TsumArgs &a, int64_t j, int64_t grow, int c,
                                            f32x4 res, f32x4 old, f32x4 cur) {
-    if (a.dh) *(f32x4 *)(a.dh + j * a.d_in + (int64_t)c * 4) = res;
+    int co = c * 16;
+    if constexpr (OFF_HERE) asm volatile("" : "+v"(co));
+    if (a.dh) {
+        if constexpr (OFF_HERE)
+            *(f32x4 *)((char *)(a.dh + j * a.d_in) + co) = res;
+        else
+            *(f32x4 *)(a.dh + j * a.d_in + (int64_t)c * 4) = res;
+    }
     if constexpr (OPT) {
         const f32x4 st = old + res * res;
         f32x4 w;
@@ -484,7 +494,8 @@ __device__ __forceinline__ void tsum_store(const TsumArgs &a, int64_t j, int64_t
             *(f32x4 *)tp = w;
         }
     } else if (a.demb) {
-        float *dp = a.demb + grow * a.d_in + (int64_t)c * 4;
+        float *dp = OFF_HERE ? (float *)((char *)(a.demb + grow * a.d_in) + co)
+                             : a.demb + grow * a.d_in + (int64_t)c * 4;
         if (a.ids_unique) {
             *(f32x4 *)dp = old + res;
         } else {
@@ -723,10 +734,14 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
             // are unique.  (Written this way, pointer chosen here and the flag test in the
             // predicate: forms that pick the pointer once before the loop measured 9%
             // slower at d = 128.)
-            const bool ok_old = OPT ? okc : (okc && a.demb != nullptr && a.ids_unique);
-            const float *ob = OPT ? a.opt_state : a.demb;
-            rw.old[p] = *gbl(ok_old ? (const f32x4 *)(ob + m.grow * a.d_in + (int64_t)c * 4)
-                                    : (const f32x4 *)zero);
+            if constexpr (MASK) {
+                rw.old[p] = f32x4{0.f, 0.f, 0.f, 0.f};   // never read (see transpose_sum_dt)
+            } else {
+                const bool ok_old = OPT ? okc : (okc && a.demb != nullptr && a.ids_unique);
+                const float *ob = OPT ? a.opt_state : a.demb;
+                rw.old[p] = *gbl(ok_old ? (const f32x4 *)(ob + m.grow * a.d_in + (int64_t)c * 4)
+                                        : (const f32x4 *)zero);
+            }
             const bool ok_self = okc && a.self_dms != nullptr && m.j < a.n_dst;
             rw.self[p] = *gbl(ok_self ? (const f32x4 *)(a.self_dms + m.j * a.self_ld + (int64_t)c * 4)
                                       : (const f32x4 *)zero);
@@ -789,7 +804,7 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
 #pragma unroll
                 for (int e = 0; e < 4; ++e) res[e] = rw.hm[p][e] > 0.f ? res[e] : 0.f;
             }
-            tsum_store<BF16IN, OPT>(a, rw.m.j, rw.m.grow, c, res, rw.old[p],
+            tsum_store<BF16IN, OPT, MASK>(a, rw.m.j, rw.m.grow, c, res, rw.old[p],
                                     MASK ? f32x4{0.f, 0.f, 0.f, 0.f} : rw.hm[p]);
         }
     };
@@ -982,9 +997,11 @@ __global__ __launch_bounds__(kThreads) void k_transpose_sum_adagrad(TsumArgs a, 
                                                                     int chunks) {
     transpose_sum_body<BF16IN, CPL, true, false>(a, G, gpw, chunks);
 }
+// the bit form at two chunks per lane (hidden layers of 512) is held to 128 registers, so
+// four of its waves share a SIMD
 template <bool BF16IN, int CPL, bool MASK>
-__global__ __launch_bounds__(kThreads) void k_transpose_pipe(TsumArgs a, int G, int gpw,
-                                                             int chunks) {
+__global__ __launch_bounds__(kThreads, (MASK && CPL == 2) ? 4 : 1) void k_transpose_pipe(
+    TsumArgs a, int G, int gpw, int chunks) {
     transpose_pipe_body<BF16IN, CPL, false, MASK>(a, G, gpw, chunks);
 }
 template <bool BF16IN, int CPL>
@@ -1232,11 +1249,13 @@ hipError_t launch_transpose_cpl(const TsumArgs &a, const GroupShape &gs, int chu
 }
 
 // kernel forms: the block dtype (B), Adagrad (O), the input's ReLU signs read as bits (K;
-// never with O: a learnable table is not a ReLU output)
+// never with O: a learnable table is not a ReLU output).  The bit form reads no row
+// before the sum, so an embedding gradient updated in place (unique ids) takes the form
+// that reads the input rows instead.
 template <bool B>
 hipError_t transpose_sum_dt(const TsumArgs &a, const GroupShape &gs, int chunks, hipStream_t s) {
     if (a.opt_state != nullptr) return launch_transpose_cpl<B, true, false>(a, gs, chunks, s);
-    if (a.input_relu && a.relu_mask != nullptr)
+    if (a.input_relu && a.relu_mask != nullptr && !(a.demb != nullptr && a.ids_unique))
         return launch_transpose_cpl<B, false, true>(a, gs, chunks, s);
     return launch_transpose_cpl<B, false, false>(a, gs, chunks, s);
 }
