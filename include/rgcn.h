@@ -70,6 +70,18 @@ typedef enum { RGCN_F32 = 0, RGCN_BF16 = 1 } rgcn_dtype;
 #define RGCN_PLAN_ENUMERATION_ORDER 0x80u /* rgcn_block_plan: keep both schedules in
                                      enumeration order (no degree sort); every result is
                                      bit-identical, only the processing order changes */
+#define RGCN_DY_HILO         0x100u /* backward (dense part), bf16: dy[t] is given in the
+                                     hi/lo form below instead of fp32 */
+#define RGCN_DH_HILO         0x200u /* backward (sparse part), bf16: dh_src[t] is written in
+                                     the hi/lo form below instead of fp32 */
+/* The hi/lo form of an fp32 gradient row of d values: d bf16 high parts followed by d bf16
+ * low parts, hi = x rounded to bf16 (nearest even), lo = (x - hi) rounded to bf16; the same
+ * 4 d bytes per row as fp32.  The bf16 backward products take dY as exactly this pair of
+ * bf16 operands (16 significant bits); a block's dh_src written in this form is the next
+ * (lower) block's dy, read without splitting it again: the weight and input gradients are
+ * bit for bit those of the fp32 row, and the bias gradient is the column sum of hi + lo
+ * (which differs from x by at most 2^-16 |x|).  Either flag with the fp32 dtype returns
+ * RGCN_ERR_UNSUPPORTED. */
 
 /* One relation (canonical edge type src_type -> dst_type) of a block, as a CSR over the
  * destination rows.  indptr[0] = 0, non-decreasing, indptr[n_dst] = nnz; indices are
@@ -208,7 +220,8 @@ rgcn_status rgcn_block_forward(const rgcn_block *block, const rgcn_input *in,
  *   demb[t]:   [num_rows x d_in] table-shaped; row row_ids[j] += dH_t[j] (scatter-ADD into
  *              caller-initialised memory; rows never named are untouched).
  * dh_src[t] / demb[t] require bit t of grad_src_types.  dw_self entries must not alias.
- * flags: RGCN_VALIDATE_DEVICE, RGCN_INPUT_RELU, RGCN_IDS_UNIQUE. */
+ * flags: RGCN_VALIDATE_DEVICE, RGCN_INPUT_RELU, RGCN_IDS_UNIQUE, and in bf16 RGCN_DY_HILO
+ * (dy in the hi/lo form) and RGCN_DH_HILO (dh_src written in the hi/lo form). */
 rgcn_status rgcn_block_backward(const rgcn_block *block, const rgcn_input *in,
                                 const rgcn_params *params, const float *const *dy,
                                 float *const *dw_rel, float *const *dw_self,
@@ -236,11 +249,11 @@ rgcn_status rgcn_block_transform(const rgcn_block *block, const rgcn_params *par
 /* The two stages of rgcn_block_backward.
  * rgcn_block_backward_dense: weight and bias gradients (dw_rel, dw_self, dbias as in
  *   rgcn_block_backward) and, for the types in grad_src_types, the per-edge input-side
- *   products dY_t W^T / deg kept in the workspace.
+ *   products dY_t W^T / deg kept in the workspace.  flags: RGCN_DY_HILO (bf16).
  * rgcn_block_backward_sparse: the transposed sums over the CSC transpose that turn those
  *   products into dh_src[t] and the scatter-add into demb[t] (as in rgcn_block_backward);
  *   must follow rgcn_block_backward_dense on the same workspace.
- *   flags: RGCN_VALIDATE_DEVICE, RGCN_INPUT_RELU, RGCN_IDS_UNIQUE. */
+ *   flags: RGCN_VALIDATE_DEVICE, RGCN_INPUT_RELU, RGCN_IDS_UNIQUE, RGCN_DH_HILO (bf16). */
 rgcn_status rgcn_block_backward_dense(const rgcn_block *block, const rgcn_params *params,
                                       const float *const *dy, float *const *dw_rel,
                                       float *const *dw_self, float *const *dbias,

@@ -26,7 +26,8 @@ class MiniBatchStack:
                  input_ids: Sequence[Optional[torch.Tensor]], weights, dtype: str,
                  dims: Sequence[int], emb_types: Sequence[int] = (), device="cuda",
                  want_weight_grads: bool = True, ids_unique: bool = True,
-                 edge_rows: bool = True, relu_masks: bool = True):
+                 edge_rows: bool = True, relu_masks: bool = True,
+                 hilo_grads: Optional[bool] = None):
         """blocks: host blocks (blocks[0] nearest the input); input_tables[t] / input_ids[t]:
         layer-0 table and int64 global row ids of each type; weights[l] = (w_rel, w_self,
         bias) device tensors of layer l; emb_types: types whose table is learnable.
@@ -34,7 +35,11 @@ class MiniBatchStack:
         sampler's global source ids) to the library when the blocks carry them and every
         type has row ids, so its gather reads each edge's table row directly.
         relu_masks: the transforms followed by a ReLU also write the signs of their output
-        as bits, and the next block's backward reads those instead of the activation rows."""
+        as bits, and the next block's backward reads those instead of the activation rows.
+        hilo_grads (default: on for bf16): the gradients passed between blocks (dh[l],
+        l >= 1) are written and read in the hi/lo form, per row d_l bf16 high parts then
+        d_l bf16 low parts (hi = bf16(g), lo = bf16(g - hi)), which is what the bf16
+        backward products take; the buffers keep their fp32 shape and size."""
         self.L = len(blocks)
         self.dtype = dtype
         self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
@@ -42,6 +47,7 @@ class MiniBatchStack:
         self.device = device
         self.emb_types = list(emb_types)
         self.ids_unique = ids_unique
+        self.hilo_grads = (dtype == "bf16") if hilo_grads is None else bool(hilo_grads)
         self.blocks: List[rgcn.DeviceBlock] = []
         rows0 = edge_rows and all(x is not None for x in input_ids)
         for l, blk in enumerate(blocks):
@@ -82,6 +88,7 @@ class MiniBatchStack:
                        for t in range(b.num_types)] if want_weight_grads else None
                       for l, b in enumerate(self.blocks)]
         # dh[l][t]: gradient w.r.t. block l's input (l >= 1) = output gradient of block l-1
+        # (in the hi/lo form with hilo_grads)
         self.dh = [None] + [[torch.empty((n, dims[l]), dtype=f32, device=device) if n > 0 else None
                              for n in b.n_src] for l, b in enumerate(self.blocks) if l >= 1]
         self.demb = [None] * len(self.blocks[0].n_src)
@@ -159,8 +166,10 @@ class MiniBatchStack:
         for l in reversed(range(self.L)):
             dy = dy_top if l == self.L - 1 else self.dh[l + 1]
             f = flags
+            if self.hilo_grads and l < self.L - 1:
+                f |= rgcn.RGCN_DY_HILO
             if l > 0:
-                f |= rgcn.RGCN_INPUT_RELU
+                f |= rgcn.RGCN_INPUT_RELU | (rgcn.RGCN_DH_HILO if self.hilo_grads else 0)
                 dh, demb = self.dh[l], None
             else:
                 dh = None

@@ -475,10 +475,20 @@ __device__ __forceinline__ void tsum_store(const TsumArgs &a, int64_t j, int64_t
     int co = c * 16;
     if constexpr (OFF_HERE) asm volatile("" : "+v"(co));
     if (a.dh) {
-        if constexpr (OFF_HERE)
+        if (a.dh_hilo) {
+            // the 4 values' bf16 high parts at element 4 c of the row's first half, their
+            // low parts at the same place in the second half
+            const uint32_t h0 = pack_bf16x2(res[0], res[1]), h1 = pack_bf16x2(res[2], res[3]);
+            const uint32_t l0 = pack_bf16x2(res[0] - bf16_lo(h0), res[1] - bf16_hi(h0));
+            const uint32_t l1 = pack_bf16x2(res[2] - bf16_lo(h1), res[3] - bf16_hi(h1));
+            char *rp = (char *)(a.dh + j * a.d_in) + co / 2;
+            *(uint2 *)rp = make_uint2(h0, h1);
+            *(uint2 *)(rp + (int64_t)a.d_in * 2) = make_uint2(l0, l1);
+        } else if constexpr (OFF_HERE) {
             *(f32x4 *)((char *)(a.dh + j * a.d_in) + co) = res;
-        else
+        } else {
             *(f32x4 *)(a.dh + j * a.d_in + (int64_t)c * 4) = res;
+        }
     }
     if constexpr (OPT) {
         const f32x4 st = old + res * res;
@@ -1029,15 +1039,25 @@ __global__ __launch_bounds__(kThreads) void k_pack_weights(WSlots ws, int nslots
 
 // Deterministic column sums: partial[split][o] over a fixed row range, then a fixed-order
 // sum over splits.
-__global__ __launch_bounds__(kThreads) void k_colsum_partial(const float *dy, int64_t rows,
-                                                             int cols, int64_t rows_per_split,
+// hilo: dy rows in the hi/lo form (cols bf16 high parts, then cols low parts); an element
+// is then hi + lo
+__global__ __launch_bounds__(kThreads) void k_colsum_partial(const float *dy, int hilo,
+                                                             int64_t rows, int cols,
+                                                             int64_t rows_per_split,
                                                              float *partial) {
     const int o = blockIdx.x * kThreads + threadIdx.x;
     if (o >= cols) return;
     const int64_t r0 = (int64_t)blockIdx.y * rows_per_split;
     const int64_t r1 = r0 + rows_per_split < rows ? r0 + rows_per_split : rows;
     float acc = 0.f;
-    for (int64_t r = r0; r < r1; ++r) acc += dy[r * cols + o];
+    if (hilo) {
+        const uint16_t *h = (const uint16_t *)dy;
+        for (int64_t r = r0; r < r1; ++r)
+            acc += __uint_as_float((uint32_t)h[r * 2 * cols + o] << 16) +
+                   __uint_as_float((uint32_t)h[r * 2 * cols + cols + o] << 16);
+    } else {
+        for (int64_t r = r0; r < r1; ++r) acc += dy[r * cols + o];
+    }
     partial[(int64_t)blockIdx.y * cols + o] = acc;
 }
 __global__ __launch_bounds__(kThreads) void k_colsum_final(const float *partial, int splits,
@@ -1291,8 +1311,8 @@ static int64_t colsum_splits(int64_t rows) {
 size_t column_sums_temp_bytes(int64_t rows, int cols) {
     return (size_t)colsum_splits(rows) * cols * 4 + 256;
 }
-hipError_t column_sums(const float *dy, int64_t rows, int cols, float *out, float *partial,
-                       int64_t max_splits, hipStream_t s) {
+hipError_t column_sums(const float *dy, bool hilo, int64_t rows, int cols, float *out,
+                       float *partial, int64_t max_splits, hipStream_t s) {
     (void)max_splits;
     if (cols == 0) return hipSuccess;
     if (rows == 0) {
@@ -1304,7 +1324,7 @@ hipError_t column_sums(const float *dy, int64_t rows, int cols, float *out, floa
     const int64_t rps = cdiv(rows, sp);
     const int64_t nsp = cdiv(rows, rps);
     hipLaunchKernelGGL(k_colsum_partial, dim3((unsigned)cdiv(cols, kThreads), (unsigned)nsp),
-                       dim3(kThreads), 0, s, dy, rows, cols, rps, partial);
+                       dim3(kThreads), 0, s, dy, hilo ? 1 : 0, rows, cols, rps, partial);
     RGCN_HIP_TRY(hipGetLastError());
     hipLaunchKernelGGL(k_colsum_final, dim3((unsigned)cdiv(cols, kThreads)), dim3(kThreads), 0, s,
                        partial, (int)nsp, cols, out);

@@ -599,6 +599,13 @@ rgcn_status rgcn_block_forward(const rgcn_block *block, const rgcn_input *in,
                                 flags & ~RGCN_VALIDATE_DEVICE, stream);
 }
 
+// the hi/lo gradient forms exist for the bf16 products only
+static rgcn_status check_hilo_flags(const Layout &L, unsigned flags) {
+    if ((flags & (RGCN_DY_HILO | RGCN_DH_HILO)) && L.dt != RGCN_BF16)
+        return fail(RGCN_ERR_UNSUPPORTED, "RGCN_DY_HILO / RGCN_DH_HILO need the bf16 dtype");
+    return RGCN_OK;
+}
+
 static rgcn_status check_dy(const rgcn_block *block, const Layout &L, const float *const *dy) {
     if (!dy) return fail(RGCN_ERR_INVALID_ARG, "dy is NULL");
     for (int t = 0; t < L.T; ++t)
@@ -633,12 +640,13 @@ rgcn_status rgcn_block_backward_dense(const rgcn_block *block, const rgcn_params
                                       float *const *dw_self, float *const *dbias,
                                       void *workspace, size_t workspace_bytes, unsigned flags,
                                       hipStream_t stream) {
-    (void)flags;
     Layout L;
     rgcn_status st = make_layout(block, params, L);
     if (st != RGCN_OK) return st;
     if ((st = check_workspace(L, workspace, workspace_bytes)) != RGCN_OK) return st;
+    if ((st = check_hilo_flags(L, flags)) != RGCN_OK) return st;
     if ((st = check_dy(block, L, dy)) != RGCN_OK) return st;
+    const bool hilo = (flags & RGCN_DY_HILO) != 0;
     for (int t = 0; t < L.T; ++t)
         if (dw_self && dw_self[t])
             for (int u = 0; u < t; ++u)
@@ -669,10 +677,10 @@ rgcn_status rgcn_block_backward_dense(const rgcn_block *block, const rgcn_params
         if (any)
             TRY_HIP(gemm_dw(L.dt, nd > 0 ? ws + L.off_mcat[t] : nullptr, nd,
                             nd > 0 ? (int)L.K[t] : out.count * L.d_in, L.d_in,
-                            nd > 0 ? dy[t] : nullptr, L.d_out, out,
+                            nd > 0 ? dy[t] : nullptr, hilo, L.d_out, out,
                             (float *)(scratch + L.off_partial), stream), "weight gradient");
         if (dbias && dbias[t])
-            TRY_HIP(column_sums(nd > 0 ? dy[t] : nullptr, nd, L.d_out, dbias[t],
+            TRY_HIP(column_sums(nd > 0 ? dy[t] : nullptr, hilo, nd, L.d_out, dbias[t],
                                 (float *)(scratch + L.off_colsum), 0, stream), "bias gradient");
         // input side: dMs_t = dY_t [W_self_t | W_r ...]^T, relation slots divided by deg
         if (nd > 0 && L.dms_nslots[t] > 0) {
@@ -687,7 +695,7 @@ rgcn_status rgcn_block_backward_dense(const rgcn_block *block, const rgcn_params
                     ds.w[L.dms_rel[r]] = params->w_rel[r];
                     ds.indptr[L.dms_rel[r]] = block->rels[r].indptr;
                 }
-            TRY_HIP(gemm_dms(L.dt, dy[t], nd, L.d_out, L.d_in, ds,
+            TRY_HIP(gemm_dms(L.dt, dy[t], hilo, nd, L.d_out, L.d_in, ds,
                              (float *)(scratch + L.off_dms[t]), stream), "input-side transform");
         }
     }
@@ -735,6 +743,7 @@ rgcn_status backward_sparse(const rgcn_block *block, const rgcn_input *in,
     rgcn_status st = make_layout(block, params, L);
     if (st != RGCN_OK) return st;
     if ((st = check_workspace(L, workspace, workspace_bytes)) != RGCN_OK) return st;
+    if ((st = check_hilo_flags(L, flags)) != RGCN_OK) return st;
     if ((st = check_sparse_outputs(block, in, L, dh_src, demb, flags)) != RGCN_OK) return st;
     if (opt && (st = check_adagrad(block, in, L, demb, opt, flags)) != RGCN_OK) return st;
     char *ws = (char *)workspace;
@@ -764,6 +773,7 @@ rgcn_status backward_sparse(const rgcn_block *block, const rgcn_input *in,
         }
         a.ids_unique = (flags & RGCN_IDS_UNIQUE) ? 1 : 0;
         a.dh = dh;
+        a.dh_hilo = (flags & RGCN_DH_HILO) ? 1 : 0;
         a.demb = de;
         if (state) {
             a.opt_state = state;
@@ -853,6 +863,7 @@ rgcn_status rgcn_block_backward(const rgcn_block *block, const rgcn_input *in,
     if (st != RGCN_OK) return st;
     if ((st = check_workspace(L, workspace, workspace_bytes)) != RGCN_OK) return st;
     if ((st = check_inputs(block, in, L, false)) != RGCN_OK) return st;
+    if ((st = check_hilo_flags(L, flags)) != RGCN_OK) return st;
     if ((st = check_dy(block, L, dy)) != RGCN_OK) return st;
     if ((st = check_sparse_outputs(block, in, L, dh_src, demb, flags)) != RGCN_OK) return st;
     if (flags & RGCN_VALIDATE_DEVICE) {

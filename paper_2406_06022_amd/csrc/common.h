@@ -210,6 +210,7 @@ struct TsumArgs {
     int32_t input_relu;
     int32_t ids_unique;
     float *dh;               // [n_src x d_in] or NULL
+    int32_t dh_hilo;         // dh rows in the hi/lo form (d_in bf16 high parts, then low)
     float *demb;             // table-shaped or NULL
     float *opt_state;        // Adagrad mode: fp32 [num_rows x d_in] squared-gradient sums, or NULL
     void *opt_table;         // Adagrad mode: the table of `in`, updated in place
@@ -307,8 +308,9 @@ hipError_t featureless_mean(const FeatArgs &a, uint32_t *words, hipStream_t s);
 
 hipError_t pack_weights(rgcn_dtype dt, int d_in, int d_out, const void *const *w_slots,
                         int nslots, void *wcat_t, hipStream_t s);
-hipError_t column_sums(const float *dy, int64_t rows, int cols, float *out, float *partial,
-                       int64_t max_splits, hipStream_t s);
+// hilo: dy rows in the hi/lo form (cols bf16 high parts, then cols low parts)
+hipError_t column_sums(const float *dy, bool hilo, int64_t rows, int cols, float *out,
+                       float *partial, int64_t max_splits, hipStream_t s);
 size_t column_sums_temp_bytes(int64_t rows, int cols);
 hipError_t validate_csr(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
                         int64_t nnz, int64_t n_src, uint32_t *err, hipStream_t s);
@@ -331,16 +333,17 @@ struct DmsSlots {
     const void *w[kMaxSlots];
     const int32_t *indptr[kMaxSlots];
 };
-hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_in,
-                    const DmsSlots &slots, float *dms, hipStream_t s);
+hipError_t gemm_dms(rgcn_dtype dt, const float *dy, bool dy_hilo, int64_t M, int d_out,
+                    int d_in, const DmsSlots &slots, float *dms, hipStream_t s);
 // Weight side: dWcat[kc][o] = sum_i Mcat[i][kc] dy[i][o], K = rows of Mcat.
 size_t gemm_dw_partial_bytes(int64_t M, int Kcat, int d_out);
 struct DwOut {
     int32_t count;            // slots
     float *w[kMaxSlots];      // destination of slot s ([d_in x d_out]) or NULL
 };
+// dy_hilo (bf16): dy rows in the hi/lo form (d_out bf16 high parts, then d_out low parts)
 hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_in,
-                   const float *dy, int d_out, const DwOut &out, float *partial,
+                   const float *dy, bool dy_hilo, int d_out, const DwOut &out, float *partial,
                    hipStream_t s);
 
 }  // namespace rgcn

@@ -273,6 +273,53 @@ struct LoadRowsF32HiLo {
     }
 };
 
+// The same tiles from dY rows in the hi/lo form (K bf16 high parts, then K low parts; a
+// row's byte pitch is that of its fp32 form): each chunk's high and low parts are loaded
+// as they are and stored without a split.
+template <class TL, int NT, int LO_OFF>
+struct LoadRowsHiLoBf16 {
+    static constexpr int CPR = TL::BK / 8;
+    static constexpr int NCH = TL::ROWS * CPR / NT;
+    static_assert(NCH * NT == TL::ROWS * CPR, "threads must divide the tile's chunks");
+    PlainRows pol;   // ld_bytes = 4 K
+    int64_t K;
+    struct State {
+        const char *rp[NCH];
+        bool rok[NCH];
+        int lr[NCH], lq[NCH];
+        u32x4 reg[NCH][2];
+    };
+    __device__ __forceinline__ void init(State &st, int64_t row0) const {
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const int chunk = threadIdx.x + c * NT;
+            st.lr[c] = chunk / CPR;
+            st.lq[c] = chunk % CPR;
+            st.rok[c] = row0 + st.lr[c] < pol.rows;
+            st.rp[c] = pol.row(row0 + st.lr[c]);
+        }
+    }
+    __device__ __forceinline__ void load(State &st, int64_t k0, int64_t kend) const {
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const int64_t k = k0 + st.lq[c] * 8;
+            const bool ok = st.rok[c] && k < K && k < kend;
+            const char *p = ok ? st.rp[c] + k * 2 : (const char *)g_zero16;
+            const int64_t lo = ok ? K * 2 : 0;
+            st.reg[c][0] = *(const u32x4 *)p;
+            st.reg[c][1] = *(const u32x4 *)(p + lo);
+        }
+    }
+    __device__ __forceinline__ void store(const State &st, char *lds) const {
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            char *d = lds + st.lr[c] * TL::PITCH + st.lq[c] * 16;
+            *(u32x4 *)d = st.reg[c][0];
+            *(u32x4 *)(d + LO_OFF) = st.reg[c][1];
+        }
+    }
+};
+
 // fp32 weight side: 16 k x (ROWS / 4) chunks of 4 columns, transposed by scalar LDS writes
 // (used only in fp32 mode).
 template <int NT>
@@ -953,7 +1000,10 @@ __device__ __forceinline__ void dw_raw_frag(const char *tile, int row0, int col,
 // parts in registers.  32 x 32 x 16 MFMA tiles (see the input-side core): the 16-lane
 // group g of a fragment read takes columns 16 (g % 2) .. of the 32 and rows 8 (g / 2) ..
 // of the 16-row K sub-step.
-template <class C, int BK, int S, int MINW>
+// HILO: dY rows come in the hi/lo form (d_out bf16 high parts, then d_out low parts): the
+// hi and lo tiles are loaded like the Mcat tile and read by the same transpose reads, with
+// no split in registers.
+template <class C, int BK, int S, int MINW, bool HILO>
 __global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw(const char *__restrict__ mcat, int64_t M,
                                                     int64_t Kcat, const float *__restrict__ dy,
                                                     int64_t d_out, int64_t tiles_m,
@@ -961,11 +1011,15 @@ __global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw(const char *__restrict_
                                                     const EpiPartial epi) {
     using Ga = DwGeom<BK, C::TM>;
     using Gb = DwRawGeom<BK, C::TN>;
+    using Gh = DwGeom<BK, C::TN>;                  // HILO: each of the hi and lo tiles
     constexpr int FM = C::FM, FN = C::FN, NW = C::NT / 64;
-    constexpr int STAGE = Ga::TILE + Gb::TILE;
-    constexpr int IA = BK / Ga::RPI / NW, IB = BK / Gb::RPI / NW;   // loads per wave per step
-    static_assert(IA * Ga::RPI * NW == BK && IB * Gb::RPI * NW == BK, "whole instructions");
-    constexpr int LPS = IA + IB;
+    constexpr int B_TILE = HILO ? 2 * Gh::TILE : Gb::TILE;
+    constexpr int STAGE = Ga::TILE + B_TILE;
+    constexpr int IA = BK / Ga::RPI / NW;
+    constexpr int IB = HILO ? BK / Gh::RPI / NW : BK / Gb::RPI / NW;   // per B tile
+    static_assert(IA * Ga::RPI * NW == BK, "whole instructions");
+    static_assert(HILO ? IB * Gh::RPI * NW == BK : IB * Gb::RPI * NW == BK, "whole instructions");
+    constexpr int LPS = IA + (HILO ? 2 : 1) * IB;
     static_assert(S >= 2 && (S - 2) * LPS < 64, "vmcnt range");
     __shared__ __attribute__((aligned(1024))) char lds[S * STAGE];
     static_assert(S * STAGE >= NW * 16 * kStagePitch * 4, "epilogue staging space");
@@ -997,12 +1051,24 @@ __global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw(const char *__restrict_
             const char *g = (m < ke && col < Kcat) ? mcat + m * Kcat * 2 + col * 2 : zp;
             lds_dma16(g, st + (wave * IA + j) * 1024);
         }
+        if constexpr (HILO) {
 #pragma unroll
-        for (int j = 0; j < IB; ++j) {
-            const int r = (wave * IB + j) * Gb::RPI + lane / Gb::CPR;
-            const int64_t m = m0 + r, col = o0 + Gb::slot(r, lane % Gb::CPR) * 4;
-            const char *g = (m < ke && col < d_out) ? (const char *)(dy + m * d_out + col) : zp;
-            lds_dma16(g, st + Ga::TILE + (wave * IB + j) * 1024);
+            for (int j = 0; j < IB; ++j) {
+                const int r = (wave * IB + j) * Gh::RPI + lane / Gh::CPR;
+                const int64_t m = m0 + r, col = o0 + Gh::slot(r, lane % Gh::CPR) * 8;
+                const bool ok = m < ke && col < d_out;
+                const char *row = (const char *)dy + m * d_out * 4 + col * 2;
+                lds_dma16(ok ? row : zp, st + Ga::TILE + (wave * IB + j) * 1024);
+                lds_dma16(ok ? row + d_out * 2 : zp, st + Ga::TILE + Gh::TILE + (wave * IB + j) * 1024);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < IB; ++j) {
+                const int r = (wave * IB + j) * Gb::RPI + lane / Gb::CPR;
+                const int64_t m = m0 + r, col = o0 + Gb::slot(r, lane % Gb::CPR) * 4;
+                const char *g = (m < ke && col < d_out) ? (const char *)(dy + m * d_out + col) : zp;
+                lds_dma16(g, st + Ga::TILE + (wave * IB + j) * 1024);
+            }
         }
     };
 
@@ -1032,16 +1098,32 @@ __global__ __launch_bounds__(C::NT, MINW) void k_gemm_dw(const char *__restrict_
 #pragma unroll
         for (int s = 0; s < BK / 16; ++s) {
             bf16x8 bh[AN], bl[AN];
+            if constexpr (HILO) {
 #pragma unroll
-            for (int ni = 0; ni < AN; ++ni)
-                dw_raw_frag<Gb>(Bs, s * 16 + 8 * (lane >> 5), wn * FN * 16 + ni * 32 + (lane & 31),
-                                bh[ni], bl[ni]);
+                for (int ni = 0; ni < AN; ++ni) {
+                    bh[ni] = dw_frag_untracked<Gh>(Bs, s * 16 + gr, wn * FN * 16 + ni * 32 + gc, j16);
+                    bl[ni] = dw_frag_untracked<Gh>(Bs + Gh::TILE, s * 16 + gr,
+                                                   wn * FN * 16 + ni * 32 + gc, j16);
+                }
+            } else {
+#pragma unroll
+                for (int ni = 0; ni < AN; ++ni)
+                    dw_raw_frag<Gb>(Bs, s * 16 + 8 * (lane >> 5),
+                                    wn * FN * 16 + ni * 32 + (lane & 31), bh[ni], bl[ni]);
+            }
             bf16x8 av[AM];
 #pragma unroll
             for (int mi = 0; mi < AM; ++mi)
                 av[mi] = dw_frag_untracked<Ga>(As, s * 16 + gr, wm * FM * 16 + mi * 32 + gc, j16);
 #pragma unroll
             for (int mi = 0; mi < AM; ++mi) lds_reads_done(av[mi]);
+            if constexpr (HILO) {
+#pragma unroll
+                for (int ni = 0; ni < AN; ++ni) {
+                    lds_reads_done(bh[ni]);
+                    lds_reads_done(bl[ni]);
+                }
+            }
 #pragma unroll
             for (int mi = 0; mi < AM; ++mi) {
 #pragma unroll
@@ -1116,7 +1198,8 @@ struct DmsStream {
     int32_t N;
     int32_t d_in;
 };
-template <int S, int NB>
+// HILO: dY rows in the hi/lo form; the loads fetch the bf16 parts as they are.
+template <int S, int NB, bool HILO>
 __global__ __launch_bounds__(kDmsStreamWaves * 64, 1) void k_dms_stream(
     const float *__restrict__ dy, int64_t M, const DmsStream p) {
     constexpr int KW = 32 * S;                       // K values per wave
@@ -1162,10 +1245,21 @@ __global__ __launch_bounds__(kDmsStreamWaves * 64, 1) void k_dms_stream(
         const int64_t m0 = ((int64_t)blockIdx.x + (int64_t)(live ? bi : 0) * P) * 16;
         const int64_t m = m0 + r16;
         const bool ok = live && m < M;
-        const float *src = ok ? dy + m * D + wave * KW + q * 8 : zp;
-        const int st = ok ? 1 : 0;
+        if constexpr (HILO) {
+            // step s: the high parts of the 8 values in v[2 s], the low parts in v[2 s + 1]
+            const char *src = ok ? (const char *)dy + m * D * 4 + (wave * KW + q * 8) * 2
+                                 : (const char *)zp;
+            const int st = ok ? 1 : 0;
 #pragma unroll
-        for (int i = 0; i < 2 * S; ++i) b.v[i] = *(const f32x4 *)(src + (32 * (i / 2) + 4 * (i % 2)) * st);
+            for (int i = 0; i < 2 * S; ++i)
+                b.v[i] = *(const f32x4 *)(src + (64 * (i / 2) + D * 2 * (i % 2)) * st);
+        } else {
+            const float *src = ok ? dy + m * D + wave * KW + q * 8 : zp;
+            const int st = ok ? 1 : 0;
+#pragma unroll
+            for (int i = 0; i < 2 * S; ++i)
+                b.v[i] = *(const f32x4 *)(src + (32 * (i / 2) + 4 * (i % 2)) * st);
+        }
         const int64_t mr = m0 + rr;
         const int32_t *d = (live && ipc != nullptr && mr < M) ? ipc + mr : (const int32_t *)zp;
         b.i0 = d[0];
@@ -1186,14 +1280,19 @@ __global__ __launch_bounds__(kDmsStreamWaves * 64, 1) void k_dms_stream(
             for (int s = 0; s < S; ++s) {
                 const f32x4 a = bufs[b].v[2 * s], c = bufs[b].v[2 * s + 1];
                 u32x4 hv, lv;
-                hv.x = pack_bf16x2(a.x, a.y);
-                hv.y = pack_bf16x2(a.z, a.w);
-                hv.z = pack_bf16x2(c.x, c.y);
-                hv.w = pack_bf16x2(c.z, c.w);
-                lv.x = pack_bf16x2(a.x - bf16_lo(hv.x), a.y - bf16_hi(hv.x));
-                lv.y = pack_bf16x2(a.z - bf16_lo(hv.y), a.w - bf16_hi(hv.y));
-                lv.z = pack_bf16x2(c.x - bf16_lo(hv.z), c.y - bf16_hi(hv.z));
-                lv.w = pack_bf16x2(c.z - bf16_lo(hv.w), c.w - bf16_hi(hv.w));
+                if constexpr (HILO) {
+                    hv = __builtin_bit_cast(u32x4, a);
+                    lv = __builtin_bit_cast(u32x4, c);
+                } else {
+                    hv.x = pack_bf16x2(a.x, a.y);
+                    hv.y = pack_bf16x2(a.z, a.w);
+                    hv.z = pack_bf16x2(c.x, c.y);
+                    hv.w = pack_bf16x2(c.z, c.w);
+                    lv.x = pack_bf16x2(a.x - bf16_lo(hv.x), a.y - bf16_hi(hv.x));
+                    lv.y = pack_bf16x2(a.z - bf16_lo(hv.y), a.w - bf16_hi(hv.y));
+                    lv.z = pack_bf16x2(c.x - bf16_lo(hv.z), c.y - bf16_hi(hv.z));
+                    lv.w = pack_bf16x2(c.z - bf16_lo(hv.w), c.w - bf16_hi(hv.w));
+                }
                 const bf16x8 bh = __builtin_bit_cast(bf16x8, hv), bl = __builtin_bit_cast(bf16x8, lv);
 #pragma unroll
                 for (int t = 0; t < 8; ++t) {
@@ -1339,8 +1438,8 @@ hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
         la, lb, EpiForward<false>{y, bias, M, N, relu, rm}, M, N, K, 1, K, s);
 }
 
-hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_in,
-                    const DmsSlots &slots, float *dms, hipStream_t s) {
+hipError_t gemm_dms(rgcn_dtype dt, const float *dy, bool dy_hilo, int64_t M, int d_out,
+                    int d_in, const DmsSlots &slots, float *dms, hipStream_t s) {
     const int es = dt == RGCN_BF16 ? 2 : 4;
     const int64_t N = (int64_t)slots.count * d_in;
     SlotRows sr;
@@ -1371,12 +1470,20 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_
         const int64_t cus = device_cus();
         if (P > cus) P = cus;
         // register blocks in flight per wave: as many as fit beside the weights
+#define RGCN_DMS_STREAM(S_, NB_)                                                             \
+    do {                                                                                     \
+        if (dy_hilo)                                                                         \
+            hipLaunchKernelGGL((k_dms_stream<S_, NB_, true>), dim3((unsigned)P),             \
+                               dim3(kDmsStreamWaves * 64), 0, s, dy, M, ps);                 \
+        else                                                                                 \
+            hipLaunchKernelGGL((k_dms_stream<S_, NB_, false>), dim3((unsigned)P),            \
+                               dim3(kDmsStreamWaves * 64), 0, s, dy, M, ps);                 \
+    } while (0)
         if (d_out == 512)
-            hipLaunchKernelGGL((k_dms_stream<2, 5>), dim3((unsigned)P), dim3(kDmsStreamWaves * 64),
-                               0, s, dy, M, ps);
+            RGCN_DMS_STREAM(2, 5);
         else
-            hipLaunchKernelGGL((k_dms_stream<1, 8>), dim3((unsigned)P), dim3(kDmsStreamWaves * 64),
-                               0, s, dy, M, ps);
+            RGCN_DMS_STREAM(1, 8);
+#undef RGCN_DMS_STREAM
         return hipGetLastError();
     }
     if (dt == RGCN_BF16) {
@@ -1384,9 +1491,14 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, int64_t M, int d_out, int d_
         // fragment meets both
         using C = CfgDms;
         using TL = TileBf16<C>;
-        LoadRowsF32HiLo<TL, C::NT, 2 * TL::BYTES> la{pa, d_out};
         LoadRows<TL, C::NT, SlotRows> lb{sr, (int64_t)d_out * 2};
         using Core = MmaBf16SplitA32<TL, C::FM, C::FN>;
+        if (dy_hilo) {
+            LoadRowsHiLoBf16<TL, C::NT, 2 * TL::BYTES> la{pa, d_out};
+            return launch_gemm<C, Core, decltype(la), decltype(lb), EpiDms, kDmsStages,
+                               kDmsRegStages>(la, lb, epi, M, N, d_out, 1, d_out, s);
+        }
+        LoadRowsF32HiLo<TL, C::NT, 2 * TL::BYTES> la{pa, d_out};
         return launch_gemm<C, Core, decltype(la), decltype(lb), EpiDms, kDmsStages,
                            kDmsRegStages>(la, lb, epi, M, N, d_out, 1, d_out, s);
     }
@@ -1407,7 +1519,7 @@ size_t gemm_dw_partial_bytes(int64_t M, int Kcat, int d_out) {
 }
 
 hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_in,
-                   const float *dy, int d_out, const DwOut &out, float *partial,
+                   const float *dy, bool dy_hilo, int d_out, const DwOut &out, float *partial,
                    hipStream_t s) {
     const bool bf = dt == RGCN_BF16;
     int64_t splits, per;
@@ -1424,10 +1536,16 @@ hipError_t gemm_dw(rgcn_dtype dt, const void *mcat, int64_t M, int Kcat, int d_i
     if (bf) {
         using C = CfgDw;
         const int64_t tiles_m = cdiv(Kcat, C::TM), tiles_n = cdiv(d_out, C::TN);
-        hipLaunchKernelGGL((k_gemm_dw<C, kDwBK, kDwStages, kDwMinWaves>),
-                           dim3((unsigned)(tiles_m * tiles_n * splits)),
-                           dim3(C::NT), 0, s, (const char *)mcat, M, (int64_t)Kcat, dy,
-                           (int64_t)d_out, tiles_m, tiles_n, per, epi);
+        if (dy_hilo)
+            hipLaunchKernelGGL((k_gemm_dw<C, kDwBK, kDwStages, kDwMinWaves, true>),
+                               dim3((unsigned)(tiles_m * tiles_n * splits)),
+                               dim3(C::NT), 0, s, (const char *)mcat, M, (int64_t)Kcat, dy,
+                               (int64_t)d_out, tiles_m, tiles_n, per, epi);
+        else
+            hipLaunchKernelGGL((k_gemm_dw<C, kDwBK, kDwStages, kDwMinWaves, false>),
+                               dim3((unsigned)(tiles_m * tiles_n * splits)),
+                               dim3(C::NT), 0, s, (const char *)mcat, M, (int64_t)Kcat, dy,
+                               (int64_t)d_out, tiles_m, tiles_n, per, epi);
         RGCN_HIP_TRY(hipGetLastError());
     } else {
         using C = CfgF32;

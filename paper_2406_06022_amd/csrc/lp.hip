@@ -586,7 +586,7 @@ hipError_t lp_loss(const LpArgs &a, const LpLayout &L, char *ws, float *loss, fl
     if (a.batch == 0) {
         const uint32_t zero = 0;
         RGCN_HIP_TRY(fill_words(loss, &zero, 4, s));
-        if (d_rel) RGCN_HIP_TRY(column_sums(nullptr, 0, a.d, d_rel, nullptr, 0, s));
+        if (d_rel) RGCN_HIP_TRY(column_sums(nullptr, false, 0, a.d, d_rel, nullptr, 0, s));
         return hipSuccess;
     }
     // (1) scores: u_i and the positives; per edge also the negatives

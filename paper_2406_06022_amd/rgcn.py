@@ -30,6 +30,8 @@ RGCN_CLEAR_GRAD = 0x10
 RGCN_PLAN_FORWARD = 0x20
 RGCN_PLAN_BACKWARD = 0x40
 RGCN_PLAN_ENUMERATION_ORDER = 0x80
+RGCN_DY_HILO = 0x100
+RGCN_DH_HILO = 0x200
 STATUS_NAMES = {0: "RGCN_OK", 1: "RGCN_ERR_INVALID_ARG", 2: "RGCN_ERR_SHAPE",
                 3: "RGCN_ERR_DTYPE", 4: "RGCN_ERR_INDEX_OOB", 5: "RGCN_ERR_BAD_CSR",
                 6: "RGCN_ERR_WORKSPACE_TOO_SMALL", 7: "RGCN_ERR_UNSUPPORTED", 8: "RGCN_ERR_HIP"}

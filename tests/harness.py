@@ -33,6 +33,22 @@ def rel_err(got, want) -> float:
     return float(np.max(np.abs(got - want) / den))
 
 
+def hilo_split(x: torch.Tensor) -> torch.Tensor:
+    """fp32 rows [n, d] in the library's hi/lo form: per row the d bf16 values hi = bf16(x)
+    then the d values lo = bf16(x - hi), both rounded to nearest even (x - hi is exact in
+    fp32), viewed as fp32 [n, d] (the same bytes per row)."""
+    hi = x.to(torch.bfloat16)
+    lo = (x - hi.to(torch.float32)).to(torch.bfloat16)
+    return torch.cat([hi, lo], dim=1).contiguous().view(torch.float32)
+
+
+def hilo_decode(x: torch.Tensor) -> np.ndarray:
+    """hi + lo in fp64 of rows in the hi/lo form."""
+    d = x.shape[1]
+    b = x.detach().to("cpu").contiguous().view(torch.bfloat16).to(torch.float64)
+    return (b[:, :d] + b[:, d:]).numpy()
+
+
 def sign_words(t: torch.Tensor) -> torch.Tensor:
     """ReLU sign bits of a [rows x d] table as the library lays them out: int64 words
     [rows x ceil(d / 64)], bit c % 64 of word c / 64 set where element c is positive."""
@@ -132,7 +148,10 @@ class BlockRun:
         # NaN in fp32 and bf16)
         self.ws.fill_(0xFF)
 
-    def run_gpu(self, validate: bool = False, repeat: int = 1, plan_flags: int = 0):
+    def run_gpu(self, validate: bool = False, repeat: int = 1, plan_flags: int = 0,
+                hilo_flags: int = 0):
+        """hilo_flags: RGCN_DY_HILO passes dy in the hi/lo form; RGCN_DH_HILO has dh written
+        in it (returned as stored)."""
         dev = self.device
         blk = self.blk
         T = len(blk.n_src)
@@ -144,7 +163,8 @@ class BlockRun:
         for _ in range(repeat):
             y = [torch.full((n, self.d_out), float("nan"), dtype=tdt, device=dev) if n > 0 else None
                  for n in blk.n_dst]
-            dy = [x.to(dev) for x in self.dy]
+            dy = [(hilo_split(x) if hilo_flags & rgcn.RGCN_DY_HILO else x).to(dev)
+                  for x in self.dy]
             dw_rel = [torch.full((self.d_in, self.d_out), float("nan"), dtype=f32, device=dev)
                       for _ in blk.rels]
             dw_self = [torch.full((self.d_in, self.d_out), float("nan"), dtype=f32, device=dev)
@@ -165,7 +185,7 @@ class BlockRun:
                                     relu_mask=ym)
             rgcn.rgcn_block_backward(self.dblk, self.inputs, self.params, dy, dw_rel, dw_self,
                                      dbias, dh, demb if self.emb_types else None, self.ws,
-                                     flags | self.flags_bwd)
+                                     flags | self.flags_bwd | hilo_flags)
             torch.cuda.synchronize()
             outs.append({"y": [x.cpu() if x is not None else None for x in y],
                          "dw_rel": [x.cpu() for x in dw_rel],
