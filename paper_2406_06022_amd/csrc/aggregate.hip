@@ -1024,16 +1024,30 @@ __global__ __launch_bounds__(kThreads) void k_transpose_pipe_adagrad(TsumArgs a,
 struct WSlots {
     const void *w[kMaxSlots];
 };
+// The slots stacked as one [K x d_out] matrix (row kk = s d_in + c) are transposed in
+// 64 x 64 tiles through LDS: a tile's rows are read along n and written along kk, so both
+// sides are whole contiguous pieces; the padded LDS row keeps the column reads off one
+// bank.
+constexpr int kPackTile = 64;
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_pack_weights(WSlots ws, int nslots, int d_in,
                                                            int d_out, T *out) {
-    const int64_t K = (int64_t)nslots * d_in;
-    const int64_t total = K * d_out;
-    for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < total;
-         e += (int64_t)gridDim.x * kThreads) {
-        const int64_t n = e / K, kk = e - n * K;
-        const int64_t s = kk / d_in, c = kk - s * d_in;
-        out[e] = ((const T *)ws.w[s])[c * d_out + n];
+    __shared__ T tile[kPackTile][kPackTile + 1];
+    const int K = nslots * d_in;
+    const int kk0 = blockIdx.x * kPackTile, n0 = blockIdx.y * kPackTile;
+    const int tx = threadIdx.x % kPackTile, ty = threadIdx.x / kPackTile;
+    constexpr int kRowsPerPass = kThreads / kPackTile;
+    for (int r = ty; r < kPackTile; r += kRowsPerPass) {
+        const int kk = kk0 + r, n = n0 + tx;
+        if (kk < K && n < d_out) {
+            const int sl = kk / d_in, c = kk - sl * d_in;
+            tile[r][tx] = ((const T *)ws.w[sl])[(int64_t)c * d_out + n];
+        }
+    }
+    __syncthreads();
+    for (int r = ty; r < kPackTile; r += kRowsPerPass) {
+        const int n = n0 + r, kk = kk0 + tx;
+        if (n < d_out && kk < K) out[(int64_t)n * K + kk] = tile[tx][r];
     }
 }
 
@@ -1292,15 +1306,15 @@ hipError_t pack_weights(rgcn_dtype dt, int d_in, int d_out, const void *const *w
                         int nslots, void *wcat_t, hipStream_t s) {
     WSlots ws;
     for (int i = 0; i < kMaxSlots; ++i) ws.w[i] = i < nslots ? w_slots[i] : nullptr;
-    const int64_t total = (int64_t)nslots * d_in * d_out;
-    if (total == 0) return hipSuccess;
-    const int64_t blocks = cdiv(total, kThreads) < 65536 ? cdiv(total, kThreads) : 65536;
+    const int64_t K = (int64_t)nslots * d_in;
+    if (K == 0 || d_out == 0) return hipSuccess;
+    const dim3 grid((unsigned)cdiv(K, kPackTile), (unsigned)cdiv(d_out, kPackTile));
     if (dt == RGCN_BF16)
-        hipLaunchKernelGGL(k_pack_weights<uint16_t>, dim3((unsigned)blocks), dim3(kThreads), 0,
-                           s, ws, nslots, d_in, d_out, (uint16_t *)wcat_t);
+        hipLaunchKernelGGL(k_pack_weights<uint16_t>, grid, dim3(kThreads), 0, s, ws, nslots, d_in,
+                           d_out, (uint16_t *)wcat_t);
     else
-        hipLaunchKernelGGL(k_pack_weights<float>, dim3((unsigned)blocks), dim3(kThreads), 0, s,
-                           ws, nslots, d_in, d_out, (float *)wcat_t);
+        hipLaunchKernelGGL(k_pack_weights<float>, grid, dim3(kThreads), 0, s, ws, nslots, d_in,
+                           d_out, (float *)wcat_t);
     return hipGetLastError();
 }
 
