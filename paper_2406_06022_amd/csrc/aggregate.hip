@@ -655,11 +655,16 @@ __device__ __forceinline__ void transpose_sum_body(const TsumArgs &a, int G, int
 // rows are too.  Edges past the group width are resolved in place.  Every load is
 // unconditional (unused lanes read a zero word).
 
+// PF (one chunk per lane): a fourth stage loads the first edge's dMs row of the next row
+// while the current one is summed, so each wave has two rows' reads in flight instead of
+// one.  (At two chunks per lane, where sources of a hidden block mostly have one edge, it
+// measured slower: the registers of the extra stage cost a wave per SIMD.)
 template <bool BF16IN, int CPL, bool OPT, bool MASK>
 __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, int gpw,
                                                     int chunks) {
     constexpr int HES = BF16IN ? 2 : 4;
     constexpr int U = 4;   // rows in flight per lane
+    constexpr bool PF = CPL == 1;
     constexpr int W = kThreads / 64;
     __shared__ TsumRel s_rel[kMaxRels];
     __shared__ int64_t s_off[W][64];
@@ -689,6 +694,7 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
         bool split;     // more than kSplitEdges edges: the piece kernels sum this row
         f32x4 old[CPL], self[CPL], hm[CPL];
         uint32_t hb[CPL];   // MASK: the 4 sign bits of each chunk (hm unused)
+        f32x4 pre[CPL];     // PF: the first edge's dMs row (zero if the row has no edge)
     };
     // stage 1: source row at schedule position q (-1 past the end)
     auto s1 = [&](int64_t q) -> int32_t {
@@ -775,11 +781,26 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
     };
     // rows [0, n) whose addresses are in goff, added into acc; a batch's unused slots re-read
     // the last row and are dropped
-    auto rows = [&](int n, f32x4 (&acc)[CPL]) {
-        row_walk<U>(goff, n, SumLoad<CPL, false>{lg, G, chunks, acc, nullptr});
+    auto rows = [&](const int64_t *go, int n, f32x4 (&acc)[CPL]) {
+        row_walk<U>(go, n, SumLoad<CPL, false>{lg, G, chunks, acc, nullptr});
     };
     auto edge_addr = [&](int r, int32_t i) -> int64_t {
         return (int64_t)(uintptr_t)(s_rel[r].dms + (int64_t)i * s_rel[r].dms_ld);
+    };
+    // stage 4 (PF): edge 0 of the row is held by the group's first lane
+    auto s4 = [&](Row &rw) {
+        const int er0 = __shfl(rw.er, g0, 64);
+        const int32_t ei0 = __shfl(rw.ei, g0, 64);
+        const bool okp = rw.total > 0;
+        const char *base = okp ? (const char *)(uintptr_t)edge_addr(er0, ei0)
+                               : (const char *)g_zero_row;
+#pragma unroll
+        for (int p = 0; p < CPL; ++p) {
+            const int c = lg + p * G;
+            const char *pa = (okp && c < chunks) ? base + (int64_t)c * 16
+                                                 : (const char *)g_zero_row + c * 16;
+            rw.pre[p] = *gbl((const f32x4 *)pa);
+        }
     };
     // last step of a row: its dMs rows, the mask, the stores
     auto finish = [&](const Row &rw) {
@@ -789,7 +810,15 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
         const int n1 = rw.total < G ? rw.total : G;
         goff[lg] = edge_addr(rw.er, rw.ei);
         __builtin_amdgcn_wave_barrier();
-        rows(n1, acc);
+        if constexpr (PF) {
+            if (rw.total > 0) {
+#pragma unroll
+                for (int p = 0; p < CPL; ++p) acc[p] += rw.pre[p];
+            }
+            rows(goff + 1, n1 > 1 ? n1 - 1 : 0, acc);
+        } else {
+            rows(goff, n1, acc);
+        }
         for (int ec = G; ec < rw.total; ec += G) {
             int ridx, pos;
             locate(rw.m, ec + lg, ridx, pos);
@@ -798,7 +827,7 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
             __builtin_amdgcn_wave_barrier();
             goff[lg] = edge_addr(ridx, i);
             __builtin_amdgcn_wave_barrier();
-            rows(rw.total - ec < G ? rw.total - ec : G, acc);
+            rows(goff, rw.total - ec < G ? rw.total - ec : G, acc);
         }
         __builtin_amdgcn_wave_barrier();
         if (rw.split) return;
@@ -819,23 +848,48 @@ __device__ __forceinline__ void transpose_pipe_body(const TsumArgs &a, int G, in
         }
     };
 
-    // pipeline prologue: row g through stage 3, row g+stride through stage 2, row
-    // g+2*stride through stage 1
-    Row cur;
-    s3(s2(s1(g)), cur);
-    Meta mn = s2(s1(g + stride));
-    int32_t jnn = s1(g + 2 * stride);
-    while (true) {
-        Row nxt;
-        s3(mn, nxt);
-        const Meta mnn = s2(jnn);
-        const int32_t jn3 = s1(g + 3 * stride);
-        finish(cur);
-        g += stride;
-        if (g >= a.n_rows) break;
-        cur = nxt;
-        mn = mnn;
-        jnn = jn3;
+    if constexpr (PF) {
+        // prologue: row g through stage 4, g+stride through stage 3, g+2 stride through
+        // stage 2, g+3 stride through stage 1
+        Row cur, nxt;
+        s3(s2(s1(g)), cur);
+        s4(cur);
+        s3(s2(s1(g + stride)), nxt);
+        Meta mn = s2(s1(g + 2 * stride));
+        int32_t jnn = s1(g + 3 * stride);
+        while (true) {
+            Row nn;
+            s3(mn, nn);
+            const Meta mnn = s2(jnn);
+            const int32_t jn4 = s1(g + 4 * stride);
+            s4(nxt);
+            finish(cur);
+            g += stride;
+            if (g >= a.n_rows) break;
+            cur = nxt;
+            nxt = nn;
+            mn = mnn;
+            jnn = jn4;
+        }
+    } else {
+        // prologue: row g through stage 3, row g+stride through stage 2, row g+2*stride
+        // through stage 1
+        Row cur;
+        s3(s2(s1(g)), cur);
+        Meta mn = s2(s1(g + stride));
+        int32_t jnn = s1(g + 2 * stride);
+        while (true) {
+            Row nxt;
+            s3(mn, nxt);
+            const Meta mnn = s2(jnn);
+            const int32_t jn3 = s1(g + 3 * stride);
+            finish(cur);
+            g += stride;
+            if (g >= a.n_rows) break;
+            cur = nxt;
+            mn = mnn;
+            jnn = jn3;
+        }
     }
 }
 
