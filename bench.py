@@ -480,7 +480,9 @@ def summarize_counters(args) -> str:
                     continue
                 if not lo <= float(r["Start_Timestamp"]) < hi:
                     continue
-                names.setdefault(pat, _short_name(r["Kernel_Name"]))
+                nm = _short_name(r["Kernel_Name"])
+                if nm not in names.setdefault(pat, []):
+                    names[pat].append(nm)
                 by_counter.setdefault(r["Counter_Name"], {}).setdefault(
                     int(r["Dispatch_Id"]), 0.0)
                 by_counter[r["Counter_Name"]][int(r["Dispatch_Id"])] += float(r["Counter_Value"])
@@ -492,7 +494,8 @@ def summarize_counters(args) -> str:
              args.command, "```", "",
              "Per-dispatch averages over the launches of the timed, eagerly launched steps "
              "(between the first gather launch of the first timed step and the gather launch "
-             "after the last step), all blocks and node types of a step together.  Derived: `gpu_cycles` = GRBM_GUI_ACTIVE / 8 (the counter "
+             "after the last step), all blocks and node types of a step together, every form "
+             "(template instance) of the kernel listed under its heading pooled.  Derived: `gpu_cycles` = GRBM_GUI_ACTIVE / 8 (the counter "
              "reads the sum over the 8 XCDs: 8x the kernel's cycles at the clock the trace "
              "durations imply); `mfma_busy` = SQ_VALU_MFMA_BUSY_CYCLES / (gpu_cycles x 256 "
              "CUs x 4 SIMDs); `valu_per_mfma` = SQ_INSTS_VALU / "
@@ -515,8 +518,11 @@ def summarize_counters(args) -> str:
             w_scale = COPY_BYTES / (sum(cw) / len(cw) * 1024.0)
     for pat in pats:
         c = per.get(pat, {})
-        lines.append(f"## `{names.get(pat, pat)}`")
+        forms = names.get(pat, [pat])
+        lines.append(f"## `{pat}`" + (f" ({len(forms)} forms)" if len(forms) > 1 else ""))
         lines.append("")
+        for nm in forms:
+            lines.append(f"- form: `{nm}`")
         for cn in sorted(c):
             lines.append(f"- {cn}: {c[cn]:.6g}")
         der = {}
