@@ -695,8 +695,11 @@ rgcn_status rgcn_block_backward_dense(const rgcn_block *block, const rgcn_params
                     ds.w[L.dms_rel[r]] = params->w_rel[r];
                     ds.indptr[L.dms_rel[r]] = block->rels[r].indptr;
                 }
+            // the packed forward weights of the type are not read again before the next
+            // transform packs them anew: their space holds the input side's weight rows
             TRY_HIP(gemm_dms(L.dt, dy[t], hilo, nd, L.d_out, L.d_in, ds,
-                             (float *)(scratch + L.off_dms[t]), stream), "input-side transform");
+                             (float *)(scratch + L.off_dms[t]), ws + L.off_wcat[t], stream),
+                    "input-side transform");
         }
     }
     return RGCN_OK;

@@ -333,8 +333,10 @@ struct DmsSlots {
     const void *w[kMaxSlots];
     const int32_t *indptr[kMaxSlots];
 };
+// wpack: device space for N x d_out block-dtype values (the input side's weight rows,
+// packed when dy is in the hi/lo form), or NULL
 hipError_t gemm_dms(rgcn_dtype dt, const float *dy, bool dy_hilo, int64_t M, int d_out,
-                    int d_in, const DmsSlots &slots, float *dms, hipStream_t s);
+                    int d_in, const DmsSlots &slots, float *dms, void *wpack, hipStream_t s);
 // Weight side: dWcat[kc][o] = sum_i Mcat[i][kc] dy[i][o], K = rows of Mcat.
 size_t gemm_dw_partial_bytes(int64_t M, int Kcat, int d_out);
 struct DwOut {

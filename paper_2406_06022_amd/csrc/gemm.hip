@@ -452,6 +452,7 @@ struct EpiForward {
 // The forward epilogue of the persistent kernel: 4 consecutive columns of one row per call,
 // their bias loaded only when there is one.
 struct EpiForwardBf16 {
+    static constexpr bool kDms = false;
     void *y;
     const void *bias;    // bf16 [N] or NULL
     int64_t M;
@@ -492,6 +493,23 @@ struct EpiForwardBf16 {
     __device__ __forceinline__ void store8(int64_t m, int64_t n, uint4 v) const {
         if (m < M && n < N) *(uint4 *)((uint16_t *)y + m * N + n) = v;
     }
+};
+
+// The input-side product dMs = dY W^T / deg in k_gemm_fwd, with dY in the hi/lo form: a
+// row of d_out hi then d_out lo bf16 values is a bf16 row of K = 2 d_out, and the weight
+// rows (packed [N x d_out]) serve K index k and k + d_out alike (kwrap = d_out), so each
+// weight meets hi and lo.  fp32 output, divided by the degree of the row's segment in the
+// column's slot (0 for an empty segment, as is for the self slot).  d_in is a multiple of
+// 64, so a wave's 64 columns lie in one slot; inv_din = ceil(2^32 / d_in) gives the slot
+// of a column as umulhi(n, inv_din) (exact for n < 2^21).
+struct EpiDmsFwd {
+    static constexpr bool kDms = true;
+    float *out;
+    int64_t M;
+    int32_t N;
+    int32_t kwrap;
+    uint32_t inv_din;
+    const int32_t *indptr[kMaxSlots];
 };
 
 // dMs rows divided by the segment's degree.  The degrees a lane's epilogue needs are read
@@ -747,11 +765,10 @@ __device__ __forceinline__ void vm_wait_barrier() {
 // columns of one row: the epilogue stores straight from registers, and LDS holds only the
 // pipeline stages.  Steps past the last tile load zero tiles, so every step issues the
 // same loads; everything lands before a workgroup exits.
-template <class C, int BK, int S>
+template <class C, int BK, int S, class E>
 __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
     const char *__restrict__ a, int64_t lda, int64_t M, const char *__restrict__ b,
-    int64_t ldb, int64_t N, int64_t K, const EpiForwardBf16 epi, int64_t tiles_m,
-    int64_t tiles_n) {
+    int64_t ldb, int64_t N, int64_t K, const E epi, int64_t tiles_m, int64_t tiles_n) {
     using Gm = DlGeom<BK>;
     constexpr int FM = C::FM, FN = C::FN, NW = C::NT / 64;
     constexpr int A_BYTES = C::TM * Gm::RB, B_BYTES = C::TN * Gm::RB;
@@ -811,7 +828,9 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
 #pragma unroll
         for (int j = 0; j < IB; ++j) {
             const int64_t k = k0 + cb[j] * 8, n = in0 + rb[j];
-            const char *g = (live && n < N && k < K) ? b + n * ldb + k * 2 : zp;
+            int64_t kb = k;
+            if constexpr (E::kDms) kb = k < epi.kwrap ? k : k - epi.kwrap;
+            const char *g = (live && n < N && k < K) ? b + n * ldb + kb * 2 : zp;
             lds_dma16(g, st + A_BYTES + (wave * IB + j) * 1024);
         }
         ++gs_issue;
@@ -826,6 +845,7 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
     for (int st = 0; st < S - 1; ++st) issue();
     const int r16 = lane & 15, q = lane >> 4;
     int64_t m0 = 0, n0 = 0, ti = 0, kk = 0;
+    int32_t deg[FM];   // kDms: the degree of each of the lane's rows in the wave's slot
     for (int64_t gs = 0; gs < nsteps; ++gs) {
         if (kk == 0) {
             tile_origin(ti, m0, n0);
@@ -833,6 +853,20 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
             for (int mi = 0; mi < FM; ++mi)
 #pragma unroll
                 for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if constexpr (E::kDms) {
+                // read now, used by this tile's epilogue: -1 where the slot has no segments
+                // (self slot) or the row is outside the output
+                const int64_t nw = n0 + wn * FN * 16;
+                const int sl = nw < N ? (int)__umulhi((uint32_t)nw, epi.inv_din) : 0;
+                const int32_t *ip = nw < N ? epi.indptr[sl] : nullptr;
+#pragma unroll
+                for (int mi = 0; mi < FM; ++mi) {
+                    const int64_t m = m0 + wm * FM * 16 + mi * 16 + r16;
+                    const bool ok = ip != nullptr && m < M;
+                    const int32_t *p = ok ? ip + m : (const int32_t *)zp;
+                    deg[mi] = ok ? p[1] - p[0] : -1;
+                }
+            }
         }
         vm_wait_barrier<(S - 2) * LPS>();
         issue();
@@ -852,7 +886,27 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
                     acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bv[ni], av, acc[mi][ni], 0, 0, 0);
             }
         }
-        if (kk == nk - 1) {
+        if constexpr (E::kDms) {
+            if (kk == nk - 1) {
+                // lane: row m0 + wm FM 16 + 16 mi + (lane % 16), columns n0 + wn FN 16 +
+                // 16 ni + 4 (lane / 16) .. + 3, stored as they are (16 bytes)
+                const int64_t nw = n0 + wn * FN * 16;
+#pragma unroll
+                for (int mi = 0; mi < FM; ++mi) {
+                    const int64_t m = m0 + wm * FM * 16 + mi * 16 + r16;
+                    const bool zero = deg[mi] == 0;
+                    const float scale = deg[mi] > 0 ? (float)deg[mi] : 1.f;
+#pragma unroll
+                    for (int ni = 0; ni < FN; ++ni) {
+                        const int64_t n = nw + 16 * ni + 4 * q;
+                        f32x4 r;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) r[e] = zero ? 0.f : acc[mi][ni][e] / scale;
+                        if (m < M && n < N) *(f32x4 *)(epi.out + m * N + n) = r;
+                    }
+                }
+            }
+        } else if (kk == nk - 1) {
             // lane: row m0 + wm FM 16 + 16 mi + (lane % 16), columns n0 + wn FN 16 + 16 ni +
             // 4 (lane / 16) .. + 3; the wave's 64 columns are one word of the sign mask, of
             // which the lane holds bits 16 ni + 4 (lane / 16) + e, kept packed as bits
@@ -1380,6 +1434,17 @@ __global__ __launch_bounds__(kThreads) void k_zero_outputs(DwOut out, int d_in, 
     if (e < per && out.w[sl]) out.w[sl][e] = 0.f;
 }
 
+// The input side's weight rows stacked as one bf16 [N x d_out] matrix (row s d_in + c =
+// row c of W_s), in 16-byte chunks (cpr per row).
+__global__ __launch_bounds__(kThreads) void k_pack_rows(SlotRows sr, int64_t chunks, int cpr,
+                                                        u32x4 *out) {
+    for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < chunks;
+         e += (int64_t)gridDim.x * kThreads) {
+        const int64_t n = e / cpr, ch = e - n * cpr;
+        out[e] = *(const u32x4 *)(sr.row(n) + ch * 16);
+    }
+}
+
 constexpr int kDwBK = 32;   // rows per K step of the bf16 weight-side kernel
 constexpr int kDwStages = 2;   // LDS stages of k_gemm_dw (three measured 2 % slower)
 // workgroups of one weight-side product: the bf16 kernel holds a CU by itself (96 KB of
@@ -1423,7 +1488,7 @@ hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
         const int64_t cus = device_cus();
         if (P > cus) P = cus;
         P = (P + 7) / 8 * 8;
-        hipLaunchKernelGGL((k_gemm_fwd<C, kFwdBK, kFwdStages>), dim3((unsigned)P),
+        hipLaunchKernelGGL((k_gemm_fwd<C, kFwdBK, kFwdStages, EpiForwardBf16>), dim3((unsigned)P),
                            dim3(C::NT), 0, s, (const char *)a, (int64_t)K * 2, M,
                            (const char *)wcat_t, (int64_t)K * 2, (int64_t)N, (int64_t)K,
                            EpiForwardBf16{y, bias, M, N, relu, rm}, tiles_m, tiles_n);
@@ -1439,7 +1504,7 @@ hipError_t gemm_forward(rgcn_dtype dt, const void *a, int64_t M, int N, int K,
 }
 
 hipError_t gemm_dms(rgcn_dtype dt, const float *dy, bool dy_hilo, int64_t M, int d_out,
-                    int d_in, const DmsSlots &slots, float *dms, hipStream_t s) {
+                    int d_in, const DmsSlots &slots, float *dms, void *wpack, hipStream_t s) {
     const int es = dt == RGCN_BF16 ? 2 : 4;
     const int64_t N = (int64_t)slots.count * d_in;
     SlotRows sr;
@@ -1447,6 +1512,33 @@ hipError_t gemm_dms(rgcn_dtype dt, const float *dy, bool dy_hilo, int64_t M, int
     sr.d_in = d_in;
     sr.es_dout = d_out * es;
     sr.rows = N;
+    if (dt == RGCN_BF16 && dy_hilo && wpack != nullptr && d_in % 64 == 0 && N > kDmsStreamCols) {
+        // the persistent product over the hi/lo rows (K = 2 d_out) and the packed weight rows
+        using C = CfgFwd;
+        const int64_t tiles_m = cdiv(M, C::TM), tiles_n = cdiv(N, C::TN);
+        if (tiles_m == 0) return hipSuccess;
+        const int64_t chunks = N * (d_out / 8);
+        const int64_t pb = cdiv(chunks, kThreads) < 4096 ? cdiv(chunks, kThreads) : 4096;
+        hipLaunchKernelGGL(k_pack_rows, dim3((unsigned)pb), dim3(kThreads), 0, s, sr, chunks,
+                           d_out / 8, (u32x4 *)wpack);
+        RGCN_HIP_TRY(hipGetLastError());
+        EpiDmsFwd e{};
+        e.out = dms;
+        e.M = M;
+        e.N = (int32_t)N;
+        e.kwrap = d_out;
+        e.inv_din = (uint32_t)(((1ull << 32) + (uint64_t)d_in - 1) / (uint64_t)d_in);
+        for (int i = 0; i < kMaxSlots; ++i) e.indptr[i] = i < slots.count ? slots.indptr[i] : nullptr;
+        int64_t P = tiles_m * tiles_n;
+        const int64_t cus = device_cus();
+        if (P > cus) P = cus;
+        P = (P + 7) / 8 * 8;
+        hipLaunchKernelGGL((k_gemm_fwd<C, kFwdBK, kFwdStages, EpiDmsFwd>), dim3((unsigned)P),
+                           dim3(C::NT), 0, s, (const char *)dy, (int64_t)d_out * 4, M,
+                           (const char *)wpack, (int64_t)d_out * 2, N, (int64_t)d_out * 2, e,
+                           tiles_m, tiles_n);
+        return hipGetLastError();
+    }
     EpiDms epi;
     epi.out = dms;
     epi.M = M;

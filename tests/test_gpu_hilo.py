@@ -5,17 +5,22 @@ hi = bf16(g) and lo = bf16(g - hi).  With RGCN_DY_HILO the dense stage reads dy 
 that form (per row d_out high parts, then d_out low parts); with RGCN_DH_HILO the sparse
 stage writes the input gradient in it.  Against the same block run on fp32 gradients:
 
-- y, the weight gradients and the embedding gradients are bit for bit the same (every
-  product sees the same bf16 operands in the same order);
-- dh is bit for bit the host's split of the fp32 result (both round to nearest even);
+- y and the weight gradients are bit for bit the same (the weight-side product sees the
+  same bf16 operands in the same order);
+- the input-side products see the same operands too; where d_in is a multiple of 64 and
+  more than 128 columns take gradients, the hi/lo rows go through the persistent product
+  as one bf16 row of 2 d_out values, so the hi and lo sums are added in another order:
+  embedding gradients agree to the fp32 bar, and dh, decoded, to that plus the form's
+  2^-16 relative representation bound; elsewhere dh is bit for bit the host's split of the
+  fp32 result (both round to nearest even);
 - the bias gradient is the column sum of hi + lo, at the fp32 summation bar against an
   fp64 sum of those values;
 - everything, dh decoded, is at the oracle's bf16 bar.
 
-The cases reach every kernel that reads or writes the form: the register-staged and the
-streamed input-side products (narrow gradient slots at d_out 256 and 512), the weight
-gradient, the bias sums, and the transposed sum at one, two and four chunks per lane, with
-and without the ReLU sign bits, and its split path for hub rows.
+The cases reach every kernel that reads or writes the form: the persistent, the
+register-staged and the streamed input-side products (narrow gradient slots at d_out 256
+and 512), the weight gradient, the bias sums, and the transposed sum at one, two and four
+chunks per lane, with and without the ReLU sign bits, and its split path for hub rows.
 """
 import numpy as np
 import pytest
@@ -27,23 +32,49 @@ from paper_2406_06022_amd import rgcn, synth
 pytestmark = pytest.mark.gpu
 
 HILO = rgcn.RGCN_DY_HILO | rgcn.RGCN_DH_HILO
+# decoded hi/lo rows against the fp32 run: 2^-16 of the form plus fp32 reassociation
+TOL_FORM = 2.5e-5
 
 
 def _bits(x: torch.Tensor) -> torch.Tensor:
     return x.contiguous().view(torch.int16 if x.element_size() == 2 else torch.int32)
 
 
+def _persistent_input_side(run: BlockRun) -> bool:
+    """Whether some destination type's input side takes the persistent product."""
+    blk = run.blk
+    want = set(run.grad_types) | set(run.emb_types)
+    for t in range(len(blk.n_dst)):
+        if blk.n_dst[t] == 0:
+            continue
+        slots = (t in want) + sum(1 for r in blk.rels if r.dst_type == t and r.src_type in want)
+        if run.d_in % 64 == 0 and slots * run.d_in > 128:
+            return True
+    return False
+
+
 def _check_against_fp32_gradients(run: BlockRun) -> None:
     ref = run.run_gpu()[0]
     got = run.run_gpu(hilo_flags=HILO)[0]
-    for key in ("y", "dw_rel", "dw_self", "demb"):
+    exact = not _persistent_input_side(run)
+    for key in ("y", "dw_rel", "dw_self") + (("demb",) if exact else ()):
         for i, (a, b) in enumerate(zip(ref[key], got[key])):
             if a is not None:
                 assert torch.equal(_bits(a), _bits(b)), f"{key}[{i}] differs from the fp32 run"
+    if not exact:
+        for t, a in enumerate(ref["demb"]):
+            if a is not None:
+                err = rel_err(to64(got["demb"][t]), to64(a))
+                assert err <= TOL["f32"], f"demb[{t}]: {err:.3g} against the fp32 run"
     for t, x in enumerate(ref["dh"]):
-        if x is not None:
+        if x is None:
+            continue
+        if exact:
             assert torch.equal(_bits(got["dh"][t]), _bits(hilo_split(x))), \
                 f"dh[{t}] is not the split of the fp32 result"
+        else:
+            err = rel_err(hilo_decode(got["dh"][t]), to64(x))
+            assert err <= TOL_FORM, f"dh[{t}]: {err:.3g} against the fp32 run"
     for t, b in enumerate(got["dbias"]):
         if b is not None:
             want = hilo_decode(hilo_split(run.dy[t])).sum(axis=0)
