@@ -522,18 +522,25 @@ __device__ __forceinline__ int32_t desc_of(const DescArgs &a, int64_t seg, int64
 // segment is heavy (a schedule key other than the last), i.e. when the sorted schedule is
 // not the identity, unless `keep` asks for enumeration order.  Otherwise (gated on that
 // flag): segment order[p].
+// The slot tables are copied into LDS first: the slot search indexes them per lane, which
+// from the kernel arguments is a chain of dependent global loads.
 template <bool IDENT>
 __global__ __launch_bounds__(kThreads) void k_fwd_desc(DescArgs a, int32_t *order,
                                                        int64_t n_seg, SegDesc *desc,
                                                        int32_t *weight, uint32_t *flag, int keep) {
     if (!IDENT && *flag == 0u) return;
+    __shared__ DescArgs s_a;
+    static_assert(sizeof(DescArgs) % 4 == 0, "copied in words");
+    for (int i = threadIdx.x; i < (int)(sizeof(DescArgs) / 4); i += kThreads)
+        ((uint32_t *)&s_a)[i] = ((const uint32_t *)&a)[i];
+    __syncthreads();
     const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const bool in = p < n_seg;
     int64_t seg = p;
     if (!IDENT && in) seg = order[p];
     if (IDENT && in) order[p] = (int32_t)p;
     bool heavy = false;
-    if (in) heavy = desc_of(a, seg, p, desc, weight) > 32;
+    if (in) heavy = desc_of(s_a, seg, p, desc, weight) > 32;
     if (IDENT && !keep && __ballot(heavy) != 0 && (threadIdx.x & 63) == 0) atomicOr(flag, 1u);
 }
 
