@@ -772,12 +772,16 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
     using Gm = DlGeom<BK>;
     constexpr int FM = C::FM, FN = C::FN, NW = C::NT / 64;
     constexpr int A_BYTES = C::TM * Gm::RB, B_BYTES = C::TN * Gm::RB;
-    constexpr int STAGE = A_BYTES + B_BYTES;
     constexpr int IA = C::TM / Gm::RPI / NW, IB = C::TN / Gm::RPI / NW;
     static_assert(IA * Gm::RPI * NW == C::TM && IB * Gm::RPI * NW == C::TN, "whole instructions");
-    constexpr int LPS = IA + IB;
-    static_assert((S - 2) * LPS < 64 && S >= 2, "vmcnt range");
-    __shared__ __attribute__((aligned(1024))) char lds[S * STAGE];
+    // A tiles (rows of the long operand, from HBM) are loaded AH + 1 steps ahead, B tiles
+    // (weights, mostly L2 hits) one step ahead: SA = 2 + AH stages of A, two of B.  The
+    // forward form takes AH = 1 (three A stages and two B stages fill the 160 KB of LDS;
+    // block-0 transform 1.95 -> 1.86 ms); the input-side form measured slower with it.
+    static_assert(S == 2, "two B stages");
+    constexpr int AH = E::kDms ? 0 : 1;
+    constexpr int SA = 2 + AH, SB = 2;
+    __shared__ __attribute__((aligned(1024))) char lds[SA * A_BYTES + SB * B_BYTES];
 
     const int64_t T = tiles_m * tiles_n;
     const int64_t wpx = (int64_t)gridDim.x / 8;          // workgroups per XCD (grid % 8 == 0)
@@ -805,44 +809,61 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
         rb[j] = (wave * IB + j) * Gm::RPI + lr;
         cb[j] = ls ^ Gm::swz(rb[j]);
     }
-    // issue cursor: the step the next issue() loads (tile it_t, K step it_k)
-    int64_t it_t = 0, it_k = 0, im0 = 0, in0 = 0;
     auto tile_origin = [&](int64_t ti, int64_t &m0, int64_t &n0) {
         const int64_t t = lo + ti * wpx;
         const int64_t tm = t / tiles_n;
         m0 = tm * C::TM;
         n0 = (t - tm * tiles_n) * C::TN;
     };
-    if (ntile > 0) tile_origin(0, im0, in0);
-    int64_t gs_issue = 0;
-    auto issue = [&]() {
-        char *st = lds + (int)(gs_issue % S) * STAGE;
-        const bool live = it_t < ntile;
-        const int64_t k0 = it_k * BK;
+    // issue cursors: A runs one step ahead of B
+    auto row_origin = [&](int ti) -> int64_t { return (lo + (int64_t)ti * wpx) / tiles_n * C::TM; };
+    auto col_origin = [&](int ti) -> int64_t {
+        const int64_t t = lo + (int64_t)ti * wpx;
+        return (t - t / tiles_n * tiles_n) * C::TN;
+    };
+    int ia_t = 0, ia_k = 0, ga = 0, ib_t = 0, ib_k = 0, gb = 0;
+    int64_t ia_m0 = ntile > 0 ? row_origin(0) : 0, ib_n0 = ntile > 0 ? col_origin(0) : 0;
+    auto issueA = [&]() {
+        char *st = lds + (ga % SA) * A_BYTES;
+        const bool live = ia_t < ntile;
+        const int64_t k0 = (int64_t)ia_k * BK;
 #pragma unroll
         for (int j = 0; j < IA; ++j) {
-            const int64_t k = k0 + ca[j] * 8, m = im0 + ra[j];
+            const int64_t k = k0 + ca[j] * 8, m = ia_m0 + ra[j];
             const char *g = (live && m < M && k < K) ? a + m * lda + k * 2 : zp;
             lds_dma16(g, st + (wave * IA + j) * 1024);
         }
+        ++ga;
+        if (++ia_k == nk) {
+            ia_k = 0;
+            ++ia_t;
+            if (ia_t < ntile) ia_m0 = row_origin(ia_t);
+        }
+    };
+    auto issueB = [&]() {
+        char *st = lds + SA * A_BYTES + (gb % SB) * B_BYTES;
+        const bool live = ib_t < ntile;
+        const int64_t k0 = (int64_t)ib_k * BK;
 #pragma unroll
         for (int j = 0; j < IB; ++j) {
-            const int64_t k = k0 + cb[j] * 8, n = in0 + rb[j];
+            const int64_t k = k0 + cb[j] * 8, n = ib_n0 + rb[j];
             int64_t kb = k;
             if constexpr (E::kDms) kb = k < epi.kwrap ? k : k - epi.kwrap;
             const char *g = (live && n < N && k < K) ? b + n * ldb + kb * 2 : zp;
-            lds_dma16(g, st + A_BYTES + (wave * IB + j) * 1024);
+            lds_dma16(g, st + (wave * IB + j) * 1024);
         }
-        ++gs_issue;
-        if (++it_k == nk) {
-            it_k = 0;
-            ++it_t;
-            if (it_t < ntile) tile_origin(it_t, im0, in0);
+        ++gb;
+        if (++ib_k == nk) {
+            ib_k = 0;
+            ++ib_t;
+            if (ib_t < ntile) ib_n0 = col_origin(ib_t);
         }
     };
 
     f32x4 acc[FM][FN];
-    for (int st = 0; st < S - 1; ++st) issue();
+    for (int i = 0; i < AH; ++i) issueA();
+    issueB();
+    issueA();
     const int r16 = lane & 15, q = lane >> 4;
     int64_t m0 = 0, n0 = 0, ti = 0, kk = 0;
     int32_t deg[FM];   // kDms: the degree of each of the lane's rows in the wave's slot
@@ -868,10 +889,12 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
                 }
             }
         }
-        vm_wait_barrier<(S - 2) * LPS>();
-        issue();
-        const char *As = lds + (int)(gs % S) * STAGE;
-        const char *Bs = As + A_BYTES;
+        // A(gs) and B(gs) have landed; with AH, A(gs + 1) may still be in flight
+        vm_wait_barrier<AH ? IA : 0>();
+        issueB();
+        issueA();
+        const char *As = lds + (int)(gs % SA) * A_BYTES;
+        const char *Bs = lds + SA * A_BYTES + (int)(gs % SB) * B_BYTES;
 #pragma unroll
         for (int s = 0; s < BK / 32; ++s) {
             bf16x8 bv[FN];
