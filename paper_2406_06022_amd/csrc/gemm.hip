@@ -809,27 +809,31 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
         rb[j] = (wave * IB + j) * Gm::RPI + lr;
         cb[j] = ls ^ Gm::swz(rb[j]);
     }
-    auto tile_origin = [&](int64_t ti, int64_t &m0, int64_t &n0) {
-        const int64_t t = lo + ti * wpx;
-        const int64_t tm = t / tiles_n;
-        m0 = tm * C::TM;
-        n0 = (t - tm * tiles_n) * C::TN;
+    // Tile origins, stepped: a workgroup's tiles are lo, lo + wpx, ..., so each cursor
+    // keeps (row block, column block) and adds wpx as a quotient and remainder of
+    // tiles_n (a division in the loop kept its divisor in a spilled register, whose reload
+    // waited for every load in flight).
+    const int tn_n = (int)tiles_n;
+    const int dq = (int)(wpx / tiles_n), dr = (int)(wpx - (int64_t)dq * tiles_n);
+    const int tm_0 = (int)(lo / tiles_n), tn_0 = (int)(lo - (int64_t)tm_0 * tiles_n);
+    auto step_tile = [&](int &tm, int &tn) {
+        tn += dr;
+        tm += dq;
+        if (tn >= tn_n) {
+            tn -= tn_n;
+            ++tm;
+        }
     };
-    // issue cursors: A runs one step ahead of B
-    auto row_origin = [&](int ti) -> int64_t { return (lo + (int64_t)ti * wpx) / tiles_n * C::TM; };
-    auto col_origin = [&](int ti) -> int64_t {
-        const int64_t t = lo + (int64_t)ti * wpx;
-        return (t - t / tiles_n * tiles_n) * C::TN;
-    };
+    // issue cursors: with AH, A runs AH steps ahead of B
     int ia_t = 0, ia_k = 0, ga = 0, ib_t = 0, ib_k = 0, gb = 0;
-    int64_t ia_m0 = ntile > 0 ? row_origin(0) : 0, ib_n0 = ntile > 0 ? col_origin(0) : 0;
+    int a_tm = tm_0, a_tn = tn_0, b_tm = tm_0, b_tn = tn_0;
     auto issueA = [&]() {
         char *st = lds + (ga % SA) * A_BYTES;
         const bool live = ia_t < ntile;
         const int64_t k0 = (int64_t)ia_k * BK;
 #pragma unroll
         for (int j = 0; j < IA; ++j) {
-            const int64_t k = k0 + ca[j] * 8, m = ia_m0 + ra[j];
+            const int64_t k = k0 + ca[j] * 8, m = (int64_t)a_tm * C::TM + ra[j];
             const char *g = (live && m < M && k < K) ? a + m * lda + k * 2 : zp;
             lds_dma16(g, st + (wave * IA + j) * 1024);
         }
@@ -837,7 +841,7 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
         if (++ia_k == nk) {
             ia_k = 0;
             ++ia_t;
-            if (ia_t < ntile) ia_m0 = row_origin(ia_t);
+            step_tile(a_tm, a_tn);
         }
     };
     auto issueB = [&]() {
@@ -846,7 +850,7 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
         const int64_t k0 = (int64_t)ib_k * BK;
 #pragma unroll
         for (int j = 0; j < IB; ++j) {
-            const int64_t k = k0 + cb[j] * 8, n = ib_n0 + rb[j];
+            const int64_t k = k0 + cb[j] * 8, n = (int64_t)b_tn * C::TN + rb[j];
             int64_t kb = k;
             if constexpr (E::kDms) kb = k < epi.kwrap ? k : k - epi.kwrap;
             const char *g = (live && n < N && k < K) ? b + n * ldb + kb * 2 : zp;
@@ -856,7 +860,7 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
         if (++ib_k == nk) {
             ib_k = 0;
             ++ib_t;
-            if (ib_t < ntile) ib_n0 = col_origin(ib_t);
+            step_tile(b_tm, b_tn);
         }
     };
 
@@ -865,11 +869,13 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
     issueB();
     issueA();
     const int r16 = lane & 15, q = lane >> 4;
-    int64_t m0 = 0, n0 = 0, ti = 0, kk = 0;
+    int64_t m0 = 0, n0 = 0, kk = 0;
+    int c_tm = tm_0, c_tn = tn_0;
     int32_t deg[FM];   // kDms: the degree of each of the lane's rows in the wave's slot
     for (int64_t gs = 0; gs < nsteps; ++gs) {
         if (kk == 0) {
-            tile_origin(ti, m0, n0);
+            m0 = (int64_t)c_tm * C::TM;
+            n0 = (int64_t)c_tn * C::TN;
 #pragma unroll
             for (int mi = 0; mi < FM; ++mi)
 #pragma unroll
@@ -979,7 +985,7 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
         }
         if (++kk == nk) {
             kk = 0;
-            ++ti;
+            step_tile(c_tm, c_tn);
         }
     }
     __builtin_amdgcn_s_waitcnt(0);   // padded steps' loads landed before the workgroup exits
