@@ -871,7 +871,10 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
     const int r16 = lane & 15, q = lane >> 4;
     int64_t m0 = 0, n0 = 0, kk = 0;
     int c_tm = tm_0, c_tn = tn_0;
-    int32_t deg[FM];   // kDms: the degree of each of the lane's rows in the wave's slot
+    // kDms: indptr[m] and indptr[m + 1] of each of the lane's rows in the wave's slot,
+    // loaded at the tile's start and subtracted only in its epilogue (a use right after
+    // the load would wait for the K step's loads issued before it)
+    int32_t dlo[FM], dhi[FM];
     for (int64_t gs = 0; gs < nsteps; ++gs) {
         if (kk == 0) {
             m0 = (int64_t)c_tm * C::TM;
@@ -881,8 +884,8 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
 #pragma unroll
                 for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
             if constexpr (E::kDms) {
-                // read now, used by this tile's epilogue: -1 where the slot has no segments
-                // (self slot) or the row is outside the output
+                // the segment offsets of the lane's rows (the zero buffer where the slot has
+                // no segments or the row is outside the output)
                 const int64_t nw = n0 + wn * FN * 16;
                 const int sl = nw < N ? (int)__umulhi((uint32_t)nw, epi.inv_din) : 0;
                 const int32_t *ip = nw < N ? epi.indptr[sl] : nullptr;
@@ -891,7 +894,8 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
                     const int64_t m = m0 + wm * FM * 16 + mi * 16 + r16;
                     const bool ok = ip != nullptr && m < M;
                     const int32_t *p = ok ? ip + m : (const int32_t *)zp;
-                    deg[mi] = ok ? p[1] - p[0] : -1;
+                    dlo[mi] = p[0];
+                    dhi[mi] = p[1];
                 }
             }
         }
@@ -920,11 +924,15 @@ __global__ __launch_bounds__(C::NT, C::NT / 256) void k_gemm_fwd(
                 // lane: row m0 + wm FM 16 + 16 mi + (lane % 16), columns n0 + wn FN 16 +
                 // 16 ni + 4 (lane / 16) .. + 3, stored as they are (16 bytes)
                 const int64_t nw = n0 + wn * FN * 16;
+                const int sl = nw < N ? (int)__umulhi((uint32_t)nw, epi.inv_din) : 0;
+                const bool seg = nw < N && epi.indptr[sl] != nullptr;
 #pragma unroll
                 for (int mi = 0; mi < FM; ++mi) {
                     const int64_t m = m0 + wm * FM * 16 + mi * 16 + r16;
-                    const bool zero = deg[mi] == 0;
-                    const float scale = deg[mi] > 0 ? (float)deg[mi] : 1.f;
+                    // -1 where the slot has no segments (self slot) or the row is outside
+                    const int32_t deg = seg && m < M ? dhi[mi] - dlo[mi] : -1;
+                    const bool zero = deg == 0;
+                    const float scale = deg > 0 ? (float)deg : 1.f;
 #pragma unroll
                     for (int ni = 0; ni < FN; ++ni) {
                         const int64_t n = nw + 16 * ni + 4 * q;
