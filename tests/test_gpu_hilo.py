@@ -88,7 +88,10 @@ def _check_against_fp32_gradients(run: BlockRun) -> None:
     run.assert_parity()
 
 
-@pytest.mark.parametrize("d_in,d_out", [(128, 256), (24, 40), (512, 128), (264, 40), (64, 64)])
+# (192, 136) and (64, 520) take the persistent input side with a part-filled last column
+# tile and a K of 2 d_out that ends inside a K step, the hi/lo boundary inside a step
+@pytest.mark.parametrize("d_in,d_out", [(128, 256), (24, 40), (512, 128), (264, 40), (64, 64),
+                                        (192, 136), (64, 520)])
 @pytest.mark.parametrize("relu", ["none", "rows", "bits"])
 def test_hilo_gradients_random_blocks(d_in, d_out, relu):
     rng = np.random.default_rng(d_in * 3 + d_out)
