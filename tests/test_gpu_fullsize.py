@@ -2,7 +2,9 @@
 
 Every block of each workload runs through the C ABI stage by stage, on one stream, with the
 benchmark's flags (fused ReLU below the last layer, ReLU-input mask above the first, unique
-ids and the embedding gradient at the first).  Inputs are seeded: the input layer reads the
+ids and the embedding gradient at the first; in bf16, the hi/lo gradient form between
+blocks: dy in it below the last layer, dh written in it above the first, decoded before the
+comparison, while the oracle takes the fp32 dy).  Inputs are seeded: the input layer reads the
 full feature and embedding tables by global row id; higher layers read a seeded ReLU'd
 dense input of the right shape.  The oracle then recomputes sampled outputs one by one:
 
@@ -31,6 +33,21 @@ from tests.harness import TOL, rel_err, to64
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda"
+
+
+def _hilo_rows(x):
+    """fp32 rows [n, d] on the device in the hi/lo form (d bf16 high parts, then d low parts,
+    both rounded to nearest even), as fp32 [n, d] of the same bytes."""
+    hi = x.to(torch.bfloat16)
+    lo = (x - hi.to(torch.float32)).to(torch.bfloat16)
+    return torch.cat([hi, lo], dim=1).contiguous().view(torch.float32)
+
+
+def _hilo_decode(x):
+    """hi + lo in fp64 (host) of rows in the hi/lo form."""
+    d = x.shape[1]
+    b = x.contiguous().view(torch.bfloat16).to(torch.float64)
+    return (b[:, :d] + b[:, d:]).cpu().numpy()
 
 
 def _dst_sample(blk, t, rng, n_random=24):
@@ -147,10 +164,16 @@ def _block_parity(spec, mb, index, l, rng, bad):
               if t in grad_types else None for t in range(T)]
     fwd_flags = 0 if last else rgcn.RGCN_FUSE_RELU
     bwd_flags = rgcn.RGCN_IDS_UNIQUE if first else rgcn.RGCN_INPUT_RELU
+    # the chain driver's gradient form between bf16 blocks
+    hilo_in = spec.dtype == "bf16" and not last
+    hilo_out = spec.dtype == "bf16" and not first
+    dy_call = [_hilo_rows(x) if hilo_in else x for x in dy]
+    bwd_flags |= (rgcn.RGCN_DY_HILO if hilo_in else 0) | (rgcn.RGCN_DH_HILO if hilo_out else 0)
     rgcn.rgcn_block_plan(dblk, params, ws)
     rgcn.rgcn_block_aggregate(dblk, inputs, params, ws, fwd_flags)
     rgcn.rgcn_block_transform(dblk, params, y, ws, fwd_flags)
-    rgcn.rgcn_block_backward_dense(dblk, params, dy, dw_rel, dw_self, None, ws, bwd_flags)
+    rgcn.rgcn_block_backward_dense(dblk, params, dy_call, dw_rel, dw_self, None, ws, bwd_flags)
+    del dy_call
     rgcn.rgcn_block_backward_sparse(dblk, inputs, params, dh, demb, ws, bwd_flags)
     torch.cuda.synchronize()
 
@@ -199,7 +222,8 @@ def _block_parity(spec, mb, index, l, rng, bad):
             got = to64(demb[s].index_select(0, gid))
             name = f"demb[{s}]"
         else:
-            got = to64(dh[s].index_select(0, torch.as_tensor(srows, device=DEV)))
+            got = dh[s].index_select(0, torch.as_tensor(srows, device=DEV))
+            got = _hilo_decode(got) if hilo_out else to64(got)
             name = f"dh[{s}]"
         if not _check(name, got, ref_rows, tol, errs):
             bad[f"block{l} {name}"] = errs[name]
