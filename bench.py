@@ -49,7 +49,7 @@ KERNEL_SOURCES = {
     "k_transpose_pipe_adagrad": ["paper_2406_06022_amd/csrc/aggregate.hip"] + _COMMON_INPUTS,
 }
 # Plain copy of known size run after the timed steps (an fp32 negation of a 1 GiB buffer:
-# one read and one write of every byte per dispatch).  Its time gives the box's attainable
+# one read and one write of every byte per dispatch).  Its time gives the device's attainable
 # streaming bandwidth; under rocprofv3 --pmc its HBM counters calibrate those of the timed
 # kernels.
 COPY_KERNEL = "neg_kernel"
@@ -126,7 +126,7 @@ def build_stack(index: int, device: str):
     return spec, mb, tables, ids, weights, stack, dy
 
 
-def survey_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
+def method_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
     """Algorithmic bytes of one launch of a stage's kernel as the method defines them (no
     cache reuse), the figures the roofline fractions use:
       aggregate (gather + segmented mean): per relation 4 (n_dst + 1) offsets, 4 nnz source
@@ -164,7 +164,7 @@ def survey_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
 
 def algorithmic_bytes(spec, blk, dev_blk, stage: str, layer: int) -> float:
     """Bytes one launch of a stage's kernel moves in this implementation's data layout (no
-    cache reuse): the method's bytes (survey_bytes) plus what the layout adds -- the
+    cache reuse): the method's bytes (method_bytes) plus what the layout adds -- the
     self-loop rows copied into the K-concatenated operand, an 8-byte id per gathered edge,
     the fp32 self-loop input-side rows and the ReLU sign bits the backward reads."""
     b = 2 if spec.dtype == "bf16" else 4
@@ -910,7 +910,7 @@ def block_ms(stack, avg) -> list:
 
 
 def stage_rooflines(spec, mb, stack, avg) -> dict:
-    """Every aggregate and sparse stage: its time, the method's bytes (survey_bytes) and
+    """Every aggregate and sparse stage: its time, the method's bytes (method_bytes) and
     the fraction of the 8 TB/s peak they make, and this layout's bytes beside them."""
     out = {}
     for l in range(stack.L):
@@ -918,7 +918,7 @@ def stage_rooflines(spec, mb, stack, avg) -> dict:
             if (s, l) not in avg:
                 continue
             t_ms = avg[(s, l)]
-            byts = survey_bytes(spec, mb.blocks[l], stack.blocks[l], s, l)
+            byts = method_bytes(spec, mb.blocks[l], stack.blocks[l], s, l)
             impl = algorithmic_bytes(spec, mb.blocks[l], stack.blocks[l], s, l)
             gbs = byts / (t_ms * 1e-3) / 1e9
             out[f"{s}[{l}]"] = {"ms": round(t_ms, 4), "bytes": byts, "GB/s": round(gbs, 1),
@@ -963,7 +963,7 @@ def gather_by_ids(spec, mb, stack, reps: int = 10) -> dict:
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / reps
-    byts = survey_bytes(spec, blk, stack.blocks[0], "aggregate", 0)
+    byts = method_bytes(spec, blk, stack.blocks[0], "aggregate", 0)
     gbs = byts / (ms * 1e-3) / 1e9
     return {"ms": round(ms, 4), "bytes": byts, "GB/s": round(gbs, 1),
             "frac": round(gbs / HBM_PEAK_GBS, 4)}
