@@ -195,3 +195,64 @@ def test_overlapped_plan_matches_serial_step(index):
         for i, (g, w_) in enumerate(zip(got, want)):
             assert not torch.isnan(w_).any(), f"serial output {i} left unwritten"
             assert torch.equal(g, w_), f"overlapped step {rep}: output {i} differs"
+
+
+@pytest.mark.parametrize("index", [1, 2, 4])
+def test_hilo_gradients_between_blocks_match_fp32(index):
+    """The chain with the gradients between bf16 blocks in the hi/lo form (the default) and
+    with them in fp32 (hilo_grads=False): the forward and the top block's weight gradients
+    bit for bit (the same operands reach the same kernels).  Below the top the results
+    differ at fp32 rounding: a hidden block's input side adds its hi and lo sums in
+    another order when the rows come in the hi/lo form (the persistent product), so its
+    input gradient differs in the last bits, which now and then moves the bf16 rounding of
+    a low part (2^-16 of the element) in the next block's operands; bias sums of hi + lo
+    differ from fp32 sums by at most 2^-16 of each term.  Through a block whose sums
+    cancel (the embedding gradient is judged per touched element) that reaches about 1e-4,
+    so the bar below the top is 1e-3, twenty times under the oracle's bf16 bar; a wrong
+    form anywhere (hi/lo bytes read as fp32, or the reverse) is off by order one."""
+    spec = synth.small_config(index)
+    assert spec.dtype == "bf16"
+    mb = synth.sample_minibatch(spec)
+    T, R, L = len(spec.ntype_names), len(spec.rels), spec.num_layers
+    tdt = synth.torch_dtype(spec.dtype)
+    emb = [t for t in range(T) if spec.featureless[t]]
+    tables = [synth.normal_table(spec.type_rows[t], spec.dims[0], tdt, 700 + t).to(DEV)
+              for t in range(T)]
+    ids = [torch.as_tensor(mb.input_ids[t]).to(DEV) for t in range(T)]
+    weights = []
+    for l in range(L):
+        w_rel, w_self, b = synth.block_weights(T, R, spec.dims[l], spec.dims[l + 1], tdt,
+                                               80 + l, with_bias=True)
+        weights.append(([x.to(DEV) for x in w_rel], [x.to(DEV) for x in w_self],
+                        [x.to(DEV) for x in b]))
+    gen = torch.Generator().manual_seed(170 + index)
+    dy = [torch.randn((n, spec.dims[-1]), generator=gen).to(DEV) if n else None
+          for n in mb.blocks[-1].n_dst]
+    outs = []
+    for hilo in (True, False):
+        stack = chain.MiniBatchStack(mb.blocks, tables, ids, weights, spec.dtype, spec.dims,
+                                     emb_types=emb, device=DEV, hilo_grads=hilo)
+        assert stack.hilo_grads == hilo
+        stack.step(dy)
+        torch.cuda.synchronize()
+        outs.append(stack)
+    h, f = outs
+    for t, (a, b) in enumerate(zip(h.y[-1], f.y[-1])):
+        if a is not None:
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16)), f"y[{t}]"
+    errs = {}
+    for l in range(L):
+        pairs = [(f"dw_rel[{l}][{r}]", h.dw_rel[l][r], f.dw_rel[l][r]) for r in range(R)]
+        pairs += [(f"dw_self[{l}][{t}]", h.dw_self[l][t], f.dw_self[l][t]) for t in range(T)]
+        pairs += [(f"dbias[{l}][{t}]", h.dbias[l][t], f.dbias[l][t]) for t in range(T)
+                  if h.dbias[l][t] is not None]
+        for name, a, b in pairs:
+            if l == L - 1 and not name.startswith("dbias"):
+                assert torch.equal(a.view(torch.int32), b.view(torch.int32)), name
+            errs[name] = rel_err(to64(a), to64(b))
+    for t in emb:
+        errs[f"demb[{t}]"] = rel_err(to64(h.demb[t]), to64(f.demb[t]))
+    bad = {k: v for k, v in errs.items() if not v <= 1e-3}
+    print(f"[chain hilo] {spec.name}: worst {max(errs.values()):.3g} ({max(errs, key=errs.get)})",
+          flush=True)
+    assert not bad, f"hi/lo vs fp32 gradients between blocks: {bad}"
