@@ -374,19 +374,54 @@ __global__ __launch_bounds__(kThreads) void k_lp_finish(LpArgs a, const float *g
                 const int64_t e = lane + 64 * j;
                 if (e < a.d) unsafeAtomicAdd(d_emb + dr * a.d + e, gp * u[j]);
             }
-        if (per_edge)
-            for (int64_t k = 0; k < a.nn; ++k) {
-                const float g = Gm[i * a.nn + k];
-                const int64_t row = a.neg[i * a.k + k];
+        if (per_edge) {
+            // Per chunk of 64 negatives, lane l loads negative l's row and weight once (the
+            // loop broadcasts them); each negative's embedding row is loaded one negative
+            // ahead, and one word of every 128-byte line of its gradient row two ahead, so
+            // the atomics find the lines in L2 (the value read is not used).
+            const int64_t lo_off = (int64_t)lane * 32;   // lane's line of a gradient row
+            for (int64_t k0 = 0; k0 < a.nn; k0 += 64) {
+                const int kn = a.nn - k0 < 64 ? (int)(a.nn - k0) : 64;
+                const bool okl = lane < kn;
+                const int32_t nrow_l = okl ? a.neg[i * a.k + k0 + lane] : 0;
+                const float g_l = okl ? Gm[i * a.nn + k0 + lane] : 0.f;
+                auto load_row = [&](int kk, float (&v)[J]) {
+                    const int64_t row = __shfl(nrow_l, kk, 64);
 #pragma unroll
-                for (int j = 0; j < J; ++j) {
-                    const int64_t e = lane + 64 * j;
-                    if (e < a.d) {
-                        du[j] += g * elem<BF16>(a, row, e);
-                        if (d_emb) unsafeAtomicAdd(d_emb + row * a.d + e, g * u[j]);
+                    for (int j = 0; j < J; ++j) {
+                        const int64_t e = lane + 64 * j;
+                        v[j] = e < a.d ? elem<BF16>(a, row, e) : 0.f;
                     }
+                };
+                auto touch = [&](int kk) -> float {
+                    const int64_t row = __shfl(nrow_l, kk, 64);
+                    return (d_emb && lo_off < a.d) ? d_emb[row * a.d + lo_off] : 0.f;
+                };
+                float nx[J];
+                load_row(0, nx);
+                float t0 = touch(0), t1 = kn > 1 ? touch(1) : 0.f;
+                for (int kk = 0; kk < kn; ++kk) {
+                    float cur[J];
+#pragma unroll
+                    for (int j = 0; j < J; ++j) cur[j] = nx[j];
+                    if (kk + 1 < kn) load_row(kk + 1, nx);
+                    const float t2 = kk + 2 < kn ? touch(kk + 2) : 0.f;
+                    asm volatile("" ::"v"(t0));   // this negative's lines have been fetched
+                    const int64_t row = __shfl(nrow_l, kk, 64);
+                    const float g = __shfl(g_l, kk, 64);
+#pragma unroll
+                    for (int j = 0; j < J; ++j) {
+                        const int64_t e = lane + 64 * j;
+                        if (e < a.d) {
+                            du[j] += g * cur[j];
+                            if (d_emb) unsafeAtomicAdd(d_emb + row * a.d + e, g * u[j]);
+                        }
+                    }
+                    t0 = t1;
+                    t1 = t2;
                 }
             }
+        }
 #pragma unroll
         for (int j = 0; j < J; ++j) {
             const int64_t e = lane + 64 * j;
